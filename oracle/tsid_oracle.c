@@ -1,0 +1,384 @@
+/*
+ * tsid_oracle.c -- plain, serial, fp64 CPU oracle for the TSID template-fit
+ * path of arXiv 2608.00977 ("TIDE-MC").
+ *
+ * TEST INFRASTRUCTURE ONLY: called by the tests, the smoke check and the
+ * CPU-baseline leg of the benchmark; never by the product library, with which
+ * it shares no code.  Every routine is the plain definition or the plain
+ * iteration, written as loops, with no blocking, fusion or reordering beyond
+ * what the definition states.  Floating point is binary64 throughout.
+ *
+ * Where the paper leaves a choice open the oracle takes these readings:
+ *  - the loss is Eq. 2 literally (regularisation once per factor row);
+ *  - the update moves against the gradient of Eqs. 3-4 (descent), applied to
+ *    all rows of P and Q simultaneously from the same (P_t, Q_t) (a
+ *    deterministic full-gradient epoch);
+ *  - the 1/n normalisation of Eq. 5 is the bucket degree, max(1, deg), and is
+ *    applied to both factors when selected;
+ *  - the asymmetric clip of Section 5.3, min(max(xi, -g), g), equals
+ *    min(g, xi); it acts once per coordinate on the aggregated, normalised
+ *    descent direction of a row;
+ *  - the optional bf16 mode rounds the factors read by the products to bf16
+ *    (nearest even) while the fp64 master takes the update.
+ */
+#include "tsid_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ---------------------------------------------------------------- helpers */
+
+typedef struct {
+    uint64_t key;
+    int64_t idx;
+} key_idx;
+
+static int cmp_key_idx(const void *x, const void *y) {
+    const key_idx *p = (const key_idx *)x, *q = (const key_idx *)y;
+    if (p->key < q->key) return -1;
+    if (p->key > q->key) return 1;
+    return 0;
+}
+
+static int cmp_u64(const void *x, const void *y) {
+    uint64_t p = *(const uint64_t *)x, q = *(const uint64_t *)y;
+    return (p > q) - (p < q);
+}
+
+uint16_t or_bf16_bits(float x) {
+    uint32_t bits;
+    memcpy(&bits, &x, 4);
+    if ((bits & 0x7f800000u) == 0x7f800000u && (bits & 0x007fffffu) != 0)
+        return (uint16_t)((bits >> 16) | 0x0040u); /* NaN stays a (quiet) NaN */
+    uint32_t lsb = (bits >> 16) & 1u;
+    return (uint16_t)((bits + 0x7fffu + lsb) >> 16);
+}
+
+static double bf16_round(double x) {
+    uint32_t bits = (uint32_t)or_bf16_bits((float)x) << 16;
+    float f;
+    memcpy(&f, &bits, 4);
+    return (double)f;
+}
+
+static double dot(const double *x, const double *y, int32_t k) {
+    double s = 0.0;
+    for (int32_t c = 0; c < k; ++c) s += x[c] * y[c];
+    return s;
+}
+
+static double sumsq(const double *x, int64_t len) {
+    double s = 0.0;
+    for (int64_t j = 0; j < len; ++j) s += x[j] * x[j];
+    return s;
+}
+
+/* ------------------------------------------------------------ index work */
+
+int or_template_maps(int64_t m, int64_t n, const int32_t *I, int32_t m_t,
+                     const int32_t *J, int32_t n_t, int32_t *row_map, int32_t *col_map) {
+    for (int32_t a = 0; a < m_t; ++a)
+        if (I[a] < 0 || I[a] >= m) return 2;
+    for (int32_t b = 0; b < n_t; ++b)
+        if (J[b] < 0 || J[b] >= n) return 2;
+    for (int64_t u = 0; u < m; ++u) row_map[u] = -1;
+    for (int64_t i = 0; i < n; ++i) col_map[i] = -1;
+    for (int32_t a = 0; a < m_t; ++a) {
+        if (row_map[I[a]] != -1) return 3;
+        row_map[I[a]] = a;
+    }
+    for (int32_t b = 0; b < n_t; ++b) {
+        if (col_map[J[b]] != -1) return 3;
+        col_map[J[b]] = b;
+    }
+    return 0;
+}
+
+int or_check_omega(int64_t m, int64_t n, int64_t nnz, const int32_t *u, const int32_t *i,
+                   const float *r) {
+    for (int64_t e = 0; e < nnz; ++e)
+        if (u[e] < 0 || u[e] >= m || i[e] < 0 || i[e] >= n) return 2;
+    for (int64_t e = 0; e < nnz; ++e)
+        if (!isfinite(r[e])) return 1;
+    if (nnz < 2) return 0;
+    uint64_t *keys = (uint64_t *)malloc((size_t)nnz * sizeof(uint64_t));
+    for (int64_t e = 0; e < nnz; ++e) keys[e] = (uint64_t)u[e] * (uint64_t)n + (uint64_t)i[e];
+    qsort(keys, (size_t)nnz, sizeof(uint64_t), cmp_u64);
+    int st = 0;
+    for (int64_t e = 1; e < nnz; ++e)
+        if (keys[e] == keys[e - 1]) { st = 3; break; }
+    free(keys);
+    return st;
+}
+
+int64_t or_filter(int64_t nnz, const int32_t *u, const int32_t *i, const float *r,
+                  const int32_t *row_map, const int32_t *col_map,
+                  int32_t *a, int32_t *b, float *v) {
+    int64_t out = 0;
+    for (int64_t e = 0; e < nnz; ++e) {
+        int32_t ra = row_map[u[e]], cb = col_map[i[e]];
+        if (ra >= 0 && cb >= 0) {
+            a[out] = ra;
+            b[out] = cb;
+            v[out] = r[e];
+            ++out;
+        }
+    }
+    return out;
+}
+
+/* Sort the entries by (major, minor) and lay them out as buckets of `major`. */
+static void bucket_one(int64_t nnz, const int32_t *major, const int32_t *minor, const float *v,
+                       int32_t n_major, int32_t n_minor, int64_t *ptr, int32_t *idx_out,
+                       float *val_out, int32_t *deg) {
+    key_idx *ki = (key_idx *)malloc((size_t)(nnz > 0 ? nnz : 1) * sizeof(key_idx));
+    for (int64_t e = 0; e < nnz; ++e) {
+        ki[e].key = (uint64_t)major[e] * (uint64_t)n_minor + (uint64_t)minor[e];
+        ki[e].idx = e;
+    }
+    qsort(ki, (size_t)nnz, sizeof(key_idx), cmp_key_idx);
+    for (int32_t x = 0; x < n_major; ++x) deg[x] = 0;
+    for (int64_t e = 0; e < nnz; ++e) deg[major[e]] += 1;
+    ptr[0] = 0;
+    for (int32_t x = 0; x < n_major; ++x) ptr[x + 1] = ptr[x] + deg[x];
+    for (int64_t e = 0; e < nnz; ++e) {
+        idx_out[e] = minor[ki[e].idx];
+        val_out[e] = v[ki[e].idx];
+    }
+    free(ki);
+}
+
+void or_bucket(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+               int32_t m_t, int32_t n_t,
+               int64_t *row_ptr, int32_t *csr_col, float *csr_val,
+               int64_t *col_ptr, int32_t *csc_row, float *csc_val,
+               int32_t *deg_r, int32_t *deg_c) {
+    bucket_one(nnz, a, b, v, m_t, n_t, row_ptr, csr_col, csr_val, deg_r);
+    bucket_one(nnz, b, a, v, n_t, m_t, col_ptr, csc_row, csc_val, deg_c);
+}
+
+/* ------------------------------------------------------------------ fit */
+
+double or_loss(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+               int32_t m_t, int32_t n_t, int32_t k, const double *P, const double *Q,
+               double lambda) {
+    double sse = 0.0;
+    for (int64_t e = 0; e < nnz; ++e) {
+        double err = (double)v[e] - dot(P + (int64_t)a[e] * k, Q + (int64_t)b[e] * k, k);
+        sse += err * err;
+    }
+    return sse + lambda * (sumsq(P, (int64_t)m_t * k) + sumsq(Q, (int64_t)n_t * k));
+}
+
+/* Residual sum of squares over the entries and, if gP/gQ are given, the data
+ * part of the gradients of Eqs. 3-4 summed per factor row. */
+static double sse_grad(int64_t nnz, const int32_t *a, const int32_t *b, const float *v, int32_t k,
+                       const double *Pr, const double *Qr, double *gP, double *gQ) {
+    double sse = 0.0;
+    for (int64_t e = 0; e < nnz; ++e) {
+        const double *p = Pr + (int64_t)a[e] * k, *q = Qr + (int64_t)b[e] * k;
+        double err = (double)v[e] - dot(p, q, k);
+        sse += err * err;
+        if (gP) {
+            double *gp = gP + (int64_t)a[e] * k, *gq = gQ + (int64_t)b[e] * k;
+            for (int32_t c = 0; c < k; ++c) {
+                gp[c] += -2.0 * err * q[c];
+                gq[c] += -2.0 * err * p[c];
+            }
+        }
+    }
+    return sse;
+}
+
+/* New value of one factor row from its data gradient g (Eqs. 3-5, Section 5.3). */
+static int update_row(const double *x, const double *g, int32_t deg, int32_t k, double lambda,
+                      double lr, int32_t step, int32_t clip, double xi, double *x_new) {
+    double s = step ? 1.0 / (double)(deg > 1 ? deg : 1) : 1.0;
+    int finite = 1;
+    for (int32_t c = 0; c < k; ++c) {
+        double grad = g[c] + 2.0 * lambda * x[c];
+        double d = -s * grad;
+        if (clip && d > xi) d = xi;
+        x_new[c] = x[c] + lr * d;
+        if (!isfinite(x_new[c])) finite = 0;
+    }
+    return finite;
+}
+
+static void round_copy(const double *x, double *y, int64_t len) {
+    for (int64_t j = 0; j < len; ++j) y[j] = bf16_round(x[j]);
+}
+
+int or_fit(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+           int32_t m_t, int32_t n_t, int32_t k, double *P, double *Q,
+           int32_t epochs, double lambda, double lr, int32_t step,
+           int32_t clip, double xi, int32_t bf16, double *loss_hist, int32_t *epochs_done) {
+    int64_t lp = (int64_t)m_t * k, lq = (int64_t)n_t * k;
+    double *gP = (double *)malloc((size_t)(lp + 1) * sizeof(double));
+    double *gQ = (double *)malloc((size_t)(lq + 1) * sizeof(double));
+    double *Pn = (double *)malloc((size_t)(lp + 1) * sizeof(double));
+    double *Qn = (double *)malloc((size_t)(lq + 1) * sizeof(double));
+    double *Ps = bf16 ? (double *)malloc((size_t)(lp + 1) * sizeof(double)) : NULL;
+    double *Qs = bf16 ? (double *)malloc((size_t)(lq + 1) * sizeof(double)) : NULL;
+    int32_t *deg_r = (int32_t *)calloc((size_t)m_t + 1, sizeof(int32_t));
+    int32_t *deg_c = (int32_t *)calloc((size_t)n_t + 1, sizeof(int32_t));
+    for (int64_t e = 0; e < nnz; ++e) {
+        deg_r[a[e]] += 1;
+        deg_c[b[e]] += 1;
+    }
+    int status = 0;
+    int32_t t;
+    for (t = 0; t < epochs; ++t) {
+        const double *Pr = P, *Qr = Q;
+        if (bf16) {
+            round_copy(P, Ps, lp);
+            round_copy(Q, Qs, lq);
+            Pr = Ps;
+            Qr = Qs;
+        }
+        memset(gP, 0, (size_t)lp * sizeof(double));
+        memset(gQ, 0, (size_t)lq * sizeof(double));
+        double sse = sse_grad(nnz, a, b, v, k, Pr, Qr, gP, gQ);
+        if (loss_hist) loss_hist[t] = sse + lambda * (sumsq(P, lp) + sumsq(Q, lq));
+        int finite = 1;
+        for (int32_t x = 0; x < m_t; ++x)
+            finite &= update_row(P + (int64_t)x * k, gP + (int64_t)x * k, deg_r[x], k, lambda, lr,
+                                 step, clip, xi, Pn + (int64_t)x * k);
+        for (int32_t x = 0; x < n_t; ++x)
+            finite &= update_row(Q + (int64_t)x * k, gQ + (int64_t)x * k, deg_c[x], k, lambda, lr,
+                                 step, clip, xi, Qn + (int64_t)x * k);
+        if (!finite) {
+            status = 7;
+            break;
+        }
+        memcpy(P, Pn, (size_t)lp * sizeof(double));
+        memcpy(Q, Qn, (size_t)lq * sizeof(double));
+    }
+    if (status == 0 && loss_hist) {
+        const double *Pr = P, *Qr = Q;
+        if (bf16) {
+            round_copy(P, Ps, lp);
+            round_copy(Q, Qs, lq);
+            Pr = Ps;
+            Qr = Qs;
+        }
+        double sse = sse_grad(nnz, a, b, v, k, Pr, Qr, NULL, NULL);
+        loss_hist[epochs] = sse + lambda * (sumsq(P, lp) + sumsq(Q, lq));
+    }
+    if (epochs_done) *epochs_done = t;
+    free(gP); free(gQ); free(Pn); free(Qn); free(Ps); free(Qs); free(deg_r); free(deg_c);
+    return status;
+}
+
+/* ------------------------------------------------------------ extension */
+
+int or_extend(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,
+              int32_t n_free, int32_t k, const double *F_fixed, double *F_free,
+              int32_t steps, double lambda, double lr, int32_t step, int32_t clip, double xi) {
+    int64_t len = (int64_t)n_free * k;
+    double *g = (double *)malloc((size_t)(len + 1) * sizeof(double));
+    double *xn = (double *)malloc((size_t)(len + 1) * sizeof(double));
+    int32_t *deg = (int32_t *)calloc((size_t)n_free + 1, sizeof(int32_t));
+    for (int64_t e = 0; e < nnz; ++e) deg[free_id[e]] += 1;
+    for (int64_t j = 0; j < len; ++j) F_free[j] = 0.0;
+    int status = 0;
+    for (int32_t s = 0; s < steps && status == 0; ++s) {
+        memset(g, 0, (size_t)len * sizeof(double));
+        for (int64_t e = 0; e < nnz; ++e) {
+            const double *p = F_fixed + (int64_t)fixed_id[e] * k;
+            double *x = F_free + (int64_t)free_id[e] * k, *gx = g + (int64_t)free_id[e] * k;
+            double err = (double)v[e] - dot(p, x, k);
+            for (int32_t c = 0; c < k; ++c) gx[c] += -2.0 * err * p[c];
+        }
+        int finite = 1;
+        for (int32_t f = 0; f < n_free; ++f)
+            finite &= update_row(F_free + (int64_t)f * k, g + (int64_t)f * k, deg[f], k, lambda,
+                                 lr, step, clip, xi, xn + (int64_t)f * k);
+        if (!finite) status = 7;
+        else memcpy(F_free, xn, (size_t)len * sizeof(double));
+    }
+    free(g); free(xn); free(deg);
+    return status;
+}
+
+int or_ridge(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,
+             int32_t n_free, int32_t k, const double *F_fixed, double lambda, double *F_free) {
+    int64_t kk = (int64_t)k * k;
+    double *A = (double *)calloc((size_t)n_free * kk + 1, sizeof(double));
+    double *y = (double *)calloc((size_t)n_free * k + 1, sizeof(double));
+    for (int64_t e = 0; e < nnz; ++e) {
+        const double *p = F_fixed + (int64_t)fixed_id[e] * k;
+        double *Af = A + (int64_t)free_id[e] * kk, *yf = y + (int64_t)free_id[e] * k;
+        for (int32_t r = 0; r < k; ++r) {
+            yf[r] += (double)v[e] * p[r];
+            for (int32_t c = 0; c < k; ++c) Af[r * k + c] += p[r] * p[c];
+        }
+    }
+    int status = 0;
+    for (int32_t f = 0; f < n_free && status == 0; ++f) {
+        double *M = A + (int64_t)f * kk, *rhs = y + (int64_t)f * k, *x = F_free + (int64_t)f * k;
+        for (int32_t r = 0; r < k; ++r) M[r * k + r] += lambda;
+        /* Cholesky M = L L^T, L stored in the lower triangle of M. */
+        for (int32_t j = 0; j < k && status == 0; ++j) {
+            double d = M[j * k + j];
+            for (int32_t c = 0; c < j; ++c) d -= M[j * k + c] * M[j * k + c];
+            if (!(d > 0.0)) { status = 1; break; }
+            double ljj = sqrt(d);
+            M[j * k + j] = ljj;
+            for (int32_t r = j + 1; r < k; ++r) {
+                double s = M[r * k + j];
+                for (int32_t c = 0; c < j; ++c) s -= M[r * k + c] * M[j * k + c];
+                M[r * k + j] = s / ljj;
+            }
+        }
+        if (status) break;
+        for (int32_t r = 0; r < k; ++r) { /* L z = rhs */
+            double s = rhs[r];
+            for (int32_t c = 0; c < r; ++c) s -= M[r * k + c] * x[c];
+            x[r] = s / M[r * k + r];
+        }
+        for (int32_t r = k - 1; r >= 0; --r) { /* L^T x = z */
+            double s = x[r];
+            for (int32_t c = r + 1; c < k; ++c) s -= M[c * k + r] * x[c];
+            x[r] = s / M[r * k + r];
+        }
+    }
+    free(A); free(y);
+    return status;
+}
+
+int32_t or_chunk_plan(const int64_t *counts, int64_t n_free, int32_t n_chunks,
+                      int64_t max_entries, int64_t *bounds, int32_t max_bounds) {
+    if (n_chunks > 0) {
+        if (max_bounds < n_chunks + 1) return -1;
+        int64_t total = 0;
+        for (int64_t f = 0; f < n_free; ++f) total += counts[f];
+        int64_t before = 0, f = 0;
+        bounds[0] = 0;
+        for (int32_t j = 1; j < n_chunks; ++j) {
+            /* ceil(j * total / n_chunks) without overflow for realistic sizes */
+            int64_t target = (int64_t)(((__int128)j * total + n_chunks - 1) / n_chunks);
+            while (f < n_free && before < target) before += counts[f++];
+            bounds[j] = f;
+        }
+        bounds[n_chunks] = n_free;
+        return n_chunks;
+    }
+    int32_t nb = 0;
+    if (max_bounds < 1) return -1;
+    bounds[nb++] = 0;
+    if (n_free == 0) return 0;
+    int64_t in_chunk = 0;
+    for (int64_t f = 0; f < n_free; ++f) {
+        if (in_chunk > 0 && in_chunk + counts[f] > max_entries) {
+            if (nb >= max_bounds) return -1;
+            bounds[nb++] = f;
+            in_chunk = 0;
+        }
+        in_chunk += counts[f];
+    }
+    if (nb >= max_bounds) return -1;
+    bounds[nb++] = n_free;
+    return nb - 1;
+}

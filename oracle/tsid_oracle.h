@@ -1,0 +1,102 @@
+/*
+ * tsid_oracle.h -- plain, serial, fp64 CPU oracle for the TSID template-fit
+ * path (arXiv 2608.00977).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library may include,
+ * link or call this file; only the tests, the smoke check and the CPU
+ * baseline leg of the benchmark use it.  It shares no code with the HIP path.
+ *
+ * All floating-point arithmetic is IEEE binary64 in straightforward loops.
+ * Inputs that arrive as fp32 (values, initial factors) are widened exactly.
+ *
+ * Status codes match the library's meaning: 0 ok, 1 invalid argument,
+ * 2 index out of range, 3 duplicate, 7 non-finite result.
+ */
+#ifndef TSID_ORACLE_H
+#define TSID_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Template index maps (Section 3.1: the index sets I and J; Section 5.1: the
+ * sampled column set).  row_map[u] = position of u in I, else -1; likewise
+ * col_map.  Range errors take precedence over duplicates. */
+int or_template_maps(int64_t m, int64_t n, const int32_t *I, int32_t m_t,
+                     const int32_t *J, int32_t n_t, int32_t *row_map, int32_t *col_map);
+
+/* Validates Omega (Definition 1: a set of cells of an m x n matrix):
+ * 2 if any (u, i) is out of range, else 1 if any value is not finite,
+ * else 3 if a cell repeats, else 0. */
+int or_check_omega(int64_t m, int64_t n, int64_t nnz, const int32_t *u, const int32_t *i,
+                   const float *r);
+
+/* Omega* = the observed cells inside the template, relabelled to local ids
+ * (a, b), in input order (Section 3.2).  Returns |Omega*|. */
+int64_t or_filter(int64_t nnz, const int32_t *u, const int32_t *i, const float *r,
+                  const int32_t *row_map, const int32_t *col_map,
+                  int32_t *a, int32_t *b, float *v);
+
+/* Buckets of Omega* by row (sorted by (a, b)) and by column (sorted by (b, a)),
+ * with degrees and exclusive-prefix pointers.  Values are copied bitwise. */
+void or_bucket(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+               int32_t m_t, int32_t n_t,
+               int64_t *row_ptr, int32_t *csr_col, float *csr_val,
+               int64_t *col_ptr, int32_t *csc_row, float *csc_val,
+               int32_t *deg_r, int32_t *deg_c);
+
+/* Regularised objective of Section 3.2 (Eq. 2):
+ * sum over Omega* of (r - p_a . q_b)^2 + lambda (||P||_F^2 + ||Q||_F^2). */
+double or_loss(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+               int32_t m_t, int32_t n_t, int32_t k, const double *P, const double *Q,
+               double lambda);
+
+/* Full-gradient (Jacobi) descent on Eq. 2 for `epochs` epochs.
+ *   step: 0 = plain gradient step, 1 = per-row/column step scaled by
+ *         1/max(1, degree) (the 1/n normalisation of Eq. 5, applied to P and Q).
+ *   clip: asymmetric clipping of Section 5.3, d <- min(d, xi) per coordinate
+ *         of the descent direction (NaN propagates).
+ *   bf16: 1 = the dots and gradient products read bf16 (round-to-nearest-even)
+ *         copies of the factors; the fp64 master takes the update.
+ * P (m_t x k) and Q (n_t x k) are updated in place; loss_hist (epochs + 1
+ * doubles, may be NULL) receives L(P_t, Q_t) for t = 0..epochs.
+ * Returns 7 and stops (factors left at the last finite iterate) if an update
+ * produces a non-finite value, else 0. */
+int or_fit(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+           int32_t m_t, int32_t n_t, int32_t k, double *P, double *Q,
+           int32_t epochs, double lambda, double lr, int32_t step,
+           int32_t clip, double xi, int32_t bf16, double *loss_hist, int32_t *epochs_done);
+
+/* One-sided extension (Section 5.2, Eq. 6 in factored form): the fixed
+ * factors F_fixed (rows indexed by fixed_id) stay constant; each free row
+ * f in [0, n_free) starts at zero and takes `steps` gradient steps on
+ * sum_{entries of f} (r - F_fixed[id] . x_f)^2 + lambda ||x_f||^2. */
+int or_extend(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,
+              int32_t n_free, int32_t k, const double *F_fixed, double *F_free,
+              int32_t steps, double lambda, double lr, int32_t step, int32_t clip, double xi);
+
+/* Exact minimiser of the same per-row ridge problems (normal equations,
+ * Cholesky).  Returns 1 if a system is not positive definite. */
+int or_ridge(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,
+             int32_t n_free, int32_t k, const double *F_fixed, double lambda, double *F_free);
+
+/* Chunk partition of the free indices (Section 5.2: column chunks processed
+ * independently).  counts[f] = entries of free index f, in order.
+ * n_chunks > 0: exactly n_chunks runs (some may be empty); run j starts at
+ *   the first index f with at least ceil(j * total / n_chunks) entries in
+ *   indices before f.
+ * else: greedy runs of at most max_entries entries (a single index above the
+ *   cap forms its own chunk).
+ * bounds receives the start of every chunk plus the end (n_free); returns
+ * the number of chunks, or -1 if max_bounds is too small. */
+int32_t or_chunk_plan(const int64_t *counts, int64_t n_free, int32_t n_chunks,
+                      int64_t max_entries, int64_t *bounds, int32_t max_bounds);
+
+/* bf16 round-to-nearest-even of an fp32 value, returned as the 16-bit pattern. */
+uint16_t or_bf16_bits(float x);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

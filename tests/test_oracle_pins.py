@@ -1,0 +1,359 @@
+"""Pins of the fp64 CPU oracle to facts fixed by the paper and by mathematics,
+independent of the oracle's own code (CPU only).
+
+Each test names what it pins and why a plausible mistake in the oracle (a
+dropped term, a wrong sign or index, a transposed operand, a Gauss-Seidel
+instead of a Jacobi sweep) would fail it.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import tsid_synth as synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _full_cells(m, n):
+    a, b = np.nonzero(np.ones((m, n)))
+    return a.astype(np.int32), b.astype(np.int32)
+
+
+# ---------------------------------------------------------------- P0 golden
+def test_hand_derived_steps(oracle_lib):
+    """Single epochs derived by hand from Eqs. 2-5 and the clip of Section 5.3."""
+    g = json.load(open(os.path.join(GOLDEN, "hand_steps.json")))
+    one = np.zeros(1, np.int32)
+    for c in g["cases"]:
+        st, P, Q, h, _ = oracle_lib.fit(one, one, np.array([c["r"]], np.float32),
+                                        np.array([[c["p"]]]), np.array([[c["q"]]]), 1,
+                                        c["lambda"], c["lr"], c["step"], c["clip"], c["xi"])
+        assert st == 0, c["name"]
+        assert h[0] == pytest.approx(c["loss0"], rel=1e-15), c["name"]
+        assert P[0, 0] == pytest.approx(c["p1"], rel=1e-14), c["name"]
+        assert Q[0, 0] == pytest.approx(c["q1"], rel=1e-14), c["name"]
+    t = g["two_cells"]
+    cells = np.array(t["cells"])
+    st, P, Q, h, _ = oracle_lib.fit(cells[:, 0].astype(np.int32), cells[:, 1].astype(np.int32),
+                                    cells[:, 2].astype(np.float32), np.array(t["P"]),
+                                    np.array(t["Q"]), 1, t["lambda"], t["lr"], "degree")
+    assert st == 0
+    assert h[0] == pytest.approx(t["loss0"], rel=1e-15)
+    np.testing.assert_allclose(P, t["P1"], rtol=1e-14)
+    np.testing.assert_allclose(Q, t["Q1"], rtol=1e-14)
+
+
+# ------------------------------------------------------------ P1 gradient
+@pytest.mark.parametrize("step", ["sum", "degree"])
+def test_gradient_matches_central_differences(oracle_lib, step):
+    """Eqs. 3-4 summed over Omega* plus 2*lambda*x is the gradient of Eq. 2.
+    L is quadratic in any single coordinate, so a central difference of the
+    loss is exact up to rounding.  The gradient is read back from one oracle
+    epoch, (x0 - x1) / lr (times the degree for the degree step); the Q part
+    must be taken at (P_t, Q_t), which pins the simultaneous (Jacobi) update."""
+    p = synth.random_case(9, 7, 30, 9, 7, 3, seed=21, lam=0.3)
+    a, b, v = p.u, p.i, p.r  # template = everything (I, J are permutations)
+    st, rm, cm = oracle_lib.template_maps(p.m, p.n, p.I, p.J)
+    a, b, v = oracle_lib.filter_template(p.u, p.i, p.r, rm, cm)
+    P0 = p.P0.astype(np.float64)
+    Q0 = p.Q0.astype(np.float64)
+    lr = 1e-3
+    st, P1, Q1, h, _ = oracle_lib.fit(a, b, v, P0, Q0, 1, p.lam, lr, step)
+    assert st == 0
+    deg_r = np.bincount(a, minlength=P0.shape[0]).clip(1, None)[:, None]
+    deg_c = np.bincount(b, minlength=Q0.shape[0]).clip(1, None)[:, None]
+    gP = (P0 - P1) / lr
+    gQ = (Q0 - Q1) / lr
+    if step == "degree":
+        gP *= deg_r
+        gQ *= deg_c
+    h_ = 1e-3
+    for X, G, isP in ((P0, gP, True), (Q0, gQ, False)):
+        for idx in np.ndindex(*X.shape):
+            Xp, Xm = X.copy(), X.copy()
+            Xp[idx] += h_
+            Xm[idx] -= h_
+            if isP:
+                Lp = oracle_lib.loss(a, b, v, P0.shape[0], Q0.shape[0], Xp, Q0, p.lam)
+                Lm = oracle_lib.loss(a, b, v, P0.shape[0], Q0.shape[0], Xm, Q0, p.lam)
+            else:
+                Lp = oracle_lib.loss(a, b, v, P0.shape[0], Q0.shape[0], P0, Xp, p.lam)
+                Lm = oracle_lib.loss(a, b, v, P0.shape[0], Q0.shape[0], P0, Xm, p.lam)
+            fd = (Lp - Lm) / (2 * h_)
+            assert abs(fd - G[idx]) <= 1e-8 * max(1.0, abs(fd)), (isP, idx, fd, G[idx])
+    # the recorded loss is Eq. 2 at (P0, Q0), with the regularisation once per row
+    direct = sum((float(v[e]) - P0[a[e]] @ Q0[b[e]]) ** 2 for e in range(v.size))
+    direct += p.lam * ((P0 ** 2).sum() + (Q0 ** 2).sum())
+    assert h[0] == pytest.approx(direct, rel=1e-13)
+
+
+# ------------------------------------------------------- P2 closed form optimum
+def test_fully_observed_optimum_is_singular_value_soft_threshold(oracle_lib):
+    """Fully observed R (6 x 5), rank-k factors:  min ||R - P Q^T||^2 +
+    lambda(||P||^2 + ||Q||^2) equals min over rank<=k X of ||R - X||^2 +
+    2 lambda ||X||_*, solved by soft-thresholding the top k singular values at
+    lambda.  Optimal value and minimiser checked against numpy's SVD."""
+    g = np.random.default_rng(5)
+    R = g.standard_normal((6, 5)).astype(np.float32).astype(np.float64)
+    a, b = _full_cells(6, 5)
+    v = R[a, b].astype(np.float32)
+    U, S, Vt = np.linalg.svd(R)
+    k, lam = 3, 0.1
+    Lstar = sum(2 * lam * s - lam * lam if s > lam else s * s for s in S[:k]) + (S[k:] ** 2).sum()
+    X = U[:, :k] @ np.diag(np.maximum(S[:k] - lam, 0)) @ Vt[:k]
+    P0 = g.normal(0, 0.5, (6, k))
+    Q0 = g.normal(0, 0.5, (5, k))
+    st, P, Q, h, _ = oracle_lib.fit(a, b, v, P0, Q0, 3000, lam, 0.02, "sum")
+    assert st == 0
+    assert abs(h[-1] - Lstar) <= 1e-10 * Lstar
+    np.testing.assert_allclose(P @ Q.T, X, atol=1e-8)
+
+
+# ------------------------------------------------------ P3 least squares
+def test_extension_matches_least_squares(oracle_lib):
+    """With the fixed side held constant (Section 5.2, Eq. 6 in factored
+    form) each free row is a ridge regression: x = argmin sum (r - p.x)^2 +
+    lambda ||x||^2, i.e. the least-squares solution of [P_obs; sqrt(lambda) I]
+    x = [r; 0].  Both the gradient iteration and the Cholesky solve must reach
+    numpy.linalg.lstsq of that stacked system."""
+    g = np.random.default_rng(9)
+    m, n, k, lam = 6, 5, 3, 0.05
+    F = g.standard_normal((m, k))
+    R = g.standard_normal((m, n)).astype(np.float32)
+    mask = g.random((m, n)) < 0.8
+    mask[:, 0] = True
+    fixed, free = np.nonzero(mask)
+    v = R[fixed, free]
+    st, Xgd = oracle_lib.extend(fixed, free, v, n, F, 4000, lam, 0.3, "degree")
+    assert st == 0
+    st, Xch = oracle_lib.ridge(fixed, free, v, n, F, lam)
+    assert st == 0
+    for f in range(n):
+        rows = fixed[free == f]
+        A = np.vstack([F[rows], math.sqrt(lam) * np.eye(k)])
+        y = np.concatenate([R[rows, f].astype(np.float64), np.zeros(k)])
+        x = np.linalg.lstsq(A, y, rcond=None)[0]
+        np.testing.assert_allclose(Xch[f], x, rtol=1e-10, atol=1e-12)
+        np.testing.assert_allclose(Xgd[f], x, rtol=1e-8, atol=1e-10)
+
+
+# ------------------------------------------------------- P4 exact recovery
+def test_exact_recovery_noiseless_low_rank(oracle_lib):
+    """A noiseless rank-2 30 x 30 matrix with 60 % of cells observed is
+    recovered by the full-gradient fit (lambda = 0): held-out RMSE < 1e-6."""
+    R, u, i = synth.dense_lowrank_case(30, 30, 2, 0.6, seed=7)
+    R = R.astype(np.float32).astype(np.float64)
+    g = np.random.default_rng(1)
+    ho = g.random(u.size) < 0.1
+    a, b = u[~ho], i[~ho]
+    P0 = g.normal(0, 0.3, (30, 2))
+    Q0 = g.normal(0, 0.3, (30, 2))
+    st, P, Q, h, _ = oracle_lib.fit(a, b, R[a, b].astype(np.float32), P0, Q0, 20000, 0.0, 0.5,
+                                    "degree")
+    assert st == 0
+    pred = (P @ Q.T)[u[ho], i[ho]]
+    rmse = float(np.sqrt(np.mean((pred - R[u[ho], i[ho]]) ** 2)))
+    assert rmse < 1e-6
+
+
+# ------------------------------------------------------- P5 monotone descent
+@pytest.mark.parametrize("step,lr", [("sum", 0.02), ("degree", 0.15)])
+def test_monotone_descent_small_step(oracle_lib, step, lr):
+    """Full-gradient descent with a small step never increases Eq. 2 (the
+    degree step is gradient descent preconditioned by a positive diagonal)."""
+    p = synth.tiny()
+    st, rm, cm = oracle_lib.template_maps(p.m, p.n, p.I, p.J)
+    a, b, v = oracle_lib.filter_template(p.u, p.i, p.r, rm, cm)
+    st, P, Q, h, _ = oracle_lib.fit(a, b, v, p.P0, p.Q0, 200, p.lam, lr, step)
+    assert st == 0
+    assert np.all(np.diff(h) <= 0.0)
+    assert h[-1] < 0.01 * h[0]
+
+
+# ------------------------------------------------------- P7 TSID identity
+def test_tsid_skeleton_identity(oracle_lib):
+    """Theorem 1 (Section 3.1): for an exactly rank-k, fully observed R and
+    |I| = |J| = k with a nonsingular core, W_L R*_k W_R^T = R_k.  Checked twice:
+    (1) the theorem's own formula with U_1, V_1 from numpy's SVD; (2) the
+    method's pipeline in the oracle -- fit the k x k template to zero loss,
+    extend the free rows from the template columns, then every free column
+    from all rows (lambda = 0, exact ridge solves) -- reproduces R."""
+    k, m, n = 3, 12, 10
+    g = np.random.default_rng(11)
+    # integer factors: R is exactly rank k and exactly representable in fp32
+    R = (g.integers(-3, 4, (m, k)) @ g.integers(-3, 4, (n, k)).T).astype(np.float64)
+    I = np.array([1, 5, 8])
+    J = np.array([0, 4, 7])
+    assert np.linalg.matrix_rank(R) == k and abs(np.linalg.det(R[np.ix_(I, J)])) > 0.5
+    U, S, Vt = np.linalg.svd(R)
+    U1, V1 = U[:, :k], Vt[:k].T
+    WL = U1 @ np.linalg.inv(U1[I])
+    WR = V1 @ np.linalg.inv(V1[J])
+    np.testing.assert_allclose(WL @ R[np.ix_(I, J)] @ WR.T, R, atol=1e-9)
+
+    aa, bb = _full_cells(k, k)
+    core = R[np.ix_(I, J)]
+    g = np.random.default_rng(3)
+    st, P, Q, h, _ = oracle_lib.fit(aa, bb, core[aa, bb].astype(np.float32), g.normal(0, .5, (k, k)),
+                                    g.normal(0, .5, (k, k)), 20000, 0.0, 0.02, "sum")
+    assert st == 0 and h[-1] < 1e-24
+    free_rows = np.setdiff1d(np.arange(m), I)
+    Qfull = np.zeros((n, k))
+    Qfull[J] = Q
+    fr, fc = np.meshgrid(np.arange(free_rows.size), J, indexing="ij")
+    fr, fc = fr.ravel(), fc.ravel()
+    st, Pfree = oracle_lib.ridge(fc, fr, R[free_rows[fr], fc].astype(np.float32), free_rows.size,
+                                 Qfull, 0.0)
+    assert st == 0
+    Pfull = np.zeros((m, k))
+    Pfull[I] = P
+    Pfull[free_rows] = Pfree
+    free_cols = np.setdiff1d(np.arange(n), J)
+    rr, cc = np.meshgrid(np.arange(m), np.arange(free_cols.size), indexing="ij")
+    rr, cc = rr.ravel(), cc.ravel()
+    st, Qfree = oracle_lib.ridge(rr, cc, R[rr, free_cols[cc]].astype(np.float32), free_cols.size,
+                                 Pfull, 0.0)
+    assert st == 0
+    Qfull[free_cols] = Qfree
+    np.testing.assert_allclose(Pfull @ Qfull.T, R, atol=1e-6)
+
+
+# ---------------------------------------------------------------- P8 clip
+def test_clip_table_and_infinite_threshold(oracle_lib):
+    """Section 5.3: min(max(xi, -g), g) == min(g, xi) per coordinate: values
+    above xi become xi, the rest pass.  A one-cell problem (k = 1, lambda = 0,
+    q = 1, p = 0) has descent direction d = 2 r for p, so r sets d."""
+    xi = 0.1
+    one = np.zeros(1, np.int32)
+    for d in [-1.0, 0.0, xi / 2, xi, 2 * xi, 7.0]:
+        st, P, Q, h, _ = oracle_lib.fit(one, one, np.array([d / 2], np.float32),
+                                        np.array([[0.0]]), np.array([[1.0]]), 1, 0.0, 1.0, "sum",
+                                        True, xi)
+        assert st == 0
+        want = min(float(np.float32(d / 2)) * 2, xi)
+        assert P[0, 0] == want
+    # xi = +inf reproduces the unclipped trajectory bit for bit
+    p = synth.tiny()
+    st, rm, cm = oracle_lib.template_maps(p.m, p.n, p.I, p.J)
+    a, b, v = oracle_lib.filter_template(p.u, p.i, p.r, rm, cm)
+    r1 = oracle_lib.fit(a, b, v, p.P0, p.Q0, 10, p.lam, p.lr, "sum", False)
+    r2 = oracle_lib.fit(a, b, v, p.P0, p.Q0, 10, p.lam, p.lr, "sum", True, math.inf)
+    assert np.array_equal(r1[1], r2[1]) and np.array_equal(r1[2], r2[2])
+    assert np.array_equal(r1[3], r2[3])
+
+
+def test_nonfinite_stops_at_last_finite_iterate(oracle_lib):
+    """A step size that overflows ends the fit with status 7; the factors are
+    those of the last epoch whose update stayed finite."""
+    p = synth.tiny()
+    st, rm, cm = oracle_lib.template_maps(p.m, p.n, p.I, p.J)
+    a, b, v = oracle_lib.filter_template(p.u, p.i, p.r, rm, cm)
+    st, P, Q, h, done = oracle_lib.fit(a, b, v, p.P0, p.Q0, 100, p.lam, 1e6, "sum")
+    assert st == 7 and 0 < done < 100
+    st2, P2, Q2, h2, _ = oracle_lib.fit(a, b, v, p.P0, p.Q0, done, p.lam, 1e6, "sum")
+    assert st2 == 0 and np.array_equal(P, P2) and np.array_equal(Q, Q2)
+    assert np.all(np.isfinite(P)) and np.array_equal(h[:done + 1], h2, equal_nan=True)
+
+
+# ---------------------------------------------------------------- P9 bf16
+def test_bf16_round_to_nearest_even_matches_torch(oracle_lib):
+    """bf16 rounding of the factors (bf16 mode) is IEEE round-to-nearest-even,
+    checked bit for bit against torch's float32 -> bfloat16 conversion."""
+    torch = pytest.importorskip("torch")
+    g = np.random.default_rng(0)
+    bits = g.integers(0, 2 ** 32, 20000, dtype=np.uint64).astype(np.uint32)
+    ties = (g.integers(0, 2 ** 16, 2000, dtype=np.uint64).astype(np.uint32) << 16) | 0x8000
+    special = np.array([0x00000000, 0x80000000, 0x7F800000, 0xFF800000, 0x7F7FFFFF, 0x00000001,
+                        0x00008000, 0x00018000, 0x3F808000, 0x3F818000, 0x7F7F8000], np.uint32)
+    allb = np.concatenate([bits, ties, special])
+    f = allb.view(np.float32)
+    ref = torch.from_numpy(f.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    ours = np.array([oracle_lib.bf16_bits(float(x)) for x in f], np.uint16)
+    nan = np.isnan(f)
+    assert np.array_equal(ours[~nan], ref[~nan])
+    ours_f = (ours[nan].astype(np.uint32) << 16).view(np.float32)
+    assert np.all(np.isnan(ours_f))
+
+
+def test_bf16_mode_fit_tracks_fp64(oracle_lib):
+    """bf16 mode changes the products only by bf16 rounding (relative 2^-9):
+    on Tiny its loss history stays within 1 % of the fp64 run."""
+    p = synth.tiny()
+    st, rm, cm = oracle_lib.template_maps(p.m, p.n, p.I, p.J)
+    a, b, v = oracle_lib.filter_template(p.u, p.i, p.r, rm, cm)
+    h64 = oracle_lib.fit(a, b, v, p.P0, p.Q0, 30, p.lam, 0.02, "sum")[3]
+    h16 = oracle_lib.fit(a, b, v, p.P0, p.Q0, 30, p.lam, 0.02, "sum", bf16=True)[3]
+    np.testing.assert_allclose(h16, h64, rtol=1e-2)
+    assert not np.array_equal(h16, h64)
+
+
+# ------------------------------------------------------- P10 index work
+def test_template_maps_filter_and_buckets_brute_force(oracle_lib):
+    """Maps, Omega* and both bucket orders against Python dicts and sorted()."""
+    p = synth.random_case(23, 17, 150, 9, 6, 4, seed=3)
+    st, rm, cm = oracle_lib.template_maps(p.m, p.n, p.I, p.J)
+    assert st == 0
+    pos_r = {int(u): a for a, u in enumerate(p.I)}
+    pos_c = {int(i): b for b, i in enumerate(p.J)}
+    assert [pos_r.get(u, -1) for u in range(p.m)] == rm.tolist()
+    assert [pos_c.get(i, -1) for i in range(p.n)] == cm.tolist()
+    a, b, v = oracle_lib.filter_template(p.u, p.i, p.r, rm, cm)
+    want = [(pos_r[int(u)], pos_c[int(i)], float(r)) for u, i, r in zip(p.u, p.i, p.r)
+            if int(u) in pos_r and int(i) in pos_c]
+    assert list(zip(a.tolist(), b.tolist(), v.astype(np.float64).tolist())) == want
+    bk = oracle_lib.bucket(a, b, v, p.I.size, p.J.size)
+    csr = sorted(want)
+    assert bk["csr_col"].tolist() == [x[1] for x in csr]
+    assert bk["csr_val"].astype(np.float64).tolist() == [x[2] for x in csr]
+    csc = sorted(want, key=lambda x: (x[1], x[0]))
+    assert bk["csc_row"].tolist() == [x[0] for x in csc]
+    assert bk["csc_val"].astype(np.float64).tolist() == [x[2] for x in csc]
+    for ptr, deg, key, n_ in ((bk["row_ptr"], bk["deg_r"], 0, p.I.size),
+                              (bk["col_ptr"], bk["deg_c"], 1, p.J.size)):
+        cnt = [sum(1 for x in want if x[key] == j) for j in range(n_)]
+        assert deg.tolist() == cnt
+        assert ptr[0] == 0 and ptr[-1] == len(want)
+        assert np.all(np.diff(ptr) == deg)
+
+
+def test_validation_codes(oracle_lib):
+    """Out-of-range ids -> 2 (before duplicates), repeated ids / cells -> 3."""
+    assert oracle_lib.template_maps(5, 4, [0, 5], [0])[0] == 2
+    assert oracle_lib.template_maps(5, 4, [1, 1], [9])[0] == 2
+    assert oracle_lib.template_maps(5, 4, [1, 1], [0])[0] == 3
+    assert oracle_lib.template_maps(5, 4, [1, 2], [3, 3])[0] == 3
+    assert oracle_lib.check_omega(3, 3, [0, 1], [0, 3], [1.0, 1.0]) == 2
+    assert oracle_lib.check_omega(3, 3, [0, 1], [0, 1], [1.0, np.nan]) == 1
+    assert oracle_lib.check_omega(3, 3, [0, 1, 0], [0, 1, 0], [1.0, 1.0, 2.0]) == 3
+    assert oracle_lib.check_omega(3, 3, [0, 1, 2], [0, 1, 0], [1.0, 1.0, 2.0]) == 0
+
+
+def test_chunk_plan_definition(oracle_lib):
+    """Chunk boundaries against the definitions, computed another way
+    (binary search on the prefix sums; an explicit greedy walk)."""
+    g = np.random.default_rng(4)
+    for trial in range(20):
+        n_free = int(g.integers(0, 60))
+        counts = g.integers(0, 50, n_free) * (g.random(n_free) < 0.8)
+        if trial % 5 == 0 and n_free:
+            counts[g.integers(0, n_free)] = 5000
+        total = int(counts.sum())
+        excl = np.concatenate([[0], np.cumsum(counts)])
+        for K in (1, 3, 10):
+            bnd = oracle_lib.chunk_plan(counts, n_chunks=K)
+            want = [0] + [int(np.searchsorted(excl, -(-j * total // K), side="left"))
+                          for j in range(1, K)] + [n_free]
+            want = [min(x, n_free) for x in want]
+            assert bnd.tolist() == want
+        C = 120
+        bnd = oracle_lib.chunk_plan(counts, max_entries=C).tolist()
+        assert bnd[0] == 0 and bnd[-1] == n_free
+        for s, e in zip(bnd[:-1], bnd[1:]):
+            assert e > s
+            tot = int(counts[s:e].sum())
+            assert tot <= C or e - s == 1
+            if e < n_free:
+                assert tot + int(counts[e]) > C

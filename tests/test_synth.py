@@ -1,0 +1,57 @@
+"""Synthetic input generators: determinism, shapes and distributions (CPU)."""
+import numpy as np
+
+import tsid_synth as synth
+
+
+def test_tiny_shape_and_determinism():
+    a, b = synth.tiny(), synth.tiny()
+    for f in ("u", "i", "r", "tu", "ti", "tr", "I", "J", "P0", "Q0"):
+        assert np.array_equal(getattr(a, f), getattr(b, f))
+    assert a.nnz + a.tu.size == 40000
+    assert 0.08 < a.tu.size / 40000 < 0.12
+    assert a.I.size == 200 and a.J.size == 160 and np.all(np.diff(a.I) > 0)
+    keys = a.u.astype(np.int64) * a.n + a.i
+    assert np.unique(keys).size == keys.size
+    # unit-variance latent products plus N(0, 0.01) noise
+    assert 0.8 < np.var(a.r) < 1.3
+
+
+def test_holdout_is_a_keyed_hash_of_the_cell():
+    u = np.arange(100000, dtype=np.int32) % 977
+    i = np.arange(100000, dtype=np.int32) // 977
+    m1 = synth.holdout_mask(u, i, 1000, 5)
+    perm = np.random.default_rng(0).permutation(u.size)
+    m2 = synth.holdout_mask(u[perm], i[perm], 1000, 5)
+    assert np.array_equal(m1[perm], m2)
+    assert abs(m1.mean() - 0.1) < 0.005
+    assert not np.array_equal(m1, synth.holdout_mask(u, i, 1000, 6))
+
+
+def test_mid_zipf_popularity_and_template():
+    p = synth.mid()
+    assert p.nnz + p.tu.size == 2_000_000
+    keys = p.u.astype(np.int64) * p.n + p.i
+    assert np.unique(keys).size == keys.size
+    assert set(np.unique(p.r).tolist()) <= {1.0, 2.0, 3.0, 4.0, 5.0}
+    deg = np.bincount(p.u, minlength=p.m)
+    # most-observed template: degree descending, ids ascending on ties
+    d_t = deg[p.I]
+    assert np.all(np.diff(d_t) <= 0)
+    assert d_t[-1] >= np.sort(deg)[-p.I.size]
+    # Zipf column popularity: the rank-frequency slope of the unsaturated
+    # middle of the distribution is near -1 on a log-log scale
+    cdeg = np.sort(np.bincount(p.i, minlength=p.n))[::-1].astype(float)
+    ranks = np.arange(1, cdeg.size + 1)
+    sel = slice(200, 3000)
+    slope = np.polyfit(np.log(ranks[sel]), np.log(cdeg[sel]), 1)[0]
+    assert -1.3 < slope < -0.6
+
+
+def test_random_case_hot_buckets_in_template():
+    p = synth.random_case(40, 30, 200, 10, 8, 4, seed=3, hot_rows=2, hot_cols=1)
+    deg = np.bincount(p.u, minlength=p.m)
+    assert np.sum(deg[p.I] == p.n) >= 2
+    cdeg = np.bincount(p.i, minlength=p.n)
+    assert np.sum(cdeg[p.J] == p.m) >= 1
+    assert not np.all(np.diff(p.I) > 0)  # local ids follow array order, not sorted

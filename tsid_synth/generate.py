@@ -1,0 +1,323 @@
+"""Workload generators (data only; see the package docstring).
+
+Shapes and value models follow the five benchmark configurations:
+
+* ``tiny``        1,000 x 800, rank 8 + N(0, 0.01) noise, 40,000 uniform cells.
+* ``mid``         20,000 x 10,000, rank-32 latent model, ratings in {1..5},
+                  2.0 M cells with Zipf(1.0) row and column popularity.
+* ``rating``      480,189 x 17,770 (the Netflix Prize shape of Section 6.1),
+                  100 M cells, Zipf(0.9) rows / Zipf(1.1) columns, rank 64.
+* ``scientific``  200,000 x 200,000, rank 32 with singular values exp(-j/8),
+                  uniform 10 % observation; only the template block is drawn.
+
+Conventions: "N(0, v)" takes v as the variance, so latent factors drawn
+N(0, 1/sqrt(k)) give unit-variance products.  Held-out cells are chosen by a
+keyed hash of (u, i) so any row range can be regenerated on its own.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Callable, Dict, Optional
+
+import numpy as np
+
+PURPOSE = {
+    "factors": 1, "rows": 2, "cols": 3, "cells": 4, "values": 5, "noise": 6,
+    "holdout": 7, "template": 8, "init": 9, "order": 10, "extra": 11,
+}
+
+
+def make_rng(seed: int, purpose: str) -> np.random.Generator:
+    """Philox stream keyed by (seed, purpose)."""
+    return np.random.Generator(
+        np.random.Philox(np.random.SeedSequence([int(seed), PURPOSE[purpose]])))
+
+
+def _splitmix64(x: np.ndarray) -> np.ndarray:
+    """SplitMix64 finaliser (Steele, Lea and Flood, 2014) on uint64 arrays."""
+    with np.errstate(over="ignore"):
+        z = x + np.uint64(0x9E3779B97F4A7C15)
+        z = (z ^ (z >> np.uint64(30))) * np.uint64(0xBF58476D1CE4E5B9)
+        z = (z ^ (z >> np.uint64(27))) * np.uint64(0x94D049BB133111EB)
+        return z ^ (z >> np.uint64(31))
+
+
+def _cell_hash(u: np.ndarray, i: np.ndarray, n: int, seed: int, purpose: str) -> np.ndarray:
+    key = u.astype(np.uint64) * np.uint64(n) + i.astype(np.uint64)
+    salt = _splitmix64(np.array([seed * 1000003 + PURPOSE[purpose]], dtype=np.uint64))[0]
+    return _splitmix64(key ^ salt)
+
+
+def _hash_below(h: np.ndarray, frac: float) -> np.ndarray:
+    return (h >> np.uint64(11)) < np.uint64(int(frac * (1 << 53)))
+
+
+def holdout_mask(u: np.ndarray, i: np.ndarray, n: int, seed: int, frac: float = 0.1) -> np.ndarray:
+    """True for the ~frac share of cells held out for RMSE (keyed hash of (u, i))."""
+    return _hash_below(_cell_hash(u, i, n, seed, "holdout"), frac)
+
+
+def init_factors(m_t: int, n_t: int, k: int, seed: int):
+    """Initial factors P0, Q0 ~ N(0, 1/sqrt(k)) (variance), fp32."""
+    g = make_rng(seed, "init")
+    sd = k ** -0.25
+    P0 = g.normal(0.0, sd, (m_t, k)).astype(np.float32)
+    Q0 = g.normal(0.0, sd, (n_t, k)).astype(np.float32)
+    return P0, Q0
+
+
+@dataclasses.dataclass
+class Problem:
+    """One workload: the training cells of Omega, a held-out split, the
+    template index sets (array order = local ids) and the fit settings."""
+    name: str
+    m: int
+    n: int
+    u: np.ndarray          # int32, training cells (row ids)
+    i: np.ndarray          # int32, training cells (column ids)
+    r: np.ndarray          # float32 values
+    tu: np.ndarray         # held-out cells
+    ti: np.ndarray
+    tr: np.ndarray
+    I: np.ndarray          # int32 template rows, local order
+    J: np.ndarray          # int32 template columns, local order
+    k: int
+    lam: float
+    lr: float
+    epochs: int
+    step: str              # "sum" | "degree"
+    prec: str              # "fp32" | "bf16"
+    clip: bool
+    xi: float
+    P0: np.ndarray         # float32 (len(I), k)
+    Q0: np.ndarray         # float32 (len(J), k)
+    extra: dict = dataclasses.field(default_factory=dict)
+
+    @property
+    def nnz(self) -> int:
+        return int(self.u.shape[0])
+
+
+def _split(u, i, r, n, seed):
+    ho = holdout_mask(u, i, n, seed)
+    tr = ~ho
+    return (u[tr], i[tr], r[tr]), (u[ho], i[ho], r[ho])
+
+
+def _zipf_cdf(size: int, s: float, g: np.random.Generator) -> np.ndarray:
+    """Popularity Zipf(s) by rank, ranks assigned through a seeded permutation."""
+    perm = g.permutation(size)
+    w = np.empty(size, dtype=np.float64)
+    w[perm] = 1.0 / np.power(np.arange(1, size + 1, dtype=np.float64), s)
+    c = np.cumsum(w)
+    return c / c[-1]
+
+
+def _distinct_zipf_cells(m, n, target, cdf_r, cdf_c, g):
+    """Exactly `target` distinct cells drawn pairwise from the two
+    popularity laws; repeated draws of a cell are discarded and topped up."""
+    keys = np.empty(0, dtype=np.int64)
+    while keys.size < target:
+        need = target - keys.size
+        batch = int(need * 1.25) + 4096
+        u = np.searchsorted(cdf_r, g.random(batch), side="right").clip(0, m - 1)
+        i = np.searchsorted(cdf_c, g.random(batch), side="right").clip(0, n - 1)
+        keys = np.unique(np.concatenate([keys, u.astype(np.int64) * n + i]))
+    if keys.size > target:
+        keys = np.sort(keys[g.choice(keys.size, target, replace=False)])
+    return keys
+
+
+def _most_observed(ids_deg: np.ndarray, count: int) -> np.ndarray:
+    """Indices of the `count` largest degrees, ordered (degree desc, id asc)."""
+    ids = np.arange(ids_deg.size)
+    order = np.lexsort((ids, -ids_deg.astype(np.int64)))
+    return order[:count].astype(np.int32)
+
+
+def _latent_values(u, i, A, B, chunk=1 << 22):
+    out = np.empty(u.size, dtype=np.float64)
+    for s in range(0, u.size, chunk):
+        e = min(u.size, s + chunk)
+        out[s:e] = np.einsum("ij,ij->i", A[u[s:e]], B[i[s:e]])
+    return out
+
+
+def _finish(name, m, n, u, i, r, seed, I, J, k, settings, extra=None) -> Problem:
+    (u_, i_, r_), (tu, ti, tr) = _split(u, i, r, n, seed)
+    P0, Q0 = init_factors(I.size, J.size, k, seed)
+    return Problem(name=name, m=m, n=n, u=u_.astype(np.int32), i=i_.astype(np.int32),
+                   r=r_.astype(np.float32), tu=tu.astype(np.int32), ti=ti.astype(np.int32),
+                   tr=tr.astype(np.float32), I=I.astype(np.int32), J=J.astype(np.int32), k=k,
+                   P0=P0, Q0=Q0, extra=extra or {}, **settings)
+
+
+# Fit settings per workload.  Step sizes were fixed once by a sweep of the
+# fp64 oracle for a monotone loss (the paper sweeps but does not fix them).
+SETTINGS = {
+    "tiny": dict(lam=1e-3, lr=0.05, epochs=50, step="sum", prec="fp32", clip=False, xi=0.1),
+    "mid": dict(lam=1e-3, lr=0.15, epochs=100, step="degree", prec="fp32", clip=False, xi=0.1),
+    "rating": dict(lam=1e-3, lr=0.5, epochs=20, step="degree", prec="bf16", clip=True, xi=0.1),
+    "scientific": dict(lam=1e-3, lr=0.5, epochs=20, step="degree", prec="fp32", clip=False, xi=0.1),
+}
+
+
+def tiny(seed: int = 1) -> Problem:
+    """1,000 x 800, R = P* Q*^T + N(0, 0.01), 5 % of cells uniform; template
+    200 rows x 160 columns drawn uniformly, ascending."""
+    m, n, k, nnz = 1000, 800, 8, 40000
+    gf = make_rng(seed, "factors")
+    sd = k ** -0.25
+    A = gf.normal(0.0, sd, (m, k))
+    B = gf.normal(0.0, sd, (n, k))
+    flat = make_rng(seed, "cells").choice(m * n, nnz, replace=False)
+    u, i = flat // n, flat % n
+    r = _latent_values(u, i, A, B) + make_rng(seed, "noise").normal(0.0, 0.1, nnz)
+    gt = make_rng(seed, "template")
+    I = np.sort(gt.choice(m, 200, replace=False))
+    J = np.sort(gt.choice(n, 160, replace=False))
+    return _finish("tiny", m, n, u, i, r, seed, I, J, k, SETTINGS["tiny"])
+
+
+def _zipf_rating_problem(name, seed, m, n, nnz, s_row, s_col, rank, m_t, n_t, settings):
+    cdf_r = _zipf_cdf(m, s_row, make_rng(seed, "rows"))
+    cdf_c = _zipf_cdf(n, s_col, make_rng(seed, "cols"))
+    keys = _distinct_zipf_cells(m, n, nnz, cdf_r, cdf_c, make_rng(seed, "cells"))
+    keys = keys[make_rng(seed, "order").permutation(keys.size)]
+    u = (keys // n).astype(np.int32)
+    i = (keys % n).astype(np.int32)
+    del keys
+    gf = make_rng(seed, "factors")
+    sd = rank ** -0.25
+    A = gf.normal(0.0, sd, (m, rank)).astype(np.float32)
+    B = gf.normal(0.0, sd, (n, rank)).astype(np.float32)
+    x = _latent_values(u, i, A, B)
+    r = np.rint(np.clip(3.0 + x, 1.0, 5.0))
+    del x
+    tr_mask = ~holdout_mask(u, i, n, seed)
+    I = _most_observed(np.bincount(u[tr_mask], minlength=m), m_t)
+    J = _most_observed(np.bincount(i[tr_mask], minlength=n), n_t)
+    return _finish(name, m, n, u, i, r, seed, I, J, rank, settings)
+
+
+def mid(seed: int = 2) -> Problem:
+    """20,000 x 10,000, rank-32 latent model, integer ratings 1..5, 2.0 M cells
+    with Zipf(1.0) rows and columns; template = top 4,096 x 2,048 by degree."""
+    return _zipf_rating_problem("mid", seed, 20000, 10000, 2_000_000, 1.0, 1.0, 32,
+                                4096, 2048, SETTINGS["mid"])
+
+
+def rating(seed: int = 3, scale: float = 1.0) -> Problem:
+    """Netflix-Prize-shaped: 480,189 x 17,770, 100 M ratings 1..5, rank 64,
+    Zipf(0.9) rows / Zipf(1.1) columns; template 65,536 x 8,192 most observed.
+    `scale` < 1 shrinks every size proportionally (test use)."""
+    m = max(64, int(480189 * scale))
+    n = max(64, int(17770 * scale))
+    nnz = max(1000, int(100_000_000 * scale * scale))
+    m_t = max(16, int(65536 * scale))
+    n_t = max(16, int(8192 * scale))
+    return _zipf_rating_problem("rating", seed, m, n, nnz, 0.9, 1.1, 64, m_t, n_t,
+                                SETTINGS["rating"])
+
+
+def scientific_template(seed: int = 4, side: int = 16384, m: int = 200000) -> Problem:
+    """200,000 x 200,000 with r_ui = sum_j a_uj s_j b_ij / ||s||, a, b ~ N(0, 1),
+    s_j = exp(-j/8), j < 32, each cell observed with probability 0.1 (keyed
+    hash).  Only the side x side uniform template block is drawn: membership is
+    a per-cell hash, so this block is exactly the template part of the full
+    matrix's Omega."""
+    n = m
+    k = 32
+    gt = make_rng(seed, "template")
+    I = np.sort(gt.choice(m, side, replace=False)).astype(np.int32)
+    J = np.sort(gt.choice(n, side, replace=False)).astype(np.int32)
+    gf = make_rng(seed, "factors")
+    sig = np.exp(-np.arange(k) / 8.0)
+    sig = sig / np.linalg.norm(sig)
+    A = gf.standard_normal((m, k)).astype(np.float32)
+    B = gf.standard_normal((n, k)).astype(np.float32)
+    us, is_ = [], []
+    rows_per = max(1, (1 << 24) // side)
+    for a0 in range(0, side, rows_per):
+        a1 = min(side, a0 + rows_per)
+        uu = np.repeat(I[a0:a1], side)
+        ii = np.tile(J, a1 - a0)
+        keep = _hash_below(_cell_hash(uu, ii, n, seed, "cells"), 0.1)
+        us.append(uu[keep])
+        is_.append(ii[keep])
+    u = np.concatenate(us)
+    i = np.concatenate(is_)
+    perm = make_rng(seed, "order").permutation(u.size)
+    u, i = u[perm], i[perm]
+    Bs = (B * sig[None, :].astype(np.float32))
+    r = _latent_values(u, i, A, Bs)
+    return _finish("scientific", m, n, u, i, r, seed, I, J, k, SETTINGS["scientific"],
+                   extra={"omega_scope": "template block only"})
+
+
+def random_case(m: int, n: int, nnz: int, m_t: int, n_t: int, k: int, seed: int,
+                hot_rows: int = 0, hot_cols: int = 0, lam: float = 1e-3, lr: float = 0.2,
+                epochs: int = 5, step: str = "degree", prec: str = "fp32", clip: bool = False,
+                xi: float = 0.1, holdout: bool = False) -> Problem:
+    """Small ragged case for parity tests: `nnz` distinct uniform cells plus
+    `hot_rows` fully observed rows and `hot_cols` fully observed columns (so
+    buckets far longer than the rest exist); values N(0, 1); the template
+    index sets are drawn in random (not ascending) order."""
+    g = make_rng(seed, "cells")
+    nnz = min(nnz, m * n)
+    flat = g.choice(m * n, nnz, replace=False).astype(np.int64)
+    extra = []
+    if hot_rows:
+        for u0 in g.choice(m, hot_rows, replace=False):
+            extra.append(u0 * n + np.arange(n, dtype=np.int64))
+    if hot_cols:
+        for i0 in g.choice(n, hot_cols, replace=False):
+            extra.append(np.arange(m, dtype=np.int64) * n + i0)
+    if extra:
+        flat = np.unique(np.concatenate([flat] + extra))
+        flat = flat[make_rng(seed, "order").permutation(flat.size)]
+    u, i = flat // n, flat % n
+    r = make_rng(seed, "values").standard_normal(flat.size)
+    gt = make_rng(seed, "template")
+    I = gt.choice(m, m_t, replace=False)
+    J = gt.choice(n, n_t, replace=False)
+    if hot_rows or hot_cols:
+        # put the fully observed rows/columns into the template so its buckets are long
+        hr = np.unique(u[np.bincount(u, minlength=m)[u] == n]) if hot_rows else np.empty(0, int)
+        hc = np.unique(i[np.bincount(i, minlength=n)[i] == m]) if hot_cols else np.empty(0, int)
+        I = np.concatenate([hr, I[~np.isin(I, hr)]])[:m_t]
+        J = np.concatenate([hc, J[~np.isin(J, hc)]])[:n_t]
+        I = I[make_rng(seed, "extra").permutation(I.size)]
+        J = J[make_rng(seed, "extra").permutation(J.size)]
+    settings = dict(lam=lam, lr=lr, epochs=epochs, step=step, prec=prec, clip=clip, xi=xi)
+    if holdout:
+        return _finish("random", m, n, u, i, r, seed, I, J, k, settings)
+    P0, Q0 = init_factors(I.size, J.size, k, seed)
+    e = np.empty(0, np.int32)
+    return Problem(name="random", m=m, n=n, u=u.astype(np.int32), i=i.astype(np.int32),
+                   r=r.astype(np.float32), tu=e, ti=e, tr=np.empty(0, np.float32),
+                   I=I.astype(np.int32), J=J.astype(np.int32), k=k, P0=P0, Q0=Q0, **settings)
+
+
+def dense_lowrank_case(m: int, n: int, rank: int, frac: float, seed: int):
+    """Noiseless rank-`rank` matrix R = A B^T (A, B ~ N(0, 1/sqrt(rank))) and a
+    uniform set of observed cells covering `frac` of R (frac = 1: all).
+    Returns (R, u, i)."""
+    g = make_rng(seed, "factors")
+    sd = rank ** -0.25
+    A = g.normal(0.0, sd, (m, rank))
+    B = g.normal(0.0, sd, (n, rank))
+    R = A @ B.T
+    cnt = int(round(frac * m * n))
+    flat = np.sort(make_rng(seed, "cells").choice(m * n, cnt, replace=False))
+    return R, (flat // n).astype(np.int32), (flat % n).astype(np.int32)
+
+
+CONFIGS: Dict[str, Callable[..., Problem]] = {
+    "tiny": tiny, "mid": mid, "rating": rating, "scientific": scientific_template,
+}
+
+
+def make(name: str, seed: Optional[int] = None, **kw) -> Problem:
+    fn = CONFIGS[name]
+    return fn(**kw) if seed is None else fn(seed=seed, **kw)
