@@ -369,14 +369,16 @@ int32_t or_chunk_plan(const int64_t *counts, int64_t n_free, int32_t n_chunks,
     if (max_bounds < 1) return -1;
     bounds[nb++] = 0;
     if (n_free == 0) return 0;
-    int64_t in_chunk = 0;
+    int64_t in_chunk = 0, rows_in_chunk = 0;
     for (int64_t f = 0; f < n_free; ++f) {
-        if (in_chunk > 0 && in_chunk + counts[f] > max_entries) {
+        if (rows_in_chunk > 0 && in_chunk + counts[f] > max_entries) {
             if (nb >= max_bounds) return -1;
             bounds[nb++] = f;
             in_chunk = 0;
+            rows_in_chunk = 0;
         }
         in_chunk += counts[f];
+        rows_in_chunk += 1;
     }
     if (nb >= max_bounds) return -1;
     bounds[nb++] = n_free;
