@@ -1,0 +1,217 @@
+/*
+ * tsid.h -- C ABI of libtsid, the MI355X (gfx950) implementation of the
+ * data-parallel hot path of TSID matrix completion (arXiv 2608.00977,
+ * "TIDE-MC"): the template fit of Stage I and the chunked one-sided extension
+ * of Stage II.
+ *
+ * Problem statement (Definition 1, Section 2): R is m x n; the observed cells
+ * Omega are given as COO triples (u, i, r) with 0 <= u < m, 0 <= i < n, each
+ * cell at most once.  A template is fixed by index sets I (rows) and J
+ * (columns) (Section 3.1); Omega* is the part of Omega inside I x J
+ * (Section 3.2).  Local ids follow the array order of I and J: row I[a] of R is
+ * template row a.
+ *
+ * Conventions for every call:
+ *  - Every call returns a tsid_status; TSID_OK == 0.  Calls on one context are
+ *    not thread-safe; separate contexts are independent.
+ *  - The caller owns every pointer it passes.  The context owns all device
+ *    memory it allocates (maps, buckets, staging, factor copies, scratch) and
+ *    frees it in tsid_destroy.
+ *  - "HOST" pointers are CPU memory (pinned memory is faster for the bulk
+ *    arrays); "DEVICE" pointers are device memory on the context's device.
+ *  - Factor matrices are row-major fp32 with k columns.
+ *  - Arguments are validated before any device work.  On failure the outputs
+ *    and the context are unchanged, except for TSID_E_NONFINITE (see
+ *    tsid_fit_template) and errors reported by tsid_sync.
+ *  - TSID_E_DEVICE: a HIP call failed; tsid_last_error gives the detail.
+ */
+#ifndef TSID_H
+#define TSID_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct tsid_ctx tsid_ctx;
+
+typedef enum {
+    TSID_OK = 0,
+    TSID_E_INVAL = 1,     /* bad argument: NULL pointer, size < 0, unsupported k, bad option */
+    TSID_E_RANGE = 2,     /* an index outside [0, m) / [0, n) / [0, n_fixed) / [0, n_free) */
+    TSID_E_DUP = 3,       /* a repeated template id, or a repeated cell (Omega is a set) */
+    TSID_E_NOMEM = 4,     /* device allocation failed or would exceed max_device_bytes */
+    TSID_E_DEVICE = 5,    /* HIP runtime error */
+    TSID_E_STATE = 6,     /* call out of order (e.g. fit before build) */
+    TSID_E_NONFINITE = 7  /* a factor update produced Inf or NaN */
+} tsid_status;
+
+typedef enum { TSID_FP32 = 0, TSID_BF16 = 1 } tsid_precision;
+
+/* Per-row step normalisation.  SUM: the plain full gradient of Eq. 2.
+ * DEGREE: the step of every factor row is divided by max(1, its number of
+ * observed cells) -- the 1/n normalisation of Eq. 5 (Section 5.1), applied to
+ * both P and Q. */
+typedef enum { TSID_STEP_SUM = 0, TSID_STEP_DEGREE = 1 } tsid_step;
+
+/* Fit options.
+ *  epochs  number of full-gradient epochs (>= 0).
+ *  lambda  l2 weight of Eq. 2 (>= 0).   lr  step size eta (> 0).
+ *  clip    1: asymmetric clipping of Section 5.3 -- each coordinate of the
+ *          descent direction d becomes min(d, clip_xi) (positive components
+ *          are capped, negative ones pass; NaN propagates).  clip_xi > 0.
+ *  prec    TSID_FP32: fp32 factors.  TSID_BF16: the products read bf16
+ *          (round-to-nearest-even) copies of the factors, accumulate in fp32,
+ *          and an fp32 master copy takes the update (the mixed precision of
+ *          Section 5.3, with bf16 in place of fp16).
+ *  step    tsid_step. */
+typedef struct {
+    int32_t epochs;
+    float lambda;
+    float lr;
+    float clip_xi;
+    int32_t clip;
+    int32_t prec;
+    int32_t step;
+} tsid_fit_opts;
+
+/* Create a context on HIP device `device`.  hip_stream: a hipStream_t to run
+ * the compute work on (for example torch's current stream), or NULL for a
+ * stream owned by the context.  The context creates two more streams (host to
+ * device copies, device to host copies), all at the default priority.
+ * max_device_bytes: cap on the context's device allocations, 0 = no cap.
+ * Errors: E_INVAL (out == NULL), E_DEVICE (bad device id or HIP failure). */
+tsid_status tsid_create(int device, void *hip_stream, size_t max_device_bytes, tsid_ctx **out);
+
+/* Release every resource of the context (waits for outstanding work first).
+ * NULL is ignored. */
+void tsid_destroy(tsid_ctx *ctx);
+
+/* Detail of the last failure on this context (static storage owned by the
+ * context; empty string if none). */
+const char *tsid_last_error(const tsid_ctx *ctx);
+
+/* Build the resident template (Section 3.2; Section 5.1 "Sampling the TSID
+ * Template Submatrix"): template maps from I and J, the filter of Omega to
+ * Omega* with local ids, and the buckets of Omega* by row (sorted by (a, b))
+ * and by column (sorted by (b, a)).  Replaces any previous template.
+ *  m, n          matrix shape (1 <= m, n < 2^31).
+ *  u, i, r       HOST, nnz entries of Omega (COO).  Streamed to the device in
+ *                pieces of stage_entries entries (0 = library default).
+ *  I, J          HOST, m_t and n_t template ids (0 <= m_t <= m, 0 <= n_t <= n).
+ *  k             rank; one of 8, 16, 32, 64, 128.
+ * Errors: E_INVAL (NULL with a nonzero size, nnz < 0, bad k, non-finite r in
+ * the template), E_RANGE (an id of I, J, u or i out of range), E_DUP (a
+ * repeated id in I or J, or a repeated cell inside the template), E_NOMEM,
+ * E_DEVICE.  Synchronous. */
+tsid_status tsid_build_template(tsid_ctx *ctx, int64_t m, int64_t n,
+                                const int32_t *u, const int32_t *i, const float *r, int64_t nnz,
+                                const int32_t *I, int32_t m_t, const int32_t *J, int32_t n_t,
+                                int32_t k, int64_t stage_entries);
+
+/* Sizes of the current template: rows m_t, columns n_t, |Omega*|, rank k.
+ * Any output pointer may be NULL.  E_STATE before a build. */
+tsid_status tsid_template_info(const tsid_ctx *ctx, int32_t *m_t, int32_t *n_t, int64_t *nnz,
+                               int32_t *k);
+
+/* Template fit (Stage I, Sections 3.2 and 5.1): opts->epochs full-gradient
+ * epochs on the objective of Eq. 2 over Omega*,
+ *   L(P, Q) = sum_(a,b) (r_ab - p_a . q_b)^2 + lambda (||P||_F^2 + ||Q||_F^2).
+ * Epoch t computes every residual and both gradients (Eqs. 3-4) at (P_t, Q_t)
+ * and moves every row of P and Q at once against its gradient (Eq. 5 with the
+ * step of opts->step and the clip of opts->clip).  Each factor row is written
+ * once per epoch by the unit that owns it; no atomic operations touch factor
+ * or gradient memory, and the result is bitwise reproducible.
+ *  P   DEVICE m_t x k: P_0 on entry, P_T on return.
+ *  Q   DEVICE n_t x k: Q_0 on entry, Q_T on return.
+ *  loss_hist  HOST epochs + 1 doubles or NULL: L(P_t, Q_t) for t = 0..epochs.
+ * Errors: E_STATE (no template), E_INVAL (NULL factors with m_t or n_t > 0,
+ * bad options), E_NOMEM, E_DEVICE, E_NONFINITE: some update of epoch t was not
+ * finite; P and Q then hold P_t and Q_t (the last finite iterate), loss_hist
+ * holds L for 0..t and NaN after.  Synchronous. */
+tsid_status tsid_fit_template(tsid_ctx *ctx, float *P, float *Q, const tsid_fit_opts *opts,
+                              double *loss_hist);
+
+/* Epochs completed by the last tsid_fit_template on this context: opts->epochs
+ * after success, t after TSID_E_NONFINITE (P and Q were returned at P_t, Q_t),
+ * 0 before any fit.  Errors: E_INVAL (ctx or epochs NULL). */
+tsid_status tsid_fit_epochs_done(const tsid_ctx *ctx, int32_t *epochs);
+
+/* Objective of Eq. 2 over the template's Omega* at (P, Q) (DEVICE, fp32),
+ * accumulated in fp64 in a fixed order.  With lambda = 0 it is the residual
+ * sum of squares (used for held-out RMSE on a template built over test cells).
+ * Errors: E_STATE, E_INVAL (NULL factors, out == NULL, lambda < 0), E_DEVICE.
+ * Synchronous. */
+tsid_status tsid_loss(tsid_ctx *ctx, const float *P, const float *Q, float lambda, double *out);
+
+/* One chunk of the extension (Stage II, Section 5.2; Eq. 6 in factored form:
+ * a free row's coefficients x_f solve the ridge problem
+ *   min sum_(entries of f) (r - F_fixed[fixed_id] . x_f)^2 + lambda ||x_f||^2
+ * with the fixed factors held constant).  Every free row starts at zero and
+ * takes opts->epochs gradient steps with the same residual/gradient kernel as
+ * the template fit (opts->step, opts->clip apply; opts->prec is ignored: the
+ * fixed side is read in fp32).
+ *  side        0: the free rows are rows of R and F_fixed holds column
+ *              factors; 1: the free rows are columns and F_fixed holds row
+ *              factors.  The arithmetic is the same; side is recorded only.
+ *  fixed_id    HOST nnz ids into F_fixed (0 <= id < n_fixed).
+ *  free_local  HOST nnz ids of the free rows (0 <= f < n_free).
+ *  r           HOST nnz values.
+ *  F_fixed     DEVICE n_fixed x k (k of the current template), read only;
+ *              must stay unchanged until the chunk completes.
+ *  F_free      HOST n_free x k, written when the chunk completes.
+ * Asynchronous: the chunk's host-to-device copy runs on the context's copy
+ * stream while the previous chunk computes, and the results return on a third
+ * stream (Section 5.2, double-buffered pipelining); at most two chunks are in
+ * flight and the call blocks only while both staging slots are busy.  All
+ * host buffers must stay valid and unchanged until tsid_sync returns.  Pinned
+ * host memory is needed for the copies to overlap.
+ * Errors returned here: E_STATE (no template: k unknown), E_INVAL, E_NOMEM,
+ * E_DEVICE.  Errors found on the device (E_RANGE for ids out of range, E_DUP
+ * for a repeated (fixed_id, free_local) cell, E_NONFINITE) are returned by the
+ * next tsid_sync; the affected chunk's F_free is then unspecified. */
+tsid_status tsid_extend_chunk(tsid_ctx *ctx, int side, const int32_t *fixed_id,
+                              const int32_t *free_local, const float *r, int64_t nnz,
+                              int32_t n_free, const float *F_fixed, int64_t n_fixed,
+                              float *F_free, const tsid_fit_opts *opts);
+
+/* Wait for every outstanding chunk; returns the first device-side error of
+ * those chunks (and clears it), else TSID_OK. */
+tsid_status tsid_sync(tsid_ctx *ctx);
+
+/* Index structures of the current template, copied to host_dst (HOST) for
+ * bit-exact checks.  which / element type / count:
+ *   TSID_IDX_ROW_MAP int32 m      TSID_IDX_COL_MAP int32 n
+ *   TSID_IDX_ROW_PTR int64 m_t+1  TSID_IDX_CSR_COL int32 nnz  TSID_IDX_CSR_VAL fp32 nnz
+ *   TSID_IDX_COL_PTR int64 n_t+1  TSID_IDX_CSC_ROW int32 nnz  TSID_IDX_CSC_VAL fp32 nnz
+ *   TSID_IDX_DEG_R   int32 m_t    TSID_IDX_DEG_C   int32 n_t
+ * bytes must equal count * element size.  Errors: E_STATE, E_INVAL, E_DEVICE. */
+enum {
+    TSID_IDX_ROW_MAP = 0, TSID_IDX_COL_MAP = 1, TSID_IDX_ROW_PTR = 2, TSID_IDX_CSR_COL = 3,
+    TSID_IDX_CSR_VAL = 4, TSID_IDX_COL_PTR = 5, TSID_IDX_CSC_ROW = 6, TSID_IDX_CSC_VAL = 7,
+    TSID_IDX_DEG_R = 8, TSID_IDX_DEG_C = 9
+};
+tsid_status tsid_export_index(const tsid_ctx *ctx, int which, void *host_dst, size_t bytes);
+
+/* Chunk partition of the free rows (Section 5.2: the matrix is split into
+ * chunks of whole rows/columns processed independently).  Host-only, needs no
+ * context or device.  counts[f] (HOST, n_free values >= 0) = observed cells
+ * of free row f, in order.
+ *  n_chunks > 0: exactly n_chunks contiguous runs (some may be empty); run j
+ *    starts at the first f that has at least ceil(j * total / n_chunks) cells
+ *    in the rows before it.
+ *  n_chunks == 0: greedy runs of at most max_entries cells (> 0); a single
+ *    row above the cap forms its own run.
+ * bounds (HOST, max_bounds entries) receives the start of every run followed
+ * by n_free.  Returns the number of runs, or -1 on a bad argument or when
+ * max_bounds is too small. */
+int32_t tsid_chunk_plan(const int64_t *counts, int64_t n_free, int32_t n_chunks,
+                        int64_t max_entries, int64_t *bounds, int32_t max_bounds);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TSID_H */

@@ -1,0 +1,265 @@
+"""ctypes binding of libtsid (``include/tsid.h``).
+
+Argument marshalling only: every step of the path runs in the HIP library.
+The functions named ``tsid_*`` mirror the C entry points one to one; the
+:class:`Tsid` class wraps a context for callers holding numpy host arrays
+and torch device tensors.  PyTorch is used for device memory, pinned host
+memory and streams, nothing else.
+
+The library must be built first (``python -m paper_2608_00977_amd.build``);
+loading fails loudly when it is missing -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+import numpy as np
+import torch  # imported before libtsid so both share one HIP runtime
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtsid.so")
+
+STATUS = {0: "TSID_OK", 1: "TSID_E_INVAL", 2: "TSID_E_RANGE", 3: "TSID_E_DUP",
+          4: "TSID_E_NOMEM", 5: "TSID_E_DEVICE", 6: "TSID_E_STATE", 7: "TSID_E_NONFINITE"}
+OK, E_INVAL, E_RANGE, E_DUP, E_NOMEM, E_DEVICE, E_STATE, E_NONFINITE = range(8)
+FP32, BF16 = 0, 1
+STEP_SUM, STEP_DEGREE = 0, 1
+IDX = {"row_map": 0, "col_map": 1, "row_ptr": 2, "csr_col": 3, "csr_val": 4, "col_ptr": 5,
+       "csc_row": 6, "csc_val": 7, "deg_r": 8, "deg_c": 9}
+
+
+class TsidError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str = ""):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)} {detail}".strip())
+
+
+class tsid_fit_opts(C.Structure):
+    _fields_ = [("epochs", C.c_int32), ("lambda_", C.c_float), ("lr", C.c_float),
+                ("clip_xi", C.c_float), ("clip", C.c_int32), ("prec", C.c_int32),
+                ("step", C.c_int32)]
+
+
+_lib: Optional[C.CDLL] = None
+
+
+def lib() -> C.CDLL:
+    """Load libtsid.so (built in-tree); raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                           "`python -m paper_2608_00977_amd.build` (no fallback exists)")
+    L = C.CDLL(LIB_PATH)
+    P, i32, i64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
+    sig = {
+        "tsid_create": (C.c_int, [C.c_int, P, sz, C.POINTER(P)]),
+        "tsid_destroy": (None, [P]),
+        "tsid_last_error": (C.c_char_p, [P]),
+        "tsid_build_template": (C.c_int, [P, i64, i64, P, P, P, i64, P, i32, P, i32, i32, i64]),
+        "tsid_template_info": (C.c_int, [P, P, P, P, P]),
+        "tsid_fit_template": (C.c_int, [P, P, P, C.POINTER(tsid_fit_opts), P]),
+        "tsid_fit_epochs_done": (C.c_int, [P, P]),
+        "tsid_loss": (C.c_int, [P, P, P, C.c_float, P]),
+        "tsid_extend_chunk": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P,
+                                        C.POINTER(tsid_fit_opts)]),
+        "tsid_sync": (C.c_int, [P]),
+        "tsid_export_index": (C.c_int, [P, C.c_int, P, sz]),
+        "tsid_chunk_plan": (i32, [P, i64, i32, i64, P, i32]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+# ------------------------------------------------------- one-to-one wrappers
+def tsid_create(device: int = 0, hip_stream: int = 0, max_device_bytes: int = 0) -> C.c_void_p:
+    ctx = C.c_void_p()
+    st = lib().tsid_create(device, C.c_void_p(hip_stream or None), max_device_bytes, C.byref(ctx))
+    if st != OK:
+        raise TsidError(st, "tsid_create")
+    return ctx
+
+
+def tsid_destroy(ctx) -> None:
+    lib().tsid_destroy(ctx)
+
+
+def tsid_last_error(ctx) -> str:
+    return lib().tsid_last_error(ctx).decode()
+
+
+def tsid_build_template(ctx, m, n, u, i, r, nnz, I, m_t, J, n_t, k, stage_entries=0) -> int:
+    return lib().tsid_build_template(ctx, m, n, u, i, r, nnz, I, m_t, J, n_t, k, stage_entries)
+
+
+def tsid_template_info(ctx):
+    m_t, n_t, k = C.c_int32(), C.c_int32(), C.c_int32()
+    nnz = C.c_int64()
+    st = lib().tsid_template_info(ctx, C.byref(m_t), C.byref(n_t), C.byref(nnz), C.byref(k))
+    return st, m_t.value, n_t.value, nnz.value, k.value
+
+
+def tsid_fit_template(ctx, P, Q, opts: tsid_fit_opts, loss_hist) -> int:
+    return lib().tsid_fit_template(ctx, P, Q, C.byref(opts), loss_hist)
+
+
+def tsid_fit_epochs_done(ctx) -> int:
+    out = C.c_int32()
+    st = lib().tsid_fit_epochs_done(ctx, C.byref(out))
+    if st != OK:
+        raise TsidError(st, "tsid_fit_epochs_done")
+    return out.value
+
+
+def tsid_loss(ctx, P, Q, lam: float, out) -> int:
+    return lib().tsid_loss(ctx, P, Q, lam, out)
+
+
+def tsid_extend_chunk(ctx, side, fixed_id, free_local, r, nnz, n_free, F_fixed, n_fixed, F_free,
+                      opts: tsid_fit_opts) -> int:
+    return lib().tsid_extend_chunk(ctx, side, fixed_id, free_local, r, nnz, n_free, F_fixed,
+                                   n_fixed, F_free, C.byref(opts))
+
+
+def tsid_sync(ctx) -> int:
+    return lib().tsid_sync(ctx)
+
+
+def tsid_export_index(ctx, which: int, host_dst, nbytes: int) -> int:
+    return lib().tsid_export_index(ctx, which, host_dst, nbytes)
+
+
+def tsid_chunk_plan(counts: np.ndarray, n_chunks: int = 0, max_entries: int = 0) -> np.ndarray:
+    counts = np.ascontiguousarray(counts, dtype=np.int64)
+    cap = (n_chunks + 1) if n_chunks > 0 else counts.size + 2
+    bounds = np.empty(max(cap, 2), np.int64)
+    nc = lib().tsid_chunk_plan(counts.ctypes.data, counts.size, n_chunks, max_entries,
+                               bounds.ctypes.data, bounds.size)
+    if nc < 0:
+        raise TsidError(E_INVAL, "tsid_chunk_plan")
+    return bounds[:nc + 1].copy()
+
+
+# ------------------------------------------------------------ convenience
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, torch.Tensor):
+        return x.data_ptr()
+    return x.ctypes.data
+
+
+def make_opts(epochs=1, lam=0.0, lr=0.1, clip=False, xi=0.1, prec="fp32", step="sum"):
+    return tsid_fit_opts(int(epochs), float(lam), float(lr), float(xi), int(bool(clip)),
+                         BF16 if prec == "bf16" else FP32,
+                         STEP_DEGREE if step == "degree" else STEP_SUM)
+
+
+class Tsid:
+    """One libtsid context on one device."""
+
+    def __init__(self, device: int = 0, stream: Optional[torch.cuda.Stream] = None,
+                 max_device_bytes: int = 0):
+        torch.cuda.init()
+        handle = stream.cuda_stream if stream is not None else 0
+        self.device = device
+        self.ctx = tsid_create(device, handle, max_device_bytes)
+        self._keep = []  # host buffers of chunks in flight
+
+    def close(self):
+        if self.ctx is not None:
+            tsid_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _check(self, st: int, where: str):
+        if st != OK:
+            raise TsidError(st, where, tsid_last_error(self.ctx))
+
+    def build_template(self, m, n, u, i, r, I, J, k, stage_entries=0):
+        u = np.ascontiguousarray(u, np.int32)
+        i = np.ascontiguousarray(i, np.int32)
+        r = np.ascontiguousarray(r, np.float32)
+        I = np.ascontiguousarray(I, np.int32)
+        J = np.ascontiguousarray(J, np.int32)
+        st = tsid_build_template(self.ctx, m, n, _ptr(u), _ptr(i), _ptr(r), u.size, _ptr(I),
+                                 I.size, _ptr(J), J.size, k, stage_entries)
+        self._check(st, "tsid_build_template")
+        self._dims = (int(m), int(n))
+
+    def info(self):
+        st, m_t, n_t, nnz, k = tsid_template_info(self.ctx)
+        self._check(st, "tsid_template_info")
+        return dict(m_t=m_t, n_t=n_t, nnz=nnz, k=k)
+
+    def fit_template(self, P: torch.Tensor, Q: torch.Tensor, opts: tsid_fit_opts,
+                     want_loss: bool = True, raise_on_error: bool = True):
+        """Runs the fit in place on P and Q (contiguous fp32 device tensors);
+        returns (status, loss history)."""
+        assert P.is_cuda and Q.is_cuda and P.dtype == torch.float32 and Q.dtype == torch.float32
+        assert P.is_contiguous() and Q.is_contiguous()
+        hist = np.full(opts.epochs + 1, np.nan) if want_loss else None
+        torch.cuda.current_stream().synchronize()
+        st = tsid_fit_template(self.ctx, _ptr(P), _ptr(Q), opts, _ptr(hist))
+        if raise_on_error:
+            self._check(st, "tsid_fit_template")
+        return st, hist
+
+    def epochs_done(self) -> int:
+        return tsid_fit_epochs_done(self.ctx)
+
+    def loss(self, P: torch.Tensor, Q: torch.Tensor, lam: float) -> float:
+        out = np.zeros(1, np.float64)
+        torch.cuda.current_stream().synchronize()
+        self._check(tsid_loss(self.ctx, _ptr(P), _ptr(Q), lam, _ptr(out)), "tsid_loss")
+        return float(out[0])
+
+    def extend_chunk(self, side, fixed_id, free_local, r, n_free, F_fixed: torch.Tensor,
+                     F_free: torch.Tensor, opts: tsid_fit_opts):
+        """Queues one chunk; fixed_id/free_local/r are host arrays or pinned CPU
+        tensors kept alive until sync(); F_free is a CPU tensor (pinned for
+        overlap) that receives the result."""
+        assert F_fixed.is_cuda and F_fixed.dtype == torch.float32 and F_fixed.is_contiguous()
+        assert not F_free.is_cuda and F_free.dtype == torch.float32 and F_free.is_contiguous()
+        arrs = []
+        for a, dt in ((fixed_id, np.int32), (free_local, np.int32), (r, np.float32)):
+            if isinstance(a, torch.Tensor):
+                arrs.append(a)
+            else:
+                arrs.append(np.ascontiguousarray(a, dt))
+        nnz = int(arrs[0].numel() if isinstance(arrs[0], torch.Tensor) else arrs[0].size)
+        self._keep.append((arrs, F_fixed, F_free, opts))
+        st = tsid_extend_chunk(self.ctx, side, _ptr(arrs[0]), _ptr(arrs[1]), _ptr(arrs[2]), nnz,
+                               n_free, _ptr(F_fixed), F_fixed.shape[0], _ptr(F_free), opts)
+        self._check(st, "tsid_extend_chunk")
+
+    def sync(self):
+        st = tsid_sync(self.ctx)
+        self._keep.clear()
+        self._check(st, "tsid_sync")
+
+    def export_index(self, name: str) -> np.ndarray:
+        inf = self.info()
+        n_rows, n_cols = inf["m_t"], inf["n_t"]
+        kind = {"row_map": (np.int32, None), "col_map": (np.int32, None),
+                "row_ptr": (np.int64, n_rows + 1), "col_ptr": (np.int64, n_cols + 1),
+                "csr_col": (np.int32, inf["nnz"]), "csr_val": (np.float32, inf["nnz"]),
+                "csc_row": (np.int32, inf["nnz"]), "csc_val": (np.float32, inf["nnz"]),
+                "deg_r": (np.int32, n_rows), "deg_c": (np.int32, n_cols)}[name]
+        count = kind[1] if kind[1] is not None else self._dims[0 if name == "row_map" else 1]
+        out = np.empty(count, kind[0])
+        self._check(tsid_export_index(self.ctx, IDX[name], _ptr(out), out.nbytes),
+                    "tsid_export_index")
+        return out

@@ -1,0 +1,940 @@
+// libtsid C ABI: context, argument validation, the template build, the
+// epoch loop of the template fit, the loss, and the chunked extension
+// pipeline.  See include/tsid.h for the contract of every entry point.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <unordered_map>
+#include <vector>
+
+#include "internal.h"
+
+namespace tsid {
+
+void fail(tsid_status st, const std::string &msg) { throw Error{st, msg}; }
+
+void hip_check(hipError_t e, const char *what) {
+    if (e != hipSuccess) fail(TSID_E_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+namespace {
+
+constexpr int64_t kDefaultStage = int64_t(1) << 24;  // entries per host-to-device piece
+// Extension items hold a fixed number of cells, so a free row is cut (and its
+// partial sums added) the same way whichever chunk carries it.
+constexpr int32_t kExtendE = 1024;
+constexpr int64_t kMaxEntries = (int64_t(1) << 32) - 1;
+
+bool valid_rank(int32_t k) { return k == 8 || k == 16 || k == 32 || k == 64 || k == 128; }
+
+// Entries per work item: enough items to keep every compute unit busy, long
+// enough that the per-item overhead (owner row load, final store) stays small.
+int32_t choose_E(int64_t nnz) {
+    int64_t e = (nnz + 65535) / 65536;
+    e = (e + 15) / 16 * 16;
+    if (e < 64) e = 64;
+    if (e > 4096) e = 4096;
+    return (int32_t)e;
+}
+
+}  // namespace
+
+// Device memory owned by a context, with an optional byte cap.
+struct Arena {
+    size_t cap = 0, used = 0;
+    std::unordered_map<void *, size_t> sizes;
+
+    template <typename T>
+    T *alloc(int64_t count) {
+        size_t bytes = (size_t)(count > 0 ? count : 1) * sizeof(T);
+        bytes = (bytes + 255) & ~size_t(255);
+        if (cap && used + bytes > cap) fail(TSID_E_NOMEM, "device byte cap exceeded");
+        void *p = nullptr;
+        if (hipMalloc(&p, bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            fail(TSID_E_NOMEM, "hipMalloc of " + std::to_string(bytes) + " bytes failed");
+        }
+        sizes[p] = bytes;
+        used += bytes;
+        return static_cast<T *>(p);
+    }
+    template <typename T>
+    void release(T *&p) {
+        if (!p) return;
+        auto it = sizes.find((void *)p);
+        if (it != sizes.end()) {
+            used -= it->second;
+            sizes.erase(it);
+        }
+        (void)hipFree((void *)p);
+        p = nullptr;
+    }
+};
+
+struct Plan {
+    uint32_t *item_off = nullptr;  // rows + 1
+    int32_t *items = nullptr;
+    int32_t n_items = 0;
+    int32_t E = 64;
+};
+
+struct Template {
+    int64_t m = 0, n = 0, nnz = 0;
+    int32_t m_t = 0, n_t = 0, k = 0;
+    int32_t *row_map = nullptr, *col_map = nullptr;
+    int2 *stream_r = nullptr, *stream_c = nullptr;
+    int64_t *row_ptr = nullptr, *col_ptr = nullptr;
+    Plan pr, pc;
+};
+
+struct FitBufs {
+    int32_t prec = -1;
+    float *P[2] = {nullptr, nullptr}, *Q[2] = {nullptr, nullptr};
+    uint16_t *Pb[2] = {nullptr, nullptr}, *Qb[2] = {nullptr, nullptr};
+    float *carry_r = nullptr, *carry_c = nullptr, *e2 = nullptr, *normP = nullptr, *normQ = nullptr;
+    double *partial = nullptr, *loss = nullptr;
+    int32_t loss_cap = 0;
+};
+
+struct ExtSlot {
+    int32_t *fid = nullptr, *free_id = nullptr;
+    float *r = nullptr;
+    float *X[2] = {nullptr, nullptr};
+    hipEvent_t ev_h2d = nullptr, ev_staged = nullptr, ev_done = nullptr, ev_flushed = nullptr;
+};
+
+struct ExtState {
+    int64_t cap_nnz = 0;
+    int32_t cap_free = 0, cap_items = 0, k = 0;
+    ExtSlot slot[2];
+    uint64_t *keys = nullptr, *keys_alt = nullptr;
+    uint32_t *vals = nullptr, *vals_alt = nullptr, *sort_scratch = nullptr;
+    int2 *stream = nullptr;
+    int64_t *ptr = nullptr;
+    uint32_t *nparts = nullptr, *scan_scratch = nullptr, *item_off = nullptr;
+    int32_t *items = nullptr;
+    float *carry = nullptr;
+    int32_t *err = nullptr;
+    int next = 0;
+    bool pending = false;
+};
+
+}  // namespace tsid
+
+using namespace tsid;
+
+struct tsid_ctx {
+    int device = 0;
+    hipStream_t comp = nullptr, h2d = nullptr, d2h = nullptr;
+    bool own_comp = false;
+    Arena arena;
+    std::string err;
+    int32_t *err_dev = nullptr;      // error slots of build / fit / loss
+    int32_t *err_host = nullptr;     // pinned mirror
+    Template *tpl = nullptr;
+    int32_t epochs_done = 0;         // of the last fit
+    FitBufs fb;
+    ExtState ext;
+};
+
+namespace {
+
+void set_device(const tsid_ctx *c) { TSID_HIP(hipSetDevice(c->device)); }
+
+template <typename F>
+tsid_status guarded(tsid_ctx *c, F &&f) {
+    if (!c) return TSID_E_INVAL;
+    try {
+        set_device(c);
+        f();
+        c->err.clear();
+        return TSID_OK;
+    } catch (const Error &e) {
+        c->err = e.msg;
+        return e.st;
+    } catch (const std::exception &e) {
+        c->err = e.what();
+        return TSID_E_DEVICE;
+    }
+}
+
+void free_template(tsid_ctx *c, Template *&t) {
+    if (!t) return;
+    Arena &A = c->arena;
+    A.release(t->row_map);
+    A.release(t->col_map);
+    A.release(t->stream_r);
+    A.release(t->stream_c);
+    A.release(t->row_ptr);
+    A.release(t->col_ptr);
+    A.release(t->pr.item_off);
+    A.release(t->pr.items);
+    A.release(t->pc.item_off);
+    A.release(t->pc.items);
+    delete t;
+    t = nullptr;
+}
+
+void free_fit(tsid_ctx *c) {
+    Arena &A = c->arena;
+    FitBufs &f = c->fb;
+    for (int b = 0; b < 2; ++b) {
+        A.release(f.P[b]);
+        A.release(f.Q[b]);
+        A.release(f.Pb[b]);
+        A.release(f.Qb[b]);
+    }
+    A.release(f.carry_r);
+    A.release(f.carry_c);
+    A.release(f.e2);
+    A.release(f.normP);
+    A.release(f.normQ);
+    A.release(f.partial);
+    A.release(f.loss);
+    f.prec = -1;
+    f.loss_cap = 0;
+}
+
+void free_ext_buffers(tsid_ctx *c) {
+    Arena &A = c->arena;
+    ExtState &x = c->ext;
+    for (auto &s : x.slot) {
+        A.release(s.fid);
+        A.release(s.free_id);
+        A.release(s.r);
+        A.release(s.X[0]);
+        A.release(s.X[1]);
+    }
+    A.release(x.keys);
+    A.release(x.keys_alt);
+    A.release(x.vals);
+    A.release(x.vals_alt);
+    A.release(x.sort_scratch);
+    A.release(x.stream);
+    A.release(x.ptr);
+    A.release(x.nparts);
+    A.release(x.scan_scratch);
+    A.release(x.item_off);
+    A.release(x.items);
+    A.release(x.carry);
+    x.cap_nnz = 0;
+    x.cap_free = 0;
+    x.cap_items = 0;
+    x.k = 0;
+}
+
+void check_opts(const tsid_fit_opts *o) {
+    if (!o) fail(TSID_E_INVAL, "opts is NULL");
+    if (o->epochs < 0) fail(TSID_E_INVAL, "epochs < 0");
+    if (!(o->lambda >= 0.f) || !std::isfinite(o->lambda)) fail(TSID_E_INVAL, "lambda must be finite and >= 0");
+    if (!(o->lr > 0.f) || !std::isfinite(o->lr)) fail(TSID_E_INVAL, "lr must be finite and > 0");
+    if (o->clip != 0 && o->clip != 1) fail(TSID_E_INVAL, "clip must be 0 or 1");
+    if (o->clip && !(o->clip_xi > 0.f)) fail(TSID_E_INVAL, "clip_xi must be > 0");
+    if (o->prec != TSID_FP32 && o->prec != TSID_BF16) fail(TSID_E_INVAL, "bad precision");
+    if (o->step != TSID_STEP_SUM && o->step != TSID_STEP_DEGREE) fail(TSID_E_INVAL, "bad step");
+}
+
+void check_aligned(const void *p, const char *what) {
+    if (reinterpret_cast<uintptr_t>(p) % 16 != 0)
+        fail(TSID_E_INVAL, std::string(what) + " must be 16-byte aligned");
+}
+
+// Validates a template id set on the host: range first, then repeats.
+void check_ids(const int32_t *ids, int32_t count, int64_t bound, const char *what) {
+    if (count > 0 && !ids) fail(TSID_E_INVAL, std::string(what) + " is NULL");
+    for (int32_t a = 0; a < count; ++a)
+        if (ids[a] < 0 || ids[a] >= bound) fail(TSID_E_RANGE, std::string(what) + " id out of range");
+    std::vector<int32_t> sorted(ids, ids + count);
+    std::sort(sorted.begin(), sorted.end());
+    if (std::adjacent_find(sorted.begin(), sorted.end()) != sorted.end())
+        fail(TSID_E_DUP, std::string(what) + " repeats an id");
+}
+
+void raise_device_errors(const int32_t *e, const char *where) {
+    if (e[ERR_RANGE]) fail(TSID_E_RANGE, std::string(where) + ": index out of range");
+    if (e[ERR_DUP]) fail(TSID_E_DUP, std::string(where) + ": repeated cell");
+    if (e[ERR_INVAL]) fail(TSID_E_INVAL, std::string(where) + ": non-finite value");
+}
+
+void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i, const float *r,
+           int64_t nnz, const int32_t *I, int32_t m_t, const int32_t *J, int32_t n_t, int32_t k,
+           int64_t stage) {
+    if (m < 1 || n < 1 || m >= (int64_t(1) << 31) || n >= (int64_t(1) << 31))
+        fail(TSID_E_INVAL, "m and n must be in [1, 2^31)");
+    if (nnz < 0) fail(TSID_E_INVAL, "nnz < 0");
+    if (nnz > 0 && (!u || !i || !r)) fail(TSID_E_INVAL, "NULL Omega arrays");
+    if (m_t < 0 || m_t > m || n_t < 0 || n_t > n) fail(TSID_E_INVAL, "template size out of range");
+    if (!valid_rank(k)) fail(TSID_E_INVAL, "k must be 8, 16, 32, 64 or 128");
+    if (stage < 0) fail(TSID_E_INVAL, "stage_entries < 0");
+    check_ids(I, m_t, m, "I");
+    check_ids(J, n_t, n, "J");
+
+    hipStream_t cs = c->comp, hs = c->h2d;
+    Arena &A = c->arena;
+    Template *t = new Template;
+    t->m = m;
+    t->n = n;
+    t->m_t = m_t;
+    t->n_t = n_t;
+    t->k = k;
+    // Scratch of this build; released on every path.
+    int32_t *dI = nullptr, *dJ = nullptr, *su[2] = {nullptr, nullptr}, *si[2] = {nullptr, nullptr};
+    float *sr[2] = {nullptr, nullptr};
+    uint32_t *bcnt = nullptr, *boffs = nullptr, *piece = nullptr, *scan_tmp = nullptr;
+    uint32_t *sort_tmp = nullptr, *nparts = nullptr, *vals = nullptr, *vals_alt = nullptr;
+    uint64_t *keys = nullptr, *keys_alt = nullptr;
+    uint32_t *piece_host = nullptr;
+    hipEvent_t ev_h2d[2] = {nullptr, nullptr}, ev_free[2] = {nullptr, nullptr};
+    auto cleanup = [&]() {
+        (void)hipStreamSynchronize(hs);
+        (void)hipStreamSynchronize(cs);
+        A.release(dI);
+        A.release(dJ);
+        for (int s = 0; s < 2; ++s) {
+            A.release(su[s]);
+            A.release(si[s]);
+            A.release(sr[s]);
+            if (ev_h2d[s]) (void)hipEventDestroy(ev_h2d[s]);
+            if (ev_free[s]) (void)hipEventDestroy(ev_free[s]);
+        }
+        A.release(bcnt);
+        A.release(boffs);
+        A.release(piece);
+        A.release(scan_tmp);
+        A.release(sort_tmp);
+        A.release(nparts);
+        A.release(keys);
+        A.release(keys_alt);
+        A.release(vals);
+        A.release(vals_alt);
+        if (piece_host) (void)hipHostFree(piece_host);
+    };
+    try {
+        // a1: template maps
+        t->row_map = A.alloc<int32_t>(m);
+        t->col_map = A.alloc<int32_t>(n);
+        fill_i32(t->row_map, m, -1, cs);
+        fill_i32(t->col_map, n, -1, cs);
+        dI = A.alloc<int32_t>(m_t);
+        dJ = A.alloc<int32_t>(n_t);
+        if (m_t) TSID_HIP(hipMemcpyAsync(dI, I, (size_t)m_t * 4, hipMemcpyHostToDevice, cs));
+        if (n_t) TSID_HIP(hipMemcpyAsync(dJ, J, (size_t)n_t * 4, hipMemcpyHostToDevice, cs));
+        scatter_map(dI, m_t, t->row_map, cs);
+        scatter_map(dJ, n_t, t->col_map, cs);
+        TSID_HIP(hipMemsetAsync(c->err_dev, 0, ERR_SLOTS * sizeof(int32_t), cs));
+
+        // a2: stream Omega through two staging slots; filter each piece to Omega*.
+        const int bits_a = bits_for(m_t), bits_b = bits_for(n_t);
+        const int64_t S = std::max<int64_t>(1, std::min<int64_t>(stage ? stage : kDefaultStage,
+                                                                 std::max<int64_t>(nnz, 1)));
+        const int64_t pieces = nnz > 0 ? (nnz + S - 1) / S : 0;
+        const int nfb = filter_blocks(S);
+        bcnt = A.alloc<uint32_t>(nfb);
+        boffs = A.alloc<uint32_t>(nfb);
+        piece = A.alloc<uint32_t>(1);
+        scan_tmp = A.alloc<uint32_t>((int64_t)scan_scratch_elems(std::max<int64_t>(nfb, m_t + n_t + 1)));
+        TSID_HIP(hipHostMalloc((void **)&piece_host, sizeof(uint32_t), hipHostMallocDefault));
+        int64_t cap = pieces ? std::min<int64_t>(nnz, std::max<int64_t>(S, int64_t(1) << 20)) : 1;
+        keys = A.alloc<uint64_t>(cap);
+        vals = A.alloc<uint32_t>(cap);
+        int64_t total = 0;
+        if (pieces) {
+            for (int s = 0; s < 2 && s < pieces; ++s) {
+                su[s] = A.alloc<int32_t>(S);
+                si[s] = A.alloc<int32_t>(S);
+                sr[s] = A.alloc<float>(S);
+                TSID_HIP(hipEventCreateWithFlags(&ev_h2d[s], hipEventDisableTiming));
+                TSID_HIP(hipEventCreateWithFlags(&ev_free[s], hipEventDisableTiming));
+            }
+            auto issue = [&](int64_t p) {
+                const int s = (int)(p & 1);
+                const int64_t off = p * S, len = std::min(S, nnz - off);
+                TSID_HIP(hipStreamWaitEvent(hs, ev_free[s], 0));
+                TSID_HIP(hipMemcpyAsync(su[s], u + off, (size_t)len * 4, hipMemcpyHostToDevice, hs));
+                TSID_HIP(hipMemcpyAsync(si[s], i + off, (size_t)len * 4, hipMemcpyHostToDevice, hs));
+                TSID_HIP(hipMemcpyAsync(sr[s], r + off, (size_t)len * 4, hipMemcpyHostToDevice, hs));
+                TSID_HIP(hipEventRecord(ev_h2d[s], hs));
+            };
+            issue(0);
+            for (int64_t p = 0; p < pieces; ++p) {
+                const int s = (int)(p & 1);
+                const int64_t len = std::min(S, nnz - p * S);
+                if (p + 1 < pieces) issue(p + 1);  // overlaps this piece's filter
+                TSID_HIP(hipStreamWaitEvent(cs, ev_h2d[s], 0));
+                filter_count(su[s], si[s], sr[s], len, t->row_map, t->col_map, m, n, bcnt,
+                             c->err_dev, cs);
+                const int nb = filter_blocks(len);
+                scan_u32(bcnt, boffs, nb, piece, scan_tmp, cs);
+                TSID_HIP(hipMemcpyAsync(piece_host, piece, 4, hipMemcpyDeviceToHost, cs));
+                TSID_HIP(hipStreamSynchronize(cs));
+                const int64_t got = *piece_host;
+                if (total + got > kMaxEntries) fail(TSID_E_INVAL, "template holds more than 2^32-1 cells");
+                if (total + got > cap) {  // grow the output, keeping what is there
+                    int64_t ncap = std::max<int64_t>(total + got, std::min<int64_t>(nnz, cap * 2));
+                    uint64_t *nk = A.alloc<uint64_t>(ncap);
+                    uint32_t *nv = A.alloc<uint32_t>(ncap);
+                    if (total) {
+                        TSID_HIP(hipMemcpyAsync(nk, keys, (size_t)total * 8, hipMemcpyDeviceToDevice, cs));
+                        TSID_HIP(hipMemcpyAsync(nv, vals, (size_t)total * 4, hipMemcpyDeviceToDevice, cs));
+                        TSID_HIP(hipStreamSynchronize(cs));
+                    }
+                    A.release(keys);
+                    A.release(vals);
+                    keys = nk;
+                    vals = nv;
+                    cap = ncap;
+                }
+                filter_write(su[s], si[s], sr[s], len, t->row_map, t->col_map, m, n, boffs, total,
+                             bits_b, keys, vals, cs);
+                TSID_HIP(hipEventRecord(ev_free[s], cs));
+                total += got;
+            }
+        }
+        t->nnz = total;
+
+        // a3: buckets by row (CSR, key a<<bits_b|b) and by column (CSC, key b<<bits_a|a).
+        keys_alt = A.alloc<uint64_t>(total);
+        vals_alt = A.alloc<uint32_t>(total);
+        sort_tmp = A.alloc<uint32_t>((int64_t)radix_scratch_elems(total));
+        const int nbits = bits_a + bits_b;
+        bool in_alt = radix_sort(keys, vals, keys_alt, vals_alt, total, nbits, sort_tmp, cs);
+        uint64_t *ck = in_alt ? keys_alt : keys;
+        uint32_t *cv = in_alt ? vals_alt : vals;
+        t->stream_r = A.alloc<int2>(total);
+        t->row_ptr = A.alloc<int64_t>((int64_t)m_t + 1);
+        keys_to_stream(ck, cv, total, bits_b, t->stream_r, c->err_dev, cs);
+        ptr_from_keys(ck, total, m_t, bits_b, t->row_ptr, cs);
+        uint64_t *ok = in_alt ? keys : keys_alt;
+        uint32_t *ov = in_alt ? vals : vals_alt;
+        swap_key_halves(ck, total, bits_b, bits_a, ok, cs);
+        if (total) TSID_HIP(hipMemcpyAsync(ov, cv, (size_t)total * 4, hipMemcpyDeviceToDevice, cs));
+        // sort (ok, ov) using (ck, cv) as the other buffer
+        bool alt2 = radix_sort(ok, ov, ck, cv, total, nbits, sort_tmp, cs);
+        uint64_t *tk = alt2 ? ck : ok;
+        uint32_t *tv = alt2 ? cv : ov;
+        t->stream_c = A.alloc<int2>(total);
+        t->col_ptr = A.alloc<int64_t>((int64_t)n_t + 1);
+        keys_to_stream(tk, tv, total, bits_a, t->stream_c, c->err_dev, cs);
+        ptr_from_keys(tk, total, n_t, bits_a, t->col_ptr, cs);
+
+        // work plans of both passes
+        nparts = A.alloc<uint32_t>(std::max(m_t, n_t));
+        const int32_t E = choose_E(total);
+        for (int side = 0; side < 2; ++side) {
+            Plan &pl = side ? t->pc : t->pr;
+            const int32_t rows = side ? n_t : m_t;
+            pl.E = E;
+            const int64_t bound = (int64_t)rows + total / E + 1;
+            pl.item_off = A.alloc<uint32_t>((int64_t)rows + 1);
+            pl.items = A.alloc<int32_t>(bound);
+            plan_items(side ? t->col_ptr : t->row_ptr, rows, E, pl.item_off, pl.items, nparts,
+                       scan_tmp, cs);
+        }
+        uint32_t counts[2] = {0, 0};
+        TSID_HIP(hipMemcpyAsync(&counts[0], t->pr.item_off + m_t, 4, hipMemcpyDeviceToHost, cs));
+        TSID_HIP(hipMemcpyAsync(&counts[1], t->pc.item_off + n_t, 4, hipMemcpyDeviceToHost, cs));
+        TSID_HIP(hipMemcpyAsync(c->err_host, c->err_dev, ERR_SLOTS * 4, hipMemcpyDeviceToHost, cs));
+        TSID_HIP(hipStreamSynchronize(cs));
+        t->pr.n_items = (int32_t)counts[0];
+        t->pc.n_items = (int32_t)counts[1];
+        raise_device_errors(c->err_host, "build");
+    } catch (...) {
+        cleanup();
+        free_template(c, t);
+        throw;
+    }
+    cleanup();
+    free_template(c, c->tpl);
+    free_fit(c);
+    c->tpl = t;
+}
+
+void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs) {
+    Template &t = *c->tpl;
+    FitBufs &f = c->fb;
+    Arena &A = c->arena;
+    const int64_t lp = (int64_t)t.m_t * t.k, lq = (int64_t)t.n_t * t.k;
+    if (!f.P[0]) {
+        for (int b = 0; b < 2; ++b) {
+            f.P[b] = A.alloc<float>(lp);
+            f.Q[b] = A.alloc<float>(lq);
+        }
+        f.carry_r = A.alloc<float>((int64_t)t.pr.n_items * t.k);
+        f.carry_c = A.alloc<float>((int64_t)t.pc.n_items * t.k);
+        f.e2 = A.alloc<float>(std::max(t.pr.n_items, t.pc.n_items));
+        f.normP = A.alloc<float>(t.m_t);
+        f.normQ = A.alloc<float>(t.n_t);
+        f.partial = A.alloc<double>((int64_t)reduce_scratch_elems());
+    }
+    if (prec == TSID_BF16 && !f.Pb[0]) {
+        for (int b = 0; b < 2; ++b) {
+            f.Pb[b] = A.alloc<uint16_t>(lp);
+            f.Qb[b] = A.alloc<uint16_t>(lq);
+        }
+    }
+    if (f.loss_cap < epochs + 1) {
+        A.release(f.loss);
+        f.loss = A.alloc<double>(epochs + 1);
+        f.loss_cap = epochs + 1;
+    }
+}
+
+PassArgs pass_args(const Template &t, int side, const tsid_fit_opts &o, int32_t *err) {
+    PassArgs a{};
+    const Plan &pl = side ? t.pc : t.pr;
+    a.stream = side ? t.stream_c : t.stream_r;
+    a.ptr = side ? t.col_ptr : t.row_ptr;
+    a.items = pl.items;
+    a.item_off = pl.item_off;
+    a.n_items_dev = nullptr;
+    a.n_items = pl.n_items;
+    a.rows = side ? t.n_t : t.m_t;
+    a.E = pl.E;
+    a.lam = o.lambda;
+    a.lr = o.lr;
+    a.xi = o.clip_xi;
+    a.clip = o.clip;
+    a.degree = o.step == TSID_STEP_DEGREE;
+    a.err = err;
+    return a;
+}
+
+void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_hist) {
+    if (!c->tpl) fail(TSID_E_STATE, "no template: call tsid_build_template first");
+    check_opts(o);
+    Template &t = *c->tpl;
+    if ((t.m_t && !P) || (t.n_t && !Q)) fail(TSID_E_INVAL, "NULL factor pointer");
+    ensure_fit_buffers(c, o->prec, o->epochs);
+    c->epochs_done = 0;
+    FitBufs &f = c->fb;
+    hipStream_t cs = c->comp;
+    const int K = t.k, prec = o->prec, T = o->epochs;
+    const int64_t lp = (int64_t)t.m_t * K, lq = (int64_t)t.n_t * K;
+    if (lp) TSID_HIP(hipMemcpyAsync(f.P[0], P, (size_t)lp * 4, hipMemcpyDeviceToDevice, cs));
+    if (lq) TSID_HIP(hipMemcpyAsync(f.Q[0], Q, (size_t)lq * 4, hipMemcpyDeviceToDevice, cs));
+    if (prec == TSID_BF16) {
+        launch_to_bf16(f.P[0], lp, f.Pb[0], cs);
+        launch_to_bf16(f.Q[0], lq, f.Qb[0], cs);
+    }
+    TSID_HIP(hipMemsetAsync(c->err_dev, 0, ERR_SLOTS * sizeof(int32_t), cs));
+    PassArgs ar = pass_args(t, 0, *o, c->err_dev), ac = pass_args(t, 1, *o, c->err_dev);
+    ar.skip_after_nonfinite = ac.skip_after_nonfinite = 1;
+    for (int ep = 0; ep < T; ++ep) {
+        const int cur = ep & 1, nxt = cur ^ 1;
+        ar.epoch = ac.epoch = ep;
+        // P pass (CSR): owner P_t, gathered Q_t
+        ar.X = f.P[cur];
+        ar.Y = prec ? (const void *)f.Qb[cur] : (const void *)f.Q[cur];
+        ar.Xn = f.P[nxt];
+        ar.Xn_b = prec ? f.Pb[nxt] : nullptr;
+        ar.carry = f.carry_r;
+        ar.e2 = f.e2;
+        ar.norm = f.normP;
+        launch_item_pass(K, prec, false, ar, cs);
+        launch_fixup(K, prec, ar, cs);
+        // Q pass (CSC): owner Q_t, gathered P_t (the old P: a simultaneous step)
+        ac.X = f.Q[cur];
+        ac.Y = prec ? (const void *)f.Pb[cur] : (const void *)f.P[cur];
+        ac.Xn = f.Q[nxt];
+        ac.Xn_b = prec ? f.Qb[nxt] : nullptr;
+        ac.carry = f.carry_c;
+        ac.e2 = nullptr;
+        ac.norm = f.normQ;
+        launch_item_pass(K, prec, false, ac, cs);
+        launch_fixup(K, prec, ac, cs);
+        launch_loss_reduce(f.e2, t.pr.n_items, f.normP, t.m_t, f.normQ, t.n_t, o->lambda, f.partial,
+                           f.loss + ep, c->err_dev, ep, cs);
+    }
+    const int fin = T & 1;
+    if (loss_hist) {  // L(P_T, Q_T)
+        ar.epoch = T;
+        ar.X = f.P[fin];
+        ar.Y = prec ? (const void *)f.Qb[fin] : (const void *)f.Q[fin];
+        ar.Xn = nullptr;
+        ar.e2 = f.e2;
+        ar.norm = f.normP;
+        launch_item_pass(K, prec, true, ar, cs);
+        launch_row_norms(K, f.Q[fin], t.n_t, f.normQ, cs);
+        launch_loss_reduce(f.e2, t.pr.n_items, f.normP, t.m_t, f.normQ, t.n_t, o->lambda, f.partial,
+                           f.loss + T, c->err_dev, T, cs);
+    }
+    std::vector<double> hist((size_t)T + 1);
+    if (loss_hist) TSID_HIP(hipMemcpyAsync(hist.data(), f.loss, (size_t)(T + 1) * 8, hipMemcpyDeviceToHost, cs));
+    TSID_HIP(hipMemcpyAsync(c->err_host, c->err_dev, ERR_SLOTS * 4, hipMemcpyDeviceToHost, cs));
+    TSID_HIP(hipStreamSynchronize(cs));
+    const int32_t bad = c->err_host[ERR_NONFINITE];
+    const int last = bad ? bad - 1 : T;  // factors to return: (P_last, Q_last)
+    c->epochs_done = last;
+    const int src = last & 1;
+    if (lp) TSID_HIP(hipMemcpyAsync(P, f.P[src], (size_t)lp * 4, hipMemcpyDeviceToDevice, cs));
+    if (lq) TSID_HIP(hipMemcpyAsync(Q, f.Q[src], (size_t)lq * 4, hipMemcpyDeviceToDevice, cs));
+    TSID_HIP(hipStreamSynchronize(cs));
+    if (loss_hist) {
+        for (int ep = 0; ep <= T; ++ep) loss_hist[ep] = ep <= last ? hist[ep] : NAN;
+    }
+    if (bad) fail(TSID_E_NONFINITE, "non-finite update in epoch " + std::to_string(bad - 1));
+}
+
+void loss(tsid_ctx *c, const float *P, const float *Q, float lambda, double *out) {
+    if (!c->tpl) fail(TSID_E_STATE, "no template");
+    Template &t = *c->tpl;
+    if (!out) fail(TSID_E_INVAL, "out is NULL");
+    if ((t.m_t && !P) || (t.n_t && !Q)) fail(TSID_E_INVAL, "NULL factor pointer");
+    if (!(lambda >= 0.f) || !std::isfinite(lambda)) fail(TSID_E_INVAL, "lambda must be finite and >= 0");
+    check_aligned(P, "P");
+    check_aligned(Q, "Q");
+    ensure_fit_buffers(c, TSID_FP32, 0);
+    FitBufs &f = c->fb;
+    hipStream_t cs = c->comp;
+    tsid_fit_opts o{0, lambda, 1.f, 1.f, 0, TSID_FP32, TSID_STEP_SUM};
+    PassArgs a = pass_args(t, 0, o, c->err_dev);
+    a.X = P;
+    a.Y = Q;
+    a.e2 = f.e2;
+    a.norm = f.normP;
+    a.epoch = 0;
+    a.skip_after_nonfinite = 0;
+    launch_item_pass(t.k, TSID_FP32, true, a, cs);
+    launch_row_norms(t.k, Q, t.n_t, f.normQ, cs);
+    launch_loss_reduce(f.e2, t.pr.n_items, f.normP, t.m_t, f.normQ, t.n_t, lambda, f.partial, f.loss,
+                       nullptr, -1, cs);
+    TSID_HIP(hipMemcpyAsync(out, f.loss, 8, hipMemcpyDeviceToHost, cs));
+    TSID_HIP(hipStreamSynchronize(cs));
+}
+
+// ------------------------------------------------------------- extension
+
+void ext_sync_all(tsid_ctx *c) {
+    TSID_HIP(hipStreamSynchronize(c->h2d));
+    TSID_HIP(hipStreamSynchronize(c->comp));
+    TSID_HIP(hipStreamSynchronize(c->d2h));
+}
+
+void ext_ensure(tsid_ctx *c, int64_t nnz, int32_t n_free, int32_t items_bound, int32_t k) {
+    ExtState &x = c->ext;
+    Arena &A = c->arena;
+    if (!x.slot[0].ev_h2d) {
+        for (auto &s : x.slot) {
+            TSID_HIP(hipEventCreateWithFlags(&s.ev_h2d, hipEventDisableTiming));
+            TSID_HIP(hipEventCreateWithFlags(&s.ev_staged, hipEventDisableTiming));
+            TSID_HIP(hipEventCreateWithFlags(&s.ev_done, hipEventDisableTiming));
+            TSID_HIP(hipEventCreateWithFlags(&s.ev_flushed, hipEventDisableTiming));
+        }
+        x.err = A.alloc<int32_t>(ERR_SLOTS);
+        TSID_HIP(hipMemsetAsync(x.err, 0, ERR_SLOTS * 4, c->comp));
+    }
+    if (nnz <= x.cap_nnz && n_free <= x.cap_free && items_bound <= x.cap_items && k == x.k) return;
+    ext_sync_all(c);  // buffers may be in use by earlier chunks
+    const int64_t cn = std::max<int64_t>({nnz, x.cap_nnz + x.cap_nnz / 2, 1024});
+    const int32_t cf = (int32_t)std::min<int64_t>(std::max<int64_t>({(int64_t)n_free, (int64_t)x.cap_free + x.cap_free / 2, 64}), INT32_MAX - 1);
+    const int32_t ci = (int32_t)std::min<int64_t>(std::max<int64_t>({(int64_t)items_bound, (int64_t)x.cap_items + x.cap_items / 2, 64}), INT32_MAX - 1);
+    int32_t *err_keep = x.err;
+    x.err = nullptr;
+    free_ext_buffers(c);
+    x.err = err_keep;
+    for (auto &s : x.slot) {
+        s.fid = A.alloc<int32_t>(cn);
+        s.free_id = A.alloc<int32_t>(cn);
+        s.r = A.alloc<float>(cn);
+        s.X[0] = A.alloc<float>((int64_t)cf * k);
+        s.X[1] = A.alloc<float>((int64_t)cf * k);
+    }
+    x.keys = A.alloc<uint64_t>(cn);
+    x.keys_alt = A.alloc<uint64_t>(cn);
+    x.vals = A.alloc<uint32_t>(cn);
+    x.vals_alt = A.alloc<uint32_t>(cn);
+    x.sort_scratch = A.alloc<uint32_t>((int64_t)radix_scratch_elems(cn));
+    x.stream = A.alloc<int2>(cn);
+    x.ptr = A.alloc<int64_t>((int64_t)cf + 1);
+    x.nparts = A.alloc<uint32_t>(cf);
+    x.scan_scratch = A.alloc<uint32_t>((int64_t)scan_scratch_elems(cf));
+    x.item_off = A.alloc<uint32_t>((int64_t)cf + 1);
+    x.items = A.alloc<int32_t>(ci);
+    x.carry = A.alloc<float>((int64_t)ci * k);
+    x.cap_nnz = cn;
+    x.cap_free = cf;
+    x.cap_items = ci;
+    x.k = k;
+}
+
+void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t *free_local,
+                  const float *r, int64_t nnz, int32_t n_free, const float *F_fixed, int64_t n_fixed,
+                  float *F_free, const tsid_fit_opts *o) {
+    if (!c->tpl) fail(TSID_E_STATE, "no template: the rank k is set by tsid_build_template");
+    check_opts(o);
+    if (side != 0 && side != 1) fail(TSID_E_INVAL, "side must be 0 or 1");
+    if (nnz < 0 || nnz > kMaxEntries) fail(TSID_E_INVAL, "nnz out of range");
+    if (n_free < 0 || n_fixed < 0 || n_fixed >= (int64_t(1) << 31)) fail(TSID_E_INVAL, "bad sizes");
+    if (nnz > 0 && (!fixed_id || !free_local || !r)) fail(TSID_E_INVAL, "NULL chunk arrays");
+    if (nnz > 0 && (!F_fixed || n_fixed == 0)) fail(TSID_E_INVAL, "no fixed factors");
+    if (n_free > 0 && !F_free) fail(TSID_E_INVAL, "F_free is NULL");
+    if (F_fixed) check_aligned(F_fixed, "F_fixed");
+    const int K = c->tpl->k;
+    const int32_t E = kExtendE;
+    const int64_t bound64 = (int64_t)n_free + nnz / E + 1;
+    if (bound64 >= INT32_MAX) fail(TSID_E_INVAL, "chunk too large");
+    ext_ensure(c, nnz, n_free, (int32_t)bound64, K);
+    ExtState &x = c->ext;
+    const int si = x.next;
+    x.next ^= 1;
+    ExtSlot &s = x.slot[si];
+    hipStream_t cs = c->comp;
+    // stage the chunk (copy stream), after the slot's previous chunk consumed it
+    TSID_HIP(hipStreamWaitEvent(c->h2d, s.ev_staged, 0));
+    if (nnz) {
+        TSID_HIP(hipMemcpyAsync(s.fid, fixed_id, (size_t)nnz * 4, hipMemcpyHostToDevice, c->h2d));
+        TSID_HIP(hipMemcpyAsync(s.free_id, free_local, (size_t)nnz * 4, hipMemcpyHostToDevice, c->h2d));
+        TSID_HIP(hipMemcpyAsync(s.r, r, (size_t)nnz * 4, hipMemcpyHostToDevice, c->h2d));
+    }
+    TSID_HIP(hipEventRecord(s.ev_h2d, c->h2d));
+    TSID_HIP(hipStreamWaitEvent(cs, s.ev_h2d, 0));
+    // bucket the chunk by free row: key = free << bits_fixed | fixed (stable sort)
+    const int bits_fixed = bits_for(std::max<int64_t>(n_fixed, 1));
+    const int bits_free = bits_for(std::max<int32_t>(n_free, 1));
+    chunk_keys(s.fid, s.free_id, s.r, nnz, n_fixed, n_free, bits_fixed, x.keys, x.vals, x.err, cs);
+    TSID_HIP(hipEventRecord(s.ev_staged, cs));
+    const bool alt = radix_sort(x.keys, x.vals, x.keys_alt, x.vals_alt, nnz, bits_fixed + bits_free,
+                                x.sort_scratch, cs);
+    const uint64_t *sk = alt ? x.keys_alt : x.keys;
+    const uint32_t *sv = alt ? x.vals_alt : x.vals;
+    keys_to_stream(sk, sv, nnz, bits_fixed, x.stream, x.err, cs);
+    ptr_from_keys(sk, nnz, n_free, bits_fixed, x.ptr, cs);
+    plan_items(x.ptr, n_free, E, x.item_off, x.items, x.nparts, x.scan_scratch, cs);
+    // the slot's factor buffers are free once its previous results were flushed
+    TSID_HIP(hipStreamWaitEvent(cs, s.ev_flushed, 0));
+    fill_f32(s.X[0], (int64_t)n_free * K, 0.f, cs);
+    PassArgs a{};
+    a.stream = x.stream;
+    a.ptr = x.ptr;
+    a.items = x.items;
+    a.item_off = x.item_off;
+    a.n_items_dev = x.item_off + n_free;
+    a.n_items = (int32_t)bound64;
+    a.rows = n_free;
+    a.E = E;
+    a.Y = F_fixed;
+    a.carry = x.carry;
+    a.lam = o->lambda;
+    a.lr = o->lr;
+    a.xi = o->clip_xi;
+    a.clip = o->clip;
+    a.degree = o->step == TSID_STEP_DEGREE;
+    a.err = x.err;
+    a.skip_after_nonfinite = 0;
+    for (int st = 0; st < o->epochs && n_free > 0; ++st) {
+        a.epoch = st;
+        a.X = s.X[st & 1];
+        a.Xn = s.X[(st + 1) & 1];
+        launch_item_pass(K, TSID_FP32, false, a, cs);
+        launch_fixup(K, TSID_FP32, a, cs);
+    }
+    TSID_HIP(hipEventRecord(s.ev_done, cs));
+    // flush the results on the third stream
+    TSID_HIP(hipStreamWaitEvent(c->d2h, s.ev_done, 0));
+    if (n_free)
+        TSID_HIP(hipMemcpyAsync(F_free, s.X[o->epochs & 1], (size_t)n_free * K * 4,
+                                hipMemcpyDeviceToHost, c->d2h));
+    TSID_HIP(hipEventRecord(s.ev_flushed, c->d2h));
+    x.pending = true;
+    (void)side;
+}
+
+void sync(tsid_ctx *c) {
+    ext_sync_all(c);
+    ExtState &x = c->ext;
+    if (!x.err) return;
+    int32_t e[ERR_SLOTS];
+    TSID_HIP(hipMemcpy(e, x.err, sizeof(e), hipMemcpyDeviceToHost));
+    TSID_HIP(hipMemset(x.err, 0, sizeof(e)));
+    x.pending = false;
+    raise_device_errors(e, "extend");
+    if (e[ERR_NONFINITE]) fail(TSID_E_NONFINITE, "extend: non-finite update");
+}
+
+void export_index(const tsid_ctx *c, int which, void *dst, size_t bytes) {
+    if (!c->tpl) fail(TSID_E_STATE, "no template");
+    if (!dst && bytes) fail(TSID_E_INVAL, "host_dst is NULL");
+    const Template &t = *c->tpl;
+    auto need = [&](size_t want) {
+        if (bytes != want) fail(TSID_E_INVAL, "bytes must be " + std::to_string(want));
+    };
+    auto copy = [&](const void *src, size_t n) {
+        if (n) TSID_HIP(hipMemcpy(dst, src, n, hipMemcpyDeviceToHost));
+    };
+    auto split = [&](const int2 *stream, int part) {
+        need((size_t)t.nnz * 4);
+        std::vector<int2> h((size_t)t.nnz);
+        copy(nullptr, 0);
+        if (t.nnz) TSID_HIP(hipMemcpy(h.data(), stream, (size_t)t.nnz * 8, hipMemcpyDeviceToHost));
+        int32_t *o = static_cast<int32_t *>(dst);
+        for (int64_t j = 0; j < t.nnz; ++j) o[j] = part ? h[j].y : h[j].x;
+    };
+    auto degrees = [&](const int64_t *ptr, int32_t rows) {
+        need((size_t)rows * 4);
+        std::vector<int64_t> h((size_t)rows + 1);
+        TSID_HIP(hipMemcpy(h.data(), ptr, (size_t)(rows + 1) * 8, hipMemcpyDeviceToHost));
+        int32_t *o = static_cast<int32_t *>(dst);
+        for (int32_t x = 0; x < rows; ++x) o[x] = (int32_t)(h[x + 1] - h[x]);
+    };
+    switch (which) {
+        case TSID_IDX_ROW_MAP: need((size_t)t.m * 4); copy(t.row_map, (size_t)t.m * 4); break;
+        case TSID_IDX_COL_MAP: need((size_t)t.n * 4); copy(t.col_map, (size_t)t.n * 4); break;
+        case TSID_IDX_ROW_PTR: need((size_t)(t.m_t + 1) * 8); copy(t.row_ptr, (size_t)(t.m_t + 1) * 8); break;
+        case TSID_IDX_COL_PTR: need((size_t)(t.n_t + 1) * 8); copy(t.col_ptr, (size_t)(t.n_t + 1) * 8); break;
+        case TSID_IDX_CSR_COL: split(t.stream_r, 0); break;
+        case TSID_IDX_CSR_VAL: split(t.stream_r, 1); break;
+        case TSID_IDX_CSC_ROW: split(t.stream_c, 0); break;
+        case TSID_IDX_CSC_VAL: split(t.stream_c, 1); break;
+        case TSID_IDX_DEG_R: degrees(t.row_ptr, t.m_t); break;
+        case TSID_IDX_DEG_C: degrees(t.col_ptr, t.n_t); break;
+        default: fail(TSID_E_INVAL, "unknown index structure");
+    }
+}
+
+}  // namespace
+
+// ================================================================ C ABI
+
+extern "C" {
+
+tsid_status tsid_create(int device, void *hip_stream, size_t max_device_bytes, tsid_ctx **out) {
+    if (!out) return TSID_E_INVAL;
+    *out = nullptr;
+    int count = 0;
+    if (hipGetDeviceCount(&count) != hipSuccess || device < 0 || device >= count) {
+        (void)hipGetLastError();
+        return TSID_E_DEVICE;
+    }
+    tsid_ctx *c = new tsid_ctx;
+    c->device = device;
+    c->arena.cap = max_device_bytes;
+    tsid_status st = guarded(c, [&]() {
+        if (hip_stream) {
+            c->comp = static_cast<hipStream_t>(hip_stream);
+        } else {
+            TSID_HIP(hipStreamCreateWithFlags(&c->comp, hipStreamDefault));
+            c->own_comp = true;
+        }
+        TSID_HIP(hipStreamCreateWithFlags(&c->h2d, hipStreamDefault));
+        TSID_HIP(hipStreamCreateWithFlags(&c->d2h, hipStreamDefault));
+        c->err_dev = c->arena.alloc<int32_t>(ERR_SLOTS);
+        TSID_HIP(hipHostMalloc((void **)&c->err_host, ERR_SLOTS * sizeof(int32_t), hipHostMallocDefault));
+        TSID_HIP(hipMemset(c->err_dev, 0, ERR_SLOTS * sizeof(int32_t)));
+    });
+    if (st != TSID_OK) {
+        tsid_destroy(c);
+        return st;
+    }
+    *out = c;
+    return TSID_OK;
+}
+
+void tsid_destroy(tsid_ctx *c) {
+    if (!c) return;
+    (void)hipSetDevice(c->device);
+    if (c->h2d) (void)hipStreamSynchronize(c->h2d);
+    if (c->comp) (void)hipStreamSynchronize(c->comp);
+    if (c->d2h) (void)hipStreamSynchronize(c->d2h);
+    free_template(c, c->tpl);
+    free_fit(c);
+    free_ext_buffers(c);
+    c->arena.release(c->ext.err);
+    for (auto &s : c->ext.slot) {
+        if (s.ev_h2d) (void)hipEventDestroy(s.ev_h2d);
+        if (s.ev_staged) (void)hipEventDestroy(s.ev_staged);
+        if (s.ev_done) (void)hipEventDestroy(s.ev_done);
+        if (s.ev_flushed) (void)hipEventDestroy(s.ev_flushed);
+    }
+    c->arena.release(c->err_dev);
+    if (c->err_host) (void)hipHostFree(c->err_host);
+    if (c->h2d) (void)hipStreamDestroy(c->h2d);
+    if (c->d2h) (void)hipStreamDestroy(c->d2h);
+    if (c->own_comp && c->comp) (void)hipStreamDestroy(c->comp);
+    delete c;
+}
+
+const char *tsid_last_error(const tsid_ctx *c) { return c ? c->err.c_str() : "NULL context"; }
+
+tsid_status tsid_build_template(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i,
+                                const float *r, int64_t nnz, const int32_t *I, int32_t m_t,
+                                const int32_t *J, int32_t n_t, int32_t k, int64_t stage_entries) {
+    return guarded(c, [&]() { build(c, m, n, u, i, r, nnz, I, m_t, J, n_t, k, stage_entries); });
+}
+
+tsid_status tsid_template_info(const tsid_ctx *c, int32_t *m_t, int32_t *n_t, int64_t *nnz, int32_t *k) {
+    if (!c) return TSID_E_INVAL;
+    if (!c->tpl) return TSID_E_STATE;
+    if (m_t) *m_t = c->tpl->m_t;
+    if (n_t) *n_t = c->tpl->n_t;
+    if (nnz) *nnz = c->tpl->nnz;
+    if (k) *k = c->tpl->k;
+    return TSID_OK;
+}
+
+tsid_status tsid_fit_template(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *opts,
+                              double *loss_hist) {
+    return guarded(c, [&]() { fit(c, P, Q, opts, loss_hist); });
+}
+
+tsid_status tsid_fit_epochs_done(const tsid_ctx *c, int32_t *epochs) {
+    if (!c || !epochs) return TSID_E_INVAL;
+    *epochs = c->epochs_done;
+    return TSID_OK;
+}
+
+tsid_status tsid_loss(tsid_ctx *c, const float *P, const float *Q, float lambda, double *out) {
+    return guarded(c, [&]() { loss(c, P, Q, lambda, out); });
+}
+
+tsid_status tsid_extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t *free_local,
+                              const float *r, int64_t nnz, int32_t n_free, const float *F_fixed,
+                              int64_t n_fixed, float *F_free, const tsid_fit_opts *opts) {
+    return guarded(c, [&]() {
+        extend_chunk(c, side, fixed_id, free_local, r, nnz, n_free, F_fixed, n_fixed, F_free, opts);
+    });
+}
+
+tsid_status tsid_sync(tsid_ctx *c) {
+    return guarded(c, [&]() { sync(c); });
+}
+
+tsid_status tsid_export_index(const tsid_ctx *c, int which, void *host_dst, size_t bytes) {
+    tsid_ctx *mc = const_cast<tsid_ctx *>(c);
+    return guarded(mc, [&]() { export_index(c, which, host_dst, bytes); });
+}
+
+int32_t tsid_chunk_plan(const int64_t *counts, int64_t n_free, int32_t n_chunks, int64_t max_entries,
+                        int64_t *bounds, int32_t max_bounds) {
+    if (n_free < 0 || (n_free > 0 && !counts) || !bounds || max_bounds < 1 || n_chunks < 0) return -1;
+    if (n_chunks == 0 && max_entries <= 0) return -1;
+    for (int64_t f = 0; f < n_free; ++f)
+        if (counts[f] < 0) return -1;
+    if (n_chunks > 0) {
+        if (max_bounds < n_chunks + 1) return -1;
+        // prefix of cells before each row; run j starts where the prefix first
+        // reaches ceil(j * total / n_chunks)
+        __int128 total = 0;
+        for (int64_t f = 0; f < n_free; ++f) total += counts[f];
+        int64_t f = 0;
+        __int128 before = 0;
+        for (int32_t j = 0; j < n_chunks; ++j) {
+            const __int128 target = (total * j + n_chunks - 1) / n_chunks;
+            while (f < n_free && before < target) before += counts[f++];
+            bounds[j] = f;
+        }
+        bounds[n_chunks] = n_free;
+        return n_chunks;
+    }
+    int32_t runs = 0;
+    bounds[0] = 0;
+    int64_t f = 0;
+    while (f < n_free) {
+        int64_t cells = counts[f++];
+        while (f < n_free && cells + counts[f] <= max_entries) cells += counts[f++];
+        if (runs + 2 > max_bounds) return -1;
+        bounds[++runs] = f;
+    }
+    return runs;
+}
+
+}  // extern "C"

@@ -1,0 +1,385 @@
+// Template-fit kernels (Stage I, Section 5.1): per observed cell the residual
+// e = r - p_a . q_b, the per-cell gradients of Eqs. 3-4 aggregated into the
+// owning factor row, and the row update of Eq. 5 with the asymmetric clip of
+// Section 5.3.  The same kernels run the one-sided extension steps of Section
+// 5.2 (owner = free rows, gathered side = fixed factors).
+//
+// Layout and mapping (gfx950, wave64):
+//  * A bucketed stream holds one 8-byte {other id, value} record per cell,
+//    grouped by the owning row (CSR for the P pass, CSC for the Q pass) and
+//    read once per pass with non-temporal loads.
+//  * A bucket is cut into work items of at most E cells.  Each item belongs
+//    to a group of G = K / V lanes; lane g of the group holds V consecutive
+//    factor coordinates [g*V, g*V + V) of the owner row in registers.
+//  * Per cell the group gathers the other factor row (16 bytes per lane), forms
+//    the dot product with a DPP butterfly inside the group (all lanes end with
+//    the same bits), and accumulates e * q into its registers.
+//  * The aggregated gradient goes straight to the owner row when the bucket is
+//    one item; split buckets leave one partial sum per item and a fixup kernel
+//    adds the parts in item order.  No atomics touch factor or gradient memory,
+//    so results are bitwise reproducible.
+//  * bf16 mode: the gathered side is a bf16 copy (2 bytes per coordinate, dots
+//    by v_dot2_f32_bf16 with fp32 accumulation); the owner row's fp32 master
+//    takes the update and a round-to-nearest-even bf16 copy is written beside it.
+#include "internal.h"
+
+namespace tsid {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kUnroll = 4;
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+    return __builtin_bit_cast(
+        float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, true));
+}
+
+// Sum over an aligned group of G lanes (G <= 16: the group lies inside one DPP
+// row).  Butterfly pairs: quad_perm [1,0,3,2], quad_perm [2,3,0,1],
+// row_half_mirror, row_mirror.  IEEE addition commutes, so every lane of the
+// group ends with the same bits.
+template <int G>
+__device__ __forceinline__ float group_sum(float x) {
+    if constexpr (G >= 2) x += dpp<0xB1>(x);
+    if constexpr (G >= 4) x += dpp<0x4E>(x);
+    if constexpr (G >= 8) x += dpp<0x141>(x);
+    if constexpr (G >= 16) x += dpp<0x140>(x);
+    return x;
+}
+
+// IEEE round-to-nearest-even of fp32 to bf16 (NaN stays NaN).
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <int V>
+__device__ __forceinline__ void load_f32(const float *p, float (&x)[V]) {
+    const float4 *q = reinterpret_cast<const float4 *>(p);
+#pragma unroll
+    for (int c = 0; c < V / 4; ++c) {
+        const float4 t = q[c];
+        x[4 * c + 0] = t.x;
+        x[4 * c + 1] = t.y;
+        x[4 * c + 2] = t.z;
+        x[4 * c + 3] = t.w;
+    }
+}
+
+template <int V>
+__device__ __forceinline__ void store_f32(float *p, const float (&x)[V]) {
+    float4 *q = reinterpret_cast<float4 *>(p);
+#pragma unroll
+    for (int c = 0; c < V / 4; ++c) q[c] = make_float4(x[4 * c], x[4 * c + 1], x[4 * c + 2], x[4 * c + 3]);
+}
+
+__device__ __forceinline__ int2 load_cell(const int2 *p) {
+    const long long v = __builtin_nontemporal_load(reinterpret_cast<const long long *>(p));
+    return make_int2((int)(uint32_t)(unsigned long long)v, (int)(uint32_t)((unsigned long long)v >> 32));
+}
+
+__device__ __forceinline__ bool skip_epoch(const PassArgs &A) {
+    if (!A.skip_after_nonfinite) return false;
+    const int32_t f = A.err[ERR_NONFINITE];
+    return f != 0 && f - 1 < A.epoch;
+}
+
+// Row update of Eq. 5 (descent on Eqs. 3-4 summed), optional 1/max(1, deg)
+// normalisation and the Section 5.3 clip, for this lane's V coordinates.
+template <int G, int V, bool BF16>
+__device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg, const float (&x)[V],
+                                             const float (&acc)[V], int64_t deg) {
+    const float s = A.degree ? 1.0f / (float)(deg > 1 ? deg : 1) : 1.0f;
+    float xn[V];
+    bool bad = false;
+    float nrm = 0.f;
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+        const float g = 2.0f * A.lam * x[v] - 2.0f * acc[v];
+        float d = -s * g;
+        if (A.clip && d > A.xi) d = A.xi;
+        xn[v] = x[v] + A.lr * d;
+        bad |= !__builtin_isfinite(xn[v]);
+        nrm += x[v] * x[v];
+    }
+    const int64_t off = (int64_t)row * (G * V) + lg * V;
+    store_f32<V>(A.Xn + off, xn);
+    if constexpr (BF16) {
+        static_assert(V == 8, "bf16 rows hold 8 coordinates per lane");
+        if (A.Xn_b) {
+            uint32_t w[4];
+#pragma unroll
+            for (int p = 0; p < 4; ++p) w[p] = bf16_bits(xn[2 * p]) | (bf16_bits(xn[2 * p + 1]) << 16);
+            *reinterpret_cast<uint4 *>(A.Xn_b + off) = make_uint4(w[0], w[1], w[2], w[3]);
+        }
+    }
+    nrm = group_sum<G>(nrm);
+    if (lg == 0 && A.norm) A.norm[row] = nrm;
+    if (bad) A.err[ERR_NONFINITE] = A.epoch + 1;
+}
+
+template <int K, int V, bool BF16, bool LOSS_ONLY>
+__global__ __launch_bounds__(kThreads) void k_item_pass(const PassArgs A) {
+    constexpr int G = K / V;
+    constexpr int NG = 64 / G;
+    static_assert(G >= 1 && G <= 16 && (G & (G - 1)) == 0, "group must fit a DPP row");
+    if (skip_epoch(A)) return;
+    const int lane = threadIdx.x & 63;
+    const int grp = lane / G, lg = lane % G;
+    const int64_t item = ((int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6)) * NG + grp;
+    const int64_t n_items = A.n_items_dev ? (int64_t)*A.n_items_dev : (int64_t)A.n_items;
+    if (item >= n_items) return;  // whole groups leave together
+    const int row = A.items[item];
+    const uint32_t i0 = A.item_off[row], i1 = A.item_off[row + 1];
+    const int64_t re = A.ptr[row + 1];
+    const int64_t beg = A.ptr[row] + (int64_t)(item - i0) * A.E;
+    const int64_t end = beg + A.E < re ? beg + A.E : re;
+
+    float x[V];
+    load_f32<V>(A.X + (int64_t)row * K + lg * V, x);
+    uint32_t xp[V / 2];  // bf16 pairs of the owner row (bf16 mode)
+    if constexpr (BF16) {
+#pragma unroll
+        for (int p = 0; p < V / 2; ++p) xp[p] = bf16_bits(x[2 * p]) | (bf16_bits(x[2 * p + 1]) << 16);
+    }
+    float acc[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) acc[v] = 0.f;
+    float e2 = 0.f;
+
+    for (int64_t j = beg; j < end; j += kUnroll) {
+        int2 cell[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) cell[u] = (j + u < end) ? load_cell(A.stream + j + u) : make_int2(0, 0);
+        if constexpr (BF16) {
+            uint32_t yw[kUnroll][V / 2];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const uint4 *src = reinterpret_cast<const uint4 *>(
+                    static_cast<const uint16_t *>(A.Y) + (int64_t)cell[u].x * K + lg * V);
+#pragma unroll
+                for (int c = 0; c < V / 8; ++c) {
+                    const uint4 t = src[c];
+                    yw[u][4 * c + 0] = t.x;
+                    yw[u][4 * c + 1] = t.y;
+                    yw[u][4 * c + 2] = t.z;
+                    yw[u][4 * c + 3] = t.w;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                float d = 0.f;
+#pragma unroll
+                for (int p = 0; p < V / 2; ++p)
+                    d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, xp[p]),
+                                                         __builtin_bit_cast(bf16x2, yw[u][p]), d, false);
+                d = group_sum<G>(d);
+                const float e = (j + u < end) ? __int_as_float(cell[u].y) - d : 0.f;
+                if constexpr (!LOSS_ONLY) {
+#pragma unroll
+                    for (int p = 0; p < V / 2; ++p) {
+                        acc[2 * p] += e * __uint_as_float(yw[u][p] << 16);
+                        acc[2 * p + 1] += e * __uint_as_float(yw[u][p] & 0xffff0000u);
+                    }
+                }
+                e2 += e * e;
+            }
+        } else {
+            float y[kUnroll][V];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+                load_f32<V>(static_cast<const float *>(A.Y) + (int64_t)cell[u].x * K + lg * V, y[u]);
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                float d = 0.f;
+#pragma unroll
+                for (int v = 0; v < V; ++v) d += x[v] * y[u][v];
+                d = group_sum<G>(d);
+                const float e = (j + u < end) ? __int_as_float(cell[u].y) - d : 0.f;
+                if constexpr (!LOSS_ONLY) {
+#pragma unroll
+                    for (int v = 0; v < V; ++v) acc[v] += e * y[u][v];
+                }
+                e2 += e * e;
+            }
+        }
+    }
+
+    if (A.e2 && lg == 0) A.e2[item] = e2;
+    if constexpr (LOSS_ONLY) {
+        if (A.norm && item == (int64_t)i0) {
+            float nrm = 0.f;
+#pragma unroll
+            for (int v = 0; v < V; ++v) nrm += x[v] * x[v];
+            nrm = group_sum<G>(nrm);
+            if (lg == 0) A.norm[row] = nrm;
+        }
+    } else {
+        if (i1 - i0 == 1) {
+            finalize_row<G, V, BF16>(A, row, lg, x, acc, re - A.ptr[row]);
+        } else {
+            store_f32<V>(A.carry + item * K + lg * V, acc);
+        }
+    }
+}
+
+// Split buckets: add the item partial sums in item order, then update the row.
+template <int K, int V, bool BF16>
+__global__ __launch_bounds__(kThreads) void k_fixup(const PassArgs A) {
+    constexpr int G = K / V;
+    constexpr int NG = 64 / G;
+    if (skip_epoch(A)) return;
+    const int lane = threadIdx.x & 63;
+    const int grp = lane / G, lg = lane % G;
+    const int64_t row = ((int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6)) * NG + grp;
+    if (row >= A.rows) return;
+    const uint32_t i0 = A.item_off[row], i1 = A.item_off[row + 1];
+    if (i1 - i0 <= 1) return;
+    float acc[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) acc[v] = 0.f;
+    for (uint32_t it = i0; it < i1; ++it) {
+        float part[V];
+        load_f32<V>(A.carry + (int64_t)it * K + lg * V, part);
+#pragma unroll
+        for (int v = 0; v < V; ++v) acc[v] += part[v];
+    }
+    float x[V];
+    load_f32<V>(A.X + row * K + lg * V, x);
+    finalize_row<G, V, BF16>(A, (int)row, lg, x, acc, A.ptr[row + 1] - A.ptr[row]);
+}
+
+template <int K>
+__global__ void k_row_norms(const float *X, int32_t rows, float *norm) {
+    const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= rows) return;
+    float x[K];
+    load_f32<K>(X + r * K, x);
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < K; ++c) s += x[c] * x[c];
+    norm[r] = s;
+}
+
+__global__ void k_to_bf16(const float *X, int64_t n, uint16_t *Xb) {
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n;
+         j += (int64_t)gridDim.x * blockDim.x)
+        Xb[j] = (uint16_t)bf16_bits(X[j]);
+}
+
+constexpr int kRedBlocks = 64;
+
+__global__ __launch_bounds__(256) void k_reduce_partial(const float *a, int64_t na, const float *b,
+                                                        int64_t nb, const float *c, int64_t nc,
+                                                        double *partial) {
+    __shared__ double lds[256];
+    const int which = blockIdx.x / kRedBlocks, blk = blockIdx.x % kRedBlocks;
+    const float *src = which == 0 ? a : (which == 1 ? b : c);
+    const int64_t n = which == 0 ? na : (which == 1 ? nb : nc);
+    const int64_t chunk = (n + kRedBlocks - 1) / kRedBlocks;
+    const int64_t lo = blk * chunk, hi = lo + chunk < n ? lo + chunk : n;
+    double s = 0.0;
+    if (src)
+        for (int64_t j = lo + threadIdx.x; j < hi; j += 256) s += (double)src[j];
+    lds[threadIdx.x] = s;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+        if (threadIdx.x < off) lds[threadIdx.x] += lds[threadIdx.x + off];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) partial[blockIdx.x] = lds[0];
+}
+
+__global__ void k_reduce_final(const double *partial, double lam, double *out, const int32_t *err,
+                               int32_t epoch) {
+    if (threadIdx.x != 0) return;
+    if (err && epoch >= 0) {
+        const int32_t f = err[ERR_NONFINITE];
+        if (f != 0 && f - 1 < epoch) return;
+    }
+    double s[3] = {0.0, 0.0, 0.0};
+    for (int w = 0; w < 3; ++w)
+        for (int b = 0; b < kRedBlocks; ++b) s[w] += partial[w * kRedBlocks + b];
+    *out = s[0] + lam * (s[1] + s[2]);
+}
+
+template <int K, int V, bool BF16>
+void item_pass_kv(bool loss_only, const PassArgs &a, hipStream_t s) {
+    constexpr int NG = 64 / (K / V);
+    const int grid = ceil_div(a.n_items, (int64_t)kWaves * NG);
+    if (grid <= 0) return;
+    if (loss_only) k_item_pass<K, V, BF16, true><<<grid, kThreads, 0, s>>>(a);
+    else k_item_pass<K, V, BF16, false><<<grid, kThreads, 0, s>>>(a);
+    TSID_HIP(hipGetLastError());
+}
+
+template <int K, int V, bool BF16>
+void fixup_kv(const PassArgs &a, hipStream_t s) {
+    constexpr int NG = 64 / (K / V);
+    const int grid = ceil_div(a.rows, (int64_t)kWaves * NG);
+    if (grid <= 0) return;
+    k_fixup<K, V, BF16><<<grid, kThreads, 0, s>>>(a);
+    TSID_HIP(hipGetLastError());
+}
+
+}  // namespace
+
+// Lanes per cell: fp32 rows use V = 4 coordinates per lane (8 for K = 128),
+// bf16 rows V = 8 (one 16-byte load per lane and cell).
+#define TSID_DISPATCH_K(K_, FN, ...)                                         \
+    switch (K_) {                                                            \
+        case 8: prec ? FN<8, 8, true>(__VA_ARGS__) : FN<8, 4, false>(__VA_ARGS__); break;       \
+        case 16: prec ? FN<16, 8, true>(__VA_ARGS__) : FN<16, 4, false>(__VA_ARGS__); break;    \
+        case 32: prec ? FN<32, 8, true>(__VA_ARGS__) : FN<32, 4, false>(__VA_ARGS__); break;    \
+        case 64: prec ? FN<64, 8, true>(__VA_ARGS__) : FN<64, 4, false>(__VA_ARGS__); break;    \
+        case 128: prec ? FN<128, 8, true>(__VA_ARGS__) : FN<128, 8, false>(__VA_ARGS__); break; \
+        default: fail(TSID_E_INVAL, "unsupported rank");                    \
+    }
+
+void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStream_t s) {
+    TSID_DISPATCH_K(K, item_pass_kv, loss_only, a, s)
+}
+
+void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s) {
+    TSID_DISPATCH_K(K, fixup_kv, a, s)
+}
+
+void launch_row_norms(int K, const float *X, int32_t rows, float *norm, hipStream_t s) {
+    if (rows <= 0) return;
+    const int grid = ceil_div(rows, 256);
+    switch (K) {
+        case 8: k_row_norms<8><<<grid, 256, 0, s>>>(X, rows, norm); break;
+        case 16: k_row_norms<16><<<grid, 256, 0, s>>>(X, rows, norm); break;
+        case 32: k_row_norms<32><<<grid, 256, 0, s>>>(X, rows, norm); break;
+        case 64: k_row_norms<64><<<grid, 256, 0, s>>>(X, rows, norm); break;
+        case 128: k_row_norms<128><<<grid, 256, 0, s>>>(X, rows, norm); break;
+        default: fail(TSID_E_INVAL, "unsupported rank");
+    }
+    TSID_HIP(hipGetLastError());
+}
+
+void launch_to_bf16(const float *X, int64_t n, uint16_t *Xb, hipStream_t s) {
+    if (n <= 0) return;
+    int64_t g = (n + 255) / 256;
+    k_to_bf16<<<(int)(g > 65536 ? 65536 : g), 256, 0, s>>>(X, n, Xb);
+    TSID_HIP(hipGetLastError());
+}
+
+size_t reduce_scratch_elems() { return 3 * kRedBlocks; }
+
+void launch_loss_reduce(const float *e2, int64_t ne, const float *np, int64_t nnp, const float *nq,
+                        int64_t nnq, double lam, double *partial, double *out, const int32_t *err,
+                        int32_t epoch, hipStream_t s) {
+    k_reduce_partial<<<3 * kRedBlocks, 256, 0, s>>>(e2, ne, np, nnp, nq, nnq, partial);
+    TSID_HIP(hipGetLastError());
+    k_reduce_final<<<1, 64, 0, s>>>(partial, lam, out, err, epoch);
+    TSID_HIP(hipGetLastError());
+}
+
+}  // namespace tsid

@@ -1,0 +1,125 @@
+// Internal declarations of libtsid (not part of the public C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "tsid.h"
+
+namespace tsid {
+
+// Failures inside the library are thrown as this and mapped to a status at
+// the C boundary.
+struct Error {
+    tsid_status st;
+    std::string msg;
+};
+
+[[noreturn]] void fail(tsid_status st, const std::string &msg);
+void hip_check(hipError_t e, const char *what);
+#define TSID_HIP(expr) ::tsid::hip_check((expr), #expr)
+
+// Device-side error slots (plain stores of 1, never atomics).
+enum ErrSlot { ERR_RANGE = 0, ERR_DUP = 1, ERR_INVAL = 2, ERR_NONFINITE = 3, ERR_SLOTS = 4 };
+
+inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+inline int bits_for(int64_t count) {  // bits to hold values 0..count-1 (at least 1)
+    int b = 1;
+    while (b < 63 && (int64_t(1) << b) < count) ++b;
+    return b;
+}
+
+// ------------------------------------------------------------ primitives
+// Exclusive prefix sum of n uint32 values (in == out allowed).  If total is
+// non-null the grand total is stored there (device).  `scratch` must hold
+// scan_scratch_elems(n) uint32.
+size_t scan_scratch_elems(int64_t n);
+void scan_u32(const uint32_t *in, uint32_t *out, int64_t n, uint32_t *total, uint32_t *scratch,
+              hipStream_t s);
+
+// Stable LSD radix sort of (key, value) pairs on the low `nbits` bits of the
+// key, 8 bits per pass.  Ping-pongs between the two buffers; returns true if
+// the sorted result ends in the *_alt buffers.  scratch: radix_scratch_elems(n).
+size_t radix_scratch_elems(int64_t n);
+bool radix_sort(uint64_t *keys, uint32_t *vals, uint64_t *keys_alt, uint32_t *vals_alt, int64_t n,
+                int nbits, uint32_t *scratch, hipStream_t s);
+
+void fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
+void fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s);
+void fill_f32(float *p, int64_t n, float v, hipStream_t s);
+void scatter_map(const int32_t *ids, int32_t count, int32_t *map, hipStream_t s);
+
+// Filter of one staging piece of Omega to the template (order preserving).
+// Writes packed keys (a << bits_b | b) and value bits at out + base.
+// bcnt/boffs: filter_blocks(S) uint32 each; piece_total: 1 uint32 (device).
+int filter_blocks(int64_t S);
+void filter_count(const int32_t *u, const int32_t *i, const float *r, int64_t S,
+                  const int32_t *row_map, const int32_t *col_map, int64_t m, int64_t n,
+                  uint32_t *bcnt, int32_t *err, hipStream_t s);
+void filter_write(const int32_t *u, const int32_t *i, const float *r, int64_t S,
+                  const int32_t *row_map, const int32_t *col_map, int64_t m, int64_t n,
+                  const uint32_t *boffs, int64_t base, int bits_b, uint64_t *out_key,
+                  uint32_t *out_val, hipStream_t s);
+
+// After a sort on packed keys: stream[j] = {key & low_mask, value}; flags a
+// repeated key as ERR_DUP.
+void keys_to_stream(const uint64_t *keys, const uint32_t *vals, int64_t n, int low_bits,
+                    int2 *stream, int32_t *err, hipStream_t s);
+// ptr[x] = first position whose key >> low_bits >= x, for x in [0, rows].
+void ptr_from_keys(const uint64_t *keys, int64_t n, int32_t rows, int low_bits, int64_t *ptr,
+                   hipStream_t s);
+// (hi << lo_bits | lo) -> (lo << hi_bits | hi).
+void swap_key_halves(const uint64_t *keys, int64_t n, int lo_bits, int hi_bits, uint64_t *out,
+                     hipStream_t s);
+// Extension chunk keys: key = free << bits_fixed | fixed; out-of-range ids -> ERR_RANGE.
+void chunk_keys(const int32_t *fixed_id, const int32_t *free_id, const float *r, int64_t nnz,
+                int64_t n_fixed, int32_t n_free, int bits_fixed, uint64_t *keys, uint32_t *vals,
+                int32_t *err, hipStream_t s);
+
+// Work plan of a bucketed stream: every bucket (row) becomes
+// max(1, ceil(deg / E)) items of at most E entries.  item_off has rows + 1
+// entries (item_off[rows] = total items); items[j] = bucket of item j.
+// nparts_scratch: rows uint32; scan_scratch: scan_scratch_elems(rows).
+void plan_items(const int64_t *ptr, int32_t rows, int32_t E, uint32_t *item_off, int32_t *items,
+                uint32_t *nparts_scratch, uint32_t *scan_scratch, hipStream_t s);
+
+// ------------------------------------------------------------------- fit
+struct PassArgs {
+    const int2 *stream;      // bucketed entries {other id, value bits}
+    const int64_t *ptr;      // bucket pointers (rows + 1)
+    const int32_t *items;    // bucket of each item
+    const uint32_t *item_off;  // first item of each bucket (rows + 1)
+    const uint32_t *n_items_dev;  // device item count (or null: use n_items)
+    int32_t n_items;         // item count, or an upper bound when n_items_dev is set
+    int32_t rows;            // buckets
+    int32_t E;               // entries per item
+    const float *X;          // owner factors, fp32 master (rows x K)
+    const void *Y;           // gathered factors: fp32, or bf16 bits in bf16 mode
+    float *Xn;               // updated owner factors (null in loss-only mode)
+    uint16_t *Xn_b;          // bf16 copy of Xn (bf16 mode) or null
+    float *carry;            // partial gradient sums of split buckets (n_items x K)
+    float *e2;               // per-item residual sum of squares, or null
+    float *norm;             // per-row ||x||^2 of the owner rows, or null
+    float lam, lr, xi;
+    int32_t clip, degree;
+    int32_t *err;            // device error slots
+    int32_t epoch;           // a non-finite update stores epoch + 1 in err[ERR_NONFINITE]
+    int32_t skip_after_nonfinite;  // 1: do nothing if an earlier epoch stored a flag
+};
+
+// prec: 0 fp32, 1 bf16.  loss_only: residuals, e2 and norms only.
+void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStream_t s);
+void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s);
+void launch_row_norms(int K, const float *X, int32_t rows, float *norm, hipStream_t s);
+void launch_to_bf16(const float *X, int64_t n, uint16_t *Xb, hipStream_t s);
+// out[slot] = S_e + lam (S_p + S_q) with S_* fixed-order fp64 sums; partial
+// scratch: reduce_scratch_elems() doubles.
+size_t reduce_scratch_elems();
+void launch_loss_reduce(const float *e2, int64_t ne, const float *np, int64_t nnp, const float *nq,
+                        int64_t nnq, double lam, double *partial, double *out,
+                        const int32_t *err, int32_t epoch, hipStream_t s);
+
+}  // namespace tsid

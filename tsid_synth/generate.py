@@ -157,7 +157,7 @@ def _finish(name, m, n, u, i, r, seed, I, J, k, settings, extra=None) -> Problem
 SETTINGS = {
     "tiny": dict(lam=1e-3, lr=0.05, epochs=50, step="sum", prec="fp32", clip=False, xi=0.1),
     "mid": dict(lam=1e-3, lr=0.15, epochs=100, step="degree", prec="fp32", clip=False, xi=0.1),
-    "rating": dict(lam=1e-3, lr=0.5, epochs=20, step="degree", prec="bf16", clip=True, xi=0.1),
+    "rating": dict(lam=1e-3, lr=0.15, epochs=20, step="degree", prec="bf16", clip=True, xi=0.1),
     "scientific": dict(lam=1e-3, lr=0.5, epochs=20, step="degree", prec="fp32", clip=False, xi=0.1),
 }
 
