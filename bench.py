@@ -1,0 +1,243 @@
+#!/usr/bin/env python3
+"""Throughput of the TSID template fit (Stage I, Section 5.1) on one MI355X.
+
+A step is one full-gradient epoch of the template fit: the P pass over the
+row buckets, its split-bucket fixup, the Q pass over the column buckets, its
+fixup and the loss reduction, i.e. every per-epoch kernel of the hot path.
+The metric is observed template cells per second per epoch
+(|Omega*_train| / epoch time).  Inputs are resident in HBM before the timed
+region starts; the template build (host stream, filter, bucketing) is timed
+separately and reported as build_s.
+
+Default workload: the Scientific configuration's template -- 200,000 x
+200,000 rank-32 ground truth, 10 % uniform observation, a 16,384 x 16,384
+uniform template (about 24 M training cells), k = 32, fp32, degree step.
+--config rating runs the Netflix-shaped template (65,536 x 8,192, k = 64,
+bf16 factors with fp32 accumulation and clipping); mid / tiny are small.
+
+Roofline: the dominant kernel is the item pass (P or Q), timed with HIP
+events on the library's compute stream during the timed region; its
+algorithmic bytes per launch are the compulsory bytes of one pass: the
+bucketed cell stream (8 B per cell), the bucket pointers (8 B per bucket), the
+owner rows read and written once and the gathered rows read once (4 B per
+coordinate in fp32; 2 B for bf16 copies).
+
+CPU baseline: the fp64 oracle (serial C) on a bounded sample of the same
+template cells, for as many epochs as fit in about --cpu-seconds.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="scientific", choices=["scientific", "rating", "mid", "tiny"])
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="time a plain device copy of 1 GiB instead (HBM probe and the "
+                         "reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
+    return ap.parse_args()
+
+
+def copy_probe(reps=20, nbytes=1 << 30):
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    moved = 2 * nbytes * reps
+    print(json.dumps({"probe": "device copy", "bytes_read_per_launch": nbytes,
+                      "bytes_written_per_launch": nbytes, "launches": reps + 3,
+                      "GBps_read_plus_write": moved / el / 1e9}), flush=True)
+    return 0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def pass_bytes(nnz, owners, others, k, prec):
+    """Compulsory bytes of one pass (see the module docstring)."""
+    fb = 4 * k
+    b = 8 * nnz + 8 * (owners + 1) + 2 * fb * owners + (2 * k if prec == "bf16" else fb) * others
+    if prec == "bf16":
+        b += 2 * k * owners  # bf16 copy of the updated rows
+    return b
+
+
+def traffic_from_profiles(kernel_src_sha, which):
+    """Measured HBM bytes per launch, from the committed counter summary, if it
+    was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        d = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    ent = d.get(which)
+    if not ent or ent.get("kernel_source_sha256") != kernel_src_sha:
+        return None
+    return ent.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(p, seconds):
+    import numpy as np
+
+    import oracle
+    st, rm, cm = oracle.template_maps(p.m, p.n, p.I, p.J)
+    a, b, v = oracle.filter_template(p.u, p.i, p.r, rm, cm)
+    S = int(min(a.size, 2_000_000))
+    a, b, v = a[:S], b[:S], v[:S]
+    t0 = time.perf_counter()
+    oracle.fit(a, b, v, p.P0, p.Q0, 1, p.lam, p.lr, p.step, p.clip, p.xi, bf16=p.prec == "bf16")
+    one = time.perf_counter() - t0
+    epochs = max(1, int(seconds / max(one, 1e-3)))
+    t0 = time.perf_counter()
+    oracle.fit(a, b, v, p.P0, p.Q0, epochs, p.lam, p.lr, p.step, p.clip, p.xi,
+               bf16=p.prec == "bf16")
+    el = time.perf_counter() - t0
+    return {"value": S * epochs / el, "unit": "entries/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {S} template cells (input order, i.e. a uniform random sample) of "
+                      f"the same workload, all {p.I.size} x {p.J.size} template factor rows, "
+                      f"{epochs} full-gradient epochs, serial fp64 C",
+            "seconds": el, "nproc": os.cpu_count()}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
+              "(the multi-GPU design is described but not built).", file=sys.stderr)
+        return 2
+    if args.copy_probe:
+        return copy_probe()
+    import torch
+
+    import paper_2608_00977_amd as tsid
+    import tsid_synth
+
+    log(f"generating {args.config}")
+    t0 = time.perf_counter()
+    p = tsid_synth.make(args.config)
+    gen_s = time.perf_counter() - t0
+    log(f"generated {p.nnz} training cells in {gen_s:.1f}s")
+
+    T = tsid.Tsid(0)
+    u = torch.from_numpy(p.u).pin_memory()
+    i = torch.from_numpy(p.i).pin_memory()
+    r = torch.from_numpy(p.r).pin_memory()
+    t0 = time.perf_counter()
+    T.build_template(p.m, p.n, u.numpy(), i.numpy(), r.numpy(), p.I, p.J, p.k)
+    build_s = time.perf_counter() - t0
+    info = T.info()
+    nnz = info["nnz"]
+    log(f"template {info['m_t']} x {info['n_t']}, |Omega*| = {nnz}, build {build_s:.3f}s")
+
+    P0 = torch.from_numpy(p.P0).cuda()
+    Q0 = torch.from_numpy(p.Q0).cuda()
+    mk = lambda ep: tsid.make_opts(epochs=ep, lam=p.lam, lr=p.lr, clip=p.clip, xi=p.xi,
+                                   prec=p.prec, step=p.step)
+    if args.warmup:
+        P, Q = P0.clone(), Q0.clone()
+        T.fit_template(P, Q, mk(args.warmup), want_loss=False)
+        log("warmup done")
+
+    # timed region: exactly `steps` epochs
+    P, Q = P0.clone(), Q0.clone()
+    T.set_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    T.fit_template(P, Q, mk(args.steps), want_loss=False)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    tm = T.timing()
+    T.set_timing(False)
+    ms_per_step = wall * 1e3 / args.steps
+    value = nnz / (ms_per_step / 1e3)
+    log(f"{args.steps} epochs in {wall:.4f}s: {ms_per_step:.4f} ms/epoch, {value:.4e} cells/s")
+
+    # loss after the timed run, as a sanity figure
+    hist_T = T.loss(P, Q, p.lam)
+
+    k = info["k"]
+    m_t, n_t = info["m_t"], info["n_t"]
+    by = [pass_bytes(nnz, m_t, n_t, k, p.prec), pass_bytes(nnz, n_t, m_t, k, p.prec)]
+    avg = [tm["pass_ms"][j] / max(1, tm["pass_launches"][j]) for j in range(2)]
+    dom = 0 if tm["pass_ms"][0] >= tm["pass_ms"][1] else 1
+    achieved = by[dom] / (avg[dom] / 1e3) / 1e9
+    src = open(os.path.join(ROOT, "paper_2608_00977_amd", "csrc", "fit.hip"), "rb").read()
+    sha = hashlib.sha256(src).hexdigest()
+    which = ["p_pass", "q_pass"][dom]
+    traffic = traffic_from_profiles(sha, f"{args.config}:{which}")
+    epoch_bytes = by[0] + by[1]
+    roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                "kernel": f"k_item_pass ({'P' if dom == 0 else 'Q'} pass)",
+                "bytes_per_launch": by[dom], "avg_launch_ms": round(avg[dom], 5)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        cpu = cpu_baseline(p, args.cpu_seconds)
+        log(f"oracle {cpu['value']:.4e} cells/s over {cpu['seconds']:.1f}s")
+
+    workload = {
+        "scientific": "Scientific template fit: 16,384 x 16,384 uniform template of a 200,000 x "
+                      "200,000 rank-32 matrix (10% observed), k=32, fp32, degree step",
+        "rating": "Rating-shaped template fit: 65,536 x 8,192 most-observed template of a "
+                  "480,189 x 17,770 Zipf matrix (100M ratings), k=64, bf16 + clip, degree step",
+        "mid": "Mid template fit: 4,096 x 2,048 of 20,000 x 10,000 (2M cells), k=32, fp32",
+        "tiny": "Tiny template fit: 200 x 160 of 1,000 x 800 (40k cells), k=8, fp32",
+    }[args.config]
+    line = {
+        "metric": "observed entries/sec per template-fit epoch; achieved HBM GB/s vs peak",
+        "value": value,
+        "unit": "entries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if p.prec == "bf16" else "f32",
+        "data": "synthetic (seeded generator standing in for the paper's datasets)",
+        "config": {"workload": workload, "config": args.config, "m": p.m, "n": p.n,
+                   "m_t": m_t, "n_t": n_t, "template_cells_train": nnz, "k": k,
+                   "precision": p.prec, "step": p.step, "lr": p.lr, "lambda": p.lam,
+                   "clip": p.clip, "parallelism": "single GPU"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "compulsory_GBps_per_epoch": round(epoch_bytes / (ms_per_step / 1e3) / 1e9, 2),
+        "device_epoch_ms": tm["epoch_ms"] / max(1, tm["epochs"]),
+        "kernel_ms_per_epoch": {"p_pass": avg[0], "q_pass": avg[1],
+                                "fixups": tm["fixup_ms"] / max(1, tm["epochs"]),
+                                "loss_reduce": tm["reduce_ms"] / max(1, tm["epochs"])},
+        "build_s": build_s,
+        "loss_after_timed_epochs": hist_T,
+    }
+    T.close()
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

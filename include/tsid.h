@@ -181,6 +181,26 @@ tsid_status tsid_extend_chunk(tsid_ctx *ctx, int side, const int32_t *fixed_id,
  * those chunks (and clears it), else TSID_OK. */
 tsid_status tsid_sync(tsid_ctx *ctx);
 
+/* Kernel timing of the template fit (a tracing aid).  While enabled, every
+ * epoch of tsid_fit_template records HIP events on the compute stream around
+ * its kernels, and the durations accumulate here until the next
+ * tsid_set_timing call resets them.  pass_ms[0] / pass_launches[0]: the P
+ * pass (row buckets); [1]: the Q pass (column buckets); fixup: the split-bucket
+ * fixups; reduce: the loss reductions; epoch_ms: first event to last event of
+ * each epoch, summed.  Timing adds a few microseconds per kernel. */
+typedef struct {
+    double pass_ms[2];
+    int64_t pass_launches[2];
+    double fixup_ms;
+    int64_t fixup_launches;
+    double reduce_ms;
+    int64_t reduce_launches;
+    double epoch_ms;
+    int64_t epochs;
+} tsid_timing;
+tsid_status tsid_set_timing(tsid_ctx *ctx, int enable);
+tsid_status tsid_get_timing(const tsid_ctx *ctx, tsid_timing *out);
+
 /* Index structures of the current template, copied to host_dst (HOST) for
  * bit-exact checks.  which / element type / count:
  *   TSID_IDX_ROW_MAP int32 m      TSID_IDX_COL_MAP int32 n

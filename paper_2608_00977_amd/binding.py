@@ -19,7 +19,8 @@ import numpy as np
 import torch  # imported before libtsid so both share one HIP runtime
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libtsid.so")
+# TSID_LIB_PATH selects another build of the same library (e.g. a tuning variant).
+LIB_PATH = os.environ.get("TSID_LIB_PATH") or os.path.join(_HERE, "libtsid.so")
 
 STATUS = {0: "TSID_OK", 1: "TSID_E_INVAL", 2: "TSID_E_RANGE", 3: "TSID_E_DUP",
           4: "TSID_E_NOMEM", 5: "TSID_E_DEVICE", 6: "TSID_E_STATE", 7: "TSID_E_NONFINITE"}
@@ -40,6 +41,13 @@ class tsid_fit_opts(C.Structure):
     _fields_ = [("epochs", C.c_int32), ("lambda_", C.c_float), ("lr", C.c_float),
                 ("clip_xi", C.c_float), ("clip", C.c_int32), ("prec", C.c_int32),
                 ("step", C.c_int32)]
+
+
+class tsid_timing(C.Structure):
+    _fields_ = [("pass_ms", C.c_double * 2), ("pass_launches", C.c_int64 * 2),
+                ("fixup_ms", C.c_double), ("fixup_launches", C.c_int64),
+                ("reduce_ms", C.c_double), ("reduce_launches", C.c_int64),
+                ("epoch_ms", C.c_double), ("epochs", C.c_int64)]
 
 
 _lib: Optional[C.CDLL] = None
@@ -63,6 +71,8 @@ def lib() -> C.CDLL:
         "tsid_template_info": (C.c_int, [P, P, P, P, P]),
         "tsid_fit_template": (C.c_int, [P, P, P, C.POINTER(tsid_fit_opts), P]),
         "tsid_fit_epochs_done": (C.c_int, [P, P]),
+        "tsid_set_timing": (C.c_int, [P, C.c_int]),
+        "tsid_get_timing": (C.c_int, [P, C.POINTER(tsid_timing)]),
         "tsid_loss": (C.c_int, [P, P, P, C.c_float, P]),
         "tsid_extend_chunk": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P,
                                         C.POINTER(tsid_fit_opts)]),
@@ -116,6 +126,21 @@ def tsid_fit_epochs_done(ctx) -> int:
     if st != OK:
         raise TsidError(st, "tsid_fit_epochs_done")
     return out.value
+
+
+def tsid_set_timing(ctx, enable: bool) -> int:
+    return lib().tsid_set_timing(ctx, int(bool(enable)))
+
+
+def tsid_get_timing(ctx) -> dict:
+    t = tsid_timing()
+    st = lib().tsid_get_timing(ctx, C.byref(t))
+    if st != OK:
+        raise TsidError(st, "tsid_get_timing")
+    return dict(pass_ms=[t.pass_ms[0], t.pass_ms[1]],
+                pass_launches=[t.pass_launches[0], t.pass_launches[1]],
+                fixup_ms=t.fixup_ms, fixup_launches=t.fixup_launches, reduce_ms=t.reduce_ms,
+                reduce_launches=t.reduce_launches, epoch_ms=t.epoch_ms, epochs=t.epochs)
 
 
 def tsid_loss(ctx, P, Q, lam: float, out) -> int:
@@ -216,6 +241,12 @@ class Tsid:
         if raise_on_error:
             self._check(st, "tsid_fit_template")
         return st, hist
+
+    def set_timing(self, enable: bool):
+        self._check(tsid_set_timing(self.ctx, enable), "tsid_set_timing")
+
+    def timing(self) -> dict:
+        return tsid_get_timing(self.ctx)
 
     def epochs_done(self) -> int:
         return tsid_fit_epochs_done(self.ctx)

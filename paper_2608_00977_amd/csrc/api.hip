@@ -29,8 +29,11 @@ bool valid_rank(int32_t k) { return k == 8 || k == 16 || k == 32 || k == 64 || k
 
 // Entries per work item: enough items to keep every compute unit busy, long
 // enough that the per-item overhead (owner row load, final store) stays small.
+#ifndef TSID_TARGET_ITEMS
+#define TSID_TARGET_ITEMS 131072
+#endif
 int32_t choose_E(int64_t nnz) {
-    int64_t e = (nnz + 65535) / 65536;
+    int64_t e = (nnz + TSID_TARGET_ITEMS - 1) / TSID_TARGET_ITEMS;
     e = (e + 15) / 16 * 16;
     if (e < 64) e = 64;
     if (e > 4096) e = 4096;
@@ -133,6 +136,9 @@ struct tsid_ctx {
     int32_t *err_host = nullptr;     // pinned mirror
     Template *tpl = nullptr;
     int32_t epochs_done = 0;         // of the last fit
+    bool timing = false;
+    tsid_timing tm{};
+    std::vector<hipEvent_t> events;  // timing markers, 6 per epoch
     FitBufs fb;
     ExtState ext;
 };
@@ -140,6 +146,42 @@ struct tsid_ctx {
 namespace {
 
 void set_device(const tsid_ctx *c) { TSID_HIP(hipSetDevice(c->device)); }
+
+constexpr int kMarks = 6;  // per epoch: P pass | P fixup | Q pass | Q fixup | reduce
+
+void ensure_events(tsid_ctx *c, size_t count) {
+    while (c->events.size() < count) {
+        hipEvent_t e;
+        TSID_HIP(hipEventCreate(&e));
+        c->events.push_back(e);
+    }
+}
+
+void mark(tsid_ctx *c, int ep, int slot) {
+    if (c->timing) TSID_HIP(hipEventRecord(c->events[(size_t)ep * kMarks + slot], c->comp));
+}
+
+void collect_timing(tsid_ctx *c, int epochs) {
+    auto dt = [&](int ep, int a, int b) {
+        float ms = 0.f;
+        TSID_HIP(hipEventElapsedTime(&ms, c->events[(size_t)ep * kMarks + a],
+                                     c->events[(size_t)ep * kMarks + b]));
+        return (double)ms;
+    };
+    tsid_timing &t = c->tm;
+    for (int ep = 0; ep < epochs; ++ep) {
+        t.pass_ms[0] += dt(ep, 0, 1);
+        t.fixup_ms += dt(ep, 1, 2) + dt(ep, 3, 4);
+        t.pass_ms[1] += dt(ep, 2, 3);
+        t.reduce_ms += dt(ep, 4, 5);
+        t.epoch_ms += dt(ep, 0, 5);
+        t.pass_launches[0] += 1;
+        t.pass_launches[1] += 1;
+        t.fixup_launches += 2;
+        t.reduce_launches += 1;
+        t.epochs += 1;
+    }
+}
 
 template <typename F>
 tsid_status guarded(tsid_ctx *c, F &&f) {
@@ -519,6 +561,7 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     TSID_HIP(hipMemsetAsync(c->err_dev, 0, ERR_SLOTS * sizeof(int32_t), cs));
     PassArgs ar = pass_args(t, 0, *o, c->err_dev), ac = pass_args(t, 1, *o, c->err_dev);
     ar.skip_after_nonfinite = ac.skip_after_nonfinite = 1;
+    if (c->timing) ensure_events(c, (size_t)T * kMarks);
     for (int ep = 0; ep < T; ++ep) {
         const int cur = ep & 1, nxt = cur ^ 1;
         ar.epoch = ac.epoch = ep;
@@ -530,8 +573,11 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
         ar.carry = f.carry_r;
         ar.e2 = f.e2;
         ar.norm = f.normP;
+        mark(c, ep, 0);
         launch_item_pass(K, prec, false, ar, cs);
+        mark(c, ep, 1);
         launch_fixup(K, prec, ar, cs);
+        mark(c, ep, 2);
         // Q pass (CSC): owner Q_t, gathered P_t (the old P: a simultaneous step)
         ac.X = f.Q[cur];
         ac.Y = prec ? (const void *)f.Pb[cur] : (const void *)f.P[cur];
@@ -541,9 +587,12 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
         ac.e2 = nullptr;
         ac.norm = f.normQ;
         launch_item_pass(K, prec, false, ac, cs);
+        mark(c, ep, 3);
         launch_fixup(K, prec, ac, cs);
+        mark(c, ep, 4);
         launch_loss_reduce(f.e2, t.pr.n_items, f.normP, t.m_t, f.normQ, t.n_t, o->lambda, f.partial,
                            f.loss + ep, c->err_dev, ep, cs);
+        mark(c, ep, 5);
     }
     const int fin = T & 1;
     if (loss_hist) {  // L(P_T, Q_T)
@@ -562,6 +611,7 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     if (loss_hist) TSID_HIP(hipMemcpyAsync(hist.data(), f.loss, (size_t)(T + 1) * 8, hipMemcpyDeviceToHost, cs));
     TSID_HIP(hipMemcpyAsync(c->err_host, c->err_dev, ERR_SLOTS * 4, hipMemcpyDeviceToHost, cs));
     TSID_HIP(hipStreamSynchronize(cs));
+    if (c->timing) collect_timing(c, T);
     const int32_t bad = c->err_host[ERR_NONFINITE];
     const int last = bad ? bad - 1 : T;  // factors to return: (P_last, Q_last)
     c->epochs_done = last;
@@ -845,6 +895,7 @@ void tsid_destroy(tsid_ctx *c) {
         if (s.ev_done) (void)hipEventDestroy(s.ev_done);
         if (s.ev_flushed) (void)hipEventDestroy(s.ev_flushed);
     }
+    for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
     c->arena.release(c->err_dev);
     if (c->err_host) (void)hipHostFree(c->err_host);
     if (c->h2d) (void)hipStreamDestroy(c->h2d);
@@ -874,6 +925,19 @@ tsid_status tsid_template_info(const tsid_ctx *c, int32_t *m_t, int32_t *n_t, in
 tsid_status tsid_fit_template(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *opts,
                               double *loss_hist) {
     return guarded(c, [&]() { fit(c, P, Q, opts, loss_hist); });
+}
+
+tsid_status tsid_set_timing(tsid_ctx *c, int enable) {
+    if (!c) return TSID_E_INVAL;
+    c->timing = enable != 0;
+    c->tm = tsid_timing{};
+    return TSID_OK;
+}
+
+tsid_status tsid_get_timing(const tsid_ctx *c, tsid_timing *out) {
+    if (!c || !out) return TSID_E_INVAL;
+    *out = c->tm;
+    return TSID_OK;
 }
 
 tsid_status tsid_fit_epochs_done(const tsid_ctx *c, int32_t *epochs) {

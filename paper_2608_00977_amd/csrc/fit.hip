@@ -29,7 +29,6 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kUnroll = 4;
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
@@ -50,6 +49,32 @@ __device__ __forceinline__ float group_sum(float x) {
     if constexpr (G >= 8) x += dpp<0x141>(x);
     if constexpr (G >= 16) x += dpp<0x140>(x);
     return x;
+}
+
+// Value of lane `t` of this lane's aligned group of G lanes, for every lane
+// of the group: ds_swizzle in bit mode, new lane = (lane & ~(G-1)) | t within
+// each 32-lane half (and_mask in bits 0-4, or_mask in bits 5-9).
+template <int G>
+__device__ __forceinline__ int group_bcast(int v, int t) {
+    if constexpr (G == 1) {
+        return v;
+    } else {
+        static_assert(G <= 32, "groups live inside one 32-lane half");
+        int out = v;
+        // t is a compile-time constant after unrolling; the switch keeps the
+        // swizzle pattern an immediate.
+        switch (t) {
+#define TSID_BCAST_CASE(T_) \
+    case T_: out = __builtin_amdgcn_ds_swizzle(v, (0x1F & ~(G - 1)) | ((T_) << 5)); break;
+            TSID_BCAST_CASE(0) TSID_BCAST_CASE(1) TSID_BCAST_CASE(2) TSID_BCAST_CASE(3)
+            TSID_BCAST_CASE(4) TSID_BCAST_CASE(5) TSID_BCAST_CASE(6) TSID_BCAST_CASE(7)
+            TSID_BCAST_CASE(8) TSID_BCAST_CASE(9) TSID_BCAST_CASE(10) TSID_BCAST_CASE(11)
+            TSID_BCAST_CASE(12) TSID_BCAST_CASE(13) TSID_BCAST_CASE(14) TSID_BCAST_CASE(15)
+#undef TSID_BCAST_CASE
+            default: break;
+        }
+        return out;
+    }
 }
 
 // IEEE round-to-nearest-even of fp32 to bf16 (NaN stays NaN).
@@ -79,8 +104,21 @@ __device__ __forceinline__ void store_f32(float *p, const float (&x)[V]) {
     for (int c = 0; c < V / 4; ++c) q[c] = make_float4(x[4 * c], x[4 * c + 1], x[4 * c + 2], x[4 * c + 3]);
 }
 
+// Cells a lane group takes per chunk (rounded to a multiple of the group).
+#ifndef TSID_CELLS_PER_GROUP
+#define TSID_CELLS_PER_GROUP 16
+#endif
+// 1: stream loads carry the non-temporal hint.
+#ifndef TSID_STREAM_NT
+#define TSID_STREAM_NT 0
+#endif
+
 __device__ __forceinline__ int2 load_cell(const int2 *p) {
+#if TSID_STREAM_NT
     const long long v = __builtin_nontemporal_load(reinterpret_cast<const long long *>(p));
+#else
+    const long long v = *reinterpret_cast<const long long *>(p);
+#endif
     return make_int2((int)(uint32_t)(unsigned long long)v, (int)(uint32_t)((unsigned long long)v >> 32));
 }
 
@@ -111,17 +149,116 @@ __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg,
     const int64_t off = (int64_t)row * (G * V) + lg * V;
     store_f32<V>(A.Xn + off, xn);
     if constexpr (BF16) {
-        static_assert(V == 8, "bf16 rows hold 8 coordinates per lane");
+        static_assert(V % 8 == 0, "bf16 rows hold a multiple of 8 coordinates per lane");
         if (A.Xn_b) {
-            uint32_t w[4];
 #pragma unroll
-            for (int p = 0; p < 4; ++p) w[p] = bf16_bits(xn[2 * p]) | (bf16_bits(xn[2 * p + 1]) << 16);
-            *reinterpret_cast<uint4 *>(A.Xn_b + off) = make_uint4(w[0], w[1], w[2], w[3]);
+            for (int c = 0; c < V / 8; ++c) {
+                uint32_t w[4];
+#pragma unroll
+                for (int p = 0; p < 4; ++p)
+                    w[p] = bf16_bits(xn[8 * c + 2 * p]) | (bf16_bits(xn[8 * c + 2 * p + 1]) << 16);
+                reinterpret_cast<uint4 *>(A.Xn_b + off)[c] = make_uint4(w[0], w[1], w[2], w[3]);
+            }
         }
     }
     nrm = group_sum<G>(nrm);
     if (lg == 0 && A.norm) A.norm[row] = nrm;
     if (bad) A.err[ERR_NONFINITE] = A.epoch + 1;
+}
+
+template <int G>
+constexpr int cells_per_lane() {
+    return (TSID_CELLS_PER_GROUP / G) < 1 ? 1 : (TSID_CELLS_PER_GROUP / G);
+}
+
+// One chunk of CH = G * CPL cells of a work item.  Lane s of the group holds
+// cells j0 + s + c*G (c < CPL) in `cur`.  The group broadcasts each cell's
+// column id and issues all CH gathers, then issues the loads of the following
+// chunk's cells into `nxt`, and only then does the arithmetic: loads retire in
+// issue order, so the slow stream loads must come after the gathers that the
+// arithmetic waits for.
+template <int K, int V, bool BF16, bool LOSS_ONLY>
+__device__ __forceinline__ void process_chunk(const PassArgs &A, int64_t j0, int64_t end,
+                                              int64_t last, int lg,
+                                              const int2 (&cur)[cells_per_lane<K / V>()],
+                                              int2 (&nxt)[cells_per_lane<K / V>()],
+                                              const float (&x)[V], const uint32_t (&xp)[V / 2],
+                                              float (&acc)[V], float &e2) {
+    constexpr int G = K / V;
+    constexpr int CPL = cells_per_lane<G>();
+    constexpr int CH = G * CPL;
+    const int64_t left = end - j0;
+    if constexpr (BF16) {
+        uint32_t yw[CH][V / 2];
+#pragma unroll
+        for (int t = 0; t < CH; ++t) {
+            const int b = group_bcast<G>(cur[t / G].x, t % G);
+            const uint4 *src = reinterpret_cast<const uint4 *>(
+                static_cast<const uint16_t *>(A.Y) + (int64_t)b * K + lg * V);
+#pragma unroll
+            for (int c = 0; c < V / 8; ++c) {
+                const uint4 q = src[c];
+                yw[t][4 * c + 0] = q.x;
+                yw[t][4 * c + 1] = q.y;
+                yw[t][4 * c + 2] = q.z;
+                yw[t][4 * c + 3] = q.w;
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const int64_t jn = j0 + CH + c * G + lg;
+            nxt[c] = load_cell(A.stream + (jn < last ? jn : last));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < CH; ++t) {
+            const float r = __int_as_float(group_bcast<G>(cur[t / G].y, t % G));
+            float d = 0.f;
+#pragma unroll
+            for (int p = 0; p < V / 2; ++p)
+                d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, xp[p]),
+                                                     __builtin_bit_cast(bf16x2, yw[t][p]), d, false);
+            d = group_sum<G>(d);
+            const float e = (t < left) ? r - d : 0.f;
+            if constexpr (!LOSS_ONLY) {
+#pragma unroll
+                for (int p = 0; p < V / 2; ++p) {
+                    acc[2 * p] += e * __uint_as_float(yw[t][p] << 16);
+                    acc[2 * p + 1] += e * __uint_as_float(yw[t][p] & 0xffff0000u);
+                }
+            }
+            e2 += e * e;
+        }
+    } else {
+        float y[CH][V];
+#pragma unroll
+        for (int t = 0; t < CH; ++t) {
+            const int b = group_bcast<G>(cur[t / G].x, t % G);
+            load_f32<V>(static_cast<const float *>(A.Y) + (int64_t)b * K + lg * V, y[t]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const int64_t jn = j0 + CH + c * G + lg;
+            nxt[c] = load_cell(A.stream + (jn < last ? jn : last));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int t = 0; t < CH; ++t) {
+            const float r = __int_as_float(group_bcast<G>(cur[t / G].y, t % G));
+            float d = 0.f;
+#pragma unroll
+            for (int v = 0; v < V; ++v) d += x[v] * y[t][v];
+            d = group_sum<G>(d);
+            const float e = (t < left) ? r - d : 0.f;
+            if constexpr (!LOSS_ONLY) {
+#pragma unroll
+                for (int v = 0; v < V; ++v) acc[v] += e * y[t][v];
+            }
+            e2 += e * e;
+        }
+    }
 }
 
 template <int K, int V, bool BF16, bool LOSS_ONLY>
@@ -143,7 +280,7 @@ __global__ __launch_bounds__(kThreads) void k_item_pass(const PassArgs A) {
 
     float x[V];
     load_f32<V>(A.X + (int64_t)row * K + lg * V, x);
-    uint32_t xp[V / 2];  // bf16 pairs of the owner row (bf16 mode)
+    uint32_t xp[V / 2] = {};  // bf16 pairs of the owner row (bf16 mode)
     if constexpr (BF16) {
 #pragma unroll
         for (int p = 0; p < V / 2; ++p) xp[p] = bf16_bits(x[2 * p]) | (bf16_bits(x[2 * p + 1]) << 16);
@@ -153,62 +290,26 @@ __global__ __launch_bounds__(kThreads) void k_item_pass(const PassArgs A) {
     for (int v = 0; v < V; ++v) acc[v] = 0.f;
     float e2 = 0.f;
 
-    for (int64_t j = beg; j < end; j += kUnroll) {
-        int2 cell[kUnroll];
+    // The group walks its cells CH = G * CPL at a time (see process_chunk);
+    // two cell buffers alternate so the next chunk's cells load into the
+    // buffer not in use.  Loads past the item's end re-read its last cell
+    // (always in bounds and unconditional, so outstanding loads are counted
+    // exactly); the slots they fill are masked inside process_chunk.
+    constexpr int CPL = cells_per_lane<G>();
+    constexpr int CH = G * CPL;
+    const int64_t last = end - 1;
+    int2 bufA[CPL], bufB[CPL];
+    if (end > beg) {
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) cell[u] = (j + u < end) ? load_cell(A.stream + j + u) : make_int2(0, 0);
-        if constexpr (BF16) {
-            uint32_t yw[kUnroll][V / 2];
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                const uint4 *src = reinterpret_cast<const uint4 *>(
-                    static_cast<const uint16_t *>(A.Y) + (int64_t)cell[u].x * K + lg * V);
-#pragma unroll
-                for (int c = 0; c < V / 8; ++c) {
-                    const uint4 t = src[c];
-                    yw[u][4 * c + 0] = t.x;
-                    yw[u][4 * c + 1] = t.y;
-                    yw[u][4 * c + 2] = t.z;
-                    yw[u][4 * c + 3] = t.w;
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                float d = 0.f;
-#pragma unroll
-                for (int p = 0; p < V / 2; ++p)
-                    d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, xp[p]),
-                                                         __builtin_bit_cast(bf16x2, yw[u][p]), d, false);
-                d = group_sum<G>(d);
-                const float e = (j + u < end) ? __int_as_float(cell[u].y) - d : 0.f;
-                if constexpr (!LOSS_ONLY) {
-#pragma unroll
-                    for (int p = 0; p < V / 2; ++p) {
-                        acc[2 * p] += e * __uint_as_float(yw[u][p] << 16);
-                        acc[2 * p + 1] += e * __uint_as_float(yw[u][p] & 0xffff0000u);
-                    }
-                }
-                e2 += e * e;
-            }
-        } else {
-            float y[kUnroll][V];
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
-                load_f32<V>(static_cast<const float *>(A.Y) + (int64_t)cell[u].x * K + lg * V, y[u]);
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                float d = 0.f;
-#pragma unroll
-                for (int v = 0; v < V; ++v) d += x[v] * y[u][v];
-                d = group_sum<G>(d);
-                const float e = (j + u < end) ? __int_as_float(cell[u].y) - d : 0.f;
-                if constexpr (!LOSS_ONLY) {
-#pragma unroll
-                    for (int v = 0; v < V; ++v) acc[v] += e * y[u][v];
-                }
-                e2 += e * e;
-            }
+        for (int c = 0; c < CPL; ++c) {
+            const int64_t jj = beg + c * G + lg;
+            bufA[c] = load_cell(A.stream + (jj < last ? jj : last));
         }
+    }
+    for (int64_t j0 = beg; j0 < end; j0 += 2 * CH) {
+        process_chunk<K, V, BF16, LOSS_ONLY>(A, j0, end, last, lg, bufA, bufB, x, xp, acc, e2);
+        if (j0 + CH >= end) break;
+        process_chunk<K, V, BF16, LOSS_ONLY>(A, j0 + CH, end, last, lg, bufB, bufA, x, xp, acc, e2);
     }
 
     if (A.e2 && lg == 0) A.e2[item] = e2;
@@ -330,16 +431,40 @@ void fixup_kv(const PassArgs &a, hipStream_t s) {
 
 }  // namespace
 
-// Lanes per cell: fp32 rows use V = 4 coordinates per lane (8 for K = 128),
-// bf16 rows V = 8 (one 16-byte load per lane and cell).
-#define TSID_DISPATCH_K(K_, FN, ...)                                         \
-    switch (K_) {                                                            \
-        case 8: prec ? FN<8, 8, true>(__VA_ARGS__) : FN<8, 4, false>(__VA_ARGS__); break;       \
-        case 16: prec ? FN<16, 8, true>(__VA_ARGS__) : FN<16, 4, false>(__VA_ARGS__); break;    \
-        case 32: prec ? FN<32, 8, true>(__VA_ARGS__) : FN<32, 4, false>(__VA_ARGS__); break;    \
-        case 64: prec ? FN<64, 8, true>(__VA_ARGS__) : FN<64, 4, false>(__VA_ARGS__); break;    \
-        case 128: prec ? FN<128, 8, true>(__VA_ARGS__) : FN<128, 8, false>(__VA_ARGS__); break; \
-        default: fail(TSID_E_INVAL, "unsupported rank");                    \
+// Coordinates per lane (V) for each rank: a cell is handled by G = K / V
+// lanes.  Smaller G means fewer DPP and swizzle steps per cell; larger G means
+// fewer distinct rows per gather instruction.
+#ifndef TSID_V_F32_8
+#define TSID_V_F32_8 4
+#endif
+#ifndef TSID_V_F32_16
+#define TSID_V_F32_16 4
+#endif
+#ifndef TSID_V_F32_32
+#define TSID_V_F32_32 4
+#endif
+#ifndef TSID_V_F32_64
+#define TSID_V_F32_64 4
+#endif
+#ifndef TSID_V_F32_128
+#define TSID_V_F32_128 8
+#endif
+#ifndef TSID_V_BF16_64
+#define TSID_V_BF16_64 8
+#endif
+#ifndef TSID_V_BF16_128
+#define TSID_V_BF16_128 8
+#endif
+#define TSID_DISPATCH_K(K_, FN, ...)                                                              \
+    switch (K_) {                                                                                 \
+        case 8: prec ? FN<8, 8, true>(__VA_ARGS__) : FN<8, TSID_V_F32_8, false>(__VA_ARGS__); break; \
+        case 16: prec ? FN<16, 8, true>(__VA_ARGS__) : FN<16, TSID_V_F32_16, false>(__VA_ARGS__); break; \
+        case 32: prec ? FN<32, 8, true>(__VA_ARGS__) : FN<32, TSID_V_F32_32, false>(__VA_ARGS__); break; \
+        case 64: prec ? FN<64, TSID_V_BF16_64, true>(__VA_ARGS__)                                   \
+                      : FN<64, TSID_V_F32_64, false>(__VA_ARGS__); break;                        \
+        case 128: prec ? FN<128, TSID_V_BF16_128, true>(__VA_ARGS__)                                \
+                       : FN<128, TSID_V_F32_128, false>(__VA_ARGS__); break;                     \
+        default: fail(TSID_E_INVAL, "unsupported rank");                                         \
     }
 
 void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStream_t s) {

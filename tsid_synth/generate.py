@@ -113,15 +113,21 @@ def _zipf_cdf(size: int, s: float, g: np.random.Generator) -> np.ndarray:
     return c / c[-1]
 
 
+def _inv_cdf(cdf: np.ndarray, x: np.ndarray) -> np.ndarray:
+    """First index with cdf > x (numpy's searchsorted 'right'), threaded."""
+    import torch
+    return torch.searchsorted(torch.from_numpy(cdf), torch.from_numpy(x), right=True).numpy()
+
+
 def _distinct_zipf_cells(m, n, target, cdf_r, cdf_c, g):
     """Exactly `target` distinct cells drawn pairwise from the two
     popularity laws; repeated draws of a cell are discarded and topped up."""
     keys = np.empty(0, dtype=np.int64)
     while keys.size < target:
         need = target - keys.size
-        batch = int(need * 1.25) + 4096
-        u = np.searchsorted(cdf_r, g.random(batch), side="right").clip(0, m - 1)
-        i = np.searchsorted(cdf_c, g.random(batch), side="right").clip(0, n - 1)
+        batch = int(need * 2.0) + 65536
+        u = _inv_cdf(cdf_r, g.random(batch)).clip(0, m - 1)
+        i = _inv_cdf(cdf_c, g.random(batch)).clip(0, n - 1)
         keys = np.unique(np.concatenate([keys, u.astype(np.int64) * n + i]))
     if keys.size > target:
         keys = np.sort(keys[g.choice(keys.size, target, replace=False)])
@@ -136,10 +142,26 @@ def _most_observed(ids_deg: np.ndarray, count: int) -> np.ndarray:
 
 
 def _latent_values(u, i, A, B, chunk=1 << 22):
+    """x_e = A[u_e] . B[i_e] for every cell (fp32 products summed by torch's
+    multi-threaded CPU kernels; the generator needs speed, not fp64 here)."""
+    import torch
+    At = torch.from_numpy(np.ascontiguousarray(A, np.float32))
+    Bt = torch.from_numpy(np.ascontiguousarray(B, np.float32))
     out = np.empty(u.size, dtype=np.float64)
+    n0 = min(chunk, u.size)
+    ga = torch.empty((n0, At.shape[1]), dtype=torch.float32)  # reused: no page faults per chunk
+    gb = torch.empty((n0, At.shape[1]), dtype=torch.float32)
+    dot = torch.empty(n0, dtype=torch.float32)
     for s in range(0, u.size, chunk):
         e = min(u.size, s + chunk)
-        out[s:e] = np.einsum("ij,ij->i", A[u[s:e]], B[i[s:e]])
+        n = e - s
+        uu = torch.from_numpy(np.ascontiguousarray(u[s:e], np.int64))
+        ii = torch.from_numpy(np.ascontiguousarray(i[s:e], np.int64))
+        torch.index_select(At, 0, uu, out=ga[:n])
+        torch.index_select(Bt, 0, ii, out=gb[:n])
+        ga[:n].mul_(gb[:n])
+        torch.sum(ga[:n], 1, out=dot[:n])
+        out[s:e] = dot[:n].numpy()
     return out
 
 
@@ -236,21 +258,23 @@ def scientific_template(seed: int = 4, side: int = 16384, m: int = 200000) -> Pr
     sig = sig / np.linalg.norm(sig)
     A = gf.standard_normal((m, k)).astype(np.float32)
     B = gf.standard_normal((n, k)).astype(np.float32)
-    us, is_ = [], []
-    rows_per = max(1, (1 << 24) // side)
+    us, is_, rs = [], [], []
+    rows_per = max(1, (1 << 20) // side)
+    Ju = J.astype(np.uint64)
+    BsT = np.ascontiguousarray((B[J] * sig[None, :].astype(np.float32)).T)
     for a0 in range(0, side, rows_per):
         a1 = min(side, a0 + rows_per)
-        uu = np.repeat(I[a0:a1], side)
-        ii = np.tile(J, a1 - a0)
-        keep = _hash_below(_cell_hash(uu, ii, n, seed, "cells"), 0.1)
-        us.append(uu[keep])
-        is_.append(ii[keep])
+        uu = I[a0:a1].astype(np.uint64)[:, None]
+        keep = _hash_below(_cell_hash(uu, Ju[None, :], n, seed, "cells"), 0.1)
+        ra, cb = np.nonzero(keep)
+        us.append(I[a0:a1][ra])
+        is_.append(J[cb])
+        rs.append((A[I[a0:a1]] @ BsT)[ra, cb])
     u = np.concatenate(us)
     i = np.concatenate(is_)
+    r = np.concatenate(rs)
     perm = make_rng(seed, "order").permutation(u.size)
-    u, i = u[perm], i[perm]
-    Bs = (B * sig[None, :].astype(np.float32))
-    r = _latent_values(u, i, A, Bs)
+    u, i, r = u[perm], i[perm], r[perm]
     return _finish("scientific", m, n, u, i, r, seed, I, J, k, SETTINGS["scientific"],
                    extra={"omega_scope": "template block only"})
 
