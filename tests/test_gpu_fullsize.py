@@ -1,0 +1,58 @@
+"""Parity at full benchmark size, in the launch configuration bench.py times,
+on sampled outputs the oracle can compute one by one.
+
+One full-gradient epoch from (P0, Q0): the new row p_a depends only on the
+cells of row a and on Q0, so the oracle, given just the cells of a sample of
+rows (or columns), reproduces those rows exactly.  The loss L(P0, Q0) over
+all of Omega* is checked as a whole.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import tsid_synth as synth
+from gpu_util import gpu_fit, note, oracle_template, rel_fro
+
+pytestmark = pytest.mark.gpu
+
+
+def _sampled_parity(T, p, n_rows=64, n_cols=64, tol=1e-4):
+    rm, cm, a, b, v = oracle_template(p)
+    note(f"fullsize {p.name}: building template over {p.nnz} cells")
+    T.build_template(p.m, p.n, p.u, p.i, p.r, p.I, p.J, p.k)
+    assert T.info()["nnz"] == a.size
+    st, P1, Q1, hist = gpu_fit(T, p, epochs=1)
+    assert st == 0
+    g = np.random.default_rng(0)
+    rows = g.choice(p.I.size, n_rows, replace=False)
+    cols = g.choice(p.J.size, n_cols, replace=False)
+    bf16 = p.prec == "bf16"
+    sel = np.isin(a, rows)
+    _, Po, _, _, _ = oracle.fit(a[sel], b[sel], v[sel], p.P0, p.Q0, 1, p.lam, p.lr, p.step, p.clip,
+                                p.xi, bf16=bf16)
+    assert rel_fro(P1[rows], Po[rows]) <= tol
+    sel = np.isin(b, cols)
+    _, _, Qo, _, _ = oracle.fit(a[sel], b[sel], v[sel], p.P0, p.Q0, 1, p.lam, p.lr, p.step, p.clip,
+                                p.xi, bf16=bf16)
+    assert rel_fro(Q1[cols], Qo[cols]) <= tol
+    if not bf16:
+        L0 = oracle.loss(a, b, v, p.I.size, p.J.size, p.P0, p.Q0, p.lam)
+        assert abs(hist[0] - L0) <= 1e-6 * L0
+
+
+@pytest.fixture(scope="module")
+def T():
+    import paper_2608_00977_amd as tsid
+    t = tsid.Tsid(0)
+    yield t
+    t.close()
+
+
+@pytest.mark.timeout(300)
+def test_scientific_fullsize_sampled(T):
+    _sampled_parity(T, synth.scientific_template())
+
+
+@pytest.mark.timeout(400)
+def test_rating_fullsize_sampled_bf16(T):
+    _sampled_parity(T, synth.rating())
