@@ -531,6 +531,7 @@ PassArgs pass_args(const Template &t, int side, const tsid_fit_opts &o, int32_t 
     a.n_items_dev = nullptr;
     a.n_items = pl.n_items;
     a.rows = side ? t.n_t : t.m_t;
+    a.y_rows = side ? t.m_t : t.n_t;
     a.E = pl.E;
     a.lam = o.lambda;
     a.lr = o.lr;
@@ -763,6 +764,7 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
     a.rows = n_free;
     a.E = E;
     a.Y = F_fixed;
+    a.y_rows = n_fixed;
     a.carry = x.carry;
     a.lam = o->lambda;
     a.lr = o->lr;

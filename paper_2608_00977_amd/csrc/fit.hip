@@ -54,10 +54,26 @@ __device__ __forceinline__ float group_sum(float x) {
 // Value of lane `t` of this lane's aligned group of G lanes, for every lane
 // of the group: ds_swizzle in bit mode, new lane = (lane & ~(G-1)) | t within
 // each 32-lane half (and_mask in bits 0-4, or_mask in bits 5-9).
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int x) {
+    return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, true);
+}
+
 template <int G>
 __device__ __forceinline__ int group_bcast(int v, int t) {
     if constexpr (G == 1) {
         return v;
+    } else if constexpr (G == 2) {
+        // DPP quad_perm [t, t, 2+t, 2+t]: a VALU move, no LDS traffic
+        return t == 0 ? dpp_i<0xA0>(v) : dpp_i<0xF5>(v);
+    } else if constexpr (G == 4) {
+        // DPP quad_perm [t, t, t, t]
+        switch (t) {
+            case 0: return dpp_i<0x00>(v);
+            case 1: return dpp_i<0x55>(v);
+            case 2: return dpp_i<0xAA>(v);
+            default: return dpp_i<0xFF>(v);
+        }
     } else {
         static_assert(G <= 32, "groups live inside one 32-lane half");
         int out = v;
@@ -106,7 +122,7 @@ __device__ __forceinline__ void store_f32(float *p, const float (&x)[V]) {
 
 // Cells a lane group takes per chunk (rounded to a multiple of the group).
 #ifndef TSID_CELLS_PER_GROUP
-#define TSID_CELLS_PER_GROUP 16
+#define TSID_CELLS_PER_GROUP 8
 #endif
 // 1: stream loads carry the non-temporal hint.
 #ifndef TSID_STREAM_NT
@@ -166,103 +182,181 @@ __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg,
     if (bad) A.err[ERR_NONFINITE] = A.epoch + 1;
 }
 
-template <int G>
-constexpr int cells_per_lane() {
-    return (TSID_CELLS_PER_GROUP / G) < 1 ? 1 : (TSID_CELLS_PER_GROUP / G);
+// Gathers of the other factor.  Within the template (tables below 4 GiB) they
+// are raw buffer loads: one 32-bit offset register per gather instead of a
+// 64-bit address, and the hardware clamps any offset past the table to zero.
+// The extension's fixed table may exceed 4 GiB and uses 64-bit global loads.
+struct YTable {
+    __amdgpu_buffer_rsrc_t rsrc;
+    const char *base;
+};
+
+template <bool BUF>
+__device__ __forceinline__ YTable make_ytable(const PassArgs &A, int row_bytes) {
+    YTable t;
+    t.base = static_cast<const char *>(A.Y);
+    if constexpr (BUF) {
+        // raw buffer, 32-bit data format (descriptor word 3 of the gfx9 family)
+        t.rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(A.Y), (short)0,
+                                                   (int)(A.y_rows * row_bytes), 0x00020000);
+    }
+    return t;
 }
 
-// One chunk of CH = G * CPL cells of a work item.  Lane s of the group holds
-// cells j0 + s + c*G (c < CPL) in `cur`.  The group broadcasts each cell's
-// column id and issues all CH gathers, then issues the loads of the following
-// chunk's cells into `nxt`, and only then does the arithmetic: loads retire in
-// issue order, so the slow stream loads must come after the gathers that the
-// arithmetic waits for.
-template <int K, int V, bool BF16, bool LOSS_ONLY>
-__device__ __forceinline__ void process_chunk(const PassArgs &A, int64_t j0, int64_t end,
-                                              int64_t last, int lg,
-                                              const int2 (&cur)[cells_per_lane<K / V>()],
-                                              int2 (&nxt)[cells_per_lane<K / V>()],
+// 16 bytes of row b of the table at byte offset `col_byte` within the row.
+template <bool BUF>
+__device__ __forceinline__ uint4 ygather16(const YTable &t, int b, int row_bytes, int col_byte) {
+    if constexpr (BUF) {
+        return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                             t.rsrc, (unsigned)(b * row_bytes + col_byte), 0, 0));
+    } else {
+        return *reinterpret_cast<const uint4 *>(t.base + (int64_t)b * row_bytes + col_byte);
+    }
+}
+
+// Stream layout of a group's walk over its item: cells arrive in blocks of
+// SB = G * SPL cells (SPL per lane: lane s holds cells s + c*G, c < SPL),
+// and are consumed in chunks of CH cells, CH gathers in flight per lane.
+#ifndef TSID_PINGPONG
+#define TSID_PINGPONG 0
+#endif
+#ifndef TSID_CHUNK_BARRIER
+#define TSID_CHUNK_BARRIER 0
+#endif
+#ifndef TSID_STREAM_SPL
+#define TSID_STREAM_SPL 16
+#endif
+template <int G>
+constexpr int chunk_cells() {
+    return TSID_CELLS_PER_GROUP < G ? G : TSID_CELLS_PER_GROUP;
+}
+template <int G>
+constexpr int block_spl() {  // stream cells per lane per block
+    return (G * TSID_STREAM_SPL) < chunk_cells<G>() ? (chunk_cells<G>() / G) : TSID_STREAM_SPL;
+}
+
+// One stream block of a work item (SB = G * SPL cells starting at j0).  Per
+// chunk of CH cells the group broadcasts each cell's column id and issues
+// all CH gathers, then does the arithmetic.  After the gathers of the last
+// chunk -- and before its arithmetic -- the group issues the loads of the
+// next block's cells into `nxt`: loads retire in issue order, so the slow
+// stream loads must come after every gather the arithmetic waits for, and
+// issuing them once per block exposes their latency once per SB cells.
+template <int K, int V, bool BF16, bool LOSS_ONLY, bool BUF>
+__device__ __forceinline__ void process_block(const PassArgs &A, const YTable &Yt, int64_t j0,
+                                              int64_t end, int64_t last, int lg,
+                                              const int2 (&cur)[block_spl<K / V>()],
+                                              int2 (&nxt)[block_spl<K / V>()],
                                               const float (&x)[V], const uint32_t (&xp)[V / 2],
                                               float (&acc)[V], float &e2) {
     constexpr int G = K / V;
-    constexpr int CPL = cells_per_lane<G>();
-    constexpr int CH = G * CPL;
+    constexpr int SPL = block_spl<G>();
+    constexpr int SB = G * SPL;
+    constexpr int CH = chunk_cells<G>();
+    static_assert(SB % CH == 0, "a stream block holds whole chunks");
     const int64_t left = end - j0;
-    if constexpr (BF16) {
-        uint32_t yw[CH][V / 2];
 #pragma unroll
-        for (int t = 0; t < CH; ++t) {
-            const int b = group_bcast<G>(cur[t / G].x, t % G);
-            const uint4 *src = reinterpret_cast<const uint4 *>(
-                static_cast<const uint16_t *>(A.Y) + (int64_t)b * K + lg * V);
+    for (int c0 = 0; c0 < SB; c0 += CH) {
+        const bool last_chunk = (c0 + CH == SB);
+        if (c0 > 0 && c0 >= left) break;  // the item ends inside this block
+#if TSID_CHUNK_BARRIER
+        __builtin_amdgcn_sched_barrier(0);  // no hoisting across chunks: fewer live registers
+#endif
+        if constexpr (BF16) {
+            uint32_t yw[CH][V / 2];
 #pragma unroll
-            for (int c = 0; c < V / 8; ++c) {
-                const uint4 q = src[c];
-                yw[t][4 * c + 0] = q.x;
-                yw[t][4 * c + 1] = q.y;
-                yw[t][4 * c + 2] = q.z;
-                yw[t][4 * c + 3] = q.w;
-            }
-        }
-        __builtin_amdgcn_sched_barrier(0);
+            for (int t = 0; t < CH; ++t) {
+                const int b = group_bcast<G>(cur[(c0 + t) / G].x, (c0 + t) % G);
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-            const int64_t jn = j0 + CH + c * G + lg;
-            nxt[c] = load_cell(A.stream + (jn < last ? jn : last));
-        }
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int t = 0; t < CH; ++t) {
-            const float r = __int_as_float(group_bcast<G>(cur[t / G].y, t % G));
-            float d = 0.f;
-#pragma unroll
-            for (int p = 0; p < V / 2; ++p)
-                d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, xp[p]),
-                                                     __builtin_bit_cast(bf16x2, yw[t][p]), d, false);
-            d = group_sum<G>(d);
-            const float e = (t < left) ? r - d : 0.f;
-            if constexpr (!LOSS_ONLY) {
-#pragma unroll
-                for (int p = 0; p < V / 2; ++p) {
-                    acc[2 * p] += e * __uint_as_float(yw[t][p] << 16);
-                    acc[2 * p + 1] += e * __uint_as_float(yw[t][p] & 0xffff0000u);
+                for (int c = 0; c < V / 8; ++c) {
+                    const uint4 q = ygather16<BUF>(Yt, b, K * 2, (lg * V + 8 * c) * 2);
+                    yw[t][4 * c + 0] = q.x;
+                    yw[t][4 * c + 1] = q.y;
+                    yw[t][4 * c + 2] = q.z;
+                    yw[t][4 * c + 3] = q.w;
                 }
             }
-            e2 += e * e;
-        }
-    } else {
-        float y[CH][V];
+            if (last_chunk) {
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int t = 0; t < CH; ++t) {
-            const int b = group_bcast<G>(cur[t / G].x, t % G);
-            load_f32<V>(static_cast<const float *>(A.Y) + (int64_t)b * K + lg * V, y[t]);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-            const int64_t jn = j0 + CH + c * G + lg;
-            nxt[c] = load_cell(A.stream + (jn < last ? jn : last));
-        }
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int t = 0; t < CH; ++t) {
-            const float r = __int_as_float(group_bcast<G>(cur[t / G].y, t % G));
-            float d = 0.f;
-#pragma unroll
-            for (int v = 0; v < V; ++v) d += x[v] * y[t][v];
-            d = group_sum<G>(d);
-            const float e = (t < left) ? r - d : 0.f;
-            if constexpr (!LOSS_ONLY) {
-#pragma unroll
-                for (int v = 0; v < V; ++v) acc[v] += e * y[t][v];
+                for (int c = 0; c < SPL; ++c) {
+                    const int64_t jn = j0 + SB + c * G + lg;
+                    nxt[c] = load_cell(A.stream + (jn < last ? jn : last));
+                }
+                __builtin_amdgcn_sched_barrier(0);
             }
-            e2 += e * e;
+#pragma unroll
+            for (int t = 0; t < CH; ++t) {
+                const float r = __int_as_float(group_bcast<G>(cur[(c0 + t) / G].y, (c0 + t) % G));
+                float d = 0.f;
+#pragma unroll
+                for (int p = 0; p < V / 2; ++p)
+                    d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, xp[p]),
+                                                         __builtin_bit_cast(bf16x2, yw[t][p]), d, false);
+                d = group_sum<G>(d);
+                const float e = (c0 + t < left) ? r - d : 0.f;
+                if constexpr (!LOSS_ONLY) {
+#pragma unroll
+                    for (int p = 0; p < V / 2; ++p) {
+                        acc[2 * p] += e * __uint_as_float(yw[t][p] << 16);
+                        acc[2 * p + 1] += e * __uint_as_float(yw[t][p] & 0xffff0000u);
+                    }
+                }
+                e2 += e * e;
+            }
+        } else {
+            float y[CH][V];
+#pragma unroll
+            for (int t = 0; t < CH; ++t) {
+                const int b = group_bcast<G>(cur[(c0 + t) / G].x, (c0 + t) % G);
+#pragma unroll
+                for (int c = 0; c < V / 4; ++c) {
+                    const uint4 q = ygather16<BUF>(Yt, b, K * 4, (lg * V + 4 * c) * 4);
+                    y[t][4 * c + 0] = __uint_as_float(q.x);
+                    y[t][4 * c + 1] = __uint_as_float(q.y);
+                    y[t][4 * c + 2] = __uint_as_float(q.z);
+                    y[t][4 * c + 3] = __uint_as_float(q.w);
+                }
+            }
+            if (last_chunk) {
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int c = 0; c < SPL; ++c) {
+                    const int64_t jn = j0 + SB + c * G + lg;
+                    nxt[c] = load_cell(A.stream + (jn < last ? jn : last));
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+#pragma unroll
+            for (int t = 0; t < CH; ++t) {
+                const float r = __int_as_float(group_bcast<G>(cur[(c0 + t) / G].y, (c0 + t) % G));
+                float d = 0.f;
+#pragma unroll
+                for (int v = 0; v < V; ++v) d += x[v] * y[t][v];
+                d = group_sum<G>(d);
+                const float e = (c0 + t < left) ? r - d : 0.f;
+                if constexpr (!LOSS_ONLY) {
+#pragma unroll
+                    for (int v = 0; v < V; ++v) acc[v] += e * y[t][v];
+                }
+                e2 += e * e;
+            }
         }
     }
 }
 
-template <int K, int V, bool BF16, bool LOSS_ONLY>
-__global__ __launch_bounds__(kThreads) void k_item_pass(const PassArgs A) {
+// Waves per SIMD the register allocation must allow (0: compiler's choice).
+#ifndef TSID_WAVES_PER_EU
+#define TSID_WAVES_PER_EU 0
+#endif
+#if TSID_WAVES_PER_EU > 0
+#define TSID_OCCUPANCY __attribute__((amdgpu_waves_per_eu(TSID_WAVES_PER_EU, TSID_WAVES_PER_EU)))
+#else
+#define TSID_OCCUPANCY
+#endif
+
+template <int K, int V, bool BF16, bool LOSS_ONLY, bool BUF>
+__global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass(const PassArgs A) {
     constexpr int G = K / V;
     constexpr int NG = 64 / G;
     static_assert(G >= 1 && G <= 16 && (G & (G - 1)) == 0, "group must fit a DPP row");
@@ -290,27 +384,41 @@ __global__ __launch_bounds__(kThreads) void k_item_pass(const PassArgs A) {
     for (int v = 0; v < V; ++v) acc[v] = 0.f;
     float e2 = 0.f;
 
-    // The group walks its cells CH = G * CPL at a time (see process_chunk);
-    // two cell buffers alternate so the next chunk's cells load into the
-    // buffer not in use.  Loads past the item's end re-read its last cell
-    // (always in bounds and unconditional, so outstanding loads are counted
-    // exactly); the slots they fill are masked inside process_chunk.
-    constexpr int CPL = cells_per_lane<G>();
-    constexpr int CH = G * CPL;
+    // The group walks its cells one stream block at a time (see
+    // process_block); two cell buffers alternate so the next block's cells
+    // load into the buffer not in use.  Loads past the item's end re-read its
+    // last cell (always in bounds and unconditional, so outstanding loads are
+    // counted exactly); the slots they fill are masked inside process_block.
+    constexpr int SPL = block_spl<G>();
+    constexpr int SB = G * SPL;
     const int64_t last = end - 1;
-    int2 bufA[CPL], bufB[CPL];
+    int2 bufA[SPL], bufB[SPL];
     if (end > beg) {
 #pragma unroll
-        for (int c = 0; c < CPL; ++c) {
+        for (int c = 0; c < SPL; ++c) {
             const int64_t jj = beg + c * G + lg;
             bufA[c] = load_cell(A.stream + (jj < last ? jj : last));
         }
     }
-    for (int64_t j0 = beg; j0 < end; j0 += 2 * CH) {
-        process_chunk<K, V, BF16, LOSS_ONLY>(A, j0, end, last, lg, bufA, bufB, x, xp, acc, e2);
-        if (j0 + CH >= end) break;
-        process_chunk<K, V, BF16, LOSS_ONLY>(A, j0 + CH, end, last, lg, bufB, bufA, x, xp, acc, e2);
+    const YTable Yt = make_ytable<BUF>(A, K * (BF16 ? 2 : 4));
+#if TSID_PINGPONG
+    for (int64_t j0 = beg; j0 < end; j0 += 2 * SB) {
+        process_block<K, V, BF16, LOSS_ONLY, BUF>(A, Yt, j0, end, last, lg, bufA, bufB, x, xp, acc, e2);
+        if (j0 + SB >= end) break;
+        process_block<K, V, BF16, LOSS_ONLY, BUF>(A, Yt, j0 + SB, end, last, lg, bufB, bufA, x, xp, acc,
+                                                  e2);
     }
+#else
+    // One block body per iteration; the block's last stream loads land in
+    // bufB and are copied over only after the block's arithmetic, where the
+    // next block needs them anyway.
+    for (int64_t j0 = beg; j0 < end; j0 += SB) {
+        process_block<K, V, BF16, LOSS_ONLY, BUF>(A, Yt, j0, end, last, lg, bufA, bufB, x, xp, acc, e2);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) bufA[c] = bufB[c];
+    }
+#endif
 
     if (A.e2 && lg == 0) A.e2[item] = e2;
     if constexpr (LOSS_ONLY) {
@@ -415,8 +523,15 @@ void item_pass_kv(bool loss_only, const PassArgs &a, hipStream_t s) {
     constexpr int NG = 64 / (K / V);
     const int grid = ceil_div(a.n_items, (int64_t)kWaves * NG);
     if (grid <= 0) return;
-    if (loss_only) k_item_pass<K, V, BF16, true><<<grid, kThreads, 0, s>>>(a);
-    else k_item_pass<K, V, BF16, false><<<grid, kThreads, 0, s>>>(a);
+    // buffer-resource gathers need the table (and every offset) below 2^31 bytes
+    const bool buf = a.y_rows * (int64_t)K * (BF16 ? 2 : 4) < (int64_t(1) << 31);
+    if (loss_only) {
+        if (buf) k_item_pass<K, V, BF16, true, true><<<grid, kThreads, 0, s>>>(a);
+        else k_item_pass<K, V, BF16, true, false><<<grid, kThreads, 0, s>>>(a);
+    } else {
+        if (buf) k_item_pass<K, V, BF16, false, true><<<grid, kThreads, 0, s>>>(a);
+        else k_item_pass<K, V, BF16, false, false><<<grid, kThreads, 0, s>>>(a);
+    }
     TSID_HIP(hipGetLastError());
 }
 

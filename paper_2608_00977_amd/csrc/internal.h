@@ -98,6 +98,7 @@ struct PassArgs {
     int32_t E;               // entries per item
     const float *X;          // owner factors, fp32 master (rows x K)
     const void *Y;           // gathered factors: fp32, or bf16 bits in bf16 mode
+    int64_t y_rows;          // rows of Y (bounds of the gathers)
     float *Xn;               // updated owner factors (null in loss-only mode)
     uint16_t *Xn_b;          // bf16 copy of Xn (bf16 mode) or null
     float *carry;            // partial gradient sums of split buckets (n_items x K)
