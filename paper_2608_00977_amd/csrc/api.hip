@@ -74,11 +74,16 @@ struct Arena {
     }
 };
 
+// Work plan of one pass for one precision (the lane grouping, hence the
+// groups per wave, depends on it).
 struct Plan {
-    uint32_t *item_off = nullptr;  // rows + 1
-    int32_t *items = nullptr;
+    bool ready = false;
+    uint32_t *item_off = nullptr;  // first item of each bucket
+    uint32_t *item_end = nullptr;  // one past its last item
+    int32_t *items = nullptr;      // bucket of each item, -1 for pads
     int32_t n_items = 0;
     int32_t E = 64;
+    bool spans = true;             // some bucket's items span two waves (fixup needed)
 };
 
 struct Template {
@@ -87,7 +92,9 @@ struct Template {
     int32_t *row_map = nullptr, *col_map = nullptr;
     int2 *stream_r = nullptr, *stream_c = nullptr;
     int64_t *row_ptr = nullptr, *col_ptr = nullptr;
-    Plan pr, pc;
+    std::vector<int64_t> hptr[2];  // host copies of row_ptr / col_ptr
+    int32_t E = 64;
+    Plan plan[2][2];               // [side][precision]
 };
 
 struct FitBufs {
@@ -97,6 +104,7 @@ struct FitBufs {
     float *carry_r = nullptr, *carry_c = nullptr, *e2 = nullptr, *normP = nullptr, *normQ = nullptr;
     double *partial = nullptr, *loss = nullptr;
     int32_t loss_cap = 0;
+    int64_t item_cap = 0;
 };
 
 struct ExtSlot {
@@ -209,10 +217,12 @@ void free_template(tsid_ctx *c, Template *&t) {
     A.release(t->stream_c);
     A.release(t->row_ptr);
     A.release(t->col_ptr);
-    A.release(t->pr.item_off);
-    A.release(t->pr.items);
-    A.release(t->pc.item_off);
-    A.release(t->pc.items);
+    for (auto &side : t->plan)
+        for (Plan &pl : side) {
+            A.release(pl.item_off);
+            A.release(pl.item_end);
+            A.release(pl.items);
+        }
     delete t;
     t = nullptr;
 }
@@ -235,6 +245,7 @@ void free_fit(tsid_ctx *c) {
     A.release(f.loss);
     f.prec = -1;
     f.loss_cap = 0;
+    f.item_cap = 0;
 }
 
 void free_ext_buffers(tsid_ctx *c) {
@@ -323,7 +334,7 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
     int32_t *dI = nullptr, *dJ = nullptr, *su[2] = {nullptr, nullptr}, *si[2] = {nullptr, nullptr};
     float *sr[2] = {nullptr, nullptr};
     uint32_t *bcnt = nullptr, *boffs = nullptr, *piece = nullptr, *scan_tmp = nullptr;
-    uint32_t *sort_tmp = nullptr, *nparts = nullptr, *vals = nullptr, *vals_alt = nullptr;
+    uint32_t *sort_tmp = nullptr, *vals = nullptr, *vals_alt = nullptr;
     uint64_t *keys = nullptr, *keys_alt = nullptr;
     uint32_t *piece_host = nullptr;
     hipEvent_t ev_h2d[2] = {nullptr, nullptr}, ev_free[2] = {nullptr, nullptr};
@@ -344,7 +355,6 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
         A.release(piece);
         A.release(scan_tmp);
         A.release(sort_tmp);
-        A.release(nparts);
         A.release(keys);
         A.release(keys_alt);
         A.release(vals);
@@ -459,26 +469,16 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
         keys_to_stream(tk, tv, total, bits_a, t->stream_c, c->err_dev, cs);
         ptr_from_keys(tk, total, n_t, bits_a, t->col_ptr, cs);
 
-        // work plans of both passes
-        nparts = A.alloc<uint32_t>(std::max(m_t, n_t));
-        const int32_t E = choose_E(total);
-        for (int side = 0; side < 2; ++side) {
-            Plan &pl = side ? t->pc : t->pr;
-            const int32_t rows = side ? n_t : m_t;
-            pl.E = E;
-            const int64_t bound = (int64_t)rows + total / E + 1;
-            pl.item_off = A.alloc<uint32_t>((int64_t)rows + 1);
-            pl.items = A.alloc<int32_t>(bound);
-            plan_items(side ? t->col_ptr : t->row_ptr, rows, E, pl.item_off, pl.items, nparts,
-                       scan_tmp, cs);
-        }
-        uint32_t counts[2] = {0, 0};
-        TSID_HIP(hipMemcpyAsync(&counts[0], t->pr.item_off + m_t, 4, hipMemcpyDeviceToHost, cs));
-        TSID_HIP(hipMemcpyAsync(&counts[1], t->pc.item_off + n_t, 4, hipMemcpyDeviceToHost, cs));
+        // host copies of the bucket pointers, for the work plans built at fit time
+        t->E = choose_E(total);
+        t->hptr[0].resize((size_t)m_t + 1);
+        t->hptr[1].resize((size_t)n_t + 1);
+        TSID_HIP(hipMemcpyAsync(t->hptr[0].data(), t->row_ptr, ((size_t)m_t + 1) * 8,
+                                hipMemcpyDeviceToHost, cs));
+        TSID_HIP(hipMemcpyAsync(t->hptr[1].data(), t->col_ptr, ((size_t)n_t + 1) * 8,
+                                hipMemcpyDeviceToHost, cs));
         TSID_HIP(hipMemcpyAsync(c->err_host, c->err_dev, ERR_SLOTS * 4, hipMemcpyDeviceToHost, cs));
         TSID_HIP(hipStreamSynchronize(cs));
-        t->pr.n_items = (int32_t)counts[0];
-        t->pc.n_items = (int32_t)counts[1];
         raise_device_errors(c->err_host, "build");
     } catch (...) {
         cleanup();
@@ -491,22 +491,95 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
     c->tpl = t;
 }
 
+// Work plan of one pass: bucket x becomes p items of at most E cells, where p
+// is max(1, ceil(deg / E)) rounded up to a power of two while it fits a wave
+// (ng groups), else to a multiple of ng.  Buckets of p <= ng items start at a
+// multiple of p (idle pad items fill the gaps), so they never straddle two
+// waves and their partial sums are combined inside the pass; only buckets of
+// more than one wave leave partial sums for the fixup kernel.
+void ensure_plan(tsid_ctx *c, int side, int prec) {
+    Template &t = *c->tpl;
+    Plan &pl = t.plan[side][prec];
+    if (pl.ready) return;
+    const std::vector<int64_t> &ptr = t.hptr[side];
+    const int32_t rows = side ? t.n_t : t.m_t;
+    const int64_t ng = items_per_wave(t.k, prec), E = t.E;
+    std::vector<uint32_t> off((size_t)rows + 1), endv((size_t)rows + 1);
+    std::vector<int32_t> items;
+    int64_t cur = 0;
+    bool spans = false;
+    for (int32_t x = 0; x < rows; ++x) {
+        const int64_t deg = ptr[x + 1] - ptr[x];
+        int64_t p = deg <= E ? 1 : (deg + E - 1) / E;
+        if (p > 1 && p <= ng) {
+            int64_t q = 1;
+            while (q < p) q <<= 1;
+            p = q;
+        } else if (p > ng) {
+            p = (p + ng - 1) / ng * ng;
+            spans = true;
+        }
+        const int64_t align = p < ng ? p : ng;
+        const int64_t start = (cur + align - 1) / align * align;
+        items.resize((size_t)(start + p), -1);
+        for (int64_t j = start; j < start + p; ++j) items[(size_t)j] = x;
+        off[(size_t)x] = (uint32_t)start;
+        endv[(size_t)x] = (uint32_t)(start + p);
+        cur = start + p;
+    }
+    if (cur >= INT32_MAX) fail(TSID_E_INVAL, "work plan too large");
+    Arena &A = c->arena;
+    uint32_t *d_off = nullptr, *d_end = nullptr;
+    int32_t *d_items = nullptr;
+    try {
+        d_off = A.alloc<uint32_t>((int64_t)rows + 1);
+        d_end = A.alloc<uint32_t>((int64_t)rows + 1);
+        d_items = A.alloc<int32_t>(cur);
+        hipStream_t cs = c->comp;
+        TSID_HIP(hipMemcpyAsync(d_off, off.data(), ((size_t)rows + 1) * 4, hipMemcpyHostToDevice, cs));
+        TSID_HIP(hipMemcpyAsync(d_end, endv.data(), ((size_t)rows + 1) * 4, hipMemcpyHostToDevice, cs));
+        if (cur) TSID_HIP(hipMemcpyAsync(d_items, items.data(), (size_t)cur * 4, hipMemcpyHostToDevice, cs));
+        TSID_HIP(hipStreamSynchronize(cs));  // the host vectors go out of scope
+    } catch (...) {
+        A.release(d_off);
+        A.release(d_end);
+        A.release(d_items);
+        throw;
+    }
+    pl.item_off = d_off;
+    pl.item_end = d_end;
+    pl.items = d_items;
+    pl.n_items = (int32_t)cur;
+    pl.E = (int32_t)E;
+    pl.spans = spans;
+    pl.ready = true;
+}
+
 void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs) {
     Template &t = *c->tpl;
     FitBufs &f = c->fb;
     Arena &A = c->arena;
     const int64_t lp = (int64_t)t.m_t * t.k, lq = (int64_t)t.n_t * t.k;
+    ensure_plan(c, 0, prec);
+    ensure_plan(c, 1, prec);
     if (!f.P[0]) {
         for (int b = 0; b < 2; ++b) {
             f.P[b] = A.alloc<float>(lp);
             f.Q[b] = A.alloc<float>(lq);
         }
-        f.carry_r = A.alloc<float>((int64_t)t.pr.n_items * t.k);
-        f.carry_c = A.alloc<float>((int64_t)t.pc.n_items * t.k);
-        f.e2 = A.alloc<float>(std::max(t.pr.n_items, t.pc.n_items));
         f.normP = A.alloc<float>(t.m_t);
         f.normQ = A.alloc<float>(t.n_t);
         f.partial = A.alloc<double>((int64_t)reduce_scratch_elems());
+    }
+    const int64_t need = std::max(t.plan[0][prec].n_items, t.plan[1][prec].n_items);
+    if (need > f.item_cap) {  // partial sums and per-item e^2, sized for this precision's plans
+        A.release(f.carry_r);
+        A.release(f.carry_c);
+        A.release(f.e2);
+        f.carry_r = A.alloc<float>(need * t.k);
+        f.carry_c = A.alloc<float>(need * t.k);
+        f.e2 = A.alloc<float>(need);
+        f.item_cap = need;
     }
     if (prec == TSID_BF16 && !f.Pb[0]) {
         for (int b = 0; b < 2; ++b) {
@@ -523,11 +596,12 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs) {
 
 PassArgs pass_args(const Template &t, int side, const tsid_fit_opts &o, int32_t *err) {
     PassArgs a{};
-    const Plan &pl = side ? t.pc : t.pr;
+    const Plan &pl = t.plan[side][o.prec];
     a.stream = side ? t.stream_c : t.stream_r;
     a.ptr = side ? t.col_ptr : t.row_ptr;
     a.items = pl.items;
     a.item_off = pl.item_off;
+    a.item_end = pl.item_end;
     a.n_items_dev = nullptr;
     a.n_items = pl.n_items;
     a.rows = side ? t.n_t : t.m_t;
@@ -577,7 +651,7 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
         mark(c, ep, 0);
         launch_item_pass(K, prec, false, ar, cs);
         mark(c, ep, 1);
-        launch_fixup(K, prec, ar, cs);
+        if (t.plan[0][prec].spans) launch_fixup(K, prec, ar, cs);
         mark(c, ep, 2);
         // Q pass (CSC): owner Q_t, gathered P_t (the old P: a simultaneous step)
         ac.X = f.Q[cur];
@@ -589,10 +663,10 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
         ac.norm = f.normQ;
         launch_item_pass(K, prec, false, ac, cs);
         mark(c, ep, 3);
-        launch_fixup(K, prec, ac, cs);
+        if (t.plan[1][prec].spans) launch_fixup(K, prec, ac, cs);
         mark(c, ep, 4);
-        launch_loss_reduce(f.e2, t.pr.n_items, f.normP, t.m_t, f.normQ, t.n_t, o->lambda, f.partial,
-                           f.loss + ep, c->err_dev, ep, cs);
+        launch_loss_reduce(f.e2, t.plan[0][prec].n_items, f.normP, t.m_t, f.normQ, t.n_t, o->lambda,
+                           f.partial, f.loss + ep, c->err_dev, ep, cs);
         mark(c, ep, 5);
     }
     const int fin = T & 1;
@@ -605,8 +679,8 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
         ar.norm = f.normP;
         launch_item_pass(K, prec, true, ar, cs);
         launch_row_norms(K, f.Q[fin], t.n_t, f.normQ, cs);
-        launch_loss_reduce(f.e2, t.pr.n_items, f.normP, t.m_t, f.normQ, t.n_t, o->lambda, f.partial,
-                           f.loss + T, c->err_dev, T, cs);
+        launch_loss_reduce(f.e2, t.plan[0][prec].n_items, f.normP, t.m_t, f.normQ, t.n_t, o->lambda,
+                           f.partial, f.loss + T, c->err_dev, T, cs);
     }
     std::vector<double> hist((size_t)T + 1);
     if (loss_hist) TSID_HIP(hipMemcpyAsync(hist.data(), f.loss, (size_t)(T + 1) * 8, hipMemcpyDeviceToHost, cs));
@@ -647,8 +721,8 @@ void loss(tsid_ctx *c, const float *P, const float *Q, float lambda, double *out
     a.skip_after_nonfinite = 0;
     launch_item_pass(t.k, TSID_FP32, true, a, cs);
     launch_row_norms(t.k, Q, t.n_t, f.normQ, cs);
-    launch_loss_reduce(f.e2, t.pr.n_items, f.normP, t.m_t, f.normQ, t.n_t, lambda, f.partial, f.loss,
-                       nullptr, -1, cs);
+    launch_loss_reduce(f.e2, t.plan[0][TSID_FP32].n_items, f.normP, t.m_t, f.normQ, t.n_t, lambda,
+                       f.partial, f.loss, nullptr, -1, cs);
     TSID_HIP(hipMemcpyAsync(out, f.loss, 8, hipMemcpyDeviceToHost, cs));
     TSID_HIP(hipStreamSynchronize(cs));
 }
@@ -759,6 +833,7 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
     a.ptr = x.ptr;
     a.items = x.items;
     a.item_off = x.item_off;
+    a.item_end = x.item_off + 1;
     a.n_items_dev = x.item_off + n_free;
     a.n_items = (int32_t)bound64;
     a.rows = n_free;

@@ -366,14 +366,24 @@ __global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass(const Pas
     const int64_t item = ((int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6)) * NG + grp;
     const int64_t n_items = A.n_items_dev ? (int64_t)*A.n_items_dev : (int64_t)A.n_items;
     if (item >= n_items) return;  // whole groups leave together
-    const int row = A.items[item];
-    const uint32_t i0 = A.item_off[row], i1 = A.item_off[row + 1];
-    const int64_t re = A.ptr[row + 1];
-    const int64_t beg = A.ptr[row] + (int64_t)(item - i0) * A.E;
-    const int64_t end = beg + A.E < re ? beg + A.E : re;
-
+    const int row = A.items[item];  // -1: a pad item that keeps buckets wave-aligned
+    uint32_t i0 = 0, i1 = 0;
+    int64_t re = 0, beg = 0, end = 0;
     float x[V];
-    load_f32<V>(A.X + (int64_t)row * K + lg * V, x);
+    if (row >= 0) {
+        // the bucket's cells split evenly over its items (at most E each)
+        i0 = A.item_off[row];
+        i1 = A.item_end[row];
+        const int64_t rb = A.ptr[row];
+        re = A.ptr[row + 1];
+        const int64_t deg = re - rb, parts = (int64_t)(i1 - i0), q = item - (int64_t)i0;
+        beg = rb + q * deg / parts;
+        end = rb + (q + 1) * deg / parts;
+        load_f32<V>(A.X + (int64_t)row * K + lg * V, x);
+    } else {
+#pragma unroll
+        for (int v = 0; v < V; ++v) x[v] = 0.f;
+    }
     uint32_t xp[V / 2] = {};  // bf16 pairs of the owner row (bf16 mode)
     if constexpr (BF16) {
 #pragma unroll
@@ -422,7 +432,7 @@ __global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass(const Pas
 
     if (A.e2 && lg == 0) A.e2[item] = e2;
     if constexpr (LOSS_ONLY) {
-        if (A.norm && item == (int64_t)i0) {
+        if (A.norm && row >= 0 && item == (int64_t)i0) {
             float nrm = 0.f;
 #pragma unroll
             for (int v = 0; v < V; ++v) nrm += x[v] * x[v];
@@ -430,10 +440,37 @@ __global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass(const Pas
             if (lg == 0) A.norm[row] = nrm;
         }
     } else {
-        if (i1 - i0 == 1) {
-            finalize_row<G, V, BF16>(A, row, lg, x, acc, re - A.ptr[row]);
-        } else {
-            store_f32<V>(A.carry + item * K + lg * V, acc);
+        // Groups of this wave that hold consecutive items of the same bucket add
+        // their partial sums through LDS, in group order, into the segment's
+        // first group.  A bucket whose items all sit in this wave is updated
+        // here; otherwise the segment leaves one partial sum, at the index of its
+        // first item, for the fixup kernel.
+        __shared__ float red[kWaves][NG][K];
+        __shared__ int seg_row[kWaves][NG];
+        const int wv = threadIdx.x >> 6;
+        store_f32<V>(&red[wv][grp][lg * V], acc);
+        if (lg == 0) seg_row[wv][grp] = row;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // items are in bucket order (pads hold -1), so the group before this one
+        // has published its bucket
+        const bool head = row >= 0 && ((grp == 0) || (seg_row[wv][grp - 1] != row));
+        if (head) {
+            int g_end = grp + 1;
+            while (g_end < NG && item + (g_end - grp) < n_items && seg_row[wv][g_end] == row) ++g_end;
+            for (int g = grp + 1; g < g_end; ++g) {
+                float part[V];
+                load_f32<V>(&red[wv][g][lg * V], part);
+#pragma unroll
+                for (int v = 0; v < V; ++v) acc[v] += part[v];
+            }
+            const int64_t seg_last = item + (g_end - grp) - 1;
+            if (item == (int64_t)i0 && seg_last == (int64_t)i1 - 1) {
+                finalize_row<G, V, BF16>(A, row, lg, x, acc, re - A.ptr[row]);
+            } else {
+                store_f32<V>(A.carry + item * K + lg * V, acc);
+            }
         }
     }
 }
@@ -448,12 +485,15 @@ __global__ __launch_bounds__(kThreads) void k_fixup(const PassArgs A) {
     const int grp = lane / G, lg = lane % G;
     const int64_t row = ((int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6)) * NG + grp;
     if (row >= A.rows) return;
-    const uint32_t i0 = A.item_off[row], i1 = A.item_off[row + 1];
-    if (i1 - i0 <= 1) return;
+    const uint32_t i0 = A.item_off[row], i1 = A.item_end[row];
+    // the pass already updated buckets whose items all sat in one wave
+    if (i1 - i0 <= 1 || i0 / NG == (i1 - 1) / NG) return;
     float acc[V];
 #pragma unroll
     for (int v = 0; v < V; ++v) acc[v] = 0.f;
-    for (uint32_t it = i0; it < i1; ++it) {
+    // one partial sum per wave segment, stored at the segment's first item:
+    // the bucket's first item and every later item that starts a wave
+    for (uint32_t it = i0; it < i1; it = (it / NG + 1) * NG) {
         float part[V];
         load_f32<V>(A.carry + (int64_t)it * K + lg * V, part);
 #pragma unroll
@@ -588,6 +628,17 @@ void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStr
 
 void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s) {
     TSID_DISPATCH_K(K, fixup_kv, a, s)
+}
+
+namespace {
+template <int K, int V, bool BF16>
+void groups_per_wave_kv(int &out) { out = 64 / (K / V); }
+}  // namespace
+
+int items_per_wave(int K, int prec) {
+    int out = 0;
+    TSID_DISPATCH_K(K, groups_per_wave_kv, out)
+    return out;
 }
 
 void launch_row_norms(int K, const float *X, int32_t rows, float *norm, hipStream_t s) {

@@ -90,8 +90,9 @@ void plan_items(const int64_t *ptr, int32_t rows, int32_t E, uint32_t *item_off,
 struct PassArgs {
     const int2 *stream;      // bucketed entries {other id, value bits}
     const int64_t *ptr;      // bucket pointers (rows + 1)
-    const int32_t *items;    // bucket of each item
-    const uint32_t *item_off;  // first item of each bucket (rows + 1)
+    const int32_t *items;    // bucket of each item (-1: an idle pad item)
+    const uint32_t *item_off;  // first item of each bucket
+    const uint32_t *item_end;  // one past the last item of each bucket
     const uint32_t *n_items_dev;  // device item count (or null: use n_items)
     int32_t n_items;         // item count, or an upper bound when n_items_dev is set
     int32_t rows;            // buckets
@@ -114,6 +115,9 @@ struct PassArgs {
 // prec: 0 fp32, 1 bf16.  loss_only: residuals, e2 and norms only.
 void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStream_t s);
 void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s);
+// Items one wave holds for rank K and precision prec (the item pass's groups
+// per wave): buckets whose items stay inside one such run need no fixup.
+int items_per_wave(int K, int prec);
 void launch_row_norms(int K, const float *X, int32_t rows, float *norm, hipStream_t s);
 void launch_to_bf16(const float *X, int64_t n, uint16_t *Xb, hipStream_t s);
 // out[slot] = S_e + lam (S_p + S_q) with S_* fixed-order fp64 sums; partial
