@@ -182,12 +182,14 @@ tsid_status tsid_extend_chunk(tsid_ctx *ctx, int side, const int32_t *fixed_id,
 tsid_status tsid_sync(tsid_ctx *ctx);
 
 /* Kernel timing of the template fit (a tracing aid).  While enabled, every
- * epoch of tsid_fit_template records HIP events on the compute stream around
- * its kernels, and the durations accumulate here until the next
+ * kernel of each epoch of tsid_fit_template is launched with a start and an
+ * end HIP event attached to its dispatch on the compute stream (no separate
+ * event packets), and the durations accumulate here until the next
  * tsid_set_timing call resets them.  pass_ms[0] / pass_launches[0]: the P
- * pass (row buckets); [1]: the Q pass (column buckets); fixup: the split-bucket
- * fixups; reduce: the loss reductions; epoch_ms: first event to last event of
- * each epoch, summed.  Timing adds a few microseconds per kernel. */
+ * pass (row buckets); [1]: the Q pass (column buckets); fixup: the fixups of
+ * buckets longer than one wave; reduce: the batched loss reductions (one per
+ * 16 epochs); epoch_ms: start of each epoch's first kernel to the end of its
+ * last, summed. */
 typedef struct {
     double pass_ms[2];
     int64_t pass_launches[2];

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstring>
 #include <unordered_map>
+#include <utility>
 #include <vector>
 
 #include "internal.h"
@@ -97,6 +98,9 @@ struct Template {
     Plan plan[2][2];               // [side][precision]
 };
 
+// Epochs whose loss terms are kept before one batched reduction.
+constexpr int kLossRing = 16;
+
 struct FitBufs {
     int32_t prec = -1;
     float *P[2] = {nullptr, nullptr}, *Q[2] = {nullptr, nullptr};
@@ -146,7 +150,8 @@ struct tsid_ctx {
     int32_t epochs_done = 0;         // of the last fit
     bool timing = false;
     tsid_timing tm{};
-    std::vector<hipEvent_t> events;  // timing markers, 6 per epoch
+    std::vector<hipEvent_t> events;  // kernel timestamps, kEvents per epoch
+    std::vector<uint8_t> launched;   // which kernel kinds each timed epoch ran
     FitBufs fb;
     ExtState ext;
 };
@@ -155,38 +160,55 @@ namespace {
 
 void set_device(const tsid_ctx *c) { TSID_HIP(hipSetDevice(c->device)); }
 
-constexpr int kMarks = 6;  // per epoch: P pass | P fixup | Q pass | Q fixup | reduce
+// Timed kernels of one epoch; each takes a start and an end event attached to
+// its dispatch (the loss reduction: start of its first kernel, end of its last).
+enum TimedKernel { TK_PPASS = 0, TK_PFIX = 1, TK_QPASS = 2, TK_QFIX = 3, TK_REDUCE = 4, kTimed = 5 };
+constexpr int kEvents = 2 * kTimed;
 
-void ensure_events(tsid_ctx *c, size_t count) {
-    while (c->events.size() < count) {
+void ensure_events(tsid_ctx *c, size_t epochs) {
+    while (c->events.size() < epochs * kEvents) {
         hipEvent_t e;
         TSID_HIP(hipEventCreate(&e));
         c->events.push_back(e);
     }
+    c->launched.assign(epochs, 0);
 }
 
-void mark(tsid_ctx *c, int ep, int slot) {
-    if (c->timing) TSID_HIP(hipEventRecord(c->events[(size_t)ep * kMarks + slot], c->comp));
+// Events for kernel kind k of epoch ep (a null pair when timing is off).
+std::pair<hipEvent_t, hipEvent_t> timed(tsid_ctx *c, int ep, int k) {
+    if (!c->timing) return {nullptr, nullptr};
+    c->launched[(size_t)ep] |= (uint8_t)(1u << k);
+    const size_t b = (size_t)ep * kEvents + 2 * k;
+    return {c->events[b], c->events[b + 1]};
 }
 
 void collect_timing(tsid_ctx *c, int epochs) {
-    auto dt = [&](int ep, int a, int b) {
+    auto ev = [&](int ep, int k, int end) { return c->events[(size_t)ep * kEvents + 2 * k + end]; };
+    auto dt = [&](hipEvent_t a, hipEvent_t b) {
         float ms = 0.f;
-        TSID_HIP(hipEventElapsedTime(&ms, c->events[(size_t)ep * kMarks + a],
-                                     c->events[(size_t)ep * kMarks + b]));
+        TSID_HIP(hipEventElapsedTime(&ms, a, b));
         return (double)ms;
     };
     tsid_timing &t = c->tm;
     for (int ep = 0; ep < epochs; ++ep) {
-        t.pass_ms[0] += dt(ep, 0, 1);
-        t.fixup_ms += dt(ep, 1, 2) + dt(ep, 3, 4);
-        t.pass_ms[1] += dt(ep, 2, 3);
-        t.reduce_ms += dt(ep, 4, 5);
-        t.epoch_ms += dt(ep, 0, 5);
-        t.pass_launches[0] += 1;
-        t.pass_launches[1] += 1;
-        t.fixup_launches += 2;
-        t.reduce_launches += 1;
+        const uint8_t l = c->launched[(size_t)ep];
+        int last = TK_PPASS;
+        for (int k = 0; k < kTimed; ++k) {
+            if (!(l & (1u << k))) continue;
+            const double ms = dt(ev(ep, k, 0), ev(ep, k, 1));
+            last = k;
+            if (k == TK_PPASS || k == TK_QPASS) {
+                t.pass_ms[k / 2] += ms;
+                t.pass_launches[k / 2] += 1;
+            } else if (k == TK_REDUCE) {
+                t.reduce_ms += ms;
+                t.reduce_launches += 1;
+            } else {
+                t.fixup_ms += ms;
+                t.fixup_launches += 1;
+            }
+        }
+        t.epoch_ms += dt(ev(ep, TK_PPASS, 0), ev(ep, last, 1));
         t.epochs += 1;
     }
 }
@@ -503,7 +525,15 @@ void ensure_plan(tsid_ctx *c, int side, int prec) {
     if (pl.ready) return;
     const std::vector<int64_t> &ptr = t.hptr[side];
     const int32_t rows = side ? t.n_t : t.m_t;
-    const int64_t ng = items_per_wave(t.k, prec), E = t.E;
+    const int64_t ng = items_per_wave(t.k, prec);
+    int64_t E = t.E, maxdeg = 0;
+    for (int32_t x = 0; x < rows; ++x) maxdeg = std::max(maxdeg, ptr[x + 1] - ptr[x]);
+    // When items up to twice the default length keep every bucket within one
+    // wave, take them: no bucket then needs the fixup kernel.
+    if (maxdeg > E * ng) {
+        const int64_t e1 = ((maxdeg + ng - 1) / ng + 15) / 16 * 16;
+        if (e1 <= 2 * E) E = e1;
+    }
     std::vector<uint32_t> off((size_t)rows + 1), endv((size_t)rows + 1);
     std::vector<int32_t> items;
     int64_t cur = 0;
@@ -567,18 +597,19 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs) {
             f.P[b] = A.alloc<float>(lp);
             f.Q[b] = A.alloc<float>(lq);
         }
-        f.normP = A.alloc<float>(t.m_t);
-        f.normQ = A.alloc<float>(t.n_t);
-        f.partial = A.alloc<double>((int64_t)reduce_scratch_elems());
+        f.normP = A.alloc<float>((int64_t)t.m_t * kLossRing);
+        f.normQ = A.alloc<float>((int64_t)t.n_t * kLossRing);
+        f.partial = A.alloc<double>((int64_t)reduce_scratch_elems(kLossRing));
     }
     const int64_t need = std::max(t.plan[0][prec].n_items, t.plan[1][prec].n_items);
     if (need > f.item_cap) {  // partial sums and per-item e^2, sized for this precision's plans
         A.release(f.carry_r);
         A.release(f.carry_c);
         A.release(f.e2);
+        f.item_cap = 0;
         f.carry_r = A.alloc<float>(need * t.k);
         f.carry_c = A.alloc<float>(need * t.k);
-        f.e2 = A.alloc<float>(need);
+        f.e2 = A.alloc<float>(need * kLossRing);
         f.item_cap = need;
     }
     if (prec == TSID_BF16 && !f.Pb[0]) {
@@ -636,9 +667,19 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     TSID_HIP(hipMemsetAsync(c->err_dev, 0, ERR_SLOTS * sizeof(int32_t), cs));
     PassArgs ar = pass_args(t, 0, *o, c->err_dev), ac = pass_args(t, 1, *o, c->err_dev);
     ar.skip_after_nonfinite = ac.skip_after_nonfinite = 1;
-    if (c->timing) ensure_events(c, (size_t)T * kMarks);
+    if (c->timing) ensure_events(c, (size_t)T);
+    // Loss terms of epoch ep go to ring slot ep % kLossRing; a full ring (and
+    // the end of the fit) is reduced in one batch into f.loss.
+    const bool want_loss = loss_hist != nullptr;
+    const int64_t ne = t.plan[0][prec].n_items;
+    int pend = 0;  // first epoch whose loss is not reduced yet
+    auto flush = [&](int upto, std::pair<hipEvent_t, hipEvent_t> ev) {
+        launch_loss_reduce(f.e2, f.item_cap, ne, f.normP, t.m_t, f.normQ, t.n_t, o->lambda, upto - pend,
+                           f.partial, f.loss + pend, c->err_dev, pend, cs, ev.first, ev.second);
+        pend = upto;
+    };
     for (int ep = 0; ep < T; ++ep) {
-        const int cur = ep & 1, nxt = cur ^ 1;
+        const int cur = ep & 1, nxt = cur ^ 1, slot = ep % kLossRing;
         ar.epoch = ac.epoch = ep;
         // P pass (CSR): owner P_t, gathered Q_t
         ar.X = f.P[cur];
@@ -646,13 +687,14 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
         ar.Xn = f.P[nxt];
         ar.Xn_b = prec ? f.Pb[nxt] : nullptr;
         ar.carry = f.carry_r;
-        ar.e2 = f.e2;
-        ar.norm = f.normP;
-        mark(c, ep, 0);
-        launch_item_pass(K, prec, false, ar, cs);
-        mark(c, ep, 1);
-        if (t.plan[0][prec].spans) launch_fixup(K, prec, ar, cs);
-        mark(c, ep, 2);
+        ar.e2 = want_loss ? f.e2 + slot * f.item_cap : nullptr;
+        ar.norm = want_loss ? f.normP + (int64_t)slot * t.m_t : nullptr;
+        auto ev = timed(c, ep, TK_PPASS);
+        launch_item_pass(K, prec, false, ar, cs, ev.first, ev.second);
+        if (t.plan[0][prec].spans) {
+            ev = timed(c, ep, TK_PFIX);
+            launch_fixup(K, prec, ar, cs, ev.first, ev.second);
+        }
         // Q pass (CSC): owner Q_t, gathered P_t (the old P: a simultaneous step)
         ac.X = f.Q[cur];
         ac.Y = prec ? (const void *)f.Pb[cur] : (const void *)f.P[cur];
@@ -660,27 +702,27 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
         ac.Xn_b = prec ? f.Qb[nxt] : nullptr;
         ac.carry = f.carry_c;
         ac.e2 = nullptr;
-        ac.norm = f.normQ;
-        launch_item_pass(K, prec, false, ac, cs);
-        mark(c, ep, 3);
-        if (t.plan[1][prec].spans) launch_fixup(K, prec, ac, cs);
-        mark(c, ep, 4);
-        launch_loss_reduce(f.e2, t.plan[0][prec].n_items, f.normP, t.m_t, f.normQ, t.n_t, o->lambda,
-                           f.partial, f.loss + ep, c->err_dev, ep, cs);
-        mark(c, ep, 5);
+        ac.norm = want_loss ? f.normQ + (int64_t)slot * t.n_t : nullptr;
+        ev = timed(c, ep, TK_QPASS);
+        launch_item_pass(K, prec, false, ac, cs, ev.first, ev.second);
+        if (t.plan[1][prec].spans) {
+            ev = timed(c, ep, TK_QFIX);
+            launch_fixup(K, prec, ac, cs, ev.first, ev.second);
+        }
+        if (want_loss && slot == kLossRing - 1) flush(ep + 1, timed(c, ep, TK_REDUCE));
     }
     const int fin = T & 1;
-    if (loss_hist) {  // L(P_T, Q_T)
+    if (want_loss) {  // L(P_T, Q_T), then the epochs not reduced yet
+        const int slot = T % kLossRing;
         ar.epoch = T;
         ar.X = f.P[fin];
         ar.Y = prec ? (const void *)f.Qb[fin] : (const void *)f.Q[fin];
         ar.Xn = nullptr;
-        ar.e2 = f.e2;
-        ar.norm = f.normP;
+        ar.e2 = f.e2 + slot * f.item_cap;
+        ar.norm = f.normP + (int64_t)slot * t.m_t;
         launch_item_pass(K, prec, true, ar, cs);
-        launch_row_norms(K, f.Q[fin], t.n_t, f.normQ, cs);
-        launch_loss_reduce(f.e2, t.plan[0][prec].n_items, f.normP, t.m_t, f.normQ, t.n_t, o->lambda,
-                           f.partial, f.loss + T, c->err_dev, T, cs);
+        launch_row_norms(K, f.Q[fin], t.n_t, f.normQ + (int64_t)slot * t.n_t, cs);
+        flush(T + 1, {nullptr, nullptr});
     }
     std::vector<double> hist((size_t)T + 1);
     if (loss_hist) TSID_HIP(hipMemcpyAsync(hist.data(), f.loss, (size_t)(T + 1) * 8, hipMemcpyDeviceToHost, cs));
@@ -721,8 +763,8 @@ void loss(tsid_ctx *c, const float *P, const float *Q, float lambda, double *out
     a.skip_after_nonfinite = 0;
     launch_item_pass(t.k, TSID_FP32, true, a, cs);
     launch_row_norms(t.k, Q, t.n_t, f.normQ, cs);
-    launch_loss_reduce(f.e2, t.plan[0][TSID_FP32].n_items, f.normP, t.m_t, f.normQ, t.n_t, lambda,
-                       f.partial, f.loss, nullptr, -1, cs);
+    launch_loss_reduce(f.e2, f.item_cap, t.plan[0][TSID_FP32].n_items, f.normP, t.m_t, f.normQ, t.n_t,
+                       lambda, 1, f.partial, f.loss, nullptr, -1, cs);
     TSID_HIP(hipMemcpyAsync(out, f.loss, 8, hipMemcpyDeviceToHost, cs));
     TSID_HIP(hipStreamSynchronize(cs));
 }

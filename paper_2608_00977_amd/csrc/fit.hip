@@ -21,6 +21,8 @@
 //  * bf16 mode: the gathered side is a bf16 copy (2 bytes per coordinate, dots
 //    by v_dot2_f32_bf16 with fp32 accumulation); the owner row's fp32 master
 //    takes the update and a round-to-nearest-even bf16 copy is written beside it.
+#include <hip/hip_ext.h>
+
 #include "internal.h"
 
 namespace tsid {
@@ -524,12 +526,14 @@ __global__ void k_to_bf16(const float *X, int64_t n, uint16_t *Xb) {
 
 constexpr int kRedBlocks = 64;
 
-__global__ __launch_bounds__(256) void k_reduce_partial(const float *a, int64_t na, const float *b,
-                                                        int64_t nb, const float *c, int64_t nc,
-                                                        double *partial) {
+__global__ __launch_bounds__(256) void k_reduce_partial(const float *a, int64_t sa, int64_t na,
+                                                        const float *b, int64_t nb, const float *c,
+                                                        int64_t nc, double *partial) {
     __shared__ double lds[256];
+    const int slot = blockIdx.y;
     const int which = blockIdx.x / kRedBlocks, blk = blockIdx.x % kRedBlocks;
-    const float *src = which == 0 ? a : (which == 1 ? b : c);
+    const float *src = which == 0 ? (a ? a + slot * sa : nullptr)
+                                  : (which == 1 ? (b ? b + slot * nb : nullptr) : (c ? c + slot * nc : nullptr));
     const int64_t n = which == 0 ? na : (which == 1 ? nb : nc);
     const int64_t chunk = (n + kRedBlocks - 1) / kRedBlocks;
     const int64_t lo = blk * chunk, hi = lo + chunk < n ? lo + chunk : n;
@@ -542,45 +546,50 @@ __global__ __launch_bounds__(256) void k_reduce_partial(const float *a, int64_t 
         if (threadIdx.x < off) lds[threadIdx.x] += lds[threadIdx.x + off];
         __syncthreads();
     }
-    if (threadIdx.x == 0) partial[blockIdx.x] = lds[0];
+    if (threadIdx.x == 0) partial[(int64_t)slot * 3 * kRedBlocks + blockIdx.x] = lds[0];
 }
 
-__global__ void k_reduce_final(const double *partial, double lam, double *out, const int32_t *err,
-                               int32_t epoch) {
-    if (threadIdx.x != 0) return;
-    if (err && epoch >= 0) {
-        const int32_t f = err[ERR_NONFINITE];
-        if (f != 0 && f - 1 < epoch) return;
+__global__ void k_reduce_final(const double *partial, int n_slots, double lam, double *out,
+                               const int32_t *err, int32_t epoch0) {
+    for (int slot = threadIdx.x; slot < n_slots; slot += blockDim.x) {
+        if (err && epoch0 >= 0) {
+            const int32_t f = err[ERR_NONFINITE];
+            if (f != 0 && f - 1 < epoch0 + slot) continue;
+        }
+        const double *p = partial + (int64_t)slot * 3 * kRedBlocks;
+        double s[3] = {0.0, 0.0, 0.0};
+        for (int w = 0; w < 3; ++w)
+            for (int b = 0; b < kRedBlocks; ++b) s[w] += p[w * kRedBlocks + b];
+        out[slot] = s[0] + lam * (s[1] + s[2]);
     }
-    double s[3] = {0.0, 0.0, 0.0};
-    for (int w = 0; w < 3; ++w)
-        for (int b = 0; b < kRedBlocks; ++b) s[w] += partial[w * kRedBlocks + b];
-    *out = s[0] + lam * (s[1] + s[2]);
 }
 
 template <int K, int V, bool BF16>
-void item_pass_kv(bool loss_only, const PassArgs &a, hipStream_t s) {
+void item_pass_kv(bool loss_only, const PassArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     constexpr int NG = 64 / (K / V);
     const int grid = ceil_div(a.n_items, (int64_t)kWaves * NG);
     if (grid <= 0) return;
     // buffer-resource gathers need the table (and every offset) below 2^31 bytes
     const bool buf = a.y_rows * (int64_t)K * (BF16 ? 2 : 4) < (int64_t(1) << 31);
+    auto go = [&](auto kernel) {
+        hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(kThreads), 0, s, ev0, ev1, 0, a);
+    };
     if (loss_only) {
-        if (buf) k_item_pass<K, V, BF16, true, true><<<grid, kThreads, 0, s>>>(a);
-        else k_item_pass<K, V, BF16, true, false><<<grid, kThreads, 0, s>>>(a);
+        if (buf) go(k_item_pass<K, V, BF16, true, true>);
+        else go(k_item_pass<K, V, BF16, true, false>);
     } else {
-        if (buf) k_item_pass<K, V, BF16, false, true><<<grid, kThreads, 0, s>>>(a);
-        else k_item_pass<K, V, BF16, false, false><<<grid, kThreads, 0, s>>>(a);
+        if (buf) go(k_item_pass<K, V, BF16, false, true>);
+        else go(k_item_pass<K, V, BF16, false, false>);
     }
     TSID_HIP(hipGetLastError());
 }
 
 template <int K, int V, bool BF16>
-void fixup_kv(const PassArgs &a, hipStream_t s) {
+void fixup_kv(const PassArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     constexpr int NG = 64 / (K / V);
     const int grid = ceil_div(a.rows, (int64_t)kWaves * NG);
     if (grid <= 0) return;
-    k_fixup<K, V, BF16><<<grid, kThreads, 0, s>>>(a);
+    hipExtLaunchKernelGGL(k_fixup<K, V, BF16>, dim3(grid), dim3(kThreads), 0, s, ev0, ev1, 0, a);
     TSID_HIP(hipGetLastError());
 }
 
@@ -622,12 +631,13 @@ void fixup_kv(const PassArgs &a, hipStream_t s) {
         default: fail(TSID_E_INVAL, "unsupported rank");                                         \
     }
 
-void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStream_t s) {
-    TSID_DISPATCH_K(K, item_pass_kv, loss_only, a, s)
+void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStream_t s,
+                      hipEvent_t ev0, hipEvent_t ev1) {
+    TSID_DISPATCH_K(K, item_pass_kv, loss_only, a, s, ev0, ev1)
 }
 
-void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s) {
-    TSID_DISPATCH_K(K, fixup_kv, a, s)
+void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+    TSID_DISPATCH_K(K, fixup_kv, a, s, ev0, ev1)
 }
 
 namespace {
@@ -662,14 +672,18 @@ void launch_to_bf16(const float *X, int64_t n, uint16_t *Xb, hipStream_t s) {
     TSID_HIP(hipGetLastError());
 }
 
-size_t reduce_scratch_elems() { return 3 * kRedBlocks; }
+size_t reduce_scratch_elems(int n_slots) { return (size_t)3 * kRedBlocks * (n_slots > 0 ? n_slots : 1); }
 
-void launch_loss_reduce(const float *e2, int64_t ne, const float *np, int64_t nnp, const float *nq,
-                        int64_t nnq, double lam, double *partial, double *out, const int32_t *err,
-                        int32_t epoch, hipStream_t s) {
-    k_reduce_partial<<<3 * kRedBlocks, 256, 0, s>>>(e2, ne, np, nnp, nq, nnq, partial);
+void launch_loss_reduce(const float *e2, int64_t e2_stride, int64_t ne, const float *np, int64_t nnp,
+                        const float *nq, int64_t nnq, double lam, int n_slots, double *partial,
+                        double *out, const int32_t *err, int32_t epoch0, hipStream_t s,
+                        hipEvent_t ev0, hipEvent_t ev1) {
+    if (n_slots <= 0) return;
+    hipExtLaunchKernelGGL(k_reduce_partial, dim3(3 * kRedBlocks, n_slots), dim3(256), 0, s, ev0,
+                          nullptr, 0, e2, e2_stride, ne, np, nnp, nq, nnq, partial);
     TSID_HIP(hipGetLastError());
-    k_reduce_final<<<1, 64, 0, s>>>(partial, lam, out, err, epoch);
+    hipExtLaunchKernelGGL(k_reduce_final, dim3(1), dim3(64), 0, s, nullptr, ev1, 0,
+                          (const double *)partial, n_slots, lam, out, err, epoch0);
     TSID_HIP(hipGetLastError());
 }
 

@@ -113,18 +113,26 @@ struct PassArgs {
 };
 
 // prec: 0 fp32, 1 bf16.  loss_only: residuals, e2 and norms only.
-void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStream_t s);
-void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s);
+// ev0 / ev1 (may be null): HIP events that take the kernel's own start and end
+// timestamps (attached to its dispatch; no extra packets on the stream).
+void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStream_t s,
+                      hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s, hipEvent_t ev0 = nullptr,
+                  hipEvent_t ev1 = nullptr);
 // Items one wave holds for rank K and precision prec (the item pass's groups
 // per wave): buckets whose items stay inside one such run need no fixup.
 int items_per_wave(int K, int prec);
 void launch_row_norms(int K, const float *X, int32_t rows, float *norm, hipStream_t s);
 void launch_to_bf16(const float *X, int64_t n, uint16_t *Xb, hipStream_t s);
-// out[slot] = S_e + lam (S_p + S_q) with S_* fixed-order fp64 sums; partial
-// scratch: reduce_scratch_elems() doubles.
-size_t reduce_scratch_elems();
-void launch_loss_reduce(const float *e2, int64_t ne, const float *np, int64_t nnp, const float *nq,
-                        int64_t nnq, double lam, double *partial, double *out,
-                        const int32_t *err, int32_t epoch, hipStream_t s);
+// Loss of n_slots epochs at once: slot j holds e2 + j * e2_stride (ne per-item
+// squared residual sums), np + j * nnp and nq + j * nnq (row norms), and
+// out[j] = S_e + lam (S_p + S_q), each S a fixed-order fp64 sum.  With err,
+// a slot whose epoch (epoch0 + j) follows a non-finite update is left
+// unwritten.  partial: reduce_scratch_elems(n_slots) doubles.
+size_t reduce_scratch_elems(int n_slots);
+void launch_loss_reduce(const float *e2, int64_t e2_stride, int64_t ne, const float *np, int64_t nnp,
+                        const float *nq, int64_t nnq, double lam, int n_slots, double *partial,
+                        double *out, const int32_t *err, int32_t epoch0, hipStream_t s,
+                        hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 }  // namespace tsid
