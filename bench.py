@@ -16,7 +16,10 @@ Default workload: the Scientific configuration's template -- 200,000 x
 200,000 rank-32 ground truth, 10 % uniform observation, a 16,384 x 16,384
 uniform template (about 24 M training cells), k = 32, fp32, degree step.
 --config rating runs the Netflix-shaped template (65,536 x 8,192, k = 64,
-bf16 factors with fp32 accumulation and clipping); mid / tiny are small.
+bf16 factors with fp32 accumulation and clipping); --config billion the
+Billion-scale template (1,000,000 x 100,000 of a 10 M x 1 M Zipf matrix,
+about 4.2e8 training cells, k = 128, bf16 + clipping; its input takes a few
+minutes to generate); mid / tiny are small.
 
 Roofline: the dominant kernel is the item pass (P or Q), timed with HIP
 events on the library's compute stream during the timed region; its
@@ -46,7 +49,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="scientific", choices=["scientific", "rating", "mid", "tiny"])
+    ap.add_argument("--config", default="scientific", choices=["scientific", "rating", "billion", "mid", "tiny"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
@@ -206,6 +209,8 @@ def main():
                       "200,000 rank-32 matrix (10% observed), k=32, fp32, degree step",
         "rating": "Rating-shaped template fit: 65,536 x 8,192 most-observed template of a "
                   "480,189 x 17,770 Zipf matrix (100M ratings), k=64, bf16 + clip, degree step",
+        "billion": "Billion-scale template fit: 1,000,000 x 100,000 most-popular template of a "
+                   "10M x 1M Zipf(1.0) matrix (1e9 cells), k=128, bf16 + clip, degree step",
         "mid": "Mid template fit: 4,096 x 2,048 of 20,000 x 10,000 (2M cells), k=32, fp32",
         "tiny": "Tiny template fit: 200 x 160 of 1,000 x 800 (40k cells), k=8, fp32",
     }[args.config]

@@ -24,14 +24,22 @@ def _sampled_parity(T, p, n_rows=64, n_cols=64, tol=1e-4):
     st, P1, Q1, hist = gpu_fit(T, p, epochs=1)
     assert st == 0
     g = np.random.default_rng(0)
-    rows = g.choice(p.I.size, n_rows, replace=False)
-    cols = g.choice(p.J.size, n_cols, replace=False)
+    # a uniform sample plus the four longest buckets of each side (those span
+    # several waves, so their updates go through the fixup kernel)
+    top_r = np.argsort(-np.bincount(a, minlength=p.I.size), kind="stable")[:4]
+    top_c = np.argsort(-np.bincount(b, minlength=p.J.size), kind="stable")[:4]
+    rows = np.union1d(g.choice(p.I.size, n_rows, replace=False), top_r)
+    cols = np.union1d(g.choice(p.J.size, n_cols, replace=False), top_c)
     bf16 = p.prec == "bf16"
-    sel = np.isin(a, rows)
+    mask = np.zeros(p.I.size, dtype=bool)
+    mask[rows] = True
+    sel = mask[a]
     _, Po, _, _, _ = oracle.fit(a[sel], b[sel], v[sel], p.P0, p.Q0, 1, p.lam, p.lr, p.step, p.clip,
                                 p.xi, bf16=bf16)
     assert rel_fro(P1[rows], Po[rows]) <= tol
-    sel = np.isin(b, cols)
+    mask = np.zeros(p.J.size, dtype=bool)
+    mask[cols] = True
+    sel = mask[b]
     _, _, Qo, _, _ = oracle.fit(a[sel], b[sel], v[sel], p.P0, p.Q0, 1, p.lam, p.lr, p.step, p.clip,
                                 p.xi, bf16=bf16)
     assert rel_fro(Q1[cols], Qo[cols]) <= tol
@@ -56,3 +64,10 @@ def test_scientific_fullsize_sampled(T):
 @pytest.mark.timeout(400)
 def test_rating_fullsize_sampled_bf16(T):
     _sampled_parity(T, synth.rating())
+
+
+@pytest.mark.timeout(900)
+def test_billion_fullsize_sampled_bf16(T):
+    """1,000,000 x 100,000 template, about 4.2e8 training cells, k = 128."""
+    note("fullsize billion: generating (a few minutes)")
+    _sampled_parity(T, synth.billion_template())

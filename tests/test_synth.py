@@ -55,3 +55,50 @@ def test_random_case_hot_buckets_in_template():
     cdeg = np.bincount(p.i, minlength=p.n)
     assert np.sum(cdeg[p.J] == p.m) >= 1
     assert not np.all(np.diff(p.I) > 0)  # local ids follow array order, not sorted
+
+
+def test_draw_count_solver_matches_the_exact_sum():
+    """The binned solver for the number of pairwise draws D: at its D, the exact
+    expected count of distinct cells (full double sum) is the target."""
+    from tsid_synth.generate import _draws_for_distinct, _zipf_rank_weights
+    wr = _zipf_rank_weights(3000, 1.0)
+    wc = _zipf_rank_weights(400, 1.0)
+    D = _draws_for_distinct(wr, wc, 1.0e5)
+    exact = np.sum(-np.expm1(-D * wr[:, None] * wc[None, :]))
+    assert abs(exact - 1.0e5) <= 0.01 * 1.0e5
+
+
+def test_billion_template_cells_follow_the_cell_law():
+    """Scaled-down Billion workload: distinct cells inside the template block,
+    z-scored values, and each cell observed with probability
+    1 - exp(-D w_u w_i) (checked per probability band, both the Bernoulli
+    prefix and the Poisson-drawn tail)."""
+    from tsid_synth.generate import _zipf_rank_weights
+    p = synth.billion_template(scale=0.01)
+    q = synth.billion_template(scale=0.01)
+    for f in ("u", "i", "r", "tu", "ti", "tr", "I", "J"):
+        assert np.array_equal(getattr(p, f), getattr(q, f))
+    u = np.concatenate([p.u, p.tu]).astype(np.int64)
+    i = np.concatenate([p.i, p.ti]).astype(np.int64)
+    r = np.concatenate([p.r, p.tr]).astype(np.float64)
+    assert abs(r.mean()) < 1e-3 and abs(r.std() - 1.0) < 1e-3
+    rank_u = np.full(p.m, -1)
+    rank_u[p.I] = np.arange(p.I.size)
+    rank_i = np.full(p.n, -1)
+    rank_i[p.J] = np.arange(p.J.size)
+    a, b = rank_u[u], rank_i[i]
+    assert np.all(a >= 0) and np.all(b >= 0)
+    keys = a * p.J.size + b
+    assert np.unique(keys).size == keys.size
+    assert 0.07 < p.tu.size / keys.size < 0.13
+    wr = _zipf_rank_weights(p.m, 1.0)[: p.I.size]
+    wc = _zipf_rank_weights(p.n, 1.0)[: p.J.size]
+    prob = -np.expm1(-p.extra["draws"] * wr[:, None] * wc[None, :])
+    seen = np.zeros(prob.shape, dtype=bool)
+    seen[a, b] = True
+    assert abs(seen.sum() - prob.sum()) <= 5 * np.sqrt(prob.sum())
+    for lo, hi in ((0.01, 0.05), (0.05, 0.2), (0.2, 0.5), (0.5, 0.8), (0.8, 0.99)):
+        band = (prob >= lo) & (prob < hi)
+        mean_p = prob[band].mean()
+        sd = np.sqrt(np.sum(prob[band] * (1 - prob[band]))) / band.sum()
+        assert abs(seen[band].mean() - mean_p) <= 5 * sd + 1e-3, (lo, hi)

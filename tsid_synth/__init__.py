@@ -22,6 +22,7 @@ from .generate import (  # noqa: F401
     mid,
     rating,
     scientific_template,
+    billion_template,
     random_case,
     dense_lowrank_case,
     CONFIGS,

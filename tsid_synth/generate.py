@@ -9,6 +9,9 @@ Shapes and value models follow the five benchmark configurations:
                   100 M cells, Zipf(0.9) rows / Zipf(1.1) columns, rank 64.
 * ``scientific``  200,000 x 200,000, rank 32 with singular values exp(-j/8),
                   uniform 10 % observation; only the template block is drawn.
+* ``billion``     10 M x 1 M, 1.0e9 cells, Zipf(1.0) rows and columns, rank
+                  128, values z-scored; only the 1 M x 100 k template block of
+                  the most popular rows and columns is drawn.
 
 Conventions: "N(0, v)" takes v as the variance, so latent factors drawn
 N(0, 1/sqrt(k)) give unit-variance products.  Held-out cells are chosen by a
@@ -24,6 +27,7 @@ import numpy as np
 PURPOSE = {
     "factors": 1, "rows": 2, "cols": 3, "cells": 4, "values": 5, "noise": 6,
     "holdout": 7, "template": 8, "init": 9, "order": 10, "extra": 11,
+    "dense": 12, "sparse": 13,
 }
 
 
@@ -119,6 +123,17 @@ def _inv_cdf(cdf: np.ndarray, x: np.ndarray) -> np.ndarray:
     return torch.searchsorted(torch.from_numpy(cdf), torch.from_numpy(x), right=True).numpy()
 
 
+def _sorted_distinct(x: np.ndarray) -> np.ndarray:
+    """Sorted distinct values of x (what np.unique returns, from one sort)."""
+    s = np.sort(x)
+    if s.size < 2:
+        return s
+    keep = np.empty(s.size, dtype=bool)
+    keep[0] = True
+    np.not_equal(s[1:], s[:-1], out=keep[1:])
+    return s[keep]
+
+
 def _distinct_zipf_cells(m, n, target, cdf_r, cdf_c, g):
     """Exactly `target` distinct cells drawn pairwise from the two
     popularity laws; repeated draws of a cell are discarded and topped up."""
@@ -128,7 +143,7 @@ def _distinct_zipf_cells(m, n, target, cdf_r, cdf_c, g):
         batch = int(need * 2.0) + 65536
         u = _inv_cdf(cdf_r, g.random(batch)).clip(0, m - 1)
         i = _inv_cdf(cdf_c, g.random(batch)).clip(0, n - 1)
-        keys = np.unique(np.concatenate([keys, u.astype(np.int64) * n + i]))
+        keys = _sorted_distinct(np.concatenate([keys, u.astype(np.int64) * n + i]))
     if keys.size > target:
         keys = np.sort(keys[g.choice(keys.size, target, replace=False)])
     return keys
@@ -181,6 +196,7 @@ SETTINGS = {
     "mid": dict(lam=1e-3, lr=0.15, epochs=100, step="degree", prec="fp32", clip=False, xi=0.1),
     "rating": dict(lam=1e-3, lr=0.15, epochs=20, step="degree", prec="bf16", clip=True, xi=0.1),
     "scientific": dict(lam=1e-3, lr=0.5, epochs=20, step="degree", prec="fp32", clip=False, xi=0.1),
+    "billion": dict(lam=1e-3, lr=0.1, epochs=20, step="degree", prec="bf16", clip=True, xi=0.1),
 }
 
 
@@ -279,6 +295,118 @@ def scientific_template(seed: int = 4, side: int = 16384, m: int = 200000) -> Pr
                    extra={"omega_scope": "template block only"})
 
 
+def _zipf_rank_weights(size: int, s: float) -> np.ndarray:
+    """Zipf(s) popularity by rank (rank 1 first), normalised to sum 1."""
+    w = 1.0 / np.power(np.arange(1, size + 1, dtype=np.float64), s)
+    return w / w.sum()
+
+
+def _draws_for_distinct(wr: np.ndarray, wc: np.ndarray, target: float, bins: int = 1500) -> float:
+    """Number D of independent (row, column) draws, rows ~ wr and columns ~ wc,
+    whose expected count of distinct cells is `target`.  A cell drawn with
+    probability w_u w_i is seen at least once with probability
+    1 - exp(-D w_u w_i); the double sum runs over log-spaced rank bins (each
+    bin at its mean weight) and D is found by bisection."""
+    def binned(w):
+        edges = np.unique(np.round(np.logspace(0, np.log10(w.size), bins)).astype(np.int64) - 1)
+        edges = np.append(edges[edges < w.size], w.size)
+        cnt = np.diff(edges).astype(np.float64)
+        sums = np.add.reduceat(w, edges[:-1])
+        return sums / cnt, cnt
+    ar, cr = binned(wr)
+    ac, cc = binned(wc)
+    lo, hi = target, target * 1e4
+    for _ in range(80):
+        mid = (lo * hi) ** 0.5
+        got = np.sum(cr[:, None] * cc[None, :] * -np.expm1(-mid * ar[:, None] * ac[None, :]))
+        lo, hi = (mid, hi) if got < target else (lo, mid)
+    return (lo * hi) ** 0.5
+
+
+def _block_rng(seed: int, purpose: str, block: int) -> np.random.Generator:
+    """Philox stream keyed by (seed, purpose, block): blocks draw independently,
+    so they can be generated in any order or in parallel."""
+    return np.random.Generator(
+        np.random.Philox(np.random.SeedSequence([int(seed), PURPOSE[purpose], int(block)])))
+
+
+def billion_template(seed: int = 5, scale: float = 1.0) -> Problem:
+    """Billion-scale: 10 M x 1 M, 1.0e9 distinct cells drawn pairwise with
+    Zipf(1.0) row and column popularity (ranks through seeded permutations),
+    rank 128, values z-scored to N(0, 1).  Template: the 1 M most popular rows
+    x the 100 k most popular columns (the expected most-observed ones).
+
+    Only the template block is drawn.  With D pairwise draws (D set so that
+    the whole matrix expects 1.0e9 distinct cells) a cell of popularity
+    weights w_u, w_i is observed with probability p = 1 - exp(-D w_u w_i),
+    independently of the others (the Poisson form of the draws).  Per
+    template row, the columns with p >= 1/2 (a prefix, by rank) are kept by a
+    Bernoulli trial each; the rest are reached by Poisson(D w_u x their
+    weight) draws over those columns, duplicates dropped, which observes each
+    with the same p.  Rows are cut into blocks of about 2^24 expected cells,
+    each with its own streams; cells come out grouped by row.  `scale` < 1
+    shrinks every size (test use)."""
+    import torch
+    m = max(64, int(10_000_000 * scale))
+    n = max(64, int(1_000_000 * scale))
+    nnz_full = max(1000.0, 1.0e9 * scale * scale)
+    m_t = max(16, int(1_000_000 * scale))
+    n_t = max(16, int(100_000 * scale))
+    k = 128
+    wr = _zipf_rank_weights(m, 1.0)
+    wc = _zipf_rank_weights(n, 1.0)
+    D = _draws_for_distinct(wr, wc, nnz_full)
+    I = make_rng(seed, "rows").permutation(m)[:m_t].astype(np.int32)  # id of rank a
+    J = make_rng(seed, "cols").permutation(n)[:n_t].astype(np.int32)
+    wr_t, wc_t = wr[:m_t], wc[:n_t]
+    C = np.concatenate([[0.0], np.cumsum(wc_t)])   # column weight prefix sums
+    Ct = torch.from_numpy(C[1:])
+    # dense prefix per row: columns b with D w_a w_b >= ln 2
+    K = np.searchsorted(-wc_t, -np.log(2.0) / (D * wr_t), side="right").astype(np.int64)
+    lam = D * wr_t * (C[-1] - C[K])                # expected draws past the prefix
+    # row blocks of about 2^24 expected cells (dense prefix + sparse draws)
+    expect = np.cumsum(K + lam)
+    cuts = np.searchsorted(expect, np.arange(1, int(expect[-1] // (1 << 24)) + 1) * float(1 << 24))
+    bounds = np.unique(np.concatenate([[0], cuts, [m_t]]))
+    parts = []
+    for blk in range(bounds.size - 1):
+        a0, a1 = int(bounds[blk]), int(bounds[blk + 1])
+        gd = _block_rng(seed, "dense", blk)
+        gs = _block_rng(seed, "sparse", blk)
+        rows = np.arange(a0, a1, dtype=np.int64)
+        kd = K[a0:a1]
+        rd = np.repeat(rows, kd)
+        bd = np.arange(rd.size, dtype=np.int64) - np.repeat(np.cumsum(kd) - kd, kd)
+        keep = gd.random(rd.size) < -np.expm1(-D * wr_t[rd] * wc_t[bd])
+        dense = rd[keep] * n_t + bd[keep]
+        del rd, bd, keep
+        rs = np.repeat(rows, gs.poisson(lam[a0:a1]))
+        lo = C[K[rs]]
+        y = lo + gs.random(rs.size) * (C[-1] - lo)
+        bs = torch.searchsorted(Ct, torch.from_numpy(y), right=True).numpy()
+        bs = np.clip(bs, K[rs], n_t - 1)
+        parts.append(np.sort(np.concatenate([dense, _sorted_distinct(rs * n_t + bs)])))
+        del dense, rs, bs, lo, y
+    keys = np.concatenate(parts)
+    del parts
+    a = keys // n_t
+    b = keys - a * n_t
+    del keys
+    gf = make_rng(seed, "factors")
+    sd = k ** -0.25
+    A = gf.normal(0.0, sd, (m_t, k)).astype(np.float32)
+    B = gf.normal(0.0, sd, (n_t, k)).astype(np.float32)
+    x = _latent_values(a, b, A, B)
+    del A, B
+    x -= x.mean()
+    x /= x.std()
+    u = I[a]
+    i = J[b]
+    del a, b
+    return _finish("billion", m, n, u, i, x.astype(np.float32), seed, I, J, k, SETTINGS["billion"],
+                   extra={"omega_scope": "template block only", "draws": D})
+
+
 def random_case(m: int, n: int, nnz: int, m_t: int, n_t: int, k: int, seed: int,
                 hot_rows: int = 0, hot_cols: int = 0, lam: float = 1e-3, lr: float = 0.2,
                 epochs: int = 5, step: str = "degree", prec: str = "fp32", clip: bool = False,
@@ -339,6 +467,7 @@ def dense_lowrank_case(m: int, n: int, rank: int, frac: float, seed: int):
 
 CONFIGS: Dict[str, Callable[..., Problem]] = {
     "tiny": tiny, "mid": mid, "rating": rating, "scientific": scientific_template,
+    "billion": billion_template,
 }
 
 
