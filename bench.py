@@ -52,6 +52,12 @@ def parse():
     ap.add_argument("--config", default="scientific", choices=["scientific", "rating", "billion", "mid", "tiny"])
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--extend", action="store_true",
+                    help="after the timed fit, time the end-to-end extension (row phase, then "
+                         "column phase, 16 chunks each, streamed from pinned host memory) and print "
+                         "a second JSON line; needs a workload with the whole matrix drawn "
+                         "(rating, mid, tiny)")
+    ap.add_argument("--extend-steps", type=int, default=20)
     ap.add_argument("--copy-probe", action="store_true",
                     help="time a plain device copy of 1 GiB instead (HBM probe and the "
                          "reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -125,6 +131,62 @@ def cpu_baseline(p, seconds):
                       f"the same workload, all {p.I.size} x {p.J.size} template factor rows, "
                       f"{epochs} full-gradient epochs, serial fp64 C",
             "seconds": el, "nproc": os.cpu_count()}
+
+
+def h2d_probe(nbytes, reps=5):
+    """Pinned host-to-device copy rate (bytes/s) for a buffer of nbytes."""
+    import torch
+    src = torch.empty(nbytes // 4, dtype=torch.float32).pin_memory()
+    dst = torch.empty_like(src, device="cuda")
+    dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    return nbytes * reps / (time.perf_counter() - t0)
+
+
+def extension_line(args, p, T, P, Q):
+    """End-to-end extension from the fitted template factors (Section 5.2)."""
+    import paper_2608_00977_amd as tsid
+    from paper_2608_00977_amd.extension import Extension
+    if p.extra.get("omega_scope") == "template block only":
+        raise SystemExit("--extend needs a workload whose whole matrix is drawn (rating, mid, tiny)")
+    t0 = time.perf_counter()
+    ext = Extension(p.m, p.n, p.u, p.i, p.r, p.I, p.J, n_chunks=16)
+    prep_s = time.perf_counter() - t0
+    # one-sided steps from zero: lr 0.05 keeps a free row with a single cell stable
+    opts = tsid.make_opts(epochs=args.extend_steps, lam=p.lam, lr=0.05, clip=p.clip, xi=p.xi,
+                          step="degree")
+    ext.run(T, P, Q, opts)  # warm-up (allocations, code load)
+    _, _, ph = ext.run(T, P, Q, opts)
+    n_row, n_col = ext.rows.nnz, ext.cols.nnz
+    t_ext = ph["row_phase_s"] + ph["col_phase_s"]
+    h2d_bytes = 12 * (n_row + n_col)
+    rate = h2d_probe(max(1 << 20, 12 * max(c[0].numel() for c in ext.rows.chunks + ext.cols.chunks)))
+    log(f"extension: {n_row} + {n_col} cells in {t_ext:.4f}s")
+    return {
+        "metric": "extension entries/s (row phase + column phase)",
+        "value": (n_row + n_col) / t_ext,
+        "unit": "entries/s",
+        "n_gpus": 1,
+        "higher_is_better": True,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{p.name}: extension of the {p.I.size} x {p.J.size} template to "
+                               f"{p.m} x {p.n}, 16 chunks per phase, {args.extend_steps} one-sided "
+                               "steps per chunk, degree step, fixed factors fp32",
+                   "row_phase_cells": n_row, "col_phase_cells": n_col,
+                   "row_chunks": ext.rows.bounds.size - 1, "col_chunks": ext.cols.bounds.size - 1},
+        "row_phase_s": ph["row_phase_s"],
+        "col_phase_s": ph["col_phase_s"],
+        "assemble_s": ph["assemble_s"],
+        "host_prep_s": prep_s,
+        "pcie": {"h2d_bytes": h2d_bytes, "pinned_h2d_GBps": round(rate / 1e9, 2),
+                 "h2d_only_s": h2d_bytes / rate,
+                 "frac_of_h2d_bound": round(h2d_bytes / rate / t_ext, 4)},
+    }
 
 
 def main():
@@ -242,8 +304,10 @@ def main():
         "build_s": build_s,
         "loss_after_timed_epochs": hist_T,
     }
-    T.close()
     print(json.dumps(line), flush=True)
+    if args.extend:
+        print(json.dumps(extension_line(args, p, T, P, Q)), flush=True)
+    T.close()
     return 0
 
 

@@ -1,0 +1,111 @@
+"""End-to-end extension of the template factors to the whole matrix
+(Section 5.2), on top of ``tsid_extend_chunk`` and ``tsid_chunk_plan``.
+
+Order of the two phases (every training cell outside the template block is
+used exactly once):
+
+* row phase: each row not in the template is fitted from its cells in
+  template columns, with the template column factors Q_J fixed;
+* column phase: each column not in the template is fitted from all of its
+  cells, with every row factor fixed (template rows from the fit, the other
+  rows from the row phase).
+
+Each phase groups its cells by free index on the host, cuts them into
+chunks of whole rows (or columns) with ``tsid_chunk_plan`` and streams the
+chunks through the library, which stages each chunk's host-to-device copy on
+its own stream while the previous chunk computes.  This module only slices
+and pins host arrays; all arithmetic runs in the library's kernels.
+"""
+import time
+from dataclasses import dataclass, field
+from typing import List, Tuple
+
+import numpy as np
+import torch
+
+from .binding import Tsid, tsid_chunk_plan
+
+
+@dataclass
+class Phase:
+    side: int                 # 0: free rows (fixed: template columns); 1: free columns
+    free_ids: np.ndarray      # global ids of the free rows / columns, ascending
+    bounds: np.ndarray        # chunk boundaries in free-index space
+    nnz: int
+    chunks: List[Tuple[torch.Tensor, torch.Tensor, torch.Tensor, int, int]] = field(
+        default_factory=list)  # (fixed_id, free_local, r) pinned, free range [lo, hi)
+
+
+def _phase(side, free_mask, key, fixed, r, n_chunks, max_entries) -> Phase:
+    free_ids = np.flatnonzero(free_mask)
+    pos = np.full(free_mask.size, -1, np.int64)
+    pos[free_ids] = np.arange(free_ids.size)
+    fk = pos[key]
+    order = np.argsort(fk, kind="stable")
+    fk, fixed, r = fk[order], fixed[order], r[order]
+    counts = np.bincount(fk, minlength=free_ids.size).astype(np.int64)
+    bounds = tsid_chunk_plan(counts, n_chunks, max_entries)
+    start = np.concatenate([[0], np.cumsum(counts)])
+    ph = Phase(side, free_ids, bounds, int(fk.size))
+    for j in range(bounds.size - 1):
+        lo, hi = int(bounds[j]), int(bounds[j + 1])
+        e0, e1 = int(start[lo]), int(start[hi])
+        pin = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a, dt)).pin_memory()
+        ph.chunks.append((pin(fixed[e0:e1], np.int32), pin(fk[e0:e1] - lo, np.int32),
+                          pin(r[e0:e1], np.float32), lo, hi))
+    return ph
+
+
+class Extension:
+    """Host plan of both phases for one matrix and template (built once;
+    ``run`` may be called repeatedly, e.g. with new template factors)."""
+
+    def __init__(self, m, n, u, i, r, I, J, n_chunks=16, max_entries=0):
+        u = np.asarray(u, np.int64)
+        i = np.asarray(i, np.int64)
+        r = np.asarray(r, np.float32)
+        self.m, self.n = int(m), int(n)
+        self.I = np.asarray(I, np.int64)
+        self.J = np.asarray(J, np.int64)
+        row_in = np.zeros(self.m, bool)
+        row_in[self.I] = True
+        col_in = np.zeros(self.n, bool)
+        col_in[self.J] = True
+        cm = np.full(self.n, -1, np.int64)
+        cm[self.J] = np.arange(self.J.size)
+        sel = ~row_in[u] & col_in[i]
+        self.rows = _phase(0, ~row_in, u[sel], cm[i[sel]], r[sel], n_chunks, max_entries)
+        sel = ~col_in[i]
+        self.cols = _phase(1, ~col_in, i[sel], u[sel], r[sel], n_chunks, max_entries)
+        self.template_nnz = int(np.count_nonzero(row_in[u] & col_in[i]))
+
+    def _run_phase(self, T: Tsid, ph: Phase, F_fixed: torch.Tensor, out: torch.Tensor, opts):
+        for fx, fl, rr, lo, hi in ph.chunks:
+            T.extend_chunk(ph.side, fx, fl, rr, hi - lo, F_fixed, out[lo:hi], opts)
+        T.sync()
+
+    def run(self, T: Tsid, P_t: torch.Tensor, Q_t: torch.Tensor, opts):
+        """P_t (m_t x k), Q_t (n_t x k): fp32 device factors of the template,
+        in template order.  Returns (P, Q): the full m x k and n x k factors
+        as pinned host tensors, and the wall time of each phase in seconds."""
+        k = P_t.shape[1]
+        P_free = torch.empty((self.rows.free_ids.size, k), dtype=torch.float32).pin_memory()
+        Q_free = torch.empty((self.cols.free_ids.size, k), dtype=torch.float32).pin_memory()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        self._run_phase(T, self.rows, Q_t, P_free, opts)
+        t1 = time.perf_counter()
+        P_full = torch.empty((self.m, k), dtype=torch.float32, device=P_t.device)
+        P_full[torch.from_numpy(self.I).to(P_t.device)] = P_t
+        if self.rows.free_ids.size:
+            P_full[torch.from_numpy(self.rows.free_ids).to(P_t.device)] = P_free.to(P_t.device)
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        self._run_phase(T, self.cols, P_full, Q_free, opts)
+        t3 = time.perf_counter()
+        P = P_full.cpu()
+        Q = torch.empty((self.n, k), dtype=torch.float32)
+        Q[torch.from_numpy(self.J)] = Q_t.cpu()
+        if self.cols.free_ids.size:
+            Q[torch.from_numpy(self.cols.free_ids)] = Q_free
+        return P, Q, {"row_phase_s": t1 - t0, "assemble_s": t2 - t1, "col_phase_s": t3 - t2}
