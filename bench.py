@@ -21,12 +21,16 @@ Billion-scale template (1,000,000 x 100,000 of a 10 M x 1 M Zipf matrix,
 about 4.2e8 training cells, k = 128, bf16 + clipping; its input takes a few
 minutes to generate); mid / tiny are small.
 
-Roofline: the dominant kernel is the item pass (P or Q), timed with HIP
-events on the library's compute stream during the timed region; its
-algorithmic bytes per launch are the compulsory bytes of one pass: the
-bucketed cell stream (8 B per cell), the bucket pointers (8 B per bucket), the
-owner rows read and written once and the gathered rows read once (4 B per
-coordinate in fp32; 2 B for bf16 copies).
+Roofline: the dominant kernel is the longer of the P and Q passes (the slab
+pass on evenly spread fp32 templates such as Scientific, else the item pass),
+timed with HIP events on the library's compute stream during the timed
+region; its algorithmic bytes per launch are the compulsory bytes of one
+pass: the bucketed cell stream (8 B per cell), the bucket pointers (8 B per
+bucket), the owner rows read and written once and the gathered rows read once
+(4 B per coordinate in fp32; 2 B for bf16 copies).  A slab pass whose row
+blocks are split over several workgroups leaves the row updates (the
+owner-row writes) to a finishing kernel, timed with the fixups; its bytes
+exclude them.
 
 CPU baseline: the fp64 oracle (serial C) on a bounded sample of the same
 template cells, for as many epochs as fit in about --cpu-seconds.
@@ -50,6 +54,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="scientific", choices=["scientific", "rating", "billion", "mid", "tiny"])
+    ap.add_argument("--pass-kernel", default="auto", choices=["auto", "item", "slab"],
+                    help="kernel of the P and Q passes (tsid_set_pass_kernel); auto picks the "
+                         "slab pass for evenly spread fp32 templates")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--extend", action="store_true",
@@ -87,12 +94,14 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def pass_bytes(nnz, owners, others, k, prec):
-    """Compulsory bytes of one pass (see the module docstring)."""
+def pass_bytes(nnz, owners, others, k, prec, no_owner_write=False):
+    """Compulsory bytes of one pass launch (see the module docstring)."""
     fb = 4 * k
     b = 8 * nnz + 8 * (owners + 1) + 2 * fb * owners + (2 * k if prec == "bf16" else fb) * others
     if prec == "bf16":
         b += 2 * k * owners  # bf16 copy of the updated rows
+    if no_owner_write:
+        b -= fb * owners
     return b
 
 
@@ -209,6 +218,7 @@ def main():
     log(f"generated {p.nnz} training cells in {gen_s:.1f}s")
 
     T = tsid.Tsid(0)
+    T.set_pass_kernel(args.pass_kernel)
     u = torch.from_numpy(p.u).pin_memory()
     i = torch.from_numpy(p.i).pin_memory()
     r = torch.from_numpy(p.r).pin_memory()
@@ -238,6 +248,7 @@ def main():
     wall = time.perf_counter() - t0
     tm = T.timing()
     T.set_timing(False)
+    kernels = T.pass_kernels()
     ms_per_step = wall * 1e3 / args.steps
     value = nnz / (ms_per_step / 1e3)
     log(f"{args.steps} epochs in {wall:.4f}s: {ms_per_step:.4f} ms/epoch, {value:.4e} cells/s")
@@ -246,18 +257,25 @@ def main():
 
     k = info["k"]
     m_t, n_t = info["m_t"], info["n_t"]
-    by = [pass_bytes(nnz, m_t, n_t, k, p.prec), pass_bytes(nnz, n_t, m_t, k, p.prec)]
+    # A slab pass split over several workgroups per block leaves the row
+    # updates to its finishing kernel (timed as a fixup): its own launch then
+    # does not write the owner rows.
+    split = tm["fixup_launches"] > 0
+    by = [pass_bytes(nnz, m_t, n_t, k, p.prec, kernels[0] == "slab" and split),
+          pass_bytes(nnz, n_t, m_t, k, p.prec, kernels[1] == "slab" and split)]
     avg = [tm["pass_ms"][j] / max(1, tm["pass_launches"][j]) for j in range(2)]
     dom = 0 if tm["pass_ms"][0] >= tm["pass_ms"][1] else 1
     achieved = by[dom] / (avg[dom] / 1e3) / 1e9
-    src = open(os.path.join(ROOT, "paper_2608_00977_amd", "csrc", "fit.hip"), "rb").read()
+    kname = {"item": "k_item_pass", "slab": "k_slab_pass"}[kernels[dom]]
+    ksrc = {"item": "fit.hip", "slab": "slab.hip"}[kernels[dom]]
+    src = open(os.path.join(ROOT, "paper_2608_00977_amd", "csrc", ksrc), "rb").read()
     sha = hashlib.sha256(src).hexdigest()
     which = ["p_pass", "q_pass"][dom]
-    traffic = traffic_from_profiles(sha, f"{args.config}:{which}")
+    traffic = traffic_from_profiles(sha, f"{args.config}:{which}:{kernels[dom]}")
     epoch_bytes = by[0] + by[1]
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                "kernel": f"k_item_pass ({'P' if dom == 0 else 'Q'} pass)",
+                "kernel": f"{kname} ({'P' if dom == 0 else 'Q'} pass)",
                 "bytes_per_launch": by[dom], "avg_launch_ms": round(avg[dom], 5)}
 
     cpu = None
@@ -292,7 +310,8 @@ def main():
         "config": {"workload": workload, "config": args.config, "m": p.m, "n": p.n,
                    "m_t": m_t, "n_t": n_t, "template_cells_train": nnz, "k": k,
                    "precision": p.prec, "step": p.step, "lr": p.lr, "lambda": p.lam,
-                   "clip": p.clip, "parallelism": "single GPU"},
+                   "clip": p.clip, "parallelism": "single GPU",
+                   "pass_kernels": {"p_pass": kernels[0], "q_pass": kernels[1]}},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "compulsory_GBps_per_epoch": round(epoch_bytes / (ms_per_step / 1e3) / 1e9, 2),

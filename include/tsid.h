@@ -122,8 +122,9 @@ tsid_status tsid_template_info(const tsid_ctx *ctx, int32_t *m_t, int32_t *n_t, 
  * Epoch t computes every residual and both gradients (Eqs. 3-4) at (P_t, Q_t)
  * and moves every row of P and Q at once against its gradient (Eq. 5 with the
  * step of opts->step and the clip of opts->clip).  Each factor row is written
- * once per epoch by the unit that owns it; no atomic operations touch factor
- * or gradient memory, and the result is bitwise reproducible.
+ * once per epoch by the unit that owns it; no atomic operations are used, and
+ * the result is bitwise reproducible for a given pass kernel
+ * (tsid_set_pass_kernel).
  *  P   DEVICE m_t x k: P_0 on entry, P_T on return.
  *  Q   DEVICE n_t x k: Q_0 on entry, Q_T on return.
  *  loss_hist  HOST epochs + 1 doubles or NULL: L(P_t, Q_t) for t = 0..epochs.
@@ -181,13 +182,40 @@ tsid_status tsid_extend_chunk(tsid_ctx *ctx, int side, const int32_t *fixed_id,
  * those chunks (and clears it), else TSID_OK. */
 tsid_status tsid_sync(tsid_ctx *ctx);
 
+/* Kernel that runs the P and Q passes of tsid_fit_template (the arithmetic is
+ * the same; the mapping onto the GPU differs).
+ *  TSID_PASS_ITEM  every bucket is cut into work items of a few hundred cells,
+ *                  each taken by a group of lanes that gathers the other
+ *                  factor's rows from the cache hierarchy.  Any rank,
+ *                  precision and degree distribution.
+ *  TSID_PASS_SLAB  one lane per factor row; the other factor is staged
+ *                  through LDS in 128 KiB slabs shared by a block of 512 rows.
+ *                  fp32 factors with k in {8, 16, 32, 64}; fastest when the
+ *                  cells are spread evenly (uniformly sampled templates).
+ *  TSID_PASS_AUTO  (default) the slab pass for a side whose template is fp32,
+ *                  k <= 64, holds on average at least 4 cells per staged row
+ *                  and block of 512 rows, and has no bucket longer than twice
+ *                  the mean plus 64; the item pass otherwise.
+ * Takes effect at the next tsid_fit_template.  Errors: E_INVAL (unknown mode);
+ * a fit with TSID_PASS_SLAB on an unsupported rank or precision returns
+ * E_INVAL. */
+enum { TSID_PASS_AUTO = 0, TSID_PASS_ITEM = 1, TSID_PASS_SLAB = 2 };
+tsid_status tsid_set_pass_kernel(tsid_ctx *ctx, int mode);
+
+/* Pass kernels the last tsid_fit_template ran (TSID_PASS_ITEM or
+ * TSID_PASS_SLAB) for the P pass and the Q pass; 0 before any fit.  Either
+ * output may be NULL.  Errors: E_INVAL (ctx NULL). */
+tsid_status tsid_fit_pass_kernels(const tsid_ctx *ctx, int32_t *p_pass, int32_t *q_pass);
+
 /* Kernel timing of the template fit (a tracing aid).  While enabled, every
  * kernel of each epoch of tsid_fit_template is launched with a start and an
  * end HIP event attached to its dispatch on the compute stream (no separate
  * event packets), and the durations accumulate here until the next
  * tsid_set_timing call resets them.  pass_ms[0] / pass_launches[0]: the P
- * pass (row buckets); [1]: the Q pass (column buckets); fixup: the fixups of
- * buckets longer than one wave; reduce: the batched loss reductions (one per
+ * pass (row buckets); [1]: the Q pass (column buckets); fixup: the kernels
+ * that combine partial sums after a pass (item pass: buckets longer than one
+ * wave; slab pass: blocks split over several workgroups), which also update
+ * those rows; reduce: the batched loss reductions (one per
  * 16 epochs); epoch_ms: start of each epoch's first kernel to the end of its
  * last, summed. */
 typedef struct {

@@ -27,6 +27,7 @@ STATUS = {0: "TSID_OK", 1: "TSID_E_INVAL", 2: "TSID_E_RANGE", 3: "TSID_E_DUP",
 OK, E_INVAL, E_RANGE, E_DUP, E_NOMEM, E_DEVICE, E_STATE, E_NONFINITE = range(8)
 FP32, BF16 = 0, 1
 STEP_SUM, STEP_DEGREE = 0, 1
+PASS_KERNEL = {"auto": 0, "item": 1, "slab": 2}
 IDX = {"row_map": 0, "col_map": 1, "row_ptr": 2, "csr_col": 3, "csr_val": 4, "col_ptr": 5,
        "csc_row": 6, "csc_val": 7, "deg_r": 8, "deg_c": 9}
 
@@ -72,6 +73,8 @@ def lib() -> C.CDLL:
         "tsid_fit_template": (C.c_int, [P, P, P, C.POINTER(tsid_fit_opts), P]),
         "tsid_fit_epochs_done": (C.c_int, [P, P]),
         "tsid_set_timing": (C.c_int, [P, C.c_int]),
+        "tsid_set_pass_kernel": (C.c_int, [P, C.c_int]),
+        "tsid_fit_pass_kernels": (C.c_int, [P, P, P]),
         "tsid_get_timing": (C.c_int, [P, C.POINTER(tsid_timing)]),
         "tsid_loss": (C.c_int, [P, P, P, C.c_float, P]),
         "tsid_extend_chunk": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P,
@@ -130,6 +133,20 @@ def tsid_fit_epochs_done(ctx) -> int:
 
 def tsid_set_timing(ctx, enable: bool) -> int:
     return lib().tsid_set_timing(ctx, int(bool(enable)))
+
+
+def tsid_set_pass_kernel(ctx, mode: int) -> int:
+    return lib().tsid_set_pass_kernel(ctx, int(mode))
+
+
+def tsid_fit_pass_kernels(ctx):
+    """(P pass, Q pass) kernel names of the last fit ('item', 'slab', or None)."""
+    a, b = C.c_int32(0), C.c_int32(0)
+    st = lib().tsid_fit_pass_kernels(ctx, C.byref(a), C.byref(b))
+    if st != OK:
+        raise TsidError(st, "tsid_fit_pass_kernels")
+    names = {v: k for k, v in PASS_KERNEL.items()}
+    return names.get(a.value), names.get(b.value)
 
 
 def tsid_get_timing(ctx) -> dict:
@@ -244,6 +261,14 @@ class Tsid:
 
     def set_timing(self, enable: bool):
         self._check(tsid_set_timing(self.ctx, enable), "tsid_set_timing")
+
+    def set_pass_kernel(self, mode: str):
+        """'auto', 'item' or 'slab' (tsid_set_pass_kernel)."""
+        self._check(tsid_set_pass_kernel(self.ctx, PASS_KERNEL[mode]), "tsid_set_pass_kernel")
+
+    def pass_kernels(self):
+        """Kernels of the last fit's P and Q passes: ('item' | 'slab', ...)."""
+        return tsid_fit_pass_kernels(self.ctx)
 
     def timing(self) -> dict:
         return tsid_get_timing(self.ctx)

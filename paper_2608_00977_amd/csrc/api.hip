@@ -3,6 +3,7 @@
 // pipeline.  See include/tsid.h for the contract of every entry point.
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <unordered_map>
 #include <utility>
@@ -25,6 +26,7 @@ constexpr int64_t kDefaultStage = int64_t(1) << 24;  // entries per host-to-devi
 // partial sums added) the same way whichever chunk carries it.
 constexpr int32_t kExtendE = 1024;
 constexpr int64_t kMaxEntries = (int64_t(1) << 32) - 1;
+constexpr int64_t kStreamPad = 8;
 
 bool valid_rank(int32_t k) { return k == 8 || k == 16 || k == 32 || k == 64 || k == 128; }
 
@@ -87,6 +89,19 @@ struct Plan {
     bool spans = true;             // some bucket's items span two waves (fixup needed)
 };
 
+// Slab pass of one side (fp32): slab pointers, the carry of partial sums and
+// the unit split.  `use` says whether the fit runs this side's pass with
+// the slab kernel.
+struct SlabPlan {
+    bool ready = false, use = false;
+    int32_t suits = -1;        // cached slab_suits() of the template (-1: not evaluated)
+    int32_t C = 0, n_slabs = 0, S = 0, U = 0, n_blocks = 0;
+    uint32_t *seg = nullptr;
+    float *carry = nullptr;
+    int64_t units() const { return (int64_t)n_blocks * U; }
+    int64_t lanes() const { return units() * kSlabLanes; }
+};
+
 struct Template {
     int64_t m = 0, n = 0, nnz = 0;
     int32_t m_t = 0, n_t = 0, k = 0;
@@ -96,6 +111,7 @@ struct Template {
     std::vector<int64_t> hptr[2];  // host copies of row_ptr / col_ptr
     int32_t E = 64;
     Plan plan[2][2];               // [side][precision]
+    SlabPlan slab[2];              // [side], fp32 only
 };
 
 // Epochs whose loss terms are kept before one batched reduction.
@@ -154,6 +170,8 @@ struct tsid_ctx {
     std::vector<uint8_t> launched;   // which kernel kinds each timed epoch ran
     FitBufs fb;
     ExtState ext;
+    int32_t pass_kernel = TSID_PASS_AUTO;
+    int32_t used_kernel[2] = {0, 0};  // pass kernel of each side in the last fit
 };
 
 namespace {
@@ -245,6 +263,10 @@ void free_template(tsid_ctx *c, Template *&t) {
             A.release(pl.item_end);
             A.release(pl.items);
         }
+    for (SlabPlan &sp : t->slab) {
+        A.release(sp.seg);
+        A.release(sp.carry);
+    }
     delete t;
     t = nullptr;
 }
@@ -474,7 +496,10 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
         bool in_alt = radix_sort(keys, vals, keys_alt, vals_alt, total, nbits, sort_tmp, cs);
         uint64_t *ck = in_alt ? keys_alt : keys;
         uint32_t *cv = in_alt ? vals_alt : vals;
-        t->stream_r = A.alloc<int2>(total);
+        // eight zero records after each stream: the slab pass reads whole
+        // groups of eight records
+        t->stream_r = A.alloc<int2>(total + kStreamPad);
+        TSID_HIP(hipMemsetAsync(t->stream_r + total, 0, kStreamPad * sizeof(int2), cs));
         t->row_ptr = A.alloc<int64_t>((int64_t)m_t + 1);
         keys_to_stream(ck, cv, total, bits_b, t->stream_r, c->err_dev, cs);
         ptr_from_keys(ck, total, m_t, bits_b, t->row_ptr, cs);
@@ -486,7 +511,8 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
         bool alt2 = radix_sort(ok, ov, ck, cv, total, nbits, sort_tmp, cs);
         uint64_t *tk = alt2 ? ck : ok;
         uint32_t *tv = alt2 ? cv : ov;
-        t->stream_c = A.alloc<int2>(total);
+        t->stream_c = A.alloc<int2>(total + kStreamPad);
+        TSID_HIP(hipMemsetAsync(t->stream_c + total, 0, kStreamPad * sizeof(int2), cs));
         t->col_ptr = A.alloc<int64_t>((int64_t)n_t + 1);
         keys_to_stream(tk, tv, total, bits_a, t->stream_c, c->err_dev, cs);
         ptr_from_keys(tk, total, n_t, bits_a, t->col_ptr, cs);
@@ -585,6 +611,90 @@ void ensure_plan(tsid_ctx *c, int side, int prec) {
     pl.ready = true;
 }
 
+// Whether the slab pass suits one side of the template: the expected number
+// of cells per slab row and block of owner rows (the LDS reuse of a staged
+// row) is at least 4, and no bucket is much longer than the mean, since one
+// lane walks a whole bucket.  (The item pass takes the rest.)
+#ifndef TSID_SLAB_MIN_REUSE
+#define TSID_SLAB_MIN_REUSE 4.0
+#endif
+bool slab_suits(const Template &t, int side) {
+    const int64_t rows = side ? t.n_t : t.m_t, y_rows = side ? t.m_t : t.n_t;
+    if (rows < 1 || y_rows < 1 || t.nnz < 1) return false;
+    const double density = (double)t.nnz / ((double)rows * (double)y_rows);
+    if (density * kSlabLanes < TSID_SLAB_MIN_REUSE) return false;
+    const std::vector<int64_t> &ptr = t.hptr[side];
+    int64_t maxdeg = 0;
+    for (int64_t x = 0; x < rows; ++x) maxdeg = std::max(maxdeg, ptr[(size_t)x + 1] - ptr[(size_t)x]);
+    const double mean = (double)t.nnz / (double)rows;
+    return (double)maxdeg <= 2.0 * mean + 64.0;
+}
+
+// Workgroups the slab pass aims for: one round of the compute units, with as
+// many resident workgroups per unit as its LDS holds slabs (TSID_SLAB_UNITS
+// overrides, a tuning knob).
+int64_t slab_target_units(int device) {
+    if (const char *e = std::getenv("TSID_SLAB_UNITS")) {
+        const long v = std::strtol(e, nullptr, 10);
+        if (v > 0) return v;
+    }
+    int cus = 0, lds = 0;
+    TSID_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device));
+    TSID_HIP(hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, device));
+    return (int64_t)std::max(1, cus) * std::max(1, lds / kSlabBytes);
+}
+
+// Decides (per fit, from the pass-kernel mode and the precision) whether side
+// `side` runs the slab pass, and builds its plan the first time it does.
+void ensure_slab(tsid_ctx *c, int side, int prec) {
+    Template &t = *c->tpl;
+    SlabPlan &sp = t.slab[side];
+    const int mode = c->pass_kernel;
+    bool want = false;
+    if (mode == TSID_PASS_SLAB) {
+        if (!slab_supported(t.k, prec))
+            fail(TSID_E_INVAL, "the slab pass needs fp32 factors and k in {8, 16, 32, 64}");
+        want = true;
+    } else if (mode == TSID_PASS_AUTO) {
+        if (sp.suits < 0) sp.suits = slab_supported(t.k, TSID_FP32) && slab_suits(t, side);
+        want = sp.suits == 1 && prec == TSID_FP32;
+    }
+    const int32_t rows = side ? t.n_t : t.m_t, y_rows = side ? t.m_t : t.n_t;
+    want = want && rows > 0 && y_rows > 0;  // an empty side has no cells: the item pass shrinks it
+    if (want && !sp.ready) {
+        Arena &A = c->arena;
+        hipStream_t cs = c->comp;
+        const int32_t C = slab_rows(t.k);
+        const int32_t n_slabs = std::max(1, ceil_div(y_rows, C));
+        const int32_t n_blocks = ceil_div(rows, kSlabLanes);
+        const int64_t u_target = std::max<int64_t>(1, slab_target_units(c->device) / n_blocks);
+        const int32_t S = ceil_div(n_slabs, std::min<int64_t>(u_target, n_slabs));
+        const int32_t U = ceil_div(n_slabs, S);
+        uint32_t *seg = nullptr;
+        float *carry = nullptr;
+        try {
+            seg = A.alloc<uint32_t>((int64_t)(n_slabs + 1) * rows);
+            if (U > 1) carry = A.alloc<float>((int64_t)n_blocks * U * kSlabLanes * t.k);
+            launch_slab_seg(side ? t.stream_c : t.stream_r, side ? t.col_ptr : t.row_ptr, rows, n_slabs, C,
+                            seg, cs);
+            TSID_HIP(hipStreamSynchronize(cs));
+        } catch (...) {
+            A.release(seg);
+            A.release(carry);
+            throw;
+        }
+        sp.seg = seg;
+        sp.carry = carry;
+        sp.C = C;
+        sp.n_slabs = n_slabs;
+        sp.n_blocks = n_blocks;
+        sp.S = S;
+        sp.U = U;
+        sp.ready = true;
+    }
+    sp.use = want;
+}
+
 void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs) {
     Template &t = *c->tpl;
     FitBufs &f = c->fb;
@@ -592,6 +702,8 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs) {
     const int64_t lp = (int64_t)t.m_t * t.k, lq = (int64_t)t.n_t * t.k;
     ensure_plan(c, 0, prec);
     ensure_plan(c, 1, prec);
+    ensure_slab(c, 0, prec);
+    ensure_slab(c, 1, prec);
     if (!f.P[0]) {
         for (int b = 0; b < 2; ++b) {
             f.P[b] = A.alloc<float>(lp);
@@ -601,7 +713,8 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs) {
         f.normQ = A.alloc<float>((int64_t)t.n_t * kLossRing);
         f.partial = A.alloc<double>((int64_t)reduce_scratch_elems(kLossRing));
     }
-    const int64_t need = std::max(t.plan[0][prec].n_items, t.plan[1][prec].n_items);
+    const int64_t need = std::max({(int64_t)t.plan[0][prec].n_items, (int64_t)t.plan[1][prec].n_items,
+                                   t.slab[0].use ? t.slab[0].lanes() : 0, t.slab[1].use ? t.slab[1].lanes() : 0});
     if (need > f.item_cap) {  // partial sums and per-item e^2, sized for this precision's plans
         A.release(f.carry_r);
         A.release(f.carry_c);
@@ -647,6 +760,27 @@ PassArgs pass_args(const Template &t, int side, const tsid_fit_opts &o, int32_t 
     return a;
 }
 
+SlabArgs slab_args(const Template &t, int side, const tsid_fit_opts &o, int32_t *err) {
+    const SlabPlan &sp = t.slab[side];
+    SlabArgs a{};
+    a.stream = side ? t.stream_c : t.stream_r;
+    a.seg = sp.seg;
+    a.rows = side ? t.n_t : t.m_t;
+    a.y_rows = side ? t.m_t : t.n_t;
+    a.C = sp.C;
+    a.n_slabs = sp.n_slabs;
+    a.slabs_per_unit = sp.S;
+    a.units_per_block = sp.U;
+    a.carry = sp.carry;
+    a.lam = o.lambda;
+    a.lr = o.lr;
+    a.xi = o.clip_xi;
+    a.clip = o.clip;
+    a.degree = o.step == TSID_STEP_DEGREE;
+    a.err = err;
+    return a;
+}
+
 void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_hist) {
     if (!c->tpl) fail(TSID_E_STATE, "no template: call tsid_build_template first");
     check_opts(o);
@@ -667,11 +801,16 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     TSID_HIP(hipMemsetAsync(c->err_dev, 0, ERR_SLOTS * sizeof(int32_t), cs));
     PassArgs ar = pass_args(t, 0, *o, c->err_dev), ac = pass_args(t, 1, *o, c->err_dev);
     ar.skip_after_nonfinite = ac.skip_after_nonfinite = 1;
+    SlabArgs sr = slab_args(t, 0, *o, c->err_dev), sc = slab_args(t, 1, *o, c->err_dev);
+    sr.skip_after_nonfinite = sc.skip_after_nonfinite = 1;
+    const SlabPlan &sp_r = t.slab[0], &sp_c = t.slab[1];
+    c->used_kernel[0] = sp_r.use ? TSID_PASS_SLAB : TSID_PASS_ITEM;
+    c->used_kernel[1] = sp_c.use ? TSID_PASS_SLAB : TSID_PASS_ITEM;
     if (c->timing) ensure_events(c, (size_t)T);
     // Loss terms of epoch ep go to ring slot ep % kLossRing; a full ring (and
     // the end of the fit) is reduced in one batch into f.loss.
     const bool want_loss = loss_hist != nullptr;
-    const int64_t ne = t.plan[0][prec].n_items;
+    const int64_t ne = sp_r.use ? sp_r.lanes() : t.plan[0][prec].n_items;
     int pend = 0;  // first epoch whose loss is not reduced yet
     auto flush = [&](int upto, std::pair<hipEvent_t, hipEvent_t> ev) {
         launch_loss_reduce(f.e2, f.item_cap, ne, f.normP, t.m_t, f.normQ, t.n_t, o->lambda, upto - pend,
@@ -680,47 +819,89 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     };
     for (int ep = 0; ep < T; ++ep) {
         const int cur = ep & 1, nxt = cur ^ 1, slot = ep % kLossRing;
-        ar.epoch = ac.epoch = ep;
         // P pass (CSR): owner P_t, gathered Q_t
-        ar.X = f.P[cur];
-        ar.Y = prec ? (const void *)f.Qb[cur] : (const void *)f.Q[cur];
-        ar.Xn = f.P[nxt];
-        ar.Xn_b = prec ? f.Pb[nxt] : nullptr;
-        ar.carry = f.carry_r;
-        ar.e2 = want_loss ? f.e2 + slot * f.item_cap : nullptr;
-        ar.norm = want_loss ? f.normP + (int64_t)slot * t.m_t : nullptr;
+        float *e2 = want_loss ? f.e2 + slot * f.item_cap : nullptr;
+        float *normp = want_loss ? f.normP + (int64_t)slot * t.m_t : nullptr;
         auto ev = timed(c, ep, TK_PPASS);
-        launch_item_pass(K, prec, false, ar, cs, ev.first, ev.second);
-        if (t.plan[0][prec].spans) {
-            ev = timed(c, ep, TK_PFIX);
-            launch_fixup(K, prec, ar, cs, ev.first, ev.second);
+        if (sp_r.use) {
+            sr.epoch = ep;
+            sr.X = f.P[cur];
+            sr.Y = f.Q[cur];
+            sr.Xn = f.P[nxt];
+            sr.e2 = e2;
+            sr.norm = normp;
+            launch_slab_pass(K, false, sr, sp_r.units(), cs, ev.first, ev.second);
+            if (sp_r.U > 1) {
+                ev = timed(c, ep, TK_PFIX);
+                launch_slab_finish(K, sr, cs, ev.first, ev.second);
+            }
+        } else {
+            ar.epoch = ep;
+            ar.X = f.P[cur];
+            ar.Y = prec ? (const void *)f.Qb[cur] : (const void *)f.Q[cur];
+            ar.Xn = f.P[nxt];
+            ar.Xn_b = prec ? f.Pb[nxt] : nullptr;
+            ar.carry = f.carry_r;
+            ar.e2 = e2;
+            ar.norm = normp;
+            launch_item_pass(K, prec, false, ar, cs, ev.first, ev.second);
+            if (t.plan[0][prec].spans) {
+                ev = timed(c, ep, TK_PFIX);
+                launch_fixup(K, prec, ar, cs, ev.first, ev.second);
+            }
         }
         // Q pass (CSC): owner Q_t, gathered P_t (the old P: a simultaneous step)
-        ac.X = f.Q[cur];
-        ac.Y = prec ? (const void *)f.Pb[cur] : (const void *)f.P[cur];
-        ac.Xn = f.Q[nxt];
-        ac.Xn_b = prec ? f.Qb[nxt] : nullptr;
-        ac.carry = f.carry_c;
-        ac.e2 = nullptr;
-        ac.norm = want_loss ? f.normQ + (int64_t)slot * t.n_t : nullptr;
+        float *normq = want_loss ? f.normQ + (int64_t)slot * t.n_t : nullptr;
         ev = timed(c, ep, TK_QPASS);
-        launch_item_pass(K, prec, false, ac, cs, ev.first, ev.second);
-        if (t.plan[1][prec].spans) {
-            ev = timed(c, ep, TK_QFIX);
-            launch_fixup(K, prec, ac, cs, ev.first, ev.second);
+        if (sp_c.use) {
+            sc.epoch = ep;
+            sc.X = f.Q[cur];
+            sc.Y = f.P[cur];
+            sc.Xn = f.Q[nxt];
+            sc.e2 = nullptr;
+            sc.norm = normq;
+            launch_slab_pass(K, false, sc, sp_c.units(), cs, ev.first, ev.second);
+            if (sp_c.U > 1) {
+                ev = timed(c, ep, TK_QFIX);
+                launch_slab_finish(K, sc, cs, ev.first, ev.second);
+            }
+        } else {
+            ac.epoch = ep;
+            ac.X = f.Q[cur];
+            ac.Y = prec ? (const void *)f.Pb[cur] : (const void *)f.P[cur];
+            ac.Xn = f.Q[nxt];
+            ac.Xn_b = prec ? f.Qb[nxt] : nullptr;
+            ac.carry = f.carry_c;
+            ac.e2 = nullptr;
+            ac.norm = normq;
+            launch_item_pass(K, prec, false, ac, cs, ev.first, ev.second);
+            if (t.plan[1][prec].spans) {
+                ev = timed(c, ep, TK_QFIX);
+                launch_fixup(K, prec, ac, cs, ev.first, ev.second);
+            }
         }
         if (want_loss && slot == kLossRing - 1) flush(ep + 1, timed(c, ep, TK_REDUCE));
     }
     const int fin = T & 1;
     if (want_loss) {  // L(P_T, Q_T), then the epochs not reduced yet
         const int slot = T % kLossRing;
-        ar.epoch = T;
-        ar.X = f.P[fin];
-        ar.Y = prec ? (const void *)f.Qb[fin] : (const void *)f.Q[fin];
-        ar.Xn = nullptr;
-        ar.e2 = f.e2 + slot * f.item_cap;
-        ar.norm = f.normP + (int64_t)slot * t.m_t;
-        launch_item_pass(K, prec, true, ar, cs);
+        if (sp_r.use) {
+            sr.epoch = T;
+            sr.X = f.P[fin];
+            sr.Y = f.Q[fin];
+            sr.Xn = nullptr;
+            sr.e2 = f.e2 + slot * f.item_cap;
+            sr.norm = f.normP + (int64_t)slot * t.m_t;
+            launch_slab_pass(K, true, sr, sp_r.units(), cs);
+        } else {
+            ar.epoch = T;
+            ar.X = f.P[fin];
+            ar.Y = prec ? (const void *)f.Qb[fin] : (const void *)f.Q[fin];
+            ar.Xn = nullptr;
+            ar.e2 = f.e2 + slot * f.item_cap;
+            ar.norm = f.normP + (int64_t)slot * t.m_t;
+            launch_item_pass(K, prec, true, ar, cs);
+        }
         launch_row_norms(K, f.Q[fin], t.n_t, f.normQ + (int64_t)slot * t.n_t, cs);
         flush(T + 1, {nullptr, nullptr});
     }
@@ -1044,6 +1225,21 @@ tsid_status tsid_template_info(const tsid_ctx *c, int32_t *m_t, int32_t *n_t, in
 tsid_status tsid_fit_template(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *opts,
                               double *loss_hist) {
     return guarded(c, [&]() { fit(c, P, Q, opts, loss_hist); });
+}
+
+tsid_status tsid_set_pass_kernel(tsid_ctx *c, int mode) {
+    return guarded(c, [&]() {
+        if (mode != TSID_PASS_AUTO && mode != TSID_PASS_ITEM && mode != TSID_PASS_SLAB)
+            fail(TSID_E_INVAL, "unknown pass kernel mode");
+        c->pass_kernel = mode;
+    });
+}
+
+tsid_status tsid_fit_pass_kernels(const tsid_ctx *c, int32_t *p_pass, int32_t *q_pass) {
+    if (!c) return TSID_E_INVAL;
+    if (p_pass) *p_pass = c->used_kernel[0];
+    if (q_pass) *q_pass = c->used_kernel[1];
+    return TSID_OK;
 }
 
 tsid_status tsid_set_timing(tsid_ctx *c, int enable) {

@@ -135,4 +135,51 @@ void launch_loss_reduce(const float *e2, int64_t e2_stride, int64_t ne, const fl
                         double *out, const int32_t *err, int32_t epoch0, hipStream_t s,
                         hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
+// ------------------------------------------------------------- slab pass
+// Owner rows per workgroup (one lane each) and LDS bytes of one slab of the
+// gathered factor.
+#ifndef TSID_SLAB_LANES
+#define TSID_SLAB_LANES 512
+#endif
+#ifndef TSID_SLAB_KIB
+#define TSID_SLAB_KIB 128
+#endif
+constexpr int kSlabLanes = TSID_SLAB_LANES;
+constexpr int kSlabBytes = TSID_SLAB_KIB * 1024;
+
+struct SlabArgs {
+    const int2 *stream;      // bucketed cells {other id, value bits}, padded by 8 records
+    const uint32_t *seg;     // seg[s * rows + x]: first cell of bucket x with other id >= s * C
+    int32_t rows;            // owner rows (buckets)
+    int32_t y_rows;          // rows of the gathered factor
+    int32_t C;               // gathered rows per slab
+    int32_t n_slabs;         // ceil(y_rows / C)
+    int32_t slabs_per_unit;  // S: slabs one workgroup walks
+    int32_t units_per_block; // U = ceil(n_slabs / S): workgroups per block of kSlabLanes rows
+    const float *X;          // owner factors (rows x K)
+    const float *Y;          // gathered factors (y_rows x K)
+    float *Xn;               // updated owner factors
+    float *carry;            // partial sums, [units][kSlabLanes][K] (U > 1)
+    float *e2;               // per-lane residual sum of squares [units * kSlabLanes], or null
+    float *norm;             // per-row ||x||^2 of the owner rows, or null
+    float lam, lr, xi;
+    int32_t clip, degree;
+    int32_t *err;
+    int32_t epoch;
+    int32_t skip_after_nonfinite;
+};
+
+// fp32 factors with k in {8, 16, 32, 64}.
+bool slab_supported(int K, int prec);
+int slab_rows(int K);  // C for rank K
+void launch_slab_seg(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_slabs, int32_t C,
+                     uint32_t *seg, hipStream_t s);
+// The pass over n_units workgroups.  With U == 1 it updates the rows itself;
+// with U > 1 (and not loss-only) launch_slab_finish then adds each row's U
+// partial sums and updates it.
+void launch_slab_pass(int K, bool loss_only, const SlabArgs &a, int64_t n_units, hipStream_t s,
+                      hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+void launch_slab_finish(int K, const SlabArgs &a, hipStream_t s, hipEvent_t ev0 = nullptr,
+                        hipEvent_t ev1 = nullptr);
+
 }  // namespace tsid

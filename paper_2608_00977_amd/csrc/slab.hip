@@ -1,0 +1,416 @@
+// Slab pass of the template fit (Stage I, Section 5.1) for templates whose
+// observed cells are spread evenly over the template (uniform sampling, as in
+// the scientific-data workloads).  Per observed cell it computes the residual
+// e = r - p_a . q_b, aggregates the per-cell gradients of Eqs. 3-4 into the
+// owning factor row and applies the row update of Eq. 5 (with the clip of
+// Section 5.3), exactly as the item pass does; only the mapping differs.
+//
+// Mapping (gfx950, wave64, workgroups of kSlabLanes = 512 lanes, one per
+// compute unit):
+//  * One lane owns one factor row: a block of 512 consecutive owner rows per
+//    workgroup.  The lane keeps the row and its gradient sum in registers for
+//    the whole pass, so a cell costs k fused multiply-adds for the dot
+//    product and k for the gradient, with no cross-lane reduction.
+//  * The gathered factor is cut into slabs of C rows (128 KiB each).  The
+//    workgroup copies one slab at a time into LDS with coalesced loads, then
+//    every lane walks the cells of its row whose other index lies in the slab
+//    (a contiguous run of the bucketed stream, located by the slab pointers
+//    seg[s][x]) and reads the other factor rows from LDS.  A slab row is read
+//    by every owner row of the block that observes it, so the gathers leave
+//    the cache hierarchy and cost LDS bandwidth only.  A wave runs as long as
+//    its busiest lane, so slabs are as large as LDS allows: the longer each
+//    lane's run per slab, the smaller the relative spread between lanes.
+//  * Lanes read the 16-byte chunks of an LDS row in an order rotated by their
+//    lane id, so the eight lanes served together touch eight different bank
+//    groups whatever rows they read; the owner row and the gradient sum are
+//    held in the same rotated order, which costs nothing.
+//  * A workgroup covers a range of S slabs.  When a block of rows is split
+//    over several workgroups (U > 1) each leaves its partial gradient sums in
+//    a carry buffer, and a second kernel adds the U parts of every row in a
+//    fixed order and updates the row.  No atomic operation is used, and the
+//    result does not depend on the order in which workgroups run.
+#include <hip/hip_ext.h>
+
+#include "internal.h"
+
+namespace tsid {
+
+namespace {
+
+constexpr int kLanes = kSlabLanes;
+
+// Cells whose gathered rows are read before their arithmetic (a scheduling
+// group), and the waves per SIMD the register budget must allow (LDS allows
+// 160 KiB / slab bytes workgroups of four waves per compute unit).
+#ifndef TSID_SLAB_GROUP
+#define TSID_SLAB_GROUP 2
+#endif
+#ifndef TSID_SLAB_WAVES_PER_EU
+#define TSID_SLAB_WAVES_PER_EU 2
+#endif
+// Dependency chains of the dot product (1: one chain of k fused multiply-adds).
+#ifndef TSID_SLAB_CHAINS
+#define TSID_SLAB_CHAINS 4
+#endif
+
+__device__ __forceinline__ float4 f4_zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+
+// Chunk of the row held in register slot c of this lane (rotation by lane id;
+// NCH is a power of two).
+template <int NCH>
+__device__ __forceinline__ int slot_chunk(int c, int rot) {
+    return (c + rot) & (NCH - 1);
+}
+
+// Eq. 5 (descent on the summed gradients of Eqs. 3-4), the 1/max(1, deg)
+// normalisation of the degree step and the Section 5.3 clip, for one row held
+// by one lane in rotated chunk order.
+template <int K>
+__device__ __forceinline__ void finalize_lane(const SlabArgs &A, int xr, int rot,
+                                              const float4 (&x)[K / 4], const float4 (&acc)[K / 4]) {
+    constexpr int NCH = K / 4;
+    const uint32_t deg = A.seg[(int64_t)A.n_slabs * A.rows + xr] - A.seg[xr];
+    const float s = A.degree ? 1.0f / (float)(deg > 1 ? deg : 1) : 1.0f;
+    float4 *out = reinterpret_cast<float4 *>(A.Xn + (int64_t)xr * K);
+    bool bad = false;
+    float nrm = 0.f;
+    auto upd = [&](float xv, float av) {
+        const float g = 2.0f * A.lam * xv - 2.0f * av;
+        float d = -s * g;
+        if (A.clip && d > A.xi) d = A.xi;
+        const float xn = xv + A.lr * d;
+        bad |= !__builtin_isfinite(xn);
+        nrm += xv * xv;
+        return xn;
+    };
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        float4 o;
+        o.x = upd(x[c].x, acc[c].x);
+        o.y = upd(x[c].y, acc[c].y);
+        o.z = upd(x[c].z, acc[c].z);
+        o.w = upd(x[c].w, acc[c].w);
+        out[slot_chunk<NCH>(c, rot)] = o;
+    }
+    if (A.norm) A.norm[xr] = nrm;
+    if (bad) A.err[ERR_NONFINITE] = A.epoch + 1;
+}
+
+// Eight consecutive stream records starting at p (the stream is padded by
+// eight records, so the read never leaves the buffer).
+__device__ __forceinline__ void load8(const int2 *p, int2 (&r)[8]) {
+#pragma unroll
+    for (int c = 0; c < 8; ++c) r[c] = p[c];
+}
+
+// The cells at stream positions j .. j+7 of this lane's run [.., q) in slab
+// rows sbase .. sbase + C - 1: residuals against the LDS rows, e^2 and the
+// gradient sums.  Records at or past q belong to other rows or slabs: their
+// LDS row is replaced by row 0 and their residual by 0 (bit masks, so the
+// work stays branch-free).
+template <int K, bool LOSS_ONLY>
+__device__ __forceinline__ void slab_burst(const int2 (&rec)[8], uint32_t j, uint32_t q, int32_t sbase,
+                                           const char *ysb, const uint32_t (&koff)[K / 4],
+                                           const float4 (&x)[K / 4], float4 (&acc)[K / 4], float &e2) {
+    constexpr int NCH = K / 4;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+        // at most TSID_SLAB_GROUP cells' rows in flight: bounds the registers
+        if (c % TSID_SLAB_GROUP == 0 && c > 0) __builtin_amdgcn_sched_barrier(0);
+        const uint32_t keep = j + c < q ? 0xffffffffu : 0u;
+        const uint32_t row_off = ((uint32_t)(rec[c].x - sbase) * (uint32_t)(K * 4)) & keep;
+        float4 y[NCH];
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) y[i] = *reinterpret_cast<const float4 *>(ysb + row_off + koff[i]);
+#if TSID_SLAB_CHAINS == 1
+        float d = 0.f;
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+            d += x[i].x * y[i].x;
+            d += x[i].y * y[i].y;
+            d += x[i].z * y[i].z;
+            d += x[i].w * y[i].w;
+        }
+#else
+        float d0 = 0.f, d1 = 0.f, d2 = 0.f, d3 = 0.f;
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+            d0 += x[i].x * y[i].x;
+            d1 += x[i].y * y[i].y;
+            d2 += x[i].z * y[i].z;
+            d3 += x[i].w * y[i].w;
+        }
+        const float d = (d0 + d1) + (d2 + d3);
+#endif
+        const float e = __uint_as_float(__float_as_uint(__int_as_float(rec[c].y) - d) & keep);
+        e2 += e * e;
+        if constexpr (!LOSS_ONLY) {
+#pragma unroll
+            for (int i = 0; i < NCH; ++i) {
+                acc[i].x += e * y[i].x;
+                acc[i].y += e * y[i].y;
+                acc[i].z += e * y[i].z;
+                acc[i].w += e * y[i].w;
+            }
+        }
+    }
+}
+
+template <int K, bool LOSS_ONLY>
+__global__ __launch_bounds__(kLanes) __attribute__((amdgpu_waves_per_eu(TSID_SLAB_WAVES_PER_EU)))
+void k_slab_pass(const SlabArgs A) {
+    constexpr int NCH = K / 4;                        // 16-byte chunks per factor row
+    constexpr int RM = (NCH < 8 ? NCH : 8) - 1;       // lane rotation mask
+    static_assert((NCH & (NCH - 1)) == 0, "rows hold a power-of-two number of chunks");
+    extern __shared__ float4 ys[];                    // one slab: C rows x NCH chunks
+    if (A.skip_after_nonfinite) {
+        const int32_t f = A.err[ERR_NONFINITE];
+        if (f != 0 && f - 1 < A.epoch) return;  // same outcome for every workgroup
+    }
+    const int tid = threadIdx.x;
+    const int u = blockIdx.x;
+    const int U = A.units_per_block;
+    const int blk = u / U, ur = u - blk * U;
+    const int s0 = ur * A.slabs_per_unit;
+    const int s1 = min(s0 + A.slabs_per_unit, A.n_slabs);
+    const int xr = blk * kLanes + tid;
+    const bool own = xr < A.rows;
+    const int rot = tid & RM;
+
+    float4 x[NCH], acc[NCH];
+    uint32_t koff[NCH];  // byte offset of slot c's chunk within an LDS row
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        koff[c] = (uint32_t)slot_chunk<NCH>(c, rot) * 16u;
+        x[c] = own ? reinterpret_cast<const float4 *>(A.X + (int64_t)xr * K)[slot_chunk<NCH>(c, rot)]
+                   : f4_zero();
+        acc[c] = f4_zero();
+    }
+    float e2 = 0.f;
+
+    const float4 *Y4 = reinterpret_cast<const float4 *>(A.Y);
+    constexpr int nf4 = kSlabBytes / 16;              // chunks per slab (a multiple of 4 * kLanes)
+    static_assert(nf4 % (4 * kLanes) == 0, "the slab fill takes whole rounds");
+    const int64_t ylast = (int64_t)A.y_rows * NCH - 1;  // last chunk of the table
+    const char *ysb = reinterpret_cast<const char *>(ys);
+    for (int s = s0; s < s1; ++s) {
+        __syncthreads();  // every lane is done with the previous slab
+        // Chunks past the table's end (last slab only) repeat its last chunk;
+        // no cell refers to those LDS rows.
+        const int64_t g0 = (int64_t)s * nf4;
+#pragma unroll
+        for (int i = tid; i < nf4; i += 4 * kLanes) {
+            float4 t[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int64_t g = g0 + i + q * kLanes;
+                t[q] = Y4[g < ylast ? g : ylast];
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) ys[i + q * kLanes] = t[q];
+        }
+        __syncthreads();
+        uint32_t p = 0, q = 0;
+        if (own) {
+            p = A.seg[(int64_t)s * A.rows + xr];
+            q = A.seg[(int64_t)(s + 1) * A.rows + xr];
+        }
+        const int32_t sbase = s * A.C;
+        // The lane's cells in this slab, eight records per burst; the next
+        // burst's records load while this one computes.
+        int2 ra[8], rc[8];
+        if (p < q) load8(A.stream + p, ra);
+        for (uint32_t j = p; j < q; j += 16) {
+            if (j + 8 < q) load8(A.stream + j + 8, rc);
+            slab_burst<K, LOSS_ONLY>(ra, j, q, sbase, ysb, koff, x, acc, e2);
+            if (j + 8 >= q) break;
+            if (j + 16 < q) load8(A.stream + j + 16, ra);
+            slab_burst<K, LOSS_ONLY>(rc, j + 8, q, sbase, ysb, koff, x, acc, e2);
+        }
+    }
+
+    if (A.e2) A.e2[(int64_t)u * kLanes + tid] = e2;
+    if constexpr (LOSS_ONLY) {
+        if (A.norm && own && ur == 0) {
+            float nrm = 0.f;
+#pragma unroll
+            for (int c = 0; c < NCH; ++c)
+                nrm += x[c].x * x[c].x + x[c].y * x[c].y + x[c].z * x[c].z + x[c].w * x[c].w;
+            A.norm[xr] = nrm;
+        }
+    } else {
+        if (U == 1) {
+            if (own) finalize_lane<K>(A, xr, rot, x, acc);
+            return;
+        }
+        // Partial sums of this unit (natural chunk order); k_slab_finish adds
+        // the U parts of each row in unit order and updates the row.
+        if (own) {
+            float4 *cp = reinterpret_cast<float4 *>(A.carry + ((int64_t)u * kLanes + tid) * K);
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) cp[slot_chunk<NCH>(c, rot)] = acc[c];
+        }
+    }
+}
+
+// Blocks split over U > 1 workgroups: the U partial sums of every row are
+// added in unit order, then the row takes the update of Eq. 5.  One lane per
+// 16-byte chunk of a row (NCH consecutive lanes per row), so every load is
+// coalesced and all U loads of a lane are in flight together.
+template <int K>
+__global__ __launch_bounds__(256) void k_slab_finish(const SlabArgs A) {
+    constexpr int NCH = K / 4;
+    static_assert(NCH <= 64 && (64 % NCH) == 0, "a row's lanes sit inside one wave");
+    if (A.skip_after_nonfinite) {
+        const int32_t f = A.err[ERR_NONFINITE];
+        if (f != 0 && f - 1 < A.epoch) return;
+    }
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t xr = t / NCH;
+    const int ch = (int)(t % NCH);
+    const bool own = xr < A.rows;
+    const int64_t xs = own ? xr : 0;  // rows past the end mirror row 0 and store nothing
+    const int U = A.units_per_block;
+    const int64_t blk = xs / kLanes, lane = xs % kLanes;
+    const float4 *cp = reinterpret_cast<const float4 *>(A.carry) + ((blk * U) * kLanes + lane) * NCH + ch;
+    const int64_t unit_stride = (int64_t)kLanes * NCH;  // float4 between consecutive units
+    float4 tot = f4_zero();
+    int v = 0;
+    for (; v + 4 <= U; v += 4) {
+        float4 q[4];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) q[w] = cp[(v + w) * unit_stride];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            tot.x += q[w].x;
+            tot.y += q[w].y;
+            tot.z += q[w].z;
+            tot.w += q[w].w;
+        }
+    }
+    for (; v < U; ++v) {
+        const float4 q = cp[v * unit_stride];
+        tot.x += q.x;
+        tot.y += q.y;
+        tot.z += q.z;
+        tot.w += q.w;
+    }
+    const float4 x = reinterpret_cast<const float4 *>(A.X + xs * K)[ch];
+    const uint32_t deg = A.seg[(int64_t)A.n_slabs * A.rows + xs] - A.seg[xs];
+    const float s = A.degree ? 1.0f / (float)(deg > 1 ? deg : 1) : 1.0f;
+    bool bad = false;
+    float nrm = 0.f;
+    auto upd = [&](float xv, float av) {
+        const float g = 2.0f * A.lam * xv - 2.0f * av;
+        float d = -s * g;
+        if (A.clip && d > A.xi) d = A.xi;
+        const float xn = xv + A.lr * d;
+        bad |= !__builtin_isfinite(xn);
+        nrm += xv * xv;
+        return xn;
+    };
+    float4 o;
+    o.x = upd(x.x, tot.x);
+    o.y = upd(x.y, tot.y);
+    o.z = upd(x.z, tot.z);
+    o.w = upd(x.w, tot.w);
+    // row norm over the NCH lanes of the row (butterfly: every lane ends with
+    // the same bits)
+#pragma unroll
+    for (int off = 1; off < NCH; off <<= 1) nrm += __shfl_xor(nrm, off, 64);
+    if (own) {
+        reinterpret_cast<float4 *>(A.Xn + xr * K)[ch] = o;
+        if (A.norm && ch == 0) A.norm[xr] = nrm;
+        if (bad) A.err[ERR_NONFINITE] = A.epoch + 1;
+    }
+}
+
+// seg[s * rows + x] = first cell of bucket x whose other index is >= s * C
+// (binary search in the bucket's sorted other indices), s = 0..n_slabs.
+__global__ void k_slab_seg(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_slabs,
+                           int32_t C, uint32_t *seg) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (int64_t)(n_slabs + 1) * rows) return;
+    const int32_t s = (int32_t)(t / rows), x = (int32_t)(t % rows);
+    const int64_t key = (int64_t)s * C;
+    int64_t lo = ptr[x], hi = ptr[x + 1];
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if ((int64_t)stream[mid].x < key) lo = mid + 1;
+        else hi = mid;
+    }
+    seg[t] = (uint32_t)lo;
+}
+
+// Slabs above 64 KiB need the kernel's dynamic LDS limit raised (once).
+template <typename Kern>
+void allow_lds(Kern kernel, size_t bytes) {
+    if (bytes > 64 * 1024)
+        TSID_HIP(hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes));
+}
+
+template <int K>
+void slab_pass_k(bool loss_only, const SlabArgs &a, int64_t n_units, hipStream_t s, hipEvent_t ev0,
+                 hipEvent_t ev1) {
+    const size_t lds = (size_t)a.C * K * 4;
+    static const bool lds_ok = (allow_lds(k_slab_pass<K, true>, kSlabBytes),
+                                allow_lds(k_slab_pass<K, false>, kSlabBytes), true);
+    (void)lds_ok;
+    if (loss_only)
+        hipExtLaunchKernelGGL(k_slab_pass<K, true>, dim3((unsigned)n_units), dim3(kLanes), lds, s, ev0, ev1,
+                              0, a);
+    else
+        hipExtLaunchKernelGGL(k_slab_pass<K, false>, dim3((unsigned)n_units), dim3(kLanes), lds, s, ev0,
+                              ev1, 0, a);
+    TSID_HIP(hipGetLastError());
+}
+
+template <int K>
+void slab_finish_k(const SlabArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+    const int64_t threads = (int64_t)a.rows * (K / 4);
+    const unsigned blocks = (unsigned)((threads + 255) / 256);
+    hipExtLaunchKernelGGL(k_slab_finish<K>, dim3(blocks), dim3(256), 0, s, ev0, ev1, 0, a);
+    TSID_HIP(hipGetLastError());
+}
+
+}  // namespace
+
+bool slab_supported(int K, int prec) {
+    return prec == TSID_FP32 && (K == 8 || K == 16 || K == 32 || K == 64);
+}
+
+int slab_rows(int K) { return kSlabBytes / (4 * K); }
+
+void launch_slab_seg(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_slabs, int32_t C,
+                     uint32_t *seg, hipStream_t s) {
+    const int64_t n = (int64_t)(n_slabs + 1) * rows;
+    if (n <= 0) return;
+    k_slab_seg<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(stream, ptr, rows, n_slabs, C, seg);
+    TSID_HIP(hipGetLastError());
+}
+
+void launch_slab_finish(int K, const SlabArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+    if (a.rows <= 0) return;
+    switch (K) {
+        case 8: slab_finish_k<8>(a, s, ev0, ev1); break;
+        case 16: slab_finish_k<16>(a, s, ev0, ev1); break;
+        case 32: slab_finish_k<32>(a, s, ev0, ev1); break;
+        case 64: slab_finish_k<64>(a, s, ev0, ev1); break;
+        default: fail(TSID_E_INVAL, "the slab pass supports k = 8, 16, 32, 64");
+    }
+}
+
+void launch_slab_pass(int K, bool loss_only, const SlabArgs &a, int64_t n_units, hipStream_t s,
+                      hipEvent_t ev0, hipEvent_t ev1) {
+    if (n_units <= 0) return;
+    switch (K) {
+        case 8: slab_pass_k<8>(loss_only, a, n_units, s, ev0, ev1); break;
+        case 16: slab_pass_k<16>(loss_only, a, n_units, s, ev0, ev1); break;
+        case 32: slab_pass_k<32>(loss_only, a, n_units, s, ev0, ev1); break;
+        case 64: slab_pass_k<64>(loss_only, a, n_units, s, ev0, ev1); break;
+        default: fail(TSID_E_INVAL, "the slab pass supports k = 8, 16, 32, 64");
+    }
+}
+
+}  // namespace tsid
