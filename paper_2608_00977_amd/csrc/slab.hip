@@ -189,37 +189,42 @@ void k_slab_pass(const SlabArgs A) {
     float e2 = 0.f;
 
     const float4 *Y4 = reinterpret_cast<const float4 *>(A.Y);
-    constexpr int nf4 = kSlabBytes / 16;              // chunks per slab (a multiple of 4 * kLanes)
-    static_assert(nf4 % (4 * kLanes) == 0, "the slab fill takes whole rounds");
+    constexpr int nf4 = kSlabBytes / 16;              // chunks per slab
+    static_assert(nf4 % kLanes == 0, "every lane copies the same number of chunks");
     const int64_t ylast = (int64_t)A.y_rows * NCH - 1;  // last chunk of the table
     const char *ysb = reinterpret_cast<const char *>(ys);
+    constexpr int NF = nf4 / kLanes;  // slab chunks each lane copies
+    // LDS byte address of this wave's first chunk in each copy round: the
+    // direct global-to-LDS loads write 16 bytes per lane at consecutive
+    // addresses from a wave-uniform base.
+    const int wave_base = __builtin_amdgcn_readfirstlane(tid & ~63);
     for (int s = s0; s < s1; ++s) {
-        __syncthreads();  // every lane is done with the previous slab
-        // Chunks past the table's end (last slab only) repeat its last chunk;
-        // no cell refers to those LDS rows.
-        const int64_t g0 = (int64_t)s * nf4;
-#pragma unroll
-        for (int i = tid; i < nf4; i += 4 * kLanes) {
-            float4 t[4];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int64_t g = g0 + i + q * kLanes;
-                t[q] = Y4[g < ylast ? g : ylast];
-            }
-#pragma unroll
-            for (int q = 0; q < 4; ++q) ys[i + q * kLanes] = t[q];
-        }
-        __syncthreads();
+        // The lane's run bounds and its first records are requested before
+        // the barrier, the slab right after it with every copy in flight, so
+        // the workgroup waits for about one memory round trip per slab.
         uint32_t p = 0, q = 0;
         if (own) {
             p = A.seg[(int64_t)s * A.rows + xr];
             q = A.seg[(int64_t)(s + 1) * A.rows + xr];
         }
+        int2 ra[8], rc[8];
+        if (p < q) load8(A.stream + p, ra);
+        __syncthreads();  // every lane is done with the previous slab
+        // Chunks past the table's end (last slab only) repeat its last chunk;
+        // no cell refers to those LDS rows.
+        const int64_t g0 = (int64_t)s * nf4 + tid;
+#pragma unroll
+        for (int f = 0; f < NF; ++f) {
+            const int64_t g = g0 + (int64_t)f * kLanes;
+            __builtin_amdgcn_global_load_lds(Y4 + (g < ylast ? g : ylast),
+                                             (__attribute__((address_space(3))) void *)(ys + f * kLanes + wave_base),
+                                             16, 0, 0);
+        }
+        __builtin_amdgcn_s_waitcnt(0);  // the copies have landed in LDS
+        __syncthreads();
         const int32_t sbase = s * A.C;
         // The lane's cells in this slab, eight records per burst; the next
         // burst's records load while this one computes.
-        int2 ra[8], rc[8];
-        if (p < q) load8(A.stream + p, ra);
         for (uint32_t j = p; j < q; j += 16) {
             if (j + 8 < q) load8(A.stream + j + 8, rc);
             slab_burst<K, LOSS_ONLY>(ra, j, q, sbase, ysb, koff, x, acc, e2);
