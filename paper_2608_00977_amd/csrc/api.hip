@@ -22,9 +22,6 @@ void hip_check(hipError_t e, const char *what) {
 namespace {
 
 constexpr int64_t kDefaultStage = int64_t(1) << 24;  // entries per host-to-device piece
-// Extension items hold a fixed number of cells, so a free row is cut (and its
-// partial sums added) the same way whichever chunk carries it.
-constexpr int32_t kExtendE = 1024;
 constexpr int64_t kMaxEntries = (int64_t(1) << 32) - 1;
 constexpr int64_t kStreamPad = 8;
 
@@ -130,21 +127,18 @@ struct FitBufs {
 struct ExtSlot {
     int32_t *fid = nullptr, *free_id = nullptr;
     float *r = nullptr;
-    float *X[2] = {nullptr, nullptr};
+    float *X = nullptr;  // the chunk's free rows after the last step
     hipEvent_t ev_h2d = nullptr, ev_staged = nullptr, ev_done = nullptr, ev_flushed = nullptr;
 };
 
 struct ExtState {
     int64_t cap_nnz = 0;
-    int32_t cap_free = 0, cap_items = 0, k = 0;
+    int32_t cap_free = 0, k = 0;
     ExtSlot slot[2];
     uint64_t *keys = nullptr, *keys_alt = nullptr;
     uint32_t *vals = nullptr, *vals_alt = nullptr, *sort_scratch = nullptr;
     int2 *stream = nullptr;
     int64_t *ptr = nullptr;
-    uint32_t *nparts = nullptr, *scan_scratch = nullptr, *item_off = nullptr;
-    int32_t *items = nullptr;
-    float *carry = nullptr;
     int32_t *err = nullptr;
     int next = 0;
     bool pending = false;
@@ -299,8 +293,7 @@ void free_ext_buffers(tsid_ctx *c) {
         A.release(s.fid);
         A.release(s.free_id);
         A.release(s.r);
-        A.release(s.X[0]);
-        A.release(s.X[1]);
+        A.release(s.X);
     }
     A.release(x.keys);
     A.release(x.keys_alt);
@@ -309,14 +302,8 @@ void free_ext_buffers(tsid_ctx *c) {
     A.release(x.sort_scratch);
     A.release(x.stream);
     A.release(x.ptr);
-    A.release(x.nparts);
-    A.release(x.scan_scratch);
-    A.release(x.item_off);
-    A.release(x.items);
-    A.release(x.carry);
     x.cap_nnz = 0;
     x.cap_free = 0;
-    x.cap_items = 0;
     x.k = 0;
 }
 
@@ -958,7 +945,7 @@ void ext_sync_all(tsid_ctx *c) {
     TSID_HIP(hipStreamSynchronize(c->d2h));
 }
 
-void ext_ensure(tsid_ctx *c, int64_t nnz, int32_t n_free, int32_t items_bound, int32_t k) {
+void ext_ensure(tsid_ctx *c, int64_t nnz, int32_t n_free, int32_t k) {
     ExtState &x = c->ext;
     Arena &A = c->arena;
     if (!x.slot[0].ev_h2d) {
@@ -971,11 +958,10 @@ void ext_ensure(tsid_ctx *c, int64_t nnz, int32_t n_free, int32_t items_bound, i
         x.err = A.alloc<int32_t>(ERR_SLOTS);
         TSID_HIP(hipMemsetAsync(x.err, 0, ERR_SLOTS * 4, c->comp));
     }
-    if (nnz <= x.cap_nnz && n_free <= x.cap_free && items_bound <= x.cap_items && k == x.k) return;
+    if (nnz <= x.cap_nnz && n_free <= x.cap_free && k == x.k) return;
     ext_sync_all(c);  // buffers may be in use by earlier chunks
     const int64_t cn = std::max<int64_t>({nnz, x.cap_nnz + x.cap_nnz / 2, 1024});
     const int32_t cf = (int32_t)std::min<int64_t>(std::max<int64_t>({(int64_t)n_free, (int64_t)x.cap_free + x.cap_free / 2, 64}), INT32_MAX - 1);
-    const int32_t ci = (int32_t)std::min<int64_t>(std::max<int64_t>({(int64_t)items_bound, (int64_t)x.cap_items + x.cap_items / 2, 64}), INT32_MAX - 1);
     int32_t *err_keep = x.err;
     x.err = nullptr;
     free_ext_buffers(c);
@@ -984,8 +970,7 @@ void ext_ensure(tsid_ctx *c, int64_t nnz, int32_t n_free, int32_t items_bound, i
         s.fid = A.alloc<int32_t>(cn);
         s.free_id = A.alloc<int32_t>(cn);
         s.r = A.alloc<float>(cn);
-        s.X[0] = A.alloc<float>((int64_t)cf * k);
-        s.X[1] = A.alloc<float>((int64_t)cf * k);
+        s.X = A.alloc<float>((int64_t)cf * k);
     }
     x.keys = A.alloc<uint64_t>(cn);
     x.keys_alt = A.alloc<uint64_t>(cn);
@@ -994,14 +979,8 @@ void ext_ensure(tsid_ctx *c, int64_t nnz, int32_t n_free, int32_t items_bound, i
     x.sort_scratch = A.alloc<uint32_t>((int64_t)radix_scratch_elems(cn));
     x.stream = A.alloc<int2>(cn);
     x.ptr = A.alloc<int64_t>((int64_t)cf + 1);
-    x.nparts = A.alloc<uint32_t>(cf);
-    x.scan_scratch = A.alloc<uint32_t>((int64_t)scan_scratch_elems(cf));
-    x.item_off = A.alloc<uint32_t>((int64_t)cf + 1);
-    x.items = A.alloc<int32_t>(ci);
-    x.carry = A.alloc<float>((int64_t)ci * k);
     x.cap_nnz = cn;
     x.cap_free = cf;
-    x.cap_items = ci;
     x.k = k;
 }
 
@@ -1018,10 +997,7 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
     if (n_free > 0 && !F_free) fail(TSID_E_INVAL, "F_free is NULL");
     if (F_fixed) check_aligned(F_fixed, "F_fixed");
     const int K = c->tpl->k;
-    const int32_t E = kExtendE;
-    const int64_t bound64 = (int64_t)n_free + nnz / E + 1;
-    if (bound64 >= INT32_MAX) fail(TSID_E_INVAL, "chunk too large");
-    ext_ensure(c, nnz, n_free, (int32_t)bound64, K);
+    ext_ensure(c, nnz, n_free, K);
     ExtState &x = c->ext;
     const int si = x.next;
     x.next ^= 1;
@@ -1047,43 +1023,28 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
     const uint32_t *sv = alt ? x.vals_alt : x.vals;
     keys_to_stream(sk, sv, nnz, bits_fixed, x.stream, x.err, cs);
     ptr_from_keys(sk, nnz, n_free, bits_fixed, x.ptr, cs);
-    plan_items(x.ptr, n_free, E, x.item_off, x.items, x.nparts, x.scan_scratch, cs);
-    // the slot's factor buffers are free once its previous results were flushed
+    // the slot's result buffer is free once its previous results were flushed
     TSID_HIP(hipStreamWaitEvent(cs, s.ev_flushed, 0));
-    fill_f32(s.X[0], (int64_t)n_free * K, 0.f, cs);
     PassArgs a{};
     a.stream = x.stream;
     a.ptr = x.ptr;
-    a.items = x.items;
-    a.item_off = x.item_off;
-    a.item_end = x.item_off + 1;
-    a.n_items_dev = x.item_off + n_free;
-    a.n_items = (int32_t)bound64;
     a.rows = n_free;
-    a.E = E;
     a.Y = F_fixed;
     a.y_rows = n_fixed;
-    a.carry = x.carry;
+    a.Xn = s.X;
     a.lam = o->lambda;
     a.lr = o->lr;
     a.xi = o->clip_xi;
     a.clip = o->clip;
     a.degree = o->step == TSID_STEP_DEGREE;
     a.err = x.err;
-    a.skip_after_nonfinite = 0;
-    for (int st = 0; st < o->epochs && n_free > 0; ++st) {
-        a.epoch = st;
-        a.X = s.X[st & 1];
-        a.Xn = s.X[(st + 1) & 1];
-        launch_item_pass(K, TSID_FP32, false, a, cs);
-        launch_fixup(K, TSID_FP32, a, cs);
-    }
+    // every step of every free row in one launch (one wave per free row)
+    launch_extend_steps(K, a, o->epochs, cs);
     TSID_HIP(hipEventRecord(s.ev_done, cs));
     // flush the results on the third stream
     TSID_HIP(hipStreamWaitEvent(c->d2h, s.ev_done, 0));
     if (n_free)
-        TSID_HIP(hipMemcpyAsync(F_free, s.X[o->epochs & 1], (size_t)n_free * K * 4,
-                                hipMemcpyDeviceToHost, c->d2h));
+        TSID_HIP(hipMemcpyAsync(F_free, s.X, (size_t)n_free * K * 4, hipMemcpyDeviceToHost, c->d2h));
     TSID_HIP(hipEventRecord(s.ev_flushed, c->d2h));
     x.pending = true;
     (void)side;

@@ -244,15 +244,13 @@ constexpr int block_spl() {  // stream cells per lane per block
 // next block's cells into `nxt`: loads retire in issue order, so the slow
 // stream loads must come after every gather the arithmetic waits for, and
 // issuing them once per block exposes their latency once per SB cells.
-template <int K, int V, bool BF16, bool LOSS_ONLY, bool BUF>
+// NEXT = false skips those loads (the caller's cells all fit one block).
+template <int K, int V, bool BF16, bool LOSS_ONLY, bool BUF, bool NEXT = true, int SPL = block_spl<K / V>()>
 __device__ __forceinline__ void process_block(const PassArgs &A, const YTable &Yt, int64_t j0,
-                                              int64_t end, int64_t last, int lg,
-                                              const int2 (&cur)[block_spl<K / V>()],
-                                              int2 (&nxt)[block_spl<K / V>()],
-                                              const float (&x)[V], const uint32_t (&xp)[V / 2],
-                                              float (&acc)[V], float &e2) {
+                                              int64_t end, int64_t last, int lg, const int2 (&cur)[SPL],
+                                              int2 (&nxt)[SPL], const float (&x)[V],
+                                              const uint32_t (&xp)[V / 2], float (&acc)[V], float &e2) {
     constexpr int G = K / V;
-    constexpr int SPL = block_spl<G>();
     constexpr int SB = G * SPL;
     constexpr int CH = chunk_cells<G>();
     static_assert(SB % CH == 0, "a stream block holds whole chunks");
@@ -278,7 +276,7 @@ __device__ __forceinline__ void process_block(const PassArgs &A, const YTable &Y
                     yw[t][4 * c + 3] = q.w;
                 }
             }
-            if (last_chunk) {
+            if (NEXT && last_chunk) {
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int c = 0; c < SPL; ++c) {
@@ -320,7 +318,7 @@ __device__ __forceinline__ void process_block(const PassArgs &A, const YTable &Y
                     y[t][4 * c + 3] = __uint_as_float(q.w);
                 }
             }
-            if (last_chunk) {
+            if (NEXT && last_chunk) {
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int c = 0; c < SPL; ++c) {
@@ -506,6 +504,103 @@ __global__ __launch_bounds__(kThreads) void k_fixup(const PassArgs A) {
     finalize_row<G, V, BF16>(A, (int)row, lg, x, acc, A.ptr[row + 1] - A.ptr[row]);
 }
 
+// One-sided extension steps (Section 5.2, Eq. 6 in factored form), all T of
+// them in one launch.  A free row's steps need nothing from other rows, so a
+// wave owns one free row (bucket) for the whole run: its NG lane groups split
+// the row's cells, each step they add their partial gradient sums through LDS
+// in group order, and every group applies the same update to its register
+// copy of the row (Eq. 5 with the step option and the clip).  The row starts
+// at zero and is stored once, after the last step.  The per-cell work is the
+// item pass's (process_block), so a step is the same computation as one
+// launch of the item pass on the chunk.
+// Stream records per lane per block in the extension kernel: a group's share
+// of a free row of up to G * TSID_EXT_SPL cells stays in registers.
+#ifndef TSID_EXT_SPL
+#define TSID_EXT_SPL 4
+#endif
+
+template <int K, int V, bool BUF>
+__global__ __launch_bounds__(kThreads) void k_extend_steps(const PassArgs A, int32_t steps) {
+    constexpr int G = K / V;
+    constexpr int NG = 64 / G;
+    constexpr int SPL = (G * TSID_EXT_SPL) % chunk_cells<G>() == 0 ? TSID_EXT_SPL : chunk_cells<G>() / G;
+    constexpr int SB = G * SPL;
+    const int lane = threadIdx.x & 63;
+    const int grp = lane / G, lg = lane % G, wv = threadIdx.x >> 6;
+    const int64_t row = (int64_t)blockIdx.x * kWaves + wv;
+    if (row >= A.rows) return;  // whole waves leave together
+    const int64_t rb = A.ptr[row], deg = A.ptr[row + 1] - rb;
+    const int64_t beg = rb + grp * deg / NG, end = rb + (grp + 1) * deg / NG;
+    const int64_t last = end - 1;
+    const float s = A.degree ? 1.0f / (float)(deg > 1 ? deg : 1) : 1.0f;
+    const YTable Yt = make_ytable<BUF>(A, K * 4);
+    __shared__ float red[kWaves][NG][K];
+    float x[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) x[v] = 0.f;
+    const uint32_t xp[V / 2] = {};  // bf16 pairs: unused in fp32
+    bool bad = false;
+    // A group whose share of the row fits one stream block keeps its records
+    // in registers for all steps (extension rows are short); longer shares
+    // stream their records again each step.
+    const bool one_block = end - beg <= SB;
+    int2 keep[SPL], bufA[SPL], bufB[SPL];
+    if (end > beg) {
+#pragma unroll
+        for (int c = 0; c < SPL; ++c) {
+            const int64_t jj = beg + c * G + lg;
+            keep[c] = load_cell(A.stream + (jj < last ? jj : last));
+        }
+    }
+    for (int st = 0; st < steps; ++st) {
+        float acc[V];
+#pragma unroll
+        for (int v = 0; v < V; ++v) acc[v] = 0.f;
+        float e2 = 0.f;
+        if (one_block) {
+            if (end > beg)
+                process_block<K, V, false, false, BUF, false, SPL>(A, Yt, beg, end, last, lg, keep, bufB, x,
+                                                                   xp, acc, e2);
+        } else {
+#pragma unroll
+            for (int c = 0; c < SPL; ++c) bufA[c] = keep[c];
+            for (int64_t j0 = beg; j0 < end; j0 += SB) {
+                process_block<K, V, false, false, BUF, true, SPL>(A, Yt, j0, end, last, lg, bufA, bufB, x, xp,
+                                                                  acc, e2);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int c = 0; c < SPL; ++c) bufA[c] = bufB[c];
+            }
+        }
+        // the row's gradient sum: the groups' partial sums in group order
+        store_f32<V>(&red[wv][grp][lg * V], acc);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        float tot[V];
+        load_f32<V>(&red[wv][0][lg * V], tot);
+        for (int g = 1; g < NG; ++g) {
+            float part[V];
+            load_f32<V>(&red[wv][g][lg * V], part);
+#pragma unroll
+            for (int v = 0; v < V; ++v) tot[v] += part[v];
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();  // every lane has read red before the next step writes it
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+            const float g = 2.0f * A.lam * x[v] - 2.0f * tot[v];
+            float d = -s * g;
+            if (A.clip && d > A.xi) d = A.xi;
+            x[v] = x[v] + A.lr * d;
+            bad |= !__builtin_isfinite(x[v]);
+        }
+    }
+    if (grp == 0) store_f32<V>(A.Xn + row * K + lg * V, x);
+    if (bad) A.err[ERR_NONFINITE] = 1;
+}
+
 template <int K>
 __global__ void k_row_norms(const float *X, int32_t rows, float *norm) {
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -585,6 +680,22 @@ void item_pass_kv(bool loss_only, const PassArgs &a, hipStream_t s, hipEvent_t e
 }
 
 template <int K, int V, bool BF16>
+void extend_steps_kv(const PassArgs &a, int32_t steps, hipStream_t s) {
+    if constexpr (BF16) {
+        fail(TSID_E_INVAL, "the extension runs in fp32");
+    } else {
+        const int grid = ceil_div(a.rows, (int64_t)kWaves);
+        if (grid <= 0) return;  // steps == 0 still runs: it stores the zero start
+        const bool buf = a.y_rows * (int64_t)K * 4 < (int64_t(1) << 31);
+        if (buf)
+            hipLaunchKernelGGL((k_extend_steps<K, V, true>), dim3(grid), dim3(kThreads), 0, s, a, steps);
+        else
+            hipLaunchKernelGGL((k_extend_steps<K, V, false>), dim3(grid), dim3(kThreads), 0, s, a, steps);
+        TSID_HIP(hipGetLastError());
+    }
+}
+
+template <int K, int V, bool BF16>
 void fixup_kv(const PassArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     constexpr int NG = 64 / (K / V);
     const int grid = ceil_div(a.rows, (int64_t)kWaves * NG);
@@ -638,6 +749,11 @@ void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStr
 
 void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     TSID_DISPATCH_K(K, fixup_kv, a, s, ev0, ev1)
+}
+
+void launch_extend_steps(int K, const PassArgs &a, int32_t steps, hipStream_t s) {
+    const int prec = TSID_FP32;
+    TSID_DISPATCH_K(K, extend_steps_kv, a, steps, s)
 }
 
 namespace {

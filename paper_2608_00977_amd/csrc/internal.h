@@ -119,6 +119,10 @@ void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStr
                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s, hipEvent_t ev0 = nullptr,
                   hipEvent_t ev1 = nullptr);
+// `steps` one-sided extension steps from zero in one launch, one wave per
+// bucket (a.rows buckets over a.stream / a.ptr; fp32; a.X unused, the result
+// goes to a.Xn; a non-finite update stores 1 in a.err[ERR_NONFINITE]).
+void launch_extend_steps(int K, const PassArgs &a, int32_t steps, hipStream_t s);
 // Items one wave holds for rank K and precision prec (the item pass's groups
 // per wave): buckets whose items stay inside one such run need no fixup.
 int items_per_wave(int K, int prec);
