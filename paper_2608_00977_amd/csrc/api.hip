@@ -23,6 +23,8 @@ namespace {
 
 constexpr int64_t kDefaultStage = int64_t(1) << 24;  // entries per host-to-device piece
 constexpr int64_t kMaxEntries = (int64_t(1) << 32) - 1;
+// Zero records after the slab pass's stream copy: it reads whole groups of
+// eight records.
 constexpr int64_t kStreamPad = 8;
 
 bool valid_rank(int32_t k) { return k == 8 || k == 16 || k == 32 || k == 64 || k == 128; }
@@ -94,6 +96,7 @@ struct SlabPlan {
     int32_t suits = -1;        // cached slab_suits() of the template (-1: not evaluated)
     int32_t C = 0, n_slabs = 0, S = 0, U = 0, n_blocks = 0;
     uint32_t *seg = nullptr;
+    int2 *stream = nullptr;    // slab-ordered copy of the side's stream (launch_slab_order)
     float *carry = nullptr;
     int64_t units() const { return (int64_t)n_blocks * U; }
     int64_t lanes() const { return units() * kSlabLanes; }
@@ -259,6 +262,7 @@ void free_template(tsid_ctx *c, Template *&t) {
         }
     for (SlabPlan &sp : t->slab) {
         A.release(sp.seg);
+        A.release(sp.stream);
         A.release(sp.carry);
     }
     delete t;
@@ -483,10 +487,7 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
         bool in_alt = radix_sort(keys, vals, keys_alt, vals_alt, total, nbits, sort_tmp, cs);
         uint64_t *ck = in_alt ? keys_alt : keys;
         uint32_t *cv = in_alt ? vals_alt : vals;
-        // eight zero records after each stream: the slab pass reads whole
-        // groups of eight records
-        t->stream_r = A.alloc<int2>(total + kStreamPad);
-        TSID_HIP(hipMemsetAsync(t->stream_r + total, 0, kStreamPad * sizeof(int2), cs));
+        t->stream_r = A.alloc<int2>(total);
         t->row_ptr = A.alloc<int64_t>((int64_t)m_t + 1);
         keys_to_stream(ck, cv, total, bits_b, t->stream_r, c->err_dev, cs);
         ptr_from_keys(ck, total, m_t, bits_b, t->row_ptr, cs);
@@ -498,8 +499,7 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
         bool alt2 = radix_sort(ok, ov, ck, cv, total, nbits, sort_tmp, cs);
         uint64_t *tk = alt2 ? ck : ok;
         uint32_t *tv = alt2 ? cv : ov;
-        t->stream_c = A.alloc<int2>(total + kStreamPad);
-        TSID_HIP(hipMemsetAsync(t->stream_c + total, 0, kStreamPad * sizeof(int2), cs));
+        t->stream_c = A.alloc<int2>(total);
         t->col_ptr = A.alloc<int64_t>((int64_t)n_t + 1);
         keys_to_stream(tk, tv, total, bits_a, t->stream_c, c->err_dev, cs);
         ptr_from_keys(tk, total, n_t, bits_a, t->col_ptr, cs);
@@ -658,19 +658,25 @@ void ensure_slab(tsid_ctx *c, int side, int prec) {
         const int32_t S = ceil_div(n_slabs, std::min<int64_t>(u_target, n_slabs));
         const int32_t U = ceil_div(n_slabs, S);
         uint32_t *seg = nullptr;
+        int2 *stream = nullptr;
         float *carry = nullptr;
         try {
             seg = A.alloc<uint32_t>((int64_t)(n_slabs + 1) * rows);
+            stream = A.alloc<int2>(t.nnz + kStreamPad);
             if (U > 1) carry = A.alloc<float>((int64_t)n_blocks * U * kSlabLanes * t.k);
-            launch_slab_seg(side ? t.stream_c : t.stream_r, side ? t.col_ptr : t.row_ptr, rows, n_slabs, C,
-                            seg, cs);
+            const int2 *src = side ? t.stream_c : t.stream_r;
+            launch_slab_seg(src, side ? t.col_ptr : t.row_ptr, rows, n_slabs, C, seg, cs);
+            launch_slab_order(src, seg, rows, n_slabs, stream, cs);
+            TSID_HIP(hipMemsetAsync(stream + t.nnz, 0, kStreamPad * sizeof(int2), cs));
             TSID_HIP(hipStreamSynchronize(cs));
         } catch (...) {
             A.release(seg);
+            A.release(stream);
             A.release(carry);
             throw;
         }
         sp.seg = seg;
+        sp.stream = stream;
         sp.carry = carry;
         sp.C = C;
         sp.n_slabs = n_slabs;
@@ -750,7 +756,7 @@ PassArgs pass_args(const Template &t, int side, const tsid_fit_opts &o, int32_t 
 SlabArgs slab_args(const Template &t, int side, const tsid_fit_opts &o, int32_t *err) {
     const SlabPlan &sp = t.slab[side];
     SlabArgs a{};
-    a.stream = side ? t.stream_c : t.stream_r;
+    a.stream = sp.stream;
     a.seg = sp.seg;
     a.rows = side ? t.n_t : t.m_t;
     a.y_rows = side ? t.m_t : t.n_t;

@@ -152,7 +152,7 @@ constexpr int kSlabLanes = TSID_SLAB_LANES;
 constexpr int kSlabBytes = TSID_SLAB_KIB * 1024;
 
 struct SlabArgs {
-    const int2 *stream;      // bucketed cells {other id, value bits}, padded by 8 records
+    const int2 *stream;      // the slab-ordered copy of the bucketed cells, padded by 8 records
     const uint32_t *seg;     // seg[s * rows + x]: first cell of bucket x with other id >= s * C
     int32_t rows;            // owner rows (buckets)
     int32_t y_rows;          // rows of the gathered factor
@@ -178,6 +178,10 @@ bool slab_supported(int K, int prec);
 int slab_rows(int K);  // C for rank K
 void launch_slab_seg(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_slabs, int32_t C,
                      uint32_t *seg, hipStream_t s);
+// The slab pass's copy of a stream: every slab run of bucket x lists the cells
+// whose other index has parity (x >> 3) & 1 first (see slab.hip).
+void launch_slab_order(const int2 *stream, const uint32_t *seg, int32_t rows, int32_t n_slabs, int2 *out,
+                       hipStream_t s);
 // The pass over n_units workgroups.  With U == 1 it updates the rows itself;
 // with U > 1 (and not loss-only) launch_slab_finish then adds each row's U
 // partial sums and updates it.

@@ -21,9 +21,14 @@
 //    its busiest lane, so slabs are as large as LDS allows: the longer each
 //    lane's run per slab, the smaller the relative spread between lanes.
 //  * Lanes read the 16-byte chunks of an LDS row in an order rotated by their
-//    lane id, so the eight lanes served together touch eight different bank
-//    groups whatever rows they read; the owner row and the gradient sum are
-//    held in the same rotated order, which costs nothing.
+//    lane id, so eight consecutive lanes touch eight different bank groups
+//    whatever rows they read; the owner row and the gradient sum are held in
+//    the same rotated order, which costs nothing.  gfx950 serves 16 lanes at
+//    a time over 64 banks, and a 128-byte row sits in one half of them by the
+//    parity of its index, so lanes x and x + 8 (same chunk index) would still
+//    collide whenever their rows' parities agree: the pass walks its own copy
+//    of the stream in which each run lists the cells of one parity first --
+//    even for lanes with bit 3 clear, odd for the others (k_slab_order).
 //  * A workgroup covers a range of S slabs.  When a block of rows is split
 //    over several workgroups (U > 1) each leaves its partial gradient sums in
 //    a carry buffer, and a second kernel adds the U parts of every row in a
@@ -39,12 +44,8 @@ namespace {
 
 constexpr int kLanes = kSlabLanes;
 
-// Cells whose gathered rows are read before their arithmetic (a scheduling
-// group), and the waves per SIMD the register budget must allow (LDS allows
-// 160 KiB / slab bytes workgroups of four waves per compute unit).
-#ifndef TSID_SLAB_GROUP
-#define TSID_SLAB_GROUP 2
-#endif
+// Waves per SIMD the register budget must allow (one 512-lane workgroup per
+// compute unit: two).
 #ifndef TSID_SLAB_WAVES_PER_EU
 #define TSID_SLAB_WAVES_PER_EU 2
 #endif
@@ -107,52 +108,89 @@ __device__ __forceinline__ void load8(const int2 *p, int2 (&r)[8]) {
 // rows sbase .. sbase + C - 1: residuals against the LDS rows, e^2 and the
 // gradient sums.  Records at or past q belong to other rows or slabs: their
 // LDS row is replaced by row 0 and their residual by 0 (bit masks, so the
-// work stays branch-free).
+// work stays branch-free).  The LDS reads of cell c + 1 are issued before the
+// arithmetic of cell c, so a wave has one row in flight while it computes.
+template <int K>
+__device__ __forceinline__ uint32_t slab_row_off(const int2 &rec, uint32_t keep, int32_t sbase) {
+    return ((uint32_t)(rec.x - sbase) * (uint32_t)(K * 4)) & keep;
+}
+
+template <int K>
+__device__ __forceinline__ void slab_read_row(const char *ysb, uint32_t row_off, const uint32_t (&koff)[K / 4],
+                                              float4 (&y)[K / 4]) {
+#pragma unroll
+    for (int i = 0; i < K / 4; ++i) y[i] = *reinterpret_cast<const float4 *>(ysb + row_off + koff[i]);
+}
+
+template <int K, bool LOSS_ONLY>
+__device__ __forceinline__ void slab_cell(const float4 (&y)[K / 4], float r, uint32_t keep,
+                                          const float4 (&x)[K / 4], float4 (&acc)[K / 4], float &e2) {
+    constexpr int NCH = K / 4;
+#if TSID_SLAB_CHAINS == 1
+    float d = 0.f;
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+        d += x[i].x * y[i].x;
+        d += x[i].y * y[i].y;
+        d += x[i].z * y[i].z;
+        d += x[i].w * y[i].w;
+    }
+#else
+    float d0 = 0.f, d1 = 0.f, d2 = 0.f, d3 = 0.f;
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+        d0 += x[i].x * y[i].x;
+        d1 += x[i].y * y[i].y;
+        d2 += x[i].z * y[i].z;
+        d3 += x[i].w * y[i].w;
+    }
+    const float d = (d0 + d1) + (d2 + d3);
+#endif
+    const float e = __uint_as_float(__float_as_uint(r - d) & keep);
+    e2 += e * e;
+    if constexpr (!LOSS_ONLY) {
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+            acc[i].x += e * y[i].x;
+            acc[i].y += e * y[i].y;
+            acc[i].z += e * y[i].z;
+            acc[i].w += e * y[i].w;
+        }
+    }
+}
+
 template <int K, bool LOSS_ONLY>
 __device__ __forceinline__ void slab_burst(const int2 (&rec)[8], uint32_t j, uint32_t q, int32_t sbase,
                                            const char *ysb, const uint32_t (&koff)[K / 4],
                                            const float4 (&x)[K / 4], float4 (&acc)[K / 4], float &e2) {
     constexpr int NCH = K / 4;
+    uint32_t keep[8];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-        // at most TSID_SLAB_GROUP cells' rows in flight: bounds the registers
-        if (c % TSID_SLAB_GROUP == 0 && c > 0) __builtin_amdgcn_sched_barrier(0);
-        const uint32_t keep = j + c < q ? 0xffffffffu : 0u;
-        const uint32_t row_off = ((uint32_t)(rec[c].x - sbase) * (uint32_t)(K * 4)) & keep;
-        float4 y[NCH];
+    for (int c = 0; c < 8; ++c) keep[c] = j + c < q ? 0xffffffffu : 0u;
+    if constexpr (K > 32) {
+        // k = 64: two rows of 64 registers in flight would spill; read and
+        // compute two cells at a time instead
 #pragma unroll
-        for (int i = 0; i < NCH; ++i) y[i] = *reinterpret_cast<const float4 *>(ysb + row_off + koff[i]);
-#if TSID_SLAB_CHAINS == 1
-        float d = 0.f;
-#pragma unroll
-        for (int i = 0; i < NCH; ++i) {
-            d += x[i].x * y[i].x;
-            d += x[i].y * y[i].y;
-            d += x[i].z * y[i].z;
-            d += x[i].w * y[i].w;
+        for (int c = 0; c < 8; c += 2) {
+            __builtin_amdgcn_sched_barrier(0);
+            float4 y0[NCH], y1[NCH];
+            slab_read_row<K>(ysb, slab_row_off<K>(rec[c], keep[c], sbase), koff, y0);
+            slab_read_row<K>(ysb, slab_row_off<K>(rec[c + 1], keep[c + 1], sbase), koff, y1);
+            slab_cell<K, LOSS_ONLY>(y0, __int_as_float(rec[c].y), keep[c], x, acc, e2);
+            slab_cell<K, LOSS_ONLY>(y1, __int_as_float(rec[c + 1].y), keep[c + 1], x, acc, e2);
         }
-#else
-        float d0 = 0.f, d1 = 0.f, d2 = 0.f, d3 = 0.f;
+        return;
+    }
+    float4 ya[NCH], yb[NCH];
+    slab_read_row<K>(ysb, slab_row_off<K>(rec[0], keep[0], sbase), koff, ya);
 #pragma unroll
-        for (int i = 0; i < NCH; ++i) {
-            d0 += x[i].x * y[i].x;
-            d1 += x[i].y * y[i].y;
-            d2 += x[i].z * y[i].z;
-            d3 += x[i].w * y[i].w;
-        }
-        const float d = (d0 + d1) + (d2 + d3);
-#endif
-        const float e = __uint_as_float(__float_as_uint(__int_as_float(rec[c].y) - d) & keep);
-        e2 += e * e;
-        if constexpr (!LOSS_ONLY) {
-#pragma unroll
-            for (int i = 0; i < NCH; ++i) {
-                acc[i].x += e * y[i].x;
-                acc[i].y += e * y[i].y;
-                acc[i].z += e * y[i].z;
-                acc[i].w += e * y[i].w;
-            }
-        }
+    for (int c = 0; c < 8; c += 2) {
+        __builtin_amdgcn_sched_barrier(0);
+        slab_read_row<K>(ysb, slab_row_off<K>(rec[c + 1], keep[c + 1], sbase), koff, yb);
+        slab_cell<K, LOSS_ONLY>(ya, __int_as_float(rec[c].y), keep[c], x, acc, e2);
+        __builtin_amdgcn_sched_barrier(0);
+        if (c + 2 < 8) slab_read_row<K>(ysb, slab_row_off<K>(rec[c + 2], keep[c + 2], sbase), koff, ya);
+        slab_cell<K, LOSS_ONLY>(yb, __int_as_float(rec[c + 1].y), keep[c + 1], x, acc, e2);
     }
 }
 
@@ -355,6 +393,31 @@ void allow_lds(Kern kernel, size_t bytes) {
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes));
 }
 
+// The slab pass's own copy of a bucketed stream.  Within every slab run of
+// bucket x the cells whose other index b has the parity (x >> 3) & 1 come
+// first, then the rest, each part in the stream's order.  A staged LDS row
+// lies in one half of the 64 banks according to the parity of b, and the
+// lanes x and x + 8 of a 16-lane LDS group read the same chunk index (lane
+// rotation), so with this order they read opposite halves for most of their
+// runs instead of colliding whenever their rows' parities agree.
+__global__ void k_slab_order(const int2 *stream, const uint32_t *seg, int32_t rows, int32_t n_slabs,
+                             int2 *out) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (int64_t)n_slabs * rows) return;
+    const int32_t s = (int32_t)(t / rows), x = (int32_t)(t % rows);
+    const uint32_t p = seg[(int64_t)s * rows + x], q = seg[(int64_t)(s + 1) * rows + x];
+    const int first = (x >> 3) & 1;
+    uint32_t o = p;
+    for (uint32_t j = p; j < q; ++j) {
+        const int2 c = stream[j];
+        if ((c.x & 1) == first) out[o++] = c;
+    }
+    for (uint32_t j = p; j < q; ++j) {
+        const int2 c = stream[j];
+        if ((c.x & 1) != first) out[o++] = c;
+    }
+}
+
 template <int K>
 void slab_pass_k(bool loss_only, const SlabArgs &a, int64_t n_units, hipStream_t s, hipEvent_t ev0,
                  hipEvent_t ev1) {
@@ -392,6 +455,14 @@ void launch_slab_seg(const int2 *stream, const int64_t *ptr, int32_t rows, int32
     const int64_t n = (int64_t)(n_slabs + 1) * rows;
     if (n <= 0) return;
     k_slab_seg<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(stream, ptr, rows, n_slabs, C, seg);
+    TSID_HIP(hipGetLastError());
+}
+
+void launch_slab_order(const int2 *stream, const uint32_t *seg, int32_t rows, int32_t n_slabs, int2 *out,
+                       hipStream_t s) {
+    const int64_t n = (int64_t)n_slabs * rows;
+    if (n <= 0) return;
+    k_slab_order<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(stream, seg, rows, n_slabs, out);
     TSID_HIP(hipGetLastError());
 }
 
