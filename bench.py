@@ -23,8 +23,10 @@ minutes to generate); mid / tiny are small.
 
 Roofline: the dominant kernel is the longer of the P and Q passes (the slab
 pass on evenly spread fp32 templates such as Scientific, else the item pass),
-timed with HIP events on the library's compute stream during the timed
-region; its algorithmic bytes per launch are the compulsory bytes of one
+timed with HIP events attached to its dispatches on the library's compute
+stream during the timed region (every --time-every-th epoch: a timed dispatch
+costs a few microseconds of wall time, which would otherwise slow the
+throughput being measured); its algorithmic bytes per launch are the compulsory bytes of one
 pass: the bucketed cell stream (8 B per cell), the bucket pointers (8 B per
 bucket), the owner rows read and written once and the gathered rows read once
 (4 B per coordinate in fp32; 2 B for bf16 copies).  A slab pass whose row
@@ -57,6 +59,9 @@ def parse():
     ap.add_argument("--pass-kernel", default="auto", choices=["auto", "item", "slab"],
                     help="kernel of the P and Q passes (tsid_set_pass_kernel); auto picks the "
                          "slab pass for evenly spread fp32 templates")
+    ap.add_argument("--time-every", type=int, default=10,
+                    help="attach HIP timing events to the kernels of every n-th timed epoch (each "
+                         "timed dispatch costs a few microseconds of wall time)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--extend", action="store_true",
@@ -240,7 +245,7 @@ def main():
 
     # timed region: exactly `steps` epochs
     P, Q = P0.clone(), Q0.clone()
-    T.set_timing(True)
+    T.set_timing(max(1, args.time_every))
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     _, hist = T.fit_template(P, Q, mk(args.steps), want_loss=True)
@@ -316,9 +321,10 @@ def main():
         "cpu_baseline": cpu,
         "compulsory_GBps_per_epoch": round(epoch_bytes / (ms_per_step / 1e3) / 1e9, 2),
         "device_epoch_ms": tm["epoch_ms"] / max(1, tm["epochs"]),
+        "timed_epochs": tm["epochs"],
         "kernel_ms_per_epoch": {"p_pass": avg[0], "q_pass": avg[1],
                                 "fixups": tm["fixup_ms"] / max(1, tm["epochs"]),
-                                "loss_reduce": tm["reduce_ms"] / max(1, tm["epochs"])},
+                                "loss_reduce": tm["reduce_ms"] / max(1, tm["reduce_launches"]) / 16},
         "loss_first_epoch": float(hist[0]),
         "build_s": build_s,
         "loss_after_timed_epochs": hist_T,

@@ -207,17 +207,22 @@ tsid_status tsid_set_pass_kernel(tsid_ctx *ctx, int mode);
  * output may be NULL.  Errors: E_INVAL (ctx NULL). */
 tsid_status tsid_fit_pass_kernels(const tsid_ctx *ctx, int32_t *p_pass, int32_t *q_pass);
 
-/* Kernel timing of the template fit (a tracing aid).  While enabled, every
- * kernel of each epoch of tsid_fit_template is launched with a start and an
- * end HIP event attached to its dispatch on the compute stream (no separate
- * event packets), and the durations accumulate here until the next
- * tsid_set_timing call resets them.  pass_ms[0] / pass_launches[0]: the P
- * pass (row buckets); [1]: the Q pass (column buckets); fixup: the kernels
- * that combine partial sums after a pass (item pass: buckets longer than one
- * wave; slab pass: blocks split over several workgroups), which also update
- * those rows; reduce: the batched loss reductions (one per
- * 16 epochs); epoch_ms: start of each epoch's first kernel to the end of its
- * last, summed. */
+/* Kernel timing of the template fit (a tracing aid).  With every = n > 0,
+ * the kernels of every n-th epoch of tsid_fit_template (epochs 0, n, 2n, ...)
+ * are launched with a start and an end HIP event attached to their dispatch
+ * on the compute stream (no separate event packets), and so is every loss
+ * reduction; the durations accumulate here until the next tsid_set_timing
+ * call resets them.  Each timed dispatch costs a few microseconds of wall
+ * time, so timing a sample of the epochs keeps the fit's own throughput
+ * nearly unchanged.  every = 0 turns timing off.
+ *  pass_ms[0] / pass_launches[0]: the P pass (row buckets); [1]: the Q pass
+ *  (column buckets); fixup: the kernels that combine partial sums after a
+ *  pass (item pass: buckets longer than one wave; slab pass: blocks split
+ *  over several workgroups), which also update those rows; reduce: the
+ *  batched loss reductions (one per 16 epochs); epoch_ms: from the start of
+ *  a timed epoch's P pass to the end of its last pass or fixup kernel, summed
+ *  over the timed epochs, whose number is `epochs`.
+ * Errors: E_INVAL (ctx NULL or every < 0). */
 typedef struct {
     double pass_ms[2];
     int64_t pass_launches[2];
@@ -228,7 +233,7 @@ typedef struct {
     double epoch_ms;
     int64_t epochs;
 } tsid_timing;
-tsid_status tsid_set_timing(tsid_ctx *ctx, int enable);
+tsid_status tsid_set_timing(tsid_ctx *ctx, int every);
 tsid_status tsid_get_timing(const tsid_ctx *ctx, tsid_timing *out);
 
 /* Index structures of the current template, copied to host_dst (HOST) for

@@ -131,8 +131,8 @@ def tsid_fit_epochs_done(ctx) -> int:
     return out.value
 
 
-def tsid_set_timing(ctx, enable: bool) -> int:
-    return lib().tsid_set_timing(ctx, int(bool(enable)))
+def tsid_set_timing(ctx, every: int) -> int:
+    return lib().tsid_set_timing(ctx, int(every))
 
 
 def tsid_set_pass_kernel(ctx, mode: int) -> int:
@@ -259,8 +259,10 @@ class Tsid:
             self._check(st, "tsid_fit_template")
         return st, hist
 
-    def set_timing(self, enable: bool):
-        self._check(tsid_set_timing(self.ctx, enable), "tsid_set_timing")
+    def set_timing(self, every):
+        """Time the kernels of every `every`-th epoch (True: every epoch; 0 /
+        False: off); see tsid_set_timing."""
+        self._check(tsid_set_timing(self.ctx, int(every)), "tsid_set_timing")
 
     def set_pass_kernel(self, mode: str):
         """'auto', 'item' or 'slab' (tsid_set_pass_kernel)."""

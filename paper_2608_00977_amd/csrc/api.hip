@@ -161,7 +161,7 @@ struct tsid_ctx {
     int32_t *err_host = nullptr;     // pinned mirror
     Template *tpl = nullptr;
     int32_t epochs_done = 0;         // of the last fit
-    bool timing = false;
+    int32_t timing = 0;              // time every timing-th epoch (0: off)
     tsid_timing tm{};
     std::vector<hipEvent_t> events;  // kernel timestamps, kEvents per epoch
     std::vector<uint8_t> launched;   // which kernel kinds each timed epoch ran
@@ -189,9 +189,12 @@ void ensure_events(tsid_ctx *c, size_t epochs) {
     c->launched.assign(epochs, 0);
 }
 
-// Events for kernel kind k of epoch ep (a null pair when timing is off).
+// Events for kernel kind k of epoch ep: a null pair when timing is off or the
+// epoch is not sampled.  The loss reduction (one per 16 epochs) is always
+// timed while timing is on.
 std::pair<hipEvent_t, hipEvent_t> timed(tsid_ctx *c, int ep, int k) {
     if (!c->timing) return {nullptr, nullptr};
+    if (k != TK_REDUCE && ep % c->timing != 0) return {nullptr, nullptr};
     c->launched[(size_t)ep] |= (uint8_t)(1u << k);
     const size_t b = (size_t)ep * kEvents + 2 * k;
     return {c->events[b], c->events[b + 1]};
@@ -207,22 +210,24 @@ void collect_timing(tsid_ctx *c, int epochs) {
     tsid_timing &t = c->tm;
     for (int ep = 0; ep < epochs; ++ep) {
         const uint8_t l = c->launched[(size_t)ep];
-        int last = TK_PPASS;
+        int last = -1;
         for (int k = 0; k < kTimed; ++k) {
             if (!(l & (1u << k))) continue;
             const double ms = dt(ev(ep, k, 0), ev(ep, k, 1));
-            last = k;
             if (k == TK_PPASS || k == TK_QPASS) {
                 t.pass_ms[k / 2] += ms;
                 t.pass_launches[k / 2] += 1;
+                last = k;
             } else if (k == TK_REDUCE) {
                 t.reduce_ms += ms;
                 t.reduce_launches += 1;
             } else {
                 t.fixup_ms += ms;
                 t.fixup_launches += 1;
+                last = k;
             }
         }
+        if (last < 0 || !(l & (1u << TK_PPASS))) continue;  // not a sampled epoch
         t.epoch_ms += dt(ev(ep, TK_PPASS, 0), ev(ep, last, 1));
         t.epochs += 1;
     }
@@ -1209,9 +1214,9 @@ tsid_status tsid_fit_pass_kernels(const tsid_ctx *c, int32_t *p_pass, int32_t *q
     return TSID_OK;
 }
 
-tsid_status tsid_set_timing(tsid_ctx *c, int enable) {
-    if (!c) return TSID_E_INVAL;
-    c->timing = enable != 0;
+tsid_status tsid_set_timing(tsid_ctx *c, int every) {
+    if (!c || every < 0) return TSID_E_INVAL;
+    c->timing = every;
     c->tm = tsid_timing{};
     return TSID_OK;
 }
