@@ -76,3 +76,77 @@ def test_extension_end_to_end_matches_oracle(n_chunks):
     assert np.array_equal(P[p.I], p.P0) and np.array_equal(Q[p.J], p.Q0)
     assert rel_fro(P[F_rows], Xr) <= TOL, rel_fro(P[F_rows], Xr)
     assert rel_fro(Q[F_cols], Xc) <= TOL, rel_fro(Q[F_cols], Xc)
+
+
+@pytest.mark.timeout(900)
+def test_extension_fullsize_sampled_rating():
+    """The full Rating-shaped extension (480,189 x 17,770, 100 M cells, 16
+    chunks per phase, 20 one-sided steps: the bench.py --extend setting),
+    checked on sampled outputs the oracle computes one by one: 64 free rows
+    (plus the two with the most cells) from their template-column cells, and
+    64 free columns (plus the two longest) from all their cells, with the
+    row factors of the rows they touch taken from the oracle's own row phase
+    of those rows."""
+    import torch
+
+    import paper_2608_00977_amd as tsid
+    from paper_2608_00977_amd.extension import Extension
+    p = synth.rating()
+    steps, lam, lr, step = 20, p.lam, 0.05, "degree"
+    note(f"extension fullsize rating nnz={p.nnz}")
+    T = tsid.Tsid(0)
+    try:
+        T.build_template(p.m, p.n, p.u[:0], p.i[:0], p.r[:0], p.I, p.J, p.k)  # sets k
+        ext = Extension(p.m, p.n, p.u, p.i, p.r, p.I, p.J, n_chunks=16)
+        opts = tsid.make_opts(epochs=steps, lam=lam, lr=lr, step=step)
+        P, Q, _ = ext.run(T, torch.from_numpy(p.P0).cuda(), torch.from_numpy(p.Q0).cuda(), opts)
+    finally:
+        T.close()
+    P, Q = P.numpy(), Q.numpy()
+    u = p.u.astype(np.int64)
+    i = p.i.astype(np.int64)
+    row_in = np.zeros(p.m, bool)
+    row_in[p.I] = True
+    col_in = np.zeros(p.n, bool)
+    col_in[p.J] = True
+    cm = np.full(p.n, -1, np.int64)
+    cm[p.J] = np.arange(p.J.size)
+    in_tc = col_in[i]  # cells in template columns
+
+    def row_phase(rows):
+        """Oracle row phase of the given free rows (ascending global ids)."""
+        pos = np.full(p.m, -1, np.int64)
+        pos[rows] = np.arange(rows.size)
+        sel = in_tc & (pos[u] >= 0)
+        st, X = oracle.extend(cm[i[sel]], pos[u[sel]], p.r[sel], rows.size, p.Q0, steps, lam, lr,
+                              step)
+        assert st == 0
+        return X
+
+    g = np.random.default_rng(7)
+    F_rows = np.flatnonzero(~row_in)
+    cnt_r = np.bincount(u[in_tc & ~row_in[u]], minlength=p.m)[F_rows]
+    rows = np.union1d(g.choice(F_rows, 64, replace=False), F_rows[np.argsort(-cnt_r, kind="stable")[:2]])
+    assert rel_fro(P[rows], row_phase(rows)) <= TOL
+
+    F_cols = np.flatnonzero(~col_in)
+    cnt_c = np.bincount(i[~col_in[i]], minlength=p.n)[F_cols]
+    cols = np.union1d(g.choice(F_cols, 64, replace=False), F_cols[np.argsort(-cnt_c, kind="stable")[:2]])
+    posc = np.full(p.n, -1, np.int64)
+    posc[cols] = np.arange(cols.size)
+    sel = posc[i] >= 0
+    touched = np.unique(u[sel])
+    free_t = touched[~row_in[touched]]
+    # row factors of the touched rows: template rows from P0, free rows from the oracle
+    Psub = np.zeros((touched.size, p.k))
+    tpos = np.full(p.m, -1, np.int64)
+    tpos[p.I] = np.arange(p.I.size)
+    is_t = row_in[touched]
+    Psub[is_t] = p.P0[tpos[touched[is_t]]]
+    Psub[~is_t] = row_phase(free_t)
+    idx = np.full(p.m, -1, np.int64)
+    idx[touched] = np.arange(touched.size)
+    note(f"extension fullsize: {cols.size} columns over {touched.size} rows ({free_t.size} free)")
+    st, Xc = oracle.extend(idx[u[sel]], posc[i[sel]], p.r[sel], cols.size, Psub, steps, lam, lr, step)
+    assert st == 0
+    assert rel_fro(Q[cols], Xc) <= TOL
