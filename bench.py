@@ -59,6 +59,9 @@ def parse():
     ap.add_argument("--pass-kernel", default="auto", choices=["auto", "item", "slab"],
                     help="kernel of the P and Q passes (tsid_set_pass_kernel); auto picks the "
                          "slab pass for evenly spread fp32 templates")
+    ap.add_argument("--dense-fill", type=float, default=-1.0,
+                    help="dense head tiles of bf16 fits (tsid_set_dense_tiles): < 0 automatic, "
+                         "0 off, in (0, 1] forced with that tile fill")
     ap.add_argument("--time-every", type=int, default=10,
                     help="attach HIP timing events to the kernels of every n-th timed epoch (each "
                          "timed dispatch costs a few microseconds of wall time)")
@@ -108,6 +111,22 @@ def pass_bytes(nnz, owners, others, k, prec, no_owner_write=False):
     if no_owner_write:
         b -= fb * owners
     return b
+
+
+def dense_bytes(tiles, stripes_own, stripes_other, k):
+    """Compulsory bytes of one dense-tile launch: the tile values (fp32, 1 KiB
+    per tile), the tile list (4 B per tile and stripe), the owner rows of the
+    stripes holding a tile read once as bf16 copies and their fp32 gradient
+    sums written once, the other rows those tiles touch read once (bf16)."""
+    return (1024 + 4) * tiles + 4 * stripes_own + 16 * stripes_own * (2 * k + 4 * k) \
+        + 16 * stripes_other * 2 * k
+
+
+def dense_flops(tiles, k):
+    """Matrix-core flops of one dense-tile launch: per tile the 16 x 16 x k
+    product of the residuals and the two 16 x 16 x k products of the
+    gradient (high and low bf16 parts of the residual)."""
+    return 3 * 2 * 256 * k * tiles
 
 
 def traffic_from_profiles(kernel_src_sha, which):
@@ -224,6 +243,7 @@ def main():
 
     T = tsid.Tsid(0)
     T.set_pass_kernel(args.pass_kernel)
+    T.set_dense_tiles(args.dense_fill)
     u = torch.from_numpy(p.u).pin_memory()
     i = torch.from_numpy(p.i).pin_memory()
     r = torch.from_numpy(p.r).pin_memory()
@@ -266,22 +286,45 @@ def main():
     # updates to its finishing kernel (timed as a fixup): its own launch then
     # does not write the owner rows.
     split = tm["fixup_launches"] > 0
-    by = [pass_bytes(nnz, m_t, n_t, k, p.prec, kernels[0] == "slab" and split),
-          pass_bytes(nnz, n_t, m_t, k, p.prec, kernels[1] == "slab" and split)]
+    di = T.dense_info()
+    sparse_nnz = nnz - di["cells"]
+    by = [pass_bytes(sparse_nnz, m_t, n_t, k, p.prec, kernels[0] == "slab" and split),
+          pass_bytes(sparse_nnz, n_t, m_t, k, p.prec, kernels[1] == "slab" and split)]
+    if di["tiles"]:
+        # with dense tiles the item pass also reads the full bucket pointers
+        # (degrees) and the tile sums of the rows in stripes holding a tile
+        for j, own in ((0, m_t), (1, n_t)):
+            by[j] += 8 * (own + 1) + 4 * k * min(own, 16 * di["stripes"][j])
     avg = [tm["pass_ms"][j] / max(1, tm["pass_launches"][j]) for j in range(2)]
-    dom = 0 if tm["pass_ms"][0] >= tm["pass_ms"][1] else 1
-    achieved = by[dom] / (avg[dom] / 1e3) / 1e9
-    kname = {"item": "k_item_pass", "slab": "k_slab_pass"}[kernels[dom]]
-    ksrc = {"item": "fit.hip", "slab": "slab.hip"}[kernels[dom]]
+    cand = [(avg[0], by[0], {"item": "k_item_pass", "slab": "k_slab_pass"}[kernels[0]], "P pass",
+             {"item": "fit.hip", "slab": "slab.hip"}[kernels[0]], "p_pass", kernels[0]),
+            (avg[1], by[1], {"item": "k_item_pass", "slab": "k_slab_pass"}[kernels[1]], "Q pass",
+             {"item": "fit.hip", "slab": "slab.hip"}[kernels[1]], "q_pass", kernels[1])]
+    dense_avg = [tm["dense_ms"][j] / max(1, tm["dense_launches"][j]) for j in range(2)]
+    if di["tiles"]:
+        for j in range(2):
+            cand.append((dense_avg[j], dense_bytes(di["tiles"], di["stripes"][j], di["stripes"][1 - j], k),
+                         "k_dense_pass", ["P", "Q"][j] + " side dense tiles", "dense.hip",
+                         ["p_dense", "q_dense"][j], "dense"))
+    dom_ms, dom_by, kname, kside, ksrc, which, kkind = max(cand, key=lambda c: c[0])
+    achieved = dom_by / (dom_ms / 1e3) / 1e9
     src = open(os.path.join(ROOT, "paper_2608_00977_amd", "csrc", ksrc), "rb").read()
     sha = hashlib.sha256(src).hexdigest()
-    which = ["p_pass", "q_pass"][dom]
-    traffic = traffic_from_profiles(sha, f"{args.config}:{which}:{kernels[dom]}")
-    epoch_bytes = by[0] + by[1]
+    traffic = traffic_from_profiles(sha, f"{args.config}:{which}:{kkind}")
+    epoch_bytes = by[0] + by[1] + (sum(c[1] for c in cand[2:]) if di["tiles"] else 0)
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                "kernel": f"{kname} ({'P' if dom == 0 else 'Q'} pass)",
-                "bytes_per_launch": by[dom], "avg_launch_ms": round(avg[dom], 5)}
+                "kernel": f"{kname} ({kside})",
+                "bytes_per_launch": dom_by, "avg_launch_ms": round(dom_ms, 5)}
+    dense = None
+    if di["tiles"]:
+        fl = dense_flops(di["tiles"], k)
+        dense = {"cells": di["cells"], "tiles": di["tiles"], "stripes": di["stripes"],
+                 "share_of_cells": round(di["cells"] / max(1, nnz), 4),
+                 "flops_per_launch": fl,
+                 "mfma_TFLOPs": [round(fl / (dense_avg[j] / 1e3) / 1e12, 2) if dense_avg[j] else None
+                                 for j in range(2)],
+                 "bytes_per_launch": [cand[2][1], cand[3][1]]}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -316,13 +359,15 @@ def main():
                    "m_t": m_t, "n_t": n_t, "template_cells_train": nnz, "k": k,
                    "precision": p.prec, "step": p.step, "lr": p.lr, "lambda": p.lam,
                    "clip": p.clip, "parallelism": "single GPU",
-                   "pass_kernels": {"p_pass": kernels[0], "q_pass": kernels[1]}},
+                   "pass_kernels": {"p_pass": kernels[0], "q_pass": kernels[1]},
+                   "dense_tiles": dense},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "compulsory_GBps_per_epoch": round(epoch_bytes / (ms_per_step / 1e3) / 1e9, 2),
         "device_epoch_ms": tm["epoch_ms"] / max(1, tm["epochs"]),
         "timed_epochs": tm["epochs"],
         "kernel_ms_per_epoch": {"p_pass": avg[0], "q_pass": avg[1],
+                                "p_dense": dense_avg[0], "q_dense": dense_avg[1],
                                 "fixups": tm["fixup_ms"] / max(1, tm["epochs"]),
                                 "loss_reduce": tm["reduce_ms"] / max(1, tm["reduce_launches"]) / 16},
         "loss_first_epoch": float(hist[0]),

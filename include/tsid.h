@@ -207,6 +207,44 @@ tsid_status tsid_set_pass_kernel(tsid_ctx *ctx, int mode);
  * output may be NULL.  Errors: E_INVAL (ctx NULL). */
 tsid_status tsid_fit_pass_kernels(const tsid_ctx *ctx, int32_t *p_pass, int32_t *q_pass);
 
+/* Dense head tiles for bf16 fits (Eqs. 2-4 evaluated on the matrix cores).
+ * The template's cells are grouped into 16 x 16 tiles of the (row, column)
+ * grid; a tile holding at least fill * 256 cells is handled by a
+ * matrix-core kernel: with the tile's residuals E (zero at unobserved
+ * cells), the row-side gradient sums E Q_J and the column-side sums E^T P_I
+ * are products of a 16 x 16 tile and a 16 x k slab of factors, computed
+ * with bf16 inputs and fp32 accumulation (the residual is split into a
+ * bf16 high part and a bf16 remainder, so its fp32 value enters the
+ * product to about 2^-16 relative).  The item pass then walks only the
+ * remaining cells and adds the tile sums before the update.  The epochs are
+ * the same; rounding differs from the all-item path at the level of the
+ * bf16 factors (Section 5.3).
+ *  fill < 0   (default) automatic: fill 0.25, used when bf16, k in
+ *             {16, 32, 64, 128}, and the dense tiles hold at least 10% of
+ *             the cells.
+ *  fill = 0   off.
+ *  0 < fill <= 1  forced with this fill threshold (bf16 fits with k in
+ *             {16, 32, 64, 128}; other fits return E_INVAL).
+ * The tiles are laid out at the first bf16 fit after a template or mode
+ * change and kept with the template: 1 KiB of device memory per dense tile
+ * and side (its values, fp32, NaN at unobserved cells), the other cells'
+ * streams (8 bytes per cell and side) and a rows x k fp32 buffer of tile
+ * sums per side.  Takes effect at the next tsid_fit_template.
+ * Errors: E_INVAL (ctx NULL, fill > 1 or NaN). */
+tsid_status tsid_set_dense_tiles(tsid_ctx *ctx, float fill);
+
+/* What the last tsid_fit_template handled as dense tiles (all zero when it
+ * used none): cells in dense tiles, dense tiles, and the 16-row stripes of
+ * the P pass (stripes[0], rows of the template) and of the Q pass
+ * (stripes[1], columns) that hold at least one dense tile.
+ * Errors: E_INVAL (ctx or out NULL). */
+typedef struct {
+    int64_t cells;
+    int64_t tiles;
+    int64_t stripes[2];
+} tsid_dense_info;
+tsid_status tsid_fit_dense_info(const tsid_ctx *ctx, tsid_dense_info *out);
+
 /* Kernel timing of the template fit (a tracing aid).  With every = n > 0,
  * the kernels of every n-th epoch of tsid_fit_template (epochs 0, n, 2n, ...)
  * are launched with a start and an end HIP event attached to their dispatch
@@ -219,9 +257,10 @@ tsid_status tsid_fit_pass_kernels(const tsid_ctx *ctx, int32_t *p_pass, int32_t 
  *  (column buckets); fixup: the kernels that combine partial sums after a
  *  pass (item pass: buckets longer than one wave; slab pass: blocks split
  *  over several workgroups), which also update those rows; reduce: the
- *  batched loss reductions (one per 16 epochs); epoch_ms: from the start of
- *  a timed epoch's P pass to the end of its last pass or fixup kernel, summed
- *  over the timed epochs, whose number is `epochs`.
+ *  batched loss reductions (one per 16 epochs); dense_ms[0] / [1]: the
+ *  dense-tile kernels before the P / Q pass (tsid_set_dense_tiles);
+ *  epoch_ms: from the start of a timed epoch's first kernel to the end of
+ *  its last, summed over the timed epochs, whose number is `epochs`.
  * Errors: E_INVAL (ctx NULL or every < 0). */
 typedef struct {
     double pass_ms[2];
@@ -232,6 +271,8 @@ typedef struct {
     int64_t reduce_launches;
     double epoch_ms;
     int64_t epochs;
+    double dense_ms[2];
+    int64_t dense_launches[2];
 } tsid_timing;
 tsid_status tsid_set_timing(tsid_ctx *ctx, int every);
 tsid_status tsid_get_timing(const tsid_ctx *ctx, tsid_timing *out);

@@ -48,7 +48,12 @@ class tsid_timing(C.Structure):
     _fields_ = [("pass_ms", C.c_double * 2), ("pass_launches", C.c_int64 * 2),
                 ("fixup_ms", C.c_double), ("fixup_launches", C.c_int64),
                 ("reduce_ms", C.c_double), ("reduce_launches", C.c_int64),
-                ("epoch_ms", C.c_double), ("epochs", C.c_int64)]
+                ("epoch_ms", C.c_double), ("epochs", C.c_int64),
+                ("dense_ms", C.c_double * 2), ("dense_launches", C.c_int64 * 2)]
+
+
+class tsid_dense_info(C.Structure):
+    _fields_ = [("cells", C.c_int64), ("tiles", C.c_int64), ("stripes", C.c_int64 * 2)]
 
 
 _lib: Optional[C.CDLL] = None
@@ -76,6 +81,8 @@ def lib() -> C.CDLL:
         "tsid_set_pass_kernel": (C.c_int, [P, C.c_int]),
         "tsid_fit_pass_kernels": (C.c_int, [P, P, P]),
         "tsid_get_timing": (C.c_int, [P, C.POINTER(tsid_timing)]),
+        "tsid_set_dense_tiles": (C.c_int, [P, C.c_float]),
+        "tsid_fit_dense_info": (C.c_int, [P, C.POINTER(tsid_dense_info)]),
         "tsid_loss": (C.c_int, [P, P, P, C.c_float, P]),
         "tsid_extend_chunk": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P,
                                         C.POINTER(tsid_fit_opts)]),
@@ -157,7 +164,22 @@ def tsid_get_timing(ctx) -> dict:
     return dict(pass_ms=[t.pass_ms[0], t.pass_ms[1]],
                 pass_launches=[t.pass_launches[0], t.pass_launches[1]],
                 fixup_ms=t.fixup_ms, fixup_launches=t.fixup_launches, reduce_ms=t.reduce_ms,
-                reduce_launches=t.reduce_launches, epoch_ms=t.epoch_ms, epochs=t.epochs)
+                reduce_launches=t.reduce_launches, epoch_ms=t.epoch_ms, epochs=t.epochs,
+                dense_ms=[t.dense_ms[0], t.dense_ms[1]],
+                dense_launches=[t.dense_launches[0], t.dense_launches[1]])
+
+
+def tsid_set_dense_tiles(ctx, fill: float) -> int:
+    return lib().tsid_set_dense_tiles(ctx, float(fill))
+
+
+def tsid_fit_dense_info(ctx) -> dict:
+    """Dense tiles of the last fit: cells, tiles, stripes (P pass, Q pass)."""
+    d = tsid_dense_info()
+    st = lib().tsid_fit_dense_info(ctx, C.byref(d))
+    if st != OK:
+        raise TsidError(st, "tsid_fit_dense_info")
+    return dict(cells=d.cells, tiles=d.tiles, stripes=[d.stripes[0], d.stripes[1]])
 
 
 def tsid_loss(ctx, P, Q, lam: float, out) -> int:
@@ -274,6 +296,16 @@ class Tsid:
 
     def timing(self) -> dict:
         return tsid_get_timing(self.ctx)
+
+    def set_dense_tiles(self, fill: float):
+        """Dense head tiles of bf16 fits: fill < 0 automatic, 0 off, in (0, 1]
+        forced with that tile fill (tsid_set_dense_tiles)."""
+        self._check(tsid_set_dense_tiles(self.ctx, fill), "tsid_set_dense_tiles")
+
+    def dense_info(self) -> dict:
+        """cells, tiles and stripes (P pass, Q pass) of the last fit's dense
+        head tiles (tsid_fit_dense_info)."""
+        return tsid_fit_dense_info(self.ctx)
 
     def epochs_done(self) -> int:
         return tsid_fit_epochs_done(self.ctx)

@@ -102,6 +102,31 @@ struct SlabPlan {
     int64_t lanes() const { return units() * kSlabLanes; }
 };
 
+// Dense head tiles of a bf16 fit (dense.hip): for each side the stripe
+// pointers, the other-side tile index and the owner-major values of every
+// dense tile, the streams of the remaining (sparse) cells with their bucket
+// pointers and work plans, and the per-row dense gradient sums.
+struct DensePlan {
+    bool ready = false;
+    float fill = 0.f;          // tile fill it was built for
+    int64_t tiles = 0, cells = 0, sparse_nnz = 0;
+    int64_t stripes[2] = {0, 0};  // stripes holding a dense tile, per side
+    uint32_t *tile_ptr[2] = {nullptr, nullptr};
+    // work segments (one wave each) and the stripes split over several
+    int64_t n_segs[2] = {0, 0}, n_multi[2] = {0, 0};
+    uint32_t *seg_tile[2] = {nullptr, nullptr};
+    int32_t *seg_stripe[2] = {nullptr, nullptr};
+    uint32_t *stripe_seg[2] = {nullptr, nullptr};
+    int32_t *multi[2] = {nullptr, nullptr};
+    float *part[2] = {nullptr, nullptr};
+    int32_t *tile_other[2] = {nullptr, nullptr};
+    float *R[2] = {nullptr, nullptr};
+    int2 *sparse[2] = {nullptr, nullptr};
+    int64_t *sparse_ptr[2] = {nullptr, nullptr};
+    Plan plan[2];
+    float *gd[2] = {nullptr, nullptr};
+};
+
 struct Template {
     int64_t m = 0, n = 0, nnz = 0;
     int32_t m_t = 0, n_t = 0, k = 0;
@@ -112,6 +137,8 @@ struct Template {
     int32_t E = 64;
     Plan plan[2][2];               // [side][precision]
     SlabPlan slab[2];              // [side], fp32 only
+    DensePlan dense;               // bf16 only
+    bool dense_use = false;        // the current fit runs the dense tiles
 };
 
 // Epochs whose loss terms are kept before one batched reduction.
@@ -168,6 +195,8 @@ struct tsid_ctx {
     FitBufs fb;
     ExtState ext;
     int32_t pass_kernel = TSID_PASS_AUTO;
+    float dense_fill = -1.f;           // tsid_set_dense_tiles: < 0 auto, 0 off, > 0 fill
+    tsid_dense_info dense_used{};       // of the last fit
     int32_t used_kernel[2] = {0, 0};  // pass kernel of each side in the last fit
 };
 
@@ -177,7 +206,9 @@ void set_device(const tsid_ctx *c) { TSID_HIP(hipSetDevice(c->device)); }
 
 // Timed kernels of one epoch; each takes a start and an end event attached to
 // its dispatch (the loss reduction: start of its first kernel, end of its last).
-enum TimedKernel { TK_PPASS = 0, TK_PFIX = 1, TK_QPASS = 2, TK_QFIX = 3, TK_REDUCE = 4, kTimed = 5 };
+enum TimedKernel {
+    TK_PPASS = 0, TK_PFIX = 1, TK_QPASS = 2, TK_QFIX = 3, TK_REDUCE = 4, TK_PDENSE = 5, TK_QDENSE = 6, kTimed = 7
+};
 constexpr int kEvents = 2 * kTimed;
 
 void ensure_events(tsid_ctx *c, size_t epochs) {
@@ -210,25 +241,30 @@ void collect_timing(tsid_ctx *c, int epochs) {
     tsid_timing &t = c->tm;
     for (int ep = 0; ep < epochs; ++ep) {
         const uint8_t l = c->launched[(size_t)ep];
-        int last = -1;
         for (int k = 0; k < kTimed; ++k) {
             if (!(l & (1u << k))) continue;
             const double ms = dt(ev(ep, k, 0), ev(ep, k, 1));
             if (k == TK_PPASS || k == TK_QPASS) {
                 t.pass_ms[k / 2] += ms;
                 t.pass_launches[k / 2] += 1;
-                last = k;
             } else if (k == TK_REDUCE) {
                 t.reduce_ms += ms;
                 t.reduce_launches += 1;
+            } else if (k == TK_PDENSE || k == TK_QDENSE) {
+                t.dense_ms[k == TK_QDENSE] += ms;
+                t.dense_launches[k == TK_QDENSE] += 1;
             } else {
                 t.fixup_ms += ms;
                 t.fixup_launches += 1;
-                last = k;
             }
         }
-        if (last < 0 || !(l & (1u << TK_PPASS))) continue;  // not a sampled epoch
-        t.epoch_ms += dt(ev(ep, TK_PPASS, 0), ev(ep, last, 1));
+        if (!(l & (1u << TK_PPASS))) continue;  // not a sampled epoch
+        // an epoch runs dense P, P pass, P fixup, dense Q, Q pass, Q fixup in that order
+        const int first = (l & (1u << TK_PDENSE)) ? (int)TK_PDENSE : (int)TK_PPASS;
+        int end_k = TK_PPASS;
+        for (int k : {TK_PPASS, TK_PFIX, TK_QDENSE, TK_QPASS, TK_QFIX})
+            if (l & (1u << k)) end_k = k;
+        t.epoch_ms += dt(ev(ep, first, 0), ev(ep, end_k, 1));
         t.epochs += 1;
     }
 }
@@ -248,6 +284,27 @@ tsid_status guarded(tsid_ctx *c, F &&f) {
         c->err = e.what();
         return TSID_E_DEVICE;
     }
+}
+
+void free_dense(tsid_ctx *c, DensePlan &d) {
+    Arena &A = c->arena;
+    for (int sd = 0; sd < 2; ++sd) {
+        A.release(d.tile_ptr[sd]);
+        A.release(d.tile_other[sd]);
+        A.release(d.R[sd]);
+        A.release(d.sparse[sd]);
+        A.release(d.sparse_ptr[sd]);
+        A.release(d.plan[sd].item_off);
+        A.release(d.plan[sd].item_end);
+        A.release(d.plan[sd].items);
+        A.release(d.gd[sd]);
+        A.release(d.seg_tile[sd]);
+        A.release(d.seg_stripe[sd]);
+        A.release(d.stripe_seg[sd]);
+        A.release(d.multi[sd]);
+        A.release(d.part[sd]);
+    }
+    d = DensePlan{};
 }
 
 void free_template(tsid_ctx *c, Template *&t) {
@@ -270,6 +327,7 @@ void free_template(tsid_ctx *c, Template *&t) {
         A.release(sp.stream);
         A.release(sp.carry);
     }
+    free_dense(c, t->dense);
     delete t;
     t = nullptr;
 }
@@ -537,14 +595,8 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
 // multiple of p (idle pad items fill the gaps), so they never straddle two
 // waves and their partial sums are combined inside the pass; only buckets of
 // more than one wave leave partial sums for the fixup kernel.
-void ensure_plan(tsid_ctx *c, int side, int prec) {
-    Template &t = *c->tpl;
-    Plan &pl = t.plan[side][prec];
-    if (pl.ready) return;
-    const std::vector<int64_t> &ptr = t.hptr[side];
-    const int32_t rows = side ? t.n_t : t.m_t;
-    const int64_t ng = items_per_wave(t.k, prec);
-    int64_t E = t.E, maxdeg = 0;
+Plan build_plan(tsid_ctx *c, const std::vector<int64_t> &ptr, int32_t rows, int64_t E, int64_t ng) {
+    int64_t maxdeg = 0;
     for (int32_t x = 0; x < rows; ++x) maxdeg = std::max(maxdeg, ptr[x + 1] - ptr[x]);
     // When items up to twice the default length keep every bucket within one
     // wave, take them: no bucket then needs the fixup kernel.
@@ -594,6 +646,7 @@ void ensure_plan(tsid_ctx *c, int side, int prec) {
         A.release(d_items);
         throw;
     }
+    Plan pl;
     pl.item_off = d_off;
     pl.item_end = d_end;
     pl.items = d_items;
@@ -601,6 +654,15 @@ void ensure_plan(tsid_ctx *c, int side, int prec) {
     pl.E = (int32_t)E;
     pl.spans = spans;
     pl.ready = true;
+    return pl;
+}
+
+void ensure_plan(tsid_ctx *c, int side, int prec) {
+    Template &t = *c->tpl;
+    Plan &pl = t.plan[side][prec];
+    if (pl.ready) return;
+    const int32_t rows = side ? t.n_t : t.m_t;
+    pl = build_plan(c, t.hptr[side], rows, t.E, items_per_wave(t.k, prec));
 }
 
 // Whether the slab pass suits one side of the template: the expected number
@@ -693,7 +755,201 @@ void ensure_slab(tsid_ctx *c, int side, int prec) {
     sp.use = want;
 }
 
-void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs) {
+// Work segments of one side: a stripe's tile list is cut into
+// ceil(len / L) near-equal runs of consecutive tiles, L = max(seg_min,
+// ceil(len / seg_max)), so that a long stripe (a Zipf head row block meets
+// nearly every other block) spreads over up to seg_max waves and a short one
+// takes one.  Also counts the stripes that hold a tile.
+#ifndef TSID_DENSE_SEG_MIN
+#define TSID_DENSE_SEG_MIN 16
+#endif
+#ifndef TSID_DENSE_SEG_MAX
+#define TSID_DENSE_SEG_MAX 64
+#endif
+void dense_segments(tsid_ctx *c, DensePlan &d, int sd, const std::vector<uint32_t> &tp) {
+    const int64_t n_st = (int64_t)tp.size() - 1;
+    std::vector<uint32_t> seg_tile, stripe_seg((size_t)n_st + 1);
+    std::vector<int32_t> seg_stripe, multi;
+    for (int64_t x = 0; x < n_st; ++x) {
+        stripe_seg[(size_t)x] = (uint32_t)seg_stripe.size();
+        const int64_t len = (int64_t)tp[(size_t)x + 1] - tp[(size_t)x];
+        if (len <= 0) continue;
+        d.stripes[sd] += 1;
+        const int64_t L = std::max<int64_t>(TSID_DENSE_SEG_MIN, (len + TSID_DENSE_SEG_MAX - 1) / TSID_DENSE_SEG_MAX);
+        const int64_t n = (len + L - 1) / L;
+        for (int64_t q = 0; q < n; ++q) {
+            seg_tile.push_back(tp[(size_t)x] + (uint32_t)(q * len / n));
+            seg_stripe.push_back((int32_t)x);
+        }
+        if (n > 1) multi.push_back((int32_t)x);
+    }
+    stripe_seg[(size_t)n_st] = (uint32_t)seg_stripe.size();
+    seg_tile.push_back(tp[(size_t)n_st]);
+    Arena &A = c->arena;
+    hipStream_t cs = c->comp;
+    const int64_t ns = (int64_t)seg_stripe.size();
+    d.n_segs[sd] = ns;
+    d.n_multi[sd] = (int64_t)multi.size();
+    d.seg_tile[sd] = A.alloc<uint32_t>(ns + 1);
+    d.seg_stripe[sd] = A.alloc<int32_t>(std::max<int64_t>(ns, 1));
+    d.stripe_seg[sd] = A.alloc<uint32_t>(n_st + 1);
+    d.multi[sd] = A.alloc<int32_t>(std::max<int64_t>(d.n_multi[sd], 1));
+    d.part[sd] = d.n_multi[sd] ? A.alloc<float>(ns * 16 * c->tpl->k) : nullptr;
+    TSID_HIP(hipMemcpyAsync(d.seg_tile[sd], seg_tile.data(), seg_tile.size() * 4, hipMemcpyHostToDevice, cs));
+    if (ns)
+        TSID_HIP(hipMemcpyAsync(d.seg_stripe[sd], seg_stripe.data(), (size_t)ns * 4, hipMemcpyHostToDevice, cs));
+    TSID_HIP(hipMemcpyAsync(d.stripe_seg[sd], stripe_seg.data(), stripe_seg.size() * 4, hipMemcpyHostToDevice, cs));
+    if (!multi.empty())
+        TSID_HIP(hipMemcpyAsync(d.multi[sd], multi.data(), multi.size() * 4, hipMemcpyHostToDevice, cs));
+    TSID_HIP(hipStreamSynchronize(cs));  // the host vectors go out of scope
+}
+
+// Builds the dense head tiles of the template for tile fill `fill` (a tile is
+// dense when it holds at least ceil(fill * 256) cells): tile counts, flags and
+// their prefix sums in both orientations, the tile lists, the owner-major
+// tile values, the sparse streams of the other cells with their pointers and
+// work plans, and the dense gradient buffers.
+void build_dense(tsid_ctx *c, float fill) {
+    Template &t = *c->tpl;
+    DensePlan &d = t.dense;
+    free_dense(c, d);
+    Arena &A = c->arena;
+    hipStream_t cs = c->comp;
+    const int K = t.k;
+    const int64_t n_ti = (t.m_t + 15) / 16, n_tj = (t.n_t + 15) / 16, NT = n_ti * n_tj;
+    const uint32_t thr = std::max<uint32_t>(1u, (uint32_t)std::ceil(fill * 256.f));
+    uint32_t *cnt = nullptr, *flag_p = nullptr, *idx_p = nullptr, *flag_q = nullptr, *idx_q = nullptr;
+    uint32_t *scratch = nullptr, *total = nullptr;
+    int64_t *cnt_sp[2] = {nullptr, nullptr};
+    auto cleanup = [&]() {
+        (void)hipStreamSynchronize(cs);
+        A.release(cnt);
+        A.release(flag_p);
+        A.release(idx_p);
+        A.release(flag_q);
+        A.release(idx_q);
+        A.release(scratch);
+        A.release(total);
+        A.release(cnt_sp[0]);
+        A.release(cnt_sp[1]);
+    };
+    try {
+        d.fill = fill;
+        if (NT > 0 && t.nnz > 0) {
+            cnt = A.alloc<uint32_t>(NT);
+            flag_p = A.alloc<uint32_t>(NT);
+            idx_p = A.alloc<uint32_t>(NT);
+            flag_q = A.alloc<uint32_t>(NT);
+            idx_q = A.alloc<uint32_t>(NT);
+            scratch = A.alloc<uint32_t>((int64_t)scan_scratch_elems(NT));
+            total = A.alloc<uint32_t>(2);
+            TSID_HIP(hipMemsetAsync(cnt, 0, (size_t)NT * 4, cs));
+            tile_count(t.stream_r, t.row_ptr, t.m_t, n_tj, cnt, cs);
+            tile_flag(cnt, n_ti, n_tj, thr, false, flag_p, cs);
+            scan_u32(flag_p, idx_p, NT, total, scratch, cs);
+            tile_flag(cnt, n_ti, n_tj, thr, true, flag_q, cs);
+            scan_u32(flag_q, idx_q, NT, total + 1, scratch, cs);
+            uint32_t h_total = 0;
+            TSID_HIP(hipMemcpyAsync(&h_total, total, 4, hipMemcpyDeviceToHost, cs));
+            TSID_HIP(hipStreamSynchronize(cs));
+            d.tiles = h_total;
+        }
+        const int64_t nd = d.tiles;
+        const int32_t rows[2] = {t.m_t, t.n_t};
+        const int64_t stripes[2] = {n_ti, n_tj}, others[2] = {n_tj, n_ti};
+        for (int sd = 0; sd < 2; ++sd) {
+            d.tile_ptr[sd] = A.alloc<uint32_t>(stripes[sd] + 1);
+            d.tile_other[sd] = A.alloc<int32_t>(std::max<int64_t>(nd, 1));
+            d.R[sd] = A.alloc<float>(std::max<int64_t>(nd, 1) * 256);
+            d.gd[sd] = A.alloc<float>((int64_t)rows[sd] * K);
+            d.sparse_ptr[sd] = A.alloc<int64_t>((int64_t)rows[sd] + 1);
+            cnt_sp[sd] = A.alloc<int64_t>(std::max<int32_t>(rows[sd], 1));
+        }
+        std::vector<int64_t> hsp[2];
+        if (nd > 0) {
+            tile_list(flag_p, idx_p, n_ti, n_tj, d.tile_other[0], d.tile_ptr[0], cs);
+            tile_list(flag_q, idx_q, n_tj, n_ti, d.tile_other[1], d.tile_ptr[1], cs);
+            for (int sd = 0; sd < 2; ++sd) {
+                std::vector<uint32_t> tp((size_t)stripes[sd] + 1);
+                TSID_HIP(hipMemcpyAsync(tp.data(), d.tile_ptr[sd], (size_t)stripes[sd] * 4, hipMemcpyDeviceToHost,
+                                        cs));
+                TSID_HIP(hipStreamSynchronize(cs));
+                tp[(size_t)stripes[sd]] = (uint32_t)nd;
+                dense_segments(c, d, sd, tp);
+            }
+            fill_nan(d.R[0], nd * 256, cs);
+            fill_nan(d.R[1], nd * 256, cs);
+            sparse_count(t.stream_r, t.row_ptr, t.m_t, 0, n_tj, flag_p, cnt_sp[0], cs);
+            sparse_count(t.stream_c, t.col_ptr, t.n_t, 1, n_tj, flag_p, cnt_sp[1], cs);
+        }
+        const uint32_t h_nd = (uint32_t)nd;
+        for (int sd = 0; sd < 2; ++sd) {
+            TSID_HIP(hipMemcpyAsync(d.tile_ptr[sd] + stripes[sd], &h_nd, 4, hipMemcpyHostToDevice, cs));
+            if (nd == 0) TSID_HIP(hipMemsetAsync(d.tile_ptr[sd], 0, (size_t)stripes[sd] * 4, cs));
+            std::vector<int64_t> cnt_h((size_t)rows[sd]);
+            if (nd > 0 && rows[sd] > 0) {
+                TSID_HIP(hipMemcpyAsync(cnt_h.data(), cnt_sp[sd], (size_t)rows[sd] * 8, hipMemcpyDeviceToHost, cs));
+            } else {
+                for (int32_t x = 0; x < rows[sd]; ++x) cnt_h[(size_t)x] = t.hptr[sd][x + 1] - t.hptr[sd][x];
+            }
+            TSID_HIP(hipStreamSynchronize(cs));
+            hsp[sd].resize((size_t)rows[sd] + 1);
+            hsp[sd][0] = 0;
+            for (int32_t x = 0; x < rows[sd]; ++x) hsp[sd][x + 1] = hsp[sd][x] + cnt_h[(size_t)x];
+            TSID_HIP(hipMemcpyAsync(d.sparse_ptr[sd], hsp[sd].data(), ((size_t)rows[sd] + 1) * 8,
+                                    hipMemcpyHostToDevice, cs));
+            d.sparse[sd] = A.alloc<int2>(std::max<int64_t>(hsp[sd][(size_t)rows[sd]], 1));
+        }
+        d.sparse_nnz = hsp[0][(size_t)t.m_t];
+        d.cells = t.nnz - d.sparse_nnz;
+        if (nd > 0) {
+            tile_split(t.stream_r, t.row_ptr, t.m_t, 0, n_ti, n_tj, flag_p, idx_p, flag_q, idx_q, d.R[0], d.R[1],
+                       d.sparse_ptr[0], d.sparse[0], cs);
+            tile_split(t.stream_c, t.col_ptr, t.n_t, 1, n_ti, n_tj, flag_p, idx_p, flag_q, idx_q, d.R[0], d.R[1],
+                       d.sparse_ptr[1], d.sparse[1], cs);
+        } else {
+            for (int sd = 0; sd < 2; ++sd)
+                if (t.nnz)
+                    TSID_HIP(hipMemcpyAsync(d.sparse[sd], sd ? t.stream_c : t.stream_r, (size_t)t.nnz * 8,
+                                            hipMemcpyDeviceToDevice, cs));
+        }
+        TSID_HIP(hipStreamSynchronize(cs));
+        const int64_t ng = items_per_wave(K, TSID_BF16);
+        for (int sd = 0; sd < 2; ++sd) d.plan[sd] = build_plan(c, hsp[sd], rows[sd], choose_E(d.sparse_nnz), ng);
+        d.ready = true;
+    } catch (...) {
+        cleanup();
+        free_dense(c, d);
+        throw;
+    }
+    cleanup();
+}
+
+// Whether the current fit runs the dense head tiles: bf16 factors, k in
+// {16, 32, 64, 128}, and either a forced tile fill (tsid_set_dense_tiles) or
+// the default fill 1/4 with at least a tenth of the cells in dense tiles.
+#ifndef TSID_DENSE_FILL
+#define TSID_DENSE_FILL 0.25f
+#endif
+#ifndef TSID_DENSE_MIN_SHARE
+#define TSID_DENSE_MIN_SHARE 0.10
+#endif
+void ensure_dense(tsid_ctx *c, int prec) {
+    Template &t = *c->tpl;
+    const float mode = c->dense_fill;
+    t.dense_use = false;
+    if (mode == 0.f) return;
+    if (!dense_supported(t.k, prec)) {
+        if (mode > 0.f) fail(TSID_E_INVAL, "dense tiles need bf16 factors and k in {16, 32, 64, 128}");
+        return;
+    }
+    const float fill = mode > 0.f ? mode : TSID_DENSE_FILL;
+    if (!t.dense.ready || t.dense.fill != fill) build_dense(c, fill);
+    t.dense_use = mode > 0.f ? true : t.dense.cells >= TSID_DENSE_MIN_SHARE * (double)t.nnz && t.dense.tiles > 0;
+}
+
+// dense: whether a fit is about to run (the loss evaluation uses no tiles)
+void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs, bool dense) {
     Template &t = *c->tpl;
     FitBufs &f = c->fb;
     Arena &A = c->arena;
@@ -702,6 +958,10 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs) {
     ensure_plan(c, 1, prec);
     ensure_slab(c, 0, prec);
     ensure_slab(c, 1, prec);
+    if (dense)
+        ensure_dense(c, prec);
+    else
+        t.dense_use = false;
     if (!f.P[0]) {
         for (int b = 0; b < 2; ++b) {
             f.P[b] = A.alloc<float>(lp);
@@ -712,7 +972,9 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs) {
         f.partial = A.alloc<double>((int64_t)reduce_scratch_elems(kLossRing));
     }
     const int64_t need = std::max({(int64_t)t.plan[0][prec].n_items, (int64_t)t.plan[1][prec].n_items,
-                                   t.slab[0].use ? t.slab[0].lanes() : 0, t.slab[1].use ? t.slab[1].lanes() : 0});
+                                   t.slab[0].use ? t.slab[0].lanes() : 0, t.slab[1].use ? t.slab[1].lanes() : 0,
+                                   t.dense_use ? (int64_t)t.dense.plan[0].n_items + t.dense.n_segs[0] : 0,
+                                   t.dense_use ? (int64_t)t.dense.plan[1].n_items : 0});
     if (need > f.item_cap) {  // partial sums and per-item e^2, sized for this precision's plans
         A.release(f.carry_r);
         A.release(f.carry_c);
@@ -738,9 +1000,14 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs) {
 
 PassArgs pass_args(const Template &t, int side, const tsid_fit_opts &o, int32_t *err) {
     PassArgs a{};
-    const Plan &pl = t.plan[side][o.prec];
-    a.stream = side ? t.stream_c : t.stream_r;
-    a.ptr = side ? t.col_ptr : t.row_ptr;
+    // with dense head tiles the item pass walks the other cells only
+    const bool dn = t.dense_use && o.prec == TSID_BF16;
+    const Plan &pl = dn ? t.dense.plan[side] : t.plan[side][o.prec];
+    a.stream = dn ? t.dense.sparse[side] : (side ? t.stream_c : t.stream_r);
+    a.ptr = dn ? t.dense.sparse_ptr[side] : (side ? t.col_ptr : t.row_ptr);
+    a.dptr = dn ? (side ? t.col_ptr : t.row_ptr) : nullptr;
+    a.gd = dn ? t.dense.gd[side] : nullptr;
+    a.gd_tile_ptr = dn ? t.dense.tile_ptr[side] : nullptr;
     a.items = pl.items;
     a.item_off = pl.item_off;
     a.item_end = pl.item_end;
@@ -754,6 +1021,25 @@ PassArgs pass_args(const Template &t, int side, const tsid_fit_opts &o, int32_t 
     a.xi = o.clip_xi;
     a.clip = o.clip;
     a.degree = o.step == TSID_STEP_DEGREE;
+    a.err = err;
+    return a;
+}
+
+DenseArgs dense_args(const Template &t, int side, int32_t *err) {
+    DenseArgs a{};
+    const DensePlan &d = t.dense;
+    a.rows = side ? t.n_t : t.m_t;
+    a.y_rows = side ? t.m_t : t.n_t;
+    a.n_segs = d.n_segs[side];
+    a.seg_tile = d.seg_tile[side];
+    a.seg_stripe = d.seg_stripe[side];
+    a.stripe_seg = d.stripe_seg[side];
+    a.tile_other = d.tile_other[side];
+    a.R = d.R[side];
+    a.gd = d.gd[side];
+    a.part = d.part[side];
+    a.multi = d.multi[side];
+    a.n_multi = d.n_multi[side];
     a.err = err;
     return a;
 }
@@ -784,7 +1070,7 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     check_opts(o);
     Template &t = *c->tpl;
     if ((t.m_t && !P) || (t.n_t && !Q)) fail(TSID_E_INVAL, "NULL factor pointer");
-    ensure_fit_buffers(c, o->prec, o->epochs);
+    ensure_fit_buffers(c, o->prec, o->epochs, true);
     c->epochs_done = 0;
     FitBufs &f = c->fb;
     hipStream_t cs = c->comp;
@@ -802,13 +1088,21 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     SlabArgs sr = slab_args(t, 0, *o, c->err_dev), sc = slab_args(t, 1, *o, c->err_dev);
     sr.skip_after_nonfinite = sc.skip_after_nonfinite = 1;
     const SlabPlan &sp_r = t.slab[0], &sp_c = t.slab[1];
+    const bool dn = t.dense_use && prec == TSID_BF16;
+    DenseArgs dr = dense_args(t, 0, c->err_dev), dc = dense_args(t, 1, c->err_dev);
+    dr.skip_after_nonfinite = dc.skip_after_nonfinite = 1;
+    c->dense_used = tsid_dense_info{};
+    if (dn) c->dense_used = tsid_dense_info{t.dense.cells, t.dense.tiles, {t.dense.stripes[0], t.dense.stripes[1]}};
     c->used_kernel[0] = sp_r.use ? TSID_PASS_SLAB : TSID_PASS_ITEM;
     c->used_kernel[1] = sp_c.use ? TSID_PASS_SLAB : TSID_PASS_ITEM;
     if (c->timing) ensure_events(c, (size_t)T);
     // Loss terms of epoch ep go to ring slot ep % kLossRing; a full ring (and
     // the end of the fit) is reduced in one batch into f.loss.
     const bool want_loss = loss_hist != nullptr;
-    const int64_t ne = sp_r.use ? sp_r.lanes() : t.plan[0][prec].n_items;
+    // loss terms per epoch: one per item of the P pass (or per lane of the
+    // slab pass), then with dense tiles one per work segment
+    const int64_t ne_items = sp_r.use ? sp_r.lanes() : (int64_t)ar.n_items;
+    const int64_t ne = ne_items + (dn ? dr.n_segs : 0);
     int pend = 0;  // first epoch whose loss is not reduced yet
     auto flush = [&](int upto, std::pair<hipEvent_t, hipEvent_t> ev) {
         launch_loss_reduce(f.e2, f.item_cap, ne, f.normP, t.m_t, f.normQ, t.n_t, o->lambda, upto - pend,
@@ -834,6 +1128,14 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
                 launch_slab_finish(K, sr, cs, ev.first, ev.second);
             }
         } else {
+            if (dn && dr.n_segs) {
+                dr.epoch = ep;
+                dr.X = f.Pb[cur];
+                dr.Y = f.Qb[cur];
+                dr.e2 = e2 ? e2 + ne_items : nullptr;
+                auto evd = timed(c, ep, TK_PDENSE);
+                launch_dense_pass(K, false, dr, cs, evd.first, evd.second);
+            }
             ar.epoch = ep;
             ar.X = f.P[cur];
             ar.Y = prec ? (const void *)f.Qb[cur] : (const void *)f.Q[cur];
@@ -843,7 +1145,7 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
             ar.e2 = e2;
             ar.norm = normp;
             launch_item_pass(K, prec, false, ar, cs, ev.first, ev.second);
-            if (t.plan[0][prec].spans) {
+            if ((dn ? t.dense.plan[0] : t.plan[0][prec]).spans) {
                 ev = timed(c, ep, TK_PFIX);
                 launch_fixup(K, prec, ar, cs, ev.first, ev.second);
             }
@@ -864,6 +1166,14 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
                 launch_slab_finish(K, sc, cs, ev.first, ev.second);
             }
         } else {
+            if (dn && dc.n_segs) {
+                dc.epoch = ep;
+                dc.X = f.Qb[cur];
+                dc.Y = f.Pb[cur];
+                dc.e2 = nullptr;
+                auto evd = timed(c, ep, TK_QDENSE);
+                launch_dense_pass(K, false, dc, cs, evd.first, evd.second);
+            }
             ac.epoch = ep;
             ac.X = f.Q[cur];
             ac.Y = prec ? (const void *)f.Pb[cur] : (const void *)f.P[cur];
@@ -873,7 +1183,7 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
             ac.e2 = nullptr;
             ac.norm = normq;
             launch_item_pass(K, prec, false, ac, cs, ev.first, ev.second);
-            if (t.plan[1][prec].spans) {
+            if ((dn ? t.dense.plan[1] : t.plan[1][prec]).spans) {
                 ev = timed(c, ep, TK_QFIX);
                 launch_fixup(K, prec, ac, cs, ev.first, ev.second);
             }
@@ -892,6 +1202,13 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
             sr.norm = f.normP + (int64_t)slot * t.m_t;
             launch_slab_pass(K, true, sr, sp_r.units(), cs);
         } else {
+            if (dn && dr.n_segs) {
+                dr.epoch = T;
+                dr.X = f.Pb[fin];
+                dr.Y = f.Qb[fin];
+                dr.e2 = f.e2 + slot * f.item_cap + ne_items;
+                launch_dense_pass(K, true, dr, cs);
+            }
             ar.epoch = T;
             ar.X = f.P[fin];
             ar.Y = prec ? (const void *)f.Qb[fin] : (const void *)f.Q[fin];
@@ -929,7 +1246,7 @@ void loss(tsid_ctx *c, const float *P, const float *Q, float lambda, double *out
     if (!(lambda >= 0.f) || !std::isfinite(lambda)) fail(TSID_E_INVAL, "lambda must be finite and >= 0");
     check_aligned(P, "P");
     check_aligned(Q, "Q");
-    ensure_fit_buffers(c, TSID_FP32, 0);
+    ensure_fit_buffers(c, TSID_FP32, 0, false);
     FitBufs &f = c->fb;
     hipStream_t cs = c->comp;
     tsid_fit_opts o{0, lambda, 1.f, 1.f, 0, TSID_FP32, TSID_STEP_SUM};
@@ -1211,6 +1528,18 @@ tsid_status tsid_fit_pass_kernels(const tsid_ctx *c, int32_t *p_pass, int32_t *q
     if (!c) return TSID_E_INVAL;
     if (p_pass) *p_pass = c->used_kernel[0];
     if (q_pass) *q_pass = c->used_kernel[1];
+    return TSID_OK;
+}
+
+tsid_status tsid_set_dense_tiles(tsid_ctx *c, float fill) {
+    if (!c || !(fill <= 1.f)) return TSID_E_INVAL;  // NaN fails the comparison
+    c->dense_fill = fill < 0.f ? -1.f : fill;
+    return TSID_OK;
+}
+
+tsid_status tsid_fit_dense_info(const tsid_ctx *c, tsid_dense_info *out) {
+    if (!c || !out) return TSID_E_INVAL;
+    *out = c->dense_used;
     return TSID_OK;
 }
 

@@ -150,7 +150,21 @@ __device__ __forceinline__ bool skip_epoch(const PassArgs &A) {
 // normalisation and the Section 5.3 clip, for this lane's V coordinates.
 template <int G, int V, bool BF16>
 __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg, const float (&x)[V],
-                                             const float (&acc)[V], int64_t deg) {
+                                             const float (&acc_in)[V], int64_t deg) {
+    float acc[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) acc[v] = acc_in[v];
+    if (A.dptr) {
+        // dense head tiles: the stream holds the other cells only; the degree
+        // counts every cell and the tiles' gradient sums are added here
+        deg = A.dptr[row + 1] - A.dptr[row];
+        if (A.gd_tile_ptr[(row >> 4) + 1] > A.gd_tile_ptr[row >> 4]) {
+            float g[V];
+            load_f32<V>(A.gd + (int64_t)row * (G * V) + lg * V, g);
+#pragma unroll
+            for (int v = 0; v < V; ++v) acc[v] += g[v];
+        }
+    }
     const float s = A.degree ? 1.0f / (float)(deg > 1 ? deg : 1) : 1.0f;
     float xn[V];
     bool bad = false;

@@ -110,6 +110,13 @@ struct PassArgs {
     int32_t *err;            // device error slots
     int32_t epoch;           // a non-finite update stores epoch + 1 in err[ERR_NONFINITE]
     int32_t skip_after_nonfinite;  // 1: do nothing if an earlier epoch stored a flag
+    // With dense head tiles (bf16): the stream holds the cells outside them,
+    // dptr gives each bucket's full degree (for the degree step), and gd the
+    // dense cells' gradient sums of the rows whose 16-row stripe has dense
+    // tiles (gd_tile_ptr[st + 1] > gd_tile_ptr[st]), added before the update.
+    const int64_t *dptr;     // or null: degrees from ptr
+    const float *gd;         // rows x K, or null
+    const uint32_t *gd_tile_ptr;
 };
 
 // prec: 0 fp32, 1 bf16.  loss_only: residuals, e2 and norms only.
@@ -189,5 +196,47 @@ void launch_slab_pass(int K, bool loss_only, const SlabArgs &a, int64_t n_units,
                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 void launch_slab_finish(int K, const SlabArgs &a, hipStream_t s, hipEvent_t ev0 = nullptr,
                         hipEvent_t ev1 = nullptr);
+
+// ----------------------------------------------------------- dense tiles
+struct DenseArgs {
+    const uint16_t *X;        // owner side bf16 copy (rows x K)
+    const uint16_t *Y;        // other side bf16 copy (y_rows x K)
+    int64_t rows, y_rows;
+    // Work: segments of at most a few dozen consecutive dense tiles of one
+    // stripe (16 owner rows), one wave each.
+    int64_t n_segs;
+    const uint32_t *seg_tile;   // tiles of segment g: seg_tile[g] .. seg_tile[g + 1]
+    const int32_t *seg_stripe;  // stripe of segment g
+    const uint32_t *stripe_seg; // segments of stripe s: stripe_seg[s] .. stripe_seg[s + 1]
+    const int32_t *tile_other;  // other-side tile index (t0 / 16) of each dense tile
+    const float *R;             // dense tiles, owner-major 16 x 16 fp32, NaN = not observed
+    float *gd;                  // rows x K: gradient sums of the dense cells (stripes with tiles)
+    float *part;                // n_segs x 16 x K: partial sums of segments of split stripes
+    const int32_t *multi;       // stripes with more than one segment
+    int64_t n_multi;
+    float *e2;                  // per segment residual sum of squares, or null
+    int32_t *err;
+    int32_t epoch;
+    int32_t skip_after_nonfinite;
+};
+
+// bf16 factors with k in {16, 32, 64, 128}.
+bool dense_supported(int K, int prec);
+// The tile kernel, then (when a stripe has several segments) the kernel that
+// adds their partial sums in segment order; ev0 / ev1 bracket both.
+void launch_dense_pass(int K, bool loss_only, const DenseArgs &a, hipStream_t s, hipEvent_t ev0 = nullptr,
+                       hipEvent_t ev1 = nullptr);
+// Build steps (see dense.hip).  Tiles: t = ti * n_tj + tj over 16 x 16 blocks.
+void tile_count(const int2 *stream, const int64_t *ptr, int32_t rows, int64_t n_tj, uint32_t *cnt, hipStream_t s);
+void tile_flag(const uint32_t *cnt, int64_t n_ti, int64_t n_tj, uint32_t thr, bool transpose, uint32_t *flag,
+               hipStream_t s);
+void tile_list(const uint32_t *flag, const uint32_t *idx, int64_t n_stripes, int64_t n_other, int32_t *tile_other,
+               uint32_t *tile_ptr, hipStream_t s);
+void sparse_count(const int2 *stream, const int64_t *ptr, int32_t rows, int side, int64_t n_tj,
+                  const uint32_t *flag_p, int64_t *count, hipStream_t s);
+void tile_split(const int2 *stream, const int64_t *ptr, int32_t rows, int side, int64_t n_ti, int64_t n_tj,
+                const uint32_t *flag_p, const uint32_t *idx_p, const uint32_t *flag_q, const uint32_t *idx_q,
+                float *Rp, float *Rq, const int64_t *sparse_ptr, int2 *sparse, hipStream_t s);
+void fill_nan(float *p, int64_t n, hipStream_t s);
 
 }  // namespace tsid

@@ -31,6 +31,26 @@ def _sampled_parity(T, p, n_rows=64, n_cols=64, tol=1e-4):
     rows = np.union1d(g.choice(p.I.size, n_rows, replace=False), top_r)
     cols = np.union1d(g.choice(p.J.size, n_cols, replace=False), top_c)
     bf16 = p.prec == "bf16"
+    if bf16:
+        # the automatic rule takes the dense head tiles (16 x 16 tiles at
+        # least a quarter full) when they hold a tenth of the cells: the
+        # library's count must equal one made here, and rows of stripes with
+        # tiles join the sample
+        n_ti, n_tj = (p.I.size + 15) // 16, (p.J.size + 15) // 16
+        cnt = np.bincount((a // 16).astype(np.int64) * n_tj + b // 16, minlength=n_ti * n_tj)
+        dense = (cnt >= 64).reshape(n_ti, n_tj)
+        cells = int(cnt[cnt >= 64].sum())
+        del cnt
+        info = T.dense_info()
+        if cells >= 0.10 * a.size:
+            assert info["cells"] == cells and info["tiles"] == int(dense.sum())
+            sr = np.flatnonzero(dense.any(axis=1))
+            sc = np.flatnonzero(dense.any(axis=0))
+            rows = np.union1d(rows, np.minimum(g.choice(sr, 16) * 16 + g.integers(0, 16, 16), p.I.size - 1))
+            cols = np.union1d(cols, np.minimum(g.choice(sc, 16) * 16 + g.integers(0, 16, 16), p.J.size - 1))
+        else:
+            assert info["tiles"] == 0
+        del dense
     mask = np.zeros(p.I.size, dtype=bool)
     mask[rows] = True
     sel = mask[a]
