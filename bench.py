@@ -73,6 +73,10 @@ def parse():
                          "a second JSON line; needs a workload with the whole matrix drawn "
                          "(rating, mid, tiny)")
     ap.add_argument("--extend-steps", type=int, default=20)
+    ap.add_argument("--extend-solver", default="steps", choices=["steps", "ridge"],
+                    help="extension solver: one-sided gradient steps (tsid_extend_chunk) or the "
+                         "exact ridge solve per free row (tsid_extend_chunk_ridge, fp64 Gram on the "
+                         "matrix cores + Cholesky), both with the fit's lambda")
     ap.add_argument("--copy-probe", action="store_true",
                     help="time a plain device copy of 1 GiB instead (HBM probe and the "
                          "reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -189,9 +193,14 @@ def extension_line(args, p, T, P, Q):
     t0 = time.perf_counter()
     ext = Extension(p.m, p.n, p.u, p.i, p.r, p.I, p.J, n_chunks=16)
     prep_s = time.perf_counter() - t0
-    # one-sided steps from zero: lr 0.05 keeps a free row with a single cell stable
-    opts = tsid.make_opts(epochs=args.extend_steps, lam=p.lam, lr=0.05, clip=p.clip, xi=p.xi,
-                          step="degree")
+    if args.extend_solver == "ridge":
+        opts = float(p.lam)  # exact solve per free row
+        how = f"exact ridge solve per free row (lambda {p.lam}, fp64 Gram + Cholesky)"
+    else:
+        # one-sided steps from zero: lr 0.05 keeps a free row with a single cell stable
+        opts = tsid.make_opts(epochs=args.extend_steps, lam=p.lam, lr=0.05, clip=p.clip, xi=p.xi,
+                              step="degree")
+        how = f"{args.extend_steps} one-sided steps per chunk, degree step"
     ext.run(T, P, Q, opts)  # warm-up (allocations, code load)
     _, _, ph = ext.run(T, P, Q, opts)
     n_row, n_col = ext.rows.nnz, ext.cols.nnz
@@ -208,8 +217,8 @@ def extension_line(args, p, T, P, Q):
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": f"{p.name}: extension of the {p.I.size} x {p.J.size} template to "
-                               f"{p.m} x {p.n}, 16 chunks per phase, {args.extend_steps} one-sided "
-                               "steps per chunk, degree step, fixed factors fp32",
+                               f"{p.m} x {p.n}, 16 chunks per phase, {how}, fixed factors fp32",
+                   "solver": args.extend_solver,
                    "row_phase_cells": n_row, "col_phase_cells": n_col,
                    "row_chunks": ext.rows.bounds.size - 1, "col_chunks": ext.cols.bounds.size - 1},
         "row_phase_s": ph["row_phase_s"],

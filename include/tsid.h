@@ -178,6 +178,28 @@ tsid_status tsid_extend_chunk(tsid_ctx *ctx, int side, const int32_t *fixed_id,
                               int32_t n_free, const float *F_fixed, int64_t n_fixed,
                               float *F_free, const tsid_fit_opts *opts);
 
+/* One chunk of the extension solved exactly (Stage II, Section 5.2; Eq. 6 in
+ * factored form, the alternating-least-squares step): each free row is the
+ * ridge regression
+ *   x_f = (sum_(entries of f) p p^T + lambda I)^{-1} sum_(entries of f) r p,
+ * p = F_fixed[fixed_id], the minimiser that tsid_extend_chunk's gradient
+ * steps approach.  The Gram matrices are accumulated on the matrix cores in
+ * fp64 (v_mfma_f64_16x16x4f64) and each is factored (Cholesky) and solved in
+ * fp64 by one wavefront; F_free receives the fp32 rounding of the solution.
+ * A free row without entries gets x_f = 0.
+ * Arguments, layout, ownership, asynchrony and the staging slots are those of
+ * tsid_extend_chunk; lambda >= 0 replaces the options.
+ * Errors returned here: E_STATE (no template), E_INVAL (bad sizes or
+ * pointers, lambda negative or not finite, k not in {8, 16, 32, 64}), E_NOMEM,
+ * E_DEVICE.  At the next tsid_sync: E_RANGE / E_DUP as for tsid_extend_chunk,
+ * and E_NONFINITE when a Gram matrix is not positive definite (lambda = 0 and
+ * fewer independent entries than k in some row) or a solution is not finite;
+ * the affected chunk's F_free is then unspecified. */
+tsid_status tsid_extend_chunk_ridge(tsid_ctx *ctx, int side, const int32_t *fixed_id,
+                                    const int32_t *free_local, const float *r, int64_t nnz,
+                                    int32_t n_free, const float *F_fixed, int64_t n_fixed,
+                                    float *F_free, float lambda);
+
 /* Wait for every outstanding chunk; returns the first device-side error of
  * those chunks (and clears it), else TSID_OK. */
 tsid_status tsid_sync(tsid_ctx *ctx);

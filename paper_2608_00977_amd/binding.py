@@ -86,6 +86,7 @@ def lib() -> C.CDLL:
         "tsid_loss": (C.c_int, [P, P, P, C.c_float, P]),
         "tsid_extend_chunk": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P,
                                         C.POINTER(tsid_fit_opts)]),
+        "tsid_extend_chunk_ridge": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P, C.c_float]),
         "tsid_sync": (C.c_int, [P]),
         "tsid_export_index": (C.c_int, [P, C.c_int, P, sz]),
         "tsid_chunk_plan": (i32, [P, i64, i32, i64, P, i32]),
@@ -190,6 +191,12 @@ def tsid_extend_chunk(ctx, side, fixed_id, free_local, r, nnz, n_free, F_fixed, 
                       opts: tsid_fit_opts) -> int:
     return lib().tsid_extend_chunk(ctx, side, fixed_id, free_local, r, nnz, n_free, F_fixed,
                                    n_fixed, F_free, C.byref(opts))
+
+
+def tsid_extend_chunk_ridge(ctx, side, fixed_id, free_local, r, nnz, n_free, F_fixed, n_fixed,
+                            F_free, lam: float) -> int:
+    return lib().tsid_extend_chunk_ridge(ctx, side, fixed_id, free_local, r, nnz, n_free, F_fixed,
+                                         n_fixed, F_free, float(lam))
 
 
 def tsid_sync(ctx) -> int:
@@ -317,10 +324,12 @@ class Tsid:
         return float(out[0])
 
     def extend_chunk(self, side, fixed_id, free_local, r, n_free, F_fixed: torch.Tensor,
-                     F_free: torch.Tensor, opts: tsid_fit_opts):
+                     F_free: torch.Tensor, opts):
         """Queues one chunk; fixed_id/free_local/r are host arrays or pinned CPU
         tensors kept alive until sync(); F_free is a CPU tensor (pinned for
-        overlap) that receives the result."""
+        overlap) that receives the result.  opts: tsid_fit_opts for the
+        one-sided gradient steps (tsid_extend_chunk), or a float lambda for
+        the exact ridge solve (tsid_extend_chunk_ridge)."""
         assert F_fixed.is_cuda and F_fixed.dtype == torch.float32 and F_fixed.is_contiguous()
         assert not F_free.is_cuda and F_free.dtype == torch.float32 and F_free.is_contiguous()
         arrs = []
@@ -331,9 +340,15 @@ class Tsid:
                 arrs.append(np.ascontiguousarray(a, dt))
         nnz = int(arrs[0].numel() if isinstance(arrs[0], torch.Tensor) else arrs[0].size)
         self._keep.append((arrs, F_fixed, F_free, opts))
-        st = tsid_extend_chunk(self.ctx, side, _ptr(arrs[0]), _ptr(arrs[1]), _ptr(arrs[2]), nnz,
-                               n_free, _ptr(F_fixed), F_fixed.shape[0], _ptr(F_free), opts)
-        self._check(st, "tsid_extend_chunk")
+        if isinstance(opts, tsid_fit_opts):
+            st = tsid_extend_chunk(self.ctx, side, _ptr(arrs[0]), _ptr(arrs[1]), _ptr(arrs[2]), nnz,
+                                   n_free, _ptr(F_fixed), F_fixed.shape[0], _ptr(F_free), opts)
+            self._check(st, "tsid_extend_chunk")
+        else:
+            st = tsid_extend_chunk_ridge(self.ctx, side, _ptr(arrs[0]), _ptr(arrs[1]), _ptr(arrs[2]),
+                                         nnz, n_free, _ptr(F_fixed), F_fixed.shape[0], _ptr(F_free),
+                                         float(opts))
+            self._check(st, "tsid_extend_chunk_ridge")
 
     def sync(self):
         st = tsid_sync(self.ctx)

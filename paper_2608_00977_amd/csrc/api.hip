@@ -1312,11 +1312,19 @@ void ext_ensure(tsid_ctx *c, int64_t nnz, int32_t n_free, int32_t k) {
     x.k = k;
 }
 
+// One chunk of the extension: staging, bucketing by free row, then either
+// the one-sided gradient steps of `o` or (ridge != null) the exact solve
+// with lambda = *ridge.
 void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t *free_local,
                   const float *r, int64_t nnz, int32_t n_free, const float *F_fixed, int64_t n_fixed,
-                  float *F_free, const tsid_fit_opts *o) {
+                  float *F_free, const tsid_fit_opts *o, const float *ridge) {
     if (!c->tpl) fail(TSID_E_STATE, "no template: the rank k is set by tsid_build_template");
-    check_opts(o);
+    if (ridge) {
+        if (!(*ridge >= 0.f) || !std::isfinite(*ridge)) fail(TSID_E_INVAL, "lambda must be finite and >= 0");
+        if (!ridge_supported(c->tpl->k)) fail(TSID_E_INVAL, "the exact extension solve supports k in {8, 16, 32, 64}");
+    } else {
+        check_opts(o);
+    }
     if (side != 0 && side != 1) fail(TSID_E_INVAL, "side must be 0 or 1");
     if (nnz < 0 || nnz > kMaxEntries) fail(TSID_E_INVAL, "nnz out of range");
     if (n_free < 0 || n_fixed < 0 || n_fixed >= (int64_t(1) << 31)) fail(TSID_E_INVAL, "bad sizes");
@@ -1353,21 +1361,33 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
     ptr_from_keys(sk, nnz, n_free, bits_fixed, x.ptr, cs);
     // the slot's result buffer is free once its previous results were flushed
     TSID_HIP(hipStreamWaitEvent(cs, s.ev_flushed, 0));
-    PassArgs a{};
-    a.stream = x.stream;
-    a.ptr = x.ptr;
-    a.rows = n_free;
-    a.Y = F_fixed;
-    a.y_rows = n_fixed;
-    a.Xn = s.X;
-    a.lam = o->lambda;
-    a.lr = o->lr;
-    a.xi = o->clip_xi;
-    a.clip = o->clip;
-    a.degree = o->step == TSID_STEP_DEGREE;
-    a.err = x.err;
-    // every step of every free row in one launch (one wave per free row)
-    launch_extend_steps(K, a, o->epochs, cs);
+    if (ridge) {
+        RidgeArgs a{};
+        a.stream = x.stream;
+        a.ptr = x.ptr;
+        a.rows = n_free;
+        a.F = F_fixed;
+        a.lambda = *ridge;
+        a.X = s.X;
+        a.err = x.err;
+        launch_ridge_rows(K, a, cs);  // one wave per free row
+    } else {
+        PassArgs a{};
+        a.stream = x.stream;
+        a.ptr = x.ptr;
+        a.rows = n_free;
+        a.Y = F_fixed;
+        a.y_rows = n_fixed;
+        a.Xn = s.X;
+        a.lam = o->lambda;
+        a.lr = o->lr;
+        a.xi = o->clip_xi;
+        a.clip = o->clip;
+        a.degree = o->step == TSID_STEP_DEGREE;
+        a.err = x.err;
+        // every step of every free row in one launch (one wave per free row)
+        launch_extend_steps(K, a, o->epochs, cs);
+    }
     TSID_HIP(hipEventRecord(s.ev_done, cs));
     // flush the results on the third stream
     TSID_HIP(hipStreamWaitEvent(c->d2h, s.ev_done, 0));
@@ -1570,7 +1590,15 @@ tsid_status tsid_extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, co
                               const float *r, int64_t nnz, int32_t n_free, const float *F_fixed,
                               int64_t n_fixed, float *F_free, const tsid_fit_opts *opts) {
     return guarded(c, [&]() {
-        extend_chunk(c, side, fixed_id, free_local, r, nnz, n_free, F_fixed, n_fixed, F_free, opts);
+        extend_chunk(c, side, fixed_id, free_local, r, nnz, n_free, F_fixed, n_fixed, F_free, opts, nullptr);
+    });
+}
+
+tsid_status tsid_extend_chunk_ridge(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t *free_local,
+                                    const float *r, int64_t nnz, int32_t n_free, const float *F_fixed,
+                                    int64_t n_fixed, float *F_free, float lambda) {
+    return guarded(c, [&]() {
+        extend_chunk(c, side, fixed_id, free_local, r, nnz, n_free, F_fixed, n_fixed, F_free, nullptr, &lambda);
     });
 }
 

@@ -197,6 +197,19 @@ void launch_slab_pass(int K, bool loss_only, const SlabArgs &a, int64_t n_units,
 void launch_slab_finish(int K, const SlabArgs &a, hipStream_t s, hipEvent_t ev0 = nullptr,
                         hipEvent_t ev1 = nullptr);
 
+// ------------------------------------------------- exact extension solve
+struct RidgeArgs {
+    const int2 *stream;   // chunk cells bucketed by free row: {fixed id, value bits}
+    const int64_t *ptr;   // bucket pointers [rows + 1]
+    int64_t rows;         // free rows
+    const float *F;       // fixed factors (rows indexed by fixed id), fp32
+    float lambda;
+    float *X;             // rows x K results
+    int32_t *err;
+};
+bool ridge_supported(int K);
+void launch_ridge_rows(int K, const RidgeArgs &a, hipStream_t s);
+
 // ----------------------------------------------------------- dense tiles
 struct DenseArgs {
     const uint16_t *X;        // owner side bf16 copy (rows x K)

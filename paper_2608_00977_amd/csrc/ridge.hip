@@ -1,0 +1,194 @@
+// Exact one-sided solve of an extension chunk (Section 5.2; Eq. 6 in factored
+// form): with the fixed side's factors held constant, each free row x_f is
+// the ridge regression
+//   x_f = argmin sum_(u in cells of f) (r_u - p_u . x)^2 + lambda ||x||^2
+//       = (sum_u p_u p_u^T + lambda I)^{-1} sum_u r_u p_u,
+// the fixed point that the gradient steps of k_extend_steps approach (the
+// alternating-least-squares step of the paper's Stage II).  Everything is
+// fp64: the Gram matrix of a row with fewer cells than k is singular up to
+// lambda, and fp32 would lose the directions lambda alone fixes.
+//
+// One wave per free row:
+//  1. Gram and right-hand side.  Four cells at a time, each lane loads one
+//     coordinate of each 16-coordinate block of one cell's fixed row (lane l:
+//     cell l/16, coordinate 16 I + l%16), which is at once the A operand
+//     A[l%16][l/16] and the B operand B[l/16][l%16] of v_mfma_f64_16x16x4f64,
+//     so block (I, J) of the Gram matrix accumulates with one MFMA per block
+//     pair I <= J (10 at k = 64).  Lane l, slot j of a result holds
+//     C[4 j + l/16][l%16].  The right-hand side accumulates per lane and is
+//     summed over the four cell slots at the end.
+//  2. The blocks go through LDS (and their mirror images), lane i reads row i
+//     and adds lambda on the diagonal.
+//  3. Cholesky G = L L^T, right-looking, with row i of the trailing matrix in
+//     lane i's registers: per column j, lane j's diagonal and every lane's
+//     L[i][j] are broadcast with readlane, and each lane updates its row.
+//     Entries above the diagonal are updated too and never read.
+//  4. L z = b column by column in registers, then L^T x = z column by column
+//     with the rows of L read back from LDS.
+// A pivot that is not positive (lambda = 0 and fewer independent cells than
+// k) raises the non-finite error; a row without cells gets x = 0.
+#include <hip/hip_ext.h>
+
+#include "internal.h"
+
+namespace tsid {
+
+namespace {
+
+typedef double d4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), l);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+template <int K>
+struct RidgeShape {
+    static constexpr int NB = (K + 15) / 16;          // 16-coordinate blocks
+    static constexpr int NP = NB * (NB + 1) / 2;      // block pairs I <= J
+    static constexpr int PITCH = K + 1;               // LDS row pitch (doubles)
+};
+
+template <int K>
+__global__ __launch_bounds__(64) void k_ridge_rows(const RidgeArgs A) {
+    using S = RidgeShape<K>;
+    __shared__ double G[K * S::PITCH];
+    const int lane = threadIdx.x;
+    const int64_t f = blockIdx.x;  // free row
+    if (f >= A.rows) return;
+    const int lr = lane & 15, lq = lane >> 4;
+    const int64_t b0 = A.ptr[f], b1 = A.ptr[f + 1];
+    if (b0 == b1) {  // no cells: the minimiser is 0
+        if (lane < K) A.X[f * K + lane] = 0.f;
+        return;
+    }
+    // 1. Gram blocks and right-hand side
+    d4 acc[S::NP];
+#pragma unroll
+    for (int q = 0; q < S::NP; ++q) acc[q] = d4{0.0, 0.0, 0.0, 0.0};
+    double rhs[S::NB];
+#pragma unroll
+    for (int I = 0; I < S::NB; ++I) rhs[I] = 0.0;
+    for (int64_t c0 = b0; c0 < b1; c0 += 4) {
+        const int64_t c = c0 + lq;
+        double pv[S::NB];
+        double rv = 0.0;
+#pragma unroll
+        for (int I = 0; I < S::NB; ++I) pv[I] = 0.0;
+        if (c < b1) {
+            const int2 rec = A.stream[c];
+            rv = (double)__int_as_float(rec.y);
+            const float *p = A.F + (int64_t)rec.x * K;
+#pragma unroll
+            for (int I = 0; I < S::NB; ++I)
+                if (K % 16 == 0 || 16 * I + lr < K) pv[I] = (double)p[16 * I + lr];
+        }
+        int q = 0;
+#pragma unroll
+        for (int I = 0; I < S::NB; ++I) {
+            rhs[I] = fma(rv, pv[I], rhs[I]);
+#pragma unroll
+            for (int J = I; J < S::NB; ++J, ++q) acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(pv[I], pv[J], acc[q], 0, 0, 0);
+        }
+    }
+    // 2. blocks to LDS (with their mirror images), lane i reads row i
+    {
+        int q = 0;
+#pragma unroll
+        for (int I = 0; I < S::NB; ++I) {
+#pragma unroll
+            for (int J = I; J < S::NB; ++J, ++q) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int row = 16 * I + 4 * j + lq, col = 16 * J + lr;
+                    if (row < K && col < K) {
+                        G[row * S::PITCH + col] = acc[q][j];
+                        G[col * S::PITCH + row] = acc[q][j];
+                    }
+                }
+            }
+        }
+    }
+    // the right-hand side: sum over the four cell slots, then lane i takes
+    // coordinate i = 16 (i / 16) + i % 16
+#pragma unroll
+    for (int I = 0; I < S::NB; ++I) {
+        rhs[I] += __shfl_xor(rhs[I], 16, 64);
+        rhs[I] += __shfl_xor(rhs[I], 32, 64);
+    }
+    double b = 0.0;
+#pragma unroll
+    for (int I = 0; I < S::NB; ++I) b = (lq == I) ? rhs[I] : b;
+    __syncthreads();
+    const int ri = lane < K ? lane : K - 1;  // lanes past k mirror the last row (never read back)
+    double g[K];
+#pragma unroll
+    for (int c = 0; c < K; ++c) g[c] = G[ri * S::PITCH + c] + ((c == lane) ? (double)A.lambda : 0.0);
+    // 3. Cholesky, right-looking; lane i ends with L[i][0..i] in g[0..i]
+    bool bad = false;
+    double dinv = 1.0;  // 1 / L[i][i] of this lane's row
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        const double djj = readlane_f64(g[j], j);
+        bad |= !(djj > 0.0);
+        const double ljj = sqrt(djj > 0.0 ? djj : 1.0);
+        const double inv = 1.0 / ljj;
+        const double lij = (lane == j) ? ljj : g[j] * inv;
+        dinv = (lane == j) ? inv : dinv;
+        g[j] = (lane >= j) ? lij : g[j];
+#pragma unroll
+        for (int l = j + 1; l < K; ++l) g[l] = fma(-lij, readlane_f64(lij, l), g[l]);
+    }
+    // 4a. L z = b (column-oriented): lane c finishes z_c, the lanes below take it out
+#pragma unroll
+    for (int c = 0; c < K; ++c) {
+        const double zc = readlane_f64(b * dinv, c);
+        b = (lane == c) ? zc : ((lane > c) ? fma(-g[c], zc, b) : b);
+    }
+    // 4b. L^T x = z: rows of L back through LDS (lane i reads L[r][i])
+    __syncthreads();
+    if (lane < K) {
+#pragma unroll
+        for (int c = 0; c < K; ++c)
+            if (c <= lane) G[lane * S::PITCH + c] = g[c];
+    }
+    __syncthreads();
+    double x = 0.0;
+#pragma unroll
+    for (int r = K - 1; r >= 0; --r) {
+        const double xr = readlane_f64(b * dinv, r);
+        x = (lane == r) ? xr : x;
+        if (lane < r) b = fma(-G[r * S::PITCH + lane], xr, b);
+    }
+    bad = __builtin_amdgcn_ballot_w64(bad) != 0;  // a bad pivot anywhere spoils the whole row
+    if (lane < K) {
+        const float xf = (float)x;
+        A.X[f * K + lane] = xf;
+        if (bad || !__builtin_isfinite(xf)) A.err[ERR_NONFINITE] = 1;
+    }
+}
+
+template <int K>
+void ridge_k(const RidgeArgs &a, hipStream_t s) {
+    hipLaunchKernelGGL(k_ridge_rows<K>, dim3((unsigned)a.rows), dim3(64), 0, s, a);
+    TSID_HIP(hipGetLastError());
+}
+
+}  // namespace
+
+bool ridge_supported(int K) { return K == 8 || K == 16 || K == 32 || K == 64; }
+
+void launch_ridge_rows(int K, const RidgeArgs &a, hipStream_t s) {
+    if (a.rows <= 0) return;
+    switch (K) {
+        case 8: ridge_k<8>(a, s); break;
+        case 16: ridge_k<16>(a, s); break;
+        case 32: ridge_k<32>(a, s); break;
+        case 64: ridge_k<64>(a, s); break;
+        default: fail(TSID_E_INVAL, "the exact extension solve supports k in {8, 16, 32, 64}");
+    }
+}
+
+}  // namespace tsid

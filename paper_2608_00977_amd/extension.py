@@ -86,7 +86,8 @@ class Extension:
 
     def run(self, T: Tsid, P_t: torch.Tensor, Q_t: torch.Tensor, opts):
         """P_t (m_t x k), Q_t (n_t x k): fp32 device factors of the template,
-        in template order.  Returns (P, Q): the full m x k and n x k factors
+        in template order.  opts: tsid_fit_opts for one-sided gradient steps,
+        or a float lambda for the exact ridge solve of every free row.  Returns (P, Q): the full m x k and n x k factors
         as pinned host tensors, and the wall time of each phase in seconds."""
         k = P_t.shape[1]
         P_free = torch.empty((self.rows.free_ids.size, k), dtype=torch.float32).pin_memory()
