@@ -761,7 +761,7 @@ void ensure_slab(tsid_ctx *c, int side, int prec) {
 // nearly every other block) spreads over up to seg_max waves and a short one
 // takes one.  Also counts the stripes that hold a tile.
 #ifndef TSID_DENSE_SEG_MIN
-#define TSID_DENSE_SEG_MIN 16
+#define TSID_DENSE_SEG_MIN 32
 #endif
 #ifndef TSID_DENSE_SEG_MAX
 #define TSID_DENSE_SEG_MAX 64
@@ -927,9 +927,9 @@ void build_dense(tsid_ctx *c, float fill) {
 
 // Whether the current fit runs the dense head tiles: bf16 factors, k in
 // {16, 32, 64, 128}, and either a forced tile fill (tsid_set_dense_tiles) or
-// the default fill 1/4 with at least a tenth of the cells in dense tiles.
+// the default fill 0.15 with at least a tenth of the cells in dense tiles.
 #ifndef TSID_DENSE_FILL
-#define TSID_DENSE_FILL 0.25f
+#define TSID_DENSE_FILL 0.15f
 #endif
 #ifndef TSID_DENSE_MIN_SHARE
 #define TSID_DENSE_MIN_SHARE 0.10

@@ -1,7 +1,7 @@
 // Dense head tiles of the template fit on MFMA (Section 5.1, Tensor-Core
 // batching).  A most-observed (Zipf) template concentrates its cells in its
-// head: a third to a half of them lie in 16 x 16 tiles that are at least a
-// quarter full.  For those tiles the residuals and both gradients of Eqs. 3-4
+// head: a third to two thirds of them lie in 16 x 16 tiles that are at
+// least 15% full.  For those tiles the residuals and both gradients of Eqs. 3-4
 // are dense 16 x 16 x k products, so they run as bf16 MFMA with fp32
 // accumulation instead of one cell at a time; the remaining cells stay on the
 // item pass, which adds each row's dense gradient sum before the update of
@@ -37,7 +37,10 @@ namespace tsid {
 
 namespace {
 
-constexpr int kDenseWaves = 4;  // waves (stripes) per workgroup
+#ifndef TSID_DENSE_WAVES
+#define TSID_DENSE_WAVES 4
+#endif
+constexpr int kDenseWaves = TSID_DENSE_WAVES;  // waves (segments) per workgroup
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));

@@ -742,7 +742,7 @@ void fixup_kv(const PassArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) 
 #define TSID_V_BF16_64 8
 #endif
 #ifndef TSID_V_BF16_128
-#define TSID_V_BF16_128 8
+#define TSID_V_BF16_128 16
 #endif
 #define TSID_DISPATCH_K(K_, FN, ...)                                                              \
     switch (K_) {                                                                                 \

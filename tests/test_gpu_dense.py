@@ -34,6 +34,7 @@ EPOCH_TOL = 1e-4
 LOSS0_TOL = 1e-5
 LOSS_TRAJ_TOL = 1e-2
 BF16_RMSE_TOL = 1e-2
+AUTO_FILL = 0.15  # the automatic rule's tile fill (tsid_set_dense_tiles)
 
 
 def _case(name):
@@ -149,7 +150,7 @@ def test_dense_mid_fit_rmse_matches_oracle(T):
     assert st == 0
     info = T.dense_info()
     _, _, a, b, v = oracle_template(p)
-    assert info == _tile_info(a, b, p.I.size, p.J.size, 0.25)  # the automatic rule took the tiles
+    assert info == _tile_info(a, b, p.I.size, p.J.size, AUTO_FILL)  # the automatic rule took the tiles
     assert info["cells"] >= 0.10 * a.size
     sto, Po, Qo, ho, _ = oracle.fit(a, b, v, p.P0, p.Q0, p.epochs, p.lam, p.lr, p.step, True, p.xi,
                                     bf16=True)
@@ -198,7 +199,7 @@ def test_dense_automatic_choice():
         assert gpu_fit(t, p, epochs=1, prec="bf16")[0] == 0
         assert t.dense_info()["tiles"] == 0
         t.set_dense_tiles(-1)
-        # uniform cells at 1% density: no tile reaches a quarter
+        # uniform cells at 1% density: no tile reaches 15%
         p = synth.random_case(3000, 2800, 90000, 1100, 900, 32, seed=36, epochs=1, prec="bf16")
         _build(t, p)
         note("dense auto: sparse uniform")

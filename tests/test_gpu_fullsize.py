@@ -32,14 +32,15 @@ def _sampled_parity(T, p, n_rows=64, n_cols=64, tol=1e-4):
     cols = np.union1d(g.choice(p.J.size, n_cols, replace=False), top_c)
     bf16 = p.prec == "bf16"
     if bf16:
-        # the automatic rule takes the dense head tiles (16 x 16 tiles at
-        # least a quarter full) when they hold a tenth of the cells: the
-        # library's count must equal one made here, and rows of stripes with
-        # tiles join the sample
+        # the automatic rule takes the dense head tiles (16 x 16 tiles holding
+        # at least ceil(0.15 * 256) = 39 cells) when they hold a tenth of the
+        # cells: the library's count must equal one made here, and rows of
+        # stripes with tiles join the sample
+        thr = 39
         n_ti, n_tj = (p.I.size + 15) // 16, (p.J.size + 15) // 16
         cnt = np.bincount((a // 16).astype(np.int64) * n_tj + b // 16, minlength=n_ti * n_tj)
-        dense = (cnt >= 64).reshape(n_ti, n_tj)
-        cells = int(cnt[cnt >= 64].sum())
+        dense = (cnt >= thr).reshape(n_ti, n_tj)
+        cells = int(cnt[cnt >= thr].sum())
         del cnt
         info = T.dense_info()
         if cells >= 0.10 * a.size:
