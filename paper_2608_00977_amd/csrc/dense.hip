@@ -74,30 +74,57 @@ __device__ __forceinline__ uint32_t pk_bf16(float a, float b) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector((fl2){a, b}, bf2));
 }
 
-// A tile's operands: the other rows t0 .. t0 + 15 (A operand of step 1:
-// row t0 + lr, coordinates 32 c + 8 lq .. + 7 of chunk c) and the tile
-// values (owner lr, others 4 lq .. 4 lq + 3).
+// A tile's operands: its 16 other rows t0 .. t0 + 15 read as whole rows
+// (lane l of load c holds the 16 bytes at chunk l % (k/8) of row
+// (64 c + l) / (k/8); whole 128-byte lines per load instead of a quarter of
+// 16 lines, which halves the L1 tag work per tile) and the tile values
+// (owner lr, others 4 lq .. 4 lq + 3).
 template <int K>
 __device__ __forceinline__ void load_tile(const DenseArgs &A, int32_t other, uint32_t t, int lr, int lq,
                                           bf8 (&y)[DenseShape<K>::NC], float4 &r) {
+    constexpr int LPR = K / 8;  // lanes per row
     const int64_t t0 = (int64_t)other * 16;
-    // rows past the table repeat its last row (their cells are all unobserved)
-    const int64_t yrow = t0 + lr < A.y_rows ? t0 + lr : A.y_rows - 1;
+    const int lane = lq * 16 + lr;
 #pragma unroll
-    for (int c = 0; c < DenseShape<K>::NC; ++c) y[c] = load8_bf16<K>(A.Y, yrow, c * 32 + 8 * lq);
+    for (int c = 0; c < DenseShape<K>::NC; ++c) {
+        const int rr = (c * 64 + lane) / LPR;  // row of the tile (16 and up only at k = 16: not used)
+        const int64_t row = t0 + (rr < 16 ? rr : 15);
+        // rows past the table repeat its last row (their cells are all unobserved)
+        const int64_t yrow = row < A.y_rows ? row : A.y_rows - 1;
+        y[c] = __builtin_bit_cast(bf8, *reinterpret_cast<const uint4 *>(A.Y + yrow * K + (lane % LPR) * 8));
+    }
     r = *reinterpret_cast<const float4 *>(A.R + (int64_t)t * 256 + lr * 16 + 4 * lq);
 }
 
 // Steps 1-3 for one tile (v_mfma_f32_16x16x32_bf16: lane l holds
 // A[l%16][8(l/16)+j], B[8(l/16)+j][l%16], j = 0..7, and C[4(l/16)+j][l%16],
 // j = 0..3): e^2 into e2, E Y_t into acc.  yl: this wave's LDS copy of the
-// tile's other rows.  valid = false (a stand-in past the end of the segment)
-// zeroes the residuals, so the tile adds exactly nothing.
+// tile's other rows, through which the whole-row loads reach both MFMA
+// layouts.  valid = false (a stand-in past the end of the segment) zeroes
+// the residuals, so the tile adds exactly nothing.
 template <int K, bool LOSS_ONLY>
-__device__ __forceinline__ void dense_tile(const bf8 (&ya)[DenseShape<K>::NC], const float4 &r,
+__device__ __forceinline__ void dense_tile(const bf8 (&yraw)[DenseShape<K>::NC], const float4 &r,
                                            const bf8 (&xb)[DenseShape<K>::NC], f4 (&acc)[DenseShape<K>::NB],
                                            float &e2, uint16_t *yl, int lr, int lq, bool valid) {
     using D = DenseShape<K>;
+    constexpr int LPR = K / 8;
+    const int lane = lq * 16 + lr;
+#pragma unroll
+    for (int c = 0; c < D::NC; ++c) {
+        const int rr = (c * 64 + lane) / LPR;
+        if (rr < 16) *reinterpret_cast<uint4 *>(yl + rr * D::ROW + (lane % LPR) * 8) = __builtin_bit_cast(uint4, yraw[c]);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // the A operand of step 1: row lr, coordinates 32 c + 8 lq .. + 7
+    bf8 ya[D::NC];
+#pragma unroll
+    for (int c = 0; c < D::NC; ++c) {
+        uint4 w = make_uint4(0u, 0u, 0u, 0u);
+        if (K % 32 == 0 || 8 * lq < K) w = *reinterpret_cast<const uint4 *>(yl + lr * D::ROW + c * 32 + 8 * lq);
+        ya[c] = __builtin_bit_cast(bf8, w);
+    }
     // 1. S^T = Y_t X_t^T: lane holds S[owner lr][other 4 lq + j]
     f4 st = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -114,19 +141,12 @@ __device__ __forceinline__ void dense_tile(const bf8 (&ya)[DenseShape<K>::NC], c
         // 3. G += E Y_t with one k = 32 product per 16-coordinate block: the
         // A operand holds the residuals' bf16 high parts in slots 0-3 and
         // their remainders in slots 4-7, the B operand the same four other
-        // rows twice, so the product adds (high + low) Y, about 16 bits of
-        // each residual.  Y_t is staged in LDS for the B operand.
-#pragma unroll
-        for (int c = 0; c < D::NC; ++c)
-            if (K % 32 == 0 || 8 * lq < K)
-                *reinterpret_cast<uint4 *>(yl + lr * D::ROW + c * 32 + 8 * lq) = __builtin_bit_cast(uint4, ya[c]);
+        // rows twice (a column of the LDS copy), so the product adds
+        // (high + low) Y, about 16 bits of each residual.
         const uint32_t h0 = pk_bf16(e[0], e[1]), h1 = pk_bf16(e[2], e[3]);
         const uint32_t l0 = pk_bf16(e[0] - __uint_as_float(h0 << 16), e[1] - __uint_as_float(h0 & 0xffff0000u));
         const uint32_t l1 = pk_bf16(e[2] - __uint_as_float(h1 << 16), e[3] - __uint_as_float(h1 & 0xffff0000u));
         const bf8 ea = __builtin_bit_cast(bf8, make_uint4(h0, h1, l0, l1));
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
         for (int nb = 0; nb < D::NB; ++nb) {
             const uint16_t *col = yl + 4 * lq * D::ROW + nb * 16 + lr;
@@ -135,14 +155,24 @@ __device__ __forceinline__ void dense_tile(const bf8 (&ya)[DenseShape<K>::NC], c
             const bf8 b = __builtin_bit_cast(bf8, make_uint4(b01, b23, b01, b23));
             acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ea, b, acc[nb], 0, 0, 0);
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();  // the tile's reads are done before the next writes
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();  // the tile's reads are done before the next writes
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Waves per SIMD the register allocation aims for (0: the compiler's choice).
+#ifndef TSID_DENSE_WPE
+#define TSID_DENSE_WPE 0
+#endif
+#if TSID_DENSE_WPE > 0
+#define TSID_DENSE_OCC __attribute__((amdgpu_waves_per_eu(TSID_DENSE_WPE)))
+#else
+#define TSID_DENSE_OCC
+#endif
+
 template <int K, bool LOSS_ONLY>
-__global__ __launch_bounds__(64 * kDenseWaves) void k_dense_pass(const DenseArgs A) {
+__global__ __launch_bounds__(64 * kDenseWaves) TSID_DENSE_OCC void k_dense_pass(const DenseArgs A) {
     using D = DenseShape<K>;
     static_assert(K % 16 == 0, "dense tiles need k a multiple of 16");
     if (A.skip_after_nonfinite) {
