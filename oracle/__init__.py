@@ -51,6 +51,8 @@ def lib() -> C.CDLL:
                                  i32, P, P]),
             "or_extend": (C.c_int, [i64, P, P, P, i32, i32, P, P, i32, f64, f64, i32, i32, f64]),
             "or_ridge": (C.c_int, [i64, P, P, P, i32, i32, P, f64, P]),
+            "or_extend_adam": (C.c_int, [i64, P, P, P, i32, i32, P, i32, P, i32, f64, f64, f64, f64,
+                                         f64, P, P]),
             "or_chunk_plan": (i32, [P, i64, i32, i64, P, i32]),
             "or_bf16_bits": (C.c_uint16, [C.c_float]),
         }
@@ -146,6 +148,22 @@ def ridge(fixed_id, free_id, v, n_free, F_fixed, lam):
     X = np.zeros((n_free, k), np.float64)
     st = lib().or_ridge(v.size, _p(fixed_id), _p(free_id), _p(v), n_free, k, _p(F), lam, _p(X))
     return st, X
+
+
+def extend_adam(fixed_id, free_id, v, n_free, F_fixed, B, steps, lam, lr, beta1=0.9, beta2=0.999,
+                eps=1e-8):
+    """Stage II as Eq. 10 states it (Section 5.2): Adam on the coefficients C of
+    each free line in the template basis B.  Returns (status, B^T C per free
+    line (n_free x k), C (n_free x n_b))."""
+    fixed_id, free_id, v = _c(fixed_id, np.int32), _c(free_id, np.int32), _c(v, np.float32)
+    F = _c(F_fixed, np.float64)
+    Bm = _c(B, np.float64)
+    k, n_b = F.shape[1], Bm.shape[0]
+    X = np.zeros((n_free, k), np.float64)
+    Cm = np.zeros((n_free, n_b), np.float64)
+    st = lib().or_extend_adam(v.size, _p(fixed_id), _p(free_id), _p(v), n_free, k, _p(F), n_b, _p(Bm),
+                              steps, lam, lr, beta1, beta2, eps, _p(X), _p(Cm))
+    return st, X, Cm
 
 
 def chunk_plan(counts, n_chunks=0, max_entries=0):

@@ -348,6 +348,58 @@ int or_ridge(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const
     return status;
 }
 
+int or_extend_adam(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,
+                   int32_t n_free, int32_t k, const double *F_fixed, int32_t n_b, const double *B,
+                   int32_t steps, double lambda, double lr, double beta1, double beta2, double eps,
+                   double *F_free, double *C_out) {
+    const int64_t nc = (int64_t)n_free * n_b, nx = (int64_t)n_free * k;
+    double *C = (double *)calloc((size_t)nc + 1, sizeof(double));
+    double *m = (double *)calloc((size_t)nc + 1, sizeof(double));
+    double *w = (double *)calloc((size_t)nc + 1, sizeof(double));
+    double *gt = (double *)malloc((size_t)(nx + 1) * sizeof(double));
+    int status = 0;
+    double b1t = 1.0, b2t = 1.0;
+    for (int32_t t = 1; t <= steps && status == 0; ++t) {
+        /* x_f = B^T c_f, the factor the coefficients represent */
+        for (int32_t f = 0; f < n_free; ++f)
+            for (int32_t c = 0; c < k; ++c) {
+                double s = 0.0;
+                for (int32_t l = 0; l < n_b; ++l) s += B[(int64_t)l * k + c] * C[(int64_t)f * n_b + l];
+                F_free[(int64_t)f * k + c] = s;
+            }
+        /* dL/dx_f = -2 sum (r - p . x_f) p over the entries of f */
+        memset(gt, 0, (size_t)nx * sizeof(double));
+        for (int64_t e = 0; e < nnz; ++e) {
+            const double *p = F_fixed + (int64_t)fixed_id[e] * k;
+            const int64_t f = free_id[e];
+            const double err = (double)v[e] - dot(p, F_free + f * k, k);
+            for (int32_t c = 0; c < k; ++c) gt[f * k + c] += -2.0 * err * p[c];
+        }
+        /* dL/dc_f = B dL/dx_f + 2 lambda c_f, then the Adam step */
+        b1t *= beta1;
+        b2t *= beta2;
+        for (int32_t f = 0; f < n_free; ++f)
+            for (int32_t l = 0; l < n_b; ++l) {
+                const int64_t j = (int64_t)f * n_b + l;
+                const double g = dot(B + (int64_t)l * k, gt + (int64_t)f * k, k) + 2.0 * lambda * C[j];
+                m[j] = beta1 * m[j] + (1.0 - beta1) * g;
+                w[j] = beta2 * w[j] + (1.0 - beta2) * g * g;
+                const double mh = m[j] / (1.0 - b1t), wh = w[j] / (1.0 - b2t);
+                C[j] -= lr * mh / (sqrt(wh) + eps);
+                if (!isfinite(C[j])) status = 7;
+            }
+    }
+    for (int32_t f = 0; f < n_free; ++f)
+        for (int32_t c = 0; c < k; ++c) {
+            double s = 0.0;
+            for (int32_t l = 0; l < n_b; ++l) s += B[(int64_t)l * k + c] * C[(int64_t)f * n_b + l];
+            F_free[(int64_t)f * k + c] = s;
+        }
+    if (C_out) memcpy(C_out, C, (size_t)nc * sizeof(double));
+    free(C); free(m); free(w); free(gt);
+    return status;
+}
+
 int32_t or_chunk_plan(const int64_t *counts, int64_t n_free, int32_t n_chunks,
                       int64_t max_entries, int64_t *bounds, int32_t max_bounds) {
     if (n_chunks > 0) {

@@ -81,6 +81,23 @@ int or_extend(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, cons
 int or_ridge(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,
              int32_t n_free, int32_t k, const double *F_fixed, double lambda, double *F_free);
 
+/* Stage II as stated in Section 5.2 (Eq. 10): free line f is represented in
+ * the fixed template basis by a coefficient vector c_f (n_b entries), and
+ * its entries are predicted as R*_i c_f = p . (B^T c_f), with p the fixed
+ * factor row F_fixed[fixed_id] and B (n_b x k) the basis factors of the
+ * template (R* = P B^T in factored form).  Minimises
+ *   L(C) = sum (r - p . B^T c_f)^2 + lambda ||C||_F^2
+ * with the Adam method from C = 0 for `steps` steps: per step the gradient
+ * G = dL/dC, the moment estimates m <- beta1 m + (1 - beta1) G and
+ * w <- beta2 w + (1 - beta2) G^2, their bias corrections by 1 - beta^t at
+ * step t = 1, 2, ..., and C <- C - lr m^ / (sqrt(w^) + eps), elementwise.
+ * Outputs F_free[f] = B^T c_f (n_free x k) and, if C_out is not NULL, C
+ * (n_free x n_b).  Returns 7 if a coefficient becomes non-finite. */
+int or_extend_adam(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,
+                   int32_t n_free, int32_t k, const double *F_fixed, int32_t n_b, const double *B,
+                   int32_t steps, double lambda, double lr, double beta1, double beta2, double eps,
+                   double *F_free, double *C_out);
+
 /* Chunk partition of the free indices (Section 5.2: column chunks processed
  * independently).  counts[f] = entries of free index f, in order.
  * n_chunks > 0: exactly n_chunks runs (some may be empty); run j starts at

@@ -140,6 +140,73 @@ def test_extension_matches_least_squares(oracle_lib):
         np.testing.assert_allclose(Xgd[f], x, rtol=1e-8, atol=1e-10)
 
 
+def _adam_case(seed, n_b=6, k=3, n_free=3, n_fixed=9):
+    g = np.random.default_rng(seed)
+    F = g.standard_normal((n_fixed, k))
+    B = g.standard_normal((n_b, k))
+    fixed, free = np.nonzero(g.random((n_fixed, n_free)) < 0.8)
+    v = g.standard_normal(fixed.size).astype(np.float32)
+    return F, B, fixed.astype(np.int32), free.astype(np.int32), v
+
+
+def test_extension_adam_first_step_is_normalised_gradient(oracle_lib):
+    """Stage II as Eq. 10 states it, Adam on the coefficients C (Section 5.2).
+    From C = 0 the gradient of L(C) is G_f = -2 sum r B p (the predictions are
+    zero), and after the bias correction Adam's first step is exactly
+    -lr G / (|G| + eps) elementwise, whatever beta1 and beta2 are.  A dropped
+    bias correction, a transposed basis or a wrong sign fails this."""
+    F, B, fixed, free, v = _adam_case(31)
+    lr, eps = 0.01, 1e-8
+    for b1, b2 in ((0.9, 0.999), (0.5, 0.9)):
+        st, X, C1 = oracle_lib.extend_adam(fixed, free, v, 3, F, B, 1, 0.2, lr, b1, b2, eps)
+        assert st == 0
+        for f in range(3):
+            sel = free == f
+            G = -2.0 * B @ (F[fixed[sel]].T @ v[sel].astype(np.float64))
+            np.testing.assert_allclose(C1[f], -lr * G / (np.abs(G) + eps), rtol=1e-12, atol=1e-15)
+            np.testing.assert_allclose(X[f], B.T @ C1[f], rtol=1e-12, atol=1e-15)
+
+
+def test_extension_adam_without_moments_is_sign_descent(oracle_lib):
+    """With beta1 = beta2 = 0 and eps = 0 the moment estimates are the current
+    gradient and its square, so each Adam step is C <- C - lr sign(dL/dC): the
+    textbook sign-gradient method, run here from the loss's own gradient
+    (least squares in the coefficients, with the design rows B p)."""
+    F, B, fixed, free, v = _adam_case(32)
+    lam, lr, steps = 0.3, 0.02, 7
+    st, _, C = oracle_lib.extend_adam(fixed, free, v, 3, F, B, steps, lam, lr, 0.0, 0.0, 0.0)
+    assert st == 0
+    for f in range(3):
+        sel = free == f
+        A = F[fixed[sel]] @ B.T          # design rows: prediction = A c
+        y = v[sel].astype(np.float64)
+        c = np.zeros(B.shape[0])
+        for _ in range(steps):
+            grad = -2.0 * A.T @ (y - A @ c) + 2.0 * lam * c
+            c = c - lr * np.sign(grad)
+        np.testing.assert_allclose(C[f], c, rtol=1e-12, atol=1e-14)
+
+
+def test_extension_adam_converges_to_coefficient_ridge(oracle_lib):
+    """Many small Adam steps reach the minimiser of L(C), a ridge regression in
+    the coefficients: c_f = argmin ||A c - r||^2 + lambda ||c||^2 with design
+    rows A = (B p)^T, solved here by numpy.linalg.lstsq of the stacked system
+    [A; sqrt(lambda) I] c = [r; 0].  (Its factor B^T c_f differs from the
+    factored extension's: the penalty is on C, not on B^T C.)"""
+    F, B, fixed, free, v = _adam_case(33)
+    lam = 0.3
+    st, X, C = oracle_lib.extend_adam(fixed, free, v, 3, F, B, 30000, lam, 2e-3)
+    assert st == 0
+    for f in range(3):
+        sel = free == f
+        A = F[fixed[sel]] @ B.T
+        M = np.vstack([A, math.sqrt(lam) * np.eye(B.shape[0])])
+        y = np.concatenate([v[sel].astype(np.float64), np.zeros(B.shape[0])])
+        c = np.linalg.lstsq(M, y, rcond=None)[0]
+        np.testing.assert_allclose(C[f], c, rtol=0, atol=2e-3 * np.abs(c).max())
+        np.testing.assert_allclose(X[f], B.T @ c, rtol=0, atol=2e-3 * np.abs(B.T @ c).max() * 3)
+
+
 # ------------------------------------------------------- P4 exact recovery
 def test_exact_recovery_noiseless_low_rank(oracle_lib):
     """A noiseless rank-2 30 x 30 matrix with 60 % of cells observed is
