@@ -73,10 +73,13 @@ def parse():
                          "a second JSON line; needs a workload with the whole matrix drawn "
                          "(rating, mid, tiny)")
     ap.add_argument("--extend-steps", type=int, default=20)
-    ap.add_argument("--extend-solver", default="steps", choices=["steps", "ridge"],
-                    help="extension solver: one-sided gradient steps (tsid_extend_chunk) or the "
+    ap.add_argument("--extend-solver", default="steps", choices=["steps", "ridge", "adam"],
+                    help="extension solver: one-sided gradient steps (tsid_extend_chunk), the "
                          "exact ridge solve per free row (tsid_extend_chunk_ridge, fp64 Gram on the "
-                         "matrix cores + Cholesky), both with the fit's lambda")
+                         "matrix cores + Cholesky), or the column phase as Eq. 10 states it (Adam "
+                         "on each free column's coefficients over the template columns' factors, "
+                         "--extend-steps steps, lr 0.01; rows by the exact solve); all with the "
+                         "fit's lambda")
     ap.add_argument("--copy-probe", action="store_true",
                     help="time a plain device copy of 1 GiB instead (HBM probe and the "
                          "reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters)")
@@ -193,16 +196,23 @@ def extension_line(args, p, T, P, Q):
     t0 = time.perf_counter()
     ext = Extension(p.m, p.n, p.u, p.i, p.r, p.I, p.J, n_chunks=16)
     prep_s = time.perf_counter() - t0
+    col_opts = None
     if args.extend_solver == "ridge":
         opts = float(p.lam)  # exact solve per free row
         how = f"exact ridge solve per free row (lambda {p.lam}, fp64 Gram + Cholesky)"
+    elif args.extend_solver == "adam":
+        opts = float(p.lam)
+        col_opts = tsid.make_adam_opts(args.extend_steps, p.lam, 0.01)
+        how = (f"rows by the exact ridge solve; columns by {args.extend_steps} Adam steps on their "
+               f"coefficients over the {p.J.size} template columns' factors (Eq. 10; lr 0.01, "
+               f"lambda {p.lam})")
     else:
         # one-sided steps from zero: lr 0.05 keeps a free row with a single cell stable
         opts = tsid.make_opts(epochs=args.extend_steps, lam=p.lam, lr=0.05, clip=p.clip, xi=p.xi,
                               step="degree")
         how = f"{args.extend_steps} one-sided steps per chunk, degree step"
-    ext.run(T, P, Q, opts)  # warm-up (allocations, code load)
-    _, _, ph = ext.run(T, P, Q, opts)
+    ext.run(T, P, Q, opts, col_opts)  # warm-up (allocations, code load)
+    _, _, ph = ext.run(T, P, Q, opts, col_opts)
     n_row, n_col = ext.rows.nnz, ext.cols.nnz
     t_ext = ph["row_phase_s"] + ph["col_phase_s"]
     h2d_bytes = 12 * (n_row + n_col)

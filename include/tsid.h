@@ -200,6 +200,39 @@ tsid_status tsid_extend_chunk_ridge(tsid_ctx *ctx, int side, const int32_t *fixe
                                     int32_t n_free, const float *F_fixed, int64_t n_fixed,
                                     float *F_free, float lambda);
 
+/* One chunk of the extension as Eq. 10 states it (Stage II, Section 5.2):
+ * free line f is represented in the fixed template basis by a coefficient
+ * vector c_f with one entry per basis line, its entries are predicted as
+ * p . (B^T c_f) with p = F_fixed[fixed_id] (R* = P B^T in factored form), and
+ *   L(C) = sum_(entries) (r - p . B^T c_f)^2 + lambda ||C||_F^2
+ * is minimised by the Adam method from C = 0 for opts->steps steps: per step
+ * the gradient G = dL/dC, m <- beta1 m + (1 - beta1) G,
+ * w <- beta2 w + (1 - beta2) G^2, and C <- C - lr m^ / (sqrt(w^) + eps) with
+ * the bias corrections m^ = m / (1 - beta1^t), w^ = w / (1 - beta2^t) at step
+ * t = 1, 2, ...  All arithmetic is fp32 on the device; every sum has a fixed
+ * order.
+ *  basis     DEVICE n_basis x k fp32 (the template's factors of the side the
+ *            coefficients span: Q_J for free columns, P_I for free rows),
+ *            16-byte aligned; must stay unchanged until the chunk completes.
+ *  F_free    HOST n_free x k: receives B^T c_f after the last step.
+ *  C_out     HOST n_free x n_basis, or NULL: receives C.
+ * The other arguments, asynchrony and staging are those of tsid_extend_chunk;
+ * device memory per staging slot grows by 12 n_free n_basis bytes.
+ * Errors returned here: E_STATE (no template), E_INVAL (bad sizes or
+ * pointers, steps < 0, lambda or eps negative or not finite, lr not finite,
+ * beta1 or beta2 outside [0, 1), k not in {8, 16, 32, 64}), E_NOMEM,
+ * E_DEVICE.  At the next tsid_sync: E_RANGE / E_DUP as for
+ * tsid_extend_chunk, E_NONFINITE if a coefficient becomes non-finite. */
+typedef struct {
+    int32_t steps;
+    float lambda, lr, beta1, beta2, eps;
+} tsid_adam_opts;
+tsid_status tsid_extend_chunk_adam(tsid_ctx *ctx, int side, const int32_t *fixed_id,
+                                   const int32_t *free_local, const float *r, int64_t nnz,
+                                   int32_t n_free, const float *F_fixed, int64_t n_fixed,
+                                   const float *basis, int64_t n_basis, float *F_free,
+                                   float *C_out, const tsid_adam_opts *opts);
+
 /* Wait for every outstanding chunk; returns the first device-side error of
  * those chunks (and clears it), else TSID_OK. */
 tsid_status tsid_sync(tsid_ctx *ctx);

@@ -6,6 +6,7 @@ from .binding import (  # noqa: F401
     Tsid,
     TsidError,
     make_opts,
+    make_adam_opts,
     tsid_chunk_plan,
     lib,
     LIB_PATH,

@@ -52,6 +52,11 @@ class tsid_timing(C.Structure):
                 ("dense_ms", C.c_double * 2), ("dense_launches", C.c_int64 * 2)]
 
 
+class tsid_adam_opts(C.Structure):
+    _fields_ = [("steps", C.c_int32), ("lambda_", C.c_float), ("lr", C.c_float),
+                ("beta1", C.c_float), ("beta2", C.c_float), ("eps", C.c_float)]
+
+
 class tsid_dense_info(C.Structure):
     _fields_ = [("cells", C.c_int64), ("tiles", C.c_int64), ("stripes", C.c_int64 * 2)]
 
@@ -87,6 +92,8 @@ def lib() -> C.CDLL:
         "tsid_extend_chunk": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P,
                                         C.POINTER(tsid_fit_opts)]),
         "tsid_extend_chunk_ridge": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P, C.c_float]),
+        "tsid_extend_chunk_adam": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P, i64, P, P,
+                                             C.POINTER(tsid_adam_opts)]),
         "tsid_sync": (C.c_int, [P]),
         "tsid_export_index": (C.c_int, [P, C.c_int, P, sz]),
         "tsid_chunk_plan": (i32, [P, i64, i32, i64, P, i32]),
@@ -227,6 +234,11 @@ def _ptr(x) -> Optional[int]:
     return x.ctypes.data
 
 
+def make_adam_opts(steps=1, lam=0.0, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8):
+    """Options of tsid_extend_chunk_adam (Adam on the coefficients in a basis)."""
+    return tsid_adam_opts(int(steps), float(lam), float(lr), float(beta1), float(beta2), float(eps))
+
+
 def make_opts(epochs=1, lam=0.0, lr=0.1, clip=False, xi=0.1, prec="fp32", step="sum"):
     return tsid_fit_opts(int(epochs), float(lam), float(lr), float(xi), int(bool(clip)),
                          BF16 if prec == "bf16" else FP32,
@@ -349,6 +361,28 @@ class Tsid:
                                          nnz, n_free, _ptr(F_fixed), F_fixed.shape[0], _ptr(F_free),
                                          float(opts))
             self._check(st, "tsid_extend_chunk_ridge")
+
+    def extend_chunk_adam(self, side, fixed_id, free_local, r, n_free, F_fixed: torch.Tensor,
+                          basis: torch.Tensor, F_free: torch.Tensor, opts: tsid_adam_opts,
+                          C_out: Optional[torch.Tensor] = None):
+        """Queues one chunk solved by Adam on its coefficients in `basis`
+        (tsid_extend_chunk_adam); F_free (and C_out, n_free x n_basis, if given)
+        are CPU tensors that receive the results at sync()."""
+        assert F_fixed.is_cuda and F_fixed.dtype == torch.float32 and F_fixed.is_contiguous()
+        assert basis.is_cuda and basis.dtype == torch.float32 and basis.is_contiguous()
+        assert not F_free.is_cuda and F_free.dtype == torch.float32 and F_free.is_contiguous()
+        if C_out is not None:
+            assert not C_out.is_cuda and C_out.dtype == torch.float32 and C_out.is_contiguous()
+        arrs = []
+        for a, dt in ((fixed_id, np.int32), (free_local, np.int32), (r, np.float32)):
+            arrs.append(a if isinstance(a, torch.Tensor) else np.ascontiguousarray(a, dt))
+        nnz = int(arrs[0].numel() if isinstance(arrs[0], torch.Tensor) else arrs[0].size)
+        self._keep.append((arrs, F_fixed, basis, F_free, C_out, opts))
+        st = lib().tsid_extend_chunk_adam(self.ctx, side, _ptr(arrs[0]), _ptr(arrs[1]), _ptr(arrs[2]), nnz,
+                                          n_free, _ptr(F_fixed), F_fixed.shape[0], _ptr(basis),
+                                          basis.shape[0], _ptr(F_free),
+                                          _ptr(C_out) if C_out is not None else None, C.byref(opts))
+        self._check(st, "tsid_extend_chunk_adam")
 
     def sync(self):
         st = tsid_sync(self.ctx)

@@ -158,6 +158,9 @@ struct ExtSlot {
     int32_t *fid = nullptr, *free_id = nullptr;
     float *r = nullptr;
     float *X = nullptr;  // the chunk's free rows after the last step
+    // Adam extension state (coefficients, moments, partial products, gradients)
+    float *Cst = nullptr, *Mst = nullptr, *Vst = nullptr, *qpart = nullptr, *gt = nullptr;
+    int64_t adam_cap = 0, qpart_cap = 0, gt_cap = 0;
     hipEvent_t ev_h2d = nullptr, ev_staged = nullptr, ev_done = nullptr, ev_flushed = nullptr;
 };
 
@@ -361,6 +364,12 @@ void free_ext_buffers(tsid_ctx *c) {
         A.release(s.free_id);
         A.release(s.r);
         A.release(s.X);
+        A.release(s.Cst);
+        A.release(s.Mst);
+        A.release(s.Vst);
+        A.release(s.qpart);
+        A.release(s.gt);
+        s.adam_cap = s.qpart_cap = s.gt_cap = 0;
     }
     A.release(x.keys);
     A.release(x.keys_alt);
@@ -1312,14 +1321,59 @@ void ext_ensure(tsid_ctx *c, int64_t nnz, int32_t n_free, int32_t k) {
     x.k = k;
 }
 
-// One chunk of the extension: staging, bucketing by free row, then either
-// the one-sided gradient steps of `o` or (ridge != null) the exact solve
-// with lambda = *ridge.
+// The Adam extension's request: options, basis and the optional C output.
+struct AdamReq {
+    const tsid_adam_opts *o;
+    const float *basis;
+    int64_t n_b;
+    float *C_out;
+};
+
+// Per-slot Adam state for n_free x n_b coefficients (grown, never shrunk;
+// growth waits for every chunk in flight, which may still read the old ones).
+void adam_ensure(tsid_ctx *c, ExtSlot &s, int64_t n_free, int64_t n_b, int K) {
+    const int64_t nc = std::max<int64_t>(n_free * n_b, 1), nq = std::max<int64_t>(n_free * adam_slices(n_b) * K, 1),
+                  ng = std::max<int64_t>(n_free * K, 1);
+    if (nc <= s.adam_cap && nq <= s.qpart_cap && ng <= s.gt_cap) return;
+    ext_sync_all(c);
+    Arena &A = c->arena;
+    A.release(s.Cst);
+    A.release(s.Mst);
+    A.release(s.Vst);
+    A.release(s.qpart);
+    A.release(s.gt);
+    s.adam_cap = s.qpart_cap = s.gt_cap = 0;
+    s.Cst = A.alloc<float>(nc);
+    s.Mst = A.alloc<float>(nc);
+    s.Vst = A.alloc<float>(nc);
+    s.qpart = A.alloc<float>(nq);
+    s.gt = A.alloc<float>(ng);
+    s.adam_cap = nc;
+    s.qpart_cap = nq;
+    s.gt_cap = ng;
+}
+
+// One chunk of the extension: staging, bucketing by free row, then the
+// one-sided gradient steps of `o`, or (ridge != null) the exact solve with
+// lambda = *ridge, or (adam != null) Adam on the coefficients in a basis.
 void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t *free_local,
                   const float *r, int64_t nnz, int32_t n_free, const float *F_fixed, int64_t n_fixed,
-                  float *F_free, const tsid_fit_opts *o, const float *ridge) {
+                  float *F_free, const tsid_fit_opts *o, const float *ridge, const AdamReq *adam = nullptr) {
     if (!c->tpl) fail(TSID_E_STATE, "no template: the rank k is set by tsid_build_template");
-    if (ridge) {
+    if (adam) {
+        const tsid_adam_opts *ao = adam->o;
+        if (!ao) fail(TSID_E_INVAL, "opts is NULL");
+        if (ao->steps < 0) fail(TSID_E_INVAL, "steps < 0");
+        if (!(ao->lambda >= 0.f) || !std::isfinite(ao->lambda)) fail(TSID_E_INVAL, "lambda must be finite and >= 0");
+        if (!std::isfinite(ao->lr)) fail(TSID_E_INVAL, "lr must be finite");
+        if (!(ao->beta1 >= 0.f && ao->beta1 < 1.f) || !(ao->beta2 >= 0.f && ao->beta2 < 1.f))
+            fail(TSID_E_INVAL, "beta1 and beta2 must lie in [0, 1)");
+        if (!(ao->eps >= 0.f) || !std::isfinite(ao->eps)) fail(TSID_E_INVAL, "eps must be finite and >= 0");
+        if (!adam_supported(c->tpl->k)) fail(TSID_E_INVAL, "the Adam extension supports k in {8, 16, 32, 64}");
+        if (adam->n_b < 1 || adam->n_b >= (int64_t(1) << 31)) fail(TSID_E_INVAL, "n_basis out of range");
+        if (!adam->basis) fail(TSID_E_INVAL, "basis is NULL");
+        check_aligned(adam->basis, "basis");
+    } else if (ridge) {
         if (!(*ridge >= 0.f) || !std::isfinite(*ridge)) fail(TSID_E_INVAL, "lambda must be finite and >= 0");
         if (!ridge_supported(c->tpl->k)) fail(TSID_E_INVAL, "the exact extension solve supports k in {8, 16, 32, 64}");
     } else {
@@ -1361,7 +1415,38 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
     ptr_from_keys(sk, nnz, n_free, bits_fixed, x.ptr, cs);
     // the slot's result buffer is free once its previous results were flushed
     TSID_HIP(hipStreamWaitEvent(cs, s.ev_flushed, 0));
-    if (ridge) {
+    if (adam) {
+        adam_ensure(c, s, n_free, adam->n_b, K);
+        const int64_t nc = (int64_t)n_free * adam->n_b, nq = (int64_t)n_free * adam_slices(adam->n_b) * K;
+        if (nc) {
+            TSID_HIP(hipMemsetAsync(s.Cst, 0, (size_t)nc * 4, cs));
+            TSID_HIP(hipMemsetAsync(s.Mst, 0, (size_t)nc * 4, cs));
+            TSID_HIP(hipMemsetAsync(s.Vst, 0, (size_t)nc * 4, cs));
+            TSID_HIP(hipMemsetAsync(s.qpart, 0, (size_t)nq * 4, cs));
+        }
+        AdamArgs a{};
+        a.stream = x.stream;
+        a.ptr = x.ptr;
+        a.n_free = n_free;
+        a.F = F_fixed;
+        a.B = adam->basis;
+        a.n_b = adam->n_b;
+        a.n_slices = adam_slices(adam->n_b);
+        a.C = s.Cst;
+        a.M = s.Mst;
+        a.V = s.Vst;
+        a.qpart = s.qpart;
+        a.gt = s.gt;
+        a.X = s.X;
+        a.lambda = adam->o->lambda;
+        a.lr = adam->o->lr;
+        a.beta1 = adam->o->beta1;
+        a.beta2 = adam->o->beta2;
+        a.eps = adam->o->eps;
+        a.err = x.err;
+        a.skip_after_nonfinite = 1;
+        launch_adam(K, a, adam->o->steps, cs);
+    } else if (ridge) {
         RidgeArgs a{};
         a.stream = x.stream;
         a.ptr = x.ptr;
@@ -1393,6 +1478,8 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
     TSID_HIP(hipStreamWaitEvent(c->d2h, s.ev_done, 0));
     if (n_free)
         TSID_HIP(hipMemcpyAsync(F_free, s.X, (size_t)n_free * K * 4, hipMemcpyDeviceToHost, c->d2h));
+    if (adam && adam->C_out && n_free)
+        TSID_HIP(hipMemcpyAsync(adam->C_out, s.Cst, (size_t)n_free * adam->n_b * 4, hipMemcpyDeviceToHost, c->d2h));
     TSID_HIP(hipEventRecord(s.ev_flushed, c->d2h));
     x.pending = true;
     (void)side;
@@ -1591,6 +1678,17 @@ tsid_status tsid_extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, co
                               int64_t n_fixed, float *F_free, const tsid_fit_opts *opts) {
     return guarded(c, [&]() {
         extend_chunk(c, side, fixed_id, free_local, r, nnz, n_free, F_fixed, n_fixed, F_free, opts, nullptr);
+    });
+}
+
+tsid_status tsid_extend_chunk_adam(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t *free_local,
+                                   const float *r, int64_t nnz, int32_t n_free, const float *F_fixed,
+                                   int64_t n_fixed, const float *basis, int64_t n_basis, float *F_free,
+                                   float *C_out, const tsid_adam_opts *opts) {
+    return guarded(c, [&]() {
+        const AdamReq req{opts, basis, n_basis, C_out};
+        extend_chunk(c, side, fixed_id, free_local, r, nnz, n_free, F_fixed, n_fixed, F_free, nullptr, nullptr,
+                     &req);
     });
 }
 

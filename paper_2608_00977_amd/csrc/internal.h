@@ -210,6 +210,27 @@ struct RidgeArgs {
 bool ridge_supported(int K);
 void launch_ridge_rows(int K, const RidgeArgs &a, hipStream_t s);
 
+// ---------------------------------------- extension by Adam on coefficients
+struct AdamArgs {
+    const int2 *stream;   // chunk cells bucketed by free line: {fixed id, value bits}
+    const int64_t *ptr;   // bucket pointers [n_free + 1]
+    int64_t n_free;
+    const float *F;       // fixed factors (rows indexed by fixed id), fp32, K per row
+    const float *B;       // basis factors, n_b x K, fp32
+    int64_t n_b;
+    int32_t n_slices;     // ceil(n_b / 256)
+    float *C, *M, *V;     // coefficients and moments, n_free x n_b
+    float *qpart;         // partial products B^T c_f per slice, n_free x n_slices x K
+    float *gt;            // dL/dx_f, n_free x K
+    float *X;             // results B^T c_f, n_free x K
+    float lambda, lr, beta1, beta2, eps;
+    int32_t *err;
+    int32_t skip_after_nonfinite;
+};
+bool adam_supported(int K);
+int32_t adam_slices(int64_t n_b);
+void launch_adam(int K, const AdamArgs &a, int32_t steps, hipStream_t s);
+
 // ----------------------------------------------------------- dense tiles
 struct DenseArgs {
     const uint16_t *X;        // owner side bf16 copy (rows x K)

@@ -23,7 +23,7 @@ from typing import List, Tuple
 import numpy as np
 import torch
 
-from .binding import Tsid, tsid_chunk_plan
+from .binding import Tsid, tsid_adam_opts, tsid_chunk_plan
 
 
 @dataclass
@@ -79,22 +79,30 @@ class Extension:
         self.cols = _phase(1, ~col_in, i[sel], u[sel], r[sel], n_chunks, max_entries)
         self.template_nnz = int(np.count_nonzero(row_in[u] & col_in[i]))
 
-    def _run_phase(self, T: Tsid, ph: Phase, F_fixed: torch.Tensor, out: torch.Tensor, opts):
+    def _run_phase(self, T: Tsid, ph: Phase, F_fixed: torch.Tensor, out: torch.Tensor, opts,
+                   basis: torch.Tensor):
         for fx, fl, rr, lo, hi in ph.chunks:
-            T.extend_chunk(ph.side, fx, fl, rr, hi - lo, F_fixed, out[lo:hi], opts)
+            if isinstance(opts, tsid_adam_opts):
+                T.extend_chunk_adam(ph.side, fx, fl, rr, hi - lo, F_fixed, basis, out[lo:hi], opts)
+            else:
+                T.extend_chunk(ph.side, fx, fl, rr, hi - lo, F_fixed, out[lo:hi], opts)
         T.sync()
 
-    def run(self, T: Tsid, P_t: torch.Tensor, Q_t: torch.Tensor, opts):
+    def run(self, T: Tsid, P_t: torch.Tensor, Q_t: torch.Tensor, opts, col_opts=None):
         """P_t (m_t x k), Q_t (n_t x k): fp32 device factors of the template,
-        in template order.  opts: tsid_fit_opts for one-sided gradient steps,
-        or a float lambda for the exact ridge solve of every free row.  Returns (P, Q): the full m x k and n x k factors
+        in template order.  opts (and col_opts for the column phase, if given):
+        tsid_fit_opts for one-sided gradient steps, a float lambda for the
+        exact ridge solve of every free line, or tsid_adam_opts for Adam on
+        the coefficients of each free line in the template basis (Eq. 10:
+        free columns over the template columns' factors Q_t, free rows over
+        the template rows' factors P_t).  Returns (P, Q): the full m x k and n x k factors
         as pinned host tensors, and the wall time of each phase in seconds."""
         k = P_t.shape[1]
         P_free = torch.empty((self.rows.free_ids.size, k), dtype=torch.float32).pin_memory()
         Q_free = torch.empty((self.cols.free_ids.size, k), dtype=torch.float32).pin_memory()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        self._run_phase(T, self.rows, Q_t, P_free, opts)
+        self._run_phase(T, self.rows, Q_t, P_free, opts, P_t)
         t1 = time.perf_counter()
         P_full = torch.empty((self.m, k), dtype=torch.float32, device=P_t.device)
         P_full[torch.from_numpy(self.I).to(P_t.device)] = P_t
@@ -102,7 +110,7 @@ class Extension:
             P_full[torch.from_numpy(self.rows.free_ids).to(P_t.device)] = P_free.to(P_t.device)
         torch.cuda.synchronize()
         t2 = time.perf_counter()
-        self._run_phase(T, self.cols, P_full, Q_free, opts)
+        self._run_phase(T, self.cols, P_full, Q_free, opts if col_opts is None else col_opts, Q_t)
         t3 = time.perf_counter()
         P = P_full.cpu()
         Q = torch.empty((self.n, k), dtype=torch.float32)

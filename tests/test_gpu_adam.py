@@ -1,0 +1,221 @@
+"""The extension as Eq. 10 states it (tsid_extend_chunk_adam; Section 5.2:
+Adam on the coefficients C of each free line in the template basis) against
+the oracle's fp64 iteration of the same steps.
+
+Bars.  The library computes in fp32, the oracle in fp64; the only
+differences are rounding and the order of the sums.  How far rounding moves
+the result depends on the case: Adam divides each gradient by its own running
+magnitude, so a coefficient whose gradient passes close to zero amplifies a
+small perturbation (a 2^-24 relative change of the inputs moved the oracle's
+C by 9e-5 in one case below and by 2e-7 in another).  Each parity test
+therefore measures the oracle's own response to perturbations of its inputs
+at the fp32 rounding level (2^-23 relative, three draws) and requires the
+library's C and B^T C within ten times that response (at least 1e-5)
+relative Frobenius error.  With the common eps = 1e-8 the first step is
+lr sign(G), which a gradient within rounding of zero can flip; there the
+objective L(C) is compared instead (1e-4 relative).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import tsid_synth as synth
+from gpu_util import note, rel_fro
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+
+def _ctx(k):
+    import paper_2608_00977_amd as tsid
+    t = tsid.Tsid(0)
+    p = synth.random_case(200, 150, 2000, 64, 48, k, seed=5)
+    t.build_template(p.m, p.n, p.u, p.i, p.r, p.I, p.J, p.k)  # sets the rank
+    return t
+
+
+def _chunk(seed, n_fixed, n_free, n_b, nnz, k):
+    g = np.random.default_rng(seed)
+    F = g.normal(0, k ** -0.25, (n_fixed, k)).astype(np.float32)
+    B = g.normal(0, k ** -0.25, (n_b, k)).astype(np.float32)
+    cells = g.choice(n_fixed * n_free, nnz, replace=False)
+    cells = cells[(cells % n_free) != 0]  # free line 0 has no entries
+    fixed = (cells // n_free).astype(np.int32)
+    free = (cells % n_free).astype(np.int32)
+    r = g.standard_normal(cells.size).astype(np.float32)
+    return F, B, fixed, free, r
+
+
+def _run(T, F, B, fixed, free, r, n_free, opts, side=1):
+    import torch
+    Fd = torch.from_numpy(F).cuda()
+    Bd = torch.from_numpy(B).cuda()
+    X = torch.empty((n_free, F.shape[1]), dtype=torch.float32).pin_memory()
+    C = torch.empty((n_free, B.shape[0]), dtype=torch.float32).pin_memory()
+    T.extend_chunk_adam(side, fixed, free, r, n_free, Fd, Bd, X, opts, C)
+    T.sync()
+    return X.numpy().copy(), C.numpy().copy()
+
+
+def _oracle_with_bar(fixed, free, r, n_free, F, B, steps, lam, lr, b1, b2, eps):
+    """The oracle's result and the parity bars for C and B^T C: ten times its
+    own change under 2^-23 relative perturbations of F and B, at least 1e-5."""
+    st, Xo, Co = oracle.extend_adam(fixed, free, r, n_free, F, B, steps, lam, lr, b1, b2, eps)
+    assert st == 0
+    g = np.random.default_rng(12345)
+    dc = dx = 0.0
+    for _ in range(3):
+        Fp = F.astype(np.float64) * (1 + 2.0 ** -23 * g.standard_normal(F.shape))
+        Bp = B.astype(np.float64) * (1 + 2.0 ** -23 * g.standard_normal(B.shape))
+        st, Xp, Cp = oracle.extend_adam(fixed, free, r, n_free, Fp, Bp, steps, lam, lr, b1, b2, eps)
+        assert st == 0
+        dc, dx = max(dc, rel_fro(Cp, Co)), max(dx, rel_fro(Xp, Xo))
+    return Xo, Co, max(1e-5, 10 * dx), max(1e-5, 10 * dc)
+
+
+def _loss(F, B, fixed, free, r, C, lam):
+    X = np.asarray(C, np.float64) @ np.asarray(B, np.float64)
+    e = r.astype(np.float64) - np.einsum("ij,ij->i", F[fixed].astype(np.float64), X[free])
+    return float(e @ e + lam * np.sum(np.asarray(C, np.float64) ** 2))
+
+
+@pytest.mark.parametrize("k", [8, 16, 32, 64])
+def test_adam_matches_oracle(k):
+    from paper_2608_00977_amd import make_adam_opts
+    n_free, n_b = 120, 300  # two basis slices, the second ragged
+    F, B, fixed, free, r = _chunk(40 + k, 500, n_free, n_b, 6000, k)
+    steps, lam, lr, eps = 15, 0.1, 0.01, 1e-4
+    T = _ctx(k)
+    try:
+        note(f"adam k={k} nnz={r.size}")
+        X, C = _run(T, F, B, fixed, free, r, n_free, make_adam_opts(steps, lam, lr, 0.9, 0.999, eps))
+    finally:
+        T.close()
+    Xo, Co, bar_x, bar_c = _oracle_with_bar(fixed, free, r, n_free, F, B, steps, lam, lr, 0.9, 0.999, eps)
+    assert np.all(C[0] == 0) and np.all(X[0] == 0)  # no entries: the gradient is 2 lambda c = 0
+    assert rel_fro(C, Co) <= bar_c, (rel_fro(C, Co), bar_c)
+    assert rel_fro(X, Xo) <= bar_x, (rel_fro(X, Xo), bar_x)
+
+
+def test_adam_default_eps_objective_matches_oracle():
+    from paper_2608_00977_amd import make_adam_opts
+    k, n_free, n_b = 32, 80, 520
+    F, B, fixed, free, r = _chunk(7, 400, n_free, n_b, 5000, k)
+    steps, lam, lr = 25, 0.05, 0.005
+    T = _ctx(k)
+    try:
+        note("adam default eps")
+        X, C = _run(T, F, B, fixed, free, r, n_free, make_adam_opts(steps, lam, lr))
+    finally:
+        T.close()
+    st, Xo, Co = oracle.extend_adam(fixed, free, r, n_free, F, B, steps, lam, lr)
+    assert st == 0
+    L, Lo = _loss(F, B, fixed, free, r, C, lam), _loss(F, B, fixed, free, r, Co, lam)
+    L0 = _loss(F, B, fixed, free, r, np.zeros_like(Co), lam)
+    assert Lo < 0.9 * L0  # the steps make progress
+    assert abs(L - Lo) <= TOL * Lo, (L, Lo)
+
+
+def test_adam_chunking_is_invariant_and_steps_zero_is_zero():
+    import torch
+    from paper_2608_00977_amd import make_adam_opts
+    k, n_free, n_b = 16, 90, 260
+    F, B, fixed, free, r = _chunk(8, 300, n_free, n_b, 4000, k)
+    opts = make_adam_opts(12, 0.1, 0.01, 0.9, 0.999, 1e-4)
+    T = _ctx(k)
+    try:
+        note("adam chunking")
+        whole, Cw = _run(T, F, B, fixed, free, r, n_free, opts)
+        Fd, Bd = torch.from_numpy(F).cuda(), torch.from_numpy(B).cuda()
+        outs = []
+        for lo, hi in ((0, 30), (30, 61), (61, 90)):
+            m = (free >= lo) & (free < hi)
+            X = torch.empty((hi - lo, k), dtype=torch.float32).pin_memory()
+            C = torch.empty((hi - lo, n_b), dtype=torch.float32).pin_memory()
+            T.extend_chunk_adam(1, fixed[m], (free[m] - lo).astype(np.int32), r[m], hi - lo, Fd, Bd, X, opts, C)
+            outs.append((X, C))
+        T.sync()
+        assert np.array_equal(np.concatenate([o[0].numpy() for o in outs]), whole)
+        assert np.array_equal(np.concatenate([o[1].numpy() for o in outs]), Cw)
+        X0, C0 = _run(T, F, B, fixed, free, r, n_free, make_adam_opts(0, 0.1, 0.01))
+        assert np.all(X0 == 0) and np.all(C0 == 0)
+    finally:
+        T.close()
+
+
+def test_adam_rejects_bad_arguments():
+    import paper_2608_00977_amd as tsid
+    from paper_2608_00977_amd import make_adam_opts
+    F, B, fixed, free, r = _chunk(9, 50, 10, 8, 100, 64)
+    T = _ctx(128)
+    try:
+        with pytest.raises(tsid.TsidError) as ei:
+            _run(T, np.zeros((50, 128), np.float32), np.zeros((8, 128), np.float32), fixed, free, r, 10,
+                 make_adam_opts(3, 0.1, 0.01))
+        assert ei.value.status == tsid.binding.E_INVAL
+    finally:
+        T.close()
+    T = _ctx(64)
+    try:
+        for bad in (make_adam_opts(-1, 0.1, 0.01), make_adam_opts(3, -0.1, 0.01),
+                    make_adam_opts(3, 0.1, float("nan")), make_adam_opts(3, 0.1, 0.01, beta1=1.0),
+                    make_adam_opts(3, 0.1, 0.01, beta2=-0.5), make_adam_opts(3, 0.1, 0.01, eps=-1.0)):
+            with pytest.raises(tsid.TsidError) as ei:
+                _run(T, F, B, fixed, free, r, 10, bad)
+            assert ei.value.status == tsid.binding.E_INVAL
+        # a step size that overflows is reported at sync
+        with pytest.raises(tsid.TsidError) as ei:
+            _run(T, F, B, fixed, free, r, 10, make_adam_opts(3, 0.1, 3e38))
+        assert ei.value.status == tsid.binding.E_NONFINITE
+        X, _ = _run(T, F, B, fixed, free, r, 10, make_adam_opts(3, 0.1, 0.01))  # still usable
+        assert np.all(np.isfinite(X))
+    finally:
+        T.close()
+
+
+def test_adam_extension_column_phase_end_to_end():
+    """Both extension phases on a Rating-shaped matrix at 5% scale: rows by
+    the exact ridge solve, then columns by Adam on their coefficients over the
+    template columns' factors, against the oracle's ridge and Adam iterations
+    of the same cells from the same template factors."""
+    import torch
+    import paper_2608_00977_amd as tsid
+    from paper_2608_00977_amd import make_adam_opts
+    from paper_2608_00977_amd.extension import Extension
+    p = synth.rating(scale=0.05)
+    lam, steps, lr, eps = 0.05, 20, 0.01, 1e-4
+    g = np.random.default_rng(4)
+    Pt = g.normal(0, p.k ** -0.25, (p.I.size, p.k)).astype(np.float32)
+    Qt = g.normal(0, p.k ** -0.25, (p.J.size, p.k)).astype(np.float32)
+    T = tsid.Tsid(0)
+    try:
+        T.build_template(p.m, p.n, p.u, p.i, p.r, p.I, p.J, p.k)
+        ext = Extension(p.m, p.n, p.u, p.i, p.r, p.I, p.J, n_chunks=4)
+        note(f"adam extension cols={ext.cols.free_ids.size} basis={p.J.size}")
+        P, Q, _ = ext.run(T, torch.from_numpy(Pt).cuda(), torch.from_numpy(Qt).cuda(), lam,
+                          col_opts=make_adam_opts(steps, lam, lr, 0.9, 0.999, eps))
+    finally:
+        T.close()
+    P, Q = P.numpy(), Q.numpy()
+    row_in = np.zeros(p.m, bool)
+    row_in[p.I] = True
+    col_pos = np.full(p.n, -1, np.int64)
+    col_pos[p.J] = np.arange(p.J.size)
+    free_rows = ext.rows.free_ids
+    rpos = np.full(p.m, -1, np.int64)
+    rpos[free_rows] = np.arange(free_rows.size)
+    sel = (~row_in[p.u]) & (col_pos[p.i] >= 0)
+    st, Pf = oracle.ridge(col_pos[p.i[sel]].astype(np.int32), rpos[p.u[sel]].astype(np.int32), p.r[sel],
+                          free_rows.size, Qt, lam)
+    assert st == 0
+    # the column phase reads the library's row factors (the ridge solves agree to 1e-6)
+    free_cols = ext.cols.free_ids
+    cpos = np.full(p.n, -1, np.int64)
+    cpos[free_cols] = np.arange(free_cols.size)
+    sel = cpos[p.i] >= 0
+    Qf, _, bar_x, _ = _oracle_with_bar(p.u[sel].astype(np.int32), cpos[p.i[sel]].astype(np.int32), p.r[sel],
+                                       free_cols.size, P, Qt, steps, lam, lr, 0.9, 0.999, eps)
+    assert rel_fro(P[free_rows], Pf) <= 1e-5
+    assert rel_fro(Q[free_cols], Qf) <= bar_x, (rel_fro(Q[free_cols], Qf), bar_x)
+    assert np.array_equal(Q[p.J], Qt)
