@@ -51,6 +51,10 @@ def lib() -> C.CDLL:
                                  i32, P, P]),
             "or_extend": (C.c_int, [i64, P, P, P, i32, i32, P, P, i32, f64, f64, i32, i32, f64]),
             "or_ridge": (C.c_int, [i64, P, P, P, i32, i32, P, f64, P]),
+            "or_splitmix64": (C.c_uint64, [C.c_uint64]),
+            "or_batch_of": (i32, [i32, i32, C.c_uint64, i32]),
+            "or_fit_minibatch": (C.c_int, [i64, P, P, P, i32, i32, i32, P, P, i32, f64, f64, i32, i32,
+                                           f64, i32, i32, C.c_uint64, P, P]),
             "or_extend_adam": (C.c_int, [i64, P, P, P, i32, i32, P, i32, P, i32, f64, f64, f64, f64,
                                          f64, P, P]),
             "or_chunk_plan": (i32, [P, i64, i32, i64, P, i32]),
@@ -127,6 +131,27 @@ def fit(a, b, v, P0, Q0, epochs, lam, lr, step="sum", clip=False, xi=0.1, bf16=F
     st = lib().or_fit(a.size, _p(a), _p(b), _p(v), P.shape[0], Q.shape[0], P.shape[1], _p(P),
                       _p(Q), epochs, lam, lr, STEP[step], int(clip), xi, int(bf16), _p(hist),
                       _p(done))
+    return st, P, Q, hist, int(done[0])
+
+
+def splitmix64(x: int) -> int:
+    return int(lib().or_splitmix64(C.c_uint64(x & 0xFFFFFFFFFFFFFFFF)))
+
+
+def batch_of(a: int, b: int, seed: int, n_batches: int) -> int:
+    return int(lib().or_batch_of(int(a), int(b), C.c_uint64(seed), int(n_batches)))
+
+
+def fit_minibatch(a, b, v, P0, Q0, epochs, lam, lr, step="sum", clip=False, xi=0.1, bf16=False,
+                  n_batches=2, seed=0):
+    a, b, v = _c(a, np.int32), _c(b, np.int32), _c(v, np.float32)
+    P = np.array(P0, np.float64, order="C", copy=True)
+    Q = np.array(Q0, np.float64, order="C", copy=True)
+    hist = np.full(epochs + 1, np.nan)
+    done = np.zeros(1, np.int32)
+    st = lib().or_fit_minibatch(a.size, _p(a), _p(b), _p(v), P.shape[0], Q.shape[0], P.shape[1], _p(P),
+                                _p(Q), epochs, lam, lr, STEP[step], int(clip), xi, int(bf16), n_batches,
+                                C.c_uint64(seed), _p(hist), _p(done))
     return st, P, Q, hist, int(done[0])
 
 

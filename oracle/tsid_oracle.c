@@ -271,6 +271,112 @@ int or_fit(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
     return status;
 }
 
+/* ------------------------------------------------------ mini-batch epochs */
+
+uint64_t or_splitmix64(uint64_t x) {
+    uint64_t z = x + 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+int32_t or_batch_of(int32_t a, int32_t b, uint64_t seed, int32_t n_batches) {
+    const uint64_t key = ((uint64_t)(uint32_t)a << 32) | (uint64_t)(uint32_t)b;
+    return (int32_t)(or_splitmix64(seed ^ key) % (uint64_t)n_batches);
+}
+
+int or_fit_minibatch(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+                     int32_t m_t, int32_t n_t, int32_t k, double *P, double *Q,
+                     int32_t epochs, double lambda, double lr, int32_t step,
+                     int32_t clip, double xi, int32_t bf16, int32_t n_batches, uint64_t seed,
+                     double *loss_hist, int32_t *epochs_done) {
+    int64_t lp = (int64_t)m_t * k, lq = (int64_t)n_t * k;
+    double *gP = (double *)malloc((size_t)(lp + 1) * sizeof(double));
+    double *gQ = (double *)malloc((size_t)(lq + 1) * sizeof(double));
+    double *Pn = (double *)malloc((size_t)(lp + 1) * sizeof(double));
+    double *Qn = (double *)malloc((size_t)(lq + 1) * sizeof(double));
+    double *Ps = (double *)malloc((size_t)(lp + 1) * sizeof(double));
+    double *Qs = (double *)malloc((size_t)(lq + 1) * sizeof(double));
+    int32_t *deg_r = (int32_t *)malloc(((size_t)m_t + 1) * sizeof(int32_t));
+    int32_t *deg_c = (int32_t *)malloc(((size_t)n_t + 1) * sizeof(int32_t));
+    int32_t *batch = (int32_t *)malloc(((size_t)nnz + 1) * sizeof(int32_t));
+    for (int64_t e = 0; e < nnz; ++e) batch[e] = or_batch_of(a[e], b[e], seed, n_batches);
+    int status = 0;
+    int32_t t;
+    for (t = 0; t < epochs && status == 0; ++t) {
+        /* L(P_t, Q_t) at the start of the epoch, over every cell */
+        const double *Pr = P, *Qr = Q;
+        if (bf16) {
+            round_copy(P, Ps, lp);
+            round_copy(Q, Qs, lq);
+            Pr = Ps;
+            Qr = Qs;
+        }
+        if (loss_hist)
+            loss_hist[t] = sse_grad(nnz, a, b, v, k, Pr, Qr, NULL, NULL) + lambda * (sumsq(P, lp) + sumsq(Q, lq));
+        /* one full-gradient step per batch, on the batch's cells only, each
+           from the factors the previous batch left */
+        for (int32_t beta = 0; beta < n_batches && status == 0; ++beta) {
+            Pr = P;
+            Qr = Q;
+            if (bf16) {
+                round_copy(P, Ps, lp);
+                round_copy(Q, Qs, lq);
+                Pr = Ps;
+                Qr = Qs;
+            }
+            memset(gP, 0, (size_t)lp * sizeof(double));
+            memset(gQ, 0, (size_t)lq * sizeof(double));
+            memset(deg_r, 0, ((size_t)m_t + 1) * sizeof(int32_t));
+            memset(deg_c, 0, ((size_t)n_t + 1) * sizeof(int32_t));
+            for (int64_t e = 0; e < nnz; ++e) {
+                if (batch[e] != beta) continue;
+                const double *p = Pr + (int64_t)a[e] * k, *q = Qr + (int64_t)b[e] * k;
+                const double err = (double)v[e] - dot(p, q, k);
+                double *gp = gP + (int64_t)a[e] * k, *gq = gQ + (int64_t)b[e] * k;
+                for (int32_t c = 0; c < k; ++c) {
+                    gp[c] += -2.0 * err * q[c];
+                    gq[c] += -2.0 * err * p[c];
+                }
+                deg_r[a[e]] += 1;
+                deg_c[b[e]] += 1;
+            }
+            int finite = 1;
+            /* rows and columns without a cell in the batch are not touched */
+            for (int32_t x = 0; x < m_t; ++x) {
+                if (deg_r[x] == 0) memcpy(Pn + (int64_t)x * k, P + (int64_t)x * k, (size_t)k * sizeof(double));
+                else finite &= update_row(P + (int64_t)x * k, gP + (int64_t)x * k, deg_r[x], k, lambda, lr, step,
+                                          clip, xi, Pn + (int64_t)x * k);
+            }
+            for (int32_t x = 0; x < n_t; ++x) {
+                if (deg_c[x] == 0) memcpy(Qn + (int64_t)x * k, Q + (int64_t)x * k, (size_t)k * sizeof(double));
+                else finite &= update_row(Q + (int64_t)x * k, gQ + (int64_t)x * k, deg_c[x], k, lambda, lr, step,
+                                          clip, xi, Qn + (int64_t)x * k);
+            }
+            if (!finite) {
+                status = 7;
+                break;
+            }
+            memcpy(P, Pn, (size_t)lp * sizeof(double));
+            memcpy(Q, Qn, (size_t)lq * sizeof(double));
+        }
+    }
+    if (status) t -= 1; /* the failing epoch did not complete */
+    if (status == 0 && loss_hist) {
+        const double *Pr = P, *Qr = Q;
+        if (bf16) {
+            round_copy(P, Ps, lp);
+            round_copy(Q, Qs, lq);
+            Pr = Ps;
+            Qr = Qs;
+        }
+        loss_hist[epochs] = sse_grad(nnz, a, b, v, k, Pr, Qr, NULL, NULL) + lambda * (sumsq(P, lp) + sumsq(Q, lq));
+    }
+    if (epochs_done) *epochs_done = t;
+    free(gP); free(gQ); free(Pn); free(Qn); free(Ps); free(Qs); free(deg_r); free(deg_c); free(batch);
+    return status;
+}
+
 /* ------------------------------------------------------------ extension */
 
 int or_extend(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,

@@ -68,6 +68,29 @@ int or_fit(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
            int32_t epochs, double lambda, double lr, int32_t step,
            int32_t clip, double xi, int32_t bf16, double *loss_hist, int32_t *epochs_done);
 
+/* splitmix64 (the published 64-bit finaliser of the SplitMix generator):
+ * z = x + 0x9E3779B97F4A7C15, then two xor-shift-multiply rounds and a final
+ * xor-shift.  Cell (a, b) of the template (positions in I and J) belongs to
+ * mini-batch splitmix64(seed ^ (a << 32 | b)) mod n_batches. */
+uint64_t or_splitmix64(uint64_t x);
+int32_t or_batch_of(int32_t a, int32_t b, uint64_t seed, int32_t n_batches);
+
+/* Mini-batch epochs (the in-epoch updates of the stochastic method of
+ * Section 5.1, Eq. 9, grouped into mini-batches): each epoch visits the
+ * n_batches batches in order and takes, for each, the full-gradient step of
+ * or_fit restricted to the batch's cells (the degree step divides by the
+ * batch degree, Eq. 9's 1/n over the contributing entries), from the factors
+ * the previous batch left; rows and columns without a cell in the batch are
+ * not touched.  loss_hist[t] = L(P_t, Q_t) over every cell at the start of
+ * epoch t, loss_hist[epochs] at the end.  On a non-finite update the factors
+ * are those before the failing batch step, *epochs_done the whole epochs
+ * completed, and the status 7. */
+int or_fit_minibatch(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+                     int32_t m_t, int32_t n_t, int32_t k, double *P, double *Q,
+                     int32_t epochs, double lambda, double lr, int32_t step,
+                     int32_t clip, double xi, int32_t bf16, int32_t n_batches, uint64_t seed,
+                     double *loss_hist, int32_t *epochs_done);
+
 /* One-sided extension (Section 5.2, Eq. 6 in factored form): the fixed
  * factors F_fixed (rows indexed by fixed_id) stay constant; each free row
  * f in [0, n_free) starts at zero and takes `steps` gradient steps on

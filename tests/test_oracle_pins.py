@@ -427,3 +427,120 @@ def test_chunk_plan_definition(oracle_lib):
             assert tot <= C or e - s == 1
             if e < n_free:
                 assert tot + int(counts[e]) > C
+
+
+# ------------------------------------------------------- NEXT-4 mini-batches
+def test_splitmix64_published_outputs(oracle_lib):
+    """The batch hash is SplitMix64's output function (Steele, Lea and Flood,
+    2014): from state 0 the generator's first outputs are the published
+    values, the state advancing by the golden-ratio increment."""
+    gamma = 0x9E3779B97F4A7C15
+    want = [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F, 0xF88BB8A8724C81EC]
+    got = [oracle_lib.splitmix64((i * gamma) & (2 ** 64 - 1)) for i in range(4)]
+    assert got == want
+
+
+def test_minibatch_batches_are_balanced(oracle_lib):
+    """Every cell falls in exactly one of B batches, and the batch sizes of
+    many cells are those of a uniform draw (within five standard deviations)."""
+    g = np.random.default_rng(4)
+    a = g.integers(0, 5000, 40000)
+    b = g.integers(0, 5000, 40000)
+    for B in (2, 3, 8):
+        idx = np.array([oracle_lib.batch_of(x, y, 11, B) for x, y in zip(a, b)])
+        assert idx.min() >= 0 and idx.max() < B
+        cnt = np.bincount(idx, minlength=B)
+        sd = math.sqrt(a.size * (1 / B) * (1 - 1 / B))
+        assert np.all(np.abs(cnt - a.size / B) < 5 * sd), cnt
+
+
+def _every_line_observed(seed, m, n, nnz):
+    g = np.random.default_rng(seed)
+    cells = {(x, int(g.integers(n))) for x in range(m)} | {(int(g.integers(m)), y) for y in range(n)}
+    while len(cells) < nnz:
+        cells.add((int(g.integers(m)), int(g.integers(n))))
+    c = np.array(sorted(cells))
+    return c[:, 0].astype(np.int32), c[:, 1].astype(np.int32), g.standard_normal(len(c)).astype(np.float32)
+
+
+@pytest.mark.parametrize("step", ["sum", "degree"])
+def test_minibatch_one_batch_is_the_full_gradient_epoch(oracle_lib, step):
+    """With one batch every epoch is a single full-gradient step (Eqs. 3-5):
+    the Jacobi fit's factors and losses, bit for bit, when every row and
+    column has a cell (a line without one is left alone by a batch step)."""
+    a, b, v = _every_line_observed(0, 30, 25, 300)
+    g = np.random.default_rng(1)
+    P0, Q0 = g.normal(0, .5, (30, 8)), g.normal(0, .5, (25, 8))
+    r1 = oracle_lib.fit(a, b, v, P0, Q0, 6, 0.1, 0.01, step, True, 0.1)
+    r2 = oracle_lib.fit_minibatch(a, b, v, P0, Q0, 6, 0.1, 0.01, step, True, 0.1, n_batches=1, seed=9)
+    assert r1[0] == r2[0] == 0 and r2[4] == 6
+    for x, y in zip(r1[1:4], r2[1:4]):
+        assert np.array_equal(x, y)
+
+
+def test_minibatch_two_batches_by_hand(oracle_lib):
+    """One row and two columns, k = 1, each cell in its own batch (seed 2:
+    cell (0, 0) in batch 0, cell (0, 1) in batch 1).  The first batch moves p
+    and q0 by Eqs. 3-5 on its one cell and leaves q1 alone; the second moves p
+    again, from its new value, and q1."""
+    assert oracle_lib.batch_of(0, 0, 2, 2) == 0 and oracle_lib.batch_of(0, 1, 2, 2) == 1
+    p, q0, q1, v0, v1, lam, lr = 0.7, -0.4, 1.3, 2.0, -1.0, 0.25, 0.1
+    e = v0 - p * q0
+    p1 = p - lr * (-2 * e * q0 + 2 * lam * p)
+    q01 = q0 - lr * (-2 * e * p + 2 * lam * q0)
+    e = v1 - p1 * q1
+    p2 = p1 - lr * (-2 * e * q1 + 2 * lam * p1)
+    q11 = q1 - lr * (-2 * e * p1 + 2 * lam * q1)
+    loss0 = (v0 - p * q0) ** 2 + (v1 - p * q1) ** 2 + lam * (p * p + q0 * q0 + q1 * q1)
+    for step in ("sum", "degree"):  # one cell per line per batch: both rules agree
+        st, P, Q, h, done = oracle_lib.fit_minibatch(
+            np.zeros(2, np.int32), np.array([0, 1], np.int32), np.array([v0, v1], np.float32),
+            np.array([[p]]), np.array([[q0], [q1]]), 1, lam, lr, step, n_batches=2, seed=2)
+        assert st == 0 and done == 1
+        assert h[0] == pytest.approx(loss0, rel=1e-15)
+        assert P[0, 0] == pytest.approx(p2, rel=1e-14)
+        assert Q[0, 0] == pytest.approx(q01, rel=1e-14) and Q[1, 0] == pytest.approx(q11, rel=1e-14)
+
+
+def test_minibatch_brute_force_tiny(oracle_lib):
+    """Three batches on a tiny matrix against a per-cell Python sweep of the
+    same rule: each batch's gradient from the factors the previous batch
+    left, rows and columns divided by their cell count in the batch."""
+    a, b, v = _every_line_observed(5, 6, 5, 18)
+    g = np.random.default_rng(6)
+    P0, Q0 = g.normal(0, .5, (6, 3)), g.normal(0, .5, (5, 3))
+    lam, lr, B, seed, epochs = 0.2, 0.05, 3, 123, 3
+    P, Q = P0.copy(), Q0.copy()
+    for _ in range(epochs):
+        for beta in range(B):
+            gP, gQ = np.zeros_like(P), np.zeros_like(Q)
+            dP, dQ = np.zeros(6), np.zeros(5)
+            for x, y, r in zip(a, b, v):
+                if oracle_lib.batch_of(x, y, seed, B) != beta:
+                    continue
+                err = float(r) - sum(P[x, c] * Q[y, c] for c in range(3))
+                for c in range(3):
+                    gP[x, c] -= 2 * err * Q[y, c]
+                    gQ[y, c] -= 2 * err * P[x, c]
+                dP[x] += 1
+                dQ[y] += 1
+            for F, G, D in ((P, gP, dP), (Q, gQ, dQ)):
+                for x in range(F.shape[0]):
+                    if D[x]:
+                        F[x] = F[x] - lr * (G[x] + 2 * lam * F[x]) / D[x]
+    st, Po, Qo, h, done = oracle_lib.fit_minibatch(a, b, v, P0, Q0, epochs, lam, lr, "degree",
+                                                   n_batches=B, seed=seed)
+    assert st == 0 and done == epochs
+    np.testing.assert_allclose(Po, P, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(Qo, Q, rtol=1e-12, atol=1e-14)
+
+
+def test_minibatch_nonfinite_reports_whole_epochs(oracle_lib):
+    """A step size that overflows ends the mini-batch fit with status 7 and
+    counts only the epochs that completed; the factors stay finite."""
+    a, b, v = _every_line_observed(7, 20, 20, 150)
+    g = np.random.default_rng(8)
+    st, P, Q, h, done = oracle_lib.fit_minibatch(a, b, v, g.normal(0, 1, (20, 4)), g.normal(0, 1, (20, 4)),
+                                                 100, 0.1, 1e6, "sum", n_batches=4, seed=1)
+    assert st == 7 and 0 <= done < 100
+    assert np.all(np.isfinite(P)) and np.all(np.isfinite(Q))
