@@ -62,6 +62,10 @@ def parse():
     ap.add_argument("--dense-fill", type=float, default=-1.0,
                     help="dense head tiles of bf16 fits (tsid_set_dense_tiles): < 0 automatic, "
                          "0 off, in (0, 1] forced with that tile fill")
+    ap.add_argument("--minibatch", type=int, default=0,
+                    help="mini-batch epochs with this many batches (tsid_set_minibatch; 0: full-gradient "
+                         "epochs); they run the item pass without dense tiles")
+    ap.add_argument("--minibatch-seed", type=int, default=1)
     ap.add_argument("--time-every", type=int, default=10,
                     help="attach HIP timing events to the kernels of every n-th timed epoch (each "
                          "timed dispatch costs a few microseconds of wall time)")
@@ -150,7 +154,7 @@ def traffic_from_profiles(kernel_src_sha, which):
     return ent.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(p, seconds):
+def cpu_baseline(p, seconds, batches=0, seed=0):
     import numpy as np
 
     import oracle
@@ -158,18 +162,24 @@ def cpu_baseline(p, seconds):
     a, b, v = oracle.filter_template(p.u, p.i, p.r, rm, cm)
     S = int(min(a.size, 2_000_000))
     a, b, v = a[:S], b[:S], v[:S]
+    if batches:
+        run = lambda ep: oracle.fit_minibatch(a, b, v, p.P0, p.Q0, ep, p.lam, p.lr, p.step, p.clip, p.xi,
+                                              bf16=p.prec == "bf16", n_batches=batches, seed=seed)
+    else:
+        run = lambda ep: oracle.fit(a, b, v, p.P0, p.Q0, ep, p.lam, p.lr, p.step, p.clip, p.xi,
+                                    bf16=p.prec == "bf16")
     t0 = time.perf_counter()
-    oracle.fit(a, b, v, p.P0, p.Q0, 1, p.lam, p.lr, p.step, p.clip, p.xi, bf16=p.prec == "bf16")
+    run(1)
     one = time.perf_counter() - t0
     epochs = max(1, int(seconds / max(one, 1e-3)))
     t0 = time.perf_counter()
-    oracle.fit(a, b, v, p.P0, p.Q0, epochs, p.lam, p.lr, p.step, p.clip, p.xi,
-               bf16=p.prec == "bf16")
+    run(epochs)
     el = time.perf_counter() - t0
     return {"value": S * epochs / el, "unit": "entries/s", "cores": 1, "kind": "oracle",
             "sample": f"first {S} template cells (input order, i.e. a uniform random sample) of "
                       f"the same workload, all {p.I.size} x {p.J.size} template factor rows, "
-                      f"{epochs} full-gradient epochs, serial fp64 C",
+                      f"{epochs} " + (f"mini-batch epochs ({batches} batches)" if batches else
+                                      "full-gradient epochs") + ", serial fp64 C",
             "seconds": el, "nproc": os.cpu_count()}
 
 
@@ -263,6 +273,10 @@ def main():
     T = tsid.Tsid(0)
     T.set_pass_kernel(args.pass_kernel)
     T.set_dense_tiles(args.dense_fill)
+    if args.minibatch:
+        T.set_minibatch(args.minibatch, args.minibatch_seed)
+        T.set_pass_kernel("item")
+        T.set_dense_tiles(0)
     u = torch.from_numpy(p.u).pin_memory()
     i = torch.from_numpy(p.i).pin_memory()
     r = torch.from_numpy(p.r).pin_memory()
@@ -307,6 +321,11 @@ def main():
     split = tm["fixup_launches"] > 0
     di = T.dense_info()
     sparse_nnz = nnz - di["cells"]
+    if args.minibatch:
+        # timed launches are the first batch's passes: its own cells, every
+        # owner row read and written (lines without a cell keep theirs)
+        bp = T.export_index("batch_ptr_r")
+        sparse_nnz = int(bp[m_t] - bp[0])
     by = [pass_bytes(sparse_nnz, m_t, n_t, k, p.prec, kernels[0] == "slab" and split),
           pass_bytes(sparse_nnz, n_t, m_t, k, p.prec, kernels[1] == "slab" and split)]
     if di["tiles"]:
@@ -329,7 +348,8 @@ def main():
     achieved = dom_by / (dom_ms / 1e3) / 1e9
     src = open(os.path.join(ROOT, "paper_2608_00977_amd", "csrc", ksrc), "rb").read()
     sha = hashlib.sha256(src).hexdigest()
-    traffic = traffic_from_profiles(sha, f"{args.config}:{which}:{kkind}")
+    traffic = traffic_from_profiles(sha, f"{args.config}:{which}:{kkind}"
+                                    + (f":minibatch{args.minibatch}" if args.minibatch else ""))
     epoch_bytes = by[0] + by[1] + (sum(c[1] for c in cand[2:]) if di["tiles"] else 0)
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
@@ -348,7 +368,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
-        cpu = cpu_baseline(p, args.cpu_seconds)
+        cpu = cpu_baseline(p, args.cpu_seconds, args.minibatch, args.minibatch_seed)
         log(f"oracle {cpu['value']:.4e} cells/s over {cpu['seconds']:.1f}s")
 
     workload = {
@@ -361,6 +381,8 @@ def main():
         "mid": "Mid template fit: 4,096 x 2,048 of 20,000 x 10,000 (2M cells), k=32, fp32",
         "tiny": "Tiny template fit: 200 x 160 of 1,000 x 800 (40k cells), k=8, fp32",
     }[args.config]
+    if args.minibatch:
+        workload += f"; mini-batch epochs, {args.minibatch} batches (seed {args.minibatch_seed}), loss pass each epoch"
     line = {
         "metric": "observed entries/sec per template-fit epoch; achieved HBM GB/s vs peak",
         "value": value,
@@ -379,7 +401,9 @@ def main():
                    "precision": p.prec, "step": p.step, "lr": p.lr, "lambda": p.lam,
                    "clip": p.clip, "parallelism": "single GPU",
                    "pass_kernels": {"p_pass": kernels[0], "q_pass": kernels[1]},
-                   "dense_tiles": dense},
+                   "dense_tiles": dense,
+                   "minibatch": {"batches": args.minibatch, "seed": args.minibatch_seed,
+                                 "first_batch_cells": sparse_nnz} if args.minibatch else None},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "compulsory_GBps_per_epoch": round(epoch_bytes / (ms_per_step / 1e3) / 1e9, 2),

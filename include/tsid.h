@@ -300,6 +300,36 @@ typedef struct {
 } tsid_dense_info;
 tsid_status tsid_fit_dense_info(const tsid_ctx *ctx, tsid_dense_info *out);
 
+/* Mini-batch epochs for tsid_fit_template (Section 5.1: the stochastic
+ * method updates the factors within an epoch, Eq. 9 averaging each update
+ * over the entries it uses; here the entries are grouped into mini-batches).
+ * Cell (a, b) of the template (a: position of its row in I, b: of its column
+ * in J) belongs to batch splitmix64(seed ^ (a << 32 | b)) mod n_batches, with
+ * splitmix64 the output function of the SplitMix64 generator (Steele, Lea and
+ * Flood, 2014).  Each epoch then takes one step per batch, in batch order:
+ * the Jacobi step of Eqs. 3-5 (with the options' step rule and clip) on the
+ * batch's cells only, from the factors the previous batch left, where the
+ * degree step divides by the line's cell count in the batch and rows and
+ * columns without a cell in the batch keep their values.  The loss history
+ * holds L(P, Q) over every cell at the start of each epoch and after the
+ * last.  On a non-finite update the fit returns E_NONFINITE with the factors
+ * before the failing batch step; tsid_fit_epochs_done gives the whole epochs
+ * completed before it, and the loss entries of later epochs are NaN.
+ *  n_batches = 0   (default) full-gradient (Jacobi) epochs.
+ *  1 <= n_batches <= TSID_MAX_BATCHES   mini-batch epochs; they run the item
+ *                  pass (a fit with TSID_PASS_SLAB or forced dense tiles
+ *                  returns E_INVAL), and n_batches times the template's rows
+ *                  (and columns) must be below 2^31.
+ * The batch-major copies of the streams (8 bytes per cell and side) and the
+ * batch pointers (8 bytes per batch and row or column) are built at the
+ * first such fit after a template, batch-count or seed change and kept with
+ * the template.  With timing on, pass_ms / fixup_ms cover the first batch's
+ * passes of a timed epoch and epoch_ms the whole epoch (its loss pass
+ * included).  Takes effect at the next tsid_fit_template.
+ * Errors: E_INVAL (ctx NULL, n_batches outside [0, TSID_MAX_BATCHES]). */
+#define TSID_MAX_BATCHES 4096
+tsid_status tsid_set_minibatch(tsid_ctx *ctx, int32_t n_batches, uint64_t seed);
+
 /* Kernel timing of the template fit (a tracing aid).  With every = n > 0,
  * the kernels of every n-th epoch of tsid_fit_template (epochs 0, n, 2n, ...)
  * are launched with a start and an end HIP event attached to their dispatch
@@ -338,11 +368,16 @@ tsid_status tsid_get_timing(const tsid_ctx *ctx, tsid_timing *out);
  *   TSID_IDX_ROW_PTR int64 m_t+1  TSID_IDX_CSR_COL int32 nnz  TSID_IDX_CSR_VAL fp32 nnz
  *   TSID_IDX_COL_PTR int64 n_t+1  TSID_IDX_CSC_ROW int32 nnz  TSID_IDX_CSC_VAL fp32 nnz
  *   TSID_IDX_DEG_R   int32 m_t    TSID_IDX_DEG_C   int32 n_t
+ *   TSID_IDX_BATCH_PTR_R int64 B*m_t+1   TSID_IDX_BATCH_PTR_C int64 B*n_t+1
+ * The batch pointers (after a mini-batch fit, B its batch count; E_STATE
+ * before): entry beta * rows + x is the first cell of row (column) x of
+ * batch beta in the batch-major stream, so the cells of row x in batch beta
+ * number ptr[beta * m_t + x + 1] - ptr[beta * m_t + x].
  * bytes must equal count * element size.  Errors: E_STATE, E_INVAL, E_DEVICE. */
 enum {
     TSID_IDX_ROW_MAP = 0, TSID_IDX_COL_MAP = 1, TSID_IDX_ROW_PTR = 2, TSID_IDX_CSR_COL = 3,
     TSID_IDX_CSR_VAL = 4, TSID_IDX_COL_PTR = 5, TSID_IDX_CSC_ROW = 6, TSID_IDX_CSC_VAL = 7,
-    TSID_IDX_DEG_R = 8, TSID_IDX_DEG_C = 9
+    TSID_IDX_DEG_R = 8, TSID_IDX_DEG_C = 9, TSID_IDX_BATCH_PTR_R = 10, TSID_IDX_BATCH_PTR_C = 11
 };
 tsid_status tsid_export_index(const tsid_ctx *ctx, int which, void *host_dst, size_t bytes);
 

@@ -29,7 +29,7 @@ FP32, BF16 = 0, 1
 STEP_SUM, STEP_DEGREE = 0, 1
 PASS_KERNEL = {"auto": 0, "item": 1, "slab": 2}
 IDX = {"row_map": 0, "col_map": 1, "row_ptr": 2, "csr_col": 3, "csr_val": 4, "col_ptr": 5,
-       "csc_row": 6, "csc_val": 7, "deg_r": 8, "deg_c": 9}
+       "csc_row": 6, "csc_val": 7, "deg_r": 8, "deg_c": 9, "batch_ptr_r": 10, "batch_ptr_c": 11}
 
 
 class TsidError(RuntimeError):
@@ -87,6 +87,7 @@ def lib() -> C.CDLL:
         "tsid_fit_pass_kernels": (C.c_int, [P, P, P]),
         "tsid_get_timing": (C.c_int, [P, C.POINTER(tsid_timing)]),
         "tsid_set_dense_tiles": (C.c_int, [P, C.c_float]),
+        "tsid_set_minibatch": (C.c_int, [P, i32, C.c_uint64]),
         "tsid_fit_dense_info": (C.c_int, [P, C.POINTER(tsid_dense_info)]),
         "tsid_loss": (C.c_int, [P, P, P, C.c_float, P]),
         "tsid_extend_chunk": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P,
@@ -179,6 +180,10 @@ def tsid_get_timing(ctx) -> dict:
 
 def tsid_set_dense_tiles(ctx, fill: float) -> int:
     return lib().tsid_set_dense_tiles(ctx, float(fill))
+
+
+def tsid_set_minibatch(ctx, n_batches: int, seed: int) -> int:
+    return lib().tsid_set_minibatch(ctx, int(n_batches), C.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF))
 
 
 def tsid_fit_dense_info(ctx) -> dict:
@@ -321,6 +326,13 @@ class Tsid:
         forced with that tile fill (tsid_set_dense_tiles)."""
         self._check(tsid_set_dense_tiles(self.ctx, fill), "tsid_set_dense_tiles")
 
+    def set_minibatch(self, n_batches: int, seed: int = 0):
+        """Mini-batch epochs: n_batches batches per epoch dealt by a hash of
+        each cell's template position and `seed`; 0 restores full-gradient
+        epochs (tsid_set_minibatch)."""
+        self._check(tsid_set_minibatch(self.ctx, n_batches, seed), "tsid_set_minibatch")
+        self._batches = int(n_batches)
+
     def dense_info(self) -> dict:
         """cells, tiles and stripes (P pass, Q pass) of the last fit's dense
         head tiles (tsid_fit_dense_info)."""
@@ -396,7 +408,9 @@ class Tsid:
                 "row_ptr": (np.int64, n_rows + 1), "col_ptr": (np.int64, n_cols + 1),
                 "csr_col": (np.int32, inf["nnz"]), "csr_val": (np.float32, inf["nnz"]),
                 "csc_row": (np.int32, inf["nnz"]), "csc_val": (np.float32, inf["nnz"]),
-                "deg_r": (np.int32, n_rows), "deg_c": (np.int32, n_cols)}[name]
+                "deg_r": (np.int32, n_rows), "deg_c": (np.int32, n_cols),
+                "batch_ptr_r": (np.int64, getattr(self, "_batches", 0) * n_rows + 1),
+                "batch_ptr_c": (np.int64, getattr(self, "_batches", 0) * n_cols + 1)}[name]
         count = kind[1] if kind[1] is not None else self._dims[0 if name == "row_map" else 1]
         out = np.empty(count, kind[0])
         self._check(tsid_export_index(self.ctx, IDX[name], _ptr(out), out.nbytes),

@@ -127,6 +127,20 @@ struct DensePlan {
     float *gd[2] = {nullptr, nullptr};
 };
 
+// Mini-batch epochs (minibatch.hip): batch-major copies of both streams,
+// the bucket pointers of every batch (batch beta of side s: ptr[s] +
+// beta * rows, rows + 1 entries) and, per precision, every batch's work plan.
+struct MiniPlan {
+    bool ready = false;
+    int32_t B = 0;
+    uint64_t seed = 0;
+    int2 *stream[2] = {nullptr, nullptr};
+    int64_t *ptr[2] = {nullptr, nullptr};
+    std::vector<int64_t> hptr[2];     // host copies (B * rows + 1)
+    std::vector<Plan> plan[2][2];     // [side][precision], B plans once built
+    int64_t max_items[2] = {0, 0};    // [precision]: largest plan
+};
+
 struct Template {
     int64_t m = 0, n = 0, nnz = 0;
     int32_t m_t = 0, n_t = 0, k = 0;
@@ -139,6 +153,7 @@ struct Template {
     SlabPlan slab[2];              // [side], fp32 only
     DensePlan dense;               // bf16 only
     bool dense_use = false;        // the current fit runs the dense tiles
+    MiniPlan mb;
 };
 
 // Epochs whose loss terms are kept before one batched reduction.
@@ -201,6 +216,8 @@ struct tsid_ctx {
     float dense_fill = -1.f;           // tsid_set_dense_tiles: < 0 auto, 0 off, > 0 fill
     tsid_dense_info dense_used{};       // of the last fit
     int32_t used_kernel[2] = {0, 0};  // pass kernel of each side in the last fit
+    int32_t mb_batches = 0;           // tsid_set_minibatch: 0 full-gradient epochs
+    uint64_t mb_seed = 0;
 };
 
 namespace {
@@ -210,7 +227,9 @@ void set_device(const tsid_ctx *c) { TSID_HIP(hipSetDevice(c->device)); }
 // Timed kernels of one epoch; each takes a start and an end event attached to
 // its dispatch (the loss reduction: start of its first kernel, end of its last).
 enum TimedKernel {
-    TK_PPASS = 0, TK_PFIX = 1, TK_QPASS = 2, TK_QFIX = 3, TK_REDUCE = 4, TK_PDENSE = 5, TK_QDENSE = 6, kTimed = 7
+    TK_PPASS = 0, TK_PFIX = 1, TK_QPASS = 2, TK_QFIX = 3, TK_REDUCE = 4, TK_PDENSE = 5, TK_QDENSE = 6,
+    TK_EPOCH = 7,  // a whole mini-batch epoch (events recorded on the stream around it)
+    kTimed = 8
 };
 constexpr int kEvents = 2 * kTimed;
 
@@ -244,8 +263,12 @@ void collect_timing(tsid_ctx *c, int epochs) {
     tsid_timing &t = c->tm;
     for (int ep = 0; ep < epochs; ++ep) {
         const uint8_t l = c->launched[(size_t)ep];
+        if (l & (1u << TK_EPOCH)) {
+            t.epoch_ms += dt(ev(ep, TK_EPOCH, 0), ev(ep, TK_EPOCH, 1));
+            t.epochs += 1;
+        }
         for (int k = 0; k < kTimed; ++k) {
-            if (!(l & (1u << k))) continue;
+            if (!(l & (1u << k)) || k == TK_EPOCH) continue;
             const double ms = dt(ev(ep, k, 0), ev(ep, k, 1));
             if (k == TK_PPASS || k == TK_QPASS) {
                 t.pass_ms[k / 2] += ms;
@@ -261,7 +284,7 @@ void collect_timing(tsid_ctx *c, int epochs) {
                 t.fixup_launches += 1;
             }
         }
-        if (!(l & (1u << TK_PPASS))) continue;  // not a sampled epoch
+        if (!(l & (1u << TK_PPASS)) || (l & (1u << TK_EPOCH))) continue;  // not a sampled Jacobi epoch
         // an epoch runs dense P, P pass, P fixup, dense Q, Q pass, Q fixup in that order
         const int first = (l & (1u << TK_PDENSE)) ? (int)TK_PDENSE : (int)TK_PPASS;
         int end_k = TK_PPASS;
@@ -310,6 +333,23 @@ void free_dense(tsid_ctx *c, DensePlan &d) {
     d = DensePlan{};
 }
 
+void free_plan(tsid_ctx *c, Plan &pl) {
+    c->arena.release(pl.item_off);
+    c->arena.release(pl.item_end);
+    c->arena.release(pl.items);
+    pl = Plan{};
+}
+
+void free_minibatch(tsid_ctx *c, MiniPlan &mb) {
+    for (int sd = 0; sd < 2; ++sd) {
+        c->arena.release(mb.stream[sd]);
+        c->arena.release(mb.ptr[sd]);
+        for (auto &v : mb.plan[sd])
+            for (Plan &pl : v) free_plan(c, pl);
+    }
+    mb = MiniPlan{};
+}
+
 void free_template(tsid_ctx *c, Template *&t) {
     if (!t) return;
     Arena &A = c->arena;
@@ -331,6 +371,7 @@ void free_template(tsid_ctx *c, Template *&t) {
         A.release(sp.carry);
     }
     free_dense(c, t->dense);
+    free_minibatch(c, t->mb);
     delete t;
     t = nullptr;
 }
@@ -957,16 +998,102 @@ void ensure_dense(tsid_ctx *c, int prec) {
     t.dense_use = mode > 0.f ? true : t.dense.cells >= TSID_DENSE_MIN_SHARE * (double)t.nnz && t.dense.tiles > 0;
 }
 
-// dense: whether a fit is about to run (the loss evaluation uses no tiles)
-void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs, bool dense) {
+// Mini-batch streams and pointers for the context's batch count and seed
+// (rebuilt when either changes), then the batch plans of precision prec.
+void ensure_minibatch(tsid_ctx *c, int prec) {
+    Template &t = *c->tpl;
+    MiniPlan &mb = t.mb;
+    const int32_t B = c->mb_batches;
+    if (!mb.ready || mb.B != B || mb.seed != c->mb_seed) {
+        free_minibatch(c, mb);
+        for (int sd = 0; sd < 2; ++sd)
+            if ((int64_t)B * (sd ? t.n_t : t.m_t) >= INT32_MAX)
+                fail(TSID_E_INVAL, "n_batches times the template's rows (or columns) must be below 2^31");
+        Arena &A = c->arena;
+        hipStream_t cs = c->comp;
+        const int64_t n = t.nnz;
+        uint64_t *keys = nullptr, *keys_alt = nullptr;
+        uint32_t *vals = nullptr, *vals_alt = nullptr, *tmp = nullptr;
+        auto cleanup = [&]() {
+            (void)hipStreamSynchronize(cs);
+            A.release(keys);
+            A.release(keys_alt);
+            A.release(vals);
+            A.release(vals_alt);
+            A.release(tmp);
+        };
+        try {
+            keys = A.alloc<uint64_t>(n);
+            keys_alt = A.alloc<uint64_t>(n);
+            vals = A.alloc<uint32_t>(n);
+            vals_alt = A.alloc<uint32_t>(n);
+            tmp = A.alloc<uint32_t>((int64_t)radix_scratch_elems(n));
+            for (int sd = 0; sd < 2; ++sd) {
+                const int32_t rows = sd ? t.n_t : t.m_t;
+                const int64_t nkeys = (int64_t)B * rows;
+                const int2 *st = sd ? t.stream_c : t.stream_r;
+                batch_keys(st, sd ? t.col_ptr : t.row_ptr, rows, sd, c->mb_seed, B, keys, vals, cs);
+                // stable: each batch keeps its cells bucketed by owner row in stream order
+                const bool alt = radix_sort(keys, vals, keys_alt, vals_alt, n, bits_for(nkeys), tmp, cs);
+                mb.stream[sd] = A.alloc<int2>(n);
+                mb.ptr[sd] = A.alloc<int64_t>(nkeys + 1);
+                gather_stream(st, alt ? vals_alt : vals, n, mb.stream[sd], cs);
+                ptr_from_keys(alt ? keys_alt : keys, n, (int32_t)nkeys, 0, mb.ptr[sd], cs);
+                mb.hptr[sd].resize((size_t)nkeys + 1);
+                TSID_HIP(hipMemcpyAsync(mb.hptr[sd].data(), mb.ptr[sd], ((size_t)nkeys + 1) * 8,
+                                        hipMemcpyDeviceToHost, cs));
+                TSID_HIP(hipStreamSynchronize(cs));
+            }
+        } catch (...) {
+            cleanup();
+            free_minibatch(c, mb);
+            throw;
+        }
+        cleanup();
+        mb.B = B;
+        mb.seed = c->mb_seed;
+        mb.ready = true;
+    }
+    if (mb.plan[0][prec].empty()) {
+        // items sized for a batch's share of the cells
+        const int64_t E = choose_E(std::max<int64_t>(1, t.nnz / B));
+        const int ng = items_per_wave(t.k, prec);
+        int64_t most = 0;
+        try {
+            for (int sd = 0; sd < 2; ++sd) {
+                const int32_t rows = sd ? t.n_t : t.m_t;
+                auto &v = mb.plan[sd][prec];
+                for (int32_t b = 0; b < B; ++b) {
+                    const std::vector<int64_t> sub(mb.hptr[sd].begin() + (int64_t)b * rows,
+                                                   mb.hptr[sd].begin() + (int64_t)b * rows + rows + 1);
+                    v.push_back(build_plan(c, sub, rows, E, ng));
+                    most = std::max<int64_t>(most, v.back().n_items);
+                }
+            }
+        } catch (...) {
+            for (int sd = 0; sd < 2; ++sd) {
+                for (Plan &pl : mb.plan[sd][prec]) free_plan(c, pl);
+                mb.plan[sd][prec].clear();
+            }
+            throw;
+        }
+        mb.max_items[prec] = most;
+    }
+}
+
+// dense: whether a fit is about to run (the loss evaluation uses no tiles);
+// extra_items: the largest work plan of a mini-batch fit (0 otherwise)
+void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs, bool dense, int64_t extra_items = 0) {
     Template &t = *c->tpl;
     FitBufs &f = c->fb;
     Arena &A = c->arena;
     const int64_t lp = (int64_t)t.m_t * t.k, lq = (int64_t)t.n_t * t.k;
     ensure_plan(c, 0, prec);
     ensure_plan(c, 1, prec);
-    ensure_slab(c, 0, prec);
-    ensure_slab(c, 1, prec);
+    if (c->mb_batches == 0) {  // mini-batch epochs run the item pass only
+        ensure_slab(c, 0, prec);
+        ensure_slab(c, 1, prec);
+    }
     if (dense)
         ensure_dense(c, prec);
     else
@@ -983,7 +1110,7 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs, bool dense) {
     const int64_t need = std::max({(int64_t)t.plan[0][prec].n_items, (int64_t)t.plan[1][prec].n_items,
                                    t.slab[0].use ? t.slab[0].lanes() : 0, t.slab[1].use ? t.slab[1].lanes() : 0,
                                    t.dense_use ? (int64_t)t.dense.plan[0].n_items + t.dense.n_segs[0] : 0,
-                                   t.dense_use ? (int64_t)t.dense.plan[1].n_items : 0});
+                                   t.dense_use ? (int64_t)t.dense.plan[1].n_items : 0, extra_items});
     if (need > f.item_cap) {  // partial sums and per-item e^2, sized for this precision's plans
         A.release(f.carry_r);
         A.release(f.carry_c);
@@ -1074,11 +1201,140 @@ SlabArgs slab_args(const Template &t, int side, const tsid_fit_opts &o, int32_t 
     return a;
 }
 
+// Mini-batch epochs: epoch ep takes one step per batch beta (global step
+// s = ep * B + beta), each an item pass of both sides over the batch's cells
+// from the factors the previous step left (P and Q of one step both move
+// from the same iterate, as in a Jacobi epoch); lines without a cell in the
+// batch keep their rows.  The loss of epoch ep is evaluated over every cell
+// before its first step.  The factor buffers alternate every step, so the
+// iterate before step s sits in buffer s & 1.
+void fit_minibatch(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_hist) {
+    Template &t = *c->tpl;
+    if (c->pass_kernel == TSID_PASS_SLAB)
+        fail(TSID_E_INVAL, "mini-batch epochs run the item pass (the slab pass walks whole buckets)");
+    if (c->dense_fill > 0.f) fail(TSID_E_INVAL, "mini-batch epochs do not use dense tiles");
+    const int32_t B = c->mb_batches;
+    if ((int64_t)o->epochs * B >= INT32_MAX - 1) fail(TSID_E_INVAL, "epochs times n_batches must be below 2^31 - 1");
+    const int K = t.k, prec = o->prec, T = o->epochs;
+    ensure_minibatch(c, prec);
+    MiniPlan &mb = t.mb;
+    ensure_fit_buffers(c, prec, T, false, mb.max_items[prec]);
+    c->epochs_done = 0;
+    c->dense_used = tsid_dense_info{};
+    c->used_kernel[0] = c->used_kernel[1] = TSID_PASS_ITEM;
+    FitBufs &f = c->fb;
+    hipStream_t cs = c->comp;
+    const int64_t lp = (int64_t)t.m_t * K, lq = (int64_t)t.n_t * K;
+    if (lp) TSID_HIP(hipMemcpyAsync(f.P[0], P, (size_t)lp * 4, hipMemcpyDeviceToDevice, cs));
+    if (lq) TSID_HIP(hipMemcpyAsync(f.Q[0], Q, (size_t)lq * 4, hipMemcpyDeviceToDevice, cs));
+    if (prec == TSID_BF16) {
+        launch_to_bf16(f.P[0], lp, f.Pb[0], cs);
+        launch_to_bf16(f.Q[0], lq, f.Qb[0], cs);
+    }
+    TSID_HIP(hipMemsetAsync(c->err_dev, 0, ERR_SLOTS * sizeof(int32_t), cs));
+    // the loss pass walks the whole stream with the template's own plan
+    PassArgs full = pass_args(t, 0, *o, c->err_dev);
+    full.skip_after_nonfinite = 1;
+    full.Xn = nullptr;
+    const int64_t ne = full.n_items;
+    PassArgs step[2] = {pass_args(t, 0, *o, c->err_dev), pass_args(t, 1, *o, c->err_dev)};
+    for (int sd = 0; sd < 2; ++sd) {
+        step[sd].stream = mb.stream[sd];
+        step[sd].keep_empty = 1;
+        step[sd].skip_after_nonfinite = 1;
+        step[sd].e2 = nullptr;
+        step[sd].norm = nullptr;
+    }
+    step[0].carry = f.carry_r;
+    step[1].carry = f.carry_c;
+    if (c->timing) ensure_events(c, (size_t)T);
+    const bool want_loss = loss_hist != nullptr;
+    int pend = 0;
+    auto flush = [&](int upto, std::pair<hipEvent_t, hipEvent_t> ev) {
+        launch_loss_reduce(f.e2, f.item_cap, ne, f.normP, t.m_t, f.normQ, t.n_t, o->lambda, upto - pend,
+                           f.partial, f.loss + pend, nullptr, pend, cs, ev.first, ev.second);
+        pend = upto;
+    };
+    auto loss_pass = [&](int ep, int buf) {
+        const int slot = ep % kLossRing;
+        full.epoch = ep * B;  // skipped after a failure in an earlier step
+        full.X = f.P[buf];
+        full.Y = prec ? (const void *)f.Qb[buf] : (const void *)f.Q[buf];
+        full.e2 = f.e2 + slot * f.item_cap;
+        full.norm = f.normP + (int64_t)slot * t.m_t;
+        launch_item_pass(K, prec, true, full, cs);
+        launch_row_norms(K, f.Q[buf], t.n_t, f.normQ + (int64_t)slot * t.n_t, cs);
+    };
+    int cur = 0;
+    for (int ep = 0; ep < T; ++ep) {
+        auto eve = timed(c, ep, TK_EPOCH);
+        if (eve.first) TSID_HIP(hipEventRecord(eve.first, cs));
+        if (want_loss) loss_pass(ep, cur);
+        for (int32_t beta = 0; beta < B; ++beta) {
+            const int nxt = cur ^ 1;
+            for (int sd = 0; sd < 2; ++sd) {
+                PassArgs &a = step[sd];
+                const int32_t rows = sd ? t.n_t : t.m_t;
+                const Plan &pl = mb.plan[sd][prec][(size_t)beta];
+                a.ptr = mb.ptr[sd] + (int64_t)beta * rows;
+                a.items = pl.items;
+                a.item_off = pl.item_off;
+                a.item_end = pl.item_end;
+                a.n_items = pl.n_items;
+                a.E = pl.E;
+                a.epoch = ep * B + beta;
+                float *const *X = sd ? f.Q : f.P;
+                float *const *Y = sd ? f.P : f.Q;
+                uint16_t *const *Xb = sd ? f.Qb : f.Pb;
+                uint16_t *const *Yb = sd ? f.Pb : f.Qb;
+                a.X = X[cur];
+                a.Y = prec ? (const void *)Yb[cur] : (const void *)Y[cur];
+                a.Xn = X[nxt];
+                a.Xn_b = prec ? Xb[nxt] : nullptr;
+                auto ev = beta == 0 ? timed(c, ep, sd ? TK_QPASS : TK_PPASS) : std::pair<hipEvent_t, hipEvent_t>{};
+                launch_item_pass(K, prec, false, a, cs, ev.first, ev.second);
+                if (pl.spans) {
+                    ev = beta == 0 ? timed(c, ep, sd ? TK_QFIX : TK_PFIX) : std::pair<hipEvent_t, hipEvent_t>{};
+                    launch_fixup(K, prec, a, cs, ev.first, ev.second);
+                }
+            }
+            cur = nxt;
+        }
+        if (eve.second) TSID_HIP(hipEventRecord(eve.second, cs));
+        if (want_loss && ep % kLossRing == kLossRing - 1) flush(ep + 1, timed(c, ep, TK_REDUCE));
+    }
+    if (want_loss) {  // L(P_T, Q_T), then the epochs not reduced yet
+        loss_pass(T, cur);
+        flush(T + 1, {nullptr, nullptr});
+    }
+    std::vector<double> hist((size_t)T + 1);
+    if (loss_hist) TSID_HIP(hipMemcpyAsync(hist.data(), f.loss, (size_t)(T + 1) * 8, hipMemcpyDeviceToHost, cs));
+    TSID_HIP(hipMemcpyAsync(c->err_host, c->err_dev, ERR_SLOTS * 4, hipMemcpyDeviceToHost, cs));
+    TSID_HIP(hipStreamSynchronize(cs));
+    if (c->timing) collect_timing(c, T);
+    const int32_t bad = c->err_host[ERR_NONFINITE];
+    // with a failure in step s: the iterate before it, and the whole epochs before it
+    const int64_t s_fail = bad ? bad - 1 : (int64_t)T * B;
+    const int last = bad ? (int)(s_fail / B) : T;
+    c->epochs_done = last;
+    const int src = (int)(s_fail & 1);
+    if (lp) TSID_HIP(hipMemcpyAsync(P, f.P[src], (size_t)lp * 4, hipMemcpyDeviceToDevice, cs));
+    if (lq) TSID_HIP(hipMemcpyAsync(Q, f.Q[src], (size_t)lq * 4, hipMemcpyDeviceToDevice, cs));
+    TSID_HIP(hipStreamSynchronize(cs));
+    if (loss_hist) {
+        for (int ep = 0; ep <= T; ++ep) loss_hist[ep] = ep <= last ? hist[ep] : NAN;
+    }
+    if (bad)
+        fail(TSID_E_NONFINITE, "non-finite update in epoch " + std::to_string(last) + ", batch " +
+                                   std::to_string(s_fail % B));
+}
+
 void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_hist) {
     if (!c->tpl) fail(TSID_E_STATE, "no template: call tsid_build_template first");
     check_opts(o);
     Template &t = *c->tpl;
     if ((t.m_t && !P) || (t.n_t && !Q)) fail(TSID_E_INVAL, "NULL factor pointer");
+    if (c->mb_batches > 0) return fit_minibatch(c, P, Q, o, loss_hist);
     ensure_fit_buffers(c, o->prec, o->epochs, true);
     c->epochs_done = 0;
     FitBufs &f = c->fb;
@@ -1533,6 +1789,14 @@ void export_index(const tsid_ctx *c, int which, void *dst, size_t bytes) {
         case TSID_IDX_CSC_VAL: split(t.stream_c, 1); break;
         case TSID_IDX_DEG_R: degrees(t.row_ptr, t.m_t); break;
         case TSID_IDX_DEG_C: degrees(t.col_ptr, t.n_t); break;
+        case TSID_IDX_BATCH_PTR_R:
+        case TSID_IDX_BATCH_PTR_C: {
+            const int sd = which == TSID_IDX_BATCH_PTR_C;
+            if (!t.mb.ready) fail(TSID_E_STATE, "no mini-batch fit has run on this template");
+            need(t.mb.hptr[sd].size() * 8);
+            std::memcpy(dst, t.mb.hptr[sd].data(), bytes);
+            break;
+        }
         default: fail(TSID_E_INVAL, "unknown index structure");
     }
 }
@@ -1641,6 +1905,13 @@ tsid_status tsid_fit_pass_kernels(const tsid_ctx *c, int32_t *p_pass, int32_t *q
 tsid_status tsid_set_dense_tiles(tsid_ctx *c, float fill) {
     if (!c || !(fill <= 1.f)) return TSID_E_INVAL;  // NaN fails the comparison
     c->dense_fill = fill < 0.f ? -1.f : fill;
+    return TSID_OK;
+}
+
+tsid_status tsid_set_minibatch(tsid_ctx *c, int32_t n_batches, uint64_t seed) {
+    if (!c || n_batches < 0 || n_batches > TSID_MAX_BATCHES) return TSID_E_INVAL;
+    c->mb_batches = n_batches;
+    c->mb_seed = seed;
     return TSID_OK;
 }
 

@@ -166,6 +166,7 @@ __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg,
         }
     }
     const float s = A.degree ? 1.0f / (float)(deg > 1 ? deg : 1) : 1.0f;
+    const bool keep = A.keep_empty && deg == 0;
     float xn[V];
     bool bad = false;
     float nrm = 0.f;
@@ -174,7 +175,7 @@ __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg,
         const float g = 2.0f * A.lam * x[v] - 2.0f * acc[v];
         float d = -s * g;
         if (A.clip && d > A.xi) d = A.xi;
-        xn[v] = x[v] + A.lr * d;
+        xn[v] = keep ? x[v] : x[v] + A.lr * d;
         bad |= !__builtin_isfinite(xn[v]);
         nrm += x[v] * x[v];
     }

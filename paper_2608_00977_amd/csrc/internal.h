@@ -86,6 +86,13 @@ void chunk_keys(const int32_t *fixed_id, const int32_t *free_id, const float *r,
 void plan_items(const int64_t *ptr, int32_t rows, int32_t E, uint32_t *item_off, int32_t *items,
                 uint32_t *nparts_scratch, uint32_t *scan_scratch, hipStream_t s);
 
+// Mini-batch epochs (minibatch.hip): keys[j] = batch * rows + owner row of
+// cell j of a bucketed stream (side 0: rows of the template, side 1: its
+// columns) and vals[j] = j; then out[j] = in[idx[j]].
+void batch_keys(const int2 *stream, const int64_t *ptr, int32_t rows, int side, uint64_t seed, int32_t n_batches,
+                uint64_t *keys, uint32_t *vals, hipStream_t s);
+void gather_stream(const int2 *in, const uint32_t *idx, int64_t n, int2 *out, hipStream_t s);
+
 // ------------------------------------------------------------------- fit
 struct PassArgs {
     const int2 *stream;      // bucketed entries {other id, value bits}
@@ -117,6 +124,9 @@ struct PassArgs {
     const int64_t *dptr;     // or null: degrees from ptr
     const float *gd;         // rows x K, or null
     const uint32_t *gd_tile_ptr;
+    // 1: a bucket without cells keeps its row as it is (a mini-batch step
+    // touches only the rows and columns of the batch's cells)
+    int32_t keep_empty;
 };
 
 // prec: 0 fp32, 1 bf16.  loss_only: residuals, e2 and norms only.
