@@ -191,15 +191,53 @@ static double sse_grad(int64_t nnz, const int32_t *a, const int32_t *b, const fl
     return sse;
 }
 
-/* New value of one factor row from its data gradient g (Eqs. 3-5, Section 5.3). */
+/* Per-entry order of the clipped update (Section 5.3 applied to each entry's
+ * own gradient, Eqs. 3-4, before the 1/n average of Eq. 9): cell (p, q) with
+ * residual err adds, per coordinate, its descent direction 2 err q - 2 lambda
+ * p clipped at xi to the row sums gp, and likewise to gq.  Products use the
+ * (possibly bf16-rounded) pr, qr; the regulariser uses the masters p, q. */
+static void cell_terms_per_entry(const double *pr, const double *qr, const double *p, const double *q,
+                                 double err, int32_t k, double lambda, double xi, double *gp, double *gq) {
+    for (int32_t c = 0; c < k; ++c) {
+        double dp = 2.0 * err * qr[c] - 2.0 * lambda * p[c];
+        double dq = 2.0 * err * pr[c] - 2.0 * lambda * q[c];
+        if (dp > xi) dp = xi;
+        if (dq > xi) dq = xi;
+        gp[c] += dp;
+        gq[c] += dq;
+    }
+}
+
+/* The per-entry sums of every cell (clip mode 2), with the squared residuals. */
+static double sse_terms_per_entry(int64_t nnz, const int32_t *a, const int32_t *b, const float *v, int32_t k,
+                                  const double *Pr, const double *Qr, const double *P, const double *Q,
+                                  double lambda, double xi, double *gP, double *gQ) {
+    double sse = 0.0;
+    for (int64_t e = 0; e < nnz; ++e) {
+        const int64_t oa = (int64_t)a[e] * k, ob = (int64_t)b[e] * k;
+        const double err = (double)v[e] - dot(Pr + oa, Qr + ob, k);
+        sse += err * err;
+        cell_terms_per_entry(Pr + oa, Qr + ob, P + oa, Q + ob, err, k, lambda, xi, gP + oa, gQ + ob);
+    }
+    return sse;
+}
+
+/* New value of one factor row (Eqs. 3-5, Section 5.3).  clip 0 / 1: g holds
+ * the data gradient -2 sum e q; the regulariser is added once, the step
+ * scaled by s, and with clip 1 the direction clipped.  clip 2: g holds the
+ * clipped per-entry directions, and the row moves by lr s g. */
 static int update_row(const double *x, const double *g, int32_t deg, int32_t k, double lambda,
                       double lr, int32_t step, int32_t clip, double xi, double *x_new) {
     double s = step ? 1.0 / (double)(deg > 1 ? deg : 1) : 1.0;
     int finite = 1;
     for (int32_t c = 0; c < k; ++c) {
-        double grad = g[c] + 2.0 * lambda * x[c];
-        double d = -s * grad;
-        if (clip && d > xi) d = xi;
+        double d;
+        if (clip == 2) {
+            d = s * g[c];
+        } else {
+            d = -s * (g[c] + 2.0 * lambda * x[c]);
+            if (clip && d > xi) d = xi;
+        }
         x_new[c] = x[c] + lr * d;
         if (!isfinite(x_new[c])) finite = 0;
     }
@@ -239,7 +277,8 @@ int or_fit(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
         }
         memset(gP, 0, (size_t)lp * sizeof(double));
         memset(gQ, 0, (size_t)lq * sizeof(double));
-        double sse = sse_grad(nnz, a, b, v, k, Pr, Qr, gP, gQ);
+        double sse = clip == 2 ? sse_terms_per_entry(nnz, a, b, v, k, Pr, Qr, P, Q, lambda, xi, gP, gQ)
+                               : sse_grad(nnz, a, b, v, k, Pr, Qr, gP, gQ);
         if (loss_hist) loss_hist[t] = sse + lambda * (sumsq(P, lp) + sumsq(Q, lq));
         int finite = 1;
         for (int32_t x = 0; x < m_t; ++x)
@@ -334,9 +373,14 @@ int or_fit_minibatch(int64_t nnz, const int32_t *a, const int32_t *b, const floa
                 const double *p = Pr + (int64_t)a[e] * k, *q = Qr + (int64_t)b[e] * k;
                 const double err = (double)v[e] - dot(p, q, k);
                 double *gp = gP + (int64_t)a[e] * k, *gq = gQ + (int64_t)b[e] * k;
-                for (int32_t c = 0; c < k; ++c) {
-                    gp[c] += -2.0 * err * q[c];
-                    gq[c] += -2.0 * err * p[c];
+                if (clip == 2) {
+                    cell_terms_per_entry(p, q, P + (int64_t)a[e] * k, Q + (int64_t)b[e] * k, err, k, lambda, xi,
+                                         gp, gq);
+                } else {
+                    for (int32_t c = 0; c < k; ++c) {
+                        gp[c] += -2.0 * err * q[c];
+                        gq[c] += -2.0 * err * p[c];
+                    }
                 }
                 deg_r[a[e]] += 1;
                 deg_c[b[e]] += 1;
@@ -382,6 +426,7 @@ int or_fit_minibatch(int64_t nnz, const int32_t *a, const int32_t *b, const floa
 int or_extend(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,
               int32_t n_free, int32_t k, const double *F_fixed, double *F_free,
               int32_t steps, double lambda, double lr, int32_t step, int32_t clip, double xi) {
+    if (clip == 2) return 1; /* the per-entry order is a template-fit option */
     int64_t len = (int64_t)n_free * k;
     double *g = (double *)malloc((size_t)(len + 1) * sizeof(double));
     double *xn = (double *)malloc((size_t)(len + 1) * sizeof(double));

@@ -56,7 +56,12 @@ double or_loss(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
  *   step: 0 = plain gradient step, 1 = per-row/column step scaled by
  *         1/max(1, degree) (the 1/n normalisation of Eq. 5, applied to P and Q).
  *   clip: asymmetric clipping of Section 5.3, d <- min(d, xi) per coordinate
- *         of the descent direction (NaN propagates).
+ *         of the descent direction (NaN propagates).  1 = on the row's summed
+ *         direction (regulariser once per row, Eq. 2).  2 = per entry, before
+ *         the sum (the clipped update of Section 5.3 applied to Eqs. 3-4 entry
+ *         by entry): each cell contributes min(2 e q - 2 lambda p, xi) per
+ *         coordinate, so the regulariser enters once per cell; the row then
+ *         moves by lr s times the sum, and a row without cells stays.
  *   bf16: 1 = the dots and gradient products read bf16 (round-to-nearest-even)
  *         copies of the factors; the fp64 master takes the update.
  * P (m_t x k) and Q (n_t x k) are updated in place; loss_hist (epochs + 1
@@ -94,7 +99,8 @@ int or_fit_minibatch(int64_t nnz, const int32_t *a, const int32_t *b, const floa
 /* One-sided extension (Section 5.2, Eq. 6 in factored form): the fixed
  * factors F_fixed (rows indexed by fixed_id) stay constant; each free row
  * f in [0, n_free) starts at zero and takes `steps` gradient steps on
- * sum_{entries of f} (r - F_fixed[id] . x_f)^2 + lambda ||x_f||^2. */
+ * sum_{entries of f} (r - F_fixed[id] . x_f)^2 + lambda ||x_f||^2.
+ * clip 0 or 1 as for or_fit; clip 2 (per entry) returns 1 untouched. */
 int or_extend(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,
               int32_t n_free, int32_t k, const double *F_fixed, double *F_free,
               int32_t steps, double lambda, double lr, int32_t step, int32_t clip, double xi);

@@ -544,3 +544,88 @@ def test_minibatch_nonfinite_reports_whole_epochs(oracle_lib):
                                                  100, 0.1, 1e6, "sum", n_batches=4, seed=1)
     assert st == 7 and 0 <= done < 100
     assert np.all(np.isfinite(P)) and np.all(np.isfinite(Q))
+
+
+# ------------------------------------------ NEXT-4 per-entry clipping order
+def test_per_entry_clip_without_regulariser_or_threshold_is_plain_descent(oracle_lib):
+    """clip 2 with lambda = 0 and xi = inf adds each cell's 2 e q, whose sum is
+    the negated data gradient exactly: the unclipped fit bit for bit (both
+    step rules, Jacobi and mini-batch epochs)."""
+    p = synth.tiny()
+    st, rm, cm = oracle_lib.template_maps(p.m, p.n, p.I, p.J)
+    a, b, v = oracle_lib.filter_template(p.u, p.i, p.r, rm, cm)
+    for step in ("sum", "degree"):
+        lr = p.lr if step == "degree" else 0.01
+        r0 = oracle_lib.fit(a, b, v, p.P0, p.Q0, 5, 0.0, lr, step, 0, 0.1)
+        r2 = oracle_lib.fit(a, b, v, p.P0, p.Q0, 5, 0.0, lr, step, 2, math.inf)
+        assert r0[0] == r2[0] == 0
+        for x, y in zip(r0[1:4], r2[1:4]):
+            assert np.array_equal(x, y)
+        m0 = oracle_lib.fit_minibatch(a, b, v, p.P0, p.Q0, 3, 0.0, lr, step, 0, 0.1, n_batches=3, seed=4)
+        m2 = oracle_lib.fit_minibatch(a, b, v, p.P0, p.Q0, 3, 0.0, lr, step, 2, math.inf, n_batches=3, seed=4)
+        assert np.array_equal(m0[1], m2[1]) and np.array_equal(m0[2], m2[2])
+
+
+def test_per_entry_clip_with_one_cell_per_line_is_the_summed_clip(oracle_lib):
+    """A line with one cell has one term: clipping it before or after the
+    sum is the same, bit for bit (cells on a permutation, both step rules)."""
+    g = np.random.default_rng(3)
+    n = 40
+    a = np.arange(n, dtype=np.int32)
+    b = g.permutation(n).astype(np.int32)
+    v = g.normal(0, 2, n).astype(np.float32)
+    P0, Q0 = g.normal(0, 1, (n, 4)), g.normal(0, 1, (n, 4))
+    for step in ("sum", "degree"):
+        r1 = oracle_lib.fit(a, b, v, P0, Q0, 6, 0.2, 0.05, step, 1, 0.05)
+        r2 = oracle_lib.fit(a, b, v, P0, Q0, 6, 0.2, 0.05, step, 2, 0.05)
+        for x, y in zip(r1[1:4], r2[1:4]):
+            assert np.array_equal(x, y)
+
+
+def test_per_entry_clip_by_hand(oracle_lib):
+    """One row (p = 1) and two columns (q0 = 2, q1 = -1), values 5 and 0.5,
+    lambda 0.1, xi 1, lr 0.1, sum step.  Residuals 3 and 1.5.  Per entry the
+    row's terms are 11.8 -> 1 and -3.2, so p' = 1 + 0.1 (1 - 3.2) = 0.78; the
+    summed direction would be 8.8 -> 1 and p' = 1.1.  Columns: 5.6 -> 1 and
+    3.2 -> 1, so q0' = 2.1 and q1' = -0.9."""
+    a = np.zeros(2, np.int32)
+    b = np.array([0, 1], np.int32)
+    v = np.array([5.0, 0.5], np.float32)
+    P0, Q0 = np.array([[1.0]]), np.array([[2.0], [-1.0]])
+    st, P, Q, h, _ = oracle_lib.fit(a, b, v, P0, Q0, 1, 0.1, 0.1, "sum", 2, 1.0)
+    assert st == 0
+    assert P[0, 0] == pytest.approx(0.78, rel=1e-14)
+    assert Q[:, 0] == pytest.approx([2.1, -0.9], rel=1e-14)
+    st, P, Q, h, _ = oracle_lib.fit(a, b, v, P0, Q0, 1, 0.1, 0.1, "sum", 1, 1.0)
+    assert P[0, 0] == pytest.approx(1.1, rel=1e-14)
+
+
+def test_per_entry_clip_brute_force_tiny(oracle_lib):
+    """Two Jacobi epochs of the per-entry order against a per-cell Python
+    sweep: every term from the same iterate, clipped, summed per line and
+    divided by the line's cell count."""
+    a, b, v = _every_line_observed(9, 7, 6, 20)
+    g = np.random.default_rng(10)
+    P0, Q0 = g.normal(0, .7, (7, 3)), g.normal(0, .7, (6, 3))
+    lam, lr, xi = 0.3, 0.1, 0.2
+    P, Q = P0.copy(), Q0.copy()
+    dP, dQ = np.bincount(a, minlength=7), np.bincount(b, minlength=6)
+    for _ in range(2):
+        gP, gQ = np.zeros_like(P), np.zeros_like(Q)
+        for x, y, r in zip(a, b, v):
+            err = float(r) - sum(P[x, c] * Q[y, c] for c in range(3))
+            for c in range(3):
+                gP[x, c] += min(2 * err * Q[y, c] - 2 * lam * P[x, c], xi)
+                gQ[y, c] += min(2 * err * P[x, c] - 2 * lam * Q[y, c], xi)
+        P, Q = P + lr * gP / dP[:, None], Q + lr * gQ / dQ[:, None]
+    st, Po, Qo, _, _ = oracle_lib.fit(a, b, v, P0, Q0, 2, lam, lr, "degree", 2, xi)
+    assert st == 0
+    np.testing.assert_allclose(Po, P, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(Qo, Q, rtol=1e-12, atol=1e-14)
+
+
+def test_per_entry_clip_is_not_an_extension_option(oracle_lib):
+    F = np.ones((3, 2))
+    st, X = oracle_lib.extend(np.zeros(1, np.int32), np.zeros(1, np.int32), np.ones(1, np.float32), 1, F, 3,
+                              0.1, 0.1, "degree", 2, 0.1)
+    assert st == 1
