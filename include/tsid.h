@@ -62,6 +62,15 @@ typedef enum { TSID_STEP_SUM = 0, TSID_STEP_DEGREE = 1 } tsid_step;
  *  clip    1: asymmetric clipping of Section 5.3 -- each coordinate of the
  *          descent direction d becomes min(d, clip_xi) (positive components
  *          are capped, negative ones pass; NaN propagates).  clip_xi > 0.
+ *          2: the same clip in the per-entry order (Section 5.3 applied to
+ *          Eqs. 3-4 entry by entry, then the 1/n average of Eq. 9): each
+ *          cell adds min(2 e q - 2 lambda p, clip_xi) per coordinate (the
+ *          regulariser once per cell, the master p in it) and the row moves by
+ *          lr times the sum (divided by its degree with the DEGREE step); a
+ *          row without cells stays.  Template fits only, on the item pass
+ *          (E_INVAL with TSID_PASS_SLAB or forced dense tiles; the automatic
+ *          modes use neither); the extension returns E_INVAL.
+ *          0: no clip.
  *  prec    TSID_FP32: fp32 factors.  TSID_BF16: the products read bf16
  *          (round-to-nearest-even) copies of the factors, accumulate in fp32,
  *          and an fp32 master copy takes the update (the mixed precision of

@@ -245,7 +245,10 @@ def make_adam_opts(steps=1, lam=0.0, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8):
 
 
 def make_opts(epochs=1, lam=0.0, lr=0.1, clip=False, xi=0.1, prec="fp32", step="sum"):
-    return tsid_fit_opts(int(epochs), float(lam), float(lr), float(xi), int(bool(clip)),
+    """clip: False / True (the clip on each row's summed direction) or
+    "per_entry" (each cell's direction clipped before the sum)."""
+    return tsid_fit_opts(int(epochs), float(lam), float(lr), float(xi),
+                         2 if clip == "per_entry" else int(bool(clip)),
                          BF16 if prec == "bf16" else FP32,
                          STEP_DEGREE if step == "degree" else STEP_SUM)
 

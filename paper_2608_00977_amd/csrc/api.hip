@@ -34,8 +34,13 @@ bool valid_rank(int32_t k) { return k == 8 || k == 16 || k == 32 || k == 64 || k
 #ifndef TSID_TARGET_ITEMS
 #define TSID_TARGET_ITEMS 131072
 #endif
-int32_t choose_E(int64_t nnz) {
-    int64_t e = (nnz + TSID_TARGET_ITEMS - 1) / TSID_TARGET_ITEMS;
+// Work items of a mini-batch step: each batch holds a fraction of the cells
+// but every owner row still costs its row load and update.
+#ifndef TSID_MB_TARGET_ITEMS
+#define TSID_MB_TARGET_ITEMS 131072
+#endif
+int32_t choose_E(int64_t nnz, int64_t target = TSID_TARGET_ITEMS) {
+    int64_t e = (nnz + target - 1) / target;
     e = (e + 15) / 16 * 16;
     if (e < 64) e = 64;
     if (e > 4096) e = 4096;
@@ -429,7 +434,7 @@ void check_opts(const tsid_fit_opts *o) {
     if (o->epochs < 0) fail(TSID_E_INVAL, "epochs < 0");
     if (!(o->lambda >= 0.f) || !std::isfinite(o->lambda)) fail(TSID_E_INVAL, "lambda must be finite and >= 0");
     if (!(o->lr > 0.f) || !std::isfinite(o->lr)) fail(TSID_E_INVAL, "lr must be finite and > 0");
-    if (o->clip != 0 && o->clip != 1) fail(TSID_E_INVAL, "clip must be 0 or 1");
+    if (o->clip < 0 || o->clip > 2) fail(TSID_E_INVAL, "clip must be 0, 1 or 2");
     if (o->clip && !(o->clip_xi > 0.f)) fail(TSID_E_INVAL, "clip_xi must be > 0");
     if (o->prec != TSID_FP32 && o->prec != TSID_BF16) fail(TSID_E_INVAL, "bad precision");
     if (o->step != TSID_STEP_SUM && o->step != TSID_STEP_DEGREE) fail(TSID_E_INVAL, "bad step");
@@ -1056,7 +1061,7 @@ void ensure_minibatch(tsid_ctx *c, int prec) {
     }
     if (mb.plan[0][prec].empty()) {
         // items sized for a batch's share of the cells
-        const int64_t E = choose_E(std::max<int64_t>(1, t.nnz / B));
+        const int64_t E = choose_E(std::max<int64_t>(1, t.nnz / B), TSID_MB_TARGET_ITEMS);
         const int ng = items_per_wave(t.k, prec);
         int64_t most = 0;
         try {
@@ -1083,14 +1088,18 @@ void ensure_minibatch(tsid_ctx *c, int prec) {
 
 // dense: whether a fit is about to run (the loss evaluation uses no tiles);
 // extra_items: the largest work plan of a mini-batch fit (0 otherwise)
-void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs, bool dense, int64_t extra_items = 0) {
+// item_only: the fit runs the item pass on both sides (no slab pass)
+void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs, bool dense, int64_t extra_items = 0,
+                        bool item_only = false) {
     Template &t = *c->tpl;
     FitBufs &f = c->fb;
     Arena &A = c->arena;
     const int64_t lp = (int64_t)t.m_t * t.k, lq = (int64_t)t.n_t * t.k;
     ensure_plan(c, 0, prec);
     ensure_plan(c, 1, prec);
-    if (c->mb_batches == 0) {  // mini-batch epochs run the item pass only
+    if (item_only) {
+        t.slab[0].use = t.slab[1].use = false;
+    } else {
         ensure_slab(c, 0, prec);
         ensure_slab(c, 1, prec);
     }
@@ -1218,7 +1227,7 @@ void fit_minibatch(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, doub
     const int K = t.k, prec = o->prec, T = o->epochs;
     ensure_minibatch(c, prec);
     MiniPlan &mb = t.mb;
-    ensure_fit_buffers(c, prec, T, false, mb.max_items[prec]);
+    ensure_fit_buffers(c, prec, T, false, mb.max_items[prec], true);
     c->epochs_done = 0;
     c->dense_used = tsid_dense_info{};
     c->used_kernel[0] = c->used_kernel[1] = TSID_PASS_ITEM;
@@ -1334,8 +1343,12 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     check_opts(o);
     Template &t = *c->tpl;
     if ((t.m_t && !P) || (t.n_t && !Q)) fail(TSID_E_INVAL, "NULL factor pointer");
+    if (o->clip == 2) {  // per-entry terms: the item pass only
+        if (c->pass_kernel == TSID_PASS_SLAB) fail(TSID_E_INVAL, "per-entry clipping runs the item pass");
+        if (c->dense_fill > 0.f) fail(TSID_E_INVAL, "per-entry clipping does not use dense tiles");
+    }
     if (c->mb_batches > 0) return fit_minibatch(c, P, Q, o, loss_hist);
-    ensure_fit_buffers(c, o->prec, o->epochs, true);
+    ensure_fit_buffers(c, o->prec, o->epochs, o->clip != 2, 0, o->clip == 2);
     c->epochs_done = 0;
     FitBufs &f = c->fb;
     hipStream_t cs = c->comp;
@@ -1634,6 +1647,7 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
         if (!ridge_supported(c->tpl->k)) fail(TSID_E_INVAL, "the exact extension solve supports k in {8, 16, 32, 64}");
     } else {
         check_opts(o);
+        if (o->clip == 2) fail(TSID_E_INVAL, "per-entry clipping (clip 2) is a template-fit option");
     }
     if (side != 0 && side != 1) fail(TSID_E_INVAL, "side must be 0 or 1");
     if (nnz < 0 || nnz > kMaxEntries) fail(TSID_E_INVAL, "nnz out of range");

@@ -172,9 +172,14 @@ __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg,
     float nrm = 0.f;
 #pragma unroll
     for (int v = 0; v < V; ++v) {
-        const float g = 2.0f * A.lam * x[v] - 2.0f * acc[v];
-        float d = -s * g;
-        if (A.clip && d > A.xi) d = A.xi;
+        float d;
+        if (A.clip == 2) {
+            d = s * acc[v];  // the cells' clipped directions (per-entry order)
+        } else {
+            const float g = 2.0f * A.lam * x[v] - 2.0f * acc[v];
+            d = -s * g;
+            if (A.clip && d > A.xi) d = A.xi;
+        }
         xn[v] = keep ? x[v] : x[v] + A.lr * d;
         bad |= !__builtin_isfinite(xn[v]);
         nrm += x[v] * x[v];
@@ -260,7 +265,10 @@ constexpr int block_spl() {  // stream cells per lane per block
 // stream loads must come after every gather the arithmetic waits for, and
 // issuing them once per block exposes their latency once per SB cells.
 // NEXT = false skips those loads (the caller's cells all fit one block).
-template <int K, int V, bool BF16, bool LOSS_ONLY, bool BUF, bool NEXT = true, int SPL = block_spl<K / V>()>
+// PE: the per-entry order of the clipped update -- each cell adds its own
+// descent direction 2 e y - 2 lambda x, clipped at xi, instead of e y.
+template <int K, int V, bool BF16, bool LOSS_ONLY, bool BUF, bool NEXT = true, int SPL = block_spl<K / V>(),
+          bool PE = false>
 __device__ __forceinline__ void process_block(const PassArgs &A, const YTable &Yt, int64_t j0,
                                               int64_t end, int64_t last, int lg, const int2 (&cur)[SPL],
                                               int2 (&nxt)[SPL], const float (&x)[V],
@@ -309,8 +317,19 @@ __device__ __forceinline__ void process_block(const PassArgs &A, const YTable &Y
                     d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, xp[p]),
                                                          __builtin_bit_cast(bf16x2, yw[t][p]), d, false);
                 d = group_sum<G>(d);
-                const float e = (c0 + t < left) ? r - d : 0.f;
-                if constexpr (!LOSS_ONLY) {
+                const bool in = c0 + t < left;
+                const float e = in ? r - d : 0.f;
+                if constexpr (!LOSS_ONLY && PE) {
+#pragma unroll
+                    for (int p = 0; p < V / 2; ++p) {
+                        float d0 = 2.0f * e * __uint_as_float(yw[t][p] << 16) - 2.0f * A.lam * x[2 * p];
+                        float d1 = 2.0f * e * __uint_as_float(yw[t][p] & 0xffff0000u) - 2.0f * A.lam * x[2 * p + 1];
+                        if (d0 > A.xi) d0 = A.xi;
+                        if (d1 > A.xi) d1 = A.xi;
+                        acc[2 * p] += in ? d0 : 0.f;
+                        acc[2 * p + 1] += in ? d1 : 0.f;
+                    }
+                } else if constexpr (!LOSS_ONLY) {
 #pragma unroll
                     for (int p = 0; p < V / 2; ++p) {
                         acc[2 * p] += e * __uint_as_float(yw[t][p] << 16);
@@ -349,8 +368,16 @@ __device__ __forceinline__ void process_block(const PassArgs &A, const YTable &Y
 #pragma unroll
                 for (int v = 0; v < V; ++v) d += x[v] * y[t][v];
                 d = group_sum<G>(d);
-                const float e = (c0 + t < left) ? r - d : 0.f;
-                if constexpr (!LOSS_ONLY) {
+                const bool in = c0 + t < left;
+                const float e = in ? r - d : 0.f;
+                if constexpr (!LOSS_ONLY && PE) {
+#pragma unroll
+                    for (int v = 0; v < V; ++v) {
+                        float dv = 2.0f * e * y[t][v] - 2.0f * A.lam * x[v];
+                        if (dv > A.xi) dv = A.xi;
+                        acc[v] += in ? dv : 0.f;
+                    }
+                } else if constexpr (!LOSS_ONLY) {
 #pragma unroll
                     for (int v = 0; v < V; ++v) acc[v] += e * y[t][v];
                 }
@@ -370,7 +397,7 @@ __device__ __forceinline__ void process_block(const PassArgs &A, const YTable &Y
 #define TSID_OCCUPANCY
 #endif
 
-template <int K, int V, bool BF16, bool LOSS_ONLY, bool BUF>
+template <int K, int V, bool BF16, bool LOSS_ONLY, bool BUF, bool PE = false>
 __global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass(const PassArgs A) {
     constexpr int G = K / V;
     constexpr int NG = 64 / G;
@@ -428,9 +455,9 @@ __global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass(const Pas
     const YTable Yt = make_ytable<BUF>(A, K * (BF16 ? 2 : 4));
 #if TSID_PINGPONG
     for (int64_t j0 = beg; j0 < end; j0 += 2 * SB) {
-        process_block<K, V, BF16, LOSS_ONLY, BUF>(A, Yt, j0, end, last, lg, bufA, bufB, x, xp, acc, e2);
+        process_block<K, V, BF16, LOSS_ONLY, BUF, true, block_spl<K / V>(), PE>(A, Yt, j0, end, last, lg, bufA, bufB, x, xp, acc, e2);
         if (j0 + SB >= end) break;
-        process_block<K, V, BF16, LOSS_ONLY, BUF>(A, Yt, j0 + SB, end, last, lg, bufB, bufA, x, xp, acc,
+        process_block<K, V, BF16, LOSS_ONLY, BUF, true, block_spl<K / V>(), PE>(A, Yt, j0 + SB, end, last, lg, bufB, bufA, x, xp, acc,
                                                   e2);
     }
 #else
@@ -438,7 +465,7 @@ __global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass(const Pas
     // bufB and are copied over only after the block's arithmetic, where the
     // next block needs them anyway.
     for (int64_t j0 = beg; j0 < end; j0 += SB) {
-        process_block<K, V, BF16, LOSS_ONLY, BUF>(A, Yt, j0, end, last, lg, bufA, bufB, x, xp, acc, e2);
+        process_block<K, V, BF16, LOSS_ONLY, BUF, true, block_spl<K / V>(), PE>(A, Yt, j0, end, last, lg, bufA, bufB, x, xp, acc, e2);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int c = 0; c < SPL; ++c) bufA[c] = bufB[c];
@@ -687,6 +714,9 @@ void item_pass_kv(bool loss_only, const PassArgs &a, hipStream_t s, hipEvent_t e
     if (loss_only) {
         if (buf) go(k_item_pass<K, V, BF16, true, true>);
         else go(k_item_pass<K, V, BF16, true, false>);
+    } else if (a.clip == 2) {
+        if (buf) go(k_item_pass<K, V, BF16, false, true, true>);
+        else go(k_item_pass<K, V, BF16, false, false, true>);
     } else {
         if (buf) go(k_item_pass<K, V, BF16, false, true>);
         else go(k_item_pass<K, V, BF16, false, false>);
