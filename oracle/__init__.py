@@ -58,6 +58,10 @@ def lib() -> C.CDLL:
             "or_extend_adam": (C.c_int, [i64, P, P, P, i32, i32, P, i32, P, i32, f64, f64, f64, f64,
                                          f64, P, P]),
             "or_chunk_plan": (i32, [P, i64, i32, i64, P, i32]),
+            "or_loss_mv": (f64, [i64, P, P, P, i32, i32, i32, P, P, f64, i64, P, P, P, f64]),
+            "or_fit_mv": (C.c_int, [i64, P, P, P, i32, i32, i32, P, P, i32, f64, f64, i32, i32, f64, i32,
+                                    i64, P, P, P, f64, P, P]),
+            "or_similarity": (None, [i32, i32, P, P]),
             "or_bf16_bits": (C.c_uint16, [C.c_float]),
         }
         for name, (res, args) in sig.items():
@@ -132,6 +136,38 @@ def fit(a, b, v, P0, Q0, epochs, lam, lr, step="sum", clip=False, xi=0.1, bf16=F
                       _p(Q), epochs, lam, lr, STEP[step], int(clip), xi, int(bf16), _p(hist),
                       _p(done))
     return st, P, Q, hist, int(done[0])
+
+
+def loss_mv(a, b, v, m_t, n_t, P, Q, lam, s_row, s_col, s_val, beta) -> float:
+    a, b, v = _c(a, np.int32), _c(b, np.int32), _c(v, np.float32)
+    P, Q = _c(P, np.float64), _c(Q, np.float64)
+    s_row, s_col, s_val = _c(s_row, np.int32), _c(s_col, np.int32), _c(s_val, np.float32)
+    return lib().or_loss_mv(a.size, _p(a), _p(b), _p(v), m_t, n_t, P.shape[1], _p(P), _p(Q), lam, s_val.size,
+                            _p(s_row), _p(s_col), _p(s_val), beta)
+
+
+def fit_mv(a, b, v, P0, Q0, epochs, lam, lr, s_row, s_col, s_val, beta, step="sum", clip=False, xi=0.1,
+           bf16=False):
+    """The fit with the multi-view similarity term; returns as fit()."""
+    a, b, v = _c(a, np.int32), _c(b, np.int32), _c(v, np.float32)
+    s_row, s_col, s_val = _c(s_row, np.int32), _c(s_col, np.int32), _c(s_val, np.float32)
+    P = np.array(P0, np.float64, order="C", copy=True)
+    Q = np.array(Q0, np.float64, order="C", copy=True)
+    hist = np.full(epochs + 1, np.nan)
+    done = np.zeros(1, np.int32)
+    st = lib().or_fit_mv(a.size, _p(a), _p(b), _p(v), P.shape[0], Q.shape[0], P.shape[1], _p(P), _p(Q), epochs,
+                         lam, lr, STEP[step], int(clip), xi, int(bf16), s_val.size, _p(s_row), _p(s_col),
+                         _p(s_val), beta, _p(hist), _p(done))
+    return st, P, Q, hist, int(done[0])
+
+
+def similarity(attr) -> np.ndarray:
+    """Dense item similarity from categorical attributes (n x n_attr int)."""
+    attr = _c(attr, np.int32)
+    n, na = attr.shape
+    S = np.zeros((n, n), np.float64)
+    lib().or_similarity(n, na, _p(attr), _p(S))
+    return S
 
 
 def splitmix64(x: int) -> int:

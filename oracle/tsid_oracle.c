@@ -248,10 +248,95 @@ static void round_copy(const double *x, double *y, int64_t len) {
     for (int64_t j = 0; j < len; ++j) y[j] = bf16_round(x[j]);
 }
 
+/* ------------------------------------------------ multi-view similarity */
+
+/* The similarity term of the multi-view item update (Section 5.1, with the
+ * similarity matrix S of Eq. 1 over the template's columns, symmetric, as COO
+ * entries (row[e], col[e], val[e])):
+ *   (beta / 2) sum_(i, i') S_ii' ||q_i - q_i'||^2,
+ * whose gradient with respect to q_i is 2 beta sum_i' S_ii' (q_i - q_i').
+ * Returns the term; adds the gradient to gQ when it is given. */
+typedef struct {
+    int64_t nnz;
+    const int32_t *row, *col;
+    const float *val;
+    double beta;
+} sim_t;
+
+static double sim_terms(const sim_t *S, int32_t k, const double *Q, double *gQ) {
+    if (!S) return 0.0;
+    double tot = 0.0;
+    for (int64_t e = 0; e < S->nnz; ++e) {
+        const double *qi = Q + (int64_t)S->row[e] * k, *qj = Q + (int64_t)S->col[e] * k;
+        const double w = (double)S->val[e];
+        double d2 = 0.0;
+        for (int32_t c = 0; c < k; ++c) {
+            const double d = qi[c] - qj[c];
+            d2 += d * d;
+            if (gQ) gQ[(int64_t)S->row[e] * k + c] += 2.0 * S->beta * w * d;
+        }
+        tot += w * d2;
+    }
+    return 0.5 * S->beta * tot;
+}
+
+void or_similarity(int32_t n, int32_t n_attr, const int32_t *attr, double *S) {
+    for (int32_t i = 0; i < n; ++i)
+        for (int32_t j = 0; j < n; ++j) {
+            int32_t same = 0;
+            for (int32_t t = 0; t < n_attr; ++t)
+                same += attr[(int64_t)i * n_attr + t] == attr[(int64_t)j * n_attr + t];
+            S[(int64_t)i * n + j] = (double)same / (double)n_attr;
+        }
+}
+
+static int sim_valid(const sim_t *S, int32_t n_t) {
+    if (!S) return 1;
+    for (int64_t e = 0; e < S->nnz; ++e)
+        if (S->row[e] < 0 || S->row[e] >= n_t || S->col[e] < 0 || S->col[e] >= n_t) return 0;
+    return 1;
+}
+
+double or_loss_mv(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+                  int32_t m_t, int32_t n_t, int32_t k, const double *P, const double *Q,
+                  double lambda, int64_t s_nnz, const int32_t *s_row, const int32_t *s_col,
+                  const float *s_val, double beta) {
+    const sim_t S = {s_nnz, s_row, s_col, s_val, beta};
+    return or_loss(nnz, a, b, v, m_t, n_t, k, P, Q, lambda) + sim_terms(&S, k, Q, NULL);
+}
+
+static int fit_impl(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+                    int32_t m_t, int32_t n_t, int32_t k, double *P, double *Q,
+                    int32_t epochs, double lambda, double lr, int32_t step,
+                    int32_t clip, double xi, int32_t bf16, const sim_t *S,
+                    double *loss_hist, int32_t *epochs_done);
+
 int or_fit(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
            int32_t m_t, int32_t n_t, int32_t k, double *P, double *Q,
            int32_t epochs, double lambda, double lr, int32_t step,
            int32_t clip, double xi, int32_t bf16, double *loss_hist, int32_t *epochs_done) {
+    return fit_impl(nnz, a, b, v, m_t, n_t, k, P, Q, epochs, lambda, lr, step, clip, xi, bf16, NULL,
+                    loss_hist, epochs_done);
+}
+
+int or_fit_mv(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+              int32_t m_t, int32_t n_t, int32_t k, double *P, double *Q,
+              int32_t epochs, double lambda, double lr, int32_t step,
+              int32_t clip, double xi, int32_t bf16, int64_t s_nnz, const int32_t *s_row,
+              const int32_t *s_col, const float *s_val, double beta, double *loss_hist,
+              int32_t *epochs_done) {
+    const sim_t S = {s_nnz, s_row, s_col, s_val, beta};
+    if (clip == 2) return 1; /* the per-entry order has no per-entry similarity term */
+    if (!sim_valid(&S, n_t)) return 2;
+    return fit_impl(nnz, a, b, v, m_t, n_t, k, P, Q, epochs, lambda, lr, step, clip, xi, bf16, &S,
+                    loss_hist, epochs_done);
+}
+
+static int fit_impl(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+                    int32_t m_t, int32_t n_t, int32_t k, double *P, double *Q,
+                    int32_t epochs, double lambda, double lr, int32_t step,
+                    int32_t clip, double xi, int32_t bf16, const sim_t *S,
+                    double *loss_hist, int32_t *epochs_done) {
     int64_t lp = (int64_t)m_t * k, lq = (int64_t)n_t * k;
     double *gP = (double *)malloc((size_t)(lp + 1) * sizeof(double));
     double *gQ = (double *)malloc((size_t)(lq + 1) * sizeof(double));
@@ -279,7 +364,8 @@ int or_fit(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
         memset(gQ, 0, (size_t)lq * sizeof(double));
         double sse = clip == 2 ? sse_terms_per_entry(nnz, a, b, v, k, Pr, Qr, P, Q, lambda, xi, gP, gQ)
                                : sse_grad(nnz, a, b, v, k, Pr, Qr, gP, gQ);
-        if (loss_hist) loss_hist[t] = sse + lambda * (sumsq(P, lp) + sumsq(Q, lq));
+        const double sim = sim_terms(S, k, Q, gQ); /* from the fp64 master Q */
+        if (loss_hist) loss_hist[t] = sse + lambda * (sumsq(P, lp) + sumsq(Q, lq)) + sim;
         int finite = 1;
         for (int32_t x = 0; x < m_t; ++x)
             finite &= update_row(P + (int64_t)x * k, gP + (int64_t)x * k, deg_r[x], k, lambda, lr,
@@ -303,7 +389,7 @@ int or_fit(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
             Qr = Qs;
         }
         double sse = sse_grad(nnz, a, b, v, k, Pr, Qr, NULL, NULL);
-        loss_hist[epochs] = sse + lambda * (sumsq(P, lp) + sumsq(Q, lq));
+        loss_hist[epochs] = sse + lambda * (sumsq(P, lp) + sumsq(Q, lq)) + sim_terms(S, k, Q, NULL);
     }
     if (epochs_done) *epochs_done = t;
     free(gP); free(gQ); free(Pn); free(Qn); free(Ps); free(Qs); free(deg_r); free(deg_c);

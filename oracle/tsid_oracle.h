@@ -73,6 +73,30 @@ int or_fit(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
            int32_t epochs, double lambda, double lr, int32_t step,
            int32_t clip, double xi, int32_t bf16, double *loss_hist, int32_t *epochs_done);
 
+/* Multi-view similarity term (the item-factor update of Section 5.1 with the
+ * similarity regulariser of Eq. 1).  S is a symmetric matrix over the
+ * template's columns given as COO entries (s_row, s_col, s_val), both
+ * orientations listed.  The objective gains
+ *   (beta / 2) sum_(i, i') S_ii' ||q_i - q_i'||^2,
+ * whose gradient 2 beta sum_i' S_ii' (q_i - q_i') is the printed update term;
+ * it joins q_i's summed gradient before the step rule and the clip (modes 0
+ * and 1; mode 2 returns 1) and is evaluated at the fp64 master Q.  Ids out
+ * of [0, n_t) return 2.  Otherwise as or_fit. */
+double or_loss_mv(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+                  int32_t m_t, int32_t n_t, int32_t k, const double *P, const double *Q,
+                  double lambda, int64_t s_nnz, const int32_t *s_row, const int32_t *s_col,
+                  const float *s_val, double beta);
+int or_fit_mv(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+              int32_t m_t, int32_t n_t, int32_t k, double *P, double *Q,
+              int32_t epochs, double lambda, double lr, int32_t step,
+              int32_t clip, double xi, int32_t bf16, int64_t s_nnz, const int32_t *s_row,
+              const int32_t *s_col, const float *s_val, double beta, double *loss_hist,
+              int32_t *epochs_done);
+/* The item similarity of Section 2.2 from n_attr categorical attributes per
+ * item (attr: n x n_attr): S[i][j] = (1 / n_attr) * #{t : attr[i][t] ==
+ * attr[j][t]}, dense n x n. */
+void or_similarity(int32_t n, int32_t n_attr, const int32_t *attr, double *S);
+
 /* splitmix64 (the published 64-bit finaliser of the SplitMix generator):
  * z = x + 0x9E3779B97F4A7C15, then two xor-shift-multiply rounds and a final
  * xor-shift.  Cell (a, b) of the template (positions in I and J) belongs to

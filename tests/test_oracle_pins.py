@@ -629,3 +629,88 @@ def test_per_entry_clip_is_not_an_extension_option(oracle_lib):
     st, X = oracle_lib.extend(np.zeros(1, np.int32), np.zeros(1, np.int32), np.ones(1, np.float32), 1, F, 3,
                               0.1, 0.1, "degree", 2, 0.1)
     assert st == 1
+
+
+# ------------------------------------------------ NEXT-4 multi-view term
+def _sym_coo(S):
+    """Off-diagonal nonzeros of a dense symmetric S as COO (both orientations)."""
+    r, c = np.nonzero(S - np.diag(np.diag(S)))
+    return r.astype(np.int32), c.astype(np.int32), S[r, c].astype(np.float32)
+
+
+def test_similarity_from_attributes_brute_force(oracle_lib):
+    """S_ii' = (1/J) sum_j [a_ij == a_i'j] (Section 2.2): a Python double loop,
+    unit diagonal, symmetric."""
+    g = np.random.default_rng(30)
+    A = g.integers(0, 3, (9, 5))
+    S = oracle_lib.similarity(A)
+    want = np.array([[np.mean(A[i] == A[j]) for j in range(9)] for i in range(9)])
+    assert np.array_equal(S, want) and np.all(np.diag(S) == 1.0) and np.array_equal(S, S.T)
+
+
+def test_multiview_beta_zero_is_the_plain_fit(oracle_lib):
+    p = synth.tiny()
+    st, rm, cm = oracle_lib.template_maps(p.m, p.n, p.I, p.J)
+    a, b, v = oracle_lib.filter_template(p.u, p.i, p.r, rm, cm)
+    S = oracle_lib.similarity(np.random.default_rng(31).integers(0, 4, (p.J.size, 3)))
+    r, c, w = _sym_coo(S)
+    r0 = oracle_lib.fit(a, b, v, p.P0, p.Q0, 5, p.lam, p.lr, "degree", True, 0.1)
+    r1 = oracle_lib.fit_mv(a, b, v, p.P0, p.Q0, 5, p.lam, p.lr, r, c, w, 0.0, "degree", True, 0.1)
+    for x, y in zip(r0[:4], r1[:4]):
+        assert np.array_equal(x, y)
+
+
+def test_multiview_gradient_matches_central_differences(oracle_lib):
+    """The objective with the similarity term, (beta/2) sum S_ii' ||q_i - q_i'||^2,
+    has the printed update term 2 beta sum_i' S_ii' (q_i - q_i') as its
+    gradient: one epoch's step against central differences of the loss
+    (quadratic per coordinate, so exact up to rounding)."""
+    p = synth.random_case(9, 7, 30, 9, 7, 3, seed=21, lam=0.3)
+    st, rm, cm = oracle_lib.template_maps(p.m, p.n, p.I, p.J)
+    a, b, v = oracle_lib.filter_template(p.u, p.i, p.r, rm, cm)
+    S = oracle_lib.similarity(np.random.default_rng(32).integers(0, 3, (7, 4)))
+    r, c, w = _sym_coo(S)
+    beta, lr = 0.7, 1e-3
+    P0, Q0 = p.P0.astype(np.float64), p.Q0.astype(np.float64)
+    st, P1, Q1, h, _ = oracle_lib.fit_mv(a, b, v, P0, Q0, 1, p.lam, lr, r, c, w, beta, "sum")
+    assert st == 0
+    h_ = 1e-3
+    for X, G, isP in ((P0, (P0 - P1) / lr, True), (Q0, (Q0 - Q1) / lr, False)):
+        for idx in np.ndindex(*X.shape):
+            Xp, Xm = X.copy(), X.copy()
+            Xp[idx] += h_
+            Xm[idx] -= h_
+            args = ((Xp, Q0), (Xm, Q0)) if isP else ((P0, Xp), (P0, Xm))
+            Lp, Lm = (oracle_lib.loss_mv(a, b, v, 9, 7, PP, QQ, p.lam, r, c, w, beta) for PP, QQ in args)
+            fd = (Lp - Lm) / (2 * h_)
+            assert abs(fd - G[idx]) <= 1e-8 * max(1.0, abs(fd)), (isP, idx, fd, G[idx])
+    direct = oracle_lib.loss(a, b, v, 9, 7, P0, Q0, p.lam) + beta / 2 * sum(
+        S[i, j] * ((Q0[i] - Q0[j]) ** 2).sum() for i in range(7) for j in range(7))
+    assert h[0] == pytest.approx(direct, rel=1e-13)
+
+
+def test_multiview_without_cells_is_laplacian_smoothing(oracle_lib):
+    """No observed cells and lambda = 0: one epoch is Q <- Q - 2 lr beta (D - S) Q
+    with D the diagonal of S's row sums (the graph Laplacian), P unchanged."""
+    g = np.random.default_rng(33)
+    S = oracle_lib.similarity(g.integers(0, 3, (8, 4)))
+    r, c, w = _sym_coo(S)
+    Sf = np.zeros((8, 8))
+    Sf[r, c] = w.astype(np.float64)
+    Lap = np.diag(Sf.sum(1)) - Sf
+    P0, Q0 = g.normal(0, 1, (5, 3)), g.normal(0, 1, (8, 3))
+    beta, lr = 0.4, 0.05
+    none = np.zeros(0, np.int32)
+    st, P1, Q1, _, _ = oracle_lib.fit_mv(none, none, np.zeros(0, np.float32), P0, Q0, 1, 0.0, lr, r, c, w, beta)
+    assert st == 0 and np.array_equal(P1, P0)
+    np.testing.assert_allclose(Q1, Q0 - 2 * lr * beta * Lap @ Q0, rtol=1e-13, atol=1e-15)
+
+
+def test_multiview_rejections(oracle_lib):
+    none = np.zeros(0, np.int32)
+    P0, Q0 = np.ones((2, 2)), np.ones((3, 2))
+    bad = (np.array([0], np.int32), np.array([3], np.int32), np.ones(1, np.float32))
+    assert oracle_lib.fit_mv(none, none, np.zeros(0, np.float32), P0, Q0, 1, 0.1, 0.1, *bad, 0.5)[0] == 2
+    ok = (np.array([0, 1], np.int32), np.array([1, 0], np.int32), np.ones(2, np.float32))
+    assert oracle_lib.fit_mv(none, none, np.zeros(0, np.float32), P0, Q0, 1, 0.1, 0.1, *ok, 0.5, "sum", 2,
+                             0.1)[0] == 1
