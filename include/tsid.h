@@ -309,6 +309,30 @@ typedef struct {
 } tsid_dense_info;
 tsid_status tsid_fit_dense_info(const tsid_ctx *ctx, tsid_dense_info *out);
 
+/* Multi-view similarity term for tsid_fit_template (Section 5.1: the
+ * item-factor update with the similarity regulariser of Eq. 1, the item
+ * similarity S of Section 2.2 given here as a sparse matrix).  S is over the
+ * template's columns (ids are positions in J), symmetric, with both
+ * orientations of every off-diagonal entry listed once (HOST COO row, col,
+ * val; nnz entries; values finite and >= 0; diagonal entries allowed, they
+ * add nothing).  The objective of Eq. 2 gains
+ *   (beta / 2) sum_(i, i') S_ii' ||q_i - q_i'||^2,
+ * whose gradient with respect to q_i, 2 beta sum_i' S_ii' (q_i - q_i'), is the
+ * update's similarity term: every epoch it is evaluated at Q_t (the fp32
+ * master) and joins q_i's summed gradient before the step rule and the clip
+ * (opts->clip 0 or 1); the loss history includes the term.  The fits then
+ * run the item pass on both sides (dense tiles allowed): a fit with
+ * TSID_PASS_SLAB, clip 2 or mini-batch epochs returns E_INVAL.  tsid_loss
+ * stays Eq. 2.  S is copied to the device (CSR, 12 bytes per entry, plus 4k
+ * bytes per column for the gradient sums) and kept with the template until
+ * the next call or template; nnz = 0 or beta = 0 turns the term off.
+ * Errors: E_STATE (no template), E_INVAL (NULL arrays with nnz > 0, nnz < 0,
+ * beta negative or not finite, a value negative or not finite, S not
+ * symmetric), E_RANGE (an id outside [0, n_t)), E_DUP (a repeated entry),
+ * E_NOMEM, E_DEVICE. */
+tsid_status tsid_set_similarity(tsid_ctx *ctx, const int32_t *row, const int32_t *col, const float *val,
+                                int64_t nnz, float beta);
+
 /* Mini-batch epochs for tsid_fit_template (Section 5.1: the stochastic
  * method updates the factors within an epoch, Eq. 9 averaging each update
  * over the entries it uses; here the entries are grouped into mini-batches).

@@ -88,6 +88,7 @@ def lib() -> C.CDLL:
         "tsid_get_timing": (C.c_int, [P, C.POINTER(tsid_timing)]),
         "tsid_set_dense_tiles": (C.c_int, [P, C.c_float]),
         "tsid_set_minibatch": (C.c_int, [P, i32, C.c_uint64]),
+        "tsid_set_similarity": (C.c_int, [P, P, P, P, i64, C.c_float]),
         "tsid_fit_dense_info": (C.c_int, [P, C.POINTER(tsid_dense_info)]),
         "tsid_loss": (C.c_int, [P, P, P, C.c_float, P]),
         "tsid_extend_chunk": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P,
@@ -184,6 +185,10 @@ def tsid_set_dense_tiles(ctx, fill: float) -> int:
 
 def tsid_set_minibatch(ctx, n_batches: int, seed: int) -> int:
     return lib().tsid_set_minibatch(ctx, int(n_batches), C.c_uint64(int(seed) & 0xFFFFFFFFFFFFFFFF))
+
+
+def tsid_set_similarity(ctx, row, col, val, nnz: int, beta: float) -> int:
+    return lib().tsid_set_similarity(ctx, row, col, val, int(nnz), float(beta))
 
 
 def tsid_fit_dense_info(ctx) -> dict:
@@ -335,6 +340,16 @@ class Tsid:
         epochs (tsid_set_minibatch)."""
         self._check(tsid_set_minibatch(self.ctx, n_batches, seed), "tsid_set_minibatch")
         self._batches = int(n_batches)
+
+    def set_similarity(self, row, col, val, beta: float):
+        """Multi-view similarity term: S over the template's columns as COO
+        (both orientations listed) and its weight (tsid_set_similarity)."""
+        row = np.ascontiguousarray(row, np.int32)
+        col = np.ascontiguousarray(col, np.int32)
+        val = np.ascontiguousarray(val, np.float32)
+        assert row.size == col.size == val.size
+        self._check(tsid_set_similarity(self.ctx, _ptr(row), _ptr(col), _ptr(val), val.size, beta),
+                    "tsid_set_similarity")
 
     def dense_info(self) -> dict:
         """cells, tiles and stripes (P pass, Q pass) of the last fit's dense

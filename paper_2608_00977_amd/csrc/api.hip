@@ -146,6 +146,20 @@ struct MiniPlan {
     int64_t max_items[2] = {0, 0};    // [precision]: largest plan
 };
 
+// Multi-view similarity term (similarity.hip): S over the template's
+// columns as CSR, its weight, the per-column gradient sums and a ring of
+// per-column loss terms (one slot per epoch of the loss ring).
+struct SimPlan {
+    bool on = false;
+    float beta = 0.f;
+    int64_t nnz = 0;
+    int64_t *ptr = nullptr;
+    int32_t *col = nullptr;
+    float *val = nullptr;
+    float *gs = nullptr;  // n_t x k
+    float *se = nullptr;  // ring slots x n_t
+};
+
 struct Template {
     int64_t m = 0, n = 0, nnz = 0;
     int32_t m_t = 0, n_t = 0, k = 0;
@@ -159,6 +173,7 @@ struct Template {
     DensePlan dense;               // bf16 only
     bool dense_use = false;        // the current fit runs the dense tiles
     MiniPlan mb;
+    SimPlan sim;
 };
 
 // Epochs whose loss terms are kept before one batched reduction.
@@ -355,6 +370,15 @@ void free_minibatch(tsid_ctx *c, MiniPlan &mb) {
     mb = MiniPlan{};
 }
 
+void free_sim(tsid_ctx *c, SimPlan &sp) {
+    c->arena.release(sp.ptr);
+    c->arena.release(sp.col);
+    c->arena.release(sp.val);
+    c->arena.release(sp.gs);
+    c->arena.release(sp.se);
+    sp = SimPlan{};
+}
+
 void free_template(tsid_ctx *c, Template *&t) {
     if (!t) return;
     Arena &A = c->arena;
@@ -377,6 +401,7 @@ void free_template(tsid_ctx *c, Template *&t) {
     }
     free_dense(c, t->dense);
     free_minibatch(c, t->mb);
+    free_sim(c, t->sim);
     delete t;
     t = nullptr;
 }
@@ -1210,6 +1235,67 @@ SlabArgs slab_args(const Template &t, int side, const tsid_fit_opts &o, int32_t 
     return a;
 }
 
+// S of the multi-view term: validated on the host (ids inside the template's
+// columns, values finite and >= 0, no repeated entry, symmetric with equal
+// values both ways), then stored as CSR in input order within each row.
+void set_similarity(tsid_ctx *c, const int32_t *row, const int32_t *col, const float *val, int64_t nnz,
+                    float beta) {
+    if (!c->tpl) fail(TSID_E_STATE, "no template: call tsid_build_template first");
+    Template &t = *c->tpl;
+    if (nnz < 0) fail(TSID_E_INVAL, "nnz < 0");
+    if (nnz > 0 && (!row || !col || !val)) fail(TSID_E_INVAL, "NULL similarity arrays");
+    if (!(beta >= 0.f) || !std::isfinite(beta)) fail(TSID_E_INVAL, "beta must be finite and >= 0");
+    std::vector<std::pair<uint64_t, uint32_t>> fw((size_t)nnz), bw((size_t)nnz);
+    for (int64_t e = 0; e < nnz; ++e) {
+        if (row[e] < 0 || row[e] >= t.n_t || col[e] < 0 || col[e] >= t.n_t)
+            fail(TSID_E_RANGE, "similarity id outside the template's columns");
+        if (!(val[e] >= 0.f) || !std::isfinite(val[e])) fail(TSID_E_INVAL, "similarity values must be finite and >= 0");
+        uint32_t bits;
+        std::memcpy(&bits, &val[e], 4);
+        fw[(size_t)e] = {((uint64_t)(uint32_t)row[e] << 32) | (uint32_t)col[e], bits};
+        bw[(size_t)e] = {((uint64_t)(uint32_t)col[e] << 32) | (uint32_t)row[e], bits};
+    }
+    std::sort(fw.begin(), fw.end());
+    std::sort(bw.begin(), bw.end());
+    for (size_t e = 1; e < fw.size(); ++e)
+        if (fw[e].first == fw[e - 1].first) fail(TSID_E_DUP, "repeated similarity entry");
+    if (fw != bw) fail(TSID_E_INVAL, "the similarity matrix must be symmetric");
+    free_sim(c, t.sim);
+    if (nnz == 0 || beta == 0.f) return;  // the term is off
+    std::vector<int64_t> ptr((size_t)t.n_t + 1, 0);
+    for (int64_t e = 0; e < nnz; ++e) ptr[(size_t)row[e] + 1] += 1;
+    for (int32_t x = 0; x < t.n_t; ++x) ptr[(size_t)x + 1] += ptr[(size_t)x];
+    std::vector<int64_t> fill(ptr.begin(), ptr.end() - 1);
+    std::vector<int32_t> hc((size_t)nnz);
+    std::vector<float> hv((size_t)nnz);
+    for (int64_t e = 0; e < nnz; ++e) {
+        const int64_t at = fill[(size_t)row[e]]++;
+        hc[(size_t)at] = col[e];
+        hv[(size_t)at] = val[e];
+    }
+    SimPlan sp;
+    Arena &A = c->arena;
+    hipStream_t cs = c->comp;
+    try {
+        sp.ptr = A.alloc<int64_t>((int64_t)t.n_t + 1);
+        sp.col = A.alloc<int32_t>(nnz);
+        sp.val = A.alloc<float>(nnz);
+        sp.gs = A.alloc<float>((int64_t)t.n_t * t.k);
+        sp.se = A.alloc<float>((int64_t)t.n_t * kLossRing);
+        TSID_HIP(hipMemcpyAsync(sp.ptr, ptr.data(), ptr.size() * 8, hipMemcpyHostToDevice, cs));
+        TSID_HIP(hipMemcpyAsync(sp.col, hc.data(), (size_t)nnz * 4, hipMemcpyHostToDevice, cs));
+        TSID_HIP(hipMemcpyAsync(sp.val, hv.data(), (size_t)nnz * 4, hipMemcpyHostToDevice, cs));
+        TSID_HIP(hipStreamSynchronize(cs));  // the host vectors go out of scope
+    } catch (...) {
+        free_sim(c, sp);
+        throw;
+    }
+    sp.on = true;
+    sp.beta = beta;
+    sp.nnz = nnz;
+    t.sim = sp;
+}
+
 // Mini-batch epochs: epoch ep takes one step per batch beta (global step
 // s = ep * B + beta), each an item pass of both sides over the batch's cells
 // from the factors the previous step left (P and Q of one step both move
@@ -1347,8 +1433,14 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
         if (c->pass_kernel == TSID_PASS_SLAB) fail(TSID_E_INVAL, "per-entry clipping runs the item pass");
         if (c->dense_fill > 0.f) fail(TSID_E_INVAL, "per-entry clipping does not use dense tiles");
     }
+    const SimPlan &sim = t.sim;
+    if (sim.on) {  // the similarity term joins the item pass's Q update
+        if (o->clip == 2) fail(TSID_E_INVAL, "the similarity term has no per-entry form (clip 2)");
+        if (c->mb_batches > 0) fail(TSID_E_INVAL, "the similarity term runs with full-gradient epochs only");
+        if (c->pass_kernel == TSID_PASS_SLAB) fail(TSID_E_INVAL, "the similarity term runs on the item pass");
+    }
     if (c->mb_batches > 0) return fit_minibatch(c, P, Q, o, loss_hist);
-    ensure_fit_buffers(c, o->prec, o->epochs, o->clip != 2, 0, o->clip == 2);
+    ensure_fit_buffers(c, o->prec, o->epochs, o->clip != 2, 0, o->clip == 2 || sim.on);
     c->epochs_done = 0;
     FitBufs &f = c->fb;
     hipStream_t cs = c->comp;
@@ -1363,6 +1455,10 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     TSID_HIP(hipMemsetAsync(c->err_dev, 0, ERR_SLOTS * sizeof(int32_t), cs));
     PassArgs ar = pass_args(t, 0, *o, c->err_dev), ac = pass_args(t, 1, *o, c->err_dev);
     ar.skip_after_nonfinite = ac.skip_after_nonfinite = 1;
+    if (sim.on) {
+        ac.gx = sim.gs;
+        ac.gx_scale = 2.0f * sim.beta;
+    }
     SlabArgs sr = slab_args(t, 0, *o, c->err_dev), sc = slab_args(t, 1, *o, c->err_dev);
     sr.skip_after_nonfinite = sc.skip_after_nonfinite = 1;
     const SlabPlan &sp_r = t.slab[0], &sp_c = t.slab[1];
@@ -1384,7 +1480,8 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     int pend = 0;  // first epoch whose loss is not reduced yet
     auto flush = [&](int upto, std::pair<hipEvent_t, hipEvent_t> ev) {
         launch_loss_reduce(f.e2, f.item_cap, ne, f.normP, t.m_t, f.normQ, t.n_t, o->lambda, upto - pend,
-                           f.partial, f.loss + pend, c->err_dev, pend, cs, ev.first, ev.second);
+                           f.partial, f.loss + pend, c->err_dev, pend, cs, ev.first, ev.second,
+                           sim.on ? sim.se : nullptr, t.n_t, 0.5 * (double)sim.beta);
         pend = upto;
     };
     for (int ep = 0; ep < T; ++ep) {
@@ -1430,6 +1527,9 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
         }
         // Q pass (CSC): owner Q_t, gathered P_t (the old P: a simultaneous step)
         float *normq = want_loss ? f.normQ + (int64_t)slot * t.n_t : nullptr;
+        if (sim.on)  // the similarity sums at Q_t, added to the Q gradients
+            launch_sim_terms(K, sim.ptr, sim.col, sim.val, t.n_t, f.Q[cur], sim.gs,
+                             want_loss ? sim.se + (int64_t)slot * t.n_t : nullptr, cs);
         ev = timed(c, ep, TK_QPASS);
         if (sp_c.use) {
             sc.epoch = ep;
@@ -1496,6 +1596,9 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
             launch_item_pass(K, prec, true, ar, cs);
         }
         launch_row_norms(K, f.Q[fin], t.n_t, f.normQ + (int64_t)slot * t.n_t, cs);
+        if (sim.on)
+            launch_sim_terms(K, sim.ptr, sim.col, sim.val, t.n_t, f.Q[fin], sim.gs, sim.se + (int64_t)slot * t.n_t,
+                             cs);
         flush(T + 1, {nullptr, nullptr});
     }
     std::vector<double> hist((size_t)T + 1);
@@ -1920,6 +2023,11 @@ tsid_status tsid_set_dense_tiles(tsid_ctx *c, float fill) {
     if (!c || !(fill <= 1.f)) return TSID_E_INVAL;  // NaN fails the comparison
     c->dense_fill = fill < 0.f ? -1.f : fill;
     return TSID_OK;
+}
+
+tsid_status tsid_set_similarity(tsid_ctx *c, const int32_t *row, const int32_t *col, const float *val,
+                                int64_t nnz, float beta) {
+    return guarded(c, [&]() { set_similarity(c, row, col, val, nnz, beta); });
 }
 
 tsid_status tsid_set_minibatch(tsid_ctx *c, int32_t n_batches, uint64_t seed) {

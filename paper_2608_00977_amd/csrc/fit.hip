@@ -167,6 +167,10 @@ __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg,
     }
     const float s = A.degree ? 1.0f / (float)(deg > 1 ? deg : 1) : 1.0f;
     const bool keep = A.keep_empty && deg == 0;
+    float gxv[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) gxv[v] = 0.f;
+    if (A.gx) load_f32<V>(A.gx + (int64_t)row * (G * V) + lg * V, gxv);
     float xn[V];
     bool bad = false;
     float nrm = 0.f;
@@ -176,7 +180,8 @@ __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg,
         if (A.clip == 2) {
             d = s * acc[v];  // the cells' clipped directions (per-entry order)
         } else {
-            const float g = 2.0f * A.lam * x[v] - 2.0f * acc[v];
+            float g = 2.0f * A.lam * x[v] - 2.0f * acc[v];
+            if (A.gx) g += A.gx_scale * gxv[v];
             d = -s * g;
             if (A.clip && d > A.xi) d = A.xi;
         }
@@ -663,15 +668,21 @@ __global__ void k_to_bf16(const float *X, int64_t n, uint16_t *Xb) {
 
 constexpr int kRedBlocks = 64;
 
+// Four sums per slot: a (stride sa), b, c and d (strides nb, nc, nd); a null
+// array sums to zero.
+constexpr int kRedTerms = 4;
 __global__ __launch_bounds__(256) void k_reduce_partial(const float *a, int64_t sa, int64_t na,
                                                         const float *b, int64_t nb, const float *c,
-                                                        int64_t nc, double *partial) {
+                                                        int64_t nc, const float *dd, int64_t nd,
+                                                        double *partial) {
     __shared__ double lds[256];
     const int slot = blockIdx.y;
     const int which = blockIdx.x / kRedBlocks, blk = blockIdx.x % kRedBlocks;
-    const float *src = which == 0 ? (a ? a + slot * sa : nullptr)
-                                  : (which == 1 ? (b ? b + slot * nb : nullptr) : (c ? c + slot * nc : nullptr));
-    const int64_t n = which == 0 ? na : (which == 1 ? nb : nc);
+    const float *src = which == 0   ? (a ? a + slot * sa : nullptr)
+                       : which == 1 ? (b ? b + slot * nb : nullptr)
+                       : which == 2 ? (c ? c + slot * nc : nullptr)
+                                    : (dd ? dd + slot * nd : nullptr);
+    const int64_t n = which == 0 ? na : (which == 1 ? nb : (which == 2 ? nc : nd));
     const int64_t chunk = (n + kRedBlocks - 1) / kRedBlocks;
     const int64_t lo = blk * chunk, hi = lo + chunk < n ? lo + chunk : n;
     double s = 0.0;
@@ -683,21 +694,23 @@ __global__ __launch_bounds__(256) void k_reduce_partial(const float *a, int64_t 
         if (threadIdx.x < off) lds[threadIdx.x] += lds[threadIdx.x + off];
         __syncthreads();
     }
-    if (threadIdx.x == 0) partial[(int64_t)slot * 3 * kRedBlocks + blockIdx.x] = lds[0];
+    if (threadIdx.x == 0) partial[(int64_t)slot * kRedTerms * kRedBlocks + blockIdx.x] = lds[0];
 }
 
-__global__ void k_reduce_final(const double *partial, int n_slots, double lam, double *out,
+__global__ void k_reduce_final(const double *partial, int n_slots, double lam, double w4, double *out,
                                const int32_t *err, int32_t epoch0) {
     for (int slot = threadIdx.x; slot < n_slots; slot += blockDim.x) {
         if (err && epoch0 >= 0) {
             const int32_t f = err[ERR_NONFINITE];
             if (f != 0 && f - 1 < epoch0 + slot) continue;
         }
-        const double *p = partial + (int64_t)slot * 3 * kRedBlocks;
-        double s[3] = {0.0, 0.0, 0.0};
-        for (int w = 0; w < 3; ++w)
+        const double *p = partial + (int64_t)slot * kRedTerms * kRedBlocks;
+        double s[kRedTerms] = {0.0, 0.0, 0.0, 0.0};
+        const int terms = w4 != 0.0 ? kRedTerms : kRedTerms - 1;  // the fourth only when weighted
+        for (int w = 0; w < terms; ++w)
             for (int b = 0; b < kRedBlocks; ++b) s[w] += p[w * kRedBlocks + b];
         out[slot] = s[0] + lam * (s[1] + s[2]);
+        if (w4 != 0.0) out[slot] += w4 * s[3];
     }
 }
 
@@ -833,18 +846,20 @@ void launch_to_bf16(const float *X, int64_t n, uint16_t *Xb, hipStream_t s) {
     TSID_HIP(hipGetLastError());
 }
 
-size_t reduce_scratch_elems(int n_slots) { return (size_t)3 * kRedBlocks * (n_slots > 0 ? n_slots : 1); }
+size_t reduce_scratch_elems(int n_slots) { return (size_t)kRedTerms * kRedBlocks * (n_slots > 0 ? n_slots : 1); }
 
 void launch_loss_reduce(const float *e2, int64_t e2_stride, int64_t ne, const float *np, int64_t nnp,
                         const float *nq, int64_t nnq, double lam, int n_slots, double *partial,
                         double *out, const int32_t *err, int32_t epoch0, hipStream_t s,
-                        hipEvent_t ev0, hipEvent_t ev1) {
+                        hipEvent_t ev0, hipEvent_t ev1, const float *ns, int64_t nns, double w4) {
     if (n_slots <= 0) return;
-    hipExtLaunchKernelGGL(k_reduce_partial, dim3(3 * kRedBlocks, n_slots), dim3(256), 0, s, ev0,
-                          nullptr, 0, e2, e2_stride, ne, np, nnp, nq, nnq, partial);
+    if (!ns) w4 = 0.0;
+    const int terms = w4 != 0.0 ? kRedTerms : kRedTerms - 1;
+    hipExtLaunchKernelGGL(k_reduce_partial, dim3(terms * kRedBlocks, n_slots), dim3(256), 0, s, ev0,
+                          nullptr, 0, e2, e2_stride, ne, np, nnp, nq, nnq, ns, nns, partial);
     TSID_HIP(hipGetLastError());
     hipExtLaunchKernelGGL(k_reduce_final, dim3(1), dim3(64), 0, s, nullptr, ev1, 0,
-                          (const double *)partial, n_slots, lam, out, err, epoch0);
+                          (const double *)partial, n_slots, lam, w4, out, err, epoch0);
     TSID_HIP(hipGetLastError());
 }
 

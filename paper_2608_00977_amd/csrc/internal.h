@@ -127,6 +127,9 @@ struct PassArgs {
     // 1: a bucket without cells keeps its row as it is (a mini-batch step
     // touches only the rows and columns of the batch's cells)
     int32_t keep_empty;
+    // rows x K extra gradient added (times gx_scale) before the update, or null
+    const float *gx;
+    float gx_scale;
 };
 
 // prec: 0 fp32, 1 bf16.  loss_only: residuals, e2 and norms only.
@@ -147,14 +150,23 @@ void launch_row_norms(int K, const float *X, int32_t rows, float *norm, hipStrea
 void launch_to_bf16(const float *X, int64_t n, uint16_t *Xb, hipStream_t s);
 // Loss of n_slots epochs at once: slot j holds e2 + j * e2_stride (ne per-item
 // squared residual sums), np + j * nnp and nq + j * nnq (row norms), and
-// out[j] = S_e + lam (S_p + S_q), each S a fixed-order fp64 sum.  With err,
+// out[j] = S_e + lam (S_p + S_q), each S a fixed-order fp64 sum, plus
+// w4 S_s over ns + j * nns when ns is given (the similarity term).  With err,
 // a slot whose epoch (epoch0 + j) follows a non-finite update is left
 // unwritten.  partial: reduce_scratch_elems(n_slots) doubles.
 size_t reduce_scratch_elems(int n_slots);
 void launch_loss_reduce(const float *e2, int64_t e2_stride, int64_t ne, const float *np, int64_t nnp,
                         const float *nq, int64_t nnq, double lam, int n_slots, double *partial,
                         double *out, const int32_t *err, int32_t epoch0, hipStream_t s,
-                        hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+                        hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr, const float *ns = nullptr,
+                        int64_t nns = 0, double w4 = 0.0);
+
+// Multi-view similarity term (similarity.hip): for every template column i,
+// gs[i] = sum_e S_e (q_i - q_col[e]) and se[i] = sum_e S_e ||q_i - q_col[e]||^2
+// over the entries e of row i of S (CSR ptr / col / val), from fp32 Q.  se
+// may be null.
+void launch_sim_terms(int K, const int64_t *ptr, const int32_t *col, const float *val, int32_t n, const float *Q,
+                      float *gs, float *se, hipStream_t s);
 
 // ------------------------------------------------------------- slab pass
 // Owner rows per workgroup (one lane each) and LDS bytes of one slab of the
