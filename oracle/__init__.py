@@ -53,6 +53,7 @@ def lib() -> C.CDLL:
             "or_ridge": (C.c_int, [i64, P, P, P, i32, i32, P, f64, P]),
             "or_splitmix64": (C.c_uint64, [C.c_uint64]),
             "or_batch_of": (i32, [i32, i32, C.c_uint64, i32]),
+            "or_batch_of_many": (None, [i64, P, P, C.c_uint64, i32, P]),
             "or_fit_minibatch": (C.c_int, [i64, P, P, P, i32, i32, i32, P, P, i32, f64, f64, i32, i32,
                                            f64, i32, i32, C.c_uint64, P, P]),
             "or_extend_adam": (C.c_int, [i64, P, P, P, i32, i32, P, i32, P, i32, f64, f64, f64, f64,
@@ -176,6 +177,13 @@ def splitmix64(x: int) -> int:
 
 def batch_of(a: int, b: int, seed: int, n_batches: int) -> int:
     return int(lib().or_batch_of(int(a), int(b), C.c_uint64(seed), int(n_batches)))
+
+
+def batch_of_many(a, b, seed: int, n_batches: int) -> np.ndarray:
+    a, b = _c(a, np.int32), _c(b, np.int32)
+    out = np.empty(a.size, np.int32)
+    lib().or_batch_of_many(a.size, _p(a), _p(b), C.c_uint64(seed), int(n_batches), _p(out))
+    return out
 
 
 def fit_minibatch(a, b, v, P0, Q0, epochs, lam, lr, step="sum", clip=False, xi=0.1, bf16=False,

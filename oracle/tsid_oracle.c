@@ -410,6 +410,11 @@ int32_t or_batch_of(int32_t a, int32_t b, uint64_t seed, int32_t n_batches) {
     return (int32_t)(or_splitmix64(seed ^ key) % (uint64_t)n_batches);
 }
 
+void or_batch_of_many(int64_t n, const int32_t *a, const int32_t *b, uint64_t seed, int32_t n_batches,
+                      int32_t *out) {
+    for (int64_t e = 0; e < n; ++e) out[e] = or_batch_of(a[e], b[e], seed, n_batches);
+}
+
 int or_fit_minibatch(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
                      int32_t m_t, int32_t n_t, int32_t k, double *P, double *Q,
                      int32_t epochs, double lambda, double lr, int32_t step,

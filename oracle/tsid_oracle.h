@@ -103,6 +103,9 @@ void or_similarity(int32_t n, int32_t n_attr, const int32_t *attr, double *S);
  * mini-batch splitmix64(seed ^ (a << 32 | b)) mod n_batches. */
 uint64_t or_splitmix64(uint64_t x);
 int32_t or_batch_of(int32_t a, int32_t b, uint64_t seed, int32_t n_batches);
+/* or_batch_of for n cells: out[e] = or_batch_of(a[e], b[e], seed, n_batches). */
+void or_batch_of_many(int64_t n, const int32_t *a, const int32_t *b, uint64_t seed, int32_t n_batches,
+                      int32_t *out);
 
 /* Mini-batch epochs (the in-epoch updates of the stochastic method of
  * Section 5.1, Eq. 9, grouped into mini-batches): each epoch visits the

@@ -1313,7 +1313,10 @@ void fit_minibatch(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, doub
     const int K = t.k, prec = o->prec, T = o->epochs;
     ensure_minibatch(c, prec);
     MiniPlan &mb = t.mb;
-    ensure_fit_buffers(c, prec, T, false, mb.max_items[prec], true);
+    // the steps walk the batch streams; with bf16 factors the epochs' loss
+    // passes may still take the dense head tiles (automatic rule)
+    ensure_fit_buffers(c, prec, T, loss_hist != nullptr, mb.max_items[prec], true);
+    const bool dn = t.dense_use && prec == TSID_BF16;
     c->epochs_done = 0;
     c->dense_used = tsid_dense_info{};
     c->used_kernel[0] = c->used_kernel[1] = TSID_PASS_ITEM;
@@ -1327,13 +1330,21 @@ void fit_minibatch(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, doub
         launch_to_bf16(f.Q[0], lq, f.Qb[0], cs);
     }
     TSID_HIP(hipMemsetAsync(c->err_dev, 0, ERR_SLOTS * sizeof(int32_t), cs));
-    // the loss pass walks the whole stream with the template's own plan
+    // the loss pass walks the whole stream with the template's own plan (with
+    // dense tiles: the tiles' loss-only kernel plus the item pass over the
+    // other cells, as in a Jacobi epoch)
     PassArgs full = pass_args(t, 0, *o, c->err_dev);
     full.skip_after_nonfinite = 1;
     full.Xn = nullptr;
-    const int64_t ne = full.n_items;
+    DenseArgs dfull = dense_args(t, 0, c->err_dev);
+    dfull.skip_after_nonfinite = 1;
+    const int64_t ne_items = full.n_items;
+    const int64_t ne = ne_items + (dn ? dfull.n_segs : 0);
     PassArgs step[2] = {pass_args(t, 0, *o, c->err_dev), pass_args(t, 1, *o, c->err_dev)};
     for (int sd = 0; sd < 2; ++sd) {
+        step[sd].dptr = nullptr;  // the batch streams hold every cell of the batch
+        step[sd].gd = nullptr;
+        step[sd].gd_tile_ptr = nullptr;
         step[sd].stream = mb.stream[sd];
         step[sd].keep_empty = 1;
         step[sd].skip_after_nonfinite = 1;
@@ -1357,6 +1368,13 @@ void fit_minibatch(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, doub
         full.Y = prec ? (const void *)f.Qb[buf] : (const void *)f.Q[buf];
         full.e2 = f.e2 + slot * f.item_cap;
         full.norm = f.normP + (int64_t)slot * t.m_t;
+        if (dn && dfull.n_segs) {
+            dfull.epoch = ep * B;
+            dfull.X = f.Pb[buf];
+            dfull.Y = f.Qb[buf];
+            dfull.e2 = full.e2 + ne_items;
+            launch_dense_pass(K, true, dfull, cs);
+        }
         launch_item_pass(K, prec, true, full, cs);
         launch_row_norms(K, f.Q[buf], t.n_t, f.normQ + (int64_t)slot * t.n_t, cs);
     };

@@ -92,3 +92,49 @@ def test_billion_fullsize_sampled_bf16(T):
     """1,000,000 x 100,000 template, about 4.2e8 training cells, k = 128."""
     note("fullsize billion: generating (a few minutes)")
     _sampled_parity(T, synth.billion_template())
+
+
+def _batch_ptr(own, rows, beta, B):
+    cnt = np.bincount(beta.astype(np.int64) * rows + own, minlength=B * rows)
+    return np.concatenate([[0], np.cumsum(cnt)]).astype(np.int64)
+
+
+@pytest.mark.timeout(400)
+def test_rating_fullsize_minibatch(T):
+    """Mini-batch epochs at full size (bench.py --config rating --minibatch 8,
+    seed 1).  A batch step depends on the factors every earlier step left, so
+    no row of a later batch can be recomputed from its own cells; instead:
+    the batch pointers of both sides bit-exact against the oracle's batch
+    rule over all 38.8 M cells, and with one batch the epochs equal the Jacobi
+    item-pass epochs bit for bit on every line with a cell (same plans, same
+    stream order) while lines without one keep their start rows."""
+    p = synth.rating()
+    rm, cm, a, b, v = oracle_template(p)
+    note(f"fullsize minibatch rating: building template over {p.nnz} cells")
+    T.build_template(p.m, p.n, p.u, p.i, p.r, p.I, p.J, p.k)
+    try:
+        T.set_minibatch(8, 1)
+        st, P8, Q8, h8 = gpu_fit(T, p, epochs=1)
+        assert st == 0 and np.all(np.isfinite(P8)) and np.all(np.isfinite(h8))
+        beta = oracle.batch_of_many(a, b, 1, 8)
+        assert np.array_equal(T.export_index("batch_ptr_r"), _batch_ptr(a, p.I.size, beta, 8))
+        assert np.array_equal(T.export_index("batch_ptr_c"), _batch_ptr(b, p.J.size, beta, 8))
+        del beta
+        T.set_dense_tiles(0)
+        T.set_pass_kernel("item")
+        T.set_minibatch(1, 1)
+        note("fullsize minibatch rating: one batch against the Jacobi epochs")
+        st1, P1, Q1, h1 = gpu_fit(T, p, epochs=2)
+        T.set_minibatch(0)
+        stj, Pj, Qj, hj = gpu_fit(T, p, epochs=2)
+    finally:
+        T.set_minibatch(0)
+        T.set_dense_tiles(-1)
+        T.set_pass_kernel("auto")
+    assert st1 == stj == 0
+    dr = np.bincount(a, minlength=p.I.size) > 0
+    dc = np.bincount(b, minlength=p.J.size) > 0
+    assert np.array_equal(P1[dr], Pj[dr]) and np.array_equal(Q1[dc], Qj[dc])
+    assert np.array_equal(P1[~dr], p.P0[~dr].astype(np.float32))
+    assert np.array_equal(Q1[~dc], p.Q0[~dc].astype(np.float32))
+    np.testing.assert_allclose(h1, hj, rtol=1e-6)

@@ -448,6 +448,7 @@ def test_minibatch_batches_are_balanced(oracle_lib):
     b = g.integers(0, 5000, 40000)
     for B in (2, 3, 8):
         idx = np.array([oracle_lib.batch_of(x, y, 11, B) for x, y in zip(a, b)])
+        assert np.array_equal(oracle_lib.batch_of_many(a, b, 11, B), idx)
         assert idx.min() >= 0 and idx.max() < B
         cnt = np.bincount(idx, minlength=B)
         sd = math.sqrt(a.size * (1 / B) * (1 - 1 / B))
