@@ -64,7 +64,8 @@ def parse():
                          "0 off, in (0, 1] forced with that tile fill")
     ap.add_argument("--minibatch", type=int, default=0,
                     help="mini-batch epochs with this many batches (tsid_set_minibatch; 0: full-gradient "
-                         "epochs); they run the item pass without dense tiles")
+                         "epochs); the batch steps run the item pass, the epochs' loss passes may take the "
+                         "dense tiles of bf16 fits")
     ap.add_argument("--minibatch-seed", type=int, default=1)
     ap.add_argument("--time-every", type=int, default=10,
                     help="attach HIP timing events to the kernels of every n-th timed epoch (each "
@@ -273,10 +274,9 @@ def main():
     T = tsid.Tsid(0)
     T.set_pass_kernel(args.pass_kernel)
     T.set_dense_tiles(args.dense_fill)
-    if args.minibatch:
+    if args.minibatch:  # batch steps on the item pass; the epochs' loss may use the dense tiles
         T.set_minibatch(args.minibatch, args.minibatch_seed)
         T.set_pass_kernel("item")
-        T.set_dense_tiles(0)
     u = torch.from_numpy(p.u).pin_memory()
     i = torch.from_numpy(p.i).pin_memory()
     r = torch.from_numpy(p.r).pin_memory()

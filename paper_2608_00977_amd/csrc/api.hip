@@ -1315,7 +1315,7 @@ void fit_minibatch(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, doub
     MiniPlan &mb = t.mb;
     // the steps walk the batch streams; with bf16 factors the epochs' loss
     // passes may still take the dense head tiles (automatic rule)
-    ensure_fit_buffers(c, prec, T, loss_hist != nullptr, mb.max_items[prec], true);
+    ensure_fit_buffers(c, prec, T, true, mb.max_items[prec], true);
     const bool dn = t.dense_use && prec == TSID_BF16;
     c->epochs_done = 0;
     c->dense_used = tsid_dense_info{};
