@@ -62,6 +62,8 @@ def parse():
     ap.add_argument("--dense-fill", type=float, default=-1.0,
                     help="dense head tiles of bf16 fits (tsid_set_dense_tiles): < 0 automatic, "
                          "0 off, in (0, 1] forced with that tile fill")
+    ap.add_argument("--row-blocks", type=int, default=0,
+                    help="row blocks of the item Q pass (tsid_set_row_blocks): 0 automatic, 1 off, n forced")
     ap.add_argument("--minibatch", type=int, default=0,
                     help="mini-batch epochs with this many batches (tsid_set_minibatch; 0: full-gradient "
                          "epochs); the batch steps run the item pass, the epochs' loss passes may take the "
@@ -274,6 +276,7 @@ def main():
     T = tsid.Tsid(0)
     T.set_pass_kernel(args.pass_kernel)
     T.set_dense_tiles(args.dense_fill)
+    T.set_row_blocks(args.row_blocks)
     if args.minibatch:  # batch steps on the item pass; the epochs' loss may use the dense tiles
         T.set_minibatch(args.minibatch, args.minibatch_seed)
         T.set_pass_kernel("item")
@@ -307,6 +310,7 @@ def main():
     tm = T.timing()
     T.set_timing(False)
     kernels = T.pass_kernels()
+    row_blocks = T.row_blocks()
     ms_per_step = wall * 1e3 / args.steps
     value = nnz / (ms_per_step / 1e3)
     log(f"{args.steps} epochs in {wall:.4f}s: {ms_per_step:.4f} ms/epoch, {value:.4e} cells/s")
@@ -401,6 +405,7 @@ def main():
                    "precision": p.prec, "step": p.step, "lr": p.lr, "lambda": p.lam,
                    "clip": p.clip, "parallelism": "single GPU",
                    "pass_kernels": {"p_pass": kernels[0], "q_pass": kernels[1]},
+                   "q_pass_row_blocks": row_blocks,
                    "dense_tiles": dense,
                    "minibatch": {"batches": args.minibatch, "seed": args.minibatch_seed,
                                  "first_batch_cells": sparse_nnz} if args.minibatch else None},

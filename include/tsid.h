@@ -363,6 +363,27 @@ tsid_status tsid_set_similarity(tsid_ctx *ctx, const int32_t *row, const int32_t
 #define TSID_MAX_BATCHES 4096
 tsid_status tsid_set_minibatch(tsid_ctx *ctx, int32_t n_batches, uint64_t seed);
 
+/* Row-blocked Q passes of the item pass.  The Q pass gathers a row of P for
+ * every cell; when P's table (m_t x k, bf16 or fp32) is larger than the
+ * last-level cache those gathers go to HBM.  With n blocks the Q pass runs as
+ * n launches, launch j walking in every column bucket the run of cells whose
+ * row lies in block j (rows [j * ceil(m_t / n), (j + 1) * ceil(m_t / n))) and
+ * storing the bucket's partial gradient sum (n x n_t x k fp32 of device
+ * memory), then one kernel that adds the n sums of each column in block order
+ * and updates it.  The arithmetic is the same; the fp32 sums of a column are
+ * added in another order.
+ *  n_blocks = 0  (default) automatic: blocks of about 32 MiB of P when the
+ *                table exceeds 96 MiB (Billion-scale: 8 blocks), else one.
+ *  n_blocks = 1  off.   2 <= n_blocks <= TSID_MAX_ROW_BLOCKS: forced.
+ * Applies to full-gradient fits whose Q pass runs the item pass.  Takes effect
+ * at the next tsid_fit_template.  Errors: E_INVAL (ctx NULL, n_blocks out of
+ * range). */
+#define TSID_MAX_ROW_BLOCKS 64
+tsid_status tsid_set_row_blocks(tsid_ctx *ctx, int32_t n_blocks);
+/* Row blocks the last tsid_fit_template's Q pass ran with (1: one pass).
+ * Errors: E_INVAL (ctx or n_blocks NULL). */
+tsid_status tsid_fit_row_blocks(const tsid_ctx *ctx, int32_t *n_blocks);
+
 /* Kernel timing of the template fit (a tracing aid).  With every = n > 0,
  * the kernels of every n-th epoch of tsid_fit_template (epochs 0, n, 2n, ...)
  * are launched with a start and an end HIP event attached to their dispatch

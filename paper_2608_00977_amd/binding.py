@@ -89,6 +89,8 @@ def lib() -> C.CDLL:
         "tsid_set_dense_tiles": (C.c_int, [P, C.c_float]),
         "tsid_set_minibatch": (C.c_int, [P, i32, C.c_uint64]),
         "tsid_set_similarity": (C.c_int, [P, P, P, P, i64, C.c_float]),
+        "tsid_set_row_blocks": (C.c_int, [P, i32]),
+        "tsid_fit_row_blocks": (C.c_int, [P, P]),
         "tsid_fit_dense_info": (C.c_int, [P, C.POINTER(tsid_dense_info)]),
         "tsid_loss": (C.c_int, [P, P, P, C.c_float, P]),
         "tsid_extend_chunk": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P,
@@ -189,6 +191,18 @@ def tsid_set_minibatch(ctx, n_batches: int, seed: int) -> int:
 
 def tsid_set_similarity(ctx, row, col, val, nnz: int, beta: float) -> int:
     return lib().tsid_set_similarity(ctx, row, col, val, int(nnz), float(beta))
+
+
+def tsid_set_row_blocks(ctx, n_blocks: int) -> int:
+    return lib().tsid_set_row_blocks(ctx, int(n_blocks))
+
+
+def tsid_fit_row_blocks(ctx) -> int:
+    out = C.c_int32()
+    st = lib().tsid_fit_row_blocks(ctx, C.byref(out))
+    if st != OK:
+        raise TsidError(st, "tsid_fit_row_blocks")
+    return out.value
 
 
 def tsid_fit_dense_info(ctx) -> dict:
@@ -350,6 +364,15 @@ class Tsid:
         assert row.size == col.size == val.size
         self._check(tsid_set_similarity(self.ctx, _ptr(row), _ptr(col), _ptr(val), val.size, beta),
                     "tsid_set_similarity")
+
+    def set_row_blocks(self, n_blocks: int):
+        """Row blocks of the item Q pass: 0 automatic, 1 off, n forced
+        (tsid_set_row_blocks)."""
+        self._check(tsid_set_row_blocks(self.ctx, n_blocks), "tsid_set_row_blocks")
+
+    def row_blocks(self) -> int:
+        """Row blocks the last fit's Q pass ran with (tsid_fit_row_blocks)."""
+        return tsid_fit_row_blocks(self.ctx)
 
     def dense_info(self) -> dict:
         """cells, tiles and stripes (P pass, Q pass) of the last fit's dense

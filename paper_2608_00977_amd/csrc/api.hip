@@ -160,6 +160,23 @@ struct SimPlan {
     float *se = nullptr;  // ring slots x n_t
 };
 
+// Row-blocked Q passes of the item pass: the gathered P table is split into
+// nb blocks of block_rows rows, each small enough to stay in the last-level
+// cache; block j's pass walks, in every column bucket, the run of cells whose
+// row falls in block j (bounds[j * n_t + x] .. bounds[(j + 1) * n_t + x]) and
+// stores the bucket's partial sum; a combine kernel adds the nb sums in block
+// order and updates the column.  Built over the stream the Q pass walks (the
+// other cells' stream when dense tiles are on).
+struct BlockPlan {
+    int32_t nb = 0;
+    bool dense = false;
+    int64_t block_rows = 0;
+    int64_t *bounds = nullptr;     // (nb + 1) x n_t
+    float *part = nullptr;         // nb x n_t x k
+    std::vector<Plan> plan[2];     // [precision]: nb plans once built
+    int64_t max_items[2] = {0, 0};
+};
+
 struct Template {
     int64_t m = 0, n = 0, nnz = 0;
     int32_t m_t = 0, n_t = 0, k = 0;
@@ -174,6 +191,7 @@ struct Template {
     bool dense_use = false;        // the current fit runs the dense tiles
     MiniPlan mb;
     SimPlan sim;
+    BlockPlan qb;
 };
 
 // Epochs whose loss terms are kept before one batched reduction.
@@ -238,6 +256,8 @@ struct tsid_ctx {
     int32_t used_kernel[2] = {0, 0};  // pass kernel of each side in the last fit
     int32_t mb_batches = 0;           // tsid_set_minibatch: 0 full-gradient epochs
     uint64_t mb_seed = 0;
+    int32_t row_blocks = 0;           // tsid_set_row_blocks: 0 automatic, 1 off, n forced
+    int32_t used_blocks = 1;          // row blocks of the last fit's Q pass
 };
 
 namespace {
@@ -379,6 +399,14 @@ void free_sim(tsid_ctx *c, SimPlan &sp) {
     sp = SimPlan{};
 }
 
+void free_blocks(tsid_ctx *c, BlockPlan &qb) {
+    c->arena.release(qb.bounds);
+    c->arena.release(qb.part);
+    for (auto &v : qb.plan)
+        for (Plan &pl : v) free_plan(c, pl);
+    qb = BlockPlan{};
+}
+
 void free_template(tsid_ctx *c, Template *&t) {
     if (!t) return;
     Arena &A = c->arena;
@@ -402,6 +430,7 @@ void free_template(tsid_ctx *c, Template *&t) {
     free_dense(c, t->dense);
     free_minibatch(c, t->mb);
     free_sim(c, t->sim);
+    free_blocks(c, t->qb);
     delete t;
     t = nullptr;
 }
@@ -1168,6 +1197,69 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs, bool dense, i
     }
 }
 
+// Row blocks of the Q pass for this fit: automatic when the gathered P table
+// exceeds TSID_QBLOCK_MIN_MB (blocks of about TSID_QBLOCK_MB), else one.
+#ifndef TSID_QBLOCK_MB
+#define TSID_QBLOCK_MB 32
+#endif
+#ifndef TSID_QBLOCK_MIN_MB
+#define TSID_QBLOCK_MIN_MB 96
+#endif
+int32_t ensure_qblock(tsid_ctx *c, int prec) {
+    Template &t = *c->tpl;
+    BlockPlan &qb = t.qb;
+    const int64_t table = (int64_t)t.m_t * t.k * (prec == TSID_BF16 ? 2 : 4);
+    int32_t nb = c->row_blocks;
+    if (nb == 0)
+        nb = table > (int64_t)TSID_QBLOCK_MIN_MB << 20 ? (int32_t)((table + ((int64_t)TSID_QBLOCK_MB << 20) - 1) /
+                                                                  ((int64_t)TSID_QBLOCK_MB << 20))
+                                                        : 1;
+    nb = (int32_t)std::min<int64_t>(nb, std::max<int32_t>(1, t.m_t));
+    if (nb <= 1 || t.n_t == 0 || t.slab[1].use) return 1;
+    const bool dn = t.dense_use && prec == TSID_BF16;
+    Arena &A = c->arena;
+    hipStream_t cs = c->comp;
+    if (qb.nb != nb || qb.dense != dn) {
+        free_blocks(c, qb);
+        try {
+            qb.block_rows = (t.m_t + nb - 1) / nb;
+            qb.bounds = A.alloc<int64_t>((int64_t)(nb + 1) * t.n_t);
+            qb.part = A.alloc<float>((int64_t)nb * t.n_t * t.k);
+            launch_block_bounds(dn ? t.dense.sparse[1] : t.stream_c, dn ? t.dense.sparse_ptr[1] : t.col_ptr, t.n_t,
+                                nb, qb.block_rows, qb.bounds, cs);
+            TSID_HIP(hipStreamSynchronize(cs));
+        } catch (...) {
+            free_blocks(c, qb);
+            throw;
+        }
+        qb.nb = nb;
+        qb.dense = dn;
+    }
+    if (qb.plan[prec].empty()) {
+        const int64_t n = (int64_t)(nb + 1) * t.n_t;
+        std::vector<int64_t> hb((size_t)n);
+        TSID_HIP(hipMemcpy(hb.data(), qb.bounds, (size_t)n * 8, hipMemcpyDeviceToHost));
+        const int64_t E = choose_E(std::max<int64_t>(1, (dn ? t.dense.sparse_nnz : t.nnz) / nb));
+        const int ng = items_per_wave(t.k, prec);
+        int64_t most = 0;
+        try {
+            for (int32_t j = 0; j < nb; ++j) {
+                std::vector<int64_t> fake((size_t)t.n_t + 1, 0);  // prefix sums of the runs' lengths
+                for (int32_t x = 0; x < t.n_t; ++x)
+                    fake[(size_t)x + 1] = fake[(size_t)x] + hb[(size_t)(j + 1) * t.n_t + x] - hb[(size_t)j * t.n_t + x];
+                qb.plan[prec].push_back(build_plan(c, fake, t.n_t, E, ng));
+                most = std::max<int64_t>(most, qb.plan[prec].back().n_items);
+            }
+        } catch (...) {
+            for (Plan &pl : qb.plan[prec]) free_plan(c, pl);
+            qb.plan[prec].clear();
+            throw;
+        }
+        qb.max_items[prec] = most;
+    }
+    return nb;
+}
+
 PassArgs pass_args(const Template &t, int side, const tsid_fit_opts &o, int32_t *err) {
     PassArgs a{};
     // with dense head tiles the item pass walks the other cells only
@@ -1320,6 +1412,7 @@ void fit_minibatch(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, doub
     c->epochs_done = 0;
     c->dense_used = tsid_dense_info{};
     c->used_kernel[0] = c->used_kernel[1] = TSID_PASS_ITEM;
+    c->used_blocks = 1;
     FitBufs &f = c->fb;
     hipStream_t cs = c->comp;
     const int64_t lp = (int64_t)t.m_t * K, lq = (int64_t)t.n_t * K;
@@ -1459,6 +1552,9 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     }
     if (c->mb_batches > 0) return fit_minibatch(c, P, Q, o, loss_hist);
     ensure_fit_buffers(c, o->prec, o->epochs, o->clip != 2, 0, o->clip == 2 || sim.on);
+    const int32_t nb = ensure_qblock(c, o->prec);  // row blocks of the Q pass (1: one pass)
+    if (nb > 1) ensure_fit_buffers(c, o->prec, o->epochs, o->clip != 2, t.qb.max_items[o->prec], o->clip == 2 || sim.on);
+    c->used_blocks = nb;
     c->epochs_done = 0;
     FitBufs &f = c->fb;
     hipStream_t cs = c->comp;
@@ -1578,10 +1674,32 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
             ac.carry = f.carry_c;
             ac.e2 = nullptr;
             ac.norm = normq;
-            launch_item_pass(K, prec, false, ac, cs, ev.first, ev.second);
-            if ((dn ? t.dense.plan[1] : t.plan[1][prec]).spans) {
-                ev = timed(c, ep, TK_QFIX);
-                launch_fixup(K, prec, ac, cs, ev.first, ev.second);
+            if (nb > 1) {
+                // one pass per row block (its gathers stay in the last-level
+                // cache), each leaving per-column partial sums; then the
+                // combine kernel adds them in block order and updates Q
+                for (int32_t j = 0; j < nb; ++j) {
+                    PassArgs bj = ac;
+                    const Plan &pl = t.qb.plan[prec][(size_t)j];
+                    bj.ptr = t.qb.bounds + (int64_t)j * t.n_t;
+                    bj.ptr_end = t.qb.bounds + (int64_t)(j + 1) * t.n_t;
+                    bj.items = pl.items;
+                    bj.item_off = pl.item_off;
+                    bj.item_end = pl.item_end;
+                    bj.n_items = pl.n_items;
+                    bj.E = pl.E;
+                    bj.norm = nullptr;
+                    bj.partial_out = t.qb.part + (int64_t)j * t.n_t * K;
+                    launch_item_pass(K, prec, false, bj, cs, j == 0 ? ev.first : nullptr, nullptr);
+                    if (pl.spans) launch_fixup(K, prec, bj, cs);
+                }
+                launch_block_combine(K, prec, ac, t.qb.part, nb, cs, nullptr, ev.second);
+            } else {
+                launch_item_pass(K, prec, false, ac, cs, ev.first, ev.second);
+                if ((dn ? t.dense.plan[1] : t.plan[1][prec]).spans) {
+                    ev = timed(c, ep, TK_QFIX);
+                    launch_fixup(K, prec, ac, cs, ev.first, ev.second);
+                }
             }
         }
         if (want_loss && slot == kLossRing - 1) flush(ep + 1, timed(c, ep, TK_REDUCE));
@@ -2046,6 +2164,18 @@ tsid_status tsid_set_dense_tiles(tsid_ctx *c, float fill) {
 tsid_status tsid_set_similarity(tsid_ctx *c, const int32_t *row, const int32_t *col, const float *val,
                                 int64_t nnz, float beta) {
     return guarded(c, [&]() { set_similarity(c, row, col, val, nnz, beta); });
+}
+
+tsid_status tsid_set_row_blocks(tsid_ctx *c, int32_t n_blocks) {
+    if (!c || n_blocks < 0 || n_blocks > TSID_MAX_ROW_BLOCKS) return TSID_E_INVAL;
+    c->row_blocks = n_blocks;
+    return TSID_OK;
+}
+
+tsid_status tsid_fit_row_blocks(const tsid_ctx *c, int32_t *n_blocks) {
+    if (!c || !n_blocks) return TSID_E_INVAL;
+    *n_blocks = c->used_blocks;
+    return TSID_OK;
 }
 
 tsid_status tsid_set_minibatch(tsid_ctx *c, int32_t n_batches, uint64_t seed) {

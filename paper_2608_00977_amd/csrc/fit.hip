@@ -151,6 +151,10 @@ __device__ __forceinline__ bool skip_epoch(const PassArgs &A) {
 template <int G, int V, bool BF16>
 __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg, const float (&x)[V],
                                              const float (&acc_in)[V], int64_t deg) {
+    if (A.partial_out) {  // a row block's pass: the sum only, the update comes later
+        store_f32<V>(A.partial_out + (int64_t)row * (G * V) + lg * V, acc_in);
+        return;
+    }
     float acc[V];
 #pragma unroll
     for (int v = 0; v < V; ++v) acc[v] = acc_in[v];
@@ -422,7 +426,7 @@ __global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass(const Pas
         i0 = A.item_off[row];
         i1 = A.item_end[row];
         const int64_t rb = A.ptr[row];
-        re = A.ptr[row + 1];
+        re = A.ptr_end ? A.ptr_end[row] : A.ptr[row + 1];
         const int64_t deg = re - rb, parts = (int64_t)(i1 - i0), q = item - (int64_t)i0;
         beg = rb + q * deg / parts;
         end = rb + (q + 1) * deg / parts;
@@ -545,6 +549,47 @@ __global__ __launch_bounds__(kThreads) void k_fixup(const PassArgs A) {
         load_f32<V>(A.carry + (int64_t)it * K + lg * V, part);
 #pragma unroll
         for (int v = 0; v < V; ++v) acc[v] += part[v];
+    }
+    float x[V];
+    load_f32<V>(A.X + row * K + lg * V, x);
+    finalize_row<G, V, BF16>(A, (int)row, lg, x, acc, A.ptr[row + 1] - A.ptr[row]);
+}
+
+// Row-blocked passes.  Bounds of every bucket's runs of other indices per
+// block (binary search inside the bucket; one thread per bucket and block).
+__global__ void k_block_bounds(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_blocks,
+                               int64_t block_rows, int64_t *bounds) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= (int64_t)(n_blocks + 1) * rows) return;
+    const int64_t j = t / rows, x = t % rows;
+    const int64_t target = j * block_rows;
+    int64_t lo = ptr[x], hi = ptr[x + 1];  // first position whose other index >= target
+    while (lo < hi) {
+        const int64_t mid = lo + ((hi - lo) >> 1);
+        if ((int64_t)stream[mid].x < target) lo = mid + 1;
+        else hi = mid;
+    }
+    bounds[t] = lo;
+}
+
+// The blocks' partial sums of a row added in block order, then its update
+// (one lane group per row, as in k_fixup).
+template <int K, int V, bool BF16>
+__global__ __launch_bounds__(kThreads) void k_block_combine(const PassArgs A, const float *part, int32_t n_blocks) {
+    constexpr int G = K / V;
+    constexpr int NG = 64 / G;
+    if (skip_epoch(A)) return;
+    const int lane = threadIdx.x & 63;
+    const int grp = lane / G, lg = lane % G;
+    const int64_t row = ((int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6)) * NG + grp;
+    if (row >= A.rows) return;
+    float acc[V];
+    load_f32<V>(part + row * K + lg * V, acc);
+    for (int32_t j = 1; j < n_blocks; ++j) {
+        float p[V];
+        load_f32<V>(part + ((int64_t)j * A.rows + row) * K + lg * V, p);
+#pragma unroll
+        for (int v = 0; v < V; ++v) acc[v] += p[v];
     }
     float x[V];
     load_f32<V>(A.X + row * K + lg * V, x);
@@ -754,6 +799,17 @@ void extend_steps_kv(const PassArgs &a, int32_t steps, hipStream_t s) {
 }
 
 template <int K, int V, bool BF16>
+void block_combine_kv(const PassArgs &a, const float *part, int32_t n_blocks, hipStream_t s, hipEvent_t ev0,
+                      hipEvent_t ev1) {
+    constexpr int NG = 64 / (K / V);
+    const int grid = ceil_div(a.rows, (int64_t)kWaves * NG);
+    if (grid <= 0) return;
+    hipExtLaunchKernelGGL(k_block_combine<K, V, BF16>, dim3(grid), dim3(kThreads), 0, s, ev0, ev1, 0, a, part,
+                          n_blocks);
+    TSID_HIP(hipGetLastError());
+}
+
+template <int K, int V, bool BF16>
 void fixup_kv(const PassArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     constexpr int NG = 64 / (K / V);
     const int grid = ceil_div(a.rows, (int64_t)kWaves * NG);
@@ -807,6 +863,19 @@ void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStr
 
 void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
     TSID_DISPATCH_K(K, fixup_kv, a, s, ev0, ev1)
+}
+
+void launch_block_combine(int K, int prec, const PassArgs &a, const float *part, int32_t n_blocks, hipStream_t s,
+                          hipEvent_t ev0, hipEvent_t ev1) {
+    TSID_DISPATCH_K(K, block_combine_kv, a, part, n_blocks, s, ev0, ev1)
+}
+
+void launch_block_bounds(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_blocks, int64_t block_rows,
+                         int64_t *bounds, hipStream_t s) {
+    const int64_t n = (int64_t)(n_blocks + 1) * rows;
+    if (n <= 0) return;
+    k_block_bounds<<<ceil_div(n, 256), 256, 0, s>>>(stream, ptr, rows, n_blocks, block_rows, bounds);
+    TSID_HIP(hipGetLastError());
 }
 
 void launch_extend_steps(int K, const PassArgs &a, int32_t steps, hipStream_t s) {

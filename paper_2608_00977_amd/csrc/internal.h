@@ -130,6 +130,11 @@ struct PassArgs {
     // rows x K extra gradient added (times gx_scale) before the update, or null
     const float *gx;
     float gx_scale;
+    // Row-blocked passes: bucket x spans ptr[x] .. ptr_end[x] (null: ptr[x + 1]),
+    // and with partial_out the pass stores each bucket's gradient sum there
+    // (rows x K) instead of updating the row.
+    const int64_t *ptr_end;
+    float *partial_out;
 };
 
 // prec: 0 fp32, 1 bf16.  loss_only: residuals, e2 and norms only.
@@ -139,6 +144,15 @@ void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStr
                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s, hipEvent_t ev0 = nullptr,
                   hipEvent_t ev1 = nullptr);
+// Row blocks of a bucketed stream: bounds[j * rows + x] = first cell of bucket
+// x whose other index is >= j * block_rows, for j = 0 .. n_blocks (int64).
+void launch_block_bounds(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_blocks, int64_t block_rows,
+                         int64_t *bounds, hipStream_t s);
+// After the n_blocks partial passes: row x's sums part[j * rows * K + x * K ..]
+// added in block order, then the row update of `a` (its own bucket pointers
+// give the degrees).
+void launch_block_combine(int K, int prec, const PassArgs &a, const float *part, int32_t n_blocks, hipStream_t s,
+                          hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // `steps` one-sided extension steps from zero in one launch, one wave per
 // bucket (a.rows buckets over a.stream / a.ptr; fp32; a.X unused, the result
 // goes to a.Xn; a non-finite update stores 1 in a.err[ERR_NONFINITE]).
