@@ -62,6 +62,12 @@ def parse():
     ap.add_argument("--dense-fill", type=float, default=-1.0,
                     help="dense head tiles of bf16 fits (tsid_set_dense_tiles): < 0 automatic, "
                          "0 off, in (0, 1] forced with that tile fill")
+    ap.add_argument("--clip-per-entry", action="store_true",
+                    help="the clip in the per-entry order (fit option clip = 2; item pass, no tiles)")
+    ap.add_argument("--similarity", type=float, default=0.0,
+                    help="beta of the multi-view term over a synthetic similarity graph of the template's "
+                         "columns (16 random links per column, made mutual); item pass")
+    ap.add_argument("--lr", type=float, default=None, help="step size instead of the workload's")
     ap.add_argument("--row-blocks", type=int, default=0,
                     help="row blocks of the item Q pass (tsid_set_row_blocks): 0 automatic, 1 off, n forced")
     ap.add_argument("--minibatch", type=int, default=0,
@@ -270,6 +276,8 @@ def main():
     log(f"generating {args.config}")
     t0 = time.perf_counter()
     p = tsid_synth.make(args.config)
+    if args.lr is not None:
+        p.lr = args.lr
     gen_s = time.perf_counter() - t0
     log(f"generated {p.nnz} training cells in {gen_s:.1f}s")
 
@@ -290,9 +298,19 @@ def main():
     nnz = info["nnz"]
     log(f"template {info['m_t']} x {info['n_t']}, |Omega*| = {nnz}, build {build_s:.3f}s")
 
+    sim = None
+    if args.similarity > 0:
+        sr, sc, sv = tsid_synth.similarity_graph(p.J.size, 16, 7)
+        T.set_similarity(sr, sc, sv, args.similarity)
+        T.set_pass_kernel("item")
+        sim = {"beta": args.similarity, "entries": int(sv.size), "links_per_column": 16}
+    if args.clip_per_entry:
+        T.set_pass_kernel("item")
+        T.set_dense_tiles(0)
     P0 = torch.from_numpy(p.P0).cuda()
     Q0 = torch.from_numpy(p.Q0).cuda()
-    mk = lambda ep: tsid.make_opts(epochs=ep, lam=p.lam, lr=p.lr, clip=p.clip, xi=p.xi,
+    clip = "per_entry" if args.clip_per_entry else p.clip
+    mk = lambda ep: tsid.make_opts(epochs=ep, lam=p.lam, lr=p.lr, clip=clip, xi=p.xi,
                                    prec=p.prec, step=p.step)
     if args.warmup:
         P, Q = P0.clone(), Q0.clone()
@@ -352,8 +370,9 @@ def main():
     achieved = dom_by / (dom_ms / 1e3) / 1e9
     src = open(os.path.join(ROOT, "paper_2608_00977_amd", "csrc", ksrc), "rb").read()
     sha = hashlib.sha256(src).hexdigest()
-    traffic = traffic_from_profiles(sha, f"{args.config}:{which}:{kkind}"
-                                    + (f":minibatch{args.minibatch}" if args.minibatch else ""))
+    variant = (f":minibatch{args.minibatch}" if args.minibatch else "") + (":clip2" if args.clip_per_entry else "") \
+        + (":similarity" if args.similarity > 0 else "") + (f":rowblocks{row_blocks}" if row_blocks > 1 else "")
+    traffic = traffic_from_profiles(sha, f"{args.config}:{which}:{kkind}" + variant)
     epoch_bytes = by[0] + by[1] + (sum(c[1] for c in cand[2:]) if di["tiles"] else 0)
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
@@ -385,6 +404,10 @@ def main():
         "mid": "Mid template fit: 4,096 x 2,048 of 20,000 x 10,000 (2M cells), k=32, fp32",
         "tiny": "Tiny template fit: 200 x 160 of 1,000 x 800 (40k cells), k=8, fp32",
     }[args.config]
+    if args.clip_per_entry:
+        workload += "; clip in the per-entry order"
+    if sim:
+        workload += f"; multi-view term, beta {args.similarity}, {sim['entries']:,} similarity entries"
     if args.minibatch:
         workload += f"; mini-batch epochs, {args.minibatch} batches (seed {args.minibatch_seed}), loss pass each epoch"
     line = {
@@ -403,7 +426,7 @@ def main():
         "config": {"workload": workload, "config": args.config, "m": p.m, "n": p.n,
                    "m_t": m_t, "n_t": n_t, "template_cells_train": nnz, "k": k,
                    "precision": p.prec, "step": p.step, "lr": p.lr, "lambda": p.lam,
-                   "clip": p.clip, "parallelism": "single GPU",
+                   "clip": clip, "parallelism": "single GPU", "similarity": sim,
                    "pass_kernels": {"p_pass": kernels[0], "q_pass": kernels[1]},
                    "q_pass_row_blocks": row_blocks,
                    "dense_tiles": dense,

@@ -25,6 +25,7 @@ from .generate import (  # noqa: F401
     billion_template,
     random_case,
     dense_lowrank_case,
+    similarity_graph,
     CONFIGS,
     make,
 )

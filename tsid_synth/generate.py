@@ -465,6 +465,27 @@ def dense_lowrank_case(m: int, n: int, rank: int, frac: float, seed: int):
     return R, (flat // n).astype(np.int32), (flat % n).astype(np.int32)
 
 
+def similarity_graph(n: int, degree: int, seed: int):
+    """A random sparse symmetric similarity matrix over n items, as input
+    data for the multi-view term: each item links to `degree` others drawn
+    uniformly, the links are made mutual, and each pair gets one weight drawn
+    uniformly from (0, 1].  Returns COO (row, col, val) with both orientations
+    of every pair, no diagonal, no repeated entry."""
+    g = make_rng(seed, "extra")
+    if n < 2 or degree < 1:
+        e = np.empty(0, np.int32)
+        return e, e, np.empty(0, np.float32)
+    src = np.repeat(np.arange(n, dtype=np.int64), degree)
+    dst = (src + g.integers(1, n, src.size)) % n  # never the item itself
+    lo, hi = np.minimum(src, dst), np.maximum(src, dst)
+    pairs = np.unique(lo * n + hi)
+    w = (1.0 - g.random(pairs.size)).astype(np.float32)  # (0, 1]
+    a, b = pairs // n, pairs % n
+    row = np.concatenate([a, b]).astype(np.int32)
+    col = np.concatenate([b, a]).astype(np.int32)
+    return row, col, np.concatenate([w, w])
+
+
 CONFIGS: Dict[str, Callable[..., Problem]] = {
     "tiny": tiny, "mid": mid, "rating": rating, "scientific": scientific_template,
     "billion": billion_template,
