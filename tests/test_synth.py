@@ -102,3 +102,15 @@ def test_billion_template_cells_follow_the_cell_law():
         mean_p = prob[band].mean()
         sd = np.sqrt(np.sum(prob[band] * (1 - prob[band]))) / band.sum()
         assert abs(seen[band].mean() - mean_p) <= 5 * sd + 1e-3, (lo, hi)
+
+
+def test_similarity_graph_is_symmetric_and_simple():
+    r, c, v = synth.similarity_graph(500, 8, 3)
+    assert r.size == c.size == v.size > 0
+    assert np.all(r != c) and np.all((v > 0) & (v <= 1))
+    key = r.astype(np.int64) * 500 + c
+    assert np.unique(key).size == key.size
+    fw = dict(zip(key.tolist(), v.tolist()))
+    assert all(fw[int(b) * 500 + int(a)] == w for a, b, w in zip(r, c, v))
+    r2, c2, v2 = synth.similarity_graph(500, 8, 3)
+    assert np.array_equal(r, r2) and np.array_equal(v, v2)
