@@ -1053,7 +1053,10 @@ void ensure_dense(tsid_ctx *c, int prec) {
         return;
     }
     const float fill = mode > 0.f ? mode : TSID_DENSE_FILL;
-    if (!t.dense.ready || t.dense.fill != fill) build_dense(c, fill);
+    if (!t.dense.ready || t.dense.fill != fill) {
+        build_dense(c, fill);
+        free_blocks(c, t.qb);  // the row blocks index the other cells' stream, which changed
+    }
     t.dense_use = mode > 0.f ? true : t.dense.cells >= TSID_DENSE_MIN_SHARE * (double)t.nnz && t.dense.tiles > 0;
 }
 

@@ -101,6 +101,17 @@ def test_row_blocks_bf16_dense_one_epoch(T):
     sto, Po, Qo, _, _ = oracle.fit(a, b, v, p.P0, p.Q0, 1, p.lam, p.lr, p.step, True, p.xi, bf16=True)
     assert sto == 0
     assert rel_fro(P, Po) <= FP32_TOL and rel_fro(Q, Qo) <= FP32_TOL, (rel_fro(P, Po), rel_fro(Q, Qo))
+    # another tile fill rebuilds the other cells' stream, and the blocks with it
+    T.set_row_blocks(4)
+    T.set_dense_tiles(0.5)
+    try:
+        note("row blocks bf16 mid, fill 0.5")
+        st, P, Q, _ = _fit(T, p, prec="bf16", epochs=1)
+        assert st == 0 and T.row_blocks() == 4 and T.dense_info()["tiles"] > 0
+    finally:
+        T.set_row_blocks(0)
+        T.set_dense_tiles(-1)
+    assert rel_fro(P, Po) <= FP32_TOL and rel_fro(Q, Qo) <= FP32_TOL, (rel_fro(P, Po), rel_fro(Q, Qo))
 
 
 def test_row_blocks_with_similarity_term(T):
