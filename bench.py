@@ -89,7 +89,7 @@ def parse():
     ap.add_argument("--extend-solver", default="steps", choices=["steps", "ridge", "adam"],
                     help="extension solver: one-sided gradient steps (tsid_extend_chunk), the "
                          "exact ridge solve per free row (tsid_extend_chunk_ridge, fp64 Gram on the "
-                         "matrix cores + Cholesky), or the column phase as Eq. 10 states it (Adam "
+                         "matrix cores + Cholesky), or the column phase as Eq. 6 states it (Adam "
                          "on each free column's coefficients over the template columns' factors, "
                          "--extend-steps steps, lr 0.01; rows by the exact solve); all with the "
                          "fit's lambda")
@@ -223,7 +223,7 @@ def extension_line(args, p, T, P, Q):
         opts = float(p.lam)
         col_opts = tsid.make_adam_opts(args.extend_steps, p.lam, 0.01)
         how = (f"rows by the exact ridge solve; columns by {args.extend_steps} Adam steps on their "
-               f"coefficients over the {p.J.size} template columns' factors (Eq. 10; lr 0.01, "
+               f"coefficients over the {p.J.size} template columns' factors (Eq. 6; lr 0.01, "
                f"lambda {p.lam})")
     else:
         # one-sided steps from zero: lr 0.05 keeps a free row with a single cell stable

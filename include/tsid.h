@@ -63,7 +63,7 @@ typedef enum { TSID_STEP_SUM = 0, TSID_STEP_DEGREE = 1 } tsid_step;
  *          descent direction d becomes min(d, clip_xi) (positive components
  *          are capped, negative ones pass; NaN propagates).  clip_xi > 0.
  *          2: the same clip in the per-entry order (Section 5.3 applied to
- *          Eqs. 3-4 entry by entry, then the 1/n average of Eq. 9): each
+ *          Eqs. 3-4 entry by entry, then the 1/n average of Eq. 5): each
  *          cell adds min(2 e q - 2 lambda p, clip_xi) per coordinate (the
  *          regulariser once per cell, the master p in it) and the row moves by
  *          lr times the sum (divided by its degree with the DEGREE step); a
@@ -209,7 +209,7 @@ tsid_status tsid_extend_chunk_ridge(tsid_ctx *ctx, int side, const int32_t *fixe
                                     int32_t n_free, const float *F_fixed, int64_t n_fixed,
                                     float *F_free, float lambda);
 
-/* One chunk of the extension as Eq. 10 states it (Stage II, Section 5.2):
+/* One chunk of the extension as Eq. 6 states it (Stage II, Section 5.2):
  * free line f is represented in the fixed template basis by a coefficient
  * vector c_f with one entry per basis line, its entries are predicted as
  * p . (B^T c_f) with p = F_fixed[fixed_id] (R* = P B^T in factored form), and
@@ -334,7 +334,7 @@ tsid_status tsid_set_similarity(tsid_ctx *ctx, const int32_t *row, const int32_t
                                 int64_t nnz, float beta);
 
 /* Mini-batch epochs for tsid_fit_template (Section 5.1: the stochastic
- * method updates the factors within an epoch, Eq. 9 averaging each update
+ * method updates the factors within an epoch, Eq. 5 averaging each update
  * over the entries it uses; here the entries are grouped into mini-batches).
  * Cell (a, b) of the template (a: position of its row in I, b: of its column
  * in J) belongs to batch splitmix64(seed ^ (a << 32 | b)) mod n_batches, with

@@ -221,7 +221,7 @@ def ridge(fixed_id, free_id, v, n_free, F_fixed, lam):
 
 def extend_adam(fixed_id, free_id, v, n_free, F_fixed, B, steps, lam, lr, beta1=0.9, beta2=0.999,
                 eps=1e-8):
-    """Stage II as Eq. 10 states it (Section 5.2): Adam on the coefficients C of
+    """Stage II as Eq. 6 states it (Section 5.2): Adam on the coefficients C of
     each free line in the template basis B.  Returns (status, B^T C per free
     line (n_free x k), C (n_free x n_b))."""
     fixed_id, free_id, v = _c(fixed_id, np.int32), _c(free_id, np.int32), _c(v, np.float32)

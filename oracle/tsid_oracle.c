@@ -192,7 +192,7 @@ static double sse_grad(int64_t nnz, const int32_t *a, const int32_t *b, const fl
 }
 
 /* Per-entry order of the clipped update (Section 5.3 applied to each entry's
- * own gradient, Eqs. 3-4, before the 1/n average of Eq. 9): cell (p, q) with
+ * own gradient, Eqs. 3-4, before the 1/n average of Eq. 5): cell (p, q) with
  * residual err adds, per coordinate, its descent direction 2 err q - 2 lambda
  * p clipped at xi to the row sums gp, and likewise to gq.  Products use the
  * (possibly bf16-rounded) pr, qr; the regulariser uses the masters p, q. */

@@ -108,10 +108,10 @@ void or_batch_of_many(int64_t n, const int32_t *a, const int32_t *b, uint64_t se
                       int32_t *out);
 
 /* Mini-batch epochs (the in-epoch updates of the stochastic method of
- * Section 5.1, Eq. 9, grouped into mini-batches): each epoch visits the
+ * Section 5.1, Eq. 5, grouped into mini-batches): each epoch visits the
  * n_batches batches in order and takes, for each, the full-gradient step of
  * or_fit restricted to the batch's cells (the degree step divides by the
- * batch degree, Eq. 9's 1/n over the contributing entries), from the factors
+ * batch degree, Eq. 5's 1/n over the contributing entries), from the factors
  * the previous batch left; rows and columns without a cell in the batch are
  * not touched.  loss_hist[t] = L(P_t, Q_t) over every cell at the start of
  * epoch t, loss_hist[epochs] at the end.  On a non-finite update the factors
@@ -137,7 +137,7 @@ int or_extend(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, cons
 int or_ridge(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,
              int32_t n_free, int32_t k, const double *F_fixed, double lambda, double *F_free);
 
-/* Stage II as stated in Section 5.2 (Eq. 10): free line f is represented in
+/* Stage II as stated in Section 5.2 (Eq. 6): free line f is represented in
  * the fixed template basis by a coefficient vector c_f (n_b entries), and
  * its entries are predicted as R*_i c_f = p . (B^T c_f), with p the fixed
  * factor row F_fixed[fixed_id] and B (n_b x k) the basis factors of the

@@ -1,4 +1,4 @@
-// Stage II as Eq. 10 states it (Section 5.2): each free line f (a column of
+// Stage II as Eq. 6 states it (Section 5.2): each free line f (a column of
 // R outside the template, or a row) is represented in the fixed template
 // basis by a coefficient vector c_f with one entry per basis line, and its
 // entries are predicted as R*_i c_f.  In factored form R* = P B^T, so the

@@ -1,5 +1,5 @@
 // Mini-batch epochs (the in-epoch updates of the stochastic method of
-// Section 5.1, Eq. 9, grouped into mini-batches): the template's cells are
+// Section 5.1, Eq. 5, grouped into mini-batches): the template's cells are
 // dealt into B batches by a hash of their template position, and each epoch
 // takes one batch-restricted step per batch, in batch order.
 //

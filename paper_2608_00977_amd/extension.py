@@ -93,7 +93,7 @@ class Extension:
         in template order.  opts (and col_opts for the column phase, if given):
         tsid_fit_opts for one-sided gradient steps, a float lambda for the
         exact ridge solve of every free line, or tsid_adam_opts for Adam on
-        the coefficients of each free line in the template basis (Eq. 10:
+        the coefficients of each free line in the template basis (Eq. 6:
         free columns over the template columns' factors Q_t, free rows over
         the template rows' factors P_t).  Returns (P, Q): the full m x k and n x k factors
         as pinned host tensors, and the wall time of each phase in seconds."""

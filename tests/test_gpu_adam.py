@@ -1,4 +1,4 @@
-"""The extension as Eq. 10 states it (tsid_extend_chunk_adam; Section 5.2:
+"""The extension as Eq. 6 states it (tsid_extend_chunk_adam; Section 5.2:
 Adam on the coefficients C of each free line in the template basis) against
 the oracle's fp64 iteration of the same steps.
 

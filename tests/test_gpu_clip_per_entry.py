@@ -1,5 +1,5 @@
 """The per-entry order of the clipped update (fit option clip = 2; Section 5.3
-applied to Eqs. 3-4 entry by entry, before the 1/n average of Eq. 9) against
+applied to Eqs. 3-4 entry by entry, before the 1/n average of Eq. 5) against
 the oracle's clip mode 2, through the C ABI.
 
 Each cell adds min(2 e q - 2 lambda p, xi) per coordinate; min is

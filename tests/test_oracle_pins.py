@@ -150,7 +150,7 @@ def _adam_case(seed, n_b=6, k=3, n_free=3, n_fixed=9):
 
 
 def test_extension_adam_first_step_is_normalised_gradient(oracle_lib):
-    """Stage II as Eq. 10 states it, Adam on the coefficients C (Section 5.2).
+    """Stage II as Eq. 6 states it, Adam on the coefficients C (Section 5.2).
     From C = 0 the gradient of L(C) is G_f = -2 sum r B p (the predictions are
     zero), and after the bias correction Adam's first step is exactly
     -lr G / (|G| + eps) elementwise, whatever beta1 and beta2 are.  A dropped
