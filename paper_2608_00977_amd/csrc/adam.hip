@@ -8,11 +8,12 @@
 // The coefficients move by the Adam method (bias-corrected first and second
 // moment estimates, elementwise step lr m^ / (sqrt(w^) + eps)), from C = 0.
 //
-// A step is two launches, free lines being independent:
-//  k_adam_cells   one workgroup per free line: x_f from the previous step's
-//                 partial products (slice order), then the residual of every
-//                 entry of f (eight at a time) and g_f, the four waves'
-//                 shares added in order.
+// A step is four launches, free lines being independent:
+//  k_adam_x       x_f from the previous step's partial products (slice order).
+//  the item pass  the residual of every entry of f and sum_e e p, with x_f as
+//                 the owner row and F the gathered table: the template fit's
+//                 per-cell kernel, its sums stored per free line instead of an
+//                 update, then k_fixup for the lines split over waves.
 //  k_adam_update  one wave per free line and slice of 256 basis lines (four
 //                 lanes per basis line, a quarter of its coordinates each):
 //                 the gradient of those coefficients, the Adam step, and the
@@ -27,68 +28,18 @@ namespace tsid {
 
 namespace {
 
-constexpr int kAdamCellWaves = 4;
 constexpr int kAdamUpdWaves = 4;
 
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
-    return x;  // the same bits in every lane (each step adds the same two values)
-}
-
+// x_f = B^T c_f: the slices' partial products of free line f, in slice order.
 template <int K>
-__global__ __launch_bounds__(64 * kAdamCellWaves) void k_adam_cells(const AdamArgs A, int final_pass) {
-    const int64_t f = blockIdx.x;
-    if (f >= A.n_free) return;
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    // x_f = B^T c_f: the slices' partial products, in slice order
+__global__ __launch_bounds__(256) void k_adam_x(const AdamArgs A) {
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= A.n_free * K) return;
+    const int64_t f = t / K;
+    const int c = (int)(t % K);
     float x = 0.f;
-    if (lane < K)
-        for (int32_t s = 0; s < A.n_slices; ++s) x += A.qpart[((int64_t)f * A.n_slices + s) * K + lane];
-    if (final_pass) {
-        if (wv == 0 && lane < K) A.X[f * K + lane] = x;
-        return;
-    }
-    if (A.skip_after_nonfinite && A.err[ERR_NONFINITE]) return;
-    const int64_t b0 = A.ptr[f], b1 = A.ptr[f + 1], n = b1 - b0;
-    const int64_t lo = b0 + wv * n / kAdamCellWaves, hi = b0 + (wv + 1) * n / kAdamCellWaves;
-    float g = 0.f;
-    // eight entries at a time: every load of the group is issued before the
-    // eight reductions, which then interleave
-    constexpr int U = 8;
-    int64_t j = lo;
-    for (; j + U <= hi; j += U) {
-        int2 rec[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) rec[u] = A.stream[j + u];
-        float p[U], d[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) p[u] = lane < K ? A.F[(int64_t)rec[u].x * K + lane] : 0.f;
-#pragma unroll
-        for (int u = 0; u < U; ++u) d[u] = p[u] * x;
-#pragma unroll
-        for (int off = 32; off > 0; off >>= 1) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) d[u] += __shfl_xor(d[u], off, 64);
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) g = fmaf(__int_as_float(rec[u].y) - d[u], p[u], g);
-    }
-    for (; j < hi; ++j) {
-        const int2 rec = A.stream[j];
-        const float p = lane < K ? A.F[(int64_t)rec.x * K + lane] : 0.f;
-        const float e = __int_as_float(rec.y) - wave_sum(p * x);
-        g = fmaf(e, p, g);
-    }
-    __shared__ float red[kAdamCellWaves][64];
-    red[wv][lane] = g;
-    __syncthreads();
-    if (wv == 0 && lane < K) {
-        float s = 0.f;
-#pragma unroll
-        for (int w = 0; w < kAdamCellWaves; ++w) s += red[w][lane];
-        A.gt[f * K + lane] = -2.f * s;
-    }
+    for (int32_t s = 0; s < A.n_slices; ++s) x += A.qpart[(f * A.n_slices + s) * K + c];
+    A.X[t] = x;
 }
 
 // One wave per free line and slice of 256 basis lines.  Lane l takes basis
@@ -108,7 +59,7 @@ __global__ __launch_bounds__(64 * kAdamUpdWaves) void k_adam_update(const AdamAr
     float gv[KQ], qp[KQ];
 #pragma unroll
     for (int c = 0; c < KQ; ++c) {
-        gv[c] = A.gt[fl * K + q * KQ + c];
+        gv[c] = -2.f * A.gt[fl * K + q * KQ + c];  // dL/dx_f = -2 sum_e e p
         qp[c] = 0.f;
     }
     bool bad = false;
@@ -171,16 +122,39 @@ void adam_k(const AdamArgs &a, int32_t steps, hipStream_t st) {
     const double b1 = a.beta1, b2 = a.beta2;
     double b1t = 1.0, b2t = 1.0;
     const dim3 gu((unsigned)((a.n_free + kAdamUpdWaves - 1) / kAdamUpdWaves), (unsigned)a.n_slices);
+    const unsigned gx = (unsigned)((a.n_free * K + 255) / 256);
+    // the gradient's item pass: owner rows x_f (in X), gathered rows of F,
+    // each free line's sum stored in gt instead of an update
+    PassArgs g{};
+    g.stream = a.stream;
+    g.ptr = a.ptr;
+    g.items = a.items;
+    g.item_off = a.item_off;
+    g.item_end = a.item_off + 1;
+    g.n_items_dev = a.item_off + a.n_free;
+    g.n_items = (int32_t)a.n_items_ub;
+    g.rows = (int32_t)a.n_free;
+    g.E = a.E;
+    g.X = a.X;
+    g.Y = a.F;
+    g.y_rows = a.n_fixed;
+    g.carry = a.carry;
+    g.err = a.err;
+    g.epoch = INT32_MAX;  // skipped once any step has stored a non-finite flag
+    g.skip_after_nonfinite = a.skip_after_nonfinite;
+    g.partial_out = a.gt;
     for (int32_t t = 1; t <= steps; ++t) {
         b1t *= b1;
         b2t *= b2;
-        hipLaunchKernelGGL(k_adam_cells<K>, dim3((unsigned)a.n_free), dim3(64 * kAdamCellWaves), 0, st, a, 0);
+        hipLaunchKernelGGL(k_adam_x<K>, dim3(gx), dim3(256), 0, st, a);
         TSID_HIP(hipGetLastError());
+        launch_item_pass(K, TSID_FP32, false, g, st);
+        launch_fixup(K, TSID_FP32, g, st);
         hipLaunchKernelGGL(k_adam_update<K>, gu, dim3(64 * kAdamUpdWaves), 0, st, a, (float)(1.0 / (1.0 - b1t)),
                            (float)(1.0 / (1.0 - b2t)));
         TSID_HIP(hipGetLastError());
     }
-    hipLaunchKernelGGL(k_adam_cells<K>, dim3((unsigned)a.n_free), dim3(64 * kAdamCellWaves), 0, st, a, 1);
+    hipLaunchKernelGGL(k_adam_x<K>, dim3(gx), dim3(256), 0, st, a);
     TSID_HIP(hipGetLastError());
 }
 

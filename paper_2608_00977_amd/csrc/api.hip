@@ -225,6 +225,12 @@ struct ExtState {
     uint32_t *vals = nullptr, *vals_alt = nullptr, *sort_scratch = nullptr;
     int2 *stream = nullptr;
     int64_t *ptr = nullptr;
+    // work plan of a chunk's item pass (built on the device; the Adam
+    // extension's gradient), its bound on the item count and split-bucket sums
+    uint32_t *plan_off = nullptr, *plan_nparts = nullptr, *plan_scan = nullptr;
+    int32_t *plan_items = nullptr;
+    float *plan_carry = nullptr;
+    int64_t plan_cap = 0;
     int32_t *err = nullptr;
     int next = 0;
     bool pending = false;
@@ -478,6 +484,12 @@ void free_ext_buffers(tsid_ctx *c) {
     A.release(x.sort_scratch);
     A.release(x.stream);
     A.release(x.ptr);
+    A.release(x.plan_off);
+    A.release(x.plan_nparts);
+    A.release(x.plan_scan);
+    A.release(x.plan_items);
+    A.release(x.plan_carry);
+    x.plan_cap = 0;
     x.cap_nnz = 0;
     x.cap_free = 0;
     x.k = 0;
@@ -1827,6 +1839,13 @@ void ext_ensure(tsid_ctx *c, int64_t nnz, int32_t n_free, int32_t k) {
     x.sort_scratch = A.alloc<uint32_t>((int64_t)radix_scratch_elems(cn));
     x.stream = A.alloc<int2>(cn);
     x.ptr = A.alloc<int64_t>((int64_t)cf + 1);
+    // items of at least 64 cells: at most one per row plus nnz / 64
+    x.plan_cap = (int64_t)cf + cn / 64 + 1;
+    x.plan_off = A.alloc<uint32_t>((int64_t)cf + 1);
+    x.plan_nparts = A.alloc<uint32_t>(cf);
+    x.plan_scan = A.alloc<uint32_t>((int64_t)scan_scratch_elems(cf));
+    x.plan_items = A.alloc<int32_t>(x.plan_cap);
+    x.plan_carry = A.alloc<float>(x.plan_cap * k);
     x.cap_nnz = cn;
     x.cap_free = cf;
     x.k = k;
@@ -1957,6 +1976,16 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
         a.eps = adam->o->eps;
         a.err = x.err;
         a.skip_after_nonfinite = 1;
+        // the gradient of every step runs on the item pass: its work plan
+        // (items of at most E cells of a free line) built on the device
+        const int32_t E = choose_E(nnz);
+        plan_items(x.ptr, n_free, E, x.plan_off, x.plan_items, x.plan_nparts, x.plan_scan, cs);
+        a.item_off = x.plan_off;
+        a.items = x.plan_items;
+        a.n_items_ub = (int64_t)n_free + nnz / E + 1;
+        a.E = E;
+        a.carry = x.plan_carry;
+        a.n_fixed = n_fixed;
         launch_adam(K, a, adam->o->steps, cs);
     } else if (ridge) {
         RidgeArgs a{};

@@ -262,6 +262,16 @@ struct AdamArgs {
     float lambda, lr, beta1, beta2, eps;
     int32_t *err;
     int32_t skip_after_nonfinite;
+    // the item pass that forms each step's gradient: device work plan over
+    // the chunk's buckets (item_off: n_free + 1, items), a bound on its item
+    // count, its item length, its split-bucket sums (n_items_ub x K) and the
+    // rows of F
+    const uint32_t *item_off;
+    const int32_t *items;
+    int64_t n_items_ub;
+    int32_t E;
+    float *carry;
+    int64_t n_fixed;
 };
 bool adam_supported(int K);
 int32_t adam_slices(int64_t n_b);
