@@ -138,3 +138,47 @@ def test_rating_fullsize_minibatch(T):
     assert np.array_equal(P1[~dr], p.P0[~dr].astype(np.float32))
     assert np.array_equal(Q1[~dc], p.Q0[~dc].astype(np.float32))
     np.testing.assert_allclose(h1, hj, rtol=1e-6)
+
+
+@pytest.mark.timeout(400)
+def test_scientific_fullsize_variants_sampled(T):
+    """The per-entry clip (bench.py --clip-per-entry) and the multi-view term
+    (bench.py --similarity 0.01) at full Scientific size, one epoch from
+    (P0, Q0): a row's new p depends only on its own cells and Q0, a column's
+    new q on its cells, P0 and (with the term) its neighbours' rows of Q0, so
+    the oracle reproduces sampled rows and columns from those alone."""
+    import torch
+    from paper_2608_00977_amd import make_opts
+    p = synth.scientific_template()
+    rm, cm, a, b, v = oracle_template(p)
+    note(f"fullsize scientific variants: building template over {p.nnz} cells")
+    T.build_template(p.m, p.n, p.u, p.i, p.r, p.I, p.J, p.k)
+    g = np.random.default_rng(1)
+    rows = np.sort(g.choice(p.I.size, 48, replace=False))
+    cols = np.sort(g.choice(p.J.size, 48, replace=False))
+    sr, sc, sv = synth.similarity_graph(p.J.size, 16, 7)
+    for variant in ("per_entry", "similarity"):
+        clip = "per_entry" if variant == "per_entry" else p.clip
+        beta = 0.01 if variant == "similarity" else 0.0
+        T.set_similarity(sr, sc, sv, beta)
+        P = torch.from_numpy(np.ascontiguousarray(p.P0, np.float32)).cuda()
+        Q = torch.from_numpy(np.ascontiguousarray(p.Q0, np.float32)).cuda()
+        note(f"fullsize scientific {variant}: one epoch")
+        st, _ = T.fit_template(P, Q, make_opts(epochs=1, lam=p.lam, lr=p.lr, clip=clip, xi=p.xi, prec="fp32",
+                                               step=p.step), raise_on_error=False)
+        assert st == 0
+        P1, Q1 = P.cpu().numpy(), Q.cpu().numpy()
+        mr = np.zeros(p.I.size, bool)
+        mr[rows] = True
+        mc = np.zeros(p.J.size, bool)
+        mc[cols] = True
+        for mask, sel_of, out, idx in ((mr, a, P1, rows), (mc, b, Q1, cols)):
+            sel = mask[sel_of]
+            if variant == "per_entry":
+                _, Po, Qo, _, _ = oracle.fit(a[sel], b[sel], v[sel], p.P0, p.Q0, 1, p.lam, p.lr, p.step, 2, p.xi)
+            else:
+                _, Po, Qo, _, _ = oracle.fit_mv(a[sel], b[sel], v[sel], p.P0, p.Q0, 1, p.lam, p.lr, sr, sc, sv, beta,
+                                                p.step, p.clip, p.xi)
+            ref = Po if out is P1 else Qo
+            assert rel_fro(out[idx], ref[idx]) <= 1e-4, (variant, rel_fro(out[idx], ref[idx]))
+    T.set_similarity(sr, sc, sv, 0.0)
