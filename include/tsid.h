@@ -372,8 +372,8 @@ tsid_status tsid_set_minibatch(tsid_ctx *ctx, int32_t n_batches, uint64_t seed);
  * memory), then one kernel that adds the n sums of each column in block order
  * and updates it.  The arithmetic is the same; the fp32 sums of a column are
  * added in another order.
- *  n_blocks = 0  (default) automatic: blocks of about 32 MiB of P when the
- *                table exceeds 96 MiB (Billion-scale: 8 blocks), else one.
+ *  n_blocks = 0  (default) automatic: blocks of about 16 MiB of P when the
+ *                table exceeds 96 MiB (Billion-scale: 16 blocks), else one.
  *  n_blocks = 1  off.   2 <= n_blocks <= TSID_MAX_ROW_BLOCKS: forced.
  * Applies to full-gradient fits whose Q pass runs the item pass.  Takes effect
  * at the next tsid_fit_template.  Errors: E_INVAL (ctx NULL, n_blocks out of

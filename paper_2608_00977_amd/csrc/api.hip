@@ -1215,7 +1215,7 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs, bool dense, i
 // Row blocks of the Q pass for this fit: automatic when the gathered P table
 // exceeds TSID_QBLOCK_MIN_MB (blocks of about TSID_QBLOCK_MB), else one.
 #ifndef TSID_QBLOCK_MB
-#define TSID_QBLOCK_MB 32
+#define TSID_QBLOCK_MB 16
 #endif
 #ifndef TSID_QBLOCK_MIN_MB
 #define TSID_QBLOCK_MIN_MB 96
