@@ -164,3 +164,31 @@ def test_row_blocks_repeatable_automatic_and_rejected(T):
     for bad in (-1, 65):
         with pytest.raises(tsid.TsidError):
             T.set_row_blocks(bad)
+
+
+def test_row_blocks_with_per_entry_clip_and_minibatch(T):
+    """The per-entry clip's sums go through the block partials and the
+    combine like the summed gradient's; mini-batch steps keep one pass."""
+    import torch
+    from paper_2608_00977_amd import make_opts
+    p = _case("ragged_k32")
+    T.build_template(p.m, p.n, p.u, p.i, p.r, p.I, p.J, p.k)
+    T.set_row_blocks(3)
+    try:
+        note("row blocks with the per-entry clip")
+        P = torch.from_numpy(np.ascontiguousarray(p.P0, np.float32)).cuda()
+        Q = torch.from_numpy(np.ascontiguousarray(p.Q0, np.float32)).cuda()
+        st, hist = T.fit_template(P, Q, make_opts(epochs=p.epochs, lam=p.lam, lr=p.lr, clip="per_entry", xi=0.05,
+                                                  step=p.step), raise_on_error=False)
+        assert st == 0 and T.row_blocks() == 3
+        T.set_minibatch(2, 3)
+        st2, *_ = _fit(T, p, epochs=1)
+        assert st2 == 0 and T.row_blocks() == 1
+    finally:
+        T.set_minibatch(0)
+        T.set_row_blocks(0)
+    _, _, a, b, v = oracle_template(p)
+    sto, Po, Qo, ho, _ = oracle.fit(a, b, v, p.P0, p.Q0, p.epochs, p.lam, p.lr, p.step, 2, 0.05)
+    assert sto == 0
+    assert rel_fro(P.cpu().numpy(), Po) <= FP32_TOL and rel_fro(Q.cpu().numpy(), Qo) <= FP32_TOL
+    np.testing.assert_allclose(hist, ho, rtol=LOSS_TRAJ_TOL)
