@@ -1591,6 +1591,9 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     SlabArgs sr = slab_args(t, 0, *o, c->err_dev), sc = slab_args(t, 1, *o, c->err_dev);
     sr.skip_after_nonfinite = sc.skip_after_nonfinite = 1;
     const SlabPlan &sp_r = t.slab[0], &sp_c = t.slab[1];
+    // Slab passes on both sides run as one launch per epoch (and their
+    // finishes as another): the Q pass reads only the old factors.
+    const bool slab_pair = sp_r.use && sp_c.use && !sim.on;
     const bool dn = t.dense_use && prec == TSID_BF16;
     DenseArgs dr = dense_args(t, 0, c->err_dev), dc = dense_args(t, 1, c->err_dev);
     dr.skip_after_nonfinite = dc.skip_after_nonfinite = 1;
@@ -1618,6 +1621,7 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
         // P pass (CSR): owner P_t, gathered Q_t
         float *e2 = want_loss ? f.e2 + slot * f.item_cap : nullptr;
         float *normp = want_loss ? f.normP + (int64_t)slot * t.m_t : nullptr;
+        float *normq = want_loss ? f.normQ + (int64_t)slot * t.n_t : nullptr;
         auto ev = timed(c, ep, TK_PPASS);
         if (sp_r.use) {
             sr.epoch = ep;
@@ -1626,10 +1630,27 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
             sr.Xn = f.P[nxt];
             sr.e2 = e2;
             sr.norm = normp;
-            launch_slab_pass(K, false, sr, sp_r.units(), cs, ev.first, ev.second);
-            if (sp_r.U > 1) {
-                ev = timed(c, ep, TK_PFIX);
-                launch_slab_finish(K, sr, cs, ev.first, ev.second);
+            if (slab_pair) {
+                sc.epoch = ep;
+                sc.X = f.Q[cur];
+                sc.Y = f.P[cur];
+                sc.Xn = f.Q[nxt];
+                sc.e2 = nullptr;
+                sc.norm = normq;
+                launch_slab_pass_pair(K, sr, sp_r.units(), sc, sp_c.units(), cs, ev.first, ev.second);
+                if (sp_r.U > 1 && sp_c.U > 1) {
+                    ev = timed(c, ep, TK_PFIX);
+                    launch_slab_finish_pair(K, sr, sc, cs, ev.first, ev.second);
+                } else if (sp_r.U > 1 || sp_c.U > 1) {
+                    ev = timed(c, ep, TK_PFIX);
+                    launch_slab_finish(K, sp_r.U > 1 ? sr : sc, cs, ev.first, ev.second);
+                }
+            } else {
+                launch_slab_pass(K, false, sr, sp_r.units(), cs, ev.first, ev.second);
+                if (sp_r.U > 1) {
+                    ev = timed(c, ep, TK_PFIX);
+                    launch_slab_finish(K, sr, cs, ev.first, ev.second);
+                }
             }
         } else {
             if (dn && dr.n_segs) {
@@ -1655,12 +1676,13 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
             }
         }
         // Q pass (CSC): owner Q_t, gathered P_t (the old P: a simultaneous step)
-        float *normq = want_loss ? f.normQ + (int64_t)slot * t.n_t : nullptr;
         if (sim.on)  // the similarity sums at Q_t, added to the Q gradients
             launch_sim_terms(K, sim.ptr, sim.col, sim.val, t.n_t, f.Q[cur], sim.gs,
                              want_loss ? sim.se + (int64_t)slot * t.n_t : nullptr, cs);
-        ev = timed(c, ep, TK_QPASS);
-        if (sp_c.use) {
+        ev = slab_pair ? std::pair<hipEvent_t, hipEvent_t>{} : timed(c, ep, TK_QPASS);
+        if (slab_pair) {
+            // launched with the P pass
+        } else if (sp_c.use) {
             sc.epoch = ep;
             sc.X = f.Q[cur];
             sc.Y = f.P[cur];

@@ -232,6 +232,13 @@ void launch_slab_pass(int K, bool loss_only, const SlabArgs &a, int64_t n_units,
                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 void launch_slab_finish(int K, const SlabArgs &a, hipStream_t s, hipEvent_t ev0 = nullptr,
                         hipEvent_t ev1 = nullptr);
+// The P pass (a0, n0 workgroups) and the Q pass (a1, n1) of one simultaneous
+// step in one launch (one slab size on both sides), and both finishes
+// (both sides with U > 1) in one launch.
+void launch_slab_pass_pair(int K, const SlabArgs &a0, int64_t n0, const SlabArgs &a1, int64_t n1, hipStream_t s,
+                           hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+void launch_slab_finish_pair(int K, const SlabArgs &a0, const SlabArgs &a1, hipStream_t s, hipEvent_t ev0 = nullptr,
+                             hipEvent_t ev1 = nullptr);
 
 // ------------------------------------------------- exact extension solve
 struct RidgeArgs {

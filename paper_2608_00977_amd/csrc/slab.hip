@@ -194,9 +194,9 @@ __device__ __forceinline__ void slab_burst(const int2 (&rec)[8], uint32_t j, uin
     }
 }
 
+// Workgroup u of one side's pass.
 template <int K, bool LOSS_ONLY>
-__global__ __launch_bounds__(kLanes) __attribute__((amdgpu_waves_per_eu(TSID_SLAB_WAVES_PER_EU)))
-void k_slab_pass(const SlabArgs A) {
+__device__ __forceinline__ void slab_pass_unit(const SlabArgs &A, const int u) {
     constexpr int NCH = K / 4;                        // 16-byte chunks per factor row
     constexpr int RM = (NCH < 8 ? NCH : 8) - 1;       // lane rotation mask
     static_assert((NCH & (NCH - 1)) == 0, "rows hold a power-of-two number of chunks");
@@ -206,7 +206,6 @@ void k_slab_pass(const SlabArgs A) {
         if (f != 0 && f - 1 < A.epoch) return;  // same outcome for every workgroup
     }
     const int tid = threadIdx.x;
-    const int u = blockIdx.x;
     const int U = A.units_per_block;
     const int blk = u / U, ur = u - blk * U;
     const int s0 = ur * A.slabs_per_unit;
@@ -296,19 +295,40 @@ void k_slab_pass(const SlabArgs A) {
     }
 }
 
+template <int K, bool LOSS_ONLY>
+__global__ __launch_bounds__(kLanes) __attribute__((amdgpu_waves_per_eu(TSID_SLAB_WAVES_PER_EU)))
+void k_slab_pass(const SlabArgs A) {
+    slab_pass_unit<K, LOSS_ONLY>(A, blockIdx.x);
+}
+
+// Both passes of a simultaneous step in one launch: they read only the old
+// factors and write disjoint outputs, so the n0 workgroups of the P pass
+// (A0) and then those of the Q pass (A1) share one grid, and the Q pass's
+// workgroups start as the P pass's leave the compute units instead of after
+// the whole P pass has drained.
+template <int K>
+__global__ __launch_bounds__(kLanes) __attribute__((amdgpu_waves_per_eu(TSID_SLAB_WAVES_PER_EU)))
+void k_slab_pass_pair(const SlabArgs A0, const SlabArgs A1, const int32_t n0) {
+    const int u = blockIdx.x;
+    if (u < n0)
+        slab_pass_unit<K, false>(A0, u);
+    else
+        slab_pass_unit<K, false>(A1, u - n0);
+}
+
 // Blocks split over U > 1 workgroups: the U partial sums of every row are
 // added in unit order, then the row takes the update of Eq. 5.  One lane per
 // 16-byte chunk of a row (NCH consecutive lanes per row), so every load is
 // coalesced and all U loads of a lane are in flight together.
+// Thread t of one side's finish (whole workgroups of 256 take one side).
 template <int K>
-__global__ __launch_bounds__(256) void k_slab_finish(const SlabArgs A) {
+__device__ __forceinline__ void slab_finish_lane(const SlabArgs &A, const int64_t t) {
     constexpr int NCH = K / 4;
     static_assert(NCH <= 64 && (64 % NCH) == 0, "a row's lanes sit inside one wave");
     if (A.skip_after_nonfinite) {
         const int32_t f = A.err[ERR_NONFINITE];
         if (f != 0 && f - 1 < A.epoch) return;
     }
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t xr = t / NCH;
     const int ch = (int)(t % NCH);
     const bool own = xr < A.rows;
@@ -366,6 +386,22 @@ __global__ __launch_bounds__(256) void k_slab_finish(const SlabArgs A) {
         if (A.norm && ch == 0) A.norm[xr] = nrm;
         if (bad) A.err[ERR_NONFINITE] = A.epoch + 1;
     }
+}
+
+template <int K>
+__global__ __launch_bounds__(256) void k_slab_finish(const SlabArgs A) {
+    slab_finish_lane<K>(A, (int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+}
+
+// The finishes of both passes in one launch: workgroups below b0 take the P
+// pass's rows, the rest the Q pass's.
+template <int K>
+__global__ __launch_bounds__(256) void k_slab_finish_pair(const SlabArgs A0, const SlabArgs A1, const int32_t b0) {
+    const int b = blockIdx.x;
+    if (b < b0)
+        slab_finish_lane<K>(A0, (int64_t)b * 256 + threadIdx.x);
+    else
+        slab_finish_lane<K>(A1, (int64_t)(b - b0) * 256 + threadIdx.x);
 }
 
 // seg[s * rows + x] = first cell of bucket x whose other index is >= s * C
@@ -442,6 +478,25 @@ void slab_finish_k(const SlabArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t 
     TSID_HIP(hipGetLastError());
 }
 
+template <int K>
+void slab_pass_pair_k(const SlabArgs &a0, int64_t n0, const SlabArgs &a1, int64_t n1, hipStream_t s,
+                      hipEvent_t ev0, hipEvent_t ev1) {
+    const size_t lds = (size_t)a0.C * K * 4;
+    static const bool lds_ok = (allow_lds(k_slab_pass_pair<K>, kSlabBytes), true);
+    (void)lds_ok;
+    hipExtLaunchKernelGGL(k_slab_pass_pair<K>, dim3((unsigned)(n0 + n1)), dim3(kLanes), lds, s, ev0, ev1, 0, a0,
+                          a1, (int32_t)n0);
+    TSID_HIP(hipGetLastError());
+}
+
+template <int K>
+void slab_finish_pair_k(const SlabArgs &a0, const SlabArgs &a1, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+    const int64_t b0 = ((int64_t)a0.rows * (K / 4) + 255) / 256, b1 = ((int64_t)a1.rows * (K / 4) + 255) / 256;
+    hipExtLaunchKernelGGL(k_slab_finish_pair<K>, dim3((unsigned)(b0 + b1)), dim3(256), 0, s, ev0, ev1, 0, a0, a1,
+                          (int32_t)b0);
+    TSID_HIP(hipGetLastError());
+}
+
 }  // namespace
 
 bool slab_supported(int K, int prec) {
@@ -473,6 +528,31 @@ void launch_slab_finish(int K, const SlabArgs &a, hipStream_t s, hipEvent_t ev0,
         case 16: slab_finish_k<16>(a, s, ev0, ev1); break;
         case 32: slab_finish_k<32>(a, s, ev0, ev1); break;
         case 64: slab_finish_k<64>(a, s, ev0, ev1); break;
+        default: fail(TSID_E_INVAL, "the slab pass supports k = 8, 16, 32, 64");
+    }
+}
+
+void launch_slab_pass_pair(int K, const SlabArgs &a0, int64_t n0, const SlabArgs &a1, int64_t n1, hipStream_t s,
+                           hipEvent_t ev0, hipEvent_t ev1) {
+    if (n0 <= 0 || n1 <= 0 || a0.C != a1.C || n0 + n1 > INT32_MAX)
+        fail(TSID_E_INVAL, "paired slab passes need workgroups on both sides and one slab size");
+    switch (K) {
+        case 8: slab_pass_pair_k<8>(a0, n0, a1, n1, s, ev0, ev1); break;
+        case 16: slab_pass_pair_k<16>(a0, n0, a1, n1, s, ev0, ev1); break;
+        case 32: slab_pass_pair_k<32>(a0, n0, a1, n1, s, ev0, ev1); break;
+        case 64: slab_pass_pair_k<64>(a0, n0, a1, n1, s, ev0, ev1); break;
+        default: fail(TSID_E_INVAL, "the slab pass supports k = 8, 16, 32, 64");
+    }
+}
+
+void launch_slab_finish_pair(int K, const SlabArgs &a0, const SlabArgs &a1, hipStream_t s, hipEvent_t ev0,
+                             hipEvent_t ev1) {
+    if (a0.rows <= 0 || a1.rows <= 0) fail(TSID_E_INVAL, "paired slab finishes need rows on both sides");
+    switch (K) {
+        case 8: slab_finish_pair_k<8>(a0, a1, s, ev0, ev1); break;
+        case 16: slab_finish_pair_k<16>(a0, a1, s, ev0, ev1); break;
+        case 32: slab_finish_pair_k<32>(a0, a1, s, ev0, ev1); break;
+        case 64: slab_finish_pair_k<64>(a0, a1, s, ev0, ev1); break;
         default: fail(TSID_E_INVAL, "the slab pass supports k = 8, 16, 32, 64");
     }
 }

@@ -187,3 +187,26 @@ def test_slab_nonfinite_returns_last_finite_iterate(T):
     assert np.array_equal(ref[1], P) and np.array_equal(ref[2], Q)
     assert np.all(np.isfinite(P)) and np.all(np.isfinite(Q))
     assert np.all(np.isnan(hist[done + 1:]))
+
+
+def test_slab_passes_share_one_launch(T):
+    """With the slab pass on both sides the P and Q passes of an epoch go out
+    as one launch, and their finishing kernels as another (the Q pass reads
+    only the old factors); the kernel timer sees one pass launch per timed
+    epoch, counted as the P pass, and one finish."""
+    p = _case("blocks_k32")
+    _build(T, p)
+    note("slab pair launch")
+    T.set_timing(2)
+    try:
+        st, P, Q, hist = gpu_fit(T, p, prec="fp32", epochs=6)
+        tm = T.timing()
+    finally:
+        T.set_timing(0)
+    assert st == 0 and T.pass_kernels() == ("slab", "slab")
+    assert tm["pass_launches"] == [3, 0] and tm["fixup_launches"] == 3 and tm["epochs"] == 3
+    assert tm["epoch_ms"] >= tm["pass_ms"][0] + tm["fixup_ms"] - 1e-3
+    _, _, a, b, v = oracle_template(p)
+    sto, Po, Qo, ho, _ = oracle.fit(a, b, v, p.P0, p.Q0, 6, p.lam, p.lr, p.step, p.clip, p.xi)
+    assert sto == 0 and rel_fro(P, Po) <= FP32_TOL and rel_fro(Q, Qo) <= FP32_TOL
+    np.testing.assert_allclose(hist, ho, rtol=LOSS_TRAJ_TOL)
