@@ -23,8 +23,9 @@ minutes to generate); mid / tiny are small.
 
 Roofline: the dominant kernel is the longer of the P and Q passes (the slab
 pass on evenly spread fp32 templates such as Scientific, else the item pass;
-when both sides run the slab pass the library launches the two as one kernel,
-k_slab_pass_pair, priced with both passes' bytes),
+the library launches the two passes of an epoch as one kernel,
+k_slab_pass_pair or k_item_pass_pair, priced with both passes' bytes, except
+when the Q pass runs in row blocks),
 timed with HIP events attached to its dispatches on the library's compute
 stream during the timed region (every --time-every-th epoch: a timed dispatch
 costs a few microseconds of wall time, which would otherwise slow the
@@ -362,16 +363,19 @@ def main():
              {"item": "fit.hip", "slab": "slab.hip"}[kernels[0]], "p_pass", kernels[0]),
             (avg[1], by[1], {"item": "k_item_pass", "slab": "k_slab_pass"}[kernels[1]], "Q pass",
              {"item": "fit.hip", "slab": "slab.hip"}[kernels[1]], "q_pass", kernels[1])]
-    # both slab passes in one launch (timed as the P pass; no Q pass launch)
-    slab_pair = tuple(kernels) == ("slab", "slab") and tm["pass_launches"][1] == 0 and tm["pass_launches"][0] > 0
-    if slab_pair:
-        cand = [(avg[0], by[0] + by[1], "k_slab_pass_pair", "P and Q passes", "slab.hip", "pq_pass", "slab")]
+    # both passes in one launch (timed as the P pass; no Q pass launch)
+    pair = kernels[0] == kernels[1] and tm["pass_launches"][1] == 0 and tm["pass_launches"][0] > 0
+    if pair:
+        cand = [(avg[0], by[0] + by[1], f"k_{kernels[0]}_pass_pair", "P and Q passes",
+                 {"item": "fit.hip", "slab": "slab.hip"}[kernels[0]], "pq_pass", kernels[0])]
     dense_avg = [tm["dense_ms"][j] / max(1, tm["dense_launches"][j]) for j in range(2)]
+    dcand = []
     if di["tiles"]:
         for j in range(2):
-            cand.append((dense_avg[j], dense_bytes(di["tiles"], di["stripes"][j], di["stripes"][1 - j], k),
-                         "k_dense_pass", ["P", "Q"][j] + " side dense tiles", "dense.hip",
-                         ["p_dense", "q_dense"][j], "dense"))
+            dcand.append((dense_avg[j], dense_bytes(di["tiles"], di["stripes"][j], di["stripes"][1 - j], k),
+                          "k_dense_pass", ["P", "Q"][j] + " side dense tiles", "dense.hip",
+                          ["p_dense", "q_dense"][j], "dense"))
+    cand += dcand
     dom_ms, dom_by, kname, kside, ksrc, which, kkind = max(cand, key=lambda c: c[0])
     achieved = dom_by / (dom_ms / 1e3) / 1e9
     src = open(os.path.join(ROOT, "paper_2608_00977_amd", "csrc", ksrc), "rb").read()
@@ -379,7 +383,7 @@ def main():
     variant = (f":minibatch{args.minibatch}" if args.minibatch else "") + (":clip2" if args.clip_per_entry else "") \
         + (":similarity" if args.similarity > 0 else "") + (f":rowblocks{row_blocks}" if row_blocks > 1 else "")
     traffic = traffic_from_profiles(sha, f"{args.config}:{which}:{kkind}" + variant)
-    epoch_bytes = by[0] + by[1] + (sum(c[1] for c in cand[2:]) if di["tiles"] else 0)
+    epoch_bytes = by[0] + by[1] + sum(c[1] for c in dcand)
     roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                 "kernel": f"{kname} ({kside})",
@@ -392,7 +396,7 @@ def main():
                  "flops_per_launch": fl,
                  "mfma_TFLOPs": [round(fl / (dense_avg[j] / 1e3) / 1e12, 2) if dense_avg[j] else None
                                  for j in range(2)],
-                 "bytes_per_launch": [cand[2][1], cand[3][1]]}
+                 "bytes_per_launch": [dcand[0][1], dcand[1][1]]}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -443,7 +447,7 @@ def main():
         "compulsory_GBps_per_epoch": round(epoch_bytes / (ms_per_step / 1e3) / 1e9, 2),
         "device_epoch_ms": tm["epoch_ms"] / max(1, tm["epochs"]),
         "timed_epochs": tm["epochs"],
-        "kernel_ms_per_epoch": {**({"pq_pass": avg[0]} if slab_pair else {"p_pass": avg[0], "q_pass": avg[1]}),
+        "kernel_ms_per_epoch": {**({"pq_pass": avg[0]} if pair else {"p_pass": avg[0], "q_pass": avg[1]}),
                                 "p_dense": dense_avg[0], "q_dense": dense_avg[1],
                                 "fixups": tm["fixup_ms"] / max(1, tm["epochs"]),
                                 "loss_reduce": tm["reduce_ms"] / max(1, tm["reduce_launches"]) / 16},

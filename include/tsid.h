@@ -393,9 +393,10 @@ tsid_status tsid_fit_row_blocks(const tsid_ctx *ctx, int32_t *n_blocks);
  * time, so timing a sample of the epochs keeps the fit's own throughput
  * nearly unchanged.  every = 0 turns timing off.
  *  pass_ms[0] / pass_launches[0]: the P pass (row buckets); [1]: the Q pass
- *  (column buckets).  When both sides run the slab pass, the two passes of
- *  an epoch are one launch, counted in [0] ([1] stays 0), and their two
- *  finishing kernels one launch, counted once under fixup.  fixup: the kernels that combine partial sums after a
+ *  (column buckets).  The two passes of an epoch go out as one launch,
+ *  counted in [0] ([1] stays 0), unless the Q pass runs in row blocks
+ *  (tsid_set_row_blocks); the slab pass's two finishing kernels are then one
+ *  launch too, counted once under fixup.  fixup: the kernels that combine partial sums after a
  *  pass (item pass: buckets longer than one wave; slab pass: blocks split
  *  over several workgroups), which also update those rows; reduce: the
  *  batched loss reductions (one per 16 epochs); dense_ms[0] / [1]: the

@@ -331,11 +331,18 @@ void collect_timing(tsid_ctx *c, int epochs) {
             }
         }
         if (!(l & (1u << TK_PPASS)) || (l & (1u << TK_EPOCH))) continue;  // not a sampled Jacobi epoch
-        // an epoch runs dense P, P pass, P fixup, dense Q, Q pass, Q fixup in that order
-        const int first = (l & (1u << TK_PDENSE)) ? (int)TK_PDENSE : (int)TK_PPASS;
-        int end_k = TK_PPASS;
-        for (int k : {TK_PPASS, TK_PFIX, TK_QDENSE, TK_QPASS, TK_QFIX})
-            if (l & (1u << k)) end_k = k;
+        // an epoch runs dense P, P pass, P fixup, dense Q, Q pass, Q fixup in
+        // that order; with both passes in one launch (no Q pass launch of its
+        // own): dense P, dense Q, both passes, P fixup, Q fixup
+        static const int order1[] = {TK_PDENSE, TK_PPASS, TK_PFIX, TK_QDENSE, TK_QPASS, TK_QFIX};
+        static const int order2[] = {TK_PDENSE, TK_QDENSE, TK_PPASS, TK_PFIX, TK_QFIX, TK_QFIX};
+        const int *order = (l & (1u << TK_QPASS)) ? order1 : order2;
+        int first = -1, end_k = -1;
+        for (int j = 0; j < 6; ++j)
+            if (l & (1u << order[j])) {
+                if (first < 0) first = order[j];
+                end_k = order[j];
+            }
         t.epoch_ms += dt(ev(ep, first, 0), ev(ep, end_k, 1));
         t.epochs += 1;
     }
@@ -1594,6 +1601,9 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     // Slab passes on both sides run as one launch per epoch (and their
     // finishes as another): the Q pass reads only the old factors.
     const bool slab_pair = sp_r.use && sp_c.use && !sim.on;
+    // Likewise the item passes (after both sides' dense-tile launches), unless
+    // the Q pass runs in row blocks.
+    const bool item_pair = !sp_r.use && !sp_c.use && nb <= 1;
     const bool dn = t.dense_use && prec == TSID_BF16;
     DenseArgs dr = dense_args(t, 0, c->err_dev), dc = dense_args(t, 1, c->err_dev);
     dr.skip_after_nonfinite = dc.skip_after_nonfinite = 1;
@@ -1669,17 +1679,20 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
             ar.carry = f.carry_r;
             ar.e2 = e2;
             ar.norm = normp;
-            launch_item_pass(K, prec, false, ar, cs, ev.first, ev.second);
-            if ((dn ? t.dense.plan[0] : t.plan[0][prec]).spans) {
-                ev = timed(c, ep, TK_PFIX);
-                launch_fixup(K, prec, ar, cs, ev.first, ev.second);
+            if (!item_pair) {  // else launched with the Q pass
+                launch_item_pass(K, prec, false, ar, cs, ev.first, ev.second);
+                if ((dn ? t.dense.plan[0] : t.plan[0][prec]).spans) {
+                    ev = timed(c, ep, TK_PFIX);
+                    launch_fixup(K, prec, ar, cs, ev.first, ev.second);
+                }
             }
         }
+        const auto ev_p = ev;
         // Q pass (CSC): owner Q_t, gathered P_t (the old P: a simultaneous step)
         if (sim.on)  // the similarity sums at Q_t, added to the Q gradients
             launch_sim_terms(K, sim.ptr, sim.col, sim.val, t.n_t, f.Q[cur], sim.gs,
                              want_loss ? sim.se + (int64_t)slot * t.n_t : nullptr, cs);
-        ev = slab_pair ? std::pair<hipEvent_t, hipEvent_t>{} : timed(c, ep, TK_QPASS);
+        ev = slab_pair || item_pair ? std::pair<hipEvent_t, hipEvent_t>{} : timed(c, ep, TK_QPASS);
         if (slab_pair) {
             // launched with the P pass
         } else if (sp_c.use) {
@@ -1731,6 +1744,16 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
                     if (pl.spans) launch_fixup(K, prec, bj, cs);
                 }
                 launch_block_combine(K, prec, ac, t.qb.part, nb, cs, nullptr, ev.second);
+            } else if (item_pair) {
+                launch_item_pass_pair(K, prec, ar, ac, cs, ev_p.first, ev_p.second);
+                if ((dn ? t.dense.plan[0] : t.plan[0][prec]).spans) {
+                    ev = timed(c, ep, TK_PFIX);
+                    launch_fixup(K, prec, ar, cs, ev.first, ev.second);
+                }
+                if ((dn ? t.dense.plan[1] : t.plan[1][prec]).spans) {
+                    ev = timed(c, ep, TK_QFIX);
+                    launch_fixup(K, prec, ac, cs, ev.first, ev.second);
+                }
             } else {
                 launch_item_pass(K, prec, false, ac, cs, ev.first, ev.second);
                 if ((dn ? t.dense.plan[1] : t.plan[1][prec]).spans) {

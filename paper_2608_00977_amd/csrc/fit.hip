@@ -406,15 +406,16 @@ __device__ __forceinline__ void process_block(const PassArgs &A, const YTable &Y
 #define TSID_OCCUPANCY
 #endif
 
-template <int K, int V, bool BF16, bool LOSS_ONLY, bool BUF, bool PE = false>
-__global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass(const PassArgs A) {
+// Workgroup `bid` of one side's item pass.
+template <int K, int V, bool BF16, bool LOSS_ONLY, bool BUF, bool PE>
+__device__ __forceinline__ void item_pass_group(const PassArgs &A, const int64_t bid) {
     constexpr int G = K / V;
     constexpr int NG = 64 / G;
     static_assert(G >= 1 && G <= 16 && (G & (G - 1)) == 0, "group must fit a DPP row");
     if (skip_epoch(A)) return;
     const int lane = threadIdx.x & 63;
     const int grp = lane / G, lg = lane % G;
-    const int64_t item = ((int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6)) * NG + grp;
+    const int64_t item = (bid * kWaves + (threadIdx.x >> 6)) * NG + grp;
     const int64_t n_items = A.n_items_dev ? (int64_t)*A.n_items_dev : (int64_t)A.n_items;
     if (item >= n_items) return;  // whole groups leave together
     const int row = A.items[item];  // -1: a pad item that keeps buckets wave-aligned
@@ -524,6 +525,25 @@ __global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass(const Pas
             }
         }
     }
+}
+
+template <int K, int V, bool BF16, bool LOSS_ONLY, bool BUF, bool PE = false>
+__global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass(const PassArgs A) {
+    item_pass_group<K, V, BF16, LOSS_ONLY, BUF, PE>(A, blockIdx.x);
+}
+
+// Both passes of a simultaneous step in one launch: the Q pass reads only the
+// old factors, so the b0 workgroups of the P pass (A0) and then those of the
+// Q pass (A1) share one grid, and the Q pass's workgroups start as the P
+// pass's leave the compute units.
+template <int K, int V, bool BF16, bool BUF, bool PE>
+__global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass_pair(const PassArgs A0, const PassArgs A1,
+                                                                           const int32_t b0) {
+    const int b = blockIdx.x;
+    if (b < b0)
+        item_pass_group<K, V, BF16, false, BUF, PE>(A0, b);
+    else
+        item_pass_group<K, V, BF16, false, BUF, PE>(A1, b - b0);
 }
 
 // Split buckets: add the item partial sums in item order, then update the row.
@@ -782,6 +802,34 @@ void item_pass_kv(bool loss_only, const PassArgs &a, hipStream_t s, hipEvent_t e
     TSID_HIP(hipGetLastError());
 }
 
+// Both sides' passes in one launch when their gathers use the same addressing;
+// else two launches (ev0 on the first, ev1 on the second).
+template <int K, int V, bool BF16>
+void item_pass_pair_kv(const PassArgs &a0, const PassArgs &a1, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+    constexpr int NG = 64 / (K / V);
+    const int64_t g0 = ceil_div(a0.n_items, (int64_t)kWaves * NG), g1 = ceil_div(a1.n_items, (int64_t)kWaves * NG);
+    const int64_t elt = BF16 ? 2 : 4;
+    const bool buf0 = a0.y_rows * (int64_t)K * elt < (int64_t(1) << 31);
+    const bool buf1 = a1.y_rows * (int64_t)K * elt < (int64_t(1) << 31);
+    if (g0 <= 0 || g1 <= 0 || buf0 != buf1 || a0.clip != a1.clip || g0 + g1 > INT32_MAX) {
+        item_pass_kv<K, V, BF16>(false, a0, s, ev0, nullptr);
+        item_pass_kv<K, V, BF16>(false, a1, s, nullptr, ev1);
+        return;
+    }
+    auto go = [&](auto kernel) {
+        hipExtLaunchKernelGGL(kernel, dim3((unsigned)(g0 + g1)), dim3(kThreads), 0, s, ev0, ev1, 0, a0, a1,
+                              (int32_t)g0);
+    };
+    if (a0.clip == 2) {
+        if (buf0) go(k_item_pass_pair<K, V, BF16, true, true>);
+        else go(k_item_pass_pair<K, V, BF16, false, true>);
+    } else {
+        if (buf0) go(k_item_pass_pair<K, V, BF16, true, false>);
+        else go(k_item_pass_pair<K, V, BF16, false, false>);
+    }
+    TSID_HIP(hipGetLastError());
+}
+
 template <int K, int V, bool BF16>
 void extend_steps_kv(const PassArgs &a, int32_t steps, hipStream_t s) {
     if constexpr (BF16) {
@@ -859,6 +907,11 @@ void fixup_kv(const PassArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) 
 void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStream_t s,
                       hipEvent_t ev0, hipEvent_t ev1) {
     TSID_DISPATCH_K(K, item_pass_kv, loss_only, a, s, ev0, ev1)
+}
+
+void launch_item_pass_pair(int K, int prec, const PassArgs &a0, const PassArgs &a1, hipStream_t s, hipEvent_t ev0,
+                           hipEvent_t ev1) {
+    TSID_DISPATCH_K(K, item_pass_pair_kv, a0, a1, s, ev0, ev1)
 }
 
 void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {

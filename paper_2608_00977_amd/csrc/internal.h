@@ -142,6 +142,10 @@ struct PassArgs {
 // timestamps (attached to its dispatch; no extra packets on the stream).
 void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStream_t s,
                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+// The P pass (a0) and the Q pass (a1) of one simultaneous step in one launch
+// (full-gradient, not loss-only; two launches if the sides' gathers differ).
+void launch_item_pass_pair(int K, int prec, const PassArgs &a0, const PassArgs &a1, hipStream_t s,
+                           hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s, hipEvent_t ev0 = nullptr,
                   hipEvent_t ev1 = nullptr);
 // Row blocks of a bucketed stream: bounds[j * rows + x] = first cell of bucket
