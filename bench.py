@@ -56,8 +56,8 @@ HBM_PEAK_GBPS = 8000.0
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--config", default="scientific", choices=["scientific", "rating", "billion", "mid", "tiny"])
     ap.add_argument("--pass-kernel", default="auto", choices=["auto", "item", "slab"],
                     help="kernel of the P and Q passes (tsid_set_pass_kernel); auto picks the "

@@ -252,7 +252,9 @@ struct tsid_ctx {
     int32_t epochs_done = 0;         // of the last fit
     int32_t timing = 0;              // time every timing-th epoch (0: off)
     tsid_timing tm{};
-    std::vector<hipEvent_t> events;  // kernel timestamps, kEvents per epoch
+    std::vector<hipEvent_t> events;  // pool of timing events (created by tsid_set_timing, grown on demand)
+    size_t events_used = 0;          // pool events handed out in the current fit
+    std::vector<hipEvent_t> ev_slot; // this fit's events, kEvents per epoch (null: not timed)
     std::vector<uint8_t> launched;   // which kernel kinds each timed epoch ran
     FitBufs fb;
     ExtState ext;
@@ -279,12 +281,21 @@ enum TimedKernel {
 };
 constexpr int kEvents = 2 * kTimed;
 
-void ensure_events(tsid_ctx *c, size_t epochs) {
-    while (c->events.size() < epochs * kEvents) {
+// Events a fit can draw before the pool grows: created when timing is
+// switched on, so that a timed fit creates none while it runs.
+constexpr size_t kEventPool = 1024;
+
+void grow_events(tsid_ctx *c, size_t n) {
+    while (c->events.size() < n) {
         hipEvent_t e;
         TSID_HIP(hipEventCreate(&e));
         c->events.push_back(e);
     }
+}
+
+void ensure_events(tsid_ctx *c, size_t epochs) {
+    c->ev_slot.assign(epochs * kEvents, nullptr);
+    c->events_used = 0;
     c->launched.assign(epochs, 0);
 }
 
@@ -296,11 +307,16 @@ std::pair<hipEvent_t, hipEvent_t> timed(tsid_ctx *c, int ep, int k) {
     if (k != TK_REDUCE && ep % c->timing != 0) return {nullptr, nullptr};
     c->launched[(size_t)ep] |= (uint8_t)(1u << k);
     const size_t b = (size_t)ep * kEvents + 2 * k;
-    return {c->events[b], c->events[b + 1]};
+    if (!c->ev_slot[b]) {  // a pair from the pool (reused if the kernel kind repeats in this epoch)
+        grow_events(c, c->events_used + 2);
+        c->ev_slot[b] = c->events[c->events_used++];
+        c->ev_slot[b + 1] = c->events[c->events_used++];
+    }
+    return {c->ev_slot[b], c->ev_slot[b + 1]};
 }
 
 void collect_timing(tsid_ctx *c, int epochs) {
-    auto ev = [&](int ep, int k, int end) { return c->events[(size_t)ep * kEvents + 2 * k + end]; };
+    auto ev = [&](int ep, int k, int end) { return c->ev_slot[(size_t)ep * kEvents + 2 * k + end]; };
     auto dt = [&](hipEvent_t a, hipEvent_t b) {
         float ms = 0.f;
         TSID_HIP(hipEventElapsedTime(&ms, a, b));
@@ -1212,10 +1228,11 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs, bool dense, i
             f.Qb[b] = A.alloc<uint16_t>(lq);
         }
     }
-    if (f.loss_cap < epochs + 1) {
+    if (f.loss_cap < epochs + 1) {  // at least 4096 epochs, so that later fits rarely reallocate
         A.release(f.loss);
-        f.loss = A.alloc<double>(epochs + 1);
-        f.loss_cap = epochs + 1;
+        const int32_t cap = std::max<int32_t>(epochs + 1, 4096);
+        f.loss = A.alloc<double>(cap);
+        f.loss_cap = cap;
     }
 }
 
@@ -2270,9 +2287,11 @@ tsid_status tsid_fit_dense_info(const tsid_ctx *c, tsid_dense_info *out) {
 
 tsid_status tsid_set_timing(tsid_ctx *c, int every) {
     if (!c || every < 0) return TSID_E_INVAL;
-    c->timing = every;
-    c->tm = tsid_timing{};
-    return TSID_OK;
+    return guarded(c, [&] {
+        if (every > 0) grow_events(c, kEventPool);
+        c->timing = every;
+        c->tm = tsid_timing{};
+    });
 }
 
 tsid_status tsid_get_timing(const tsid_ctx *c, tsid_timing *out) {
