@@ -370,7 +370,13 @@ def main():
                  {"item": "fit.hip", "slab": "slab.hip"}[kernels[0]], "pq_pass", kernels[0])]
     dense_avg = [tm["dense_ms"][j] / max(1, tm["dense_launches"][j]) for j in range(2)]
     dcand = []
-    if di["tiles"]:
+    # both sides' dense tiles in one launch (timed as the P side's)
+    dense_pair = di["tiles"] and tm["dense_launches"][1] == 0 and tm["dense_launches"][0] > 0
+    if dense_pair:
+        dcand.append((dense_avg[0], sum(dense_bytes(di["tiles"], di["stripes"][j], di["stripes"][1 - j], k)
+                                        for j in range(2)),
+                      "k_dense_pass_pair", "P and Q side dense tiles", "dense.hip", "pq_dense", "dense"))
+    elif di["tiles"]:
         for j in range(2):
             dcand.append((dense_avg[j], dense_bytes(di["tiles"], di["stripes"][j], di["stripes"][1 - j], k),
                           "k_dense_pass", ["P", "Q"][j] + " side dense tiles", "dense.hip",
@@ -394,9 +400,9 @@ def main():
         dense = {"cells": di["cells"], "tiles": di["tiles"], "stripes": di["stripes"],
                  "share_of_cells": round(di["cells"] / max(1, nnz), 4),
                  "flops_per_launch": fl,
-                 "mfma_TFLOPs": [round(fl / (dense_avg[j] / 1e3) / 1e12, 2) if dense_avg[j] else None
-                                 for j in range(2)],
-                 "bytes_per_launch": [dcand[0][1], dcand[1][1]]}
+                 "mfma_TFLOPs": [round(fl * (2 if dense_pair else 1) / (c[0] / 1e3) / 1e12, 2) if c[0] else None
+                                 for c in dcand],
+                 "bytes_per_launch": [c[1] for c in dcand], "launches_per_epoch": len(dcand)}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -448,7 +454,8 @@ def main():
         "device_epoch_ms": tm["epoch_ms"] / max(1, tm["epochs"]),
         "timed_epochs": tm["epochs"],
         "kernel_ms_per_epoch": {**({"pq_pass": avg[0]} if pair else {"p_pass": avg[0], "q_pass": avg[1]}),
-                                "p_dense": dense_avg[0], "q_dense": dense_avg[1],
+                                **({"pq_dense": dense_avg[0]} if dense_pair else
+                                   {"p_dense": dense_avg[0], "q_dense": dense_avg[1]}),
                                 "fixups": tm["fixup_ms"] / max(1, tm["epochs"]),
                                 "loss_reduce": tm["reduce_ms"] / max(1, tm["reduce_launches"]) / 16},
         "loss_first_epoch": float(hist[0]),

@@ -396,11 +396,13 @@ tsid_status tsid_fit_row_blocks(const tsid_ctx *ctx, int32_t *n_blocks);
  *  (column buckets).  The two passes of an epoch go out as one launch,
  *  counted in [0] ([1] stays 0), unless the Q pass runs in row blocks
  *  (tsid_set_row_blocks); the slab pass's two finishing kernels are then one
- *  launch too, counted once under fixup.  fixup: the kernels that combine partial sums after a
- *  pass (item pass: buckets longer than one wave; slab pass: blocks split
+ *  launch too, counted once under fixup.  fixup: the kernels that combine
+ *  partial sums after a pass (item pass: buckets longer than one wave; slab pass: blocks split
  *  over several workgroups), which also update those rows; reduce: the
  *  batched loss reductions (one per 16 epochs); dense_ms[0] / [1]: the
- *  dense-tile kernels before the P / Q pass (tsid_set_dense_tiles);
+ *  dense-tile kernels before the P / Q pass (tsid_set_dense_tiles); when
+ *  the passes share a launch, both sides' tiles share one too, counted in
+ *  [0];
  *  epoch_ms: from the start of a timed epoch's first kernel to the end of
  *  its last, summed over the timed epochs, whose number is `epochs`.
  * Errors: E_INVAL (ctx NULL or every < 0). */

@@ -1680,7 +1680,17 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
                 }
             }
         } else {
-            if (dn && dr.n_segs) {
+            if (dn && item_pair && (dr.n_segs || dc.n_segs)) {  // both sides' tiles in one launch
+                dr.epoch = dc.epoch = ep;
+                dr.X = f.Pb[cur];
+                dr.Y = f.Qb[cur];
+                dr.e2 = e2 ? e2 + ne_items : nullptr;
+                dc.X = f.Qb[cur];
+                dc.Y = f.Pb[cur];
+                dc.e2 = nullptr;
+                auto evd = timed(c, ep, TK_PDENSE);
+                launch_dense_pass_pair(K, dr, dc, cs, evd.first, evd.second);
+            } else if (dn && dr.n_segs) {
                 dr.epoch = ep;
                 dr.X = f.Pb[cur];
                 dr.Y = f.Qb[cur];
@@ -1725,7 +1735,7 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
                 launch_slab_finish(K, sc, cs, ev.first, ev.second);
             }
         } else {
-            if (dn && dc.n_segs) {
+            if (dn && dc.n_segs && !item_pair) {
                 dc.epoch = ep;
                 dc.X = f.Qb[cur];
                 dc.Y = f.Pb[cur];

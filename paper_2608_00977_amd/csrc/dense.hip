@@ -171,8 +171,9 @@ __device__ __forceinline__ void dense_tile(const bf8 (&yraw)[DenseShape<K>::NC],
 #define TSID_DENSE_OCC
 #endif
 
+// Workgroup `bid` of one side's tile pass.
 template <int K, bool LOSS_ONLY>
-__global__ __launch_bounds__(64 * kDenseWaves) TSID_DENSE_OCC void k_dense_pass(const DenseArgs A) {
+__device__ __forceinline__ void dense_pass_group(const DenseArgs &A, const int64_t bid) {
     using D = DenseShape<K>;
     static_assert(K % 16 == 0, "dense tiles need k a multiple of 16");
     if (A.skip_after_nonfinite) {
@@ -181,7 +182,7 @@ __global__ __launch_bounds__(64 * kDenseWaves) TSID_DENSE_OCC void k_dense_pass(
     }
     __shared__ uint16_t ylds[kDenseWaves][16 * D::ROW];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int64_t g = (int64_t)blockIdx.x * kDenseWaves + wv;  // segment
+    const int64_t g = bid * kDenseWaves + wv;  // segment
     if (g >= A.n_segs) return;  // whole waves leave together
     const uint32_t t_beg = A.seg_tile[g], t_end = A.seg_tile[g + 1];  // at least one tile
     const uint32_t last = t_end - 1;
@@ -246,16 +247,35 @@ __global__ __launch_bounds__(64 * kDenseWaves) TSID_DENSE_OCC void k_dense_pass(
     }
 }
 
+template <int K, bool LOSS_ONLY>
+__global__ __launch_bounds__(64 * kDenseWaves) TSID_DENSE_OCC void k_dense_pass(const DenseArgs A) {
+    dense_pass_group<K, LOSS_ONLY>(A, blockIdx.x);
+}
+
+// Both sides' tile passes in one launch (they read only the old factors and
+// write disjoint sums): the b0 workgroups of the P side (A0), then the Q
+// side's (A1).
+template <int K>
+__global__ __launch_bounds__(64 * kDenseWaves) TSID_DENSE_OCC void k_dense_pass_pair(const DenseArgs A0,
+                                                                                    const DenseArgs A1,
+                                                                                    const int32_t b0) {
+    const int b = blockIdx.x;
+    if (b < b0)
+        dense_pass_group<K, false>(A0, b);
+    else
+        dense_pass_group<K, false>(A1, b - b0);
+}
+
 // Gradient sums of the stripes split into several segments: the segments'
 // partial sums added in segment order (one workgroup per such stripe, one
 // lane per 4 coordinates of a row).
 template <int K>
-__global__ __launch_bounds__(256) void k_dense_combine(const DenseArgs A) {
+__device__ __forceinline__ void dense_combine_group(const DenseArgs &A, const int64_t bid) {
     if (A.skip_after_nonfinite) {
         const int32_t f = A.err[ERR_NONFINITE];
         if (f != 0 && f - 1 < A.epoch) return;
     }
-    const int64_t s = A.multi[blockIdx.x], o0 = s * 16;
+    const int64_t s = A.multi[bid], o0 = s * 16;
     const uint32_t g0 = A.stripe_seg[s], g1 = A.stripe_seg[s + 1];
     for (int idx = threadIdx.x; idx < 16 * K / 4; idx += 256) {
         const int row = idx / (K / 4), c = (idx % (K / 4)) * 4;
@@ -284,6 +304,21 @@ __global__ __launch_bounds__(256) void k_dense_combine(const DenseArgs A) {
         }
         *reinterpret_cast<float4 *>(A.gd + (o0 + row) * K + c) = acc;
     }
+}
+
+template <int K>
+__global__ __launch_bounds__(256) void k_dense_combine(const DenseArgs A) {
+    dense_combine_group<K>(A, blockIdx.x);
+}
+
+// Both sides' combines in one launch (the P side's b0 stripes first).
+template <int K>
+__global__ __launch_bounds__(256) void k_dense_combine_pair(const DenseArgs A0, const DenseArgs A1, const int32_t b0) {
+    const int b = blockIdx.x;
+    if (b < b0)
+        dense_combine_group<K>(A0, b);
+    else
+        dense_combine_group<K>(A1, b - b0);
 }
 
 // ---------------------------------------------------------------- build
@@ -399,7 +434,42 @@ void dense_pass_k(bool loss_only, const DenseArgs &a, hipStream_t s, hipEvent_t 
     }
 }
 
+// Both sides' tile passes, then both combines (ev0 at the first launch's
+// start, ev1 at the last one's end); a side without segments runs alone.
+template <int K>
+void dense_pass_pair_k(const DenseArgs &a0, const DenseArgs &a1, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+    if (a0.n_segs <= 0 || a1.n_segs <= 0) {
+        if (a0.n_segs > 0) dense_pass_k<K>(false, a0, s, ev0, ev1);
+        if (a1.n_segs > 0) dense_pass_k<K>(false, a1, s, ev0, ev1);
+        return;
+    }
+    const int64_t g0 = (a0.n_segs + kDenseWaves - 1) / kDenseWaves, g1 = (a1.n_segs + kDenseWaves - 1) / kDenseWaves;
+    if (g0 + g1 > INT32_MAX || a0.n_multi + a1.n_multi > INT32_MAX) fail(TSID_E_INVAL, "too many tile segments");
+    const bool c0 = a0.n_multi > 0, c1 = a1.n_multi > 0;
+    hipExtLaunchKernelGGL(k_dense_pass_pair<K>, dim3((unsigned)(g0 + g1)), dim3(64 * kDenseWaves), 0, s, ev0,
+                          (c0 || c1) ? nullptr : ev1, 0, a0, a1, (int32_t)g0);
+    TSID_HIP(hipGetLastError());
+    if (c0 && c1)
+        hipExtLaunchKernelGGL(k_dense_combine_pair<K>, dim3((unsigned)(a0.n_multi + a1.n_multi)), dim3(256), 0, s,
+                              nullptr, ev1, 0, a0, a1, (int32_t)a0.n_multi);
+    else if (c0 || c1)
+        hipExtLaunchKernelGGL(k_dense_combine<K>, dim3((unsigned)(c0 ? a0.n_multi : a1.n_multi)), dim3(256), 0, s,
+                              nullptr, ev1, 0, c0 ? a0 : a1);
+    TSID_HIP(hipGetLastError());
+}
+
 }  // namespace
+
+void launch_dense_pass_pair(int K, const DenseArgs &a0, const DenseArgs &a1, hipStream_t s, hipEvent_t ev0,
+                            hipEvent_t ev1) {
+    switch (K) {
+        case 16: dense_pass_pair_k<16>(a0, a1, s, ev0, ev1); break;
+        case 32: dense_pass_pair_k<32>(a0, a1, s, ev0, ev1); break;
+        case 64: dense_pass_pair_k<64>(a0, a1, s, ev0, ev1); break;
+        case 128: dense_pass_pair_k<128>(a0, a1, s, ev0, ev1); break;
+        default: fail(TSID_E_INVAL, "dense tiles need k in {16, 32, 64, 128}");
+    }
+}
 
 bool dense_supported(int K, int prec) { return prec == TSID_BF16 && K >= 16 && K % 16 == 0 && K <= 128; }
 

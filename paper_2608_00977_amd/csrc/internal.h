@@ -315,6 +315,10 @@ struct DenseArgs {
 bool dense_supported(int K, int prec);
 // The tile kernel, then (when a stripe has several segments) the kernel that
 // adds their partial sums in segment order; ev0 / ev1 bracket both.
+// Both sides' tile passes (and combines) of one simultaneous step in one
+// launch each (full-gradient, not loss-only).
+void launch_dense_pass_pair(int K, const DenseArgs &a0, const DenseArgs &a1, hipStream_t s, hipEvent_t ev0 = nullptr,
+                            hipEvent_t ev1 = nullptr);
 void launch_dense_pass(int K, bool loss_only, const DenseArgs &a, hipStream_t s, hipEvent_t ev0 = nullptr,
                        hipEvent_t ev1 = nullptr);
 // Build steps (see dense.hip).  Tiles: t = ti * n_tj + tj over 16 x 16 blocks.

@@ -278,8 +278,9 @@ def test_dense_timing_reports_dense_kernels(T):
     finally:
         T.set_timing(0)
         T.set_dense_tiles(-1)
-    assert tm["dense_launches"] == [3, 3]
-    assert tm["pass_launches"] == [3, 0]  # the item passes of an epoch share one launch
-    assert tm["dense_ms"][0] > 0 and tm["dense_ms"][1] > 0
+    # both sides' tiles share one launch (and their combines another), as do the item passes
+    assert tm["dense_launches"] == [3, 0]
+    assert tm["pass_launches"] == [3, 0]
+    assert tm["dense_ms"][0] > 0
     assert tm["epochs"] == 3
     assert tm["epoch_ms"] >= tm["dense_ms"][0] + tm["pass_ms"][0] + tm["pass_ms"][1] + tm["dense_ms"][1] - 1e-3
