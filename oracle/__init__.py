@@ -80,7 +80,10 @@ def _c(x, dtype):
     return np.ascontiguousarray(x, dtype=dtype)
 
 
-STEP = {"sum": 0, "degree": 1}
+STEP = {"sum": 0, "degree": 1, "col_degree": 2}
+# clip option: False / True (1, on the normalised direction), "per_entry" (2),
+# "printed" (3, on the summed direction before the step normalisation)
+CLIP = {False: 0, True: 1, 0: 0, 1: 1, 2: 2, 3: 3, "per_entry": 2, "printed": 3}
 
 
 def template_maps(m, n, I, J):
@@ -134,7 +137,7 @@ def fit(a, b, v, P0, Q0, epochs, lam, lr, step="sum", clip=False, xi=0.1, bf16=F
     hist = np.full(epochs + 1, np.nan)
     done = np.zeros(1, np.int32)
     st = lib().or_fit(a.size, _p(a), _p(b), _p(v), P.shape[0], Q.shape[0], P.shape[1], _p(P),
-                      _p(Q), epochs, lam, lr, STEP[step], int(clip), xi, int(bf16), _p(hist),
+                      _p(Q), epochs, lam, lr, STEP[step], CLIP[clip], xi, int(bf16), _p(hist),
                       _p(done))
     return st, P, Q, hist, int(done[0])
 
@@ -157,7 +160,7 @@ def fit_mv(a, b, v, P0, Q0, epochs, lam, lr, s_row, s_col, s_val, beta, step="su
     hist = np.full(epochs + 1, np.nan)
     done = np.zeros(1, np.int32)
     st = lib().or_fit_mv(a.size, _p(a), _p(b), _p(v), P.shape[0], Q.shape[0], P.shape[1], _p(P), _p(Q), epochs,
-                         lam, lr, STEP[step], int(clip), xi, int(bf16), s_val.size, _p(s_row), _p(s_col),
+                         lam, lr, STEP[step], CLIP[clip], xi, int(bf16), s_val.size, _p(s_row), _p(s_col),
                          _p(s_val), beta, _p(hist), _p(done))
     return st, P, Q, hist, int(done[0])
 
@@ -194,7 +197,7 @@ def fit_minibatch(a, b, v, P0, Q0, epochs, lam, lr, step="sum", clip=False, xi=0
     hist = np.full(epochs + 1, np.nan)
     done = np.zeros(1, np.int32)
     st = lib().or_fit_minibatch(a.size, _p(a), _p(b), _p(v), P.shape[0], Q.shape[0], P.shape[1], _p(P),
-                                _p(Q), epochs, lam, lr, STEP[step], int(clip), xi, int(bf16), n_batches,
+                                _p(Q), epochs, lam, lr, STEP[step], CLIP[clip], xi, int(bf16), n_batches,
                                 C.c_uint64(seed), _p(hist), _p(done))
     return st, P, Q, hist, int(done[0])
 
@@ -206,7 +209,7 @@ def extend(fixed_id, free_id, v, n_free, F_fixed, steps, lam, lr, step="degree",
     k = F.shape[1]
     X = np.zeros((n_free, k), np.float64)
     st = lib().or_extend(v.size, _p(fixed_id), _p(free_id), _p(v), n_free, k, _p(F), _p(X),
-                         steps, lam, lr, STEP[step], int(clip), xi)
+                         steps, lam, lr, STEP[step], CLIP[clip], xi)
     return st, X
 
 

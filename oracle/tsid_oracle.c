@@ -13,11 +13,15 @@
  *  - the update moves against the gradient of Eqs. 3-4 (descent), applied to
  *    all rows of P and Q simultaneously from the same (P_t, Q_t) (a
  *    deterministic full-gradient epoch);
- *  - the 1/n normalisation of Eq. 5 is the bucket degree, max(1, deg), and is
- *    applied to both factors when selected;
+ *  - the 1/n normalisation of Eq. 5 is the bucket degree, max(1, deg); step
+ *    option 1 applies it to both factors, option 2 to the column factors q
+ *    only, as Eq. 5 prints it;
  *  - the asymmetric clip of Section 5.3, min(max(xi, -g), g), equals
- *    min(g, xi); it acts once per coordinate on the aggregated, normalised
- *    descent direction of a row;
+ *    min(g, xi); option 1 applies it once per coordinate to the aggregated,
+ *    normalised descent direction of a row; option 3 applies it to the
+ *    aggregated direction before the normalisation, the order in which the
+ *    clipped update of Section 5.3 prints the 1/n (outside the min);
+ *    option 2 to each entry's own direction before the sum;
  *  - the optional bf16 mode rounds the factors read by the products to bf16
  *    (nearest even) while the fp64 master takes the update.
  */
@@ -222,18 +226,31 @@ static double sse_terms_per_entry(int64_t nnz, const int32_t *a, const int32_t *
     return sse;
 }
 
-/* New value of one factor row (Eqs. 3-5, Section 5.3).  clip 0 / 1: g holds
- * the data gradient -2 sum e q; the regulariser is added once, the step
- * scaled by s, and with clip 1 the direction clipped.  clip 2: g holds the
- * clipped per-entry directions, and the row moves by lr s g. */
+/* Step normalisation s of a factor row with deg observed cells (Eq. 5):
+ * step 0 (sum) s = 1; step 1 (degree) s = 1 / max(1, deg) on both sides;
+ * step 2 (column degree) the same on the column side (side 1) only. */
+static double step_scale(int32_t step, int side, int32_t deg) {
+    if (step == 1 || (step == 2 && side == 1)) return 1.0 / (double)(deg > 1 ? deg : 1);
+    return 1.0;
+}
+
+/* New value of one factor row (Eqs. 3-5, Section 5.3).  clip 0 / 1 / 3: g
+ * holds the data gradient -2 sum e q; the regulariser is added once, giving
+ * the summed descent direction D = -(g + 2 lambda x); the row moves by lr d
+ * with d = s D (clip 0), d = min(s D, xi) (clip 1) or d = s min(D, xi)
+ * (clip 3).  clip 2: g holds the clipped per-entry directions, d = s g. */
 static int update_row(const double *x, const double *g, int32_t deg, int32_t k, double lambda,
-                      double lr, int32_t step, int32_t clip, double xi, double *x_new) {
-    double s = step ? 1.0 / (double)(deg > 1 ? deg : 1) : 1.0;
+                      double lr, int32_t step, int side, int32_t clip, double xi, double *x_new) {
+    const double s = step_scale(step, side, deg);
     int finite = 1;
     for (int32_t c = 0; c < k; ++c) {
         double d;
         if (clip == 2) {
             d = s * g[c];
+        } else if (clip == 3) {
+            d = -(g[c] + 2.0 * lambda * x[c]);
+            if (d > xi) d = xi;
+            d = s * d;
         } else {
             d = -s * (g[c] + 2.0 * lambda * x[c]);
             if (clip && d > xi) d = xi;
@@ -369,10 +386,10 @@ static int fit_impl(int64_t nnz, const int32_t *a, const int32_t *b, const float
         int finite = 1;
         for (int32_t x = 0; x < m_t; ++x)
             finite &= update_row(P + (int64_t)x * k, gP + (int64_t)x * k, deg_r[x], k, lambda, lr,
-                                 step, clip, xi, Pn + (int64_t)x * k);
+                                 step, 0, clip, xi, Pn + (int64_t)x * k);
         for (int32_t x = 0; x < n_t; ++x)
             finite &= update_row(Q + (int64_t)x * k, gQ + (int64_t)x * k, deg_c[x], k, lambda, lr,
-                                 step, clip, xi, Qn + (int64_t)x * k);
+                                 step, 1, clip, xi, Qn + (int64_t)x * k);
         if (!finite) {
             status = 7;
             break;
@@ -481,12 +498,12 @@ int or_fit_minibatch(int64_t nnz, const int32_t *a, const int32_t *b, const floa
             for (int32_t x = 0; x < m_t; ++x) {
                 if (deg_r[x] == 0) memcpy(Pn + (int64_t)x * k, P + (int64_t)x * k, (size_t)k * sizeof(double));
                 else finite &= update_row(P + (int64_t)x * k, gP + (int64_t)x * k, deg_r[x], k, lambda, lr, step,
-                                          clip, xi, Pn + (int64_t)x * k);
+                                          0, clip, xi, Pn + (int64_t)x * k);
             }
             for (int32_t x = 0; x < n_t; ++x) {
                 if (deg_c[x] == 0) memcpy(Qn + (int64_t)x * k, Q + (int64_t)x * k, (size_t)k * sizeof(double));
                 else finite &= update_row(Q + (int64_t)x * k, gQ + (int64_t)x * k, deg_c[x], k, lambda, lr, step,
-                                          clip, xi, Qn + (int64_t)x * k);
+                                          1, clip, xi, Qn + (int64_t)x * k);
             }
             if (!finite) {
                 status = 7;
@@ -517,7 +534,8 @@ int or_fit_minibatch(int64_t nnz, const int32_t *a, const int32_t *b, const floa
 int or_extend(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,
               int32_t n_free, int32_t k, const double *F_fixed, double *F_free,
               int32_t steps, double lambda, double lr, int32_t step, int32_t clip, double xi) {
-    if (clip == 2) return 1; /* the per-entry order is a template-fit option */
+    /* the per-entry clip order and the column-only step are template-fit options */
+    if (clip == 2 || step == 2) return 1;
     int64_t len = (int64_t)n_free * k;
     double *g = (double *)malloc((size_t)(len + 1) * sizeof(double));
     double *xn = (double *)malloc((size_t)(len + 1) * sizeof(double));
@@ -536,7 +554,7 @@ int or_extend(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, cons
         int finite = 1;
         for (int32_t f = 0; f < n_free; ++f)
             finite &= update_row(F_free + (int64_t)f * k, g + (int64_t)f * k, deg[f], k, lambda,
-                                 lr, step, clip, xi, xn + (int64_t)f * k);
+                                 lr, step, 0, clip, xi, xn + (int64_t)f * k);
         if (!finite) status = 7;
         else memcpy(F_free, xn, (size_t)len * sizeof(double));
     }

@@ -54,10 +54,15 @@ double or_loss(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
 
 /* Full-gradient (Jacobi) descent on Eq. 2 for `epochs` epochs.
  *   step: 0 = plain gradient step, 1 = per-row/column step scaled by
- *         1/max(1, degree) (the 1/n normalisation of Eq. 5, applied to P and Q).
- *   clip: asymmetric clipping of Section 5.3, d <- min(d, xi) per coordinate
- *         of the descent direction (NaN propagates).  1 = on the row's summed
- *         direction (regulariser once per row, Eq. 2).  2 = per entry, before
+ *         s = 1/max(1, degree) (the 1/n normalisation of Eq. 5, applied to P
+ *         and Q), 2 = the same scale on the columns (Q) only, the rows taking
+ *         the plain step, as Eq. 5 prints it.
+ *   clip: asymmetric clipping of Section 5.3, min(D, xi) per coordinate of
+ *         the descent direction (NaN propagates), D = the row's summed
+ *         direction (regulariser once per row, Eq. 2).  1 = after the step
+ *         scale: d = min(s D, xi).  3 = before it, the order of the clipped
+ *         update as Section 5.3 prints it with eta / n outside the min:
+ *         d = s min(D, xi).  2 = per entry, before
  *         the sum (the clipped update of Section 5.3 applied to Eqs. 3-4 entry
  *         by entry): each cell contributes min(2 e q - 2 lambda p, xi) per
  *         coordinate, so the regulariser enters once per cell; the row then
@@ -127,7 +132,8 @@ int or_fit_minibatch(int64_t nnz, const int32_t *a, const int32_t *b, const floa
  * factors F_fixed (rows indexed by fixed_id) stay constant; each free row
  * f in [0, n_free) starts at zero and takes `steps` gradient steps on
  * sum_{entries of f} (r - F_fixed[id] . x_f)^2 + lambda ||x_f||^2.
- * clip 0 or 1 as for or_fit; clip 2 (per entry) returns 1 untouched. */
+ * step 0 or 1 and clip 0, 1 or 3 as for or_fit (the free rows are the side
+ * being scaled); step 2 and clip 2 (template-fit options) return 1 untouched. */
 int or_extend(int64_t nnz, const int32_t *fixed_id, const int32_t *free_id, const float *v,
               int32_t n_free, int32_t k, const double *F_fixed, double *F_free,
               int32_t steps, double lambda, double lr, int32_t step, int32_t clip, double xi);

@@ -46,6 +46,64 @@ def test_hand_derived_steps(oracle_lib):
     np.testing.assert_allclose(Q, t["Q1"], rtol=1e-14)
 
 
+def test_hand_derived_step_scale_and_clip_order(oracle_lib):
+    """Rows and columns of degree 2 where the clip acts between D/n and D:
+    the clip after the step scale (clip 1), the clip before it (clip 3, the
+    order Section 5.3 prints), the degree step on both sides and on the
+    columns only (Eq. 5 as printed) all end at different factors, each
+    derived by hand.  Swapping the clip and the 1/n, or scaling the wrong
+    side, fails one of these cases."""
+    g = json.load(open(os.path.join(GOLDEN, "hand_steps.json")))["two_lines"]
+    cells = np.array(g["cells"])
+    a, b, v = cells[:, 0].astype(np.int32), cells[:, 1].astype(np.int32), cells[:, 2].astype(np.float32)
+    seen = set()
+    for c in g["cases"]:
+        st, P, Q, h, _ = oracle_lib.fit(a, b, v, np.array(g["P"]), np.array(g["Q"]), 1, c["lambda"], g["lr"],
+                                        c["step"], c["clip"], c["xi"])
+        assert st == 0, c["name"]
+        assert h[0] == pytest.approx(c["loss0"], rel=1e-15), c["name"]
+        np.testing.assert_allclose(P, c["P1"], rtol=1e-15, err_msg=c["name"])
+        np.testing.assert_allclose(Q, c["Q1"], rtol=1e-15, err_msg=c["name"])
+        seen.add((c["lambda"], tuple(np.ravel(c["P1"])), tuple(np.ravel(c["Q1"]))))
+    assert len(seen) == len(g["cases"])  # every option pair ends elsewhere
+
+
+def test_hand_derived_bf16_epoch(oracle_lib):
+    """bf16 mode (reading R13): the products read round-to-nearest-even bf16
+    copies while the fp64 master takes the update and enters the regulariser
+    and the loss norms.  The start values straddle bf16 rounding boundaries,
+    so rounding the master, using the copy in the regulariser or the master
+    in the products each moves p1 or q1 by more than 1e-4."""
+    c = json.load(open(os.path.join(GOLDEN, "hand_steps.json")))["bf16"]
+    one = np.zeros(1, np.int32)
+    st, P, Q, h, _ = oracle_lib.fit(one, one, np.array([c["r"]], np.float32), np.array([[c["p"]]]),
+                                    np.array([[c["q"]]]), 1, c["lambda"], c["lr"], c["step"], c["clip"], c["xi"],
+                                    bf16=True)
+    assert st == 0
+    assert h[0] == pytest.approx(c["loss0"], rel=1e-15)
+    assert P[0, 0] == pytest.approx(c["p1"], rel=1e-15)
+    assert Q[0, 0] == pytest.approx(c["q1"], rel=1e-15)
+    # the fp64 run from the same start differs (the bf16 copies matter)
+    _, P64, _, _, _ = oracle_lib.fit(one, one, np.array([c["r"]], np.float32), np.array([[c["p"]]]),
+                                     np.array([[c["q"]]]), 1, c["lambda"], c["lr"], c["step"], c["clip"], c["xi"])
+    assert abs(P64[0, 0] - c["p1"]) > 1e-4
+
+
+def test_column_only_step_and_printed_clip_are_not_extension_options(oracle_lib):
+    """The extension scales the free rows by their own degree (reading R12):
+    the column-only step is a template-fit option and returns 1; clip 3 runs."""
+    fixed = np.array([0, 1, 0], np.int32)
+    free = np.array([0, 0, 1], np.int32)
+    v = np.array([1.0, 2.0, 3.0], np.float32)
+    F = np.array([[1.0, 0.0], [0.0, 1.0]])
+    assert oracle_lib.extend(fixed, free, v, 2, F, 3, 0.0, 0.1, "col_degree")[0] == 1
+    st, X3 = oracle_lib.extend(fixed, free, v, 2, F, 1, 0.0, 0.5, "degree", "printed", 0.5)
+    # free row 0: D = 2 (1*[1,0] + 2*[0,1]) = [2, 4], deg 2 -> d = (1/2) min(D, 0.5) = [0.25, 0.25]
+    # free row 1: D = 2*3*[1,0] = [6, 0], deg 1 -> d = [0.5, 0]
+    assert st == 0
+    np.testing.assert_allclose(X3, [[0.125, 0.125], [0.25, 0.0]], rtol=1e-15)
+
+
 # ------------------------------------------------------------ P1 gradient
 @pytest.mark.parametrize("step", ["sum", "degree"])
 def test_gradient_matches_central_differences(oracle_lib, step):
