@@ -278,7 +278,7 @@ def main():
 
     log(f"generating {args.config}")
     t0 = time.perf_counter()
-    p = tsid_synth.make(args.config)
+    p = tsid_synth.make_cached(args.config, os.environ.get("TSID_SYNTH_CACHE"))
     if args.lr is not None:
         p.lr = args.lr
     gen_s = time.perf_counter() - t0

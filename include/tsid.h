@@ -53,15 +53,18 @@ typedef enum { TSID_FP32 = 0, TSID_BF16 = 1 } tsid_precision;
 /* Per-row step normalisation.  SUM: the plain full gradient of Eq. 2.
  * DEGREE: the step of every factor row is divided by max(1, its number of
  * observed cells) -- the 1/n normalisation of Eq. 5 (Section 5.1), applied to
- * both P and Q. */
-typedef enum { TSID_STEP_SUM = 0, TSID_STEP_DEGREE = 1 } tsid_step;
+ * both P and Q.  COL_DEGREE: the same division for the column factors Q only,
+ * the rows of P taking the plain step, as Eq. 5 prints it (template fits
+ * only; the extension returns E_INVAL). */
+typedef enum { TSID_STEP_SUM = 0, TSID_STEP_DEGREE = 1, TSID_STEP_COL_DEGREE = 2 } tsid_step;
 
 /* Fit options.
  *  epochs  number of full-gradient epochs (>= 0).
  *  lambda  l2 weight of Eq. 2 (>= 0).   lr  step size eta (> 0).
  *  clip    1: asymmetric clipping of Section 5.3 -- each coordinate of the
- *          descent direction d becomes min(d, clip_xi) (positive components
- *          are capped, negative ones pass; NaN propagates).  clip_xi > 0.
+ *          row's summed descent direction, after the step scale of
+ *          opts->step, becomes min(d, clip_xi) (positive components are
+ *          capped, negative ones pass; NaN propagates).  clip_xi > 0.
  *          2: the same clip in the per-entry order (Section 5.3 applied to
  *          Eqs. 3-4 entry by entry, then the 1/n average of Eq. 5): each
  *          cell adds min(2 e q - 2 lambda p, clip_xi) per coordinate (the
@@ -70,6 +73,11 @@ typedef enum { TSID_STEP_SUM = 0, TSID_STEP_DEGREE = 1 } tsid_step;
  *          row without cells stays.  Template fits only, on the item pass
  *          (E_INVAL with TSID_PASS_SLAB or forced dense tiles; the automatic
  *          modes use neither); the extension returns E_INVAL.
+ *          3: the clip of Section 5.3 in the order its printed update
+ *          takes, the step scale s (1, or 1/max(1, deg) with a degree
+ *          step) outside the min: each coordinate moves by
+ *          lr * s * min(D, clip_xi), D the row's summed descent direction
+ *          (clip 1 moves it by lr * min(s * D, clip_xi)).
  *          0: no clip.
  *  prec    TSID_FP32: fp32 factors.  TSID_BF16: the products read bf16
  *          (round-to-nearest-even) copies of the factors, accumulate in fp32,

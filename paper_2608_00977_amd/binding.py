@@ -26,7 +26,7 @@ STATUS = {0: "TSID_OK", 1: "TSID_E_INVAL", 2: "TSID_E_RANGE", 3: "TSID_E_DUP",
           4: "TSID_E_NOMEM", 5: "TSID_E_DEVICE", 6: "TSID_E_STATE", 7: "TSID_E_NONFINITE"}
 OK, E_INVAL, E_RANGE, E_DUP, E_NOMEM, E_DEVICE, E_STATE, E_NONFINITE = range(8)
 FP32, BF16 = 0, 1
-STEP_SUM, STEP_DEGREE = 0, 1
+STEP_SUM, STEP_DEGREE, STEP_COL_DEGREE = 0, 1, 2
 PASS_KERNEL = {"auto": 0, "item": 1, "slab": 2}
 IDX = {"row_map": 0, "col_map": 1, "row_ptr": 2, "csr_col": 3, "csr_val": 4, "col_ptr": 5,
        "csc_row": 6, "csc_val": 7, "deg_r": 8, "deg_c": 9, "batch_ptr_r": 10, "batch_ptr_c": 11}
@@ -263,13 +263,19 @@ def make_adam_opts(steps=1, lam=0.0, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8):
     return tsid_adam_opts(int(steps), float(lam), float(lr), float(beta1), float(beta2), float(eps))
 
 
+CLIP_MODES = {"per_entry": 2, "printed": 3}
+STEP_MODES = {"sum": STEP_SUM, "degree": STEP_DEGREE, "col_degree": STEP_COL_DEGREE}
+
+
 def make_opts(epochs=1, lam=0.0, lr=0.1, clip=False, xi=0.1, prec="fp32", step="sum"):
-    """clip: False / True (the clip on each row's summed direction) or
-    "per_entry" (each cell's direction clipped before the sum)."""
+    """clip: False / True (the clip on each row's normalised summed
+    direction), "printed" (the clip on the summed direction before the step
+    scale) or "per_entry" (each cell's direction clipped before the sum).
+    step: "sum", "degree" or "col_degree"."""
     return tsid_fit_opts(int(epochs), float(lam), float(lr), float(xi),
-                         2 if clip == "per_entry" else int(bool(clip)),
+                         CLIP_MODES[clip] if isinstance(clip, str) else int(bool(clip)),
                          BF16 if prec == "bf16" else FP32,
-                         STEP_DEGREE if step == "degree" else STEP_SUM)
+                         STEP_MODES[step])
 
 
 class Tsid:

@@ -523,10 +523,17 @@ void check_opts(const tsid_fit_opts *o) {
     if (o->epochs < 0) fail(TSID_E_INVAL, "epochs < 0");
     if (!(o->lambda >= 0.f) || !std::isfinite(o->lambda)) fail(TSID_E_INVAL, "lambda must be finite and >= 0");
     if (!(o->lr > 0.f) || !std::isfinite(o->lr)) fail(TSID_E_INVAL, "lr must be finite and > 0");
-    if (o->clip < 0 || o->clip > 2) fail(TSID_E_INVAL, "clip must be 0, 1 or 2");
+    if (o->clip < 0 || o->clip > 3) fail(TSID_E_INVAL, "clip must be 0, 1, 2 or 3");
     if (o->clip && !(o->clip_xi > 0.f)) fail(TSID_E_INVAL, "clip_xi must be > 0");
     if (o->prec != TSID_FP32 && o->prec != TSID_BF16) fail(TSID_E_INVAL, "bad precision");
-    if (o->step != TSID_STEP_SUM && o->step != TSID_STEP_DEGREE) fail(TSID_E_INVAL, "bad step");
+    if (o->step != TSID_STEP_SUM && o->step != TSID_STEP_DEGREE && o->step != TSID_STEP_COL_DEGREE)
+        fail(TSID_E_INVAL, "bad step");
+}
+
+// Whether the rows of `side` (0: rows of R, P; 1: columns, Q) take the
+// 1/max(1, deg) step scale of Eq. 5.
+int32_t side_scaled(int32_t step, int side) {
+    return step == TSID_STEP_DEGREE || (step == TSID_STEP_COL_DEGREE && side == 1);
 }
 
 void check_aligned(const void *p, const char *what) {
@@ -1321,7 +1328,7 @@ PassArgs pass_args(const Template &t, int side, const tsid_fit_opts &o, int32_t 
     a.lr = o.lr;
     a.xi = o.clip_xi;
     a.clip = o.clip;
-    a.degree = o.step == TSID_STEP_DEGREE;
+    a.degree = side_scaled(o.step, side);
     a.err = err;
     return a;
 }
@@ -1361,7 +1368,7 @@ SlabArgs slab_args(const Template &t, int side, const tsid_fit_opts &o, int32_t 
     a.lr = o.lr;
     a.xi = o.clip_xi;
     a.clip = o.clip;
-    a.degree = o.step == TSID_STEP_DEGREE;
+    a.degree = side_scaled(o.step, side);
     a.err = err;
     return a;
 }
@@ -1981,6 +1988,8 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
     } else {
         check_opts(o);
         if (o->clip == 2) fail(TSID_E_INVAL, "per-entry clipping (clip 2) is a template-fit option");
+        if (o->step == TSID_STEP_COL_DEGREE)
+            fail(TSID_E_INVAL, "the column-only degree step is a template-fit option");
     }
     if (side != 0 && side != 1) fail(TSID_E_INVAL, "side must be 0 or 1");
     if (nnz < 0 || nnz > kMaxEntries) fail(TSID_E_INVAL, "nnz out of range");

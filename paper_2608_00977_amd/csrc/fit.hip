@@ -186,8 +186,7 @@ __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg,
         } else {
             float g = 2.0f * A.lam * x[v] - 2.0f * acc[v];
             if (A.gx) g += A.gx_scale * gxv[v];
-            d = -s * g;
-            if (A.clip && d > A.xi) d = A.xi;
+            d = clipped_step(g, s, A.clip, A.xi);
         }
         xn[v] = keep ? x[v] : x[v] + A.lr * d;
         bad |= !__builtin_isfinite(xn[v]);
@@ -703,8 +702,7 @@ __global__ __launch_bounds__(kThreads) void k_extend_steps(const PassArgs A, int
 #pragma unroll
         for (int v = 0; v < V; ++v) {
             const float g = 2.0f * A.lam * x[v] - 2.0f * tot[v];
-            float d = -s * g;
-            if (A.clip && d > A.xi) d = A.xi;
+            const float d = clipped_step(g, s, A.clip, A.xi);
             x[v] = x[v] + A.lr * d;
             bad |= !__builtin_isfinite(x[v]);
         }

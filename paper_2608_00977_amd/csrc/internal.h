@@ -25,6 +25,24 @@ void hip_check(hipError_t e, const char *what);
 // Device-side error slots (plain stores of 1, never atomics).
 enum ErrSlot { ERR_RANGE = 0, ERR_DUP = 1, ERR_INVAL = 2, ERR_NONFINITE = 3, ERR_SLOTS = 4 };
 
+// Step of one coordinate of a factor row (Eq. 5 with the Section 5.3 clip):
+// g is the summed gradient (Eqs. 3-4 over the row's cells plus the
+// regulariser once), s the step scale of the row (1 or 1/max(1, deg)).  The
+// descent direction is -g.  clip 0: s (-g); clip 1: min(s (-g), xi), the clip
+// on the normalised direction; clip 3: s min(-g, xi), the clip before the
+// scale, in the order the clipped update of Section 5.3 prints.  A NaN
+// compares false and passes through.
+__device__ __forceinline__ float clipped_step(float g, float s, int32_t clip, float xi) {
+    if (clip == 3) {
+        float d = -g;
+        if (d > xi) d = xi;
+        return s * d;
+    }
+    float d = -s * g;
+    if (clip && d > xi) d = xi;
+    return d;
+}
+
 inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 inline int bits_for(int64_t count) {  // bits to hold values 0..count-1 (at least 1)
     int b = 1;

@@ -77,8 +77,7 @@ __device__ __forceinline__ void finalize_lane(const SlabArgs &A, int xr, int rot
     float nrm = 0.f;
     auto upd = [&](float xv, float av) {
         const float g = 2.0f * A.lam * xv - 2.0f * av;
-        float d = -s * g;
-        if (A.clip && d > A.xi) d = A.xi;
+        const float d = clipped_step(g, s, A.clip, A.xi);
         const float xn = xv + A.lr * d;
         bad |= !__builtin_isfinite(xn);
         nrm += xv * xv;
@@ -365,8 +364,7 @@ __device__ __forceinline__ void slab_finish_lane(const SlabArgs &A, const int64_
     float nrm = 0.f;
     auto upd = [&](float xv, float av) {
         const float g = 2.0f * A.lam * xv - 2.0f * av;
-        float d = -s * g;
-        if (A.clip && d > A.xi) d = A.xi;
+        const float d = clipped_step(g, s, A.clip, A.xi);
         const float xn = xv + A.lr * d;
         bad |= !__builtin_isfinite(xn);
         nrm += xv * xv;

@@ -28,4 +28,5 @@ from .generate import (  # noqa: F401
     similarity_graph,
     CONFIGS,
     make,
+    make_cached,
 )

@@ -495,3 +495,30 @@ CONFIGS: Dict[str, Callable[..., Problem]] = {
 def make(name: str, seed: Optional[int] = None, **kw) -> Problem:
     fn = CONFIGS[name]
     return fn(**kw) if seed is None else fn(seed=seed, **kw)
+
+
+_ARRAYS = ("u", "i", "r", "tu", "ti", "tr", "I", "J", "P0", "Q0")
+
+
+def make_cached(name: str, cache_dir: Optional[str] = None) -> Problem:
+    """`make(name)`, kept as plain .npy arrays plus a JSON of the scalar fields
+    under cache_dir (None: no cache).  Loading executes nothing from the files
+    (numpy without pickles, JSON)."""
+    import json
+    import os
+    if not cache_dir:
+        return make(name)
+    base = os.path.join(cache_dir, name)
+    meta_path = base + ".json"
+    if os.path.exists(meta_path):
+        meta = json.load(open(meta_path))
+        arrs = {a: np.load(f"{base}.{a}.npy", allow_pickle=False) for a in _ARRAYS}
+        return Problem(**meta, **arrs)
+    p = make(name)
+    os.makedirs(cache_dir, exist_ok=True)
+    for a in _ARRAYS:
+        np.save(f"{base}.{a}.npy", getattr(p, a), allow_pickle=False)
+    meta = {f.name: getattr(p, f.name) for f in dataclasses.fields(p) if f.name not in _ARRAYS}
+    json.dump(meta, open(meta_path + ".tmp", "w"))
+    os.replace(meta_path + ".tmp", meta_path)
+    return p
