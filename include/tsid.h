@@ -164,6 +164,27 @@ tsid_status tsid_fit_epochs_done(const tsid_ctx *ctx, int32_t *epochs);
  * Synchronous. */
 tsid_status tsid_loss(tsid_ctx *ctx, const float *P, const float *Q, float lambda, double *out);
 
+/* tsid_loss for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same value, bit for bit, computed by the same kernels, with every buffer
+ * the kernels need (per-work-item residual sums, per-row norms, the
+ * reduction's partial sums and result) taken from a fixed device array of
+ * TSID_NOALLOC_SCRATCH_BYTES that the library's code object holds on each
+ * device it runs on, until the process ends.  The call allocates nothing
+ * (no hipMalloc, hipFree or allocating library routine); the template and
+ * its fp32 row-side work plan come from tsid_build_template.
+ * Limit: 4 bytes per work item of the row side (at least one per template
+ * row), 4 per template row and per template column, plus 2 KiB, must fit the
+ * array (a 1 M x 100 k template with 4.2e8 cells needs about 9 MB).
+ * Every call on a device shares that device's array: calls that overlap on
+ * one device (several contexts, several host threads) race and must be
+ * serialised by the caller.  Nothing in the array needs clearing between
+ * calls (every slot a call reads is written by that call first).
+ * Arguments, layout and errors as tsid_loss, plus E_NOMEM when the template
+ * exceeds the limit (nothing is launched).  Synchronous. */
+#define TSID_NOALLOC_SCRATCH_BYTES (32u << 20)
+tsid_status tsid_loss_noalloc(tsid_ctx *ctx, const float *P, const float *Q, float lambda, double *out);
+
 /* One chunk of the extension (Stage II, Section 5.2; Eq. 6 in factored form:
  * a free row's coefficients x_f solve the ridge problem
  *   min sum_(entries of f) (r - F_fixed[fixed_id] . x_f)^2 + lambda ||x_f||^2

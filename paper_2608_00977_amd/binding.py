@@ -93,6 +93,7 @@ def lib() -> C.CDLL:
         "tsid_fit_row_blocks": (C.c_int, [P, P]),
         "tsid_fit_dense_info": (C.c_int, [P, C.POINTER(tsid_dense_info)]),
         "tsid_loss": (C.c_int, [P, P, P, C.c_float, P]),
+        "tsid_loss_noalloc": (C.c_int, [P, P, P, C.c_float, P]),
         "tsid_extend_chunk": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P,
                                         C.POINTER(tsid_fit_opts)]),
         "tsid_extend_chunk_ridge": (C.c_int, [P, C.c_int, P, P, P, i64, i32, P, i64, P, C.c_float]),
@@ -216,6 +217,10 @@ def tsid_fit_dense_info(ctx) -> dict:
 
 def tsid_loss(ctx, P, Q, lam: float, out) -> int:
     return lib().tsid_loss(ctx, P, Q, lam, out)
+
+
+def tsid_loss_noalloc(ctx, P, Q, lam: float, out) -> int:
+    return lib().tsid_loss_noalloc(ctx, P, Q, lam, out)
 
 
 def tsid_extend_chunk(ctx, side, fixed_id, free_local, r, nnz, n_free, F_fixed, n_fixed, F_free,
@@ -392,6 +397,14 @@ class Tsid:
         out = np.zeros(1, np.float64)
         torch.cuda.current_stream().synchronize()
         self._check(tsid_loss(self.ctx, _ptr(P), _ptr(Q), lam, _ptr(out)), "tsid_loss")
+        return float(out[0])
+
+    def loss_noalloc(self, P: torch.Tensor, Q: torch.Tensor, lam: float) -> float:
+        """tsid_loss_noalloc: the same value from the library's fixed scratch
+        array, with no device allocation."""
+        out = np.zeros(1, np.float64)
+        torch.cuda.current_stream().synchronize()
+        self._check(tsid_loss_noalloc(self.ctx, _ptr(P), _ptr(Q), lam, _ptr(out)), "tsid_loss_noalloc")
         return float(out[0])
 
     def extend_chunk(self, side, fixed_id, free_local, r, n_free, F_fixed: torch.Tensor,

@@ -5,6 +5,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <unordered_map>
 #include <utility>
 #include <vector>
@@ -266,6 +267,7 @@ struct tsid_ctx {
     uint64_t mb_seed = 0;
     int32_t row_blocks = 0;           // tsid_set_row_blocks: 0 automatic, 1 off, n forced
     int32_t used_blocks = 1;          // row blocks of the last fit's Q pass
+    void *noalloc_scratch = nullptr;  // device address of this device's scratch array
 };
 
 namespace {
@@ -558,6 +560,8 @@ void raise_device_errors(const int32_t *e, const char *where) {
     if (e[ERR_INVAL]) fail(TSID_E_INVAL, std::string(where) + ": non-finite value");
 }
 
+Plan build_plan(tsid_ctx *c, const std::vector<int64_t> &ptr, int32_t rows, int64_t E, int64_t ng);
+
 void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i, const float *r,
            int64_t nnz, const int32_t *I, int32_t m_t, const int32_t *J, int32_t n_t, int32_t k,
            int64_t stage) {
@@ -729,6 +733,9 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
         TSID_HIP(hipMemcpyAsync(c->err_host, c->err_dev, ERR_SLOTS * 4, hipMemcpyDeviceToHost, cs));
         TSID_HIP(hipStreamSynchronize(cs));
         raise_device_errors(c->err_host, "build");
+        // the fp32 work plan of the row side comes with the template: the
+        // loss needs it, and tsid_loss_noalloc may not allocate it later
+        t->plan[0][TSID_FP32] = build_plan(c, t->hptr[0], m_t, t->E, items_per_wave(k, TSID_FP32));
     } catch (...) {
         cleanup();
         free_template(c, t);
@@ -1876,6 +1883,93 @@ void loss(tsid_ctx *c, const float *P, const float *Q, float lambda, double *out
     TSID_HIP(hipStreamSynchronize(cs));
 }
 
+// ------------------------------------------------ allocation-free loss
+
+// Device scratch of tsid_loss_noalloc: one array per device, placed by the
+// code object loader, never allocated by the library.  In host code the name
+// is a host-side stand-in; the device address comes from
+// hipGetSymbolAddress, once per device (noalloc_scratch_on), and only that
+// address is handed to kernels and copies.
+constexpr size_t kNoAllocBytes = TSID_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this device's scratch array (looked up with the device
+// current, at context creation).
+void *noalloc_scratch_on(int device) {
+    if (device < 0 || device >= kMaxDevices) fail(TSID_E_DEVICE, "device id beyond the scratch table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+        void *ptr = nullptr;
+        TSID_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+        if (!ptr) fail(TSID_E_DEVICE, "hipGetSymbolAddress returned no address for the scratch array");
+        g_scratch_ptr[device] = ptr;
+    }
+    return g_scratch_ptr[device];
+}
+
+// Bytes of the scratch the allocation-free loss needs: the reduction's
+// partial sums and result (fp64), then per-item e^2 and the per-row norms of
+// P and Q (fp32), each 256-byte aligned.
+struct NoAllocLayout {
+    size_t partial = 0, out = 0, e2 = 0, normP = 0, normQ = 0, total = 0;
+};
+NoAllocLayout noalloc_layout(int64_t n_items, int64_t m_t, int64_t n_t) {
+    auto up = [](size_t b) { return (b + 255) & ~size_t(255); };
+    NoAllocLayout L;
+    L.partial = 0;
+    L.out = up(L.partial + reduce_scratch_elems(1) * sizeof(double));
+    L.e2 = up(L.out + sizeof(double));
+    L.normP = up(L.e2 + (size_t)std::max<int64_t>(n_items, 1) * 4);
+    L.normQ = up(L.normP + (size_t)std::max<int64_t>(m_t, 1) * 4);
+    L.total = up(L.normQ + (size_t)std::max<int64_t>(n_t, 1) * 4);
+    return L;
+}
+
+// tsid_loss with every buffer in the scratch array (the same kernels in the
+// same order as loss(), so the result is the same bits).
+void loss_noalloc(tsid_ctx *c, const float *P, const float *Q, float lambda, double *out) {
+    if (!c->tpl) fail(TSID_E_STATE, "no template");
+    Template &t = *c->tpl;
+    if (!out) fail(TSID_E_INVAL, "out is NULL");
+    if ((t.m_t && !P) || (t.n_t && !Q)) fail(TSID_E_INVAL, "NULL factor pointer");
+    if (!(lambda >= 0.f) || !std::isfinite(lambda)) fail(TSID_E_INVAL, "lambda must be finite and >= 0");
+    check_aligned(P, "P");
+    check_aligned(Q, "Q");
+    const Plan &pl = t.plan[0][TSID_FP32];
+    if (!pl.ready) fail(TSID_E_STATE, "the template has no fp32 row plan");
+    const NoAllocLayout L = noalloc_layout(pl.n_items, t.m_t, t.n_t);
+    if (L.total > kNoAllocBytes)
+        fail(TSID_E_NOMEM, "the allocation-free loss needs " + std::to_string(L.total) + " bytes of scratch (" +
+                               "4 per work item, template row and column, plus 2 KiB); it has " +
+                               std::to_string(kNoAllocBytes));
+    char *base = static_cast<char *>(c->noalloc_scratch);
+    if (!base) fail(TSID_E_STATE, "no scratch address for this device");
+    double *partial = reinterpret_cast<double *>(base + L.partial);
+    double *dout = reinterpret_cast<double *>(base + L.out);
+    float *e2 = reinterpret_cast<float *>(base + L.e2);
+    float *normP = reinterpret_cast<float *>(base + L.normP);
+    float *normQ = reinterpret_cast<float *>(base + L.normQ);
+    hipStream_t cs = c->comp;
+    tsid_fit_opts o{0, lambda, 1.f, 1.f, 0, TSID_FP32, TSID_STEP_SUM};
+    PassArgs a = pass_args(t, 0, o, c->err_dev);
+    a.X = P;
+    a.Y = Q;
+    a.e2 = e2;
+    a.norm = normP;
+    a.epoch = 0;
+    a.skip_after_nonfinite = 0;
+    launch_item_pass(t.k, TSID_FP32, true, a, cs);
+    launch_row_norms(t.k, Q, t.n_t, normQ, cs);
+    launch_loss_reduce(e2, std::max<int64_t>(pl.n_items, 1), pl.n_items, normP, t.m_t, normQ, t.n_t, lambda, 1,
+                       partial, dout, nullptr, -1, cs);
+    TSID_HIP(hipMemcpyAsync(out, dout, 8, hipMemcpyDeviceToHost, cs));
+    TSID_HIP(hipStreamSynchronize(cs));
+}
+
 // ------------------------------------------------------------- extension
 
 void ext_sync_all(tsid_ctx *c) {
@@ -2196,6 +2290,7 @@ tsid_status tsid_create(int device, void *hip_stream, size_t max_device_bytes, t
         c->err_dev = c->arena.alloc<int32_t>(ERR_SLOTS);
         TSID_HIP(hipHostMalloc((void **)&c->err_host, ERR_SLOTS * sizeof(int32_t), hipHostMallocDefault));
         TSID_HIP(hipMemset(c->err_dev, 0, ERR_SLOTS * sizeof(int32_t)));
+        c->noalloc_scratch = noalloc_scratch_on(device);
     });
     if (st != TSID_OK) {
         tsid_destroy(c);
@@ -2323,6 +2418,10 @@ tsid_status tsid_fit_epochs_done(const tsid_ctx *c, int32_t *epochs) {
     if (!c || !epochs) return TSID_E_INVAL;
     *epochs = c->epochs_done;
     return TSID_OK;
+}
+
+tsid_status tsid_loss_noalloc(tsid_ctx *c, const float *P, const float *Q, float lambda, double *out) {
+    return guarded(c, [&]() { loss_noalloc(c, P, Q, lambda, out); });
 }
 
 tsid_status tsid_loss(tsid_ctx *c, const float *P, const float *Q, float lambda, double *out) {
