@@ -20,25 +20,46 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "tsid_oracle.c")
 _LIB = os.path.join(_HERE, "libtsid_oracle.so")
+_LIB_OMP = os.path.join(_HERE, "libtsid_oracle_omp.so")
+
+
+def _compile(out: str, extra) -> None:
+    tmp = out + ".tmp%d" % os.getpid()
+    subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-fPIC", "-shared", "-ffp-contract=off",
+                           "-Wall", "-Wextra", "-Wno-unknown-pragmas", *extra, _SRC, "-o", tmp, "-lm"])
+    os.replace(tmp, out)
 
 
 def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (plain -O2, IEEE semantics, no FMA contraction)."""
-    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-        tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O2", "-std=gnu11", "-fPIC", "-shared", "-ffp-contract=off",
-                               "-Wall", "-Wextra", _SRC, "-o", tmp, "-lm"])
-        os.replace(tmp, _LIB)
+    """Compile the oracle with gcc (plain -O2, IEEE semantics, no FMA
+    contraction): the serial library, and the same source with OpenMP (its
+    parallel loops are those of or_fit_lines and a few elementwise copies)."""
+    for out, extra in ((_LIB, []), (_LIB_OMP, ["-fopenmp"])):
+        if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(_SRC):
+            _compile(out, extra)
     return _LIB
 
 
 _lib: Optional[C.CDLL] = None
+_lib_omp: Optional[C.CDLL] = None
 
 
-def lib() -> C.CDLL:
-    global _lib
+def lib(omp: bool = False) -> C.CDLL:
+    """The serial oracle library, or (omp=True) the same source built with
+    OpenMP (threads from OMP_NUM_THREADS, else all cores)."""
+    global _lib, _lib_omp
+    if omp:
+        if _lib_omp is None:
+            build(force=False)
+            _lib_omp = _declare(C.CDLL(_LIB_OMP))
+        return _lib_omp
     if _lib is None:
-        _lib = C.CDLL(build(force=False))
+        _lib = _declare(C.CDLL(build(force=False)))
+    return _lib
+
+
+def _declare(lb: C.CDLL) -> C.CDLL:
+    if True:  # signatures of the exported routines
         P = C.c_void_p
         i32, i64, f64 = C.c_int32, C.c_int64, C.c_double
         sig = {
@@ -64,12 +85,15 @@ def lib() -> C.CDLL:
                                     i64, P, P, P, f64, P, P]),
             "or_similarity": (None, [i32, i32, P, P]),
             "or_bf16_bits": (C.c_uint16, [C.c_float]),
+            "or_fit_lines": (C.c_int, [i64, P, P, P, i32, i32, i32, P, P, i32, f64, f64, i32, i32, f64,
+                                       i32, P, P]),
+            "or_threads": (C.c_int, []),
         }
         for name, (res, args) in sig.items():
-            fn = getattr(_lib, name)
+            fn = getattr(lb, name)
             fn.restype = res
             fn.argtypes = args
-    return _lib
+    return lb
 
 
 def _p(x: np.ndarray):
@@ -140,6 +164,25 @@ def fit(a, b, v, P0, Q0, epochs, lam, lr, step="sum", clip=False, xi=0.1, bf16=F
                       _p(Q), epochs, lam, lr, STEP[step], CLIP[clip], xi, int(bf16), _p(hist),
                       _p(done))
     return st, P, Q, hist, int(done[0])
+
+
+def fit_lines(a, b, v, P0, Q0, epochs, lam, lr, step="sum", clip=False, xi=0.1, bf16=False, omp=True):
+    """or_fit_lines: the same result as fit(), bit for bit, with the rows and
+    then the columns split across OpenMP threads (omp=True) or run serially.
+    Returns (status, P, Q, loss_hist, epochs_done)."""
+    a, b, v = _c(a, np.int32), _c(b, np.int32), _c(v, np.float32)
+    P = np.array(P0, dtype=np.float64, order="C", copy=True)
+    Q = np.array(Q0, dtype=np.float64, order="C", copy=True)
+    hist = np.full(epochs + 1, np.nan)
+    done = np.zeros(1, np.int32)
+    st = lib(omp).or_fit_lines(a.size, _p(a), _p(b), _p(v), P.shape[0], Q.shape[0], P.shape[1], _p(P), _p(Q),
+                               epochs, lam, lr, STEP[step], CLIP[clip], xi, int(bf16), _p(hist), _p(done))
+    return st, P, Q, hist, int(done[0])
+
+
+def threads(omp: bool = True) -> int:
+    """Threads the OpenMP build runs with (1 for the serial library)."""
+    return int(lib(omp).or_threads())
 
 
 def loss_mv(a, b, v, m_t, n_t, P, Q, lam, s_row, s_col, s_val, beta) -> float:

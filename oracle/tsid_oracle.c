@@ -28,6 +28,9 @@
 #include "tsid_oracle.h"
 
 #include <math.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 #include <stdlib.h>
 #include <string.h>
 
@@ -411,6 +414,116 @@ static int fit_impl(int64_t nnz, const int32_t *a, const int32_t *b, const float
     if (epochs_done) *epochs_done = t;
     free(gP); free(gQ); free(Pn); free(Qn); free(Ps); free(Qs); free(deg_r); free(deg_c);
     return status;
+}
+
+/* ------------------------------------------- line-parallel full-gradient fit */
+
+/* Entry indices of every line (row when major = a, column when major = b),
+ * each line's entries in increasing input order (a stable counting sort):
+ * ptr[x]..ptr[x+1] index into idx. */
+static void lines_in_input_order(int64_t nnz, const int32_t *major, int32_t n_major, int64_t *ptr,
+                                 int64_t *idx) {
+    for (int32_t x = 0; x <= n_major; ++x) ptr[x] = 0;
+    for (int64_t e = 0; e < nnz; ++e) ptr[major[e] + 1] += 1;
+    for (int32_t x = 0; x < n_major; ++x) ptr[x + 1] += ptr[x];
+    int64_t *fill = (int64_t *)malloc(((size_t)n_major + 1) * sizeof(int64_t));
+    memcpy(fill, ptr, ((size_t)n_major + 1) * sizeof(int64_t));
+    for (int64_t e = 0; e < nnz; ++e) idx[fill[major[e]]++] = e;
+    free(fill);
+}
+
+/* or_fit computed line by line: the residual of every entry first, the
+ * squared residuals summed in input order, then each row's gradient sum over
+ * its entries in input order (rows in parallel when built with OpenMP), the
+ * same for columns, and the row updates.  Every sum has the operands and the
+ * order of or_fit's, so the results are the same bits; only the work is
+ * split across threads.  clip 2 and the similarity term are not offered
+ * here (return 1). */
+int or_fit_lines(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+                 int32_t m_t, int32_t n_t, int32_t k, double *P, double *Q,
+                 int32_t epochs, double lambda, double lr, int32_t step,
+                 int32_t clip, double xi, int32_t bf16, double *loss_hist, int32_t *epochs_done) {
+    if (clip == 2 || k > 128) return 1;
+    const int64_t lp = (int64_t)m_t * k, lq = (int64_t)n_t * k;
+    double *Pn = (double *)malloc((size_t)(lp + 1) * sizeof(double));
+    double *Qn = (double *)malloc((size_t)(lq + 1) * sizeof(double));
+    double *Ps = bf16 ? (double *)malloc((size_t)(lp + 1) * sizeof(double)) : NULL;
+    double *Qs = bf16 ? (double *)malloc((size_t)(lq + 1) * sizeof(double)) : NULL;
+    double *err = (double *)malloc((size_t)(nnz + 1) * sizeof(double));
+    int64_t *rptr = (int64_t *)malloc(((size_t)m_t + 1) * sizeof(int64_t));
+    int64_t *cptr = (int64_t *)malloc(((size_t)n_t + 1) * sizeof(int64_t));
+    int64_t *ridx = (int64_t *)malloc((size_t)(nnz + 1) * sizeof(int64_t));
+    int64_t *cidx = (int64_t *)malloc((size_t)(nnz + 1) * sizeof(int64_t));
+    lines_in_input_order(nnz, a, m_t, rptr, ridx);
+    lines_in_input_order(nnz, b, n_t, cptr, cidx);
+    int status = 0;
+    int32_t t;
+    for (t = 0; t <= epochs; ++t) {
+        const double *Pr = P, *Qr = Q;
+        if (bf16) {
+#pragma omp parallel for schedule(static)
+            for (int64_t j = 0; j < lp; ++j) Ps[j] = bf16_round(P[j]);
+#pragma omp parallel for schedule(static)
+            for (int64_t j = 0; j < lq; ++j) Qs[j] = bf16_round(Q[j]);
+            Pr = Ps;
+            Qr = Qs;
+        }
+#pragma omp parallel for schedule(static)
+        for (int64_t e = 0; e < nnz; ++e)
+            err[e] = (double)v[e] - dot(Pr + (int64_t)a[e] * k, Qr + (int64_t)b[e] * k, k);
+        double sse = 0.0;
+        for (int64_t e = 0; e < nnz; ++e) sse += err[e] * err[e];
+        if (loss_hist) loss_hist[t] = sse + lambda * (sumsq(P, lp) + sumsq(Q, lq));
+        if (t == epochs) break;
+        int finite = 1;
+#pragma omp parallel for schedule(dynamic, 64) reduction(&& : finite)
+        for (int32_t x = 0; x < m_t; ++x) {
+            double g[128];
+            for (int32_t c = 0; c < k; ++c) g[c] = 0.0;
+            for (int64_t j = rptr[x]; j < rptr[x + 1]; ++j) {
+                const int64_t e = ridx[j];
+                const double *q = Qr + (int64_t)b[e] * k;
+                for (int32_t c = 0; c < k; ++c) g[c] += -2.0 * err[e] * q[c];
+            }
+            finite = update_row(P + (int64_t)x * k, g, (int32_t)(rptr[x + 1] - rptr[x]), k, lambda, lr, step, 0,
+                                clip, xi, Pn + (int64_t)x * k) && finite;
+        }
+#pragma omp parallel for schedule(dynamic, 16) reduction(&& : finite)
+        for (int32_t x = 0; x < n_t; ++x) {
+            double g[128];
+            for (int32_t c = 0; c < k; ++c) g[c] = 0.0;
+            for (int64_t j = cptr[x]; j < cptr[x + 1]; ++j) {
+                const int64_t e = cidx[j];
+                const double *p = Pr + (int64_t)a[e] * k;
+                for (int32_t c = 0; c < k; ++c) g[c] += -2.0 * err[e] * p[c];
+            }
+            finite = update_row(Q + (int64_t)x * k, g, (int32_t)(cptr[x + 1] - cptr[x]), k, lambda, lr, step, 1,
+                                clip, xi, Qn + (int64_t)x * k) && finite;
+        }
+        if (!finite) {
+            status = 7;
+            break;
+        }
+        memcpy(P, Pn, (size_t)lp * sizeof(double));
+        memcpy(Q, Qn, (size_t)lq * sizeof(double));
+    }
+    if (epochs_done) *epochs_done = t < epochs ? t : epochs;
+    free(Pn); free(Qn); free(Ps); free(Qs); free(err); free(rptr); free(cptr); free(ridx); free(cidx);
+    return status;
+}
+
+int or_threads(void) {
+#ifdef _OPENMP
+    int n = 1;
+#pragma omp parallel
+    {
+#pragma omp single
+        n = omp_get_num_threads();
+    }
+    return n;
+#else
+    return 1;
+#endif
 }
 
 /* ------------------------------------------------------ mini-batch epochs */

@@ -78,6 +78,21 @@ int or_fit(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
            int32_t epochs, double lambda, double lr, int32_t step,
            int32_t clip, double xi, int32_t bf16, double *loss_hist, int32_t *epochs_done);
 
+/* or_fit evaluated line by line, for a build with OpenMP: the residuals of
+ * all entries, their squares summed in input order, then the gradient sum of
+ * every row (and then of every column) over its entries in input order, the
+ * lines split across threads, and the row updates.  Each sum has the
+ * operands and order of or_fit's, so P, Q and loss_hist are the same bits as
+ * or_fit's for any thread count.  Options as or_fit except clip 2 (returns
+ * 1) and k > 128 (returns 1). */
+int or_fit_lines(int64_t nnz, const int32_t *a, const int32_t *b, const float *v,
+                 int32_t m_t, int32_t n_t, int32_t k, double *P, double *Q,
+                 int32_t epochs, double lambda, double lr, int32_t step,
+                 int32_t clip, double xi, int32_t bf16, double *loss_hist, int32_t *epochs_done);
+
+/* Threads an OpenMP build runs its parallel loops with (1 without OpenMP). */
+int or_threads(void);
+
 /* Multi-view similarity term (the item-factor update of Section 5.1 with the
  * similarity regulariser of Eq. 1).  S is a symmetric matrix over the
  * template's columns given as COO entries (s_row, s_col, s_val), both

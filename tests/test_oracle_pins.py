@@ -104,6 +104,35 @@ def test_column_only_step_and_printed_clip_are_not_extension_options(oracle_lib)
     np.testing.assert_allclose(X3, [[0.125, 0.125], [0.25, 0.0]], rtol=1e-15)
 
 
+@pytest.mark.parametrize("case", ["tiny_sum", "ragged_degree_clip", "ragged_col_printed_bf16", "nonfinite"])
+def test_line_parallel_fit_is_the_serial_fit_bit_for_bit(oracle_lib, case):
+    """or_fit_lines (rows, then columns, split across OpenMP threads; the
+    all-core CPU baseline and the oracle of the largest workloads) gives the
+    same bits as the serial or_fit: every sum has the same operands in the
+    same order."""
+    if case == "tiny_sum":
+        p = synth.tiny()
+        opts = dict(step="sum", clip=False, bf16=False, lr=p.lr, epochs=6)
+    else:
+        p = synth.random_case(700, 500, 9000, 300, 200, 32, seed=71, hot_rows=3, hot_cols=2)
+        opts = {"ragged_degree_clip": dict(step="degree", clip=True, bf16=False, lr=0.1, epochs=5),
+                "ragged_col_printed_bf16": dict(step="col_degree", clip="printed", bf16=True, lr=0.01, epochs=5),
+                "nonfinite": dict(step="sum", clip=False, bf16=False, lr=1e5, epochs=40)}[case]
+    st, rm, cm = oracle_lib.template_maps(p.m, p.n, p.I, p.J)
+    a, b, v = oracle_lib.filter_template(p.u, p.i, p.r, rm, cm)
+    ref = oracle_lib.fit(a, b, v, p.P0, p.Q0, opts["epochs"], p.lam, opts["lr"], opts["step"], opts["clip"], 0.05,
+                         bf16=opts["bf16"])
+    for omp in (True, False):
+        got = oracle_lib.fit_lines(a, b, v, p.P0, p.Q0, opts["epochs"], p.lam, opts["lr"], opts["step"], opts["clip"],
+                                   0.05, bf16=opts["bf16"], omp=omp)
+        assert got[0] == ref[0] and got[4] == ref[4]
+        assert np.array_equal(got[1], ref[1]) and np.array_equal(got[2], ref[2])
+        assert np.array_equal(got[3], ref[3], equal_nan=True)
+    if case == "nonfinite":
+        assert ref[0] == 7
+    assert oracle_lib.threads(True) >= 1 and oracle_lib.threads(False) == 1
+
+
 # ------------------------------------------------------------ P1 gradient
 @pytest.mark.parametrize("step", ["sum", "degree"])
 def test_gradient_matches_central_differences(oracle_lib, step):
