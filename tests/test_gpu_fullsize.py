@@ -1,11 +1,19 @@
-"""Parity at full benchmark size, in the launch configuration bench.py times,
-on sampled outputs the oracle can compute one by one.
+"""Parity at full benchmark size, in the launch configuration bench.py times.
 
-One full-gradient epoch from (P0, Q0): the new row p_a depends only on the
-cells of row a and on Q0, so the oracle, given just the cells of a sample of
-rows (or columns), reproduces those rows exactly.  The loss L(P0, Q0) over
-all of Omega* is checked as a whole.
+Sampled: one full-gradient epoch from (P0, Q0): the new row p_a depends
+only on the cells of row a and on Q0, so the oracle, given just the cells of
+a sample of rows (or columns), reproduces those rows exactly.  The loss
+L(P0, Q0) over all of Omega* is checked as a whole.
+
+Whole fits: several epochs over every cell of the template against the
+oracle's line-parallel fit (or_fit_lines built with OpenMP, the same bits as
+the serial oracle): Scientific (fp32) 5 epochs, every factor within 1e-4
+relative Frobenius error; Rating-shaped (bf16) its 20 epochs and
+Billion-scale (bf16) 5 epochs, held-out RMSE within 1e-2 relative.
 """
+import functools
+import time
+
 import numpy as np
 import pytest
 
@@ -14,6 +22,15 @@ import tsid_synth as synth
 from gpu_util import gpu_fit, note, oracle_template, rel_fro
 
 pytestmark = pytest.mark.gpu
+
+
+@functools.lru_cache(maxsize=None)
+def _problem(name):
+    note(f"fullsize: generating {name}")
+    t0 = time.perf_counter()
+    p = synth.make(name)
+    note(f"fullsize: {name} has {p.nnz} training cells ({time.perf_counter() - t0:.0f}s)")
+    return p
 
 
 def _sampled_parity(T, p, n_rows=64, n_cols=64, tol=1e-4):
@@ -79,19 +96,18 @@ def T():
 
 @pytest.mark.timeout(300)
 def test_scientific_fullsize_sampled(T):
-    _sampled_parity(T, synth.scientific_template())
+    _sampled_parity(T, _problem("scientific"))
 
 
 @pytest.mark.timeout(400)
 def test_rating_fullsize_sampled_bf16(T):
-    _sampled_parity(T, synth.rating())
+    _sampled_parity(T, _problem("rating"))
 
 
 @pytest.mark.timeout(900)
 def test_billion_fullsize_sampled_bf16(T):
     """1,000,000 x 100,000 template, about 4.2e8 training cells, k = 128."""
-    note("fullsize billion: generating (a few minutes)")
-    _sampled_parity(T, synth.billion_template())
+    _sampled_parity(T, _problem("billion"))
 
 
 def _batch_ptr(own, rows, beta, B):
@@ -108,7 +124,7 @@ def test_rating_fullsize_minibatch(T):
     rule over all 38.8 M cells, and with one batch the epochs equal the Jacobi
     item-pass epochs bit for bit on every line with a cell (same plans, same
     stream order) while lines without one keep their start rows."""
-    p = synth.rating()
+    p = _problem("rating")
     rm, cm, a, b, v = oracle_template(p)
     note(f"fullsize minibatch rating: building template over {p.nnz} cells")
     T.build_template(p.m, p.n, p.u, p.i, p.r, p.I, p.J, p.k)
@@ -149,7 +165,7 @@ def test_scientific_fullsize_variants_sampled(T):
     the oracle reproduces sampled rows and columns from those alone."""
     import torch
     from paper_2608_00977_amd import make_opts
-    p = synth.scientific_template()
+    p = _problem("scientific")
     rm, cm, a, b, v = oracle_template(p)
     note(f"fullsize scientific variants: building template over {p.nnz} cells")
     T.build_template(p.m, p.n, p.u, p.i, p.r, p.I, p.J, p.k)
@@ -182,3 +198,105 @@ def test_scientific_fullsize_variants_sampled(T):
             ref = Po if out is P1 else Qo
             assert rel_fro(out[idx], ref[idx]) <= 1e-4, (variant, rel_fro(out[idx], ref[idx]))
     T.set_similarity(sr, sc, sv, 0.0)
+
+
+def _oracle_fit_lines(a, b, v, p, epochs, per_call, bf16):
+    """The OpenMP oracle over all cells, a few epochs per call (the state
+    between calls is the fp64 factors, so the bits equal one long call)."""
+    P, Q = p.P0, p.Q0
+    hist = []
+    done = 0
+    while done < epochs:
+        ep = min(per_call, epochs - done)
+        t0 = time.perf_counter()
+        st, P, Q, h, _ = oracle.fit_lines(a, b, v, P, Q, ep, p.lam, p.lr, p.step, p.clip, p.xi, bf16=bf16)
+        assert st == 0
+        hist.extend(h[:-1] if done + ep < epochs else h)
+        done += ep
+        note(f"fullsize oracle: {done}/{epochs} epochs on {oracle.threads()} threads "
+             f"({time.perf_counter() - t0:.0f}s)")
+    return P, Q, np.array(hist)
+
+
+def _heldout_rmse_gpu(p, P, Q):
+    import torch
+    import paper_2608_00977_amd as tsid
+    Tt = tsid.Tsid(0)
+    try:
+        Tt.build_template(p.m, p.n, p.tu, p.ti, p.tr, p.I, p.J, p.k)
+        n_test = Tt.info()["nnz"]
+        sse = Tt.loss(torch.from_numpy(np.ascontiguousarray(P, np.float32)).cuda(),
+                      torch.from_numpy(np.ascontiguousarray(Q, np.float32)).cuda(), 0.0)
+    finally:
+        Tt.close()
+    return float(np.sqrt(sse / max(1, n_test))), n_test
+
+
+def _heldout_rmse_oracle(p, P, Q):
+    st, rm, cm = oracle.template_maps(p.m, p.n, p.I, p.J)
+    a, b, v = oracle.filter_template(p.tu, p.ti, p.tr, rm, cm)
+    st, _, _, h, _ = oracle.fit_lines(a, b, v, P, Q, 0, 0.0, 1.0, "sum", False, 1.0)
+    return float(np.sqrt(h[0] / max(1, a.size))), a.size
+
+
+@pytest.mark.timeout(400)
+def test_scientific_fullsize_five_epochs(T):
+    """Scientific (fp32, k = 32, the slab pass): 5 epochs over all 24 M
+    training cells; every row of P and Q within 1e-4 of the oracle."""
+    p = _problem("scientific")
+    rm, cm, a, b, v = oracle_template(p)
+    T.build_template(p.m, p.n, p.u, p.i, p.r, p.I, p.J, p.k)
+    st, P, Q, hist = gpu_fit(T, p, epochs=5)
+    assert st == 0
+    note(f"fullsize scientific five epochs: pass kernels {T.pass_kernels()}")
+    Po, Qo, ho = _oracle_fit_lines(a, b, v, p, 5, 5, False)
+    eP, eQ = rel_fro(P, Po), rel_fro(Q, Qo)
+    note(f"fullsize scientific: rel err P {eP:.2e} Q {eQ:.2e}")
+    assert eP <= 1e-4 and eQ <= 1e-4
+    np.testing.assert_allclose(hist, ho, rtol=1e-3)
+    assert abs(hist[0] - ho[0]) <= 1e-6 * ho[0]
+
+
+@pytest.mark.timeout(600)
+def test_rating_fullsize_heldout_rmse_bf16(T):
+    """Rating-shaped (bf16, k = 64, clip, dense tiles by the automatic rule):
+    the benchmark's 20 epochs over all 38.8 M training cells; held-out RMSE
+    within 1e-2 relative of the oracle's bf16 mode, and the training loss
+    history within 1e-2."""
+    p = _problem("rating")
+    rm, cm, a, b, v = oracle_template(p)
+    T.build_template(p.m, p.n, p.u, p.i, p.r, p.I, p.J, p.k)
+    st, P, Q, hist = gpu_fit(T, p, epochs=p.epochs)
+    assert st == 0
+    Po, Qo, ho = _oracle_fit_lines(a, b, v, p, p.epochs, 10, True)
+    rg, n_test = _heldout_rmse_gpu(p, P, Q)
+    ro, n_test_o = _heldout_rmse_oracle(p, Po, Qo)
+    note(f"fullsize rating: held-out RMSE gpu {rg:.6f} oracle {ro:.6f} over {n_test} cells; "
+         f"factor rel err P {rel_fro(P, Po):.2e} Q {rel_fro(Q, Qo):.2e}")
+    assert n_test == n_test_o
+    assert abs(rg - ro) <= 1e-2 * ro
+    np.testing.assert_allclose(hist, ho, rtol=1e-2)
+
+
+@pytest.mark.timeout(900)
+def test_billion_fullsize_five_epochs_bf16(T):
+    """Billion-scale (bf16, k = 128, clip, dense tiles and row-blocked Q
+    passes by the automatic rules): 5 epochs over all 4.2e8 training cells;
+    held-out RMSE (4.7e7 cells) within 1e-2 relative of the OpenMP oracle's
+    bf16 mode, and the training loss history within 1e-2."""
+    p = _problem("billion")
+    rm, cm, a, b, v = oracle_template(p)
+    del rm, cm
+    T.build_template(p.m, p.n, p.u, p.i, p.r, p.I, p.J, p.k)
+    st, P, Q, hist = gpu_fit(T, p, epochs=5)
+    assert st == 0
+    note(f"fullsize billion: gpu fit done, row blocks {T.row_blocks()}, dense {T.dense_info()}")
+    Po, Qo, ho = _oracle_fit_lines(a, b, v, p, 5, 2, True)
+    del a, b, v
+    rg, n_test = _heldout_rmse_gpu(p, P, Q)
+    ro, n_test_o = _heldout_rmse_oracle(p, Po, Qo)
+    note(f"fullsize billion: held-out RMSE gpu {rg:.6f} oracle {ro:.6f} over {n_test} cells; "
+         f"factor rel err P {rel_fro(P, Po):.2e} Q {rel_fro(Q, Qo):.2e}")
+    assert n_test == n_test_o
+    assert abs(rg - ro) <= 1e-2 * ro
+    np.testing.assert_allclose(hist, ho, rtol=1e-2)
