@@ -114,3 +114,67 @@ def test_similarity_graph_is_symmetric_and_simple():
     assert all(fw[int(b) * 500 + int(a)] == w for a, b, w in zip(r, c, v))
     r2, c2, v2 = synth.similarity_graph(500, 8, 3)
     assert np.array_equal(r, r2) and np.array_equal(v, v2)
+
+
+def test_scientific_stream_partitions_the_matrix():
+    """Template block + row phase + column phase of the streamed Scientific
+    matrix are exactly the training cells of a brute-force pass over every
+    cell with the generator's two hash tests, and the C generator reproduces
+    the template block's cells and values."""
+    from tsid_synth.generate import _cell_hash, _hash_below, holdout_mask
+    from tsid_synth.stream import _p, lib
+    p = synth.scientific_template(side=192, m=2500)
+    om = synth.omega_outside_template(p)
+    rows, cols = om.row_phase(), om.col_phase()
+    uu, ii = np.meshgrid(np.arange(p.m, dtype=np.uint64), np.arange(p.n, dtype=np.uint64), indexing="ij")
+    train = _hash_below(_cell_hash(uu, ii, p.n, 4, "cells"), 0.1) & ~holdout_mask(uu, ii, p.n, 4)
+    assert rows.nnz + cols.nnz + p.nnz == int(train.sum())
+    # the row phase's cells of each free row are its training cells in the template columns
+    a, fl, _ = rows.cells(np.arange(0, rows.free_ids.size, 97))
+    for f in np.unique(fl)[:5]:
+        u = rows.free_ids[f]
+        want = np.flatnonzero(train[u, p.J])  # template positions
+        assert np.array_equal(np.sort(a[fl == f]), want)
+    # the column phase's cells of a free column: every training row
+    a, fl, _ = cols.cells([3])
+    assert np.array_equal(a, np.flatnonzero(train[:, cols.free_ids[3]]))
+    # the template block through the C generator equals the Python generator's
+    I, J = np.ascontiguousarray(p.I, np.int32), np.ascontiguousarray(p.J, np.int32)
+    cnt = np.empty(I.size, np.int64)
+    lib().sci_count(1, _p(I), I.size, _p(J), J.size, p.n, *om.keys, _p(cnt))
+    off = np.concatenate([[0], np.cumsum(cnt)]).astype(np.int64)
+    f, fl, r = (np.empty(off[-1], t) for t in (np.int32, np.int32, np.float32))
+    lib().sci_fill(1, _p(I), I.size, _p(J), J.size, 1, p.n, *om.keys, _p(om.A), _p(om.Bs), p.k, _p(off), _p(f),
+                   _p(fl), _p(r))
+    kc = I[fl].astype(np.int64) * p.n + f
+    kp = p.u.astype(np.int64) * p.n + p.i
+    oc, op = np.argsort(kc), np.argsort(kp)
+    assert np.array_equal(kc[oc], kp[op])
+    np.testing.assert_allclose(r[oc], p.r[op], rtol=1e-5, atol=1e-5)
+
+
+def test_billion_stream_is_consistent_and_reproducible():
+    """The streamed Billion-scale cells: fixed ids in range, free lines
+    outside the template, values z-scored with the template's scale, any
+    range of lines generated alone gives the same cells, and the template
+    block plus both phases hold about the matrix's expected cells."""
+    p = synth.billion_template(scale=0.02)
+    om = synth.omega_outside_template(p)
+    rows, cols = om.row_phase(), om.col_phase()
+    assert not np.isin(rows.free_ids, p.I).any() and not np.isin(cols.free_ids, p.J).any()
+    total = (rows.nnz + cols.nnz + p.nnz) / 0.9
+    assert abs(total / (1e9 * 0.02 * 0.02) - 1.0) < 0.05
+    for ph, n_fixed in ((rows, p.J.size), (cols, p.m)):
+        fx, fl, r = (np.empty(ph.nnz, t) for t in (np.int32, np.int32, np.float32))
+        assert ph.fill(0, ph.free_ids.size, fx, fl, r) == ph.nnz
+        assert fx.min() >= 0 and fx.max() < n_fixed
+        assert np.array_equal(np.bincount(fl, minlength=ph.free_ids.size), ph.counts)
+        assert np.all(np.diff(fl) >= 0)
+        assert abs(r.mean()) < 0.1 and abs(r.std() - 1.0) < 0.1
+        lines = np.array([1, 7, ph.free_ids.size - 1])
+        a, f2, v = ph.cells(lines)
+        for ln in lines:
+            assert np.array_equal(a[f2 == ln], fx[fl == ln]) and np.array_equal(v[f2 == ln], r[fl == ln])
+        # no repeated cell within a line
+        key = fl.astype(np.int64) * (n_fixed + 1) + fx
+        assert np.unique(key).size == key.size

@@ -30,3 +30,4 @@ from .generate import (  # noqa: F401
     make,
     make_cached,
 )
+from .stream import Phase, omega_outside_template  # noqa: F401,E402

@@ -292,7 +292,7 @@ def scientific_template(seed: int = 4, side: int = 16384, m: int = 200000) -> Pr
     perm = make_rng(seed, "order").permutation(u.size)
     u, i, r = u[perm], i[perm], r[perm]
     return _finish("scientific", m, n, u, i, r, seed, I, J, k, SETTINGS["scientific"],
-                   extra={"omega_scope": "template block only"})
+                   extra={"omega_scope": "template block only", "side": side, "seed": seed})
 
 
 def _zipf_rank_weights(size: int, s: float) -> np.ndarray:
@@ -398,13 +398,18 @@ def billion_template(seed: int = 5, scale: float = 1.0) -> Problem:
     B = gf.normal(0.0, sd, (n_t, k)).astype(np.float32)
     x = _latent_values(a, b, A, B)
     del A, B
-    x -= x.mean()
-    x /= x.std()
+    mu = float(x.mean())
+    x -= mu
+    sd = float(x.std())
+    x /= sd
     u = I[a]
     i = J[b]
     del a, b
+    # the cells outside the block (tsid_synth.stream) share D, the z-scoring
+    # and the scale
     return _finish("billion", m, n, u, i, x.astype(np.float32), seed, I, J, k, SETTINGS["billion"],
-                   extra={"omega_scope": "template block only", "draws": D})
+                   extra={"omega_scope": "template block only", "draws": D, "zmean": mu, "zstd": sd,
+                          "scale": scale, "seed": seed})
 
 
 def random_case(m: int, n: int, nnz: int, m_t: int, n_t: int, k: int, seed: int,
