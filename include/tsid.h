@@ -121,7 +121,9 @@ const char *tsid_last_error(const tsid_ctx *ctx);
  *  k             rank; one of 8, 16, 32, 64, 128.
  * Errors: E_INVAL (NULL with a nonzero size, nnz < 0, bad k, non-finite r in
  * the template), E_RANGE (an id of I, J, u or i out of range), E_DUP (a
- * repeated id in I or J, or a repeated cell inside the template), E_NOMEM,
+ * repeated id in I or J, or a cell (u, i) given twice anywhere in Omega:
+ * when some cells fall outside the template, every cell's key is sorted on
+ * the device, with 24 bytes per cell of temporary device memory), E_NOMEM,
  * E_DEVICE.  Synchronous. */
 tsid_status tsid_build_template(tsid_ctx *ctx, int64_t m, int64_t n,
                                 const int32_t *u, const int32_t *i, const float *r, int64_t nnz,
@@ -203,10 +205,14 @@ tsid_status tsid_loss_noalloc(tsid_ctx *ctx, const float *P, const float *Q, flo
  *  F_free      HOST n_free x k, written when the chunk completes.
  * Asynchronous: the chunk's host-to-device copy runs on the context's copy
  * stream while the previous chunk computes, and the results return on a third
- * stream (Section 5.2, double-buffered pipelining); at most two chunks are in
- * flight and the call blocks only while both staging slots are busy.  All
- * host buffers must stay valid and unchanged until tsid_sync returns.  Pinned
- * host memory is needed for the copies to overlap.
+ * stream (Section 5.2, double-buffered pipelining); two device staging slots
+ * alternate between consecutive chunks.  The call returns once the previous
+ * chunk's host-to-device copy has finished: from then on that chunk's host
+ * input arrays (fixed_id, free_local, r) are no longer read and may be
+ * refilled, so a caller can stream chunks through two pinned host buffers.
+ * Every other host buffer (this chunk's inputs, every F_free) must stay valid
+ * until tsid_sync returns, which also writes the last F_free.  Pinned host
+ * memory is needed for the copies to overlap.
  * Errors returned here: E_STATE (no template: k unknown), E_INVAL, E_NOMEM,
  * E_DEVICE.  Errors found on the device (E_RANGE for ids out of range, E_DUP
  * for a repeated (fixed_id, free_local) cell, E_NONFINITE) are returned by the
@@ -223,12 +229,14 @@ tsid_status tsid_extend_chunk(tsid_ctx *ctx, int side, const int32_t *fixed_id,
  * p = F_fixed[fixed_id], the minimiser that tsid_extend_chunk's gradient
  * steps approach.  The Gram matrices are accumulated on the matrix cores in
  * fp64 (v_mfma_f64_16x16x4f64) and each is factored (Cholesky) and solved in
- * fp64 by one wavefront; F_free receives the fp32 rounding of the solution.
+ * fp64, by one wavefront for k <= 64 (the matrix in registers) and by a
+ * workgroup of four wavefronts for k = 128 (the matrix in 130 KiB of LDS);
+ * F_free receives the fp32 rounding of the solution.
  * A free row without entries gets x_f = 0.
  * Arguments, layout, ownership, asynchrony and the staging slots are those of
  * tsid_extend_chunk; lambda >= 0 replaces the options.
  * Errors returned here: E_STATE (no template), E_INVAL (bad sizes or
- * pointers, lambda negative or not finite, k not in {8, 16, 32, 64}), E_NOMEM,
+ * pointers, lambda negative or not finite, k not in {8, 16, 32, 64, 128}), E_NOMEM,
  * E_DEVICE.  At the next tsid_sync: E_RANGE / E_DUP as for tsid_extend_chunk,
  * and E_NONFINITE when a Gram matrix is not positive definite (lambda = 0 and
  * fewer independent entries than k in some row) or a solution is not finite;
@@ -258,7 +266,7 @@ tsid_status tsid_extend_chunk_ridge(tsid_ctx *ctx, int side, const int32_t *fixe
  * device memory per staging slot grows by 12 n_free n_basis bytes.
  * Errors returned here: E_STATE (no template), E_INVAL (bad sizes or
  * pointers, steps < 0, lambda or eps negative or not finite, lr not finite,
- * beta1 or beta2 outside [0, 1), k not in {8, 16, 32, 64}), E_NOMEM,
+ * beta1 or beta2 outside [0, 1), k not in {8, 16, 32, 64, 128}), E_NOMEM,
  * E_DEVICE.  At the next tsid_sync: E_RANGE / E_DUP as for
  * tsid_extend_chunk, E_NONFINITE if a coefficient becomes non-finite. */
 typedef struct {
@@ -394,13 +402,16 @@ tsid_status tsid_set_minibatch(tsid_ctx *ctx, int32_t n_batches, uint64_t seed);
 
 /* Row-blocked Q passes of the item pass.  The Q pass gathers a row of P for
  * every cell; when P's table (m_t x k, bf16 or fp32) is larger than the
- * last-level cache those gathers go to HBM.  With n blocks the Q pass runs as
- * n launches, launch j walking in every column bucket the run of cells whose
- * row lies in block j (rows [j * ceil(m_t / n), (j + 1) * ceil(m_t / n))) and
- * storing the bucket's partial gradient sum (n x n_t x k fp32 of device
- * memory), then one kernel that adds the n sums of each column in block order
- * and updates it.  The arithmetic is the same; the fp32 sums of a column are
- * added in another order.
+ * last-level cache those gathers go to HBM and the cache hierarchy's miss
+ * bandwidth bounds the pass.  With n blocks, the rows of P are cut into n
+ * ranges holding about equal shares of the Q pass's cells; every column's
+ * cells whose row falls in block j form one work bucket, all blocks run in
+ * one launch, and the workgroups of each group of 8 consecutive blocks are
+ * dealt in turn to the device's 8 XCDs, so that each XCD gathers from its
+ * own block.  Each bucket stores its partial gradient sum
+ * (n x n_t x k fp32 of device memory); a second kernel adds the n sums of a
+ * column in block order and updates it.  The arithmetic is the same; the fp32
+ * sums of a column are added in another order.
  *  n_blocks = 0  (default) automatic: blocks of about 16 MiB of P when the
  *                table exceeds 96 MiB (Billion-scale: 16 blocks), else one.
  *  n_blocks = 1  off.   2 <= n_blocks <= TSID_MAX_ROW_BLOCKS: forced.
@@ -433,7 +444,12 @@ tsid_status tsid_fit_row_blocks(const tsid_ctx *ctx, int32_t *n_blocks);
  *  the passes share a launch, both sides' tiles share one too, counted in
  *  [0];
  *  epoch_ms: from the start of a timed epoch's first kernel to the end of
- *  its last, summed over the timed epochs, whose number is `epochs`.
+ *  its last, summed over the timed epochs, whose number is `epochs`;
+ *  ext_h2d_ms / ext_compute_ms / ext_chunks: for the extension chunks queued
+ *  while timing is on (every chunk, whatever `every`), the host-to-device
+ *  copy of each chunk on the copy stream and its compute on the compute
+ *  stream (bucketing and solve), summed, and the chunk count; a chunk is
+ *  counted once the slot it used is reused or at tsid_sync.
  * Errors: E_INVAL (ctx NULL or every < 0). */
 typedef struct {
     double pass_ms[2];
@@ -446,6 +462,9 @@ typedef struct {
     int64_t epochs;
     double dense_ms[2];
     int64_t dense_launches[2];
+    double ext_h2d_ms;
+    double ext_compute_ms;
+    int64_t ext_chunks;
 } tsid_timing;
 tsid_status tsid_set_timing(tsid_ctx *ctx, int every);
 tsid_status tsid_get_timing(const tsid_ctx *ctx, tsid_timing *out);

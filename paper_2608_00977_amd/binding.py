@@ -49,7 +49,8 @@ class tsid_timing(C.Structure):
                 ("fixup_ms", C.c_double), ("fixup_launches", C.c_int64),
                 ("reduce_ms", C.c_double), ("reduce_launches", C.c_int64),
                 ("epoch_ms", C.c_double), ("epochs", C.c_int64),
-                ("dense_ms", C.c_double * 2), ("dense_launches", C.c_int64 * 2)]
+                ("dense_ms", C.c_double * 2), ("dense_launches", C.c_int64 * 2),
+                ("ext_h2d_ms", C.c_double), ("ext_compute_ms", C.c_double), ("ext_chunks", C.c_int64)]
 
 
 class tsid_adam_opts(C.Structure):
@@ -179,7 +180,8 @@ def tsid_get_timing(ctx) -> dict:
                 fixup_ms=t.fixup_ms, fixup_launches=t.fixup_launches, reduce_ms=t.reduce_ms,
                 reduce_launches=t.reduce_launches, epoch_ms=t.epoch_ms, epochs=t.epochs,
                 dense_ms=[t.dense_ms[0], t.dense_ms[1]],
-                dense_launches=[t.dense_launches[0], t.dense_launches[1]])
+                dense_launches=[t.dense_launches[0], t.dense_launches[1]],
+                ext_h2d_ms=t.ext_h2d_ms, ext_compute_ms=t.ext_compute_ms, ext_chunks=t.ext_chunks)
 
 
 def tsid_set_dense_tiles(ctx, fill: float) -> int:

@@ -108,11 +108,13 @@ __global__ __launch_bounds__(64 * kAdamUpdWaves) void k_adam_update(const AdamAr
 #pragma unroll
     for (int c = 0; c < KQ; ++c) red[wv][lane][c] = qp[c];
     __syncthreads();
-    if (live && lane < K) {
-        const int qq = lane / KQ, cc = lane % KQ;
-        float t = 0.f;
-        for (int r = 0; r < 16; ++r) t += red[wv][r * 4 + qq][cc];
-        A.qpart[((int64_t)f * A.n_slices + s) * K + lane] = t;
+    if (live) {
+        for (int o = lane; o < K; o += 64) {  // coordinate o (two per lane at k = 128)
+            const int qq = o / KQ, cc = o % KQ;
+            float t = 0.f;
+            for (int r = 0; r < 16; ++r) t += red[wv][r * 4 + qq][cc];
+            A.qpart[((int64_t)f * A.n_slices + s) * K + o] = t;
+        }
     }
     if (bad) A.err[ERR_NONFINITE] = 1;
 }
@@ -160,7 +162,7 @@ void adam_k(const AdamArgs &a, int32_t steps, hipStream_t st) {
 
 }  // namespace
 
-bool adam_supported(int K) { return K == 8 || K == 16 || K == 32 || K == 64; }
+bool adam_supported(int K) { return K == 8 || K == 16 || K == 32 || K == 64 || K == 128; }
 
 int32_t adam_slices(int64_t n_b) { return (int32_t)((n_b + 255) / 256); }
 
@@ -171,7 +173,8 @@ void launch_adam(int K, const AdamArgs &a, int32_t steps, hipStream_t s) {
         case 16: adam_k<16>(a, steps, s); break;
         case 32: adam_k<32>(a, steps, s); break;
         case 64: adam_k<64>(a, steps, s); break;
-        default: fail(TSID_E_INVAL, "the Adam extension supports k in {8, 16, 32, 64}");
+        case 128: adam_k<128>(a, steps, s); break;
+        default: fail(TSID_E_INVAL, "the Adam extension supports k in {8, 16, 32, 64, 128}");
     }
 }
 

@@ -161,21 +161,32 @@ struct SimPlan {
     float *se = nullptr;  // ring slots x n_t
 };
 
-// Row-blocked Q passes of the item pass: the gathered P table is split into
-// nb blocks of block_rows rows, each small enough to stay in the last-level
-// cache; block j's pass walks, in every column bucket, the run of cells whose
-// row falls in block j (bounds[j * n_t + x] .. bounds[(j + 1) * n_t + x]) and
-// stores the bucket's partial sum; a combine kernel adds the nb sums in block
-// order and updates the column.  Built over the stream the Q pass walks (the
-// other cells' stream when dense tiles are on).
+// Row-blocked Q passes of the item pass.  The gathered P table is cut into nb
+// blocks of consecutive rows holding about equal shares of the Q pass's cells
+// (row_bounds).  In every column bucket x the run of cells whose row falls in
+// block j (bounds[j * n_t + x] .. bounds[(j + 1) * n_t + x]) is bucket
+// v = j * n_t + x of one combined work plan, in which every block starts on a
+// workgroup boundary; one launch runs all blocks, with the workgroups of each
+// group of 8 consecutive blocks dealt in turn to the 8 XCDs (the dispatcher's
+// order), so that an XCD gathers from its own block of P while the other XCDs
+// gather from theirs.  Each bucket's partial sum goes to part[v]; a combine
+// kernel adds the nb sums of a column in block order and updates it.  Built
+// over the stream the Q pass walks (the other cells' stream when dense tiles
+// are on).
 struct BlockPlan {
     int32_t nb = 0;
     bool dense = false;
-    int64_t block_rows = 0;
-    int64_t *bounds = nullptr;     // (nb + 1) x n_t
-    float *part = nullptr;         // nb x n_t x k
-    std::vector<Plan> plan[2];     // [precision]: nb plans once built
-    int64_t max_items[2] = {0, 0};
+    std::vector<int64_t> hrow_bounds;  // nb + 1 row boundaries (host)
+    int64_t *row_bounds = nullptr;     // the same on the device
+    int64_t *bounds = nullptr;         // (nb + 1) x n_t
+    float *part = nullptr;             // nb x n_t x k
+    struct Combined {
+        bool ready = false;
+        Plan plan;                 // over nb x n_t buckets
+        int32_t *sched = nullptr;  // chunk of each workgroup (-1: idle)
+        int64_t n_wg = 0;
+        float *carry = nullptr;    // one partial sum per wave (carry_per_wave)
+    } comb[2];                     // [precision]
 };
 
 struct Template {
@@ -216,6 +227,10 @@ struct ExtSlot {
     float *Cst = nullptr, *Mst = nullptr, *Vst = nullptr, *qpart = nullptr, *gt = nullptr;
     int64_t adam_cap = 0, qpart_cap = 0, gt_cap = 0;
     hipEvent_t ev_h2d = nullptr, ev_staged = nullptr, ev_done = nullptr, ev_flushed = nullptr;
+    // with timing on: start and end of the chunk's copy (copy stream) and of
+    // its compute (compute stream); pending until read
+    hipEvent_t tm[4] = {nullptr, nullptr, nullptr, nullptr};
+    bool tm_pending = false;
 };
 
 struct ExtState {
@@ -431,10 +446,14 @@ void free_sim(tsid_ctx *c, SimPlan &sp) {
 }
 
 void free_blocks(tsid_ctx *c, BlockPlan &qb) {
+    c->arena.release(qb.row_bounds);
     c->arena.release(qb.bounds);
     c->arena.release(qb.part);
-    for (auto &v : qb.plan)
-        for (Plan &pl : v) free_plan(c, pl);
+    for (auto &cb : qb.comb) {
+        free_plan(c, cb.plan);
+        c->arena.release(cb.sched);
+        c->arena.release(cb.carry);
+    }
     qb = BlockPlan{};
 }
 
@@ -561,6 +580,54 @@ void raise_device_errors(const int32_t *e, const char *where) {
 }
 
 Plan build_plan(tsid_ctx *c, const std::vector<int64_t> &ptr, int32_t rows, int64_t E, int64_t ng);
+
+// E_DUP when a cell (u, i) occurs twice anywhere in Omega: every cell's key
+// u * n + i, streamed from the host in pieces of S, sorted on the device, and
+// neighbours compared.  Needs 24 bytes per cell of temporary device memory.
+void check_omega_unique(tsid_ctx *c, const int32_t *u, const int32_t *i, int64_t nnz, int64_t m, int64_t n,
+                        int64_t S) {
+    Arena &A = c->arena;
+    hipStream_t cs = c->comp;
+    uint64_t *keys = nullptr, *alt = nullptr;
+    uint32_t *vals = nullptr, *valt = nullptr, *tmp = nullptr;
+    int32_t *du = nullptr, *di = nullptr;
+    auto cleanup = [&]() {
+        (void)hipStreamSynchronize(cs);
+        A.release(keys);
+        A.release(alt);
+        A.release(vals);
+        A.release(valt);
+        A.release(tmp);
+        A.release(du);
+        A.release(di);
+    };
+    try {
+        S = std::max<int64_t>(1, std::min<int64_t>(S, nnz));
+        keys = A.alloc<uint64_t>(nnz);
+        alt = A.alloc<uint64_t>(nnz);
+        vals = A.alloc<uint32_t>(nnz);
+        valt = A.alloc<uint32_t>(nnz);
+        tmp = A.alloc<uint32_t>((int64_t)radix_scratch_elems(nnz));
+        du = A.alloc<int32_t>(S);
+        di = A.alloc<int32_t>(S);
+        for (int64_t p0 = 0; p0 < nnz; p0 += S) {
+            const int64_t len = std::min<int64_t>(S, nnz - p0);
+            TSID_HIP(hipMemcpyAsync(du, u + p0, (size_t)len * 4, hipMemcpyHostToDevice, cs));
+            TSID_HIP(hipMemcpyAsync(di, i + p0, (size_t)len * 4, hipMemcpyHostToDevice, cs));
+            cell_keys(du, di, len, n, keys + p0, vals + p0, cs);
+        }
+        const bool in_alt = radix_sort(keys, vals, alt, valt, nnz, bits_for(m * n), tmp, cs);
+        TSID_HIP(hipMemsetAsync(c->err_dev, 0, ERR_SLOTS * sizeof(int32_t), cs));
+        adjacent_equal(in_alt ? alt : keys, nnz, c->err_dev, cs);
+        TSID_HIP(hipMemcpyAsync(c->err_host, c->err_dev, ERR_SLOTS * 4, hipMemcpyDeviceToHost, cs));
+        TSID_HIP(hipStreamSynchronize(cs));
+        if (c->err_host[ERR_DUP]) fail(TSID_E_DUP, "build: a cell (u, i) occurs twice in Omega");
+    } catch (...) {
+        cleanup();
+        throw;
+    }
+    cleanup();
+}
 
 void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i, const float *r,
            int64_t nnz, const int32_t *I, int32_t m_t, const int32_t *J, int32_t n_t, int32_t k,
@@ -742,6 +809,17 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
         throw;
     }
     cleanup();
+    // Omega is a set (Definition 1).  The template's own check sees repeats
+    // among its cells only; when cells fall outside it, all of Omega is
+    // checked as well.
+    if (t->nnz < nnz) {
+        try {
+            check_omega_unique(c, u, i, nnz, m, n, stage ? stage : kDefaultStage);
+        } catch (...) {
+            free_template(c, t);
+            throw;
+        }
+    }
     free_template(c, c->tpl);
     free_fit(c);
     c->tpl = t;
@@ -753,7 +831,15 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
 // multiple of p (idle pad items fill the gaps), so they never straddle two
 // waves and their partial sums are combined inside the pass; only buckets of
 // more than one wave leave partial sums for the fixup kernel.
-Plan build_plan(tsid_ctx *c, const std::vector<int64_t> &ptr, int32_t rows, int64_t E, int64_t ng) {
+// The host layout of such a plan: off / endv (rows + 1) and items; returns
+// the item length it settled on.
+struct PlanLayout {
+    std::vector<uint32_t> off, endv;
+    std::vector<int32_t> items;
+    int64_t E = 64;
+    bool spans = false;
+};
+PlanLayout layout_plan(const std::vector<int64_t> &ptr, int32_t rows, int64_t E, int64_t ng) {
     int64_t maxdeg = 0;
     for (int32_t x = 0; x < rows; ++x) maxdeg = std::max(maxdeg, ptr[x + 1] - ptr[x]);
     // When items up to twice the default length keep every bucket within one
@@ -762,10 +848,10 @@ Plan build_plan(tsid_ctx *c, const std::vector<int64_t> &ptr, int32_t rows, int6
         const int64_t e1 = ((maxdeg + ng - 1) / ng + 15) / 16 * 16;
         if (e1 <= 2 * E) E = e1;
     }
-    std::vector<uint32_t> off((size_t)rows + 1), endv((size_t)rows + 1);
-    std::vector<int32_t> items;
+    PlanLayout L;
+    L.off.resize((size_t)rows + 1);
+    L.endv.resize((size_t)rows + 1);
     int64_t cur = 0;
-    bool spans = false;
     for (int32_t x = 0; x < rows; ++x) {
         const int64_t deg = ptr[x + 1] - ptr[x];
         int64_t p = deg <= E ? 1 : (deg + E - 1) / E;
@@ -775,17 +861,23 @@ Plan build_plan(tsid_ctx *c, const std::vector<int64_t> &ptr, int32_t rows, int6
             p = q;
         } else if (p > ng) {
             p = (p + ng - 1) / ng * ng;
-            spans = true;
+            L.spans = true;
         }
         const int64_t align = p < ng ? p : ng;
         const int64_t start = (cur + align - 1) / align * align;
-        items.resize((size_t)(start + p), -1);
-        for (int64_t j = start; j < start + p; ++j) items[(size_t)j] = x;
-        off[(size_t)x] = (uint32_t)start;
-        endv[(size_t)x] = (uint32_t)(start + p);
+        L.items.resize((size_t)(start + p), -1);
+        for (int64_t j = start; j < start + p; ++j) L.items[(size_t)j] = x;
+        L.off[(size_t)x] = (uint32_t)start;
+        L.endv[(size_t)x] = (uint32_t)(start + p);
         cur = start + p;
     }
     if (cur >= INT32_MAX) fail(TSID_E_INVAL, "work plan too large");
+    L.E = E;
+    return L;
+}
+
+Plan upload_plan(tsid_ctx *c, const PlanLayout &L, int32_t rows) {
+    const int64_t cur = (int64_t)L.items.size();
     Arena &A = c->arena;
     uint32_t *d_off = nullptr, *d_end = nullptr;
     int32_t *d_items = nullptr;
@@ -794,10 +886,10 @@ Plan build_plan(tsid_ctx *c, const std::vector<int64_t> &ptr, int32_t rows, int6
         d_end = A.alloc<uint32_t>((int64_t)rows + 1);
         d_items = A.alloc<int32_t>(cur);
         hipStream_t cs = c->comp;
-        TSID_HIP(hipMemcpyAsync(d_off, off.data(), ((size_t)rows + 1) * 4, hipMemcpyHostToDevice, cs));
-        TSID_HIP(hipMemcpyAsync(d_end, endv.data(), ((size_t)rows + 1) * 4, hipMemcpyHostToDevice, cs));
-        if (cur) TSID_HIP(hipMemcpyAsync(d_items, items.data(), (size_t)cur * 4, hipMemcpyHostToDevice, cs));
-        TSID_HIP(hipStreamSynchronize(cs));  // the host vectors go out of scope
+        TSID_HIP(hipMemcpyAsync(d_off, L.off.data(), ((size_t)rows + 1) * 4, hipMemcpyHostToDevice, cs));
+        TSID_HIP(hipMemcpyAsync(d_end, L.endv.data(), ((size_t)rows + 1) * 4, hipMemcpyHostToDevice, cs));
+        if (cur) TSID_HIP(hipMemcpyAsync(d_items, L.items.data(), (size_t)cur * 4, hipMemcpyHostToDevice, cs));
+        TSID_HIP(hipStreamSynchronize(cs));  // the host vectors may go out of scope
     } catch (...) {
         A.release(d_off);
         A.release(d_end);
@@ -809,10 +901,14 @@ Plan build_plan(tsid_ctx *c, const std::vector<int64_t> &ptr, int32_t rows, int6
     pl.item_end = d_end;
     pl.items = d_items;
     pl.n_items = (int32_t)cur;
-    pl.E = (int32_t)E;
-    pl.spans = spans;
+    pl.E = (int32_t)L.E;
+    pl.spans = L.spans;
     pl.ready = true;
     return pl;
+}
+
+Plan build_plan(tsid_ctx *c, const std::vector<int64_t> &ptr, int32_t rows, int64_t E, int64_t ng) {
+    return upload_plan(c, layout_plan(ptr, rows, E, ng), rows);
 }
 
 void ensure_plan(tsid_ctx *c, int side, int prec) {
@@ -1251,22 +1347,32 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs, bool dense, i
 }
 
 // Row blocks of the Q pass for this fit: automatic when the gathered P table
-// exceeds TSID_QBLOCK_MIN_MB (blocks of about TSID_QBLOCK_MB), else one.
+// exceeds TSID_QBLOCK_MIN_MB (blocks of about TSID_QBLOCK_MB of the table
+// each, at most TSID_MAX_ROW_BLOCKS), else one.  More blocks raise the L2 hit
+// rate of the gathers (Billion-scale: 53 % with 16, 76 % with 64) but cut
+// the columns' runs shorter, and the per-run work (owner row, partial sum)
+// then outweighs it (Q pass 6.1 ms with 16 blocks, 6.3 with 32, 7.2 with 64).
 #ifndef TSID_QBLOCK_MB
 #define TSID_QBLOCK_MB 16
 #endif
 #ifndef TSID_QBLOCK_MIN_MB
 #define TSID_QBLOCK_MIN_MB 96
 #endif
+// XCDs of the device (gfx950: 8); the dispatcher hands consecutive
+// workgroups to them in turn.
+constexpr int kXcds = 8;
+
 int32_t ensure_qblock(tsid_ctx *c, int prec) {
     Template &t = *c->tpl;
     BlockPlan &qb = t.qb;
     const int64_t table = (int64_t)t.m_t * t.k * (prec == TSID_BF16 ? 2 : 4);
     int32_t nb = c->row_blocks;
     if (nb == 0)
-        nb = table > (int64_t)TSID_QBLOCK_MIN_MB << 20 ? (int32_t)((table + ((int64_t)TSID_QBLOCK_MB << 20) - 1) /
-                                                                  ((int64_t)TSID_QBLOCK_MB << 20))
-                                                        : 1;
+        nb = table > (int64_t)TSID_QBLOCK_MIN_MB << 20
+                 ? (int32_t)std::min<int64_t>((table + ((int64_t)TSID_QBLOCK_MB << 20) - 1) /
+                                                  ((int64_t)TSID_QBLOCK_MB << 20),
+                                              TSID_MAX_ROW_BLOCKS)
+                 : 1;
     nb = (int32_t)std::min<int64_t>(nb, std::max<int32_t>(1, t.m_t));
     if (nb <= 1 || t.n_t == 0 || t.slab[1].use) return 1;
     const bool dn = t.dense_use && prec == TSID_BF16;
@@ -1275,11 +1381,36 @@ int32_t ensure_qblock(tsid_ctx *c, int prec) {
     if (qb.nb != nb || qb.dense != dn) {
         free_blocks(c, qb);
         try {
-            qb.block_rows = (t.m_t + nb - 1) / nb;
+            // the cells the Q pass walks, counted by their row (the P row it
+            // gathers); block j starts at the first row with at least
+            // j / nb of them before it
+            std::vector<int64_t> rptr;
+            if (dn) {
+                rptr.resize((size_t)t.m_t + 1);
+                TSID_HIP(hipMemcpy(rptr.data(), t.dense.sparse_ptr[0], rptr.size() * 8, hipMemcpyDeviceToHost));
+            }
+            const std::vector<int64_t> &rp = dn ? rptr : t.hptr[0];
+            const int64_t total = rp[(size_t)t.m_t];
+            qb.hrow_bounds.assign((size_t)nb + 1, (int64_t)t.m_t);
+            qb.hrow_bounds[0] = 0;
+            const bool equal_rows = std::getenv("TSID_QBLOCK_EQUAL_ROWS") != nullptr;  // tuning knob
+            int64_t r = 0;
+            for (int32_t j = 1; j < nb; ++j) {
+                if (equal_rows || total == 0) {
+                    qb.hrow_bounds[(size_t)j] = std::min<int64_t>((int64_t)j * ((t.m_t + nb - 1) / nb), t.m_t);
+                    continue;
+                }
+                const int64_t target = (int64_t)(((__int128)j * total + nb - 1) / nb);
+                while (r < t.m_t && rp[(size_t)r] - rp[0] < target) ++r;
+                qb.hrow_bounds[(size_t)j] = r;
+            }
+            qb.row_bounds = A.alloc<int64_t>((int64_t)nb + 1);
             qb.bounds = A.alloc<int64_t>((int64_t)(nb + 1) * t.n_t);
             qb.part = A.alloc<float>((int64_t)nb * t.n_t * t.k);
+            TSID_HIP(hipMemcpyAsync(qb.row_bounds, qb.hrow_bounds.data(), ((size_t)nb + 1) * 8, hipMemcpyHostToDevice,
+                                    cs));
             launch_block_bounds(dn ? t.dense.sparse[1] : t.stream_c, dn ? t.dense.sparse_ptr[1] : t.col_ptr, t.n_t,
-                                nb, qb.block_rows, qb.bounds, cs);
+                                nb, qb.row_bounds, qb.bounds, cs);
             TSID_HIP(hipStreamSynchronize(cs));
         } catch (...) {
             free_blocks(c, qb);
@@ -1288,27 +1419,68 @@ int32_t ensure_qblock(tsid_ctx *c, int prec) {
         qb.nb = nb;
         qb.dense = dn;
     }
-    if (qb.plan[prec].empty()) {
+    BlockPlan::Combined &cb = qb.comb[prec];
+    if (!cb.ready) {
         const int64_t n = (int64_t)(nb + 1) * t.n_t;
         std::vector<int64_t> hb((size_t)n);
         TSID_HIP(hipMemcpy(hb.data(), qb.bounds, (size_t)n * 8, hipMemcpyDeviceToHost));
         const int64_t E = choose_E(std::max<int64_t>(1, (dn ? t.dense.sparse_nnz : t.nnz) / nb));
-        const int ng = items_per_wave(t.k, prec);
-        int64_t most = 0;
-        try {
-            for (int32_t j = 0; j < nb; ++j) {
-                std::vector<int64_t> fake((size_t)t.n_t + 1, 0);  // prefix sums of the runs' lengths
-                for (int32_t x = 0; x < t.n_t; ++x)
-                    fake[(size_t)x + 1] = fake[(size_t)x] + hb[(size_t)(j + 1) * t.n_t + x] - hb[(size_t)j * t.n_t + x];
-                qb.plan[prec].push_back(build_plan(c, fake, t.n_t, E, ng));
-                most = std::max<int64_t>(most, qb.plan[prec].back().n_items);
+        const int ng = items_per_wave(t.k, prec), wg = items_per_workgroup(t.k, prec);
+        const int64_t nv = (int64_t)nb * t.n_t;
+        if (nv >= INT32_MAX) fail(TSID_E_INVAL, "too many row-block buckets");
+        PlanLayout C;
+        C.off.resize((size_t)nv + 1);
+        C.endv.resize((size_t)nv + 1);
+        C.E = E;
+        std::vector<int64_t> base((size_t)nb), chunks((size_t)nb);
+        int64_t cur = 0;
+        for (int32_t j = 0; j < nb; ++j) {
+            std::vector<int64_t> fake((size_t)t.n_t + 1, 0);  // prefix sums of the runs' lengths
+            for (int32_t x = 0; x < t.n_t; ++x)
+                fake[(size_t)x + 1] = fake[(size_t)x] + hb[(size_t)(j + 1) * t.n_t + x] - hb[(size_t)j * t.n_t + x];
+            const PlanLayout L = layout_plan(fake, t.n_t, E, ng);
+            const int64_t b0 = (cur + wg - 1) / wg * wg;  // every block starts a workgroup
+            const int64_t nj = (int64_t)L.items.size();
+            if (b0 + nj >= INT32_MAX) fail(TSID_E_INVAL, "row-block work plan too large");
+            C.items.resize((size_t)(b0 + nj), -1);
+            for (int64_t it = 0; it < nj; ++it)
+                if (L.items[(size_t)it] >= 0) C.items[(size_t)(b0 + it)] = (int32_t)((int64_t)j * t.n_t + L.items[(size_t)it]);
+            for (int32_t x = 0; x < t.n_t; ++x) {
+                C.off[(size_t)j * t.n_t + x] = (uint32_t)(b0 + L.off[(size_t)x]);
+                C.endv[(size_t)j * t.n_t + x] = (uint32_t)(b0 + L.endv[(size_t)x]);
             }
+            C.spans = C.spans || L.spans;
+            base[(size_t)j] = b0;
+            chunks[(size_t)j] = (nj + wg - 1) / wg;
+            cur = b0 + nj;
+        }
+        C.off[(size_t)nv] = C.endv[(size_t)nv] = (uint32_t)cur;
+        // workgroup schedule: groups of kXcds consecutive blocks; in a group,
+        // workgroup w takes the next chunk of block (group start + w % kXcds)
+        std::vector<int32_t> sched;
+        for (int32_t g0 = 0; g0 < nb; g0 += kXcds) {
+            int64_t most = 0;
+            for (int32_t j = g0; j < std::min(nb, g0 + kXcds); ++j) most = std::max(most, chunks[(size_t)j]);
+            for (int64_t ch = 0; ch < most; ++ch)
+                for (int x = 0; x < kXcds; ++x) {
+                    const int32_t j = g0 + x;
+                    sched.push_back(j < nb && ch < chunks[(size_t)j] ? (int32_t)(base[(size_t)j] / wg + ch) : -1);
+                }
+        }
+        try {
+            cb.plan = upload_plan(c, C, (int32_t)nv);
+            cb.sched = A.alloc<int32_t>((int64_t)sched.size());
+            TSID_HIP(hipMemcpy(cb.sched, sched.data(), sched.size() * 4, hipMemcpyHostToDevice));
+            cb.n_wg = (int64_t)sched.size();
+            cb.carry = A.alloc<float>((cur / ng + 1) * t.k);
         } catch (...) {
-            for (Plan &pl : qb.plan[prec]) free_plan(c, pl);
-            qb.plan[prec].clear();
+            free_plan(c, cb.plan);
+            A.release(cb.sched);
+            A.release(cb.carry);
+            cb = BlockPlan::Combined{};
             throw;
         }
-        qb.max_items[prec] = most;
+        cb.ready = true;
     }
     return nb;
 }
@@ -1606,7 +1778,6 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     if (c->mb_batches > 0) return fit_minibatch(c, P, Q, o, loss_hist);
     ensure_fit_buffers(c, o->prec, o->epochs, o->clip != 2, 0, o->clip == 2 || sim.on);
     const int32_t nb = ensure_qblock(c, o->prec);  // row blocks of the Q pass (1: one pass)
-    if (nb > 1) ensure_fit_buffers(c, o->prec, o->epochs, o->clip != 2, t.qb.max_items[o->prec], o->clip == 2 || sim.on);
     c->used_blocks = nb;
     c->epochs_done = 0;
     FitBufs &f = c->fb;
@@ -1766,25 +1937,31 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
             ac.e2 = nullptr;
             ac.norm = normq;
             if (nb > 1) {
-                // one pass per row block (its gathers stay in the last-level
-                // cache), each leaving per-column partial sums; then the
-                // combine kernel adds them in block order and updates Q
-                for (int32_t j = 0; j < nb; ++j) {
-                    PassArgs bj = ac;
-                    const Plan &pl = t.qb.plan[prec][(size_t)j];
-                    bj.ptr = t.qb.bounds + (int64_t)j * t.n_t;
-                    bj.ptr_end = t.qb.bounds + (int64_t)(j + 1) * t.n_t;
-                    bj.items = pl.items;
-                    bj.item_off = pl.item_off;
-                    bj.item_end = pl.item_end;
-                    bj.n_items = pl.n_items;
-                    bj.E = pl.E;
-                    bj.norm = nullptr;
-                    bj.partial_out = t.qb.part + (int64_t)j * t.n_t * K;
-                    launch_item_pass(K, prec, false, bj, cs, j == 0 ? ev.first : nullptr, nullptr);
-                    if (pl.spans) launch_fixup(K, prec, bj, cs);
-                }
-                launch_block_combine(K, prec, ac, t.qb.part, nb, cs, nullptr, ev.second);
+                // every row block in one launch, each XCD on its own block of
+                // P at a time, each (block, column) run leaving its partial
+                // sum; then the combine kernel adds them in block order and
+                // updates Q
+                const BlockPlan::Combined &cb = t.qb.comb[prec];
+                PassArgs bj = ac;
+                bj.ptr = t.qb.bounds;
+                bj.ptr_end = t.qb.bounds + t.n_t;
+                bj.rows = (int32_t)((int64_t)nb * t.n_t);
+                bj.owner_mod = t.n_t;
+                bj.items = cb.plan.items;
+                bj.item_off = cb.plan.item_off;
+                bj.item_end = cb.plan.item_end;
+                bj.n_items = cb.plan.n_items;
+                bj.E = cb.plan.E;
+                bj.carry = cb.carry;
+                bj.carry_per_wave = 1;
+                bj.norm = nullptr;
+                bj.partial_out = t.qb.part;
+                launch_item_pass_sched(K, prec, bj, cb.sched, cb.n_wg, cs, ev.first, ev.second);
+                // the fixup of runs longer than a wave and the combine are
+                // timed as the Q pass's fixups
+                ev = timed(c, ep, TK_QFIX);
+                if (cb.plan.spans) launch_fixup(K, prec, bj, cs, ev.first, nullptr);
+                launch_block_combine(K, prec, ac, t.qb.part, nb, cs, cb.plan.spans ? nullptr : ev.first, ev.second);
             } else if (item_pair) {
                 launch_item_pass_pair(K, prec, ar, ac, cs, ev_p.first, ev_p.second);
                 if ((dn ? t.dense.plan[0] : t.plan[0][prec]).spans) {
@@ -2059,6 +2236,18 @@ void adam_ensure(tsid_ctx *c, ExtSlot &s, int64_t n_free, int64_t n_b, int K) {
 // One chunk of the extension: staging, bucketing by free row, then the
 // one-sided gradient steps of `o`, or (ridge != null) the exact solve with
 // lambda = *ridge, or (adam != null) Adam on the coefficients in a basis.
+// Adds a finished chunk's copy and compute durations to the timing totals.
+void ext_take_timing(tsid_ctx *c, ExtSlot &s) {
+    if (!s.tm_pending) return;
+    float h = 0.f, k = 0.f;
+    TSID_HIP(hipEventElapsedTime(&h, s.tm[0], s.tm[1]));
+    TSID_HIP(hipEventElapsedTime(&k, s.tm[2], s.tm[3]));
+    c->tm.ext_h2d_ms += h;
+    c->tm.ext_compute_ms += k;
+    c->tm.ext_chunks += 1;
+    s.tm_pending = false;
+}
+
 void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t *free_local,
                   const float *r, int64_t nnz, int32_t n_free, const float *F_fixed, int64_t n_fixed,
                   float *F_free, const tsid_fit_opts *o, const float *ridge, const AdamReq *adam = nullptr) {
@@ -2072,13 +2261,13 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
         if (!(ao->beta1 >= 0.f && ao->beta1 < 1.f) || !(ao->beta2 >= 0.f && ao->beta2 < 1.f))
             fail(TSID_E_INVAL, "beta1 and beta2 must lie in [0, 1)");
         if (!(ao->eps >= 0.f) || !std::isfinite(ao->eps)) fail(TSID_E_INVAL, "eps must be finite and >= 0");
-        if (!adam_supported(c->tpl->k)) fail(TSID_E_INVAL, "the Adam extension supports k in {8, 16, 32, 64}");
+        if (!adam_supported(c->tpl->k)) fail(TSID_E_INVAL, "the Adam extension supports k in {8, 16, 32, 64, 128}");
         if (adam->n_b < 1 || adam->n_b >= (int64_t(1) << 31)) fail(TSID_E_INVAL, "n_basis out of range");
         if (!adam->basis) fail(TSID_E_INVAL, "basis is NULL");
         check_aligned(adam->basis, "basis");
     } else if (ridge) {
         if (!(*ridge >= 0.f) || !std::isfinite(*ridge)) fail(TSID_E_INVAL, "lambda must be finite and >= 0");
-        if (!ridge_supported(c->tpl->k)) fail(TSID_E_INVAL, "the exact extension solve supports k in {8, 16, 32, 64}");
+        if (!ridge_supported(c->tpl->k)) fail(TSID_E_INVAL, "the exact extension solve supports k in {8, 16, 32, 64, 128}");
     } else {
         check_opts(o);
         if (o->clip == 2) fail(TSID_E_INVAL, "per-entry clipping (clip 2) is a template-fit option");
@@ -2099,15 +2288,27 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
     x.next ^= 1;
     ExtSlot &s = x.slot[si];
     hipStream_t cs = c->comp;
+    const bool tmo = c->timing > 0;
+    if (tmo) {
+        if (s.tm_pending) {  // the slot's previous chunk: finished before its events are reused
+            TSID_HIP(hipEventSynchronize(s.tm[3]));
+            ext_take_timing(c, s);
+        }
+        for (auto &e : s.tm)
+            if (!e) TSID_HIP(hipEventCreate(&e));
+    }
     // stage the chunk (copy stream), after the slot's previous chunk consumed it
     TSID_HIP(hipStreamWaitEvent(c->h2d, s.ev_staged, 0));
+    if (tmo) TSID_HIP(hipEventRecord(s.tm[0], c->h2d));
     if (nnz) {
         TSID_HIP(hipMemcpyAsync(s.fid, fixed_id, (size_t)nnz * 4, hipMemcpyHostToDevice, c->h2d));
         TSID_HIP(hipMemcpyAsync(s.free_id, free_local, (size_t)nnz * 4, hipMemcpyHostToDevice, c->h2d));
         TSID_HIP(hipMemcpyAsync(s.r, r, (size_t)nnz * 4, hipMemcpyHostToDevice, c->h2d));
     }
     TSID_HIP(hipEventRecord(s.ev_h2d, c->h2d));
+    if (tmo) TSID_HIP(hipEventRecord(s.tm[1], c->h2d));
     TSID_HIP(hipStreamWaitEvent(cs, s.ev_h2d, 0));
+    if (tmo) TSID_HIP(hipEventRecord(s.tm[2], cs));
     // bucket the chunk by free row: key = free << bits_fixed | fixed (stable sort)
     const int bits_fixed = bits_for(std::max<int64_t>(n_fixed, 1));
     const int bits_free = bits_for(std::max<int32_t>(n_free, 1));
@@ -2189,6 +2390,10 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
         // every step of every free row in one launch (one wave per free row)
         launch_extend_steps(K, a, o->epochs, cs);
     }
+    if (tmo) {
+        TSID_HIP(hipEventRecord(s.tm[3], cs));
+        s.tm_pending = true;
+    }
     TSID_HIP(hipEventRecord(s.ev_done, cs));
     // flush the results on the third stream
     TSID_HIP(hipStreamWaitEvent(c->d2h, s.ev_done, 0));
@@ -2198,11 +2403,17 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
         TSID_HIP(hipMemcpyAsync(adam->C_out, s.Cst, (size_t)n_free * adam->n_b * 4, hipMemcpyDeviceToHost, c->d2h));
     TSID_HIP(hipEventRecord(s.ev_flushed, c->d2h));
     x.pending = true;
+    // The previous chunk (the other slot) was queued before this one; once
+    // its host-to-device copy has finished, its host input arrays are free
+    // for the caller to refill, so two pinned host buffers can feed the
+    // stream while this chunk's copy and the previous chunk's compute run.
+    TSID_HIP(hipEventSynchronize(x.slot[si ^ 1].ev_h2d));
     (void)side;
 }
 
 void sync(tsid_ctx *c) {
     ext_sync_all(c);
+    for (auto &s : c->ext.slot) ext_take_timing(c, s);
     ExtState &x = c->ext;
     if (!x.err) return;
     int32_t e[ERR_SLOTS];
@@ -2315,6 +2526,8 @@ void tsid_destroy(tsid_ctx *c) {
         if (s.ev_staged) (void)hipEventDestroy(s.ev_staged);
         if (s.ev_done) (void)hipEventDestroy(s.ev_done);
         if (s.ev_flushed) (void)hipEventDestroy(s.ev_flushed);
+        for (auto &e : s.tm)
+            if (e) (void)hipEventDestroy(e);
     }
     for (hipEvent_t e : c->events) (void)hipEventDestroy(e);
     c->arena.release(c->err_dev);

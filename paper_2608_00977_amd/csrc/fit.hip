@@ -430,7 +430,8 @@ __device__ __forceinline__ void item_pass_group(const PassArgs &A, const int64_t
         const int64_t deg = re - rb, parts = (int64_t)(i1 - i0), q = item - (int64_t)i0;
         beg = rb + q * deg / parts;
         end = rb + (q + 1) * deg / parts;
-        load_f32<V>(A.X + (int64_t)row * K + lg * V, x);
+        const int64_t orow = A.owner_mod ? row % A.owner_mod : row;
+        load_f32<V>(A.X + orow * K + lg * V, x);
     } else {
 #pragma unroll
         for (int v = 0; v < V; ++v) x[v] = 0.f;
@@ -520,7 +521,7 @@ __device__ __forceinline__ void item_pass_group(const PassArgs &A, const int64_t
             if (item == (int64_t)i0 && seg_last == (int64_t)i1 - 1) {
                 finalize_row<G, V, BF16>(A, row, lg, x, acc, re - A.ptr[row]);
             } else {
-                store_f32<V>(A.carry + item * K + lg * V, acc);
+                store_f32<V>(A.carry + (A.carry_per_wave ? item / NG : item) * K + lg * V, acc);
             }
         }
     }
@@ -545,6 +546,18 @@ __global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass_pair(cons
         item_pass_group<K, V, BF16, false, BUF, PE>(A1, b - b0);
 }
 
+// The item pass over a plan laid out in workgroup-sized chunks, in the order
+// the host chose (sched[w]: the chunk of workgroup w, < 0 for none).  The
+// row-blocked Q pass uses it to give each XCD its own block of the gathered
+// table: the dispatcher hands workgroups to the XCDs in turn, so workgroup w
+// runs on XCD w % 8.
+template <int K, int V, bool BF16, bool BUF, bool PE>
+__global__ __launch_bounds__(kThreads) TSID_OCCUPANCY void k_item_pass_sched(const PassArgs A, const int32_t *sched) {
+    const int32_t chunk = sched[blockIdx.x];
+    if (chunk < 0) return;
+    item_pass_group<K, V, BF16, false, BUF, PE>(A, chunk);
+}
+
 // Split buckets: add the item partial sums in item order, then update the row.
 template <int K, int V, bool BF16>
 __global__ __launch_bounds__(kThreads) void k_fixup(const PassArgs A) {
@@ -565,23 +578,23 @@ __global__ __launch_bounds__(kThreads) void k_fixup(const PassArgs A) {
     // the bucket's first item and every later item that starts a wave
     for (uint32_t it = i0; it < i1; it = (it / NG + 1) * NG) {
         float part[V];
-        load_f32<V>(A.carry + (int64_t)it * K + lg * V, part);
+        load_f32<V>(A.carry + (int64_t)(A.carry_per_wave ? it / NG : it) * K + lg * V, part);
 #pragma unroll
         for (int v = 0; v < V; ++v) acc[v] += part[v];
     }
     float x[V];
-    load_f32<V>(A.X + row * K + lg * V, x);
+    load_f32<V>(A.X + (A.owner_mod ? row % A.owner_mod : row) * K + lg * V, x);
     finalize_row<G, V, BF16>(A, (int)row, lg, x, acc, A.ptr[row + 1] - A.ptr[row]);
 }
 
 // Row-blocked passes.  Bounds of every bucket's runs of other indices per
 // block (binary search inside the bucket; one thread per bucket and block).
 __global__ void k_block_bounds(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_blocks,
-                               int64_t block_rows, int64_t *bounds) {
+                               const int64_t *row_bounds, int64_t *bounds) {
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (t >= (int64_t)(n_blocks + 1) * rows) return;
     const int64_t j = t / rows, x = t % rows;
-    const int64_t target = j * block_rows;
+    const int64_t target = row_bounds[j];
     int64_t lo = ptr[x], hi = ptr[x + 1];  // first position whose other index >= target
     while (lo < hi) {
         const int64_t mid = lo + ((hi - lo) >> 1);
@@ -800,6 +813,25 @@ void item_pass_kv(bool loss_only, const PassArgs &a, hipStream_t s, hipEvent_t e
     TSID_HIP(hipGetLastError());
 }
 
+template <int K, int V, bool BF16>
+void item_pass_sched_kv(const PassArgs &a, const int32_t *sched, int64_t n_wg, hipStream_t s, hipEvent_t ev0,
+                        hipEvent_t ev1) {
+    if (n_wg <= 0) return;
+    if (n_wg > INT32_MAX) fail(TSID_E_INVAL, "too many workgroups");
+    const bool buf = a.y_rows * (int64_t)K * (BF16 ? 2 : 4) < (int64_t(1) << 31);
+    auto go = [&](auto kernel) {
+        hipExtLaunchKernelGGL(kernel, dim3((unsigned)n_wg), dim3(kThreads), 0, s, ev0, ev1, 0, a, sched);
+    };
+    if (a.clip == 2) {
+        if (buf) go(k_item_pass_sched<K, V, BF16, true, true>);
+        else go(k_item_pass_sched<K, V, BF16, false, true>);
+    } else {
+        if (buf) go(k_item_pass_sched<K, V, BF16, true, false>);
+        else go(k_item_pass_sched<K, V, BF16, false, false>);
+    }
+    TSID_HIP(hipGetLastError());
+}
+
 // Both sides' passes in one launch when their gathers use the same addressing;
 // else two launches (ev0 on the first, ev1 on the second).
 template <int K, int V, bool BF16>
@@ -921,12 +953,17 @@ void launch_block_combine(int K, int prec, const PassArgs &a, const float *part,
     TSID_DISPATCH_K(K, block_combine_kv, a, part, n_blocks, s, ev0, ev1)
 }
 
-void launch_block_bounds(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_blocks, int64_t block_rows,
-                         int64_t *bounds, hipStream_t s) {
+void launch_block_bounds(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_blocks,
+                         const int64_t *row_bounds, int64_t *bounds, hipStream_t s) {
     const int64_t n = (int64_t)(n_blocks + 1) * rows;
     if (n <= 0) return;
-    k_block_bounds<<<ceil_div(n, 256), 256, 0, s>>>(stream, ptr, rows, n_blocks, block_rows, bounds);
+    k_block_bounds<<<ceil_div(n, 256), 256, 0, s>>>(stream, ptr, rows, n_blocks, row_bounds, bounds);
     TSID_HIP(hipGetLastError());
+}
+
+void launch_item_pass_sched(int K, int prec, const PassArgs &a, const int32_t *sched, int64_t n_wg, hipStream_t s,
+                            hipEvent_t ev0, hipEvent_t ev1) {
+    TSID_DISPATCH_K(K, item_pass_sched_kv, a, sched, n_wg, s, ev0, ev1)
 }
 
 void launch_extend_steps(int K, const PassArgs &a, int32_t steps, hipStream_t s) {
@@ -944,6 +981,8 @@ int items_per_wave(int K, int prec) {
     TSID_DISPATCH_K(K, groups_per_wave_kv, out)
     return out;
 }
+
+int items_per_workgroup(int K, int prec) { return kWaves * items_per_wave(K, prec); }
 
 void launch_row_norms(int K, const float *X, int32_t rows, float *norm, hipStream_t s) {
     if (rows <= 0) return;

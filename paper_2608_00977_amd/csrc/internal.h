@@ -84,6 +84,11 @@ void filter_write(const int32_t *u, const int32_t *i, const float *r, int64_t S,
 
 // After a sort on packed keys: stream[j] = {key & low_mask, value}; flags a
 // repeated key as ERR_DUP.
+// keys[j] = u[j] * n + i[j] (and vals[j] = 0) for a piece of Omega.
+void cell_keys(const int32_t *u, const int32_t *i, int64_t len, int64_t n, uint64_t *keys, uint32_t *vals,
+               hipStream_t s);
+// err[ERR_DUP] = 1 if two neighbours of the sorted keys are equal.
+void adjacent_equal(const uint64_t *keys, int64_t n, int32_t *err, hipStream_t s);
 void keys_to_stream(const uint64_t *keys, const uint32_t *vals, int64_t n, int low_bits,
                     int2 *stream, int32_t *err, hipStream_t s);
 // ptr[x] = first position whose key >> low_bits >= x, for x in [0, rows].
@@ -153,11 +158,26 @@ struct PassArgs {
     // (rows x K) instead of updating the row.
     const int64_t *ptr_end;
     float *partial_out;
+    // Row-blocked passes in one launch: buckets are (block, owner) pairs
+    // v = block * owner_mod + owner, so the owner row is v % owner_mod (0: the
+    // bucket is the owner row).
+    int32_t owner_mod;
+    // 1: the partial sum a wave leaves for a bucket longer than one wave sits
+    // at carry + (item / groups per wave) * K, one per wave (plans built on
+    // the host, whose longer buckets fill whole waves); 0: at carry + item * K.
+    int32_t carry_per_wave;
 };
 
 // prec: 0 fp32, 1 bf16.  loss_only: residuals, e2 and norms only.
 // ev0 / ev1 (may be null): HIP events that take the kernel's own start and end
 // timestamps (attached to its dispatch; no extra packets on the stream).
+// The item pass over a plan laid out in workgroup-sized chunks: workgroup w
+// runs the chunk sched[w] (its first item / (waves * groups per wave)), or
+// nothing when sched[w] < 0.  Not for loss-only passes.
+void launch_item_pass_sched(int K, int prec, const PassArgs &a, const int32_t *sched, int64_t n_wg, hipStream_t s,
+                            hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+// Items of one workgroup of the item pass (waves per workgroup x groups per wave).
+int items_per_workgroup(int K, int prec);
 void launch_item_pass(int K, int prec, bool loss_only, const PassArgs &a, hipStream_t s,
                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // The P pass (a0) and the Q pass (a1) of one simultaneous step in one launch
@@ -167,9 +187,10 @@ void launch_item_pass_pair(int K, int prec, const PassArgs &a0, const PassArgs &
 void launch_fixup(int K, int prec, const PassArgs &a, hipStream_t s, hipEvent_t ev0 = nullptr,
                   hipEvent_t ev1 = nullptr);
 // Row blocks of a bucketed stream: bounds[j * rows + x] = first cell of bucket
-// x whose other index is >= j * block_rows, for j = 0 .. n_blocks (int64).
-void launch_block_bounds(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_blocks, int64_t block_rows,
-                         int64_t *bounds, hipStream_t s);
+// x whose other index is >= row_bounds[j], for j = 0 .. n_blocks (int64;
+// row_bounds holds n_blocks + 1 nondecreasing device values).
+void launch_block_bounds(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_blocks,
+                         const int64_t *row_bounds, int64_t *bounds, hipStream_t s);
 // After the n_blocks partial passes: row x's sums part[j * rows * K + x * K ..]
 // added in block order, then the row update of `a` (its own bucket pointers
 // give the degrees).

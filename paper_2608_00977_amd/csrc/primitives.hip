@@ -227,6 +227,23 @@ __global__ void k_keys_to_stream(const uint64_t *keys, const uint32_t *vals, int
     }
 }
 
+// Global cell keys u * n + i of a piece of Omega, from offset on.
+__global__ void k_cell_keys(const int32_t *u, const int32_t *i, int64_t len, int64_t n, uint64_t *keys,
+                            uint32_t *vals) {
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < len;
+         j += (int64_t)gridDim.x * blockDim.x) {
+        keys[j] = (uint64_t)(uint32_t)u[j] * (uint64_t)n + (uint64_t)(uint32_t)i[j];
+        vals[j] = 0u;
+    }
+}
+
+// Equal neighbours in sorted keys: a repeated cell.
+__global__ void k_adjacent_equal(const uint64_t *keys, int64_t n, int32_t *err) {
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x + 1; j < n;
+         j += (int64_t)gridDim.x * blockDim.x)
+        if (keys[j - 1] == keys[j]) err[ERR_DUP] = 1;
+}
+
 __global__ void k_ptr_from_keys(const uint64_t *keys, int64_t n, int32_t rows, int low_bits,
                                 int64_t *ptr) {
     const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -393,6 +410,19 @@ void keys_to_stream(const uint64_t *keys, const uint32_t *vals, int64_t n, int l
                     int2 *stream, int32_t *err, hipStream_t s) {
     if (n <= 0) return;
     k_keys_to_stream<<<grid_for(n, 256), 256, 0, s>>>(keys, vals, n, low_bits, stream, err);
+    TSID_HIP(hipGetLastError());
+}
+
+void cell_keys(const int32_t *u, const int32_t *i, int64_t len, int64_t n, uint64_t *keys, uint32_t *vals,
+               hipStream_t s) {
+    if (len <= 0) return;
+    k_cell_keys<<<grid_for(len, 256), 256, 0, s>>>(u, i, len, n, keys, vals);
+    TSID_HIP(hipGetLastError());
+}
+
+void adjacent_equal(const uint64_t *keys, int64_t n, int32_t *err, hipStream_t s) {
+    if (n <= 1) return;
+    k_adjacent_equal<<<grid_for(n, 256), 256, 0, s>>>(keys, n, err);
     TSID_HIP(hipGetLastError());
 }
 

@@ -176,9 +176,165 @@ void ridge_k(const RidgeArgs &a, hipStream_t s) {
     TSID_HIP(hipGetLastError());
 }
 
+// k = 128: a row of the Gram matrix does not fit one lane's registers, so
+// the matrix lives in LDS (128 x 129 doubles, 129 KiB) and a workgroup of
+// four waves solves one free row:
+//  1. Gram: the 36 block pairs I <= J of the 8 x 8 blocks are dealt to the
+//     waves (pair q to wave q % 4); each wave walks all the row's cells, four
+//     at a time, with the operand layout of k_ridge_rows, and wave 0 also
+//     sums the right-hand side.
+//  2. The blocks and their mirror images go to LDS; lambda joins the
+//     diagonal.
+//  3. Cholesky, right-looking: at column j every thread reads the pivot
+//     d = G[j][j], and the trailing lower triangle takes
+//     G[r][c] -= G[r][j] G[c][j] / d (two threads per row r > j, alternate
+//     columns); column j - 1 is scaled by 1 / sqrt of its pivot in the same
+//     phase (no thread reads it any more), so one barrier per column.
+//  4. Wave 0 solves L z = b and L^T x = z, lane l holding rows l and l + 64,
+//     the pivots of each step broadcast with readlane.
+constexpr int kR128 = 128, kR128Pitch = kR128 + 1, kR128Threads = 256;
+constexpr int kR128Lds = (kR128 * kR128Pitch + kR128) * 8;
+
+__global__ __launch_bounds__(kR128Threads) void k_ridge_rows_128(const RidgeArgs A) {
+    constexpr int K = kR128, NB = K / 16, PITCH = kR128Pitch;
+    extern __shared__ double lds[];
+    double *G = lds;                  // K x PITCH
+    double *rhs = lds + K * PITCH;    // K
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int64_t f = blockIdx.x;
+    if (f >= A.rows) return;
+    const int lr = lane & 15, lq = lane >> 4;
+    const int64_t b0 = A.ptr[f], b1 = A.ptr[f + 1];
+    if (b0 == b1) {
+        if (tid < K) A.X[f * K + tid] = 0.f;
+        return;
+    }
+    // 1. this wave's block pairs (slot q / 4 of pair q = 4 s + wv)
+    d4 acc[9];
+#pragma unroll
+    for (int q = 0; q < 9; ++q) acc[q] = d4{0.0, 0.0, 0.0, 0.0};
+    double rb[NB];
+#pragma unroll
+    for (int I = 0; I < NB; ++I) rb[I] = 0.0;
+    for (int64_t c0 = b0; c0 < b1; c0 += 4) {
+        const int64_t c = c0 + lq;
+        double pv[NB];
+        double rv = 0.0;
+#pragma unroll
+        for (int I = 0; I < NB; ++I) pv[I] = 0.0;
+        if (c < b1) {
+            const int2 rec = A.stream[c];
+            rv = (double)__int_as_float(rec.y);
+            const float *p = A.F + (int64_t)rec.x * K;
+#pragma unroll
+            for (int I = 0; I < NB; ++I) pv[I] = (double)p[16 * I + lr];
+        }
+        if (wv == 0) {
+#pragma unroll
+            for (int I = 0; I < NB; ++I) rb[I] = fma(rv, pv[I], rb[I]);
+        }
+        int q = 0;
+#pragma unroll
+        for (int I = 0; I < NB; ++I) {
+#pragma unroll
+            for (int J = I; J < NB; ++J, ++q)
+                if ((q & 3) == wv) acc[q >> 2] = __builtin_amdgcn_mfma_f64_16x16x4f64(pv[I], pv[J], acc[q >> 2], 0, 0, 0);
+        }
+    }
+    // 2. blocks (and mirrors) to LDS; the right-hand side summed over the four cell slots
+    {
+        int q = 0;
+#pragma unroll
+        for (int I = 0; I < NB; ++I) {
+#pragma unroll
+            for (int J = I; J < NB; ++J, ++q) {
+                if ((q & 3) != wv) continue;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int row = 16 * I + 4 * j + lq, col = 16 * J + lr;
+                    G[row * PITCH + col] = acc[q >> 2][j];
+                    G[col * PITCH + row] = acc[q >> 2][j];
+                }
+            }
+        }
+    }
+    if (wv == 0) {
+#pragma unroll
+        for (int I = 0; I < NB; ++I) {
+            double v = rb[I];
+            v += __shfl_xor(v, 16, 64);
+            v += __shfl_xor(v, 32, 64);
+            if (lq == 0) rhs[16 * I + lr] = v;
+        }
+    }
+    __syncthreads();
+    if (tid < K) G[tid * PITCH + tid] += (double)A.lambda;
+    __syncthreads();
+    // 3. Cholesky
+    bool bad = false;
+    const int half = tid & 1;
+    double dprev = 1.0;  // the previous column's pivot (read before it was overwritten)
+    for (int j = 0; j < K; ++j) {
+        const double d = G[j * PITCH + j];
+        bad |= !(d > 0.0);
+        if (j > 0 && tid < K - j + 1) {  // scale column j - 1 (rows j - 1 .. K - 1)
+            const int r = j - 1 + tid;
+            const double lp = sqrt(dprev > 0.0 ? dprev : 1.0);
+            G[r * PITCH + (j - 1)] = r == j - 1 ? lp : G[r * PITCH + (j - 1)] / lp;
+        }
+        dprev = d;
+        const double inv = 1.0 / (d > 0.0 ? d : 1.0);
+        const int r = j + 1 + (tid >> 1);
+        if (r < K) {
+            const double a = G[r * PITCH + j] * inv;
+            for (int c = j + 1 + half; c <= r; c += 2) G[r * PITCH + c] = fma(-a, G[c * PITCH + j], G[r * PITCH + c]);
+        }
+        __syncthreads();
+    }
+    if (tid == 0)  // the last column's pivot
+        G[(K - 1) * PITCH + (K - 1)] = sqrt(dprev > 0.0 ? dprev : 1.0);
+    __syncthreads();
+    // 4. triangular solves by wave 0: lane l holds rows l and l + 64
+    bad = __syncthreads_or(bad);
+    if (wv == 0) {
+        double bl = rhs[lane], bh = rhs[lane + 64];
+        for (int c = 0; c < K; ++c) {  // L z = b, column by column
+            const double lcc = G[c * PITCH + c];
+            const double zc = (c < 64 ? readlane_f64(bl, c) : readlane_f64(bh, c - 64)) / lcc;
+            if (lane == c) bl = zc;
+            else if (lane > c) bl = fma(-G[lane * PITCH + c], zc, bl);
+            if (lane + 64 == c) bh = zc;
+            else if (lane + 64 > c) bh = fma(-G[(lane + 64) * PITCH + c], zc, bh);
+        }
+        for (int r = K - 1; r >= 0; --r) {  // L^T x = z, row by row
+            const double lrr = G[r * PITCH + r];
+            const double xr = (r < 64 ? readlane_f64(bl, r) : readlane_f64(bh, r - 64)) / lrr;
+            if (lane == r) bl = xr;
+            else if (lane < r) bl = fma(-G[r * PITCH + lane], xr, bl);
+            if (lane + 64 == r) bh = xr;
+            else if (lane + 64 < r) bh = fma(-G[r * PITCH + lane + 64], xr, bh);
+        }
+        const float xl = (float)bl, xh = (float)bh;
+        A.X[f * K + lane] = xl;
+        A.X[f * K + lane + 64] = xh;
+        if (bad || !__builtin_isfinite(xl) || !__builtin_isfinite(xh)) A.err[ERR_NONFINITE] = 1;
+    }
+}
+
+void ridge_128(const RidgeArgs &a, hipStream_t s) {
+    static const bool lds_ok = [] {
+        TSID_HIP(hipFuncSetAttribute(reinterpret_cast<const void *>(k_ridge_rows_128),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, kR128Lds));
+        return true;
+    }();
+    (void)lds_ok;
+    hipLaunchKernelGGL(k_ridge_rows_128, dim3((unsigned)a.rows), dim3(kR128Threads), kR128Lds, s, a);
+    TSID_HIP(hipGetLastError());
+}
+
 }  // namespace
 
-bool ridge_supported(int K) { return K == 8 || K == 16 || K == 32 || K == 64; }
+bool ridge_supported(int K) { return K == 8 || K == 16 || K == 32 || K == 64 || K == 128; }
 
 void launch_ridge_rows(int K, const RidgeArgs &a, hipStream_t s) {
     if (a.rows <= 0) return;
@@ -187,7 +343,8 @@ void launch_ridge_rows(int K, const RidgeArgs &a, hipStream_t s) {
         case 16: ridge_k<16>(a, s); break;
         case 32: ridge_k<32>(a, s); break;
         case 64: ridge_k<64>(a, s); break;
-        default: fail(TSID_E_INVAL, "the exact extension solve supports k in {8, 16, 32, 64}");
+        case 128: ridge_128(a, s); break;
+        default: fail(TSID_E_INVAL, "the exact extension solve supports k in {8, 16, 32, 64, 128}");
     }
 }
 

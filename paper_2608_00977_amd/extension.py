@@ -118,3 +118,104 @@ class Extension:
         if self.cols.free_ids.size:
             Q[torch.from_numpy(self.cols.free_ids)] = Q_free
         return P, Q, {"row_phase_s": t1 - t0, "assemble_s": t2 - t1, "col_phase_s": t3 - t2}
+
+
+def _pinned(n, dtype):
+    return torch.empty(max(1, int(n)), dtype=dtype).pin_memory()
+
+
+class StreamedExtension:
+    """Both phases of the extension from sources that produce their cells a
+    range of free lines at a time, for matrices whose Omega is not held in
+    memory (Section 5.2: the matrix is processed in chunks streamed from the
+    host).  A source is any object with ``side`` (0 rows, 1 columns),
+    ``free_ids`` (global id of each free line), ``counts`` (cells per free
+    line) and ``fill(lo, hi, fixed, free_local, r)`` writing the cells of free
+    lines [lo, hi) -- fixed ids as the phase's F_fixed expects them -- and
+    returning their number.
+
+    Chunks are runs of whole free lines of at most ``max_entries`` cells
+    (``tsid_chunk_plan``).  By default each chunk is filled into one of two
+    pinned host buffers just before it is queued; ``tsid_extend_chunk``
+    returns once the previous chunk's copy has finished, so the other buffer
+    is then free for the next chunk while this one copies and the previous
+    one computes.  With ``prefill`` every chunk is filled into pinned memory
+    up front (``prefill_s``), and ``run`` times the stream alone."""
+
+    def __init__(self, m, n, I, J, rows, cols, max_entries, prefill=False):
+        self.m, self.n = int(m), int(n)
+        self.I = np.asarray(I, np.int64)
+        self.J = np.asarray(J, np.int64)
+        self.rows, self.cols = rows, cols
+        self.bounds = [tsid_chunk_plan(np.asarray(ph.counts, np.int64), 0, int(max_entries)) for ph in (rows, cols)]
+        self.prefill_s = 0.0
+        self.chunks = None
+        self.fill_s = [0.0, 0.0]
+        if prefill:
+            t0 = time.perf_counter()
+            self.chunks = [self._fill_all(ph, b) for ph, b in zip((rows, cols), self.bounds)]
+            self.prefill_s = time.perf_counter() - t0
+        else:
+            cap = max(self._largest(ph, b) for ph, b in zip((rows, cols), self.bounds))
+            self.buf = [(_pinned(cap, torch.int32), _pinned(cap, torch.int32), _pinned(cap, torch.float32))
+                        for _ in range(2)]
+
+    @staticmethod
+    def _largest(ph, bounds):
+        c = np.concatenate([[0], np.cumsum(np.asarray(ph.counts, np.int64))])
+        return int(max((c[bounds[j + 1]] - c[bounds[j]] for j in range(bounds.size - 1)), default=0))
+
+    @staticmethod
+    def _fill_all(ph, bounds):
+        fx, fl, rr = _pinned(ph.nnz, torch.int32), _pinned(ph.nnz, torch.int32), _pinned(ph.nnz, torch.float32)
+        out, e0 = [], 0
+        for j in range(bounds.size - 1):
+            lo, hi = int(bounds[j]), int(bounds[j + 1])
+            n = ph.fill(lo, hi, fx[e0:].numpy(), fl[e0:].numpy(), rr[e0:].numpy())
+            out.append((fx[e0:e0 + n], fl[e0:e0 + n], rr[e0:e0 + n], lo, hi))
+            e0 += n
+        return out
+
+    def _run_phase(self, T: Tsid, which, F_fixed, out, opts):
+        ph, bounds = (self.rows, self.cols)[which], self.bounds[which]
+        for j in range(bounds.size - 1):
+            lo, hi = int(bounds[j]), int(bounds[j + 1])
+            if self.chunks is not None:
+                fx, fl, rr, _, _ = self.chunks[which][j]
+            else:
+                b = self.buf[j % 2]
+                t0 = time.perf_counter()
+                n = ph.fill(lo, hi, b[0].numpy(), b[1].numpy(), b[2].numpy())
+                self.fill_s[which] += time.perf_counter() - t0
+                fx, fl, rr = b[0][:n], b[1][:n], b[2][:n]
+            if isinstance(opts, tsid_adam_opts):
+                raise ValueError("the streamed extension runs the factored solvers")
+            T.extend_chunk(ph.side, fx, fl, rr, hi - lo, F_fixed, out[lo:hi], opts)
+        T.sync()
+
+    def run(self, T: Tsid, P_t: torch.Tensor, Q_t: torch.Tensor, opts, col_opts=None):
+        """P_t (m_t x k), Q_t (n_t x k): fp32 device factors of the template.
+        opts (and col_opts for the column phase): tsid_fit_opts for one-sided
+        gradient steps, or a float lambda for the exact ridge solve.  Returns
+        P_full (m x k, device: the template rows and the row phase's), P_free
+        and Q_free (the two phases' free lines, pinned host, in the sources'
+        order) and the wall time of each phase in seconds (with the time spent
+        filling host buffers, when not prefilled)."""
+        k = P_t.shape[1]
+        P_free = _pinned(self.rows.free_ids.size * k, torch.float32)[:self.rows.free_ids.size * k].view(-1, k)
+        Q_free = _pinned(self.cols.free_ids.size * k, torch.float32)[:self.cols.free_ids.size * k].view(-1, k)
+        self.fill_s = [0.0, 0.0]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        self._run_phase(T, 0, Q_t, P_free, opts)
+        t1 = time.perf_counter()
+        P_full = torch.empty((self.m, k), dtype=torch.float32, device=P_t.device)
+        P_full[torch.from_numpy(self.I).to(P_t.device)] = P_t
+        if self.rows.free_ids.size:
+            P_full[torch.from_numpy(np.asarray(self.rows.free_ids, np.int64)).to(P_t.device)] = P_free.to(P_t.device)
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        self._run_phase(T, 1, P_full, Q_free, opts if col_opts is None else col_opts)
+        t3 = time.perf_counter()
+        return P_full, P_free, Q_free, {"row_phase_s": t1 - t0, "assemble_s": t2 - t1, "col_phase_s": t3 - t2,
+                                        "row_fill_s": self.fill_s[0], "col_fill_s": self.fill_s[1]}

@@ -47,3 +47,14 @@ def test_chunk_plan_host_logic_matches_oracle():
         for cap in (1, 25, 100):
             assert np.array_equal(tsid_chunk_plan(counts, max_entries=cap),
                                   oracle.chunk_plan(counts, max_entries=cap))
+
+
+def test_create_with_a_device_id_no_runtime_has_is_e_device():
+    """tsid_create validates the device id before any device work: an id no
+    runtime has (here, and on any box) returns TSID_E_DEVICE and no context."""
+    from paper_2608_00977_amd import lib
+    L = lib()
+    ctx = ctypes.c_void_p()
+    st = L.tsid_create(100000, None, 0, ctypes.byref(ctx))
+    assert st == 5 and not ctx.value
+    assert L.tsid_create(0, None, 0, None) == 1  # out == NULL: TSID_E_INVAL

@@ -80,7 +80,7 @@ def _loss(F, B, fixed, free, r, C, lam):
     return float(e @ e + lam * np.sum(np.asarray(C, np.float64) ** 2))
 
 
-@pytest.mark.parametrize("k", [8, 16, 32, 64])
+@pytest.mark.parametrize("k", [8, 16, 32, 64, 128])
 def test_adam_matches_oracle(k):
     from paper_2608_00977_amd import make_adam_opts
     n_free, n_b = 120, 300  # two basis slices, the second ragged
@@ -148,14 +148,6 @@ def test_adam_rejects_bad_arguments():
     import paper_2608_00977_amd as tsid
     from paper_2608_00977_amd import make_adam_opts
     F, B, fixed, free, r = _chunk(9, 50, 10, 8, 100, 64)
-    T = _ctx(128)
-    try:
-        with pytest.raises(tsid.TsidError) as ei:
-            _run(T, np.zeros((50, 128), np.float32), np.zeros((8, 128), np.float32), fixed, free, r, 10,
-                 make_adam_opts(3, 0.1, 0.01))
-        assert ei.value.status == tsid.binding.E_INVAL
-    finally:
-        T.close()
     T = _ctx(64)
     try:
         for bad in (make_adam_opts(-1, 0.1, 0.01), make_adam_opts(3, -0.1, 0.01),

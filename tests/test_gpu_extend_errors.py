@@ -143,6 +143,14 @@ def test_build_errors_leave_template_unchanged():
         dup_r = np.append(p.r, np.float32(1.0))
         cases["repeated cell inside the template"] = (
             lambda: T.build_template(p.m, p.n, dup_u, dup_i, dup_r, p.I, p.J, 8), E_DUP)
+        outside = [e for e in range(p.nnz) if not (int(p.u[e]) in rm and int(p.i[e]) in cm)]
+        dup2_u = np.append(p.u, p.u[outside[0]])
+        dup2_i = np.append(p.i, p.i[outside[0]])
+        dup2_r = np.append(p.r, np.float32(2.0))
+        cases["repeated cell outside the template"] = (
+            lambda: T.build_template(p.m, p.n, dup2_u, dup2_i, dup2_r, p.I, p.J, 8), E_DUP)
+        cases["repeated cell outside the template, small staging pieces"] = (
+            lambda: T.build_template(p.m, p.n, dup2_u, dup2_i, dup2_r, p.I, p.J, 8, stage_entries=37), E_DUP)
         nan_r = p.r.copy()
         nan_r[inside[1]] = np.nan
         cases["NaN value inside the template"] = (
@@ -193,6 +201,15 @@ def test_extension_device_errors_reported_by_sync(T):
     assert _status(T.sync) == E_DUP
     T.extend_chunk(1, fixed, free, r, 30, Fd, out, opts)
     T.sync()  # clean again
+
+
+def test_bad_device_id():
+    """tsid_create with a device id the runtime does not have: E_DEVICE."""
+    import torch
+    from paper_2608_00977_amd.binding import E_DEVICE, TsidError, tsid_create
+    with pytest.raises(TsidError) as ei:
+        tsid_create(torch.cuda.device_count(), 0, 0)
+    assert ei.value.status == E_DEVICE
 
 
 def test_device_byte_cap():

@@ -63,7 +63,7 @@ def _row_err(X, Xo):
     return np.where(np.linalg.norm(Xo, axis=1) > 0, num / den, num)
 
 
-@pytest.mark.parametrize("k", [8, 16, 32, 64])
+@pytest.mark.parametrize("k", [8, 16, 32, 64, 128])
 @pytest.mark.parametrize("lam", [0.5, 1e-3])
 def test_ridge_rows_match_oracle(k, lam):
     F, fixed, free, r = _chunk(10 + k, 3000, 600, 50000, k, hot=2, short=40)
@@ -161,14 +161,6 @@ def test_ridge_chunking_is_invariant_and_matches_converged_steps():
 def test_ridge_rejects_bad_arguments():
     import torch
     import paper_2608_00977_amd as tsid
-    T = _ctx(128)
-    try:
-        F = np.zeros((10, 128), np.float32)
-        with pytest.raises(tsid.TsidError) as ei:
-            _run(T, F, np.zeros(1, np.int32), np.zeros(1, np.int32), np.ones(1, np.float32), 1, 0.1)
-        assert ei.value.status == tsid.binding.E_INVAL
-    finally:
-        T.close()
     T = _ctx(16)
     try:
         F = np.zeros((10, 16), np.float32)
