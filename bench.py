@@ -12,33 +12,32 @@ The metric is observed template cells per second per epoch
 region starts; the template build (host stream, filter, bucketing) is timed
 separately and reported as build_s.
 
-Default workload: the Scientific configuration's template -- 200,000 x
-200,000 rank-32 ground truth, 10 % uniform observation, a 16,384 x 16,384
-uniform template (about 24 M training cells), k = 32, fp32, degree step.
---config rating runs the Netflix-shaped template (65,536 x 8,192, k = 64,
-bf16 factors with fp32 accumulation and clipping); --config billion the
-Billion-scale template (1,000,000 x 100,000 of a 10 M x 1 M Zipf matrix,
-about 4.2e8 training cells, k = 128, bf16 + clipping; its input takes a few
-minutes to generate); mid / tiny are small.
+Default workload: the Billion-scale configuration's template, the largest
+workload that fits one GPU -- the 1,000,000 x 100,000 most-popular template of
+a 10 M x 1 M Zipf(1.0) matrix with 1e9 observed cells (about 4.2e8 training
+cells in the template), k = 128, bf16 factors with fp32 accumulation and the
+asymmetric clip, degree step.  --config scientific runs the 16,384 x 16,384
+uniform template of the 200,000 x 200,000 rank-32 matrix (k = 32, fp32);
+--config rating the Netflix-shaped template (65,536 x 8,192, k = 64, bf16);
+mid / tiny are small.
 
-Roofline: the dominant kernel is the longer of the P and Q passes (the slab
-pass on evenly spread fp32 templates such as Scientific, else the item pass;
-the library launches the two passes of an epoch as one kernel,
-k_slab_pass_pair or k_item_pass_pair, priced with both passes' bytes, except
-when the Q pass runs in row blocks),
-timed with HIP events attached to its dispatches on the library's compute
-stream during the timed region (every --time-every-th epoch: a timed dispatch
-costs a few microseconds of wall time, which would otherwise slow the
-throughput being measured); its algorithmic bytes per launch are the compulsory bytes of one
-pass: the bucketed cell stream (8 B per cell), the bucket pointers (8 B per
-bucket), the owner rows read and written once and the gathered rows read once
-(4 B per coordinate in fp32; 2 B for bf16 copies).  A slab pass whose row
-blocks are split over several workgroups leaves the row updates (the
-owner-row writes) to a finishing kernel, timed with the fixups; its bytes
-exclude them.
+Roofline: every kernel kind of an epoch (the P and Q passes or their one
+paired launch, the dense-tile launches) is priced with the algorithmic work
+of the cells it covers: per observed cell and epoch, 12 bytes (each
+(u, i, r) read once) and 6k flops (one dot product, two axpys), a launch of
+one pass taking half of both, plus each owner row it updates read and
+written once (fp32 master; in bf16 mode its bf16 copy written too).  The
+fractions of the MI355X peaks (HBM 8 TB/s, fp32 vector 157.3 TFLOP/s, bf16
+matrix cores 2.5 PFLOP/s for the dense-tile kernels) are reported for each;
+the roofline object is the kernel with the most time per epoch, bound by the
+unit with the highest fraction.  Durations come from HIP events attached to
+the dispatches on the library's compute stream during the timed region
+(every --time-every-th epoch: a timed dispatch costs a few microseconds of
+wall time, which would otherwise slow the throughput being measured).
 
-CPU baseline: the fp64 oracle (serial C) on a bounded sample of the same
-template cells, for as many epochs as fit in about --cpu-seconds.
+CPU baseline: the fp64 oracle built with OpenMP on all host cores (the
+line-parallel fit, the same bits as the serial oracle) on a bounded sample of
+the same template cells, for as many epochs as fit in about --cpu-seconds.
 """
 import argparse
 import hashlib
@@ -50,15 +49,14 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-HBM_PEAK_GBPS = 8000.0
 
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1000)
-    ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--config", default="scientific", choices=["scientific", "rating", "billion", "mid", "tiny"])
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="billion", choices=["scientific", "rating", "billion", "mid", "tiny"])
     ap.add_argument("--pass-kernel", default="auto", choices=["auto", "item", "slab"],
                     help="kernel of the P and Q passes (tsid_set_pass_kernel); auto picks the "
                          "slab pass for evenly spread fp32 templates")
@@ -81,14 +79,18 @@ def parse():
     ap.add_argument("--time-every", type=int, default=10,
                     help="attach HIP timing events to the kernels of every n-th timed epoch (each "
                          "timed dispatch costs a few microseconds of wall time)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--extend", action="store_true",
                     help="after the timed fit, time the end-to-end extension (row phase, then "
-                         "column phase, 16 chunks each, streamed from pinned host memory) and print "
-                         "a second JSON line; needs a workload with the whole matrix drawn "
-                         "(rating, mid, tiny)")
+                         "column phase, streamed in chunks from pinned host memory) and print a "
+                         "second JSON line with the PCIe fraction and the copy/compute overlap; on "
+                         "Scientific and Billion-scale the cells outside the template come from the "
+                         "streaming generator, filled into pinned memory before the timed run")
     ap.add_argument("--extend-steps", type=int, default=20)
+    ap.add_argument("--extend-chunk", type=int, default=0,
+                    help="cells per chunk of the streamed extension (0: 2^28 on Scientific, 2^26 on "
+                         "Billion-scale)")
     ap.add_argument("--extend-solver", default="steps", choices=["steps", "ridge", "adam"],
                     help="extension solver: one-sided gradient steps (tsid_extend_chunk), the "
                          "exact ridge solve per free row (tsid_extend_chunk_ridge, fp64 Gram on the "
@@ -125,31 +127,35 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def pass_bytes(nnz, owners, others, k, prec, no_owner_write=False):
-    """Compulsory bytes of one pass launch (see the module docstring)."""
-    fb = 4 * k
-    b = 8 * nnz + 8 * (owners + 1) + 2 * fb * owners + (2 * k if prec == "bf16" else fb) * others
-    if prec == "bf16":
-        b += 2 * k * owners  # bf16 copy of the updated rows
-    if no_owner_write:
-        b -= fb * owners
-    return b
+# Peaks of one MI355X (published figures): HBM3E bandwidth, the fp32 vector
+# rate (the item and slab passes' arithmetic, fp32 or bf16 dot2 with fp32
+# accumulation) and the dense bf16 matrix-core rate (the dense-tile kernels).
+PEAK = {"hbm": (8000.0, "GB/s"), "alu": (157.3, "TFLOP/s"), "mfma": (2500.0, "TFLOP/s")}
 
 
-def dense_bytes(tiles, stripes_own, stripes_other, k):
-    """Compulsory bytes of one dense-tile launch: the tile values (fp32, 1 KiB
-    per tile), the tile list (4 B per tile and stripe), the owner rows of the
-    stripes holding a tile read once as bf16 copies and their fp32 gradient
-    sums written once, the other rows those tiles touch read once (bf16)."""
-    return (1024 + 4) * tiles + 4 * stripes_own + 16 * stripes_own * (2 * k + 4 * k) \
-        + 16 * stripes_other * 2 * k
+def algorithmic(cells, owners, k, prec, sides=1, factor_rows=True):
+    """Algorithmic bytes and flops of one launch covering `sides` passes
+    (1: the P or the Q pass, 2: both) over `cells` observed cells: per cell
+    and epoch each (u, i, r) is read once (12 B) and the work is one dot
+    product and two axpys (6k flops), so a launch of one pass owns half of
+    that; each owner row it updates is read once and written once (fp32
+    master; in bf16 mode also its bf16 copy written).  `owners` is the owner
+    row count of those passes together."""
+    by = 6 * sides * cells
+    if factor_rows:
+        by += owners * (4 * k + 4 * k + (2 * k if prec == "bf16" else 0))
+    return by, 3 * k * sides * cells
 
 
-def dense_flops(tiles, k):
-    """Matrix-core flops of one dense-tile launch: per tile the 16 x 16 x k
-    product of the residuals and the two 16 x 16 x k products of the
-    gradient (high and low bf16 parts of the residual)."""
-    return 3 * 2 * 256 * k * tiles
+def roofline_of(ms, by, fl, units):
+    """Fractions of the peaks for a launch of `ms` milliseconds moving `by`
+    algorithmic bytes and doing `fl` algorithmic flops; the bound is the unit
+    with the highest fraction among `units`."""
+    s = ms / 1e3
+    got = {"hbm": by / s / 1e9, "alu": fl / s / 1e12, "mfma": fl / s / 1e12}
+    fr = {u: got[u] / PEAK[u][0] for u in units}
+    bound = max(fr, key=fr.get)
+    return bound, got[bound], fr
 
 
 def traffic_from_profiles(kernel_src_sha, which):
@@ -167,19 +173,29 @@ def traffic_from_profiles(kernel_src_sha, which):
 
 
 def cpu_baseline(p, seconds, batches=0, seed=0):
+    """The oracle timed on the host's cores: the line-parallel fp64 fit
+    (or_fit_lines, OpenMP over all cores; the same bits as the serial fit) on
+    a bounded sample of the template cells, with every template factor row,
+    for as many epochs as fit in about `seconds`.  Mini-batch epochs have no
+    parallel oracle and run the serial one."""
     import numpy as np
 
     import oracle
     st, rm, cm = oracle.template_maps(p.m, p.n, p.I, p.J)
     a, b, v = oracle.filter_template(p.u, p.i, p.r, rm, cm)
-    S = int(min(a.size, 2_000_000))
+    S = int(min(a.size, 20_000_000 if not batches else 2_000_000))
     a, b, v = a[:S], b[:S], v[:S]
+    cores = 1
     if batches:
         run = lambda ep: oracle.fit_minibatch(a, b, v, p.P0, p.Q0, ep, p.lam, p.lr, p.step, p.clip, p.xi,
                                               bf16=p.prec == "bf16", n_batches=batches, seed=seed)
+        how = f"mini-batch epochs ({batches} batches), serial fp64 C"
     else:
-        run = lambda ep: oracle.fit(a, b, v, p.P0, p.Q0, ep, p.lam, p.lr, p.step, p.clip, p.xi,
-                                    bf16=p.prec == "bf16")
+        cores = oracle.threads(True)
+        run = lambda ep: oracle.fit_lines(a, b, v, p.P0, p.Q0, ep, p.lam, p.lr, p.step, p.clip, p.xi,
+                                          bf16=p.prec == "bf16", omp=True)
+        how = (f"full-gradient epochs, fp64 C built with OpenMP ({cores} threads: rows, then columns, "
+               f"split across threads; the same bits as the serial oracle)")
     t0 = time.perf_counter()
     run(1)
     one = time.perf_counter() - t0
@@ -187,12 +203,22 @@ def cpu_baseline(p, seconds, batches=0, seed=0):
     t0 = time.perf_counter()
     run(epochs)
     el = time.perf_counter() - t0
-    return {"value": S * epochs / el, "unit": "entries/s", "cores": 1, "kind": "oracle",
+    # epochs + 1 loss evaluations: the final one costs about a third of an epoch
+    return {"value": S * epochs / el, "unit": "entries/s", "cores": cores, "kind": "oracle",
             "sample": f"first {S} template cells (input order, i.e. a uniform random sample) of "
                       f"the same workload, all {p.I.size} x {p.J.size} template factor rows, "
-                      f"{epochs} " + (f"mini-batch epochs ({batches} batches)" if batches else
-                                      "full-gradient epochs") + ", serial fp64 C",
-            "seconds": el, "nproc": os.cpu_count()}
+                      f"{epochs} {how}",
+            "seconds": el, "nproc": os.cpu_count(), "cpu": _cpu_model()}
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def h2d_probe(nbytes, reps=5):
@@ -211,18 +237,18 @@ def h2d_probe(nbytes, reps=5):
 
 def extension_line(args, p, T, P, Q):
     """End-to-end extension from the fitted template factors (Section 5.2)."""
+    import torch
+
     import paper_2608_00977_amd as tsid
-    from paper_2608_00977_amd.extension import Extension
-    if p.extra.get("omega_scope") == "template block only":
-        raise SystemExit("--extend needs a workload whose whole matrix is drawn (rating, mid, tiny)")
-    t0 = time.perf_counter()
-    ext = Extension(p.m, p.n, p.u, p.i, p.r, p.I, p.J, n_chunks=16)
-    prep_s = time.perf_counter() - t0
+    from paper_2608_00977_amd.extension import Extension, StreamedExtension
+    streamed = p.extra.get("omega_scope") == "template block only"
     col_opts = None
     if args.extend_solver == "ridge":
         opts = float(p.lam)  # exact solve per free row
         how = f"exact ridge solve per free row (lambda {p.lam}, fp64 Gram + Cholesky)"
     elif args.extend_solver == "adam":
+        if streamed:
+            raise SystemExit("--extend-solver adam runs on the workloads whose whole matrix is drawn")
         opts = float(p.lam)
         col_opts = tsid.make_adam_opts(args.extend_steps, p.lam, 0.01)
         how = (f"rows by the exact ridge solve; columns by {args.extend_steps} Adam steps on their "
@@ -233,13 +259,39 @@ def extension_line(args, p, T, P, Q):
         opts = tsid.make_opts(epochs=args.extend_steps, lam=p.lam, lr=0.05, clip=p.clip, xi=p.xi,
                               step="degree")
         how = f"{args.extend_steps} one-sided steps per chunk, degree step"
-    ext.run(T, P, Q, opts, col_opts)  # warm-up (allocations, code load)
-    _, _, ph = ext.run(T, P, Q, opts, col_opts)
-    n_row, n_col = ext.rows.nnz, ext.cols.nnz
+    t0 = time.perf_counter()
+    if streamed:
+        import tsid_synth
+        omega = tsid_synth.omega_outside_template(p)
+        rows, cols = omega.row_phase(), omega.col_phase()
+        max_entries = args.extend_chunk or (1 << 28 if p.name == "scientific" else 1 << 26)
+        log(f"extension: {rows.nnz} + {cols.nnz} cells outside the template; filling pinned chunks")
+        ext = StreamedExtension(p.m, p.n, p.I, p.J, rows, cols, max_entries, prefill=True)
+        n_row, n_col = rows.nnz, cols.nnz
+        chunks = [ext.bounds[0].size - 1, ext.bounds[1].size - 1]
+        largest = max(ext._largest(ph, b) for ph, b in zip((rows, cols), ext.bounds))
+        run = lambda: ext.run(T, P, Q, opts, col_opts)[3]  # noqa: E731
+        source = (f"streamed from pinned host memory, chunks of at most {max_entries} cells "
+                  f"(generated outside the timed region in {ext.prefill_s:.0f}s)")
+    else:
+        ext = Extension(p.m, p.n, p.u, p.i, p.r, p.I, p.J, n_chunks=16)
+        n_row, n_col = ext.rows.nnz, ext.cols.nnz
+        chunks = [ext.rows.bounds.size - 1, ext.cols.bounds.size - 1]
+        largest = max(c[0].numel() for c in ext.rows.chunks + ext.cols.chunks)
+        run = lambda: ext.run(T, P, Q, opts, col_opts)[2]  # noqa: E731
+        source = "16 chunks per phase from pinned host memory"
+    prep_s = time.perf_counter() - t0
+    run()  # warm-up (allocations, code load)
+    T.set_timing(1)
+    ph = run()
+    tm = T.timing()
+    T.set_timing(0)
     t_ext = ph["row_phase_s"] + ph["col_phase_s"]
     h2d_bytes = 12 * (n_row + n_col)
-    rate = h2d_probe(max(1 << 20, 12 * max(c[0].numel() for c in ext.rows.chunks + ext.cols.chunks)))
-    log(f"extension: {n_row} + {n_col} cells in {t_ext:.4f}s")
+    rate = h2d_probe(max(1 << 20, 12 * largest))
+    copies, compute = tm["ext_h2d_ms"] / 1e3, tm["ext_compute_ms"] / 1e3
+    overlap = (copies + compute - t_ext) / min(copies, compute) if min(copies, compute) > 0 else None
+    log(f"extension: {n_row} + {n_col} cells in {t_ext:.4f}s (copies {copies:.3f}s, compute {compute:.3f}s)")
     return {
         "metric": "extension entries/s (row phase + column phase)",
         "value": (n_row + n_col) / t_ext,
@@ -249,17 +301,19 @@ def extension_line(args, p, T, P, Q):
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": f"{p.name}: extension of the {p.I.size} x {p.J.size} template to "
-                               f"{p.m} x {p.n}, 16 chunks per phase, {how}, fixed factors fp32",
+                               f"{p.m} x {p.n}, {how}, fixed factors fp32, {source}",
                    "solver": args.extend_solver,
                    "row_phase_cells": n_row, "col_phase_cells": n_col,
-                   "row_chunks": ext.rows.bounds.size - 1, "col_chunks": ext.cols.bounds.size - 1},
+                   "row_chunks": chunks[0], "col_chunks": chunks[1]},
         "row_phase_s": ph["row_phase_s"],
         "col_phase_s": ph["col_phase_s"],
         "assemble_s": ph["assemble_s"],
         "host_prep_s": prep_s,
         "pcie": {"h2d_bytes": h2d_bytes, "pinned_h2d_GBps": round(rate / 1e9, 2),
                  "h2d_only_s": h2d_bytes / rate,
-                 "frac_of_h2d_bound": round(h2d_bytes / rate / t_ext, 4)},
+                 "frac_of_h2d_bound": round(h2d_bytes / rate / t_ext, 4),
+                 "copy_stream_s": round(copies, 4), "compute_stream_s": round(compute, 4),
+                 "overlap": None if overlap is None else round(max(0.0, min(1.0, overlap)), 4)},
     }
 
 
@@ -342,7 +396,7 @@ def main():
     m_t, n_t = info["m_t"], info["n_t"]
     # A slab pass split over several workgroups per block leaves the row
     # updates to its finishing kernel (timed as a fixup): its own launch then
-    # does not write the owner rows.
+    # reads the owner rows but does not write them.
     split = tm["fixup_launches"] > 0
     di = T.dense_info()
     sparse_nnz = nnz - di["cells"]
@@ -351,58 +405,67 @@ def main():
         # owner row read and written (lines without a cell keep theirs)
         bp = T.export_index("batch_ptr_r")
         sparse_nnz = int(bp[m_t] - bp[0])
-    by = [pass_bytes(sparse_nnz, m_t, n_t, k, p.prec, kernels[0] == "slab" and split),
-          pass_bytes(sparse_nnz, n_t, m_t, k, p.prec, kernels[1] == "slab" and split)]
-    if di["tiles"]:
-        # with dense tiles the item pass also reads the full bucket pointers
-        # (degrees) and the tile sums of the rows in stripes holding a tile
-        for j, own in ((0, m_t), (1, n_t)):
-            by[j] += 8 * (own + 1) + 4 * k * min(own, 16 * di["stripes"][j])
     avg = [tm["pass_ms"][j] / max(1, tm["pass_launches"][j]) for j in range(2)]
-    cand = [(avg[0], by[0], {"item": "k_item_pass", "slab": "k_slab_pass"}[kernels[0]], "P pass",
-             {"item": "fit.hip", "slab": "slab.hip"}[kernels[0]], "p_pass", kernels[0]),
-            (avg[1], by[1], {"item": "k_item_pass", "slab": "k_slab_pass"}[kernels[1]], "Q pass",
-             {"item": "fit.hip", "slab": "slab.hip"}[kernels[1]], "q_pass", kernels[1])]
-    # both passes in one launch (timed as the P pass; no Q pass launch)
+    src_of = {"item": "fit.hip", "slab": "slab.hip"}
+    cand = []
+
+    def add(ms, by_fl, name, desc, src, which, kind, units):
+        by_, fl_ = by_fl
+        if ms > 0:
+            cand.append(dict(ms=ms, by=by_, fl=fl_, name=name, desc=desc, src=src, which=which, kind=kind,
+                             units=units))
+
+    def pass_alg(side, sides=1):
+        owners = (m_t if side == 0 else n_t) if sides == 1 else m_t + n_t
+        by_, fl_ = algorithmic(sparse_nnz, owners, k, p.prec, sides)
+        if kernels[side] == "slab" and split:  # the finishing kernel writes the owner rows
+            by_ -= owners * 4 * k
+        return by_, fl_
+
     pair = kernels[0] == kernels[1] and tm["pass_launches"][1] == 0 and tm["pass_launches"][0] > 0
-    if pair:
-        cand = [(avg[0], by[0] + by[1], f"k_{kernels[0]}_pass_pair", "P and Q passes",
-                 {"item": "fit.hip", "slab": "slab.hip"}[kernels[0]], "pq_pass", kernels[0])]
+    if pair:  # both passes in one launch (timed as the P pass; no Q pass launch)
+        add(avg[0], pass_alg(0, 2), f"k_{kernels[0]}_pass_pair", "P and Q passes", src_of[kernels[0]], "pq_pass",
+            kernels[0], ("hbm", "alu"))
+    else:
+        add(avg[0], pass_alg(0), f"k_{kernels[0]}_pass", "P pass", src_of[kernels[0]], "p_pass", kernels[0],
+            ("hbm", "alu"))
+        qname = "k_item_pass_sched" if kernels[1] == "item" and row_blocks > 1 else f"k_{kernels[1]}_pass"
+        add(avg[1], pass_alg(1), qname, "Q pass" + (f" ({row_blocks} row blocks, one launch)" if row_blocks > 1
+                                                    else ""), src_of[kernels[1]], "q_pass", kernels[1],
+            ("hbm", "alu"))
     dense_avg = [tm["dense_ms"][j] / max(1, tm["dense_launches"][j]) for j in range(2)]
-    dcand = []
-    # both sides' dense tiles in one launch (timed as the P side's)
-    dense_pair = di["tiles"] and tm["dense_launches"][1] == 0 and tm["dense_launches"][0] > 0
-    if dense_pair:
-        dcand.append((dense_avg[0], sum(dense_bytes(di["tiles"], di["stripes"][j], di["stripes"][1 - j], k)
-                                        for j in range(2)),
-                      "k_dense_pass_pair", "P and Q side dense tiles", "dense.hip", "pq_dense", "dense"))
+    dense_pair = bool(di["tiles"]) and tm["dense_launches"][1] == 0 and tm["dense_launches"][0] > 0
+    if dense_pair:  # both sides' dense tiles in one launch (timed as the P side's)
+        add(dense_avg[0], algorithmic(di["cells"], 0, k, p.prec, 2, False), "k_dense_pass_pair",
+            "P and Q side dense tiles", "dense.hip", "pq_dense", "dense", ("hbm", "mfma"))
     elif di["tiles"]:
         for j in range(2):
-            dcand.append((dense_avg[j], dense_bytes(di["tiles"], di["stripes"][j], di["stripes"][1 - j], k),
-                          "k_dense_pass", ["P", "Q"][j] + " side dense tiles", "dense.hip",
-                          ["p_dense", "q_dense"][j], "dense"))
-    cand += dcand
-    dom_ms, dom_by, kname, kside, ksrc, which, kkind = max(cand, key=lambda c: c[0])
-    achieved = dom_by / (dom_ms / 1e3) / 1e9
-    src = open(os.path.join(ROOT, "paper_2608_00977_amd", "csrc", ksrc), "rb").read()
+            add(dense_avg[j], algorithmic(di["cells"], 0, k, p.prec, 1, False), "k_dense_pass",
+                ["P", "Q"][j] + " side dense tiles", "dense.hip", ["p_dense", "q_dense"][j], "dense",
+                ("hbm", "mfma"))
+    dom = max(cand, key=lambda c: c["ms"])
+    bound, achieved, fracs = roofline_of(dom["ms"], dom["by"], dom["fl"], dom["units"])
+    src = open(os.path.join(ROOT, "paper_2608_00977_amd", "csrc", dom["src"]), "rb").read()
     sha = hashlib.sha256(src).hexdigest()
     variant = (f":minibatch{args.minibatch}" if args.minibatch else "") + (":clip2" if args.clip_per_entry else "") \
         + (":similarity" if args.similarity > 0 else "") + (f":rowblocks{row_blocks}" if row_blocks > 1 else "")
-    traffic = traffic_from_profiles(sha, f"{args.config}:{which}:{kkind}" + variant)
-    epoch_bytes = by[0] + by[1] + sum(c[1] for c in dcand)
-    roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                "kernel": f"{kname} ({kside})",
-                "bytes_per_launch": dom_by, "avg_launch_ms": round(dom_ms, 5)}
+    traffic = traffic_from_profiles(sha, f"{args.config}:{dom['which']}:{dom['kind']}" + variant)
+    roofline = {"bound": bound, "achieved": round(achieved, 2), "peak": PEAK[bound][0], "unit": PEAK[bound][1],
+                "frac": round(fracs[bound], 4), "traffic": traffic,
+                "kernel": f"{dom['name']} ({dom['desc']})",
+                "bytes_per_launch": dom["by"], "flops_per_launch": dom["fl"], "avg_launch_ms": round(dom["ms"], 5),
+                "fracs": {u: round(f, 4) for u, f in fracs.items()}}
+    launches = [{"kernel": f"{c['name']} ({c['desc']})", "avg_launch_ms": round(c["ms"], 5),
+                 "bytes_per_launch": c["by"], "flops_per_launch": c["fl"],
+                 "fracs": {u: round(f, 4) for u, f in roofline_of(c["ms"], c["by"], c["fl"], c["units"])[2].items()}}
+                for c in cand]
+    epoch_by, epoch_fl = algorithmic(nnz, m_t + n_t, k, p.prec, 2)
     dense = None
     if di["tiles"]:
-        fl = dense_flops(di["tiles"], k)
         dense = {"cells": di["cells"], "tiles": di["tiles"], "stripes": di["stripes"],
                  "share_of_cells": round(di["cells"] / max(1, nnz), 4),
-                 "flops_per_launch": fl,
-                 "mfma_TFLOPs": [round(fl * (2 if dense_pair else 1) / (c[0] / 1e3) / 1e12, 2) if c[0] else None
-                                 for c in dcand],
-                 "bytes_per_launch": [c[1] for c in dcand], "launches_per_epoch": len(dcand)}
+                 "matrix_core_TFLOPs_issued": [round(6 * 256 * k * di["tiles"] / (c["ms"] / 1e3) / 1e12, 2)
+                                               for c in cand if c["kind"] == "dense"]}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -450,7 +513,10 @@ def main():
                                  "first_batch_cells": sparse_nnz} if args.minibatch else None},
         "roofline": roofline,
         "cpu_baseline": cpu,
-        "compulsory_GBps_per_epoch": round(epoch_bytes / (ms_per_step / 1e3) / 1e9, 2),
+        "epoch_algorithmic": {"bytes": epoch_by, "flops": epoch_fl,
+                              "GBps": round(epoch_by / (ms_per_step / 1e3) / 1e9, 2),
+                              "TFLOPs": round(epoch_fl / (ms_per_step / 1e3) / 1e12, 3)},
+        "launches": launches,
         "device_epoch_ms": tm["epoch_ms"] / max(1, tm["epochs"]),
         "timed_epochs": tm["epochs"],
         "kernel_ms_per_epoch": {**({"pq_pass": avg[0]} if pair else {"p_pass": avg[0], "q_pass": avg[1]}),
