@@ -9,11 +9,13 @@
 //    grouped by the owning row (CSR for the P pass, CSC for the Q pass) and
 //    read once per pass with non-temporal loads.
 //  * A bucket is cut into work items of at most E cells.  Each item belongs
-//    to a group of G = K / V lanes; lane g of the group holds V consecutive
-//    factor coordinates [g*V, g*V + V) of the owner row in registers.
-//  * Per cell the group gathers the other factor row (16 bytes per lane), forms
-//    the dot product with a DPP butterfly inside the group (all lanes end with
-//    the same bits), and accumulates e * q into its registers.
+//    to a group of G = K / V lanes; lane g of the group holds V coordinates of
+//    the owner row in registers: [g*V, g*V + V) when V coordinates fill one
+//    16-byte chunk of the gathered table, else chunks g, g + G, g + 2G, ...
+//    (so that each gather instruction reads consecutive bytes; see Lanes).
+//  * Per cell the group gathers the other factor row (16 bytes per lane and
+//    chunk), forms the dot product with a DPP butterfly inside the group (all
+//    lanes end with the same bits), and accumulates e * q into its registers.
 //  * The aggregated gradient goes straight to the owner row when the bucket is
 //    one item; split buckets leave one partial sum per item and a fixup kernel
 //    adds the parts in item order.  No atomics touch factor or gradient memory,
@@ -122,6 +124,51 @@ __device__ __forceinline__ void store_f32(float *p, const float (&x)[V]) {
     for (int c = 0; c < V / 4; ++c) q[c] = make_float4(x[4 * c], x[4 * c + 1], x[4 * c + 2], x[4 * c + 3]);
 }
 
+// The coordinates a lane holds.  A row of the gathered table is read in
+// 16-byte chunks (Q coordinates: 8 in bf16, 4 in fp32); lane lg of a group of
+// G lanes holds V / Q of them, its n-th being chunk n G + lg of the row, so
+// that one gather instruction of a group reads G * 16 consecutive bytes
+// (whole 128-byte lines at G = 8) instead of a strided part of every line of
+// the row.  Element n Q + j of a lane's arrays is coordinate coord(lg, n) + j;
+// with one chunk per lane this is the plain split lg V .. lg V + V - 1.
+template <int G, int V, bool BF16>
+struct Lanes {
+    static constexpr int Q = BF16 ? 8 : 4;
+    static constexpr int N = V / Q;
+    static_assert(V % Q == 0, "a lane holds whole 16-byte chunks");
+    static __device__ __forceinline__ int coord(int lg, int n) { return (n * G + lg) * Q; }
+};
+
+// This lane's coordinates of an fp32 row (row points at coordinate 0).
+template <int G, int V, bool BF16>
+__device__ __forceinline__ void load_coords(const float *row, int lg, float (&x)[V]) {
+    using L = Lanes<G, V, BF16>;
+#pragma unroll
+    for (int n = 0; n < L::N; ++n) {
+#pragma unroll
+        for (int w = 0; w < L::Q / 4; ++w) {
+            const float4 t = *reinterpret_cast<const float4 *>(row + L::coord(lg, n) + 4 * w);
+            x[n * L::Q + 4 * w + 0] = t.x;
+            x[n * L::Q + 4 * w + 1] = t.y;
+            x[n * L::Q + 4 * w + 2] = t.z;
+            x[n * L::Q + 4 * w + 3] = t.w;
+        }
+    }
+}
+
+template <int G, int V, bool BF16>
+__device__ __forceinline__ void store_coords(float *row, int lg, const float (&x)[V]) {
+    using L = Lanes<G, V, BF16>;
+#pragma unroll
+    for (int n = 0; n < L::N; ++n) {
+#pragma unroll
+        for (int w = 0; w < L::Q / 4; ++w) {
+            const int e = n * L::Q + 4 * w;
+            *reinterpret_cast<float4 *>(row + L::coord(lg, n) + 4 * w) = make_float4(x[e], x[e + 1], x[e + 2], x[e + 3]);
+        }
+    }
+}
+
 // Cells a lane group takes per chunk (rounded to a multiple of the group).
 #ifndef TSID_CELLS_PER_GROUP
 #define TSID_CELLS_PER_GROUP 8
@@ -152,7 +199,7 @@ template <int G, int V, bool BF16>
 __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg, const float (&x)[V],
                                              const float (&acc_in)[V], int64_t deg) {
     if (A.partial_out) {  // a row block's pass: the sum only, the update comes later
-        store_f32<V>(A.partial_out + (int64_t)row * (G * V) + lg * V, acc_in);
+        store_coords<G, V, BF16>(A.partial_out + (int64_t)row * (G * V), lg, acc_in);
         return;
     }
     float acc[V];
@@ -164,7 +211,7 @@ __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg,
         deg = A.dptr[row + 1] - A.dptr[row];
         if (A.gd_tile_ptr[(row >> 4) + 1] > A.gd_tile_ptr[row >> 4]) {
             float g[V];
-            load_f32<V>(A.gd + (int64_t)row * (G * V) + lg * V, g);
+            load_coords<G, V, BF16>(A.gd + (int64_t)row * (G * V), lg, g);
 #pragma unroll
             for (int v = 0; v < V; ++v) acc[v] += g[v];
         }
@@ -174,7 +221,7 @@ __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg,
     float gxv[V];
 #pragma unroll
     for (int v = 0; v < V; ++v) gxv[v] = 0.f;
-    if (A.gx) load_f32<V>(A.gx + (int64_t)row * (G * V) + lg * V, gxv);
+    if (A.gx) load_coords<G, V, BF16>(A.gx + (int64_t)row * (G * V), lg, gxv);
     float xn[V];
     bool bad = false;
     float nrm = 0.f;
@@ -192,8 +239,8 @@ __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg,
         bad |= !__builtin_isfinite(xn[v]);
         nrm += x[v] * x[v];
     }
-    const int64_t off = (int64_t)row * (G * V) + lg * V;
-    store_f32<V>(A.Xn + off, xn);
+    const int64_t off = (int64_t)row * (G * V);
+    store_coords<G, V, BF16>(A.Xn + off, lg, xn);
     if constexpr (BF16) {
         static_assert(V % 8 == 0, "bf16 rows hold a multiple of 8 coordinates per lane");
         if (A.Xn_b) {
@@ -203,7 +250,8 @@ __device__ __forceinline__ void finalize_row(const PassArgs &A, int row, int lg,
 #pragma unroll
                 for (int p = 0; p < 4; ++p)
                     w[p] = bf16_bits(xn[8 * c + 2 * p]) | (bf16_bits(xn[8 * c + 2 * p + 1]) << 16);
-                reinterpret_cast<uint4 *>(A.Xn_b + off)[c] = make_uint4(w[0], w[1], w[2], w[3]);
+                *reinterpret_cast<uint4 *>(A.Xn_b + off + Lanes<G, V, true>::coord(lg, c)) =
+                    make_uint4(w[0], w[1], w[2], w[3]);
             }
         }
     }
@@ -300,7 +348,7 @@ __device__ __forceinline__ void process_block(const PassArgs &A, const YTable &Y
                 const int b = group_bcast<G>(cur[(c0 + t) / G].x, (c0 + t) % G);
 #pragma unroll
                 for (int c = 0; c < V / 8; ++c) {
-                    const uint4 q = ygather16<BUF>(Yt, b, K * 2, (lg * V + 8 * c) * 2);
+                    const uint4 q = ygather16<BUF>(Yt, b, K * 2, Lanes<G, V, true>::coord(lg, c) * 2);
                     yw[t][4 * c + 0] = q.x;
                     yw[t][4 * c + 1] = q.y;
                     yw[t][4 * c + 2] = q.z;
@@ -353,7 +401,7 @@ __device__ __forceinline__ void process_block(const PassArgs &A, const YTable &Y
                 const int b = group_bcast<G>(cur[(c0 + t) / G].x, (c0 + t) % G);
 #pragma unroll
                 for (int c = 0; c < V / 4; ++c) {
-                    const uint4 q = ygather16<BUF>(Yt, b, K * 4, (lg * V + 4 * c) * 4);
+                    const uint4 q = ygather16<BUF>(Yt, b, K * 4, Lanes<G, V, false>::coord(lg, c) * 4);
                     y[t][4 * c + 0] = __uint_as_float(q.x);
                     y[t][4 * c + 1] = __uint_as_float(q.y);
                     y[t][4 * c + 2] = __uint_as_float(q.z);
@@ -431,7 +479,7 @@ __device__ __forceinline__ void item_pass_group(const PassArgs &A, const int64_t
         beg = rb + q * deg / parts;
         end = rb + (q + 1) * deg / parts;
         const int64_t orow = A.owner_mod ? row % A.owner_mod : row;
-        load_f32<V>(A.X + orow * K + lg * V, x);
+        load_coords<G, V, BF16>(A.X + orow * K, lg, x);
     } else {
 #pragma unroll
         for (int v = 0; v < V; ++v) x[v] = 0.f;
@@ -583,7 +631,7 @@ __global__ __launch_bounds__(kThreads) void k_fixup(const PassArgs A) {
         for (int v = 0; v < V; ++v) acc[v] += part[v];
     }
     float x[V];
-    load_f32<V>(A.X + (A.owner_mod ? row % A.owner_mod : row) * K + lg * V, x);
+    load_coords<G, V, BF16>(A.X + (A.owner_mod ? row % A.owner_mod : row) * K, lg, x);
     finalize_row<G, V, BF16>(A, (int)row, lg, x, acc, A.ptr[row + 1] - A.ptr[row]);
 }
 
@@ -616,15 +664,15 @@ __global__ __launch_bounds__(kThreads) void k_block_combine(const PassArgs A, co
     const int64_t row = ((int64_t)blockIdx.x * kWaves + (threadIdx.x >> 6)) * NG + grp;
     if (row >= A.rows) return;
     float acc[V];
-    load_f32<V>(part + row * K + lg * V, acc);
+    load_coords<G, V, BF16>(part + row * K, lg, acc);
     for (int32_t j = 1; j < n_blocks; ++j) {
         float p[V];
-        load_f32<V>(part + ((int64_t)j * A.rows + row) * K + lg * V, p);
+        load_coords<G, V, BF16>(part + ((int64_t)j * A.rows + row) * K, lg, p);
 #pragma unroll
         for (int v = 0; v < V; ++v) acc[v] += p[v];
     }
     float x[V];
-    load_f32<V>(A.X + row * K + lg * V, x);
+    load_coords<G, V, BF16>(A.X + row * K, lg, x);
     finalize_row<G, V, BF16>(A, (int)row, lg, x, acc, A.ptr[row + 1] - A.ptr[row]);
 }
 
@@ -720,7 +768,7 @@ __global__ __launch_bounds__(kThreads) void k_extend_steps(const PassArgs A, int
             bad |= !__builtin_isfinite(x[v]);
         }
     }
-    if (grp == 0) store_f32<V>(A.Xn + row * K + lg * V, x);
+    if (grp == 0) store_coords<G, V, false>(A.Xn + row * K, lg, x);
     if (bad) A.err[ERR_NONFINITE] = 1;
 }
 
