@@ -320,9 +320,9 @@ tsid_status tsid_fit_pass_kernels(const tsid_ctx *ctx, int32_t *p_pass, int32_t 
  * remaining cells and adds the tile sums before the update.  The epochs are
  * the same; rounding differs from the all-item path at the level of the
  * bf16 factors (Section 5.3).
- *  fill < 0   (default) automatic: fill 0.15, used when bf16, k in
- *             {16, 32, 64, 128}, and the dense tiles hold at least 10% of
- *             the cells.
+ *  fill < 0   (default) automatic: fill 0.15 (0.10 at k = 128), used
+ *             when bf16, k in {16, 32, 64, 128}, and the dense tiles hold
+ *             at least 10% of the cells.
  *  fill = 0   off.
  *  0 < fill <= 1  forced with this fill threshold (bf16 fits with k in
  *             {16, 32, 64, 128}; other fits return E_INVAL).

@@ -34,7 +34,12 @@ EPOCH_TOL = 1e-4
 LOSS0_TOL = 1e-5
 LOSS_TRAJ_TOL = 1e-2
 BF16_RMSE_TOL = 1e-2
-AUTO_FILL = 0.15  # the automatic rule's tile fill (tsid_set_dense_tiles)
+
+
+def auto_fill(k):
+    """The automatic rule's tile fill (tsid_set_dense_tiles): 0.15, and 0.10
+    at k = 128."""
+    return 0.10 if k >= 128 else 0.15
 
 
 def _case(name):
@@ -150,7 +155,7 @@ def test_dense_mid_fit_rmse_matches_oracle(T):
     assert st == 0
     info = T.dense_info()
     _, _, a, b, v = oracle_template(p)
-    assert info == _tile_info(a, b, p.I.size, p.J.size, AUTO_FILL)  # the automatic rule took the tiles
+    assert info == _tile_info(a, b, p.I.size, p.J.size, auto_fill(p.k))  # the automatic rule took the tiles
     assert info["cells"] >= 0.10 * a.size
     sto, Po, Qo, ho, _ = oracle.fit(a, b, v, p.P0, p.Q0, p.epochs, p.lam, p.lr, p.step, True, p.xi,
                                     bf16=True)

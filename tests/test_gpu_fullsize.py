@@ -12,6 +12,7 @@ relative Frobenius error; Rating-shaped (bf16) its 20 epochs and
 Billion-scale (bf16) 5 epochs, held-out RMSE within 1e-2 relative.
 """
 import functools
+import math
 import time
 
 import numpy as np
@@ -50,10 +51,11 @@ def _sampled_parity(T, p, n_rows=64, n_cols=64, tol=1e-4):
     bf16 = p.prec == "bf16"
     if bf16:
         # the automatic rule takes the dense head tiles (16 x 16 tiles holding
-        # at least ceil(0.15 * 256) = 39 cells) when they hold a tenth of the
-        # cells: the library's count must equal one made here, and rows of
-        # stripes with tiles join the sample
-        thr = 39
+        # at least ceil(fill * 256) cells, fill 0.15, or 0.10 at k = 128: 39
+        # or 26 cells) when they hold a tenth of the cells: the library's
+        # count must equal one made here, and rows of stripes with tiles join
+        # the sample
+        thr = math.ceil((0.10 if p.k >= 128 else 0.15) * 256)
         n_ti, n_tj = (p.I.size + 15) // 16, (p.J.size + 15) // 16
         cnt = np.bincount((a // 16).astype(np.int64) * n_tj + b // 16, minlength=n_ti * n_tj)
         dense = (cnt >= thr).reshape(n_ti, n_tj)
