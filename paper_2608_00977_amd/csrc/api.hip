@@ -24,9 +24,6 @@ namespace {
 
 constexpr int64_t kDefaultStage = int64_t(1) << 24;  // entries per host-to-device piece
 constexpr int64_t kMaxEntries = (int64_t(1) << 32) - 1;
-// Zero records after the slab pass's stream copy: it reads whole groups of
-// eight records.
-constexpr int64_t kStreamPad = 8;
 
 bool valid_rank(int32_t k) { return k == 8 || k == 16 || k == 32 || k == 64 || k == 128; }
 
@@ -101,8 +98,8 @@ struct SlabPlan {
     bool ready = false, use = false;
     int32_t suits = -1;        // cached slab_suits() of the template (-1: not evaluated)
     int32_t C = 0, n_slabs = 0, S = 0, U = 0, n_blocks = 0;
-    uint32_t *seg = nullptr;
-    int2 *stream = nullptr;    // slab-ordered copy of the side's stream (launch_slab_order)
+    uint32_t *seg = nullptr;   // run pointers of the pass's copy of the stream (SlabArgs)
+    uint4 *sblk = nullptr;     // the copy itself (launch_slab_order)
     float *carry = nullptr;
     int64_t units() const { return (int64_t)n_blocks * U; }
     int64_t lanes() const { return units() * kSlabLanes; }
@@ -474,7 +471,7 @@ void free_template(tsid_ctx *c, Template *&t) {
         }
     for (SlabPlan &sp : t->slab) {
         A.release(sp.seg);
-        A.release(sp.stream);
+        A.release(sp.sblk);
         A.release(sp.carry);
     }
     free_dense(c, t->dense);
@@ -938,10 +935,11 @@ bool slab_suits(const Template &t, int side) {
     return (double)maxdeg <= 2.0 * mean + 64.0;
 }
 
-// Workgroups the slab pass aims for: one round of the compute units, with as
-// many resident workgroups per unit as its LDS holds slabs (TSID_SLAB_UNITS
-// overrides, a tuning knob).
-int64_t slab_target_units(int device) {
+// Workgroups one side's slab pass aims for: the `sides` passes of an epoch
+// (one launch) together fill one round of the compute units, with as many
+// resident workgroups per unit as its LDS holds slabs.  TSID_SLAB_UNITS, a
+// tuning knob, sets the count per side instead.
+int64_t slab_target_units(int device, int sides) {
     if (const char *e = std::getenv("TSID_SLAB_UNITS")) {
         const long v = std::strtol(e, nullptr, 10);
         if (v > 0) return v;
@@ -949,12 +947,12 @@ int64_t slab_target_units(int device) {
     int cus = 0, lds = 0;
     TSID_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device));
     TSID_HIP(hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, device));
-    return (int64_t)std::max(1, cus) * std::max(1, lds / kSlabBytes);
+    return std::max<int64_t>(1, (int64_t)std::max(1, cus) * std::max(1, lds / kSlabBytes) / std::max(1, sides));
 }
 
-// Decides (per fit, from the pass-kernel mode and the precision) whether side
-// `side` runs the slab pass, and builds its plan the first time it does.
-void ensure_slab(tsid_ctx *c, int side, int prec) {
+// Whether side `side` runs the slab pass in this fit (from the pass-kernel
+// mode and the precision).
+bool slab_wanted(tsid_ctx *c, int side, int prec) {
     Template &t = *c->tpl;
     SlabPlan &sp = t.slab[side];
     const int mode = c->pass_kernel;
@@ -968,36 +966,62 @@ void ensure_slab(tsid_ctx *c, int side, int prec) {
         want = sp.suits == 1 && prec == TSID_FP32;
     }
     const int32_t rows = side ? t.n_t : t.m_t, y_rows = side ? t.m_t : t.n_t;
-    want = want && rows > 0 && y_rows > 0;  // an empty side has no cells: the item pass shrinks it
+    return want && rows > 0 && y_rows > 0;  // an empty side has no cells: the item pass shrinks it
+}
+
+// Sets whether side `side` runs the slab pass (`want`), and builds its plan
+// the first time it does.  `sides`: how many sides run it; their passes
+// share one launch, so together they aim for one round of the compute units.
+void ensure_slab(tsid_ctx *c, int side, bool want, int sides) {
+    Template &t = *c->tpl;
+    SlabPlan &sp = t.slab[side];
+    const int32_t rows = side ? t.n_t : t.m_t, y_rows = side ? t.m_t : t.n_t;
     if (want && !sp.ready) {
         Arena &A = c->arena;
         hipStream_t cs = c->comp;
         const int32_t C = slab_rows(t.k);
         const int32_t n_slabs = std::max(1, ceil_div(y_rows, C));
         const int32_t n_blocks = ceil_div(rows, kSlabLanes);
-        const int64_t u_target = std::max<int64_t>(1, slab_target_units(c->device) / n_blocks);
+        const int64_t u_target = std::max<int64_t>(1, slab_target_units(c->device, sides) / n_blocks);
         const int32_t S = ceil_div(n_slabs, std::min<int64_t>(u_target, n_slabs));
         const int32_t U = ceil_div(n_slabs, S);
-        uint32_t *seg = nullptr;
-        int2 *stream = nullptr;
+        uint32_t *seg = nullptr, *pseg = nullptr;
+        uint4 *sblk = nullptr;
         float *carry = nullptr;
         try {
-            seg = A.alloc<uint32_t>((int64_t)(n_slabs + 1) * rows);
-            stream = A.alloc<int2>(t.nnz + kStreamPad);
-            if (U > 1) carry = A.alloc<float>((int64_t)n_blocks * U * kSlabLanes * t.k);
+            // the runs (x, s) of the bucketed stream, then their places in the
+            // pass's copy: slab-major, each padded to a multiple of 8 records
+            const int64_t nr = (int64_t)n_slabs * rows;
+            seg = A.alloc<uint32_t>(nr + rows);
             const int2 *src = side ? t.stream_c : t.stream_r;
             launch_slab_seg(src, side ? t.col_ptr : t.row_ptr, rows, n_slabs, C, seg, cs);
-            launch_slab_order(src, seg, rows, n_slabs, stream, cs);
-            TSID_HIP(hipMemsetAsync(stream + t.nnz, 0, kStreamPad * sizeof(int2), cs));
+            std::vector<uint32_t> hs((size_t)(nr + rows)), hp((size_t)nr + 1);
+            TSID_HIP(hipMemcpyAsync(hs.data(), seg, hs.size() * 4, hipMemcpyDeviceToHost, cs));
             TSID_HIP(hipStreamSynchronize(cs));
+            int64_t pos = 0;
+            for (int64_t r = 0; r < nr; ++r) {
+                hp[(size_t)r] = (uint32_t)pos;
+                pos += ((int64_t)(hs[(size_t)(r + rows)] - hs[(size_t)r]) + 7) / 8 * 8;
+                if (pos > (int64_t)UINT32_MAX) fail(TSID_E_INVAL, "slab stream too long for 32-bit pointers");
+            }
+            hp[(size_t)nr] = (uint32_t)pos;
+            pseg = A.alloc<uint32_t>(nr + 1);
+            sblk = A.alloc<uint4>(std::max<int64_t>(pos / 8 * 3, 3));  // 48 bytes per 8 records
+            if (U > 1) carry = A.alloc<float>((int64_t)n_blocks * U * kSlabLanes * t.k);
+            TSID_HIP(hipMemcpyAsync(pseg, hp.data(), hp.size() * 4, hipMemcpyHostToDevice, cs));
+            launch_slab_order(src, seg, rows, n_slabs, C, pseg, sblk, cs);
+            TSID_HIP(hipStreamSynchronize(cs));
+            A.release(seg);
+            seg = nullptr;
         } catch (...) {
             A.release(seg);
-            A.release(stream);
+            A.release(pseg);
+            A.release(sblk);
             A.release(carry);
             throw;
         }
-        sp.seg = seg;
-        sp.stream = stream;
+        sp.seg = pseg;
+        sp.sblk = sblk;
         sp.carry = carry;
         sp.C = C;
         sp.n_slabs = n_slabs;
@@ -1309,8 +1333,9 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs, bool dense, i
     if (item_only) {
         t.slab[0].use = t.slab[1].use = false;
     } else {
-        ensure_slab(c, 0, prec);
-        ensure_slab(c, 1, prec);
+        const bool w0 = slab_wanted(c, 0, prec), w1 = slab_wanted(c, 1, prec);
+        ensure_slab(c, 0, w0, w0 + w1);
+        ensure_slab(c, 1, w1, w0 + w1);
     }
     if (dense)
         ensure_dense(c, prec);
@@ -1541,8 +1566,9 @@ DenseArgs dense_args(const Template &t, int side, int32_t *err) {
 SlabArgs slab_args(const Template &t, int side, const tsid_fit_opts &o, int32_t *err) {
     const SlabPlan &sp = t.slab[side];
     SlabArgs a{};
-    a.stream = sp.stream;
+    a.sblk = sp.sblk;
     a.seg = sp.seg;
+    a.ptr = side ? t.col_ptr : t.row_ptr;
     a.rows = side ? t.n_t : t.m_t;
     a.y_rows = side ? t.m_t : t.n_t;
     a.C = sp.C;

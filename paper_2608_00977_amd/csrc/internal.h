@@ -238,8 +238,16 @@ constexpr int kSlabLanes = TSID_SLAB_LANES;
 constexpr int kSlabBytes = TSID_SLAB_KIB * 1024;
 
 struct SlabArgs {
-    const int2 *stream;      // the slab-ordered copy of the bucketed cells, padded by 8 records
-    const uint32_t *seg;     // seg[s * rows + x]: first cell of bucket x with other id >= s * C
+    // The pass's own copy of the cells (launch_slab_order): for each slab s
+    // and bucket x (slab-major: all runs of slab 0, then slab 1, ...) the
+    // bucket's cells whose other id lies in the slab, padded to a multiple
+    // of 8 records.  Records j = 8 g .. 8 g + 7 form block g of 48 bytes,
+    // sblk[3 g .. 3 g + 2]: their rows within the slab (other id - s * C,
+    // 16 bits each; C for a pad, the zero row the pass keeps after the slab
+    // in LDS), then their values (fp32; 0 for a pad).
+    const uint4 *sblk;
+    const uint32_t *seg;     // seg[s * rows + x]: first record of run (x, s); seg[n_slabs * rows]: total
+    const int64_t *ptr;      // bucket pointers of the template (a row's degree)
     int32_t rows;            // owner rows (buckets)
     int32_t y_rows;          // rows of the gathered factor
     int32_t C;               // gathered rows per slab
@@ -264,10 +272,13 @@ bool slab_supported(int K, int prec);
 int slab_rows(int K);  // C for rank K
 void launch_slab_seg(const int2 *stream, const int64_t *ptr, int32_t rows, int32_t n_slabs, int32_t C,
                      uint32_t *seg, hipStream_t s);
-// The slab pass's copy of a stream: every slab run of bucket x lists the cells
-// whose other index has parity (x >> 3) & 1 first (see slab.hip).
-void launch_slab_order(const int2 *stream, const uint32_t *seg, int32_t rows, int32_t n_slabs, int2 *out,
-                       hipStream_t s);
+// The slab pass's copy of a stream (see SlabArgs): run (x, s) of the
+// bucketed stream, cells seg[s * rows + x] .. seg[(s + 1) * rows + x] - 1,
+// goes to records pseg[s * rows + x] .. pseg[s * rows + x + 1] - 1, the
+// cells whose other index has parity (x >> 3) & 1 first (see slab.hip),
+// then pads.
+void launch_slab_order(const int2 *stream, const uint32_t *seg, int32_t rows, int32_t n_slabs, int32_t C,
+                       const uint32_t *pseg, uint4 *sblk, hipStream_t s);
 // The pass over n_units workgroups.  With U == 1 it updates the rows itself;
 // with U > 1 (and not loss-only) launch_slab_finish then adds each row's U
 // partial sums and updates it.

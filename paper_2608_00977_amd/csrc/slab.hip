@@ -14,8 +14,11 @@
 //  * The gathered factor is cut into slabs of C rows (128 KiB each).  The
 //    workgroup copies one slab at a time into LDS with coalesced loads, then
 //    every lane walks the cells of its row whose other index lies in the slab
-//    (a contiguous run of the bucketed stream, located by the slab pointers
-//    seg[s][x]) and reads the other factor rows from LDS.  A slab row is read
+//    (a run of the pass's own copy of the stream: 2 bytes of row within the
+//    slab and 4 bytes of value per cell in 48-byte blocks of eight cells,
+//    runs padded to whole blocks and stored slab-major; see SlabArgs) and
+//    reads the other
+//    factor rows from LDS.  A slab row is read
 //    by every owner row of the block that observes it, so the gathers leave
 //    the cache hierarchy and cost LDS bandwidth only.  A wave runs as long as
 //    its busiest lane, so slabs are as large as LDS allows: the longer each
@@ -70,7 +73,7 @@ template <int K>
 __device__ __forceinline__ void finalize_lane(const SlabArgs &A, int xr, int rot,
                                               const float4 (&x)[K / 4], const float4 (&acc)[K / 4]) {
     constexpr int NCH = K / 4;
-    const uint32_t deg = A.seg[(int64_t)A.n_slabs * A.rows + xr] - A.seg[xr];
+    const int64_t deg = A.ptr[xr + 1] - A.ptr[xr];
     const float s = A.degree ? 1.0f / (float)(deg > 1 ? deg : 1) : 1.0f;
     float4 *out = reinterpret_cast<float4 *>(A.Xn + (int64_t)xr * K);
     bool bad = false;
@@ -96,22 +99,25 @@ __device__ __forceinline__ void finalize_lane(const SlabArgs &A, int xr, int rot
     if (bad) A.err[ERR_NONFINITE] = A.epoch + 1;
 }
 
-// Eight consecutive stream records starting at p (the stream is padded by
-// eight records, so the read never leaves the buffer).
-__device__ __forceinline__ void load8(const int2 *p, int2 (&r)[8]) {
-#pragma unroll
-    for (int c = 0; c < 8; ++c) r[c] = p[c];
+// The eight records of a run from record j (a multiple of 8): one 48-byte
+// block, their rows within the slab and their values.  A lane reads its run
+// block after block, so it has one partly read 128-byte line at a time.
+struct Burst {
+    uint4 ix;        // eight 16-bit rows, two per word (low half first)
+    float4 v0, v1;   // the eight values
+};
+
+__device__ __forceinline__ void load_burst(const SlabArgs &A, uint32_t j, Burst &b) {
+    const uint4 *blk = A.sblk + (size_t)(j >> 3) * 3;
+    b.ix = blk[0];
+    b.v0 = __builtin_bit_cast(float4, blk[1]);
+    b.v1 = __builtin_bit_cast(float4, blk[2]);
 }
 
-// The cells at stream positions j .. j+7 of this lane's run [.., q) in slab
-// rows sbase .. sbase + C - 1: residuals against the LDS rows, e^2 and the
-// gradient sums.  Records at or past q belong to other rows or slabs: their
-// LDS row is replaced by row 0 and their residual by 0 (bit masks, so the
-// work stays branch-free).  The LDS reads of cell c + 1 are issued before the
-// arithmetic of cell c, so a wave has one row in flight while it computes.
-template <int K>
-__device__ __forceinline__ uint32_t slab_row_off(const int2 &rec, uint32_t keep, int32_t sbase) {
-    return ((uint32_t)(rec.x - sbase) * (uint32_t)(K * 4)) & keep;
+// First record of burst i of the run [p, q): forwards, or backwards from its
+// end.
+__device__ __forceinline__ uint32_t burst_at(uint32_t p, uint32_t q, int32_t i, bool back) {
+    return back ? q - 8u * (uint32_t)(i + 1) : p + 8u * (uint32_t)i;
 }
 
 template <int K>
@@ -121,9 +127,11 @@ __device__ __forceinline__ void slab_read_row(const char *ysb, uint32_t row_off,
     for (int i = 0; i < K / 4; ++i) y[i] = *reinterpret_cast<const float4 *>(ysb + row_off + koff[i]);
 }
 
+// One cell: residual against its LDS row, e^2 and the gradient sum.  A pad
+// reads the zero row with value 0, so it adds exactly nothing.
 template <int K, bool LOSS_ONLY>
-__device__ __forceinline__ void slab_cell(const float4 (&y)[K / 4], float r, uint32_t keep,
-                                          const float4 (&x)[K / 4], float4 (&acc)[K / 4], float &e2) {
+__device__ __forceinline__ void slab_cell(const float4 (&y)[K / 4], float r, const float4 (&x)[K / 4],
+                                          float4 (&acc)[K / 4], float &e2) {
     constexpr int NCH = K / 4;
 #if TSID_SLAB_CHAINS == 1
     float d = 0.f;
@@ -145,7 +153,7 @@ __device__ __forceinline__ void slab_cell(const float4 (&y)[K / 4], float r, uin
     }
     const float d = (d0 + d1) + (d2 + d3);
 #endif
-    const float e = __uint_as_float(__float_as_uint(r - d) & keep);
+    const float e = r - d;
     e2 += e * e;
     if constexpr (!LOSS_ONLY) {
 #pragma unroll
@@ -158,14 +166,22 @@ __device__ __forceinline__ void slab_cell(const float4 (&y)[K / 4], float r, uin
     }
 }
 
+// The eight cells of a burst.  The LDS reads of cell c + 1 are issued before
+// the arithmetic of cell c, so a wave has one row in flight while it
+// computes.
 template <int K, bool LOSS_ONLY>
-__device__ __forceinline__ void slab_burst(const int2 (&rec)[8], uint32_t j, uint32_t q, int32_t sbase,
-                                           const char *ysb, const uint32_t (&koff)[K / 4],
+__device__ __forceinline__ void slab_burst(const Burst &b, const char *ysb, const uint32_t (&koff)[K / 4],
                                            const float4 (&x)[K / 4], float4 (&acc)[K / 4], float &e2) {
     constexpr int NCH = K / 4;
-    uint32_t keep[8];
+    constexpr uint32_t RB = K * 4;  // bytes per LDS row
+    const uint32_t w[4] = {b.ix.x, b.ix.y, b.ix.z, b.ix.w};
+    uint32_t off[8];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) keep[c] = j + c < q ? 0xffffffffu : 0u;
+    for (int c = 0; c < 4; ++c) {
+        off[2 * c] = (w[c] & 0xffffu) * RB;
+        off[2 * c + 1] = (w[c] >> 16) * RB;
+    }
+    const float r[8] = {b.v0.x, b.v0.y, b.v0.z, b.v0.w, b.v1.x, b.v1.y, b.v1.z, b.v1.w};
     if constexpr (K > 32) {
         // k = 64: two rows of 64 registers in flight would spill; read and
         // compute two cells at a time instead
@@ -173,23 +189,23 @@ __device__ __forceinline__ void slab_burst(const int2 (&rec)[8], uint32_t j, uin
         for (int c = 0; c < 8; c += 2) {
             __builtin_amdgcn_sched_barrier(0);
             float4 y0[NCH], y1[NCH];
-            slab_read_row<K>(ysb, slab_row_off<K>(rec[c], keep[c], sbase), koff, y0);
-            slab_read_row<K>(ysb, slab_row_off<K>(rec[c + 1], keep[c + 1], sbase), koff, y1);
-            slab_cell<K, LOSS_ONLY>(y0, __int_as_float(rec[c].y), keep[c], x, acc, e2);
-            slab_cell<K, LOSS_ONLY>(y1, __int_as_float(rec[c + 1].y), keep[c + 1], x, acc, e2);
+            slab_read_row<K>(ysb, off[c], koff, y0);
+            slab_read_row<K>(ysb, off[c + 1], koff, y1);
+            slab_cell<K, LOSS_ONLY>(y0, r[c], x, acc, e2);
+            slab_cell<K, LOSS_ONLY>(y1, r[c + 1], x, acc, e2);
         }
         return;
     }
     float4 ya[NCH], yb[NCH];
-    slab_read_row<K>(ysb, slab_row_off<K>(rec[0], keep[0], sbase), koff, ya);
+    slab_read_row<K>(ysb, off[0], koff, ya);
 #pragma unroll
     for (int c = 0; c < 8; c += 2) {
         __builtin_amdgcn_sched_barrier(0);
-        slab_read_row<K>(ysb, slab_row_off<K>(rec[c + 1], keep[c + 1], sbase), koff, yb);
-        slab_cell<K, LOSS_ONLY>(ya, __int_as_float(rec[c].y), keep[c], x, acc, e2);
+        slab_read_row<K>(ysb, off[c + 1], koff, yb);
+        slab_cell<K, LOSS_ONLY>(ya, r[c], x, acc, e2);
         __builtin_amdgcn_sched_barrier(0);
-        if (c + 2 < 8) slab_read_row<K>(ysb, slab_row_off<K>(rec[c + 2], keep[c + 2], sbase), koff, ya);
-        slab_cell<K, LOSS_ONLY>(yb, __int_as_float(rec[c + 1].y), keep[c + 1], x, acc, e2);
+        if (c + 2 < 8) slab_read_row<K>(ysb, off[c + 2], koff, ya);
+        slab_cell<K, LOSS_ONLY>(yb, r[c + 1], x, acc, e2);
     }
 }
 
@@ -199,7 +215,7 @@ __device__ __forceinline__ void slab_pass_unit(const SlabArgs &A, const int u) {
     constexpr int NCH = K / 4;                        // 16-byte chunks per factor row
     constexpr int RM = (NCH < 8 ? NCH : 8) - 1;       // lane rotation mask
     static_assert((NCH & (NCH - 1)) == 0, "rows hold a power-of-two number of chunks");
-    extern __shared__ float4 ys[];                    // one slab: C rows x NCH chunks
+    extern __shared__ float4 ys[];                    // one slab (C rows x NCH chunks), then a zero row
     if (A.skip_after_nonfinite) {
         const int32_t f = A.err[ERR_NONFINITE];
         if (f != 0 && f - 1 < A.epoch) return;  // same outcome for every workgroup
@@ -212,6 +228,7 @@ __device__ __forceinline__ void slab_pass_unit(const SlabArgs &A, const int u) {
     const int xr = blk * kLanes + tid;
     const bool own = xr < A.rows;
     const int rot = tid & RM;
+    const bool back = (xr & 1) != 0;  // this row walks its runs backwards
 
     float4 x[NCH], acc[NCH];
     uint32_t koff[NCH];  // byte offset of slot c's chunk within an LDS row
@@ -234,6 +251,9 @@ __device__ __forceinline__ void slab_pass_unit(const SlabArgs &A, const int u) {
     // direct global-to-LDS loads write 16 bytes per lane at consecutive
     // addresses from a wave-uniform base.
     const int wave_base = __builtin_amdgcn_readfirstlane(tid & ~63);
+    // the row the pads read (the slab copies never write it; the first
+    // barrier below orders this store before any read)
+    if (tid < NCH) ys[nf4 + tid] = f4_zero();
     for (int s = s0; s < s1; ++s) {
         // The lane's run bounds and its first records are requested before
         // the barrier, the slab right after it with every copy in flight, so
@@ -241,10 +261,10 @@ __device__ __forceinline__ void slab_pass_unit(const SlabArgs &A, const int u) {
         uint32_t p = 0, q = 0;
         if (own) {
             p = A.seg[(int64_t)s * A.rows + xr];
-            q = A.seg[(int64_t)(s + 1) * A.rows + xr];
+            q = A.seg[(int64_t)s * A.rows + xr + 1];
         }
-        int2 ra[8], rc[8];
-        if (p < q) load8(A.stream + p, ra);
+        Burst ba, bc;
+        if (p < q) load_burst(A, burst_at(p, q, 0, back), ba);
         __syncthreads();  // every lane is done with the previous slab
         // Chunks past the table's end (last slab only) repeat its last chunk;
         // no cell refers to those LDS rows.
@@ -258,15 +278,19 @@ __device__ __forceinline__ void slab_pass_unit(const SlabArgs &A, const int u) {
         }
         __builtin_amdgcn_s_waitcnt(0);  // the copies have landed in LDS
         __syncthreads();
-        const int32_t sbase = s * A.C;
-        // The lane's cells in this slab, eight records per burst; the next
-        // burst's records load while this one computes.
-        for (uint32_t j = p; j < q; j += 16) {
-            if (j + 8 < q) load8(A.stream + j + 8, rc);
-            slab_burst<K, LOSS_ONLY>(ra, j, q, sbase, ysb, koff, x, acc, e2);
-            if (j + 8 >= q) break;
-            if (j + 16 < q) load8(A.stream + j + 16, ra);
-            slab_burst<K, LOSS_ONLY>(rc, j + 8, q, sbase, ysb, koff, x, acc, e2);
+        // The lane's cells in this slab (a whole number of bursts of eight
+        // records); the next burst's records load while this one computes.
+        // Odd rows walk their runs backwards: a line shared by the runs of
+        // rows x and x + 1 (adjacent in memory) is then read by both lanes
+        // at about the same time, at the start or at the end of their runs,
+        // rather than once at each end of the slab.
+        const int32_t n = (int32_t)(q - p) >> 3;
+        for (int32_t i = 0; i < n; i += 2) {
+            if (i + 1 < n) load_burst(A, burst_at(p, q, i + 1, back), bc);
+            slab_burst<K, LOSS_ONLY>(ba, ysb, koff, x, acc, e2);
+            if (i + 1 >= n) break;
+            if (i + 2 < n) load_burst(A, burst_at(p, q, i + 2, back), ba);
+            slab_burst<K, LOSS_ONLY>(bc, ysb, koff, x, acc, e2);
         }
     }
 
@@ -358,7 +382,7 @@ __device__ __forceinline__ void slab_finish_lane(const SlabArgs &A, const int64_
         tot.w += q.w;
     }
     const float4 x = reinterpret_cast<const float4 *>(A.X + xs * K)[ch];
-    const uint32_t deg = A.seg[(int64_t)A.n_slabs * A.rows + xs] - A.seg[xs];
+    const int64_t deg = A.ptr[xs + 1] - A.ptr[xs];
     const float s = A.degree ? 1.0f / (float)(deg > 1 ? deg : 1) : 1.0f;
     bool bad = false;
     float nrm = 0.f;
@@ -427,37 +451,49 @@ void allow_lds(Kern kernel, size_t bytes) {
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes));
 }
 
-// The slab pass's own copy of a bucketed stream.  Within every slab run of
-// bucket x the cells whose other index b has the parity (x >> 3) & 1 come
-// first, then the rest, each part in the stream's order.  A staged LDS row
-// lies in one half of the 64 banks according to the parity of b, and the
-// lanes x and x + 8 of a 16-lane LDS group read the same chunk index (lane
-// rotation), so with this order they read opposite halves for most of their
-// runs instead of colliding whenever their rows' parities agree.
-__global__ void k_slab_order(const int2 *stream, const uint32_t *seg, int32_t rows, int32_t n_slabs,
-                             int2 *out) {
+// The slab pass's own copy of a bucketed stream (see SlabArgs).  Within
+// every run (x, s) the cells whose other index b has the parity
+// (x >> 3) & 1 come first, then the rest, each part in the stream's order,
+// then the pads.  A staged LDS row lies in one half of the 64 banks
+// according to the parity of b, and the lanes x and x + 8 of a 16-lane LDS
+// group read the same chunk index (lane rotation), so with this order they
+// read opposite halves for most of their runs instead of colliding whenever
+// their rows' parities agree.  Runs are stored slab-major, so the runs one
+// workgroup walks in a slab are one contiguous stretch of memory, and a line
+// shared by two runs is read by neighbouring lanes at the same time.
+__global__ void k_slab_order(const int2 *stream, const uint32_t *seg, int32_t rows, int32_t n_slabs, int32_t C,
+                             const uint32_t *pseg, uint4 *sblk) {
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (t >= (int64_t)n_slabs * rows) return;
     const int32_t s = (int32_t)(t / rows), x = (int32_t)(t % rows);
     const uint32_t p = seg[(int64_t)s * rows + x], q = seg[(int64_t)(s + 1) * rows + x];
     const int first = (x >> 3) & 1;
-    uint32_t o = p;
-    for (uint32_t j = p; j < q; ++j) {
-        const int2 c = stream[j];
-        if ((c.x & 1) == first) out[o++] = c;
+    const int32_t base = s * C;
+    // record o: 16-bit row o % 8 of block o / 8, then value o % 8 after the
+    // block's 16 bytes of rows
+    uint16_t *const rows16 = reinterpret_cast<uint16_t *>(sblk);
+    float *const vals = reinterpret_cast<float *>(sblk);
+    auto put = [&](uint32_t o, uint16_t r, float v) {
+        const size_t g = (size_t)(o >> 3) * 24, i = o & 7;  // block start in 16-bit units
+        rows16[g + i] = r;
+        vals[g / 2 + 4 + i] = v;
+    };
+    uint32_t o = pseg[t];
+    for (int pass = 0; pass < 2; ++pass) {
+        for (uint32_t j = p; j < q; ++j) {
+            const int2 c = stream[j];
+            if (((c.x & 1) == first) == (pass == 0)) put(o++, (uint16_t)(c.x - base), __int_as_float(c.y));
+        }
     }
-    for (uint32_t j = p; j < q; ++j) {
-        const int2 c = stream[j];
-        if ((c.x & 1) != first) out[o++] = c;
-    }
+    for (const uint32_t e = pseg[t + 1]; o < e; ++o) put(o, (uint16_t)C, 0.f);
 }
 
 template <int K>
 void slab_pass_k(bool loss_only, const SlabArgs &a, int64_t n_units, hipStream_t s, hipEvent_t ev0,
                  hipEvent_t ev1) {
-    const size_t lds = (size_t)a.C * K * 4;
-    static const bool lds_ok = (allow_lds(k_slab_pass<K, true>, kSlabBytes),
-                                allow_lds(k_slab_pass<K, false>, kSlabBytes), true);
+    const size_t lds = (size_t)(a.C + 1) * K * 4;  // the slab and the zero row
+    static const bool lds_ok = (allow_lds(k_slab_pass<K, true>, kSlabBytes + K * 4),
+                                allow_lds(k_slab_pass<K, false>, kSlabBytes + K * 4), true);
     (void)lds_ok;
     if (loss_only)
         hipExtLaunchKernelGGL(k_slab_pass<K, true>, dim3((unsigned)n_units), dim3(kLanes), lds, s, ev0, ev1,
@@ -479,8 +515,8 @@ void slab_finish_k(const SlabArgs &a, hipStream_t s, hipEvent_t ev0, hipEvent_t 
 template <int K>
 void slab_pass_pair_k(const SlabArgs &a0, int64_t n0, const SlabArgs &a1, int64_t n1, hipStream_t s,
                       hipEvent_t ev0, hipEvent_t ev1) {
-    const size_t lds = (size_t)a0.C * K * 4;
-    static const bool lds_ok = (allow_lds(k_slab_pass_pair<K>, kSlabBytes), true);
+    const size_t lds = (size_t)(a0.C + 1) * K * 4;
+    static const bool lds_ok = (allow_lds(k_slab_pass_pair<K>, kSlabBytes + K * 4), true);
     (void)lds_ok;
     hipExtLaunchKernelGGL(k_slab_pass_pair<K>, dim3((unsigned)(n0 + n1)), dim3(kLanes), lds, s, ev0, ev1, 0, a0,
                           a1, (int32_t)n0);
@@ -511,11 +547,11 @@ void launch_slab_seg(const int2 *stream, const int64_t *ptr, int32_t rows, int32
     TSID_HIP(hipGetLastError());
 }
 
-void launch_slab_order(const int2 *stream, const uint32_t *seg, int32_t rows, int32_t n_slabs, int2 *out,
-                       hipStream_t s) {
+void launch_slab_order(const int2 *stream, const uint32_t *seg, int32_t rows, int32_t n_slabs, int32_t C,
+                       const uint32_t *pseg, uint4 *sblk, hipStream_t s) {
     const int64_t n = (int64_t)n_slabs * rows;
     if (n <= 0) return;
-    k_slab_order<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(stream, seg, rows, n_slabs, out);
+    k_slab_order<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(stream, seg, rows, n_slabs, C, pseg, sblk);
     TSID_HIP(hipGetLastError());
 }
 
