@@ -46,6 +46,7 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
 typedef float fl2 __attribute__((ext_vector_type(2)));
+typedef short s4 __attribute__((ext_vector_type(4)));
 
 // Shapes for rank K: 32-coordinate chunks (the k-steps of step 1), 16-
 // coordinate blocks (the gradient products of step 3) and the row stride of
@@ -149,10 +150,16 @@ __device__ __forceinline__ void dense_tile(const bf8 (&yraw)[DenseShape<K>::NC],
         const bf8 ea = __builtin_bit_cast(bf8, make_uint4(h0, h1, l0, l1));
 #pragma unroll
         for (int nb = 0; nb < D::NB; ++nb) {
-            const uint16_t *col = yl + 4 * lq * D::ROW + nb * 16 + lr;
-            const uint32_t b01 = (uint32_t)col[0] | ((uint32_t)col[D::ROW] << 16);
-            const uint32_t b23 = (uint32_t)col[2 * D::ROW] | ((uint32_t)col[3 * D::ROW] << 16);
-            const bf8 b = __builtin_bit_cast(bf8, make_uint4(b01, b23, b01, b23));
+            // column 16 nb + lr of rows 4 lq .. 4 lq + 3 by one transposing LDS
+            // read (ds_read_b64_tr_b16): in each group of 16 lanes, lane i
+            // receives element i % 4 of the 8-byte pieces of lanes i / 4,
+            // 4 + i / 4, 8 + i / 4 and 12 + i / 4, so lane j of the group
+            // points at row 4 lq + j / 4, coordinates 16 nb + 4 (j % 4) .. + 3
+            const uint16_t *src = yl + (4 * lq + (lr >> 2)) * D::ROW + nb * 16 + 4 * (lr & 3);
+            const uint2 w = __builtin_bit_cast(
+                uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                           (__attribute__((address_space(3))) s4 *)(src)));
+            const bf8 b = __builtin_bit_cast(bf8, make_uint4(w.x, w.y, w.x, w.y));
             acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ea, b, acc[nb], 0, 0, 0);
         }
     }
