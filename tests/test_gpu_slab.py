@@ -5,7 +5,9 @@ ABI.
 The slab pass computes the same epochs as the item pass (Eqs. 2-5, Section
 5.3); these tests force it on every fp32 rank it supports, on cases with
 several row blocks, several slabs with a ragged last slab, blocks split over
-several workgroups (partial sums added by the last one) and long buckets.
+several workgroups (partial sums added by the finishing kernel), long
+buckets, and many short or empty runs (the pass's record copy pads every
+run to whole blocks of eight, and odd rows walk their runs backwards).
 Bars as for the item pass: factors within 1e-4 relative Frobenius error, the
 loss of the final iterate within 1e-6, the trajectory within 1e-3, results
 bitwise repeatable.
