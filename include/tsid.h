@@ -406,14 +406,17 @@ tsid_status tsid_set_minibatch(tsid_ctx *ctx, int32_t n_batches, uint64_t seed);
  * bandwidth bounds the pass.  With n blocks, the rows of P are cut into n
  * ranges holding about equal shares of the Q pass's cells; every column's
  * cells whose row falls in block j form one work bucket, all blocks run in
- * one launch, and the workgroups of each group of 8 consecutive blocks are
- * dealt in turn to the device's 8 XCDs, so that each XCD gathers from its
- * own block.  Each bucket stores its partial gradient sum
+ * one launch, and the workgroups of each group of 8 blocks are dealt in turn
+ * to the device's 8 XCDs, so that each XCD gathers from its own block; the
+ * groups pair the blocks from both ends of P (0, n - 1, 1, n - 2, ...), so
+ * that every group gathers from about the same share of the table.  Each
+ * bucket stores its partial gradient sum
  * (n x n_t x k fp32 of device memory); a second kernel adds the n sums of a
  * column in block order and updates it.  The arithmetic is the same; the fp32
  * sums of a column are added in another order.
- *  n_blocks = 0  (default) automatic: blocks of about 16 MiB of P when the
- *                table exceeds 96 MiB (Billion-scale: 16 blocks), else one.
+ *  n_blocks = 0  (default) automatic: blocks of about 11 MiB of P, their
+ *                count rounded up to a multiple of 8, when the table exceeds
+ *                96 MiB (Billion-scale: 24 blocks), else one.
  *  n_blocks = 1  off.   2 <= n_blocks <= TSID_MAX_ROW_BLOCKS: forced.
  * Applies to full-gradient fits whose Q pass runs the item pass.  Takes effect
  * at the next tsid_fit_template.  Errors: E_INVAL (ctx NULL, n_blocks out of

@@ -1380,12 +1380,14 @@ void ensure_fit_buffers(tsid_ctx *c, int32_t prec, int32_t epochs, bool dense, i
 
 // Row blocks of the Q pass for this fit: automatic when the gathered P table
 // exceeds TSID_QBLOCK_MIN_MB (blocks of about TSID_QBLOCK_MB of the table
-// each, at most TSID_MAX_ROW_BLOCKS), else one.  More blocks raise the L2 hit
-// rate of the gathers (Billion-scale: 53 % with 16, 76 % with 64) but cut
-// the columns' runs shorter, and the per-run work (owner row, partial sum)
-// then outweighs it (Q pass 6.1 ms with 16 blocks, 6.3 with 32, 7.2 with 64).
+// each, their count rounded up to a multiple of the XCDs, at most
+// TSID_MAX_ROW_BLOCKS), else one.  More blocks raise the L2 hit rate of the
+// gathers (Billion-scale: 53 % with 16, 76 % with 64) but cut the columns'
+// runs shorter, and the per-run work (owner row, partial sum) then outweighs
+// it; Billion-scale (256 MB of bf16 P) ran its Q pass in 5.02 ms with 16
+// blocks, 4.89-4.93 with 24 and 5.11 with 32 (interleaved order below).
 #ifndef TSID_QBLOCK_MB
-#define TSID_QBLOCK_MB 16
+#define TSID_QBLOCK_MB 11
 #endif
 #ifndef TSID_QBLOCK_MIN_MB
 #define TSID_QBLOCK_MIN_MB 96
@@ -1399,12 +1401,13 @@ int32_t ensure_qblock(tsid_ctx *c, int prec) {
     BlockPlan &qb = t.qb;
     const int64_t table = (int64_t)t.m_t * t.k * (prec == TSID_BF16 ? 2 : 4);
     int32_t nb = c->row_blocks;
-    if (nb == 0)
-        nb = table > (int64_t)TSID_QBLOCK_MIN_MB << 20
-                 ? (int32_t)std::min<int64_t>((table + ((int64_t)TSID_QBLOCK_MB << 20) - 1) /
-                                                  ((int64_t)TSID_QBLOCK_MB << 20),
-                                              TSID_MAX_ROW_BLOCKS)
-                 : 1;
+    if (nb == 0) {
+        nb = 1;
+        if (table > (int64_t)TSID_QBLOCK_MIN_MB << 20) {
+            const int64_t want = (table + ((int64_t)TSID_QBLOCK_MB << 20) - 1) / ((int64_t)TSID_QBLOCK_MB << 20);
+            nb = (int32_t)std::min<int64_t>((want + kXcds - 1) / kXcds * kXcds, TSID_MAX_ROW_BLOCKS);
+        }
+    }
     nb = (int32_t)std::min<int64_t>(nb, std::max<int32_t>(1, t.m_t));
     if (nb <= 1 || t.n_t == 0 || t.slab[1].use) return 1;
     const bool dn = t.dense_use && prec == TSID_BF16;
@@ -1487,16 +1490,31 @@ int32_t ensure_qblock(tsid_ctx *c, int prec) {
             cur = b0 + nj;
         }
         C.off[(size_t)nv] = C.endv[(size_t)nv] = (uint32_t)cur;
-        // workgroup schedule: groups of kXcds consecutive blocks; in a group,
-        // workgroup w takes the next chunk of block (group start + w % kXcds)
+        // workgroup schedule: the blocks in groups of kXcds; in a group,
+        // workgroup w takes the next chunk of the group's block w % kXcds.
+        // order[]: the blocks in schedule order, taken alternately from both
+        // ends (0, nb - 1, 1, nb - 2, ...), so that a group holds hot blocks
+        // (few rows: the most observed) and cold ones (many rows) and the
+        // rows the XCDs gather from at one time are about the same share of
+        // the table in every group.  With consecutive blocks (tuning knob
+        // TSID_QBLOCK_ORDER=0) the group of cold blocks spans most of the
+        // table at once, more than the memory-side cache holds, and the
+        // Billion-scale Q pass ran 5.47 ms instead of 5.02 (16 blocks).
+        std::vector<int32_t> order((size_t)nb);
+        const char *oe = std::getenv("TSID_QBLOCK_ORDER");
+        const int omode = oe ? std::atoi(oe) : 1;
+        for (int32_t q = 0; q < nb; ++q)
+            order[(size_t)q] = omode == 1 ? ((q & 1) ? nb - 1 - q / 2 : q / 2) : q;
         std::vector<int32_t> sched;
         for (int32_t g0 = 0; g0 < nb; g0 += kXcds) {
             int64_t most = 0;
-            for (int32_t j = g0; j < std::min(nb, g0 + kXcds); ++j) most = std::max(most, chunks[(size_t)j]);
+            for (int32_t q = g0; q < std::min(nb, g0 + kXcds); ++q)
+                most = std::max(most, chunks[(size_t)order[(size_t)q]]);
             for (int64_t ch = 0; ch < most; ++ch)
                 for (int x = 0; x < kXcds; ++x) {
-                    const int32_t j = g0 + x;
-                    sched.push_back(j < nb && ch < chunks[(size_t)j] ? (int32_t)(base[(size_t)j] / wg + ch) : -1);
+                    const int32_t q = g0 + x;
+                    const int32_t j = q < nb ? order[(size_t)q] : -1;
+                    sched.push_back(j >= 0 && ch < chunks[(size_t)j] ? (int32_t)(base[(size_t)j] / wg + ch) : -1);
                 }
         }
         try {
