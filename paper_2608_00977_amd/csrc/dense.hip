@@ -189,8 +189,9 @@ __device__ __forceinline__ void dense_pass_group(const DenseArgs &A, const int64
     }
     __shared__ uint16_t ylds[kDenseWaves][16 * D::ROW];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int64_t g = bid * kDenseWaves + wv;  // segment
-    if (g >= A.n_segs) return;  // whole waves leave together
+    const int64_t w = bid * kDenseWaves + wv;
+    if (w >= A.n_segs) return;  // whole waves leave together
+    const int64_t g = A.seg_order[w];  // segment
     const uint32_t t_beg = A.seg_tile[g], t_end = A.seg_tile[g + 1];  // at least one tile
     const uint32_t last = t_end - 1;
     const int64_t s = A.seg_stripe[g], o0 = s * 16;

@@ -346,6 +346,7 @@ struct DenseArgs {
     // Work: segments of at most a few dozen consecutive dense tiles of one
     // stripe (16 owner rows), one wave each.
     int64_t n_segs;
+    const int32_t *seg_order;   // the segment the w-th wave of the launch takes
     const uint32_t *seg_tile;   // tiles of segment g: seg_tile[g] .. seg_tile[g + 1]
     const int32_t *seg_stripe;  // stripe of segment g
     const uint32_t *stripe_seg; // segments of stripe s: stripe_seg[s] .. stripe_seg[s + 1]
