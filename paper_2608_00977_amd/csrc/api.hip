@@ -1495,7 +1495,17 @@ int32_t ensure_qblock(tsid_ctx *c, int prec) {
         const int64_t n = (int64_t)(nb + 1) * t.n_t;
         std::vector<int64_t> hb((size_t)n);
         TSID_HIP(hipMemcpy(hb.data(), qb.bounds, (size_t)n * 8, hipMemcpyDeviceToHost));
-        const int64_t E = choose_E(std::max<int64_t>(1, (dn ? t.dense.sparse_nnz : t.nnz) / nb));
+        // Items sized for the blocks that run at one time (a group of kXcds):
+        // enough of them to fill the device, each as long as that allows.
+        // Billion-scale (24 blocks): 560 cells, Q pass 4.4 ms; sized per
+        // block instead (80 cells, four times the waves) it took 4.9 ms, with
+        // 160 / 320 / 640 / 1,280 / 2,560 cells 4.75 / 4.57 / 4.38 / 4.41 /
+        // 4.45 ms.  Tuning knob TSID_QBLOCK_E: the cell count.
+        const char *ee = std::getenv("TSID_QBLOCK_E");
+        const int64_t pass_cells = dn ? t.dense.sparse_nnz : t.nnz;
+        const int64_t E = ee && std::atoi(ee) > 0
+                              ? (int64_t)std::atoi(ee)
+                              : choose_E(std::max<int64_t>(1, pass_cells * std::min(nb, kXcds) / nb));
         const int ng = items_per_wave(t.k, prec), wg = items_per_workgroup(t.k, prec);
         const int64_t nv = (int64_t)nb * t.n_t;
         if (nv >= INT32_MAX) fail(TSID_E_INVAL, "too many row-block buckets");
