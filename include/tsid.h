@@ -191,9 +191,21 @@ tsid_status tsid_loss_noalloc(tsid_ctx *ctx, const float *P, const float *Q, flo
  * a free row's coefficients x_f solve the ridge problem
  *   min sum_(entries of f) (r - F_fixed[fixed_id] . x_f)^2 + lambda ||x_f||^2
  * with the fixed factors held constant).  Every free row starts at zero and
- * takes opts->epochs gradient steps with the same residual/gradient kernel as
- * the template fit (opts->step, opts->clip apply; opts->prec is ignored: the
- * fixed side is read in fp32).
+ * takes opts->epochs gradient steps of Eq. 5 (opts->step, opts->clip apply;
+ * opts->prec is ignored: the fixed side is read in fp32).  A row's steps are
+ * taken in one of two forms with the same result up to rounding:
+ *  - per cell, with the template fit's residual/gradient kernel, in fp32,
+ *    gathering the row's fixed factors once per step;
+ *  - in Gram form, for rows of at least a threshold number of cells: the
+ *    gradient 2 lambda x - 2 (b - G x) from G = sum p p^T and b = sum r p,
+ *    accumulated once in fp64 on the matrix cores, with the steps in fp64.
+ *    The threshold weighs the forms' work at this k and step count, and
+ *    whether the fixed table fits one XCD's 4 MiB L2 (where the per-cell
+ *    gathers are cheap): at 20 steps, from 40 (k = 32) or never (k = 64)
+ *    cells with such a table, and from 69 (k = 32) or 96 (k = 64) cells
+ *    with a larger one.  k = 128 and a single step keep the per-cell form.
+ *    A row's form depends on its own cell count only, so results do not
+ *    depend on how the rows are split into chunks.
  *  side        0: the free rows are rows of R and F_fixed holds column
  *              factors; 1: the free rows are columns and F_fixed holds row
  *              factors.  The arithmetic is the same; side is recorded only.

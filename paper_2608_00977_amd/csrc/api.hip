@@ -2485,8 +2485,29 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
         a.clip = o->clip;
         a.degree = o->step == TSID_STEP_DEGREE;
         a.err = x.err;
-        // every step of every free row in one launch (one wave per free row)
+        // rows long enough for the Gram form go to k_extend_gram, the others
+        // take every step in one launch of the per-cell kernel (one wave per
+        // free row in both)
+        const int64_t gmin = extend_gram_min(K, o->epochs, o->clip, n_fixed);
+        a.skip_from = gmin;
         launch_extend_steps(K, a, o->epochs, cs);
+        if (gmin > 0) {
+            RidgeArgs g{};
+            g.stream = x.stream;
+            g.ptr = x.ptr;
+            g.rows = n_free;
+            g.F = F_fixed;
+            g.lambda = o->lambda;
+            g.X = s.X;
+            g.err = x.err;
+            g.gram_min = gmin;
+            g.steps = o->epochs;
+            g.clip = o->clip;
+            g.degree = a.degree;
+            g.lr = o->lr;
+            g.xi = o->clip_xi;
+            launch_extend_gram(K, g, cs);
+        }
     }
     if (tmo) {
         TSID_HIP(hipEventRecord(s.tm[3], cs));

@@ -702,6 +702,7 @@ __global__ __launch_bounds__(kThreads) void k_extend_steps(const PassArgs A, int
     const int64_t row = (int64_t)blockIdx.x * kWaves + wv;
     if (row >= A.rows) return;  // whole waves leave together
     const int64_t rb = A.ptr[row], deg = A.ptr[row + 1] - rb;
+    if (A.skip_from > 0 && deg >= A.skip_from) return;  // the Gram-form kernel's row
     const int64_t beg = rb + grp * deg / NG, end = rb + (grp + 1) * deg / NG;
     const int64_t last = end - 1;
     const float s = A.degree ? 1.0f / (float)(deg > 1 ? deg : 1) : 1.0f;

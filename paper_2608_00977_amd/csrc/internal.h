@@ -166,6 +166,9 @@ struct PassArgs {
     // at carry + (item / groups per wave) * K, one per wave (plans built on
     // the host, whose longer buckets fill whole waves); 0: at carry + item * K.
     int32_t carry_per_wave;
+    // Extension steps: free rows with at least this many cells are left to
+    // the Gram-form kernel (0: none).
+    int64_t skip_from;
 };
 
 // prec: 0 fp32, 1 bf16.  loss_only: residuals, e2 and norms only.
@@ -303,9 +306,20 @@ struct RidgeArgs {
     float lambda;
     float *X;             // rows x K results
     int32_t *err;
+    // Gradient steps in Gram form (launch_extend_gram): the free rows with at
+    // least gram_min cells take `steps` steps of Eq. 5 (lr, the step option
+    // `degree`, the clip and xi as in the template fit) from x = 0.
+    int64_t gram_min;
+    int32_t steps, clip, degree;
+    float lr, xi;
 };
 bool ridge_supported(int K);
 void launch_ridge_rows(int K, const RidgeArgs &a, hipStream_t s);
+// The smallest free-row length for which the Gram form of `steps` gradient
+// steps is cheaper than the per-cell form at rank K with n_fixed fixed rows
+// (0: never).
+int64_t extend_gram_min(int K, int32_t steps, int32_t clip, int64_t n_fixed);
+void launch_extend_gram(int K, const RidgeArgs &a, hipStream_t s);
 
 // ---------------------------------------- extension by Adam on coefficients
 struct AdamArgs {

@@ -29,6 +29,10 @@
 // k) raises the non-finite error; a row without cells gets x = 0.
 #include <hip/hip_ext.h>
 
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+
 #include "internal.h"
 
 namespace tsid {
@@ -51,68 +55,78 @@ struct RidgeShape {
     static constexpr int PITCH = K + 1;               // LDS row pitch (doubles)
 };
 
+// Gram blocks (block pairs I <= J) and right-hand side of one free row's
+// cells b0 .. b1 (b1 > b0), by one wave with the operand layout above.  Four
+// groups of four cells are loaded before their products, so each lane keeps
+// four gathers per block in flight; loads past the row's end re-read its
+// last cell and are masked.
 template <int K>
-__global__ __launch_bounds__(64) void k_ridge_rows(const RidgeArgs A) {
+__device__ __forceinline__ void gram_line(const RidgeArgs &A, int64_t b0, int64_t b1, int lane,
+                                          d4 (&acc)[RidgeShape<K>::NP], double (&rhs)[RidgeShape<K>::NB]) {
     using S = RidgeShape<K>;
-    __shared__ double G[K * S::PITCH];
-    const int lane = threadIdx.x;
-    const int64_t f = blockIdx.x;  // free row
-    if (f >= A.rows) return;
+    constexpr int U = 4;
     const int lr = lane & 15, lq = lane >> 4;
-    const int64_t b0 = A.ptr[f], b1 = A.ptr[f + 1];
-    if (b0 == b1) {  // no cells: the minimiser is 0
-        if (lane < K) A.X[f * K + lane] = 0.f;
-        return;
-    }
-    // 1. Gram blocks and right-hand side
-    d4 acc[S::NP];
 #pragma unroll
     for (int q = 0; q < S::NP; ++q) acc[q] = d4{0.0, 0.0, 0.0, 0.0};
-    double rhs[S::NB];
 #pragma unroll
     for (int I = 0; I < S::NB; ++I) rhs[I] = 0.0;
-    for (int64_t c0 = b0; c0 < b1; c0 += 4) {
-        const int64_t c = c0 + lq;
-        double pv[S::NB];
-        double rv = 0.0;
+    for (int64_t c0 = b0; c0 < b1; c0 += 4 * U) {
+        int2 rec[U];
 #pragma unroll
-        for (int I = 0; I < S::NB; ++I) pv[I] = 0.0;
-        if (c < b1) {
-            const int2 rec = A.stream[c];
-            rv = (double)__int_as_float(rec.y);
-            const float *p = A.F + (int64_t)rec.x * K;
-#pragma unroll
-            for (int I = 0; I < S::NB; ++I)
-                if (K % 16 == 0 || 16 * I + lr < K) pv[I] = (double)p[16 * I + lr];
+        for (int u = 0; u < U; ++u) {
+            const int64_t c = c0 + 4 * u + lq;
+            rec[u] = A.stream[c < b1 ? c : b1 - 1];
         }
-        int q = 0;
+        double pv[U][S::NB], rv[U];
 #pragma unroll
-        for (int I = 0; I < S::NB; ++I) {
-            rhs[I] = fma(rv, pv[I], rhs[I]);
+        for (int u = 0; u < U; ++u) {
+            const bool in = c0 + 4 * u + lq < b1;
+            rv[u] = in ? (double)__int_as_float(rec[u].y) : 0.0;
+            const float *p = A.F + (int64_t)rec[u].x * K;
 #pragma unroll
-            for (int J = I; J < S::NB; ++J, ++q) acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(pv[I], pv[J], acc[q], 0, 0, 0);
+            for (int I = 0; I < S::NB; ++I) {
+                const int col = (K % 16 == 0 || 16 * I + lr < K) ? 16 * I + lr : K - 1;
+                const float v = p[col];
+                pv[u][I] = (in && (K % 16 == 0 || 16 * I + lr < K)) ? (double)v : 0.0;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            int q = 0;
+#pragma unroll
+            for (int I = 0; I < S::NB; ++I) {
+                rhs[I] = fma(rv[u], pv[u][I], rhs[I]);
+#pragma unroll
+                for (int J = I; J < S::NB; ++J, ++q)
+                    acc[q] = __builtin_amdgcn_mfma_f64_16x16x4f64(pv[u][I], pv[u][J], acc[q], 0, 0, 0);
+            }
         }
     }
-    // 2. blocks to LDS (with their mirror images), lane i reads row i
-    {
-        int q = 0;
+}
+
+// The Gram blocks and their mirror images to LDS (pitch K + 1); the
+// right-hand side summed over the four cell slots, lane i returning b_i.
+template <int K>
+__device__ __forceinline__ double gram_to_lds(const d4 (&acc)[RidgeShape<K>::NP], double (&rhs)[RidgeShape<K>::NB],
+                                              double *G, int lane) {
+    using S = RidgeShape<K>;
+    const int lr = lane & 15, lq = lane >> 4;
+    int q = 0;
 #pragma unroll
-        for (int I = 0; I < S::NB; ++I) {
+    for (int I = 0; I < S::NB; ++I) {
 #pragma unroll
-            for (int J = I; J < S::NB; ++J, ++q) {
+        for (int J = I; J < S::NB; ++J, ++q) {
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int row = 16 * I + 4 * j + lq, col = 16 * J + lr;
-                    if (row < K && col < K) {
-                        G[row * S::PITCH + col] = acc[q][j];
-                        G[col * S::PITCH + row] = acc[q][j];
-                    }
+            for (int j = 0; j < 4; ++j) {
+                const int row = 16 * I + 4 * j + lq, col = 16 * J + lr;
+                if (row < K && col < K) {
+                    G[row * S::PITCH + col] = acc[q][j];
+                    G[col * S::PITCH + row] = acc[q][j];
                 }
             }
         }
     }
-    // the right-hand side: sum over the four cell slots, then lane i takes
-    // coordinate i = 16 (i / 16) + i % 16
+    // coordinate i = 16 (i / 16) + i % 16 sits in lane i after the sums
 #pragma unroll
     for (int I = 0; I < S::NB; ++I) {
         rhs[I] += __shfl_xor(rhs[I], 16, 64);
@@ -121,6 +135,26 @@ __global__ __launch_bounds__(64) void k_ridge_rows(const RidgeArgs A) {
     double b = 0.0;
 #pragma unroll
     for (int I = 0; I < S::NB; ++I) b = (lq == I) ? rhs[I] : b;
+    return b;
+}
+
+template <int K>
+__global__ __launch_bounds__(64) void k_ridge_rows(const RidgeArgs A) {
+    using S = RidgeShape<K>;
+    __shared__ double G[K * S::PITCH];
+    const int lane = threadIdx.x;
+    const int64_t f = blockIdx.x;  // free row
+    if (f >= A.rows) return;
+    const int64_t b0 = A.ptr[f], b1 = A.ptr[f + 1];
+    if (b0 == b1) {  // no cells: the minimiser is 0
+        if (lane < K) A.X[f * K + lane] = 0.f;
+        return;
+    }
+    // 1.-2. Gram blocks and right-hand side, the blocks through LDS
+    d4 acc[S::NP];
+    double rhs[S::NB];
+    gram_line<K>(A, b0, b1, lane, acc, rhs);
+    double b = gram_to_lds<K>(acc, rhs, G, lane);
     __syncthreads();
     const int ri = lane < K ? lane : K - 1;  // lanes past k mirror the last row (never read back)
     double g[K];
@@ -163,6 +197,64 @@ __global__ __launch_bounds__(64) void k_ridge_rows(const RidgeArgs A) {
         if (lane < r) b = fma(-G[r * S::PITCH + lane], xr, b);
     }
     bad = __builtin_amdgcn_ballot_w64(bad) != 0;  // a bad pivot anywhere spoils the whole row
+    if (lane < K) {
+        const float xf = (float)x;
+        A.X[f * K + lane] = xf;
+        if (bad || !__builtin_isfinite(xf)) A.err[ERR_NONFINITE] = 1;
+    }
+}
+
+// One-sided gradient steps in Gram form (Section 5.2's per-row subproblem
+// with Eq. 5's update).  With the fixed side held, the gradient of a free
+// row's loss is 2 lambda x - 2 (b - G x), G = sum_u p_u p_u^T and
+// b = sum_u r_u p_u over the row's cells, so one pass over the cells (fp64,
+// as for the exact solve) gives every step: lane i holds row i of G and b_i,
+// and a step is the product G x (x broadcast lane by lane), the gradient, the
+// step option's scale, the clip and the update, all in fp64 from x = 0.  The
+// per-cell kernel (k_extend_steps) gathers every fixed row once per step; for
+// rows of at least gram_min cells this one gathers them once.  Rows shorter
+// than gram_min are the per-cell kernel's and are left untouched here.
+template <int K>
+__global__ __launch_bounds__(64) void k_extend_gram(const RidgeArgs A) {
+    using S = RidgeShape<K>;
+    __shared__ double G[K * S::PITCH];
+    const int lane = threadIdx.x;
+    const int64_t f = blockIdx.x;
+    if (f >= A.rows) return;
+    const int64_t b0 = A.ptr[f], b1 = A.ptr[f + 1], deg = b1 - b0;
+    if (deg < A.gram_min || deg == 0) return;
+    d4 acc[S::NP];
+    double rhs[S::NB];
+    gram_line<K>(A, b0, b1, lane, acc, rhs);
+    const double b = gram_to_lds<K>(acc, rhs, G, lane);
+    __syncthreads();
+    const int ri = lane < K ? lane : K - 1;  // lanes past k mirror the last row (never stored)
+    double g[K];
+#pragma unroll
+    for (int c = 0; c < K; ++c) g[c] = G[ri * S::PITCH + c];
+    const double lam = A.lambda, lr = A.lr, xi = A.xi;
+    const double sc = A.degree ? 1.0 / (double)(deg > 1 ? deg : 1) : 1.0;
+    double x = 0.0;
+    bool bad = false;
+    for (int t = 0; t < A.steps; ++t) {
+        // G x in four independent sums (a shorter chain of dependent FMAs)
+        double gq[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int c = 0; c < K; ++c) gq[c & 3] = fma(g[c], readlane_f64(x, c), gq[c & 3]);
+        const double gx = (gq[0] + gq[1]) + (gq[2] + gq[3]);
+        const double grad = 2.0 * lam * x - 2.0 * (b - gx);
+        double d;
+        if (A.clip == 3) {  // the printed asymmetric form: the scale outside the clip
+            d = -grad;
+            if (d > xi) d = xi;
+            d *= sc;
+        } else {
+            d = -sc * grad;
+            if (A.clip && d > xi) d = xi;
+        }
+        x = fma(lr, d, x);
+        bad |= !__builtin_isfinite(x);
+    }
     if (lane < K) {
         const float xf = (float)x;
         A.X[f * K + lane] = xf;
@@ -335,6 +427,54 @@ void ridge_128(const RidgeArgs &a, hipStream_t s) {
 }  // namespace
 
 bool ridge_supported(int K) { return K == 8 || K == 16 || K == 32 || K == 64 || K == 128; }
+
+// Where the Gram form pays, per free row of d cells.  Gram form: K^2 r fp64
+// multiply-adds per cell on the matrix cores (r: the share of the 16 x 16
+// blocks it forms, the pairs I <= J) and, per step, the product G x with x
+// broadcast lane by lane (about 3 K wave instructions).  Per-cell form: 2 K
+// fp32 multiply-adds per cell and step, and the gathers of the row's fixed
+// rows again every step.
+//  - A fixed table within one XCD's L2 (4 MiB) serves those gathers from L2,
+//    and the forms compare by arithmetic: d = T K / (2 T - K r), when
+//    2 T > K r.  Rating-shaped rows (k = 64, 20 steps, a 2 MiB table): all in
+//    the per-cell form 16.8 ms, Gram form from 96 / 192 / 384 cells 18.5 /
+//    17.3 / 17.2 ms; Scientific rows (k = 32, 2 MiB, about 1,500 cells each)
+//    0.112 -> 0.094 s in Gram form.
+//  - A larger table is gathered from the memory-side cache or HBM, about
+//    4 K / 64 wave instructions' worth per cell and step, and the Gram form
+//    pays from d = 192 T / (4 T - K r), when 4 T > K r.  Rating-shaped
+//    columns (k = 64, a 123 MB table, about 1,160 cells each): 13.2 -> 7.5 ms
+//    (7.49-7.56 ms for thresholds 96 to 384); Scientific columns (k = 32,
+//    25.6 MB, about 18,000 cells) 1.38 -> 0.73 s.
+// At least 16 cells either way.  Tuning knob TSID_EXT_GRAM_MIN: -1 never,
+// n > 0 from n cells on.
+int64_t extend_gram_min(int K, int32_t steps, int32_t clip, int64_t n_fixed) {
+    if (const char *e = std::getenv("TSID_EXT_GRAM_MIN")) {
+        const long long v = std::atoll(e);
+        if (v != 0) return v < 0 || K > 64 || clip == 2 || steps < 1 ? 0 : (int64_t)v;
+    }
+    if (K > 64 || clip == 2 || steps < 1) return 0;
+    const int nb = (K + 15) / 16, np = nb * (nb + 1) / 2;
+    const double r = (double)np / (double)(nb * nb);
+    const bool in_l2 = n_fixed * K * 4 <= (int64_t(4) << 20);
+    const double den = (in_l2 ? 2.0 : 4.0) * steps - K * r;
+    if (den <= 0.0) return 0;
+    const double d = in_l2 ? (double)steps * K / den : 192.0 * steps / den;
+    return std::max<int64_t>(16, (int64_t)std::ceil(d));
+}
+
+void launch_extend_gram(int K, const RidgeArgs &a, hipStream_t s) {
+    if (a.rows <= 0 || a.gram_min <= 0) return;
+    if (a.rows > INT32_MAX) fail(TSID_E_INVAL, "too many free rows");
+    switch (K) {
+        case 8: hipLaunchKernelGGL(k_extend_gram<8>, dim3((unsigned)a.rows), dim3(64), 0, s, a); break;
+        case 16: hipLaunchKernelGGL(k_extend_gram<16>, dim3((unsigned)a.rows), dim3(64), 0, s, a); break;
+        case 32: hipLaunchKernelGGL(k_extend_gram<32>, dim3((unsigned)a.rows), dim3(64), 0, s, a); break;
+        case 64: hipLaunchKernelGGL(k_extend_gram<64>, dim3((unsigned)a.rows), dim3(64), 0, s, a); break;
+        default: fail(TSID_E_INVAL, "the Gram-form steps support k in {8, 16, 32, 64}");
+    }
+    TSID_HIP(hipGetLastError());
+}
 
 void launch_ridge_rows(int K, const RidgeArgs &a, hipStream_t s) {
     if (a.rows <= 0) return;
