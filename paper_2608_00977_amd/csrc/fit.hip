@@ -725,27 +725,9 @@ __global__ __launch_bounds__(kThreads) void k_extend_steps(const PassArgs A, int
             keep[c] = load_cell(A.stream + (jj < last ? jj : last));
         }
     }
-    for (int st = 0; st < steps; ++st) {
-        float acc[V];
-#pragma unroll
-        for (int v = 0; v < V; ++v) acc[v] = 0.f;
-        float e2 = 0.f;
-        if (one_block) {
-            if (end > beg)
-                process_block<K, V, false, false, BUF, false, SPL>(A, Yt, beg, end, last, lg, keep, bufB, x,
-                                                                   xp, acc, e2);
-        } else {
-#pragma unroll
-            for (int c = 0; c < SPL; ++c) bufA[c] = keep[c];
-            for (int64_t j0 = beg; j0 < end; j0 += SB) {
-                process_block<K, V, false, false, BUF, true, SPL>(A, Yt, j0, end, last, lg, bufA, bufB, x, xp,
-                                                                  acc, e2);
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int c = 0; c < SPL; ++c) bufA[c] = bufB[c];
-            }
-        }
-        // the row's gradient sum: the groups' partial sums in group order
+    // The row's gradient sum (the groups' partial sums in group order) and
+    // the update of every group's copy of the row.
+    auto update = [&](const float (&acc)[V]) {
         store_f32<V>(&red[wv][grp][lg * V], acc);
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_wave_barrier();
@@ -767,6 +749,72 @@ __global__ __launch_bounds__(kThreads) void k_extend_steps(const PassArgs A, int
             const float d = clipped_step(g, s, A.clip, A.xi);
             x[v] = x[v] + A.lr * d;
             bad |= !__builtin_isfinite(x[v]);
+        }
+    };
+    constexpr int CH = chunk_cells<G>();
+    static_assert(CH <= SB && CH % G == 0, "a chunk lies inside the first stream block");
+    if (deg <= (int64_t)NG * CH) {
+        // Every group's share fits one chunk (shares differ by at most one
+        // cell; the test is on the row, so the whole wave takes this branch):
+        // the fixed rows are gathered once, into registers, and every step
+        // reuses them, with the per-cell code's arithmetic in its order.
+        float yc[CH][V], rc[CH];
+        const int64_t left = end - beg;
+        if (end > beg) {
+#pragma unroll
+            for (int t = 0; t < CH; ++t) {
+                const int b = group_bcast<G>(keep[t / G].x, t % G);
+                rc[t] = __int_as_float(group_bcast<G>(keep[t / G].y, t % G));
+#pragma unroll
+                for (int c = 0; c < V / 4; ++c) {
+                    const uint4 q = ygather16<BUF>(Yt, b, K * 4, Lanes<G, V, false>::coord(lg, c) * 4);
+                    yc[t][4 * c + 0] = __uint_as_float(q.x);
+                    yc[t][4 * c + 1] = __uint_as_float(q.y);
+                    yc[t][4 * c + 2] = __uint_as_float(q.z);
+                    yc[t][4 * c + 3] = __uint_as_float(q.w);
+                }
+            }
+        }
+        for (int st = 0; st < steps; ++st) {
+            float acc[V];
+#pragma unroll
+            for (int v = 0; v < V; ++v) acc[v] = 0.f;
+            if (end > beg) {
+#pragma unroll
+                for (int t = 0; t < CH; ++t) {
+                    float d = 0.f;
+#pragma unroll
+                    for (int v = 0; v < V; ++v) d += x[v] * yc[t][v];
+                    d = group_sum<G>(d);
+                    const float e = t < left ? rc[t] - d : 0.f;
+#pragma unroll
+                    for (int v = 0; v < V; ++v) acc[v] += e * yc[t][v];
+                }
+            }
+            update(acc);
+        }
+    } else {
+        for (int st = 0; st < steps; ++st) {
+            float acc[V];
+#pragma unroll
+            for (int v = 0; v < V; ++v) acc[v] = 0.f;
+            float e2 = 0.f;
+            if (one_block) {
+                if (end > beg)
+                    process_block<K, V, false, false, BUF, false, SPL>(A, Yt, beg, end, last, lg, keep, bufB, x,
+                                                                       xp, acc, e2);
+            } else {
+#pragma unroll
+                for (int c = 0; c < SPL; ++c) bufA[c] = keep[c];
+                for (int64_t j0 = beg; j0 < end; j0 += SB) {
+                    process_block<K, V, false, false, BUF, true, SPL>(A, Yt, j0, end, last, lg, bufA, bufB, x, xp,
+                                                                      acc, e2);
+                    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                    for (int c = 0; c < SPL; ++c) bufA[c] = bufB[c];
+                }
+            }
+            update(acc);
         }
     }
     if (grp == 0) store_coords<G, V, false>(A.Xn + row * K, lg, x);
