@@ -1904,7 +1904,11 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
     // Likewise the item passes (after both sides' dense-tile launches), unless
     // the Q pass runs in row blocks.
     const bool item_pair = !sp_r.use && !sp_c.use && nb <= 1;
+    // Both sides' dense-tile launches are one grid whenever both passes are
+    // item passes (the Q side reads only the old factors' bf16 copies), also
+    // when the Q pass runs in row blocks.
     const bool dn = t.dense_use && prec == TSID_BF16;
+    const bool dense_pair = dn && !sp_r.use && !sp_c.use;
     DenseArgs dr = dense_args(t, 0, c->err_dev), dc = dense_args(t, 1, c->err_dev);
     dr.skip_after_nonfinite = dc.skip_after_nonfinite = 1;
     c->dense_used = tsid_dense_info{};
@@ -1963,7 +1967,7 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
                 }
             }
         } else {
-            if (dn && item_pair && (dr.n_segs || dc.n_segs)) {  // both sides' tiles in one launch
+            if (dense_pair && (dr.n_segs || dc.n_segs)) {  // both sides' tiles in one launch
                 dr.epoch = dc.epoch = ep;
                 dr.X = f.Pb[cur];
                 dr.Y = f.Qb[cur];
@@ -2018,7 +2022,7 @@ void fit(tsid_ctx *c, float *P, float *Q, const tsid_fit_opts *o, double *loss_h
                 launch_slab_finish(K, sc, cs, ev.first, ev.second);
             }
         } else {
-            if (dn && dc.n_segs && !item_pair) {
+            if (dn && dc.n_segs && !dense_pair) {
                 dc.epoch = ep;
                 dc.X = f.Qb[cur];
                 dc.Y = f.Pb[cur];

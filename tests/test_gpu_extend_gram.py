@@ -191,3 +191,33 @@ def test_gram_off_where_per_cell_is_cheaper(T):
         X = _run(T, F, fixed, free, r, len(lengths), make_opts(epochs=steps, lam=0.05, lr=0.05, step="degree"))
         st, Xo = oracle.extend(fixed, free, r, len(lengths), F, steps, 0.05, 0.05, "degree")
         assert st == 0 and rel_fro(X, Xo) <= FP32_TOL
+
+
+def test_nonfinite_reported_in_both_forms(T):
+    """A non-finite value on a row in Gram form, then on a row in the
+    per-cell form: the next sync reports E_NONFINITE either way, and a clean
+    chunk afterwards matches the oracle again."""
+    import torch
+    from paper_2608_00977_amd import TsidError, make_opts
+    from paper_2608_00977_amd.binding import E_NONFINITE
+    k, steps = 32, 20
+    gmin = _gram_min(k, steps, 2000)
+    opts = make_opts(epochs=steps, lam=0.05, lr=0.05, step="degree")
+    _set_rank(T, k)
+    for form, length in (("gram", 3 * gmin), ("per cell", gmin // 2)):
+        F, fixed, free, r = _chunk(11, k, 2000, [length, 5])
+        r = r.copy()
+        r[np.flatnonzero(free == 0)[1]] = np.nan
+        Fd = torch.from_numpy(F).cuda()
+        out = torch.empty((2, k), dtype=torch.float32).pin_memory()
+        note(f"gram nonfinite: {form} row of {length} cells")
+        T.extend_chunk(1, fixed, free, r, 2, Fd, out, opts)
+        with pytest.raises(TsidError) as e:
+            T.sync()
+        assert e.value.status == E_NONFINITE
+    lengths = [0, 4, 3 * gmin]
+    F, fixed, free, r = _chunk(12, k, 2000, lengths)
+    X = _run(T, F, fixed, free, r, len(lengths), opts)
+    st, Xo = oracle.extend(fixed, free, r, len(lengths), F, steps, 0.05, 0.05, "degree")
+    assert st == 0
+    _check(X, Xo, lengths, gmin)
