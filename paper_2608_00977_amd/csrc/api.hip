@@ -649,7 +649,7 @@ void build(tsid_ctx *c, int64_t m, int64_t n, const int32_t *u, const int32_t *i
     t->m_t = m_t;
     t->n_t = n_t;
     t->k = k;
-    // Scratch of this build; released on every path.
+    // Scratch memory of the template construction; released on every path.
     int32_t *dI = nullptr, *dJ = nullptr, *su[2] = {nullptr, nullptr}, *si[2] = {nullptr, nullptr};
     float *sr[2] = {nullptr, nullptr};
     uint32_t *bcnt = nullptr, *boffs = nullptr, *piece = nullptr, *scan_tmp = nullptr;
