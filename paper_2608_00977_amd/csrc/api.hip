@@ -246,6 +246,7 @@ struct ExtState {
     float *plan_carry = nullptr;
     int64_t plan_cap = 0;
     int32_t *err = nullptr;
+    uint32_t *unsorted = nullptr;  // the chunk's keys out of order (radix_sort)
     int next = 0;
     bool pending = false;
 };
@@ -2269,6 +2270,7 @@ void ext_ensure(tsid_ctx *c, int64_t nnz, int32_t n_free, int32_t k) {
         }
         x.err = A.alloc<int32_t>(ERR_SLOTS);
         TSID_HIP(hipMemsetAsync(x.err, 0, ERR_SLOTS * 4, c->comp));
+        x.unsorted = A.alloc<uint32_t>(1);
     }
     if (nnz <= x.cap_nnz && n_free <= x.cap_free && k == x.k) return;
     ext_sync_all(c);  // buffers may be in use by earlier chunks
@@ -2416,8 +2418,11 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
     const int bits_free = bits_for(std::max<int32_t>(n_free, 1));
     chunk_keys(s.fid, s.free_id, s.r, nnz, n_fixed, n_free, bits_fixed, x.keys, x.vals, x.err, cs);
     TSID_HIP(hipEventRecord(s.ev_staged, cs));
+    // a chunk already grouped by free row (fixed ids ascending within a row,
+    // as a line-by-line generator emits them) skips the sort's passes
+    keys_unsorted(x.keys, nnz, x.unsorted, cs);
     const bool alt = radix_sort(x.keys, x.vals, x.keys_alt, x.vals_alt, nnz, bits_fixed + bits_free,
-                                x.sort_scratch, cs);
+                                x.sort_scratch, cs, x.unsorted);
     const uint64_t *sk = alt ? x.keys_alt : x.keys;
     const uint32_t *sv = alt ? x.vals_alt : x.vals;
     keys_to_stream(sk, sv, nnz, bits_fixed, x.stream, x.err, cs);
@@ -2644,6 +2649,7 @@ void tsid_destroy(tsid_ctx *c) {
     free_fit(c);
     free_ext_buffers(c);
     c->arena.release(c->ext.err);
+    c->arena.release(c->ext.unsorted);
     for (auto &s : c->ext.slot) {
         if (s.ev_h2d) (void)hipEventDestroy(s.ev_h2d);
         if (s.ev_staged) (void)hipEventDestroy(s.ev_staged);

@@ -61,9 +61,14 @@ void scan_u32(const uint32_t *in, uint32_t *out, int64_t n, uint32_t *total, uin
 // Stable LSD radix sort of (key, value) pairs on the low `nbits` bits of the
 // key, 8 bits per pass.  Ping-pongs between the two buffers; returns true if
 // the sorted result ends in the *_alt buffers.  scratch: radix_scratch_elems(n).
+// unsorted (device, or null): a flag from keys_unsorted; when it holds 0 the
+// input is already in key order and the passes only leave it in the buffer
+// the return value names.
 size_t radix_scratch_elems(int64_t n);
 bool radix_sort(uint64_t *keys, uint32_t *vals, uint64_t *keys_alt, uint32_t *vals_alt, int64_t n,
-                int nbits, uint32_t *scratch, hipStream_t s);
+                int nbits, uint32_t *scratch, hipStream_t s, const uint32_t *unsorted = nullptr);
+// *unsorted = 1 if some key is smaller than the one before it, else 0.
+void keys_unsorted(const uint64_t *keys, int64_t n, uint32_t *unsorted, hipStream_t s);
 
 void fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s);
 void fill_u32(uint32_t *p, int64_t n, uint32_t v, hipStream_t s);

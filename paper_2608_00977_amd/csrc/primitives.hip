@@ -94,8 +94,19 @@ __global__ void k_scatter_map(const int32_t *ids, int32_t count, int32_t *map) {
 
 // ---------------------------------------------------------------- radix sort
 
+// Input already in key order: *unsorted stays 0 and the passes do nothing
+// (see radix_sort).
+__global__ void k_keys_unsorted(const uint64_t *keys, int64_t n, uint32_t *unsorted) {
+    bool bad = false;
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x + 1; j < n;
+         j += (int64_t)gridDim.x * blockDim.x)
+        bad |= keys[j - 1] > keys[j];
+    if (bad) *unsorted = 1u;
+}
+
 __global__ __launch_bounds__(kThreads) void k_radix_hist(const uint64_t *keys, int64_t n, int shift,
-                                                         uint32_t *counts, int nb) {
+                                                         uint32_t *counts, int nb, const uint32_t *unsorted) {
+    if (unsorted && *unsorted == 0u) return;
     __shared__ uint32_t h[256];
     h[threadIdx.x] = 0;
     __syncthreads();
@@ -109,13 +120,29 @@ __global__ __launch_bounds__(kThreads) void k_radix_hist(const uint64_t *keys, i
 }
 
 // Stable scatter: elements are ranked in index order (round, wave, lane).
+// With unsorted pointing at 0 (input in key order) the pass only copies its
+// tile when copy_if_sorted is set (the last of an odd number of passes, whose
+// result the caller expects in the other buffer).
 __global__ __launch_bounds__(kThreads) void k_radix_scatter(const uint64_t *kin, const uint32_t *vin,
                                                             uint64_t *kout, uint32_t *vout,
                                                             int64_t n, int shift,
-                                                            const uint32_t *offs, int nb) {
+                                                            const uint32_t *offs, int nb,
+                                                            const uint32_t *unsorted, int copy_if_sorted) {
     __shared__ uint32_t s_base[256];
     __shared__ uint32_t s_cnt[4][256];
     const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    if (unsorted && *unsorted == 0u) {
+        if (copy_if_sorted) {
+            for (int it = 0; it < kSortItems; ++it) {
+                const int64_t j = (int64_t)blockIdx.x * kSortTile + (int64_t)it * kThreads + t;
+                if (j < n) {
+                    kout[j] = kin[j];
+                    vout[j] = vin[j];
+                }
+            }
+        }
+        return;
+    }
     s_base[t] = offs[(int64_t)t * nb + blockIdx.x];
     const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     const int64_t base = (int64_t)blockIdx.x * kSortTile;
@@ -344,25 +371,36 @@ size_t radix_scratch_elems(int64_t n) {
 }
 
 bool radix_sort(uint64_t *keys, uint32_t *vals, uint64_t *keys_alt, uint32_t *vals_alt, int64_t n,
-                int nbits, uint32_t *scratch, hipStream_t s) {
+                int nbits, uint32_t *scratch, hipStream_t s, const uint32_t *unsorted) {
     if (n <= 1) return false;
     const int nb = ceil_div(n, kSortTile);
     const int64_t nc = 256 * (int64_t)nb;
     uint32_t *counts = scratch, *scan_tmp = scratch + nc;
+    const int passes = (nbits + 7) / 8;
     bool alt = false;
-    for (int shift = 0; shift < nbits; shift += 8) {
+    for (int p = 0; p < passes; ++p) {
+        const int shift = 8 * p;
         const uint64_t *kin = alt ? keys_alt : keys;
         const uint32_t *vin = alt ? vals_alt : vals;
         uint64_t *kout = alt ? keys : keys_alt;
         uint32_t *vout = alt ? vals : vals_alt;
-        k_radix_hist<<<nb, kThreads, 0, s>>>(kin, n, shift, counts, nb);
+        k_radix_hist<<<nb, kThreads, 0, s>>>(kin, n, shift, counts, nb, unsorted);
         TSID_HIP(hipGetLastError());
-        scan_u32(counts, counts, nc, nullptr, scan_tmp, s);
-        k_radix_scatter<<<nb, kThreads, 0, s>>>(kin, vin, kout, vout, n, shift, counts, nb);
+        scan_u32(counts, counts, nc, nullptr, scan_tmp, s);  // (its values unused when the passes skip)
+        const int copy_if_sorted = (p == passes - 1) && (passes & 1);
+        k_radix_scatter<<<nb, kThreads, 0, s>>>(kin, vin, kout, vout, n, shift, counts, nb, unsorted,
+                                                copy_if_sorted);
         TSID_HIP(hipGetLastError());
         alt = !alt;
     }
     return alt;
+}
+
+void keys_unsorted(const uint64_t *keys, int64_t n, uint32_t *unsorted, hipStream_t s) {
+    fill_u32(unsorted, 1, 0u, s);
+    if (n <= 1) return;
+    k_keys_unsorted<<<grid_for(n, 256), 256, 0, s>>>(keys, n, unsorted);
+    TSID_HIP(hipGetLastError());
 }
 
 void fill_i32(int32_t *p, int64_t n, int32_t v, hipStream_t s) {

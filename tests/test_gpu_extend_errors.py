@@ -222,3 +222,47 @@ def test_device_byte_cap():
         assert _status(lambda: T.build_template(p.m, p.n, p.u, p.i, p.r, p.I, p.J, 32)) == E_NOMEM
     finally:
         T.close()
+
+
+@pytest.mark.parametrize("n_fixed,n_free", [(200, 200), (3000, 700), (3000, 5000), (1 << 20, 5000)])
+def test_sorted_chunk_skips_the_sort_same_bits(T, n_fixed, n_free):
+    """A chunk already in (free row, fixed id) order skips the radix passes;
+    its result equals the shuffled chunk's bit for bit, with the key widths
+    giving 2, 3, 4 and 5 passes (an odd count leaves the sorted keys in the
+    other buffer), and matches the oracle."""
+    from paper_2608_00977_amd import make_opts
+    k = 32
+    g = np.random.default_rng(n_fixed + n_free)
+    nnz = min(30000, n_fixed * n_free // 4)
+    cells = g.choice(n_fixed * n_free, nnz, replace=False)
+    F = g.normal(0, k ** -0.25, (n_fixed, k)).astype(np.float32)
+    fixed = (cells % n_fixed).astype(np.int32)
+    free = (cells // n_fixed).astype(np.int32)
+    r = g.standard_normal(nnz).astype(np.float32)
+    order = np.lexsort((fixed, free))
+    opts = make_opts(epochs=10, lam=0.01, lr=0.1, step="degree")
+    note(f"sorted chunk n_fixed={n_fixed} n_free={n_free}")
+    X_shuffled = _run(T, F, fixed, free, r, n_free, opts)
+    X_sorted = _run(T, F, fixed[order], free[order], r[order], n_free, opts)
+    assert np.array_equal(X_sorted, X_shuffled)
+    st, Xo = oracle.extend(fixed, free, r, n_free, F, 10, 0.01, 0.1, "degree")
+    assert st == 0
+    assert rel_fro(X_sorted, Xo) <= 1e-4
+
+
+def test_sorted_chunk_with_a_repeat_reports_duplicate(T):
+    import torch
+    from paper_2608_00977_amd import make_opts
+    from paper_2608_00977_amd.binding import E_DUP
+    F, fixed, free, r = _chunk(4, 100, 30, 500, 32)
+    order = np.lexsort((fixed, free))
+    fixed, free, r = fixed[order], free[order], r[order]
+    j = 7  # repeat cell j right after it: the keys stay in order
+    fixed = np.insert(fixed, j + 1, fixed[j])
+    free = np.insert(free, j + 1, free[j])
+    r = np.insert(r, j + 1, r[j])
+    Fd = torch.from_numpy(F).cuda()
+    out = torch.empty((30, 32), dtype=torch.float32).pin_memory()
+    note("errors: duplicate in a sorted chunk")
+    T.extend_chunk(1, fixed, free, r, 30, Fd, out, make_opts(epochs=2, lam=0.01, lr=0.1, step="degree"))
+    assert _status(T.sync) == E_DUP
