@@ -206,6 +206,9 @@ tsid_status tsid_loss_noalloc(tsid_ctx *ctx, const float *P, const float *Q, flo
  *    with a larger one.  k = 128 and a single step keep the per-cell form.
  *    A row's form depends on its own cell count only, so results do not
  *    depend on how the rows are split into chunks.
+ * The chunk's cells are bucketed by free row on the device (a stable sort by
+ * (free_local, fixed_id)); cells that already come in that order (as a
+ * line-by-line generator emits them) skip the sort, with the same result.
  *  side        0: the free rows are rows of R and F_fixed holds column
  *              factors; 1: the free rows are columns and F_fixed holds row
  *              factors.  The arithmetic is the same; side is recorded only.
