@@ -41,7 +41,12 @@ def _phase(side, free_mask, key, fixed, r, n_chunks, max_entries) -> Phase:
     pos = np.full(free_mask.size, -1, np.int64)
     pos[free_ids] = np.arange(free_ids.size)
     fk = pos[key]
-    order = np.argsort(fk, kind="stable")
+    # each free line's cells together, fixed ids ascending within a line: the
+    # library then finds every chunk already in its bucket order and skips
+    # the device sort.  One sort of a combined (line, fixed id) key (repeated
+    # cells, an error the library reports, stay neighbours in any order).
+    nbits = max(1, int(fixed.max()).bit_length()) if fixed.size else 1
+    order = np.argsort((fk << nbits) | fixed.astype(np.int64), kind="quicksort")
     fk, fixed, r = fk[order], fixed[order], r[order]
     counts = np.bincount(fk, minlength=free_ids.size).astype(np.int64)
     bounds = tsid_chunk_plan(counts, n_chunks, max_entries)
