@@ -286,7 +286,8 @@ def extension_line(args, p, T, P, Q):
     ph = run()
     tm = T.timing()
     T.set_timing(0)
-    t_ext = ph["row_phase_s"] + ph["col_phase_s"]
+    # both phases and the assembly of the full row factors between them
+    t_ext = ph["row_phase_s"] + ph["assemble_s"] + ph["col_phase_s"]
     h2d_bytes = 12 * (n_row + n_col)
     rate = h2d_probe(max(1 << 20, 12 * largest))
     copies, compute = tm["ext_h2d_ms"] / 1e3, tm["ext_compute_ms"] / 1e3

@@ -217,7 +217,10 @@ tsid_status tsid_loss_noalloc(tsid_ctx *ctx, const float *P, const float *Q, flo
  *  r           HOST nnz values.
  *  F_fixed     DEVICE n_fixed x k (k of the current template), read only;
  *              must stay unchanged until the chunk completes.
- *  F_free      HOST n_free x k, written when the chunk completes.
+ *  F_free      n_free x k, written when the chunk completes: host memory
+ *              (pinned, for the copies to overlap), or device memory of the
+ *              context's device, where the results are copied on the device
+ *              (a caller that feeds them to a later phase keeps them in HBM).
  * Asynchronous: the chunk's host-to-device copy runs on the context's copy
  * stream while the previous chunk computes, and the results return on a third
  * stream (Section 5.2, double-buffered pipelining); two device staging slots

@@ -412,12 +412,13 @@ class Tsid:
     def extend_chunk(self, side, fixed_id, free_local, r, n_free, F_fixed: torch.Tensor,
                      F_free: torch.Tensor, opts):
         """Queues one chunk; fixed_id/free_local/r are host arrays or pinned CPU
-        tensors kept alive until sync(); F_free is a CPU tensor (pinned for
-        overlap) that receives the result.  opts: tsid_fit_opts for the
+        tensors kept alive until sync(); F_free receives the result: a CPU
+        tensor (pinned for overlap) or a tensor on the context's device.  opts: tsid_fit_opts for the
         one-sided gradient steps (tsid_extend_chunk), or a float lambda for
         the exact ridge solve (tsid_extend_chunk_ridge)."""
         assert F_fixed.is_cuda and F_fixed.dtype == torch.float32 and F_fixed.is_contiguous()
-        assert not F_free.is_cuda and F_free.dtype == torch.float32 and F_free.is_contiguous()
+        assert F_free.dtype == torch.float32 and F_free.is_contiguous()
+        assert not F_free.is_cuda or F_free.device == F_fixed.device
         arrs = []
         for a, dt in ((fixed_id, np.int32), (free_local, np.int32), (r, np.float32)):
             if isinstance(a, torch.Tensor):

@@ -2526,9 +2526,10 @@ void extend_chunk(tsid_ctx *c, int side, const int32_t *fixed_id, const int32_t 
     // flush the results on the third stream
     TSID_HIP(hipStreamWaitEvent(c->d2h, s.ev_done, 0));
     if (n_free)
-        TSID_HIP(hipMemcpyAsync(F_free, s.X, (size_t)n_free * K * 4, hipMemcpyDeviceToHost, c->d2h));
+        // host or device memory: the runtime takes the direction from the address
+        TSID_HIP(hipMemcpyAsync(F_free, s.X, (size_t)n_free * K * 4, hipMemcpyDefault, c->d2h));
     if (adam && adam->C_out && n_free)
-        TSID_HIP(hipMemcpyAsync(adam->C_out, s.Cst, (size_t)n_free * adam->n_b * 4, hipMemcpyDeviceToHost, c->d2h));
+        TSID_HIP(hipMemcpyAsync(adam->C_out, s.Cst, (size_t)n_free * adam->n_b * 4, hipMemcpyDefault, c->d2h));
     TSID_HIP(hipEventRecord(s.ev_flushed, c->d2h));
     x.pending = true;
     // The previous chunk (the other slot) was queued before this one; once

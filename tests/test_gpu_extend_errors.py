@@ -266,3 +266,20 @@ def test_sorted_chunk_with_a_repeat_reports_duplicate(T):
     note("errors: duplicate in a sorted chunk")
     T.extend_chunk(1, fixed, free, r, 30, Fd, out, make_opts(epochs=2, lam=0.01, lr=0.1, step="degree"))
     assert _status(T.sync) == E_DUP
+
+
+def test_device_output_equals_host_output(T):
+    """F_free in device memory receives the same bits as a pinned host buffer
+    (the results are copied on the device), for the steps and the exact solve."""
+    import torch
+    from paper_2608_00977_amd import make_opts
+    F, fixed, free, r = _chunk(31, 3000, 700, 40000, 32, hot=1)
+    Fd = torch.from_numpy(F).cuda()
+    for opts in (make_opts(epochs=15, lam=0.01, lr=0.2, step="degree"), 0.05):
+        note(f"device output {'steps' if not isinstance(opts, float) else 'ridge'}")
+        host = torch.empty((700, 32), dtype=torch.float32).pin_memory()
+        dev = torch.full((700, 32), float("nan"), dtype=torch.float32, device="cuda")
+        T.extend_chunk(1, fixed, free, r, 700, Fd, host, opts)
+        T.extend_chunk(1, fixed, free, r, 700, Fd, dev, opts)
+        T.sync()
+        assert np.array_equal(dev.cpu().numpy(), host.numpy())

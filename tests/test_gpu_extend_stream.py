@@ -89,6 +89,8 @@ def _run(T, p, omega, max_entries, n_sample):
     note(f"{p.name} stream: {time.perf_counter() - t0:.1f}s {ph}; copies {tm['ext_h2d_ms']:.0f} ms, compute "
          f"{tm['ext_compute_ms']:.0f} ms over {tm['ext_chunks']} chunks")
     assert tm["ext_chunks"] == ext.bounds[0].size + ext.bounds[1].size - 2
+    assert P_free.is_cuda and not Q_free.is_cuda  # the row phase's factors stay in HBM
+    P_free = P_free.cpu()
     assert np.all(np.isfinite(P_free.numpy())) and np.all(np.isfinite(Q_free.numpy()))
     Qt = Q_t.cpu().numpy()
     _check_lines(rows, _sample(rows.counts, n_sample, 1), Qt, P_free.numpy(), p.lam, f"{p.name} row phase")
