@@ -294,7 +294,7 @@ def extension_line(args, p, T, P, Q):
     overlap = (copies + compute - t_ext) / min(copies, compute) if min(copies, compute) > 0 else None
     log(f"extension: {n_row} + {n_col} cells in {t_ext:.4f}s (copies {copies:.3f}s, compute {compute:.3f}s)")
     return {
-        "metric": "extension entries/s (row phase + column phase)",
+        "metric": "extension entries/s (row phase, assembly of the row factors, column phase)",
         "value": (n_row + n_col) / t_ext,
         "unit": "entries/s",
         "n_gpus": 1,
